@@ -1,0 +1,325 @@
+/*
+ * chopper.h -- C ABI of libchopper, the GPU trace pipeline for MI355X (gfx950).
+ *
+ * The library turns per-kernel records of a multi-GPU training run into the
+ * multi-granularity view described in the paper (Chopper, arXiv 2512.08242):
+ *
+ *   chopper_align      puts every record and annotation marker on one clock
+ *                      and sorts the records      (Section III-B, alignment)
+ *   chopper_attribute  assigns each kernel to its iteration / phase / layer /
+ *                      operation marker           (Section I granularities,
+ *                                                  III-A annotations)
+ *   chopper_overlap    splits wall time into compute-only, comm-only,
+ *                      overlapped and idle; per-kernel overlapped time and
+ *                      launch bubbles              (Section V-C; V-D eqs. 1-3;
+ *                                                  caption of Fig. end_to_end)
+ *   chopper_aggregate  sums durations, bubbles, overlap and counters at every
+ *                      granularity, optionally filtered by GPU / class /
+ *                      iteration                  (Section III-C)
+ *   chopper_ratios     derived metrics per aggregated row (III-C; eq. 10)
+ *
+ * Memory.  Every pointer is a DEVICE pointer unless marked [host].  The caller
+ * owns every buffer.  The library allocates no device memory, frees nothing
+ * and keeps no data between calls; all temporary storage comes from the
+ * caller's `scratch`.  Scratch protocol (every call taking scratch): pass
+ * scratch == NULL to receive the required size in *scratch_bytes (nothing
+ * else is read or written, no GPU work is done, CHOPPER_OK is returned); then
+ * call again with a buffer of at least that many bytes, 256-byte aligned.
+ *
+ * Streams.  `stream` is a hipStream_t.  Work is enqueued on it; a call may
+ * synchronize that stream internally to size later launches, so do not
+ * capture these calls in a HIP graph.  Outputs are valid after the stream
+ * has been synchronized.  Concurrent calls must use distinct scratch buffers.
+ *
+ * Errors.  Argument errors are detected on the host before any GPU work and
+ * returned synchronously (negative codes below).  Problems in the DATA are
+ * reported as bits OR-ed into the device word *status (the caller clears it);
+ * when one of the "error" bits is set the affected outputs are unspecified
+ * but every kernel stays within its buffers.
+ *
+ * Conventions.  Times are int64 nanoseconds; intervals are half-open
+ * [start, end).  NONE = 0xFFFFFFFF.  Record classes: 0 GEMM, 1 attention,
+ * 2 elementwise, 3 RMSNorm, 4 RoPE, 5 all_gather, 6 reduce_scatter,
+ * 7 optimizer; kind = 1 (communication) iff class is 5 or 6, else 0
+ * (compute) -- communication is decided by class, not by stream (V-D).
+ * Arrays are structure-of-arrays; multi-column outputs are column-major
+ * ([column][row]).
+ */
+#ifndef CHOPPER_H
+#define CHOPPER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CHOPPER_NONE 0xFFFFFFFFu
+
+/* return codes */
+enum {
+  CHOPPER_OK = 0,
+  CHOPPER_EINVAL = -1,     /* null pointer, negative size, bad depth/level */
+  CHOPPER_ESCRATCH = -2,   /* scratch smaller than the size reported       */
+  CHOPPER_EOVERFLOW = -3,  /* clock fit outside its exact-arithmetic range */
+  CHOPPER_EHIP = -4        /* a HIP runtime call failed                    */
+};
+
+/* *status bits */
+enum {
+  CHOPPER_ST_BAD_GPU = 1u,         /* gpu >= n_gpus (record or marker)      */
+  CHOPPER_ST_BAD_CLASS = 2u,       /* record class >= 8                     */
+  CHOPPER_ST_NEG_DURATION = 4u,    /* end < start (record or marker)        */
+  CHOPPER_ST_MARKER_OVERLAP = 8u,  /* two non-empty markers of one (gpu,
+                                      level) overlap: warning only, the
+                                      attribution is still exactly defined  */
+  CHOPPER_ST_RANGE = 16u,          /* |t| >= 2^62 before or after alignment,
+                                      or a time span too wide for the keys  */
+  CHOPPER_ST_ROWS_OVERFLOW = 32u,  /* aggregate rows exceed rows->cap; the
+                                      level offsets hold the needed counts  */
+  CHOPPER_ST_BAD_LEVEL = 64u,      /* marker level >= depth                 */
+  CHOPPER_ST_PATH_CONFLICT = 128u  /* records sharing a deepest marker have
+                                      different marker paths (markers not
+                                      nested); aggregate rows unspecified   */
+};
+
+/* aggregation levels besides the marker levels 0 .. depth-1 */
+enum {
+  CHOPPER_LEVEL_GPU = 100,
+  CHOPPER_LEVEL_WORKLOAD = 101,
+  CHOPPER_LEVEL_ALL = 255
+};
+
+/* Kernel records of all GPUs of a run (runtime + hardware profiling,
+   Section III-A).  gpu < n_gpus <= 256.  counters: n_counters (0..16)
+   columns of n values each, column-major, or NULL when n_counters == 0.
+   op_id is carried for the caller and not read by the library. */
+typedef struct {
+  int64_t n;
+  int32_t n_gpus;
+  int32_t n_counters;
+  const uint8_t* gpu;
+  const uint8_t* stream;
+  const uint8_t* cls;
+  const uint32_t* op_id;
+  const int64_t* start_ns;
+  const int64_t* end_ns;
+  const uint64_t* counters;
+} chopper_records;
+
+/* Annotation markers (iteration, phase, layer, operation ... ranges,
+   Section III-A), in each GPU's local clock.  level 0 is the outermost;
+   depth = number of levels (1..8). */
+typedef struct {
+  int64_t n;
+  int32_t depth;
+  int32_t reserved;
+  const uint8_t* gpu;
+  const uint8_t* level;
+  const int64_t* start_ns;
+  const int64_t* end_ns;
+  const uint32_t* label;
+} chopper_markers;
+
+/* [host] Clock anchor pairs: the same instant read on a GPU's local clock
+   and on the reference clock. */
+typedef struct {
+  int64_t n;
+  const uint8_t* gpu;
+  const int64_t* local_ns;
+  const int64_t* ref_ns;
+} chopper_anchors;
+
+/* [host] Per-GPU clock: t_ref = t + c + floor((t - x0) * d_q48 / 2^48). */
+typedef struct {
+  int64_t x0;
+  int64_t c;
+  int64_t d_q48;
+} chopper_clock;
+
+/* [host] Selection before grouping (III-C): a record is kept iff bit gpu of
+   gpu_mask, bit cls of class_mask and, when use_iter != 0, its level-0
+   marker exists and iter_lo <= label <= iter_hi. */
+typedef struct {
+  uint64_t gpu_mask[4];
+  uint32_t class_mask;
+  uint32_t use_iter;
+  uint32_t iter_lo;
+  uint32_t iter_hi;
+} chopper_filter;
+
+/* Aggregated rows (device arrays of capacity cap).  level_offset has
+   depth + 3 entries: first row of marker levels 0..depth-1, of the GPU level,
+   of the workload level, and the total.  path has depth columns; entries
+   deeper than the row's level, and all entries of GPU / workload rows, are
+   NONE.  ctr has n_counters columns (may be NULL when n_counters == 0). */
+typedef struct {
+  int64_t cap;
+  int64_t* level_offset;
+  uint32_t* path;
+  uint8_t* gpu;
+  uint8_t* kind;
+  uint64_t* n;
+  int64_t* dur;
+  int64_t* gap;
+  int64_t* ovl;
+  int64_t* tmin;
+  int64_t* tmax;
+  uint32_t* first;
+  uint64_t* ctr;
+} chopper_rows;
+
+/*
+ * chopper_align -- clock alignment and the two record orders
+ * (Section III-B: traces are aligned so that counters attach to operations,
+ * layers and iterations).
+ *
+ * Fit (host): for each GPU g, its anchors (x = local, y = ref) sorted by
+ * (x, y); x0 = first x; u = x - x0, w = y - x; exact least squares of w on u
+ * with the slope rounded half-to-even to Q48 (d_q48) and the intercept c
+ * rounded half-to-even given d_q48.  No anchors: identity; one anchor or all
+ * x equal: d_q48 = 0.  Limits: <= 2^20 anchors per GPU, u < 2^42,
+ * |w| < 2^40, |d_q48| < 2^38, else CHOPPER_EOVERFLOW.
+ * Transform (GPU): every record start/end and marker start/end of GPU g:
+ * t' = t + c + floor((t - x0) * d_q48 / 2^48), exact 64x64->128-bit product.
+ *
+ * Outputs: clocks_out [host][n_gpus]; start_out/end_out [n] and
+ * mstart_out/mend_out [markers->n] aligned times in input order;
+ * order_out [n]: permutation sorting records stably by (gpu, stream,
+ * start'); korder_out [n]: stable by (gpu, kind, start').  Ties keep input
+ * order.  markers may be NULL (no marker outputs); anchors may be NULL
+ * (identity clocks).
+ */
+int chopper_align(const chopper_records* records,
+                  const chopper_markers* markers,
+                  const chopper_anchors* anchors, chopper_clock* clocks_out,
+                  int64_t* start_out, int64_t* end_out, int64_t* mstart_out,
+                  int64_t* mend_out, uint32_t* order_out, uint32_t* korder_out,
+                  void* scratch, size_t* scratch_bytes, uint32_t* status,
+                  void* stream);
+
+/*
+ * chopper_attribute -- kernel -> marker per granularity level
+ * (Section I: kernel, operation, layer, phase, iteration; III-A annotations).
+ *
+ * idx_out [depth][n] (column l = level l, input order): the input index of
+ * the last non-empty level-l marker of the record's GPU, in (start', input
+ * index) order, whose aligned start is <= the record's aligned start, if the
+ * record's start is before that marker's end; otherwise NONE.  For markers
+ * that do not overlap this is simply the marker containing the kernel start.
+ * Zero-length markers contain no instant and are ignored.  start_al,
+ * mstart_al, mend_al come from chopper_align.  Sets MARKER_OVERLAP,
+ * BAD_GPU, BAD_LEVEL.
+ */
+int chopper_attribute(const chopper_records* records, const int64_t* start_al,
+                      const chopper_markers* markers, const int64_t* mstart_al,
+                      const int64_t* mend_al, uint32_t* idx_out,
+                      void* scratch, size_t* scratch_bytes, uint32_t* status,
+                      void* stream);
+
+/*
+ * chopper_overlap -- compute/communication overlap and launch bubbles
+ * (Section V-C overlap ratio; V-D eqs. 1-3 and caption of Fig. end_to_end:
+ * launch overhead is the bubble before each compute kernel, communication
+ * kernels are ignored).
+ *
+ * Per GPU and instant t, c(t) / m(t) = number of compute / communication
+ * kernels with s' <= t < e'.  States: CO (c>0, m=0), MO (c=0, m>0),
+ * OV (both), ID (neither).
+ *   ovl_out [n]   ns of state OV inside [s', e') of each record;
+ *   gap_out [n]   compute record: max(0, s' - e'_prev), prev = previous
+ *                 compute record of the same (gpu, stream) in order_out;
+ *                 0 for the first one and for communication records;
+ *   mwin_out [markers->n][4]  CO, MO, OV, ID ns in each marker window
+ *                 [mstart', mend') (row-major 4 per marker; zeros when empty);
+ *   gwin_out [n_gpus][6]  start = min s', end = max e' over the GPU's records
+ *                 (zeros if none), then CO, MO, OV, ID of that window.
+ * order / korder come from chopper_align; markers may be NULL.
+ */
+int chopper_overlap(const chopper_records* records, const int64_t* start_al,
+                    const int64_t* end_al, const uint32_t* order,
+                    const uint32_t* korder, const chopper_markers* markers,
+                    const int64_t* mstart_al, const int64_t* mend_al,
+                    int64_t* ovl_out, int64_t* gap_out, int64_t* mwin_out,
+                    int64_t* gwin_out, void* scratch, size_t* scratch_bytes,
+                    uint32_t* status, void* stream);
+
+/*
+ * chopper_aggregate -- metric aggregation at a granularity (Section III-C;
+ * granularities of Section I; duration = sum of kernel durations and launch
+ * overhead = sum of bubbles, caption of Fig. end_to_end).
+ *
+ * Groups of the records kept by `filter` (NULL keeps all):
+ *   level l in [0, depth):  (gpu, idx_0 .. idx_l, kind)
+ *   CHOPPER_LEVEL_GPU:      (gpu, kind)
+ *   CHOPPER_LEVEL_WORKLOAD: (kind), gpu written as 0xFF
+ *   CHOPPER_LEVEL_ALL:      all of the above, in that order.
+ * Per row: n records, dur = sum(e'-s'), gap = sum(gap), ovl = sum(ovl),
+ * tmin = min s', tmax = max e', first = smallest input index among the
+ * group's records with s' = tmin, ctr = counters summed modulo 2^64.
+ * Rows of a level are ordered by (gpu, kind, tmin, first).
+ * idx is chopper_attribute's output (depth columns of n); gap / ovl are
+ * chopper_overlap's; korder is chopper_align's.  markers supplies n and the
+ * labels read by the iteration filter (may be NULL if depth == 0 paths are
+ * all NONE and no iteration filter is used).
+ * rows->level_offset is always written.  If the total exceeds rows->cap,
+ * ROWS_OVERFLOW is set and the rows are unspecified.  When markers are not
+ * nested so that two records with the same deepest marker have different
+ * paths, PATH_CONFLICT is set and rows are unspecified.
+ */
+int chopper_aggregate(const chopper_records* records, const int64_t* start_al,
+                      const int64_t* end_al, const uint32_t* korder,
+                      const uint32_t* idx, int32_t depth, const int64_t* gap,
+                      const int64_t* ovl, const chopper_markers* markers,
+                      int32_t level, const chopper_filter* filter,
+                      chopper_rows* rows, void* scratch, size_t* scratch_bytes,
+                      uint32_t* status, void* stream);
+
+/*
+ * chopper_ratios -- derived metrics per aggregated row (III-C: metrics derived
+ * from counters and duration, e.g. bandwidth; eq. 10 peak-clock duration).
+ * out [6][rows->cap] (doubles, column-major), rows 0 .. total-1 where total
+ * = rows->level_offset[depth + 2]:
+ *   0 overlap ratio           ovl / dur
+ *   1 HBM bandwidth (GB/s)    (ctr[4] + ctr[5]) / dur
+ *   2 mean SCLK (MHz)         ctr[13] / n
+ *   3 MFMA utilisation        ctr[1] / ctr[0]
+ *   4 peak-clock duration ns  ctr[0] * 1000 / freq_peak_mhz
+ *   5 actual / peak-clock     dur / column 4
+ * Each is IEEE double arithmetic on the integer sums converted to double
+ * (round to nearest), in exactly this operation order; x/0 follows IEEE.
+ * Columns 1-5 are NaN when n_counters < 16.
+ */
+int chopper_ratios(const chopper_rows* rows, int32_t depth, int32_t n_counters,
+                   double freq_peak_mhz, double* out, void* stream);
+
+/*
+ * chopper_window_fractions -- CO, MO, OV, ID of n windows (4 int64 each, as
+ * written by chopper_overlap) divided by their sum; out [n][4] doubles.
+ */
+int chopper_window_fractions(int64_t n, const int64_t* win, double* out,
+                             void* stream);
+
+/* Text for a return code. */
+const char* chopper_strerror(int code);
+
+/* ABI version (major * 10000 + minor * 100 + patch). */
+int chopper_version(void);
+
+/*
+ * chopper_time_kernel -- measurement hook.  Until called again, every launch
+ * of the library kernel named `name` is bracketed by hipEventRecord(start)
+ * and hipEventRecord(stop) on the launch stream (start_event / stop_event
+ * are hipEvent_t created by the caller).  name == NULL switches it off.
+ * Returns CHOPPER_EINVAL for an unknown name.  chopper_kernel_name(i) lists
+ * the names (NULL past the end).
+ */
+int chopper_time_kernel(const char* name, void* start_event, void* stop_event);
+const char* chopper_kernel_name(int i);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CHOPPER_H */

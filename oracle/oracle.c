@@ -522,7 +522,10 @@ static int cmp_slot(const void* x, const void* y) {
  * first = smallest input index among the group's records with start' = min
  * start'.  Rows are ordered by (gpu, kind, min start', first); workload rows
  * carry gpu 0xFF.  Each level is computed from the records, never from
- * another level.
+ * another level.  PATH_CONFLICT: at a requested marker level l, two kept
+ * records share (gpu, deepest non-NONE marker among levels 0..l, kind) but
+ * not the whole path 0..l, so grouping by that marker would merge different
+ * groups (markers not nested).
  */
 int orc_aggregate(int64_t n, const uint8_t* gpu, const uint8_t* cls,
                   const int64_t* s, const int64_t* e, const uint32_t* idx,
@@ -556,10 +559,11 @@ int orc_aggregate(int64_t n, const uint8_t* gpu, const uint8_t* cls,
     }
     sel[ns++] = (uint32_t)k;
   }
-  /* path-conflict check at every marker level */
+  /* path-conflict check at every requested marker level */
   g_gpu = gpu; g_cls = cls; g_s = s; g_idx = idx; g_n = n;
   uint32_t* tmp = (uint32_t*)malloc(sizeof(uint32_t) * (size_t)(ns > 0 ? ns : 1));
   for (int l = 0; l < depth; ++l) {
+    if (level != ORC_LEVEL_ALL && level != l) continue;
     memcpy(tmp, sel, sizeof(uint32_t) * (size_t)ns);
     g_lvl = l;
     qsort(tmp, (size_t)ns, sizeof(uint32_t), cmp_slot);

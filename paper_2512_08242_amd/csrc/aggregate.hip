@@ -1,0 +1,788 @@
+// chopper_aggregate: metric aggregation at every granularity (paper Section
+// III-C; granularities of Section I; duration and launch overhead as sums of
+// kernel durations and bubbles, caption of Fig. end_to_end).
+//
+// Records are visited in (gpu, kind, start') order.  At marker level l the
+// group of a record is identified by its deepest non-NONE marker among
+// levels 0..l (or its GPU when all are NONE) and its kind; for nested
+// markers that marker determines the whole path.  Rows are numbered in order
+// of each group's first record:
+//   1. election: atomicMin of the record position into a per-level owner
+//      table keyed by group (only at positions where the key changes);
+//   2. owners are counted per tile and one exclusive scan over the
+//      level-major table of tile counts yields final row numbers, level
+//      offsets included;
+//   3. owners write the row header (path, gpu, kind, first record);
+//   4. segmented reductions: tiles of 2048 items, eight consecutive items
+//      per thread, a thread-local pass plus one block-wide segmented scan per
+//      field.  The piece holding a row's first item stores the row; other
+//      pieces of the same row (rare: the group's records are not
+//      consecutive) go through a small overflow list applied with atomics.
+// The finest level reads the records (counters exactly once); each coarser
+// level reads the rows of the level below.  GPU and workload rows, which
+// are few, accumulate with atomics.
+#include "sort.h"
+
+namespace chopper {
+
+bool validate_records(const chopper_records* r);
+bool validate_markers(const chopper_markers* m);
+
+constexpr int kAggIpt = 8;
+constexpr int kAggTile = kBlock * kAggIpt;
+constexpr int kMaxLevels = 10;            // depth <= 8, + GPU + workload
+constexpr int kMaxFields = 6 + 16;        // n dur gap ovl tmin tmax ctr[16]
+
+struct FilterDev {
+  uint64_t gpu_mask[4];
+  uint32_t class_mask;
+  uint32_t use_iter;
+  uint32_t iter_lo, iter_hi;
+  uint32_t active;
+};
+
+struct RecSrc {
+  int64_t n;
+  int D;
+  int64_t M;
+  const uint32_t* korder;
+  const uint8_t* gpu;
+  const uint8_t* cls;
+  const int64_t* start;
+  const int64_t* end;
+  const uint32_t* idx;
+  const int64_t* gap;
+  const int64_t* ovl;
+  const uint64_t* ctr;
+  int nc;
+  const uint32_t* mlabel;
+  FilterDev f;
+};
+
+struct RowsDev {
+  int64_t cap;
+  uint32_t* path;
+  uint8_t* gpu;
+  uint8_t* kind;
+  uint64_t* n;
+  int64_t* dur;
+  int64_t* gap;
+  int64_t* ovl;
+  int64_t* tmin;
+  int64_t* tmax;
+  uint32_t* first;
+  uint64_t* ctr;
+  uint32_t* firstpos;   // scratch: korder position of each row's first record
+  int D;
+  int nc;
+};
+
+// key space of a level
+__host__ __device__ inline int64_t key_space(int li, int D, int64_t M) {
+  if (li < D) return 2 * (M + 256);
+  if (li == D) return 512;
+  return 2;
+}
+
+__device__ inline bool rec_pass(const RecSrc& S, uint32_t r) {
+  if (!S.f.active) return true;
+  const uint32_t g = S.gpu[r], c = S.cls[r];
+  if (!((S.f.gpu_mask[g >> 6] >> (g & 63)) & 1ull)) return false;
+  if (c >= 32 || !((S.f.class_mask >> c) & 1u)) return false;
+  if (S.f.use_iter) {
+    if (S.D < 1) return false;
+    const uint32_t m0 = S.idx[r];
+    if (m0 == kNone || (int64_t)m0 >= S.M) return false;
+    const uint32_t lab = S.mlabel[m0];
+    if (lab < S.f.iter_lo || lab > S.f.iter_hi) return false;
+  }
+  return true;
+}
+
+// group key of a record with path p at level li (kNone: not aggregated)
+__device__ inline uint32_t group_key(const uint32_t* p, int D, int64_t M,
+                                     int li, uint32_t g, uint32_t kind) {
+  if (li < D) {
+    uint32_t slot = kNone;
+    for (int l = 0; l <= li; ++l)
+      if (p[l] != kNone) slot = p[l];
+    if (slot == kNone) return (uint32_t)((M + g) * 2 + kind);
+    if ((int64_t)slot >= M) return kNone;
+    return slot * 2u + kind;
+  }
+  if (li == D) return g * 2u + kind;
+  return kind;
+}
+
+// One record position: its record, pass flag, gpu, kind and path.
+struct RecItem {
+  uint32_t r;
+  bool ok;
+  uint32_t g, kind;
+  uint32_t p[8];
+};
+
+__device__ inline void load_item(const RecSrc& S, int64_t pos, RecItem& it) {
+  it.r = S.korder[pos];
+  it.g = S.gpu[it.r];
+  it.kind = (uint32_t)kind_of(S.cls[it.r]);
+  it.ok = rec_pass(S, it.r);
+  for (int l = 0; l < S.D; ++l) it.p[l] = S.idx[(int64_t)l * S.n + it.r];
+}
+
+// ------------------------------------------------------------------ election
+__global__ __launch_bounds__(kBlock) void k_agg_elect(RecSrc S, uint32_t act,
+                                                      uint32_t** own) {
+  __shared__ uint32_t s_last[kBlock];
+  const int64_t base = (int64_t)blockIdx.x * kAggTile;
+  RecItem it[kAggIpt];
+  bool valid[kAggIpt];
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
+    valid[j] = pos < S.n;
+    if (valid[j]) load_item(S, pos, it[j]);
+  }
+  for (int li = 0; li < S.D + 2; ++li) {
+    if (!((act >> li) & 1u)) continue;
+    uint32_t key[kAggIpt];
+    for (int j = 0; j < kAggIpt; ++j)
+      key[j] = (valid[j] && it[j].ok)
+                   ? group_key(it[j].p, S.D, S.M, li, it[j].g, it[j].kind)
+                   : kNone;
+    s_last[threadIdx.x] = key[kAggIpt - 1];
+    __syncthreads();
+    uint32_t prev = threadIdx.x > 0 ? s_last[threadIdx.x - 1] : kNone;
+    for (int j = 0; j < kAggIpt; ++j) {
+      const bool head = (threadIdx.x == 0 && j == 0) || key[j] != prev;
+      if (key[j] != kNone && head) {
+        const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
+        atomicMin(&own[li][key[j]], (uint32_t)pos);
+      }
+      prev = key[j];
+    }
+    __syncthreads();
+  }
+}
+
+// owners per tile and level: position pos owns its key at level li
+__global__ __launch_bounds__(kBlock) void k_agg_count(RecSrc S, uint32_t act,
+                                                      uint32_t** own,
+                                                      int64_t ntiles,
+                                                      uint32_t* tilecnt) {
+  const int64_t base = (int64_t)blockIdx.x * kAggTile;
+  RecItem it[kAggIpt];
+  bool valid[kAggIpt];
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
+    valid[j] = pos < S.n;
+    if (valid[j]) load_item(S, pos, it[j]);
+  }
+  for (int li = 0; li < S.D + 2; ++li) {
+    uint32_t c = 0;
+    if ((act >> li) & 1u) {
+      for (int j = 0; j < kAggIpt; ++j) {
+        if (!valid[j] || !it[j].ok) continue;
+        const uint32_t key =
+            group_key(it[j].p, S.D, S.M, li, it[j].g, it[j].kind);
+        const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
+        if (key != kNone && own[li][key] == (uint32_t)pos) ++c;
+      }
+    }
+    uint32_t tot;
+    block_exclusive(c, OpAdd(), 0u, &tot);
+    if (threadIdx.x == 0) tilecnt[(int64_t)li * ntiles + blockIdx.x] = tot;
+  }
+}
+
+__global__ void k_agg_offsets(int L, int64_t ntiles, const uint32_t* tilebase,
+                              const uint32_t* total, int64_t cap,
+                              int64_t* level_offset, uint32_t* status) {
+  const int li = threadIdx.x;
+  if (li < L) level_offset[li] = ntiles > 0 ? tilebase[(int64_t)li * ntiles] : 0;
+  if (li == L) {
+    level_offset[L] = *total;
+    if ((int64_t)*total > cap) atomicOr(status, (uint32_t)CHOPPER_ST_ROWS_OVERFLOW);
+  }
+}
+
+// owners take their row: rowof[key] = row, header fields, and (atomic levels)
+// initial sums
+__global__ __launch_bounds__(kBlock) void k_agg_assign(
+    RecSrc S, uint32_t act, uint32_t atomic_levels, uint32_t** own,
+    uint32_t** rowof, int64_t ntiles, const uint32_t* tilebase, RowsDev R) {
+  const int64_t base = (int64_t)blockIdx.x * kAggTile;
+  RecItem it[kAggIpt];
+  bool valid[kAggIpt];
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
+    valid[j] = pos < S.n;
+    if (valid[j]) load_item(S, pos, it[j]);
+  }
+  for (int li = 0; li < S.D + 2; ++li) {
+    if (!((act >> li) & 1u)) continue;   // uniform across the block
+    uint32_t key[kAggIpt];
+    bool mine[kAggIpt];
+    uint32_t c = 0;
+    for (int j = 0; j < kAggIpt; ++j) {
+      const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
+      key[j] = (valid[j] && it[j].ok)
+                   ? group_key(it[j].p, S.D, S.M, li, it[j].g, it[j].kind)
+                   : kNone;
+      mine[j] = key[j] != kNone && own[li][key[j]] == (uint32_t)pos;
+      c += mine[j] ? 1u : 0u;
+    }
+    uint32_t tot;
+    uint32_t row = block_exclusive(c, OpAdd(), 0u, &tot) +
+                   tilebase[(int64_t)li * ntiles + blockIdx.x];
+    for (int j = 0; j < kAggIpt; ++j) {
+      if (!mine[j]) continue;
+      const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
+      rowof[li][key[j]] = row;
+      if ((int64_t)row < R.cap) {
+        for (int l = 0; l < S.D; ++l)
+          R.path[(int64_t)l * R.cap + row] =
+              (li < S.D && l <= li) ? it[j].p[l] : kNone;
+        R.gpu[row] = (li == S.D + 1) ? (uint8_t)0xFF : (uint8_t)it[j].g;
+        R.kind[row] = (uint8_t)it[j].kind;
+        R.first[row] = it[j].r;
+        R.firstpos[row] = (uint32_t)pos;
+        if ((atomic_levels >> li) & 1u) {
+          R.n[row] = 0;
+          R.dur[row] = 0;
+          R.gap[row] = 0;
+          R.ovl[row] = 0;
+          R.tmin[row] = kI64Max;
+          R.tmax[row] = kI64Min;
+          for (int q = 0; q < R.nc; ++q) R.ctr[(int64_t)q * R.cap + row] = 0;
+        }
+      }
+      ++row;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ reduction
+template <typename T>
+struct FV {
+  uint32_t f;
+  T v;
+};
+template <typename T>
+__device__ inline FV<T> shfl_up(FV<T> x, int d) {
+  FV<T> r;
+  r.f = __shfl_up(x.f, d, kWave);
+  r.v = __shfl_up(x.v, d, kWave);
+  return r;
+}
+
+struct CombAdd {
+  __device__ uint64_t operator()(uint64_t a, uint64_t b) const { return a + b; }
+};
+struct CombMin {
+  __device__ uint64_t operator()(uint64_t a, uint64_t b) const {
+    return (int64_t)a < (int64_t)b ? a : b;
+  }
+};
+struct CombMax {
+  __device__ uint64_t operator()(uint64_t a, uint64_t b) const {
+    return (int64_t)a > (int64_t)b ? a : b;
+  }
+};
+struct CombLeft {
+  __device__ uint64_t operator()(uint64_t a, uint64_t) const { return a; }
+};
+
+template <typename Comb>
+struct OpSeg {
+  Comb c;
+  __device__ FV<uint64_t> operator()(FV<uint64_t> a, FV<uint64_t> b) const {
+    return FV<uint64_t>{a.f | b.f, b.f ? b.v : c(a.v, b.v)};
+  }
+};
+
+// Segmented inclusive scan over the tile; items are blocked (thread t owns
+// items t*kAggIpt ..).  head[j] starts a new segment.
+template <typename Comb>
+__device__ inline void seg_scan(const bool (&head)[kAggIpt],
+                                uint64_t (&x)[kAggIpt], uint64_t identity,
+                                Comb comb) {
+  FV<uint64_t> acc{0u, identity};
+  for (int j = 0; j < kAggIpt; ++j) {
+    if (head[j]) acc = FV<uint64_t>{1u, x[j]};
+    else acc.v = comb(acc.v, x[j]);
+    x[j] = acc.v;
+  }
+  FV<uint64_t> tot;
+  FV<uint64_t> pre = block_exclusive(acc, OpSeg<Comb>{comb},
+                                     FV<uint64_t>{0u, identity}, &tot);
+  bool seen = false;
+  for (int j = 0; j < kAggIpt; ++j) {
+    seen = seen || head[j];
+    if (!seen) x[j] = comb(pre.v, x[j]);
+  }
+}
+
+// Item sources for the reduction: records in korder, or rows of a finer
+// level.  Fields: 0 n, 1 dur, 2 gap, 3 ovl, 4 tmin, 5 tmax, 6.. counters.
+struct FromRecords {
+  RecSrc S;
+  __device__ int64_t count() const { return S.n; }
+  __device__ void load(int64_t i, uint32_t& r, bool& ok, uint32_t* p,
+                       uint32_t& g, uint32_t& kind, uint32_t& fpos) const {
+    r = S.korder[i];
+    g = S.gpu[r];
+    kind = (uint32_t)kind_of(S.cls[r]);
+    ok = rec_pass(S, r);
+    for (int l = 0; l < S.D; ++l) p[l] = S.idx[(int64_t)l * S.n + r];
+    fpos = (uint32_t)i;
+  }
+  __device__ uint64_t field(int f, uint32_t r) const {
+    switch (f) {
+      case 0: return 1ull;
+      case 1: return (uint64_t)(S.end[r] - S.start[r]);
+      case 2: return (uint64_t)S.gap[r];
+      case 3: return (uint64_t)S.ovl[r];
+      case 4: return (uint64_t)S.start[r];
+      case 5: return (uint64_t)S.end[r];
+      default: return S.ctr[(int64_t)(f - 6) * S.n + r];
+    }
+  }
+};
+
+struct FromRows {
+  RowsDev R;
+  int64_t lo, hi;   // rows of the finer level
+  const int64_t* level_offset;
+  int lo_slot;      // level_offset index of the finer level
+  __device__ int64_t count() const {
+    int64_t a = level_offset[lo_slot], b = level_offset[lo_slot + 1];
+    if (b > R.cap) b = R.cap;
+    return b > a ? b - a : 0;
+  }
+  __device__ void load(int64_t i, uint32_t& r, bool& ok, uint32_t* p,
+                       uint32_t& g, uint32_t& kind, uint32_t& fpos) const {
+    r = (uint32_t)(level_offset[lo_slot] + i);
+    g = R.gpu[r];
+    kind = R.kind[r];
+    ok = true;
+    for (int l = 0; l < R.D; ++l) p[l] = R.path[(int64_t)l * R.cap + r];
+    fpos = R.firstpos[r];
+  }
+  __device__ uint64_t field(int f, uint32_t r) const {
+    switch (f) {
+      case 0: return R.n[r];
+      case 1: return (uint64_t)R.dur[r];
+      case 2: return (uint64_t)R.gap[r];
+      case 3: return (uint64_t)R.ovl[r];
+      case 4: return (uint64_t)R.tmin[r];
+      case 5: return (uint64_t)R.tmax[r];
+      default: return R.ctr[(int64_t)(f - 6) * R.cap + r];
+    }
+  }
+};
+
+struct Overflow {
+  uint32_t* count;   // entries requested
+  uint32_t* lost;    // sticky: set when an entry did not fit
+  uint32_t* row;
+  uint64_t* val;     // [kMaxFields][cap]
+  int64_t cap;
+};
+
+__device__ inline void store_field(RowsDev& R, int f, uint32_t row,
+                                   uint64_t v) {
+  switch (f) {
+    case 0: R.n[row] = v; break;
+    case 1: R.dur[row] = (int64_t)v; break;
+    case 2: R.gap[row] = (int64_t)v; break;
+    case 3: R.ovl[row] = (int64_t)v; break;
+    case 4: R.tmin[row] = (int64_t)v; break;
+    case 5: R.tmax[row] = (int64_t)v; break;
+    default: R.ctr[(int64_t)(f - 6) * R.cap + row] = v; break;
+  }
+}
+
+__device__ inline void atomic_field(RowsDev& R, int f, uint32_t row,
+                                    uint64_t v) {
+  switch (f) {
+    case 0: atomicAdd((unsigned long long*)&R.n[row], (unsigned long long)v); break;
+    case 1: atomicAdd((unsigned long long*)&R.dur[row], (unsigned long long)v); break;
+    case 2: atomicAdd((unsigned long long*)&R.gap[row], (unsigned long long)v); break;
+    case 3: atomicAdd((unsigned long long*)&R.ovl[row], (unsigned long long)v); break;
+    case 4: atomicMin((long long*)&R.tmin[row], (long long)v); break;
+    case 5: atomicMax((long long*)&R.tmax[row], (long long)v); break;
+    default:
+      atomicAdd((unsigned long long*)&R.ctr[(int64_t)(f - 6) * R.cap + row],
+                (unsigned long long)v);
+      break;
+  }
+}
+
+template <typename Src>
+__global__ __launch_bounds__(kBlock) void k_agg_reduce(
+    Src src, int li, int D, int64_t M, bool atomic_mode, const uint32_t* own,
+    const uint32_t* rowof, RowsDev R, Overflow ovf, int nfields,
+    uint32_t* status) {
+  __shared__ uint32_t s_last[kBlock];
+  __shared__ uint32_t s_head0[kBlock];
+  const int64_t cnt = src.count();
+  const int64_t base = (int64_t)blockIdx.x * kAggTile;
+  if (base >= cnt) return;   // uniform: whole block
+  uint32_t rid[kAggIpt], tgt[kAggIpt];
+  bool head[kAggIpt], last[kAggIpt], valid[kAggIpt];
+  uint64_t ownbit[kAggIpt];
+  bool conflict = false;
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int64_t i = base + (int64_t)threadIdx.x * kAggIpt + j;
+    valid[j] = i < cnt;
+    tgt[j] = kNone;
+    ownbit[j] = 0;
+    rid[j] = 0;
+    if (!valid[j]) continue;
+    uint32_t p[8], g, kind, fpos;
+    bool ok;
+    src.load(i, rid[j], ok, p, g, kind, fpos);
+    if (!ok) continue;
+    const uint32_t key = group_key(p, D, M, li, g, kind);
+    if (key == kNone) continue;
+    const uint32_t row = rowof[key];
+    tgt[j] = row;
+    ownbit[j] = (!atomic_mode && own[key] == fpos) ? 1ull : 0ull;
+    if (li < D && (int64_t)row < R.cap) {
+      for (int l = 0; l <= li; ++l)
+        if (R.path[(int64_t)l * R.cap + row] != p[l]) conflict = true;
+    }
+  }
+  if (__ballot(conflict) != 0 && (threadIdx.x & (kWave - 1)) == 0)
+    atomicOr(status, (uint32_t)CHOPPER_ST_PATH_CONFLICT);
+  // piece boundaries
+  s_last[threadIdx.x] = tgt[kAggIpt - 1];
+  __syncthreads();
+  uint32_t prev = threadIdx.x > 0 ? s_last[threadIdx.x - 1] : kNone;
+  for (int j = 0; j < kAggIpt; ++j) {
+    head[j] = (threadIdx.x == 0 && j == 0) || !valid[j] || tgt[j] != prev;
+    prev = tgt[j];
+  }
+  s_head0[threadIdx.x] = head[0] ? 1u : 0u;
+  __syncthreads();
+  for (int j = 0; j < kAggIpt; ++j) {
+    bool next_head;
+    if (j + 1 < kAggIpt) next_head = head[j + 1];
+    else next_head = threadIdx.x + 1 < kBlock ? s_head0[threadIdx.x + 1] != 0 : true;
+    last[j] = valid[j] && tgt[j] != kNone && next_head;
+  }
+  // is the piece the first piece of its row? (propagated from the head)
+  seg_scan(head, ownbit, 0ull, CombLeft());
+  // overflow slots for non-first pieces
+  uint32_t slot[kAggIpt];
+  for (int j = 0; j < kAggIpt; ++j) {
+    slot[j] = kNone;
+    if (last[j] && !atomic_mode && ownbit[j] == 0 && (int64_t)tgt[j] < R.cap) {
+      uint32_t e = atomicAdd(ovf.count, 1u);
+      if ((int64_t)e < ovf.cap) {
+        slot[j] = e;
+        ovf.row[e] = tgt[j];
+      } else {
+        atomicOr(ovf.lost, 1u);
+      }
+    }
+  }
+  for (int f = 0; f < nfields; ++f) {
+    uint64_t x[kAggIpt];
+    for (int j = 0; j < kAggIpt; ++j) {
+      const bool use = valid[j] && tgt[j] != kNone;
+      if (f == 4) x[j] = use ? src.field(f, rid[j]) : (uint64_t)kI64Max;
+      else if (f == 5) x[j] = use ? src.field(f, rid[j]) : (uint64_t)kI64Min;
+      else x[j] = use ? src.field(f, rid[j]) : 0ull;
+    }
+    if (f == 4) seg_scan(head, x, (uint64_t)kI64Max, CombMin());
+    else if (f == 5) seg_scan(head, x, (uint64_t)kI64Min, CombMax());
+    else seg_scan(head, x, 0ull, CombAdd());
+    for (int j = 0; j < kAggIpt; ++j) {
+      if (!last[j] || (int64_t)tgt[j] >= R.cap) continue;
+      if (atomic_mode) atomic_field(R, f, tgt[j], x[j]);
+      else if (ownbit[j]) store_field(R, f, tgt[j], x[j]);
+      else if (slot[j] != kNone) ovf.val[(int64_t)f * ovf.cap + slot[j]] = x[j];
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_agg_apply_overflow(
+    Overflow ovf, RowsDev R, int nfields) {
+  const int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  int64_t cnt = *ovf.count;
+  if (cnt > ovf.cap) cnt = ovf.cap;
+  if (e >= cnt) return;
+  const uint32_t row = ovf.row[e];
+  for (int f = 0; f < nfields; ++f)
+    atomic_field(R, f, row, ovf.val[(int64_t)f * ovf.cap + e]);
+}
+
+// zero the sums of rows [level_offset[a], level_offset[b]) (atomic re-run)
+__global__ __launch_bounds__(kBlock) void k_agg_zero_rows(
+    const int64_t* level_offset, int a, int b, RowsDev R) {
+  int64_t lo = level_offset[a], hi = level_offset[b];
+  if (hi > R.cap) hi = R.cap;
+  for (int64_t row = lo + (int64_t)blockIdx.x * kBlock + threadIdx.x; row < hi;
+       row += (int64_t)gridDim.x * kBlock) {
+    R.n[row] = 0;
+    R.dur[row] = 0;
+    R.gap[row] = 0;
+    R.ovl[row] = 0;
+    R.tmin[row] = kI64Max;
+    R.tmax[row] = kI64Min;
+    for (int q = 0; q < R.nc; ++q) R.ctr[(int64_t)q * R.cap + row] = 0;
+  }
+}
+
+__global__ void k_fill_u32_many(uint32_t** p, const int64_t* counts, int L,
+                                uint32_t act) {
+  const int li = blockIdx.y;
+  if (li >= L || !((act >> li) & 1u)) return;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+       i < counts[li]; i += (int64_t)gridDim.x * blockDim.x)
+    p[li][i] = 0xFFFFFFFFu;
+}
+
+__global__ void k_zero_u32(uint32_t* p, int n) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+// ---------------------------------------------------------------------------
+struct AggLayout {
+  int L;
+  int64_t ntiles;
+  uint32_t* own[kMaxLevels];
+  uint32_t* rowof[kMaxLevels];
+  int64_t ks[kMaxLevels];
+  uint32_t** own_tab;     // device copies of the pointer tables
+  uint32_t** rowof_tab;
+  int64_t* ks_dev;
+  uint32_t* tilecnt;
+  uint32_t* tilebase;
+  uint32_t* scantmp;
+  uint32_t* total;
+  uint32_t* firstpos;
+  uint32_t* ovf_count;    // [2]: count, lost
+  uint32_t* ovf_row;
+  uint64_t* ovf_val;
+  int64_t ovf_cap;
+};
+
+static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
+                            int64_t cap, uint32_t act) {
+  AggLayout L;
+  L.L = D + 2;
+  L.ntiles = ceil_div(n, kAggTile);
+  for (int li = 0; li < L.L; ++li) {
+    L.ks[li] = ((act >> li) & 1u) ? key_space(li, D, M) : 1;
+    L.own[li] = sc.take<uint32_t>(L.ks[li]);
+    L.rowof[li] = sc.take<uint32_t>(L.ks[li]);
+  }
+  L.own_tab = sc.take<uint32_t*>(kMaxLevels);
+  L.rowof_tab = sc.take<uint32_t*>(kMaxLevels);
+  L.ks_dev = sc.take<int64_t>(kMaxLevels);
+  L.tilecnt = sc.take<uint32_t>((int64_t)L.L * L.ntiles);
+  L.tilebase = sc.take<uint32_t>((int64_t)L.L * L.ntiles);
+  L.scantmp = sc.take<uint32_t>(scan_scratch_elems((int64_t)L.L * L.ntiles));
+  L.total = sc.take<uint32_t>(1);
+  L.firstpos = sc.take<uint32_t>(cap);
+  L.ovf_cap = n / 64 > 65536 ? n / 64 : 65536;
+  L.ovf_count = sc.take<uint32_t>(2);
+  L.ovf_row = sc.take<uint32_t>(L.ovf_cap);
+  L.ovf_val = sc.take<uint64_t>((int64_t)kMaxFields * L.ovf_cap);
+  return L;
+}
+
+}  // namespace chopper
+
+using namespace chopper;
+
+extern "C" int chopper_aggregate(const chopper_records* rec,
+                                 const int64_t* start_al,
+                                 const int64_t* end_al, const uint32_t* korder,
+                                 const uint32_t* idx, int32_t depth,
+                                 const int64_t* gap, const int64_t* ovl,
+                                 const chopper_markers* mk, int32_t level,
+                                 const chopper_filter* filter,
+                                 chopper_rows* rows, void* scratch,
+                                 size_t* scratch_bytes, uint32_t* status,
+                                 void* stream) {
+  if (!validate_records(rec) || !validate_markers(mk) || !rows ||
+      !scratch_bytes)
+    return CHOPPER_EINVAL;
+  const int64_t n = rec->n;
+  const int D = depth;
+  if (D < 0 || D > 8) return CHOPPER_EINVAL;
+  if (mk && mk->depth != D) return CHOPPER_EINVAL;
+  const int64_t M = mk ? mk->n : 0;
+  if (filter && filter->use_iter && (!mk || (M > 0 && !mk->label)))
+    return CHOPPER_EINVAL;
+  if (n > 0 && (!start_al || !end_al || !korder || !gap || !ovl ||
+                (D > 0 && !idx)))
+    return CHOPPER_EINVAL;
+  if (rows->cap < 0 || !rows->level_offset) return CHOPPER_EINVAL;
+  if (rows->cap > 0 && (!rows->gpu || !rows->kind || !rows->n || !rows->dur ||
+                        !rows->gap || !rows->ovl || !rows->tmin ||
+                        !rows->tmax || !rows->first ||
+                        (D > 0 && !rows->path) ||
+                        (rec->n_counters > 0 && !rows->ctr)))
+    return CHOPPER_EINVAL;
+  uint32_t act = 0;
+  if (level == CHOPPER_LEVEL_ALL) act = (1u << (D + 2)) - 1u;
+  else if (level >= 0 && level < D) act = 1u << level;
+  else if (level == CHOPPER_LEVEL_GPU) act = 1u << D;
+  else if (level == CHOPPER_LEVEL_WORKLOAD) act = 1u << (D + 1);
+  else return CHOPPER_EINVAL;
+
+  Scratch probe(nullptr);
+  agg_layout(probe, n, D, M, rows->cap, act);
+  int rc = scratch_check(scratch, scratch_bytes, probe.used);
+  if (rc != 0) return rc > 0 ? CHOPPER_OK : rc;
+  if (!status) return CHOPPER_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  Scratch sc(scratch);
+  AggLayout L = agg_layout(sc, n, D, M, rows->cap, act);
+  const int Lv = L.L;
+  const int64_t T = L.ntiles;
+  const int nc = rec->n_counters;
+  const int nfields = 6 + nc;
+
+  RecSrc S;
+  S.n = n;
+  S.D = D;
+  S.M = M;
+  S.korder = korder;
+  S.gpu = rec->gpu;
+  S.cls = rec->cls;
+  S.start = start_al;
+  S.end = end_al;
+  S.idx = idx;
+  S.gap = gap;
+  S.ovl = ovl;
+  S.ctr = rec->counters;
+  S.nc = nc;
+  S.mlabel = mk ? mk->label : nullptr;
+  memset(&S.f, 0, sizeof(S.f));
+  if (filter) {
+    for (int q = 0; q < 4; ++q) S.f.gpu_mask[q] = filter->gpu_mask[q];
+    S.f.class_mask = filter->class_mask;
+    S.f.use_iter = filter->use_iter;
+    S.f.iter_lo = filter->iter_lo;
+    S.f.iter_hi = filter->iter_hi;
+    S.f.active = 1;
+  }
+  RowsDev R;
+  R.cap = rows->cap;
+  R.path = rows->path;
+  R.gpu = rows->gpu;
+  R.kind = rows->kind;
+  R.n = rows->n;
+  R.dur = rows->dur;
+  R.gap = rows->gap;
+  R.ovl = rows->ovl;
+  R.tmin = rows->tmin;
+  R.tmax = rows->tmax;
+  R.first = rows->first;
+  R.ctr = rows->ctr;
+  R.firstpos = L.firstpos;
+  R.D = D;
+  R.nc = nc;
+
+  // pointer tables for the per-level owner / row maps
+  CHOPPER_HIP(hipMemcpyAsync(L.own_tab, L.own, sizeof(L.own),
+                             hipMemcpyHostToDevice, s));
+  CHOPPER_HIP(hipMemcpyAsync(L.rowof_tab, L.rowof, sizeof(L.rowof),
+                             hipMemcpyHostToDevice, s));
+  CHOPPER_HIP(hipMemcpyAsync(L.ks_dev, L.ks, sizeof(L.ks),
+                             hipMemcpyHostToDevice, s));
+  int64_t maxks = 1;
+  for (int li = 0; li < Lv; ++li) maxks = L.ks[li] > maxks ? L.ks[li] : maxks;
+  unsigned fx = (unsigned)ceil_div(maxks, kBlock);
+  if (fx > 4096) fx = 4096;
+  CHOPPER_HIP(launch("agg_fill_owner", k_fill_u32_many, dim3(fx, Lv),
+                     dim3(kBlock), s, L.own_tab, (const int64_t*)L.ks_dev, Lv,
+                     act));
+  const uint32_t atomic_levels = (1u << D) | (1u << (D + 1));
+  if (n > 0) {
+    CHOPPER_HIP(launch("agg_elect", k_agg_elect, dim3((unsigned)T),
+                       dim3(kBlock), s, S, act, L.own_tab));
+    CHOPPER_HIP(launch("agg_count", k_agg_count, dim3((unsigned)T),
+                       dim3(kBlock), s, S, act, L.own_tab, T, L.tilecnt));
+  }
+  CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilecnt, L.tilebase, (int64_t)Lv * T,
+                                       L.scantmp, L.total, s));
+  CHOPPER_HIP(launch("agg_offsets", k_agg_offsets, dim3(1), dim3(64), s, Lv, T,
+                     (const uint32_t*)L.tilebase, (const uint32_t*)L.total,
+                     rows->cap, rows->level_offset, status));
+  if (n == 0) return CHOPPER_OK;
+  CHOPPER_HIP(launch("agg_assign", k_agg_assign, dim3((unsigned)T),
+                     dim3(kBlock), s, S, act, atomic_levels, L.own_tab,
+                     L.rowof_tab, T, (const uint32_t*)L.tilebase, R));
+  CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
+                     L.ovf_count, 2));
+  Overflow ovf{L.ovf_count, L.ovf_count + 1, L.ovf_row, L.ovf_val, L.ovf_cap};
+
+  // order of work: finest marker level from records, coarser marker levels
+  // from the rows below, GPU rows from level-0 rows, workload from GPU rows
+  auto run_level = [&](int li, bool atomic_mode) -> int {
+    int finer = -1;                       // level whose rows feed this one
+    if (level == CHOPPER_LEVEL_ALL) {
+      if (li < D - 1) finer = li + 1;
+      else if (li == D && D > 0) finer = 0;
+      else if (li == D + 1) finer = D;
+    }
+    if (!atomic_mode)
+      CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
+                         L.ovf_count, 1));
+    if (finer < 0) {
+      FromRecords src{S};
+      CHOPPER_HIP(launch("agg_reduce_records", k_agg_reduce<FromRecords>,
+                         dim3((unsigned)T), dim3(kBlock), s, src, li, D, M,
+                         atomic_mode, (const uint32_t*)L.own[li],
+                         (const uint32_t*)L.rowof[li], R, ovf, nfields,
+                         status));
+    } else {
+      FromRows src{R, 0, 0, rows->level_offset, finer};
+      // rows of the finer level never outnumber the records
+      CHOPPER_HIP(launch("agg_reduce_rows", k_agg_reduce<FromRows>,
+                         dim3((unsigned)T), dim3(kBlock), s, src, li, D, M,
+                         atomic_mode, (const uint32_t*)L.own[li],
+                         (const uint32_t*)L.rowof[li], R, ovf, nfields,
+                         status));
+    }
+    if (!atomic_mode)
+      CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
+                         grid_for(L.ovf_cap, kBlock), dim3(kBlock), s, ovf, R,
+                         nfields));
+    return CHOPPER_OK;
+  };
+  int order_levels[kMaxLevels];
+  int nl = 0;
+  for (int li = D - 1; li >= 0; --li)
+    if ((act >> li) & 1u) order_levels[nl++] = li;
+  if ((act >> D) & 1u) order_levels[nl++] = D;
+  if ((act >> (D + 1)) & 1u) order_levels[nl++] = D + 1;
+  for (int q = 0; q < nl; ++q) {
+    const int li = order_levels[q];
+    rc = run_level(li, (atomic_levels >> li) & 1u);
+    if (rc != CHOPPER_OK) return rc;
+  }
+  // an overflow list that did not fit: redo the marker levels with atomics
+  uint32_t lost = 0;
+  CHOPPER_HIP(hipMemcpyAsync(&lost, L.ovf_count + 1, sizeof(uint32_t),
+                             hipMemcpyDeviceToHost, s));
+  CHOPPER_HIP(hipStreamSynchronize(s));
+  if (lost) {
+    for (int q = 0; q < nl; ++q) {
+      const int li = order_levels[q];
+      CHOPPER_HIP(launch("agg_zero_rows", k_agg_zero_rows, dim3(1024),
+                         dim3(kBlock), s, (const int64_t*)rows->level_offset,
+                         li, li + 1, R));
+      rc = run_level(li, true);
+      if (rc != CHOPPER_OK) return rc;
+    }
+  }
+  return CHOPPER_OK;
+}

@@ -1,0 +1,336 @@
+// chopper_align: clock fit (host), fused per-GPU clock transform of every
+// record and marker timestamp (one 64x64->128-bit product per timestamp), and
+// the two stable record orders.  Paper: Section III-B (alignment of traces so
+// that counters attach to operations, layers and iterations).
+#include <algorithm>
+#include <vector>
+
+#include "sort.h"
+
+namespace chopper {
+
+typedef __int128 int128;
+typedef unsigned __int128 uint128;
+
+struct ClockDev {
+  int64_t x0, c, d;
+};
+
+// ---------------------------------------------------------------------------
+// Host clock fit
+// ---------------------------------------------------------------------------
+// floor(p / q) and the remainder, q > 0
+static void floor_divmod(int128 p, int128 q, int128* f, int128* r) {
+  int128 a = p / q, b = p % q;
+  if (b < 0) { a -= 1; b += q; }
+  *f = a;
+  *r = b;
+}
+
+// nearest integer to p / q (q > 0), ties to even
+static int128 round_even(int128 p, int128 q) {
+  int128 f, r;
+  floor_divmod(p, q, &f, &r);
+  int128 twice = r + r;
+  if (twice > q) return f + 1;
+  if (twice == q) return (f & 1) ? f + 1 : f;
+  return f;
+}
+
+// nearest integer to |num| * 2^48 / den for 0 < den < 2^126, ties to even;
+// the quotient is produced one bit at a time so no intermediate exceeds
+// 2 * den.  Returns false when the result would reach 2^38.
+static bool q48_quotient(uint128 num, uint128 den, uint128* out) {
+  uint128 q = num / den;
+  uint128 r = num % den;
+  if (q >> 38) return false;
+  for (int i = 0; i < 48; ++i) {
+    r <<= 1;
+    q <<= 1;
+    if (r >= den) {
+      r -= den;
+      q |= 1;
+    }
+  }
+  uint128 r2 = r << 1;
+  if (r2 > den || (r2 == den && (q & 1))) q += 1;
+  if (q >> 38) return false;
+  *out = q;
+  return true;
+}
+
+static int fit_clocks(const chopper_anchors* anc, int n_gpus,
+                      chopper_clock* out) {
+  for (int g = 0; g < n_gpus; ++g) out[g] = chopper_clock{0, 0, 0};
+  if (!anc || anc->n == 0) return CHOPPER_OK;
+  std::vector<std::vector<std::pair<int64_t, int64_t>>> per(n_gpus);
+  for (int64_t j = 0; j < anc->n; ++j) {
+    int g = anc->gpu[j];
+    if (g >= n_gpus) return CHOPPER_EINVAL;
+    per[g].push_back({anc->local_ns[j], anc->ref_ns[j]});
+  }
+  const int128 lim_u = (int128)1 << 42, lim_w = (int128)1 << 40;
+  for (int g = 0; g < n_gpus; ++g) {
+    auto& v = per[g];
+    if (v.empty()) continue;
+    if (v.size() > ((size_t)1 << 20)) return CHOPPER_EOVERFLOW;
+    std::sort(v.begin(), v.end());
+    const int64_t x0 = v[0].first;
+    int128 su = 0, sw = 0, suu = 0, suw = 0;
+    for (auto& p : v) {
+      int128 u = (int128)p.first - x0;
+      int128 w = (int128)p.second - p.first;
+      if (u >= lim_u || w >= lim_w || w <= -lim_w) return CHOPPER_EOVERFLOW;
+      su += u;
+      sw += w;
+      suu += u * u;
+      suw += u * w;
+    }
+    const int128 cnt = (int128)v.size();
+    const int128 den = cnt * suu - su * su;
+    const int128 num = cnt * suw - su * sw;
+    int128 d = 0;
+    if (cnt > 1 && den > 0) {
+      uint128 mag;
+      bool neg = num < 0;
+      if (!q48_quotient((uint128)(neg ? -num : num), (uint128)den, &mag))
+        return CHOPPER_EOVERFLOW;
+      d = neg ? -(int128)mag : (int128)mag;
+    }
+    const int128 one48 = (int128)1 << 48;
+    int128 c = round_even(sw * one48 - d * su, cnt * one48);
+    out[g] = chopper_clock{x0, (int64_t)c, (int64_t)d};
+  }
+  return CHOPPER_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Device transform
+// ---------------------------------------------------------------------------
+// t + c + floor((t - x0) * d / 2^48): the signed 128-bit product is formed
+// from __mul64hi and the low 64-bit product; the floor division by 2^48 is
+// the arithmetic shift of that 128-bit value.
+__device__ inline int64_t align_time(int64_t t, ClockDev k) {
+  const int64_t u = t - k.x0;
+  const int64_t hi = __mul64hi(u, k.d);
+  const uint64_t lo = (uint64_t)u * (uint64_t)k.d;
+  const int64_t q = (int64_t)(((uint64_t)hi << 16) | (lo >> 48));
+  return t + k.c + q;
+}
+
+__device__ inline bool out_of_range(int64_t t) {
+  const int64_t lim = (int64_t)1 << 62;
+  return t >= lim || t <= -lim;
+}
+
+__device__ inline void status_or(uint32_t* status, uint32_t bits) {
+  // one atomic per wave that has anything to report
+  uint32_t v = bits;
+  for (int d = kWave / 2; d > 0; d >>= 1) v |= __shfl_xor(v, d, kWave);
+  if ((threadIdx.x & (kWave - 1)) == 0 && v) atomicOr(status, v);
+}
+
+__global__ __launch_bounds__(kBlock) void k_transform_records(
+    int64_t n, int n_gpus, const uint8_t* gpu, const uint8_t* stream,
+    const uint8_t* cls, const int64_t* start, const int64_t* end,
+    const ClockDev* clk, int64_t* s_out, int64_t* e_out, uint32_t* pres_s,
+    uint32_t* pres_k, uint32_t* status) {
+  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  uint32_t st = 0;
+  if (i < n) {
+    const uint32_t g = gpu[i];
+    const uint32_t c = cls[i];
+    const int64_t s = start[i], e = end[i];
+    ClockDev k{0, 0, 0};
+    if ((int)g < n_gpus) k = clk[g];
+    else st |= CHOPPER_ST_BAD_GPU;
+    if (c >= 8) st |= CHOPPER_ST_BAD_CLASS;
+    if (e < s) st |= CHOPPER_ST_NEG_DURATION;
+    const int64_t s2 = align_time(s, k), e2 = align_time(e, k);
+    if (out_of_range(s) || out_of_range(e) || out_of_range(s2) ||
+        out_of_range(e2))
+      st |= CHOPPER_ST_RANGE;
+    s_out[i] = s2;
+    e_out[i] = e2;
+    pres_s[g * 256u + stream[i]] = 1u;
+    pres_k[g * 2u + (uint32_t)kind_of(c)] = 1u;
+  }
+  status_or(status, st);
+}
+
+__global__ __launch_bounds__(kBlock) void k_transform_markers(
+    int64_t n, int n_gpus, int depth, const uint8_t* gpu, const uint8_t* level,
+    const int64_t* start, const int64_t* end, const ClockDev* clk,
+    int64_t* s_out, int64_t* e_out, uint32_t* status) {
+  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  uint32_t st = 0;
+  if (i < n) {
+    const uint32_t g = gpu[i];
+    const int64_t s = start[i], e = end[i];
+    ClockDev k{0, 0, 0};
+    if ((int)g < n_gpus) k = clk[g];
+    else st |= CHOPPER_ST_BAD_GPU;
+    if ((int)level[i] >= depth) st |= CHOPPER_ST_BAD_LEVEL;
+    if (e < s) st |= CHOPPER_ST_NEG_DURATION;
+    const int64_t s2 = align_time(s, k), e2 = align_time(e, k);
+    if (out_of_range(s) || out_of_range(e) || out_of_range(s2) ||
+        out_of_range(e2))
+      st |= CHOPPER_ST_RANGE;
+    s_out[i] = s2;
+    e_out[i] = e2;
+  }
+  status_or(status, st);
+}
+
+// Dense class ids in (gpu, stream) and (gpu, kind) order from presence flags.
+__global__ __launch_bounds__(kBlock) void k_dense_classes(
+    const uint32_t* pres_s, uint16_t* cmap_s, const uint32_t* pres_k,
+    uint16_t* cmap_k, uint32_t* counts) {
+  uint32_t carry = 0;
+  for (int base = 0; base < 65536; base += kBlock) {
+    uint32_t p = pres_s[base + threadIdx.x];
+    uint32_t tot;
+    uint32_t ex = block_exclusive(p, OpAdd(), 0u, &tot) + carry;
+    cmap_s[base + threadIdx.x] = (uint16_t)(p ? ex : 0u);
+    carry += tot;
+  }
+  if (threadIdx.x == 0) counts[0] = carry;
+  carry = 0;
+  for (int base = 0; base < 512; base += kBlock) {
+    uint32_t p = pres_k[base + threadIdx.x];
+    uint32_t tot;
+    uint32_t ex = block_exclusive(p, OpAdd(), 0u, &tot) + carry;
+    cmap_k[base + threadIdx.x] = (uint16_t)(p ? ex : 0u);
+    carry += tot;
+  }
+  if (threadIdx.x == 0) counts[1] = carry;
+}
+
+// ---------------------------------------------------------------------------
+// Entry point
+// ---------------------------------------------------------------------------
+struct AlignLayout {
+  ClockDev* clk;
+  uint32_t* pres_s;   // 65536 + 512, cleared together
+  uint32_t* pres_k;
+  uint16_t* cmap_s;
+  uint16_t* cmap_k;
+  uint32_t* counts;
+  uint32_t* coff;
+  ClassSortLayout sort;
+};
+
+static AlignLayout align_layout(Scratch& sc, int64_t n, int n_gpus) {
+  AlignLayout L;
+  L.clk = sc.take<ClockDev>(n_gpus);
+  L.pres_s = sc.take<uint32_t>(65536 + 512);
+  L.pres_k = L.pres_s ? L.pres_s + 65536 : nullptr;
+  L.cmap_s = sc.take<uint16_t>(65536);
+  L.cmap_k = sc.take<uint16_t>(512);
+  L.counts = sc.take<uint32_t>(4);
+  L.coff = sc.take<uint32_t>(65536 + 1);
+  L.sort = class_sort_layout(sc, n, 65536);
+  return L;
+}
+
+static bool records_ok(const chopper_records* r) {
+  if (!r || r->n < 0 || r->n >= (int64_t)0xFFFFFFFF) return false;
+  if (r->n_gpus < 1 || r->n_gpus > 256) return false;
+  if (r->n_counters < 0 || r->n_counters > 16) return false;
+  if (r->n > 0 && (!r->gpu || !r->stream || !r->cls || !r->start_ns ||
+                   !r->end_ns))
+    return false;
+  if (r->n > 0 && r->n_counters > 0 && !r->counters) return false;
+  return true;
+}
+
+static bool markers_ok(const chopper_markers* m) {
+  if (!m) return true;
+  if (m->n < 0 || m->n >= (int64_t)0xFFFFFFFF) return false;
+  if (m->depth < 1 || m->depth > 8) return false;
+  if (m->n > 0 && (!m->gpu || !m->level || !m->start_ns || !m->end_ns))
+    return false;
+  return true;
+}
+
+bool validate_records(const chopper_records* r) { return records_ok(r); }
+bool validate_markers(const chopper_markers* m) { return markers_ok(m); }
+
+}  // namespace chopper
+
+using namespace chopper;
+
+extern "C" int chopper_align(const chopper_records* rec,
+                             const chopper_markers* mk,
+                             const chopper_anchors* anc,
+                             chopper_clock* clocks_out, int64_t* start_out,
+                             int64_t* end_out, int64_t* mstart_out,
+                             int64_t* mend_out, uint32_t* order_out,
+                             uint32_t* korder_out, void* scratch,
+                             size_t* scratch_bytes, uint32_t* status,
+                             void* stream) {
+  if (!records_ok(rec) || !markers_ok(mk) || !clocks_out || !scratch_bytes)
+    return CHOPPER_EINVAL;
+  if (anc && anc->n < 0) return CHOPPER_EINVAL;
+  if (anc && anc->n > 0 && (!anc->gpu || !anc->local_ns || !anc->ref_ns))
+    return CHOPPER_EINVAL;
+  const int64_t n = rec->n;
+  const int64_t nm = mk ? mk->n : 0;
+  const int G = rec->n_gpus;
+  if (n > 0 && (!start_out || !end_out || !order_out || !korder_out))
+    return CHOPPER_EINVAL;
+  if (nm > 0 && (!mstart_out || !mend_out)) return CHOPPER_EINVAL;
+  Scratch probe(nullptr);
+  align_layout(probe, n, G);
+  int rc = scratch_check(scratch, scratch_bytes, probe.used);
+  if (rc != 0) return rc > 0 ? CHOPPER_OK : rc;
+  if (!status) return CHOPPER_EINVAL;
+
+  std::vector<chopper_clock> clocks(G);
+  rc = fit_clocks(anc, G, clocks.data());
+  if (rc != CHOPPER_OK) return rc;
+  for (int g = 0; g < G; ++g) clocks_out[g] = clocks[g];
+
+  hipStream_t s = (hipStream_t)stream;
+  Scratch sc(scratch);
+  AlignLayout L = align_layout(sc, n, G);
+  std::vector<ClockDev> cd(G);
+  for (int g = 0; g < G; ++g)
+    cd[g] = ClockDev{clocks[g].x0, clocks[g].c, clocks[g].d_q48};
+  CHOPPER_HIP(hipMemcpyAsync(L.clk, cd.data(), sizeof(ClockDev) * G,
+                             hipMemcpyHostToDevice, s));
+  if (nm > 0) {
+    CHOPPER_HIP(launch("align_transform_markers", k_transform_markers,
+                       grid_for(nm, kBlock), dim3(kBlock), s, nm, G, mk->depth,
+                       mk->gpu, mk->level, mk->start_ns, mk->end_ns,
+                       (const ClockDev*)L.clk, mstart_out, mend_out, status));
+  }
+  if (n == 0) return CHOPPER_OK;
+  CHOPPER_HIP(launch("align_fill", k_fill_u32, grid_for(65536 + 512, kBlock),
+                     dim3(kBlock), s, L.pres_s, (int64_t)(65536 + 512), 0u));
+  CHOPPER_HIP(launch("align_transform_records", k_transform_records,
+                     grid_for(n, kBlock), dim3(kBlock), s, n, G, rec->gpu,
+                     rec->stream, rec->cls, rec->start_ns, rec->end_ns,
+                     (const ClockDev*)L.clk, start_out, end_out, L.pres_s,
+                     L.pres_k, status));
+  CHOPPER_HIP(launch("align_dense_classes", k_dense_classes, dim3(1),
+                     dim3(kBlock), s, (const uint32_t*)L.pres_s, L.cmap_s,
+                     (const uint32_t*)L.pres_k, L.cmap_k, L.counts));
+  uint32_t counts[2];
+  CHOPPER_HIP(hipMemcpyAsync(counts, L.counts, sizeof(counts),
+                             hipMemcpyDeviceToHost, s));
+  CHOPPER_HIP(hipStreamSynchronize(s));
+  bool range_err = false, r2 = false;
+  KeyRecStream ks{rec->gpu, rec->stream, start_out, L.cmap_s, (int)counts[0]};
+  rc = class_sort(ks, L.sort, order_out, L.coff, &range_err, s);
+  if (rc != CHOPPER_OK) return rc;
+  KeyRecKind kk{rec->gpu, rec->cls, start_out, L.cmap_k, (int)counts[1]};
+  rc = class_sort(kk, L.sort, korder_out, L.coff, &r2, s);
+  if (rc != CHOPPER_OK) return rc;
+  if (range_err || r2) {
+    // fold the host-detected condition into the device status word
+    CHOPPER_HIP(launch("status_set", k_status_set, dim3(1), dim3(1), s,
+                       (uint32_t)CHOPPER_ST_RANGE, status));
+  }
+  return CHOPPER_OK;
+}

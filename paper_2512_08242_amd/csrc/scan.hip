@@ -1,0 +1,106 @@
+// Device-wide exclusive prefix sums (reduce-then-scan).
+//
+// Pass 1 sums each tile of kScanTile elements, pass 2 scans the tile sums in
+// a single block, pass 3 rescans every tile starting from its prefix.  Each
+// thread owns kScanIpt consecutive elements, so the block-level scan is paid
+// once per kScanIpt elements.
+#include "common.h"
+
+namespace chopper {
+
+constexpr int kScanIpt = 8;
+constexpr int kScanTile = kBlock * kScanIpt;
+
+int64_t scan_scratch_elems(int64_t n) { return ceil_div(n, kScanTile) + 1; }
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_scan_reduce(const T* in, int64_t n,
+                                                        T* tile_sum) {
+  const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  T acc = 0;
+  for (int j = 0; j < kScanIpt; ++j) {
+    int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
+    if (i < n) acc += in[i];
+  }
+  T tot;
+  block_exclusive(acc, OpAdd(), (T)0, &tot);
+  if (threadIdx.x == 0) tile_sum[blockIdx.x] = tot;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_scan_spine(T* tile_sum,
+                                                       int64_t ntiles,
+                                                       T* total) {
+  T carry = 0;
+  for (int64_t base = 0; base < ntiles; base += kScanTile) {
+    T v[kScanIpt];
+    T acc = 0;
+    for (int j = 0; j < kScanIpt; ++j) {
+      int64_t i = base + (int64_t)threadIdx.x * kScanIpt + j;
+      v[j] = (i < ntiles) ? tile_sum[i] : (T)0;
+      acc += v[j];
+    }
+    T tot;
+    T pre = block_exclusive(acc, OpAdd(), (T)0, &tot) + carry;
+    for (int j = 0; j < kScanIpt; ++j) {
+      int64_t i = base + (int64_t)threadIdx.x * kScanIpt + j;
+      if (i < ntiles) tile_sum[i] = pre;
+      pre += v[j];
+    }
+    carry += tot;
+  }
+  if (threadIdx.x == 0 && total) *total = carry;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_scan_down(const T* in, T* out,
+                                                      int64_t n,
+                                                      const T* tile_pre) {
+  const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  T v[kScanIpt];
+  T acc = 0;
+  for (int j = 0; j < kScanIpt; ++j) {
+    int64_t i = base + (int64_t)threadIdx.x * kScanIpt + j;
+    v[j] = (i < n) ? in[i] : (T)0;
+    acc += v[j];
+  }
+  T tot;
+  T pre = block_exclusive(acc, OpAdd(), (T)0, &tot) + tile_pre[blockIdx.x];
+  for (int j = 0; j < kScanIpt; ++j) {
+    int64_t i = base + (int64_t)threadIdx.x * kScanIpt + j;
+    if (i < n) out[i] = pre;
+    pre += v[j];
+  }
+}
+
+template <typename T>
+hipError_t exclusive_scan(const T* in, T* out, int64_t n, T* tmp, T* total,
+                          hipStream_t s) {
+  int64_t ntiles = ceil_div(n, kScanTile);
+  hipError_t e;
+  if (n <= 0) {
+    // total = 0
+    e = launch("scan_spine", k_scan_spine<T>, dim3(1), dim3(kBlock), s, tmp,
+               (int64_t)0, total);
+    return e;
+  }
+  e = launch("scan_reduce", k_scan_reduce<T>, dim3((unsigned)ntiles),
+             dim3(kBlock), s, in, n, tmp);
+  if (e != hipSuccess) return e;
+  e = launch("scan_spine", k_scan_spine<T>, dim3(1), dim3(kBlock), s, tmp,
+             ntiles, total);
+  if (e != hipSuccess) return e;
+  return launch("scan_down", k_scan_down<T>, dim3((unsigned)ntiles),
+                dim3(kBlock), s, in, out, n, (const T*)tmp);
+}
+
+template hipError_t exclusive_scan<uint32_t>(const uint32_t*, uint32_t*,
+                                             int64_t, uint32_t*, uint32_t*,
+                                             hipStream_t);
+template hipError_t exclusive_scan<int64_t>(const int64_t*, int64_t*, int64_t,
+                                            int64_t*, int64_t*, hipStream_t);
+template hipError_t exclusive_scan<uint64_t>(const uint64_t*, uint64_t*,
+                                             int64_t, uint64_t*, uint64_t*,
+                                             hipStream_t);
+
+}  // namespace chopper

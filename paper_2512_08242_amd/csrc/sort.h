@@ -1,0 +1,84 @@
+// Stable (class, time) sorts shared by chopper_align (record orders) and
+// chopper_attribute (marker index).
+#pragma once
+
+#include "common.h"
+
+namespace chopper {
+
+// Records keyed by (gpu, stream): dense class ids from a 256 x 256 table.
+struct KeyRecStream {
+  const uint8_t* gpu;
+  const uint8_t* stream;
+  const int64_t* t;
+  const uint16_t* cmap;   // [256 * 256]
+  int C;
+  __device__ uint32_t cls(int64_t i) const {
+    return cmap[(uint32_t)gpu[i] * 256u + stream[i]];
+  }
+  __device__ int64_t time(int64_t i) const { return t[i]; }
+  __host__ __device__ int nclass() const { return C; }
+};
+
+// Records keyed by (gpu, kind): dense class ids from a 256 x 2 table.
+struct KeyRecKind {
+  const uint8_t* gpu;
+  const uint8_t* cl;
+  const int64_t* t;
+  const uint16_t* cmap;   // [256 * 2]
+  int C;
+  __device__ uint32_t cls(int64_t i) const {
+    return cmap[(uint32_t)gpu[i] * 2u + (uint32_t)kind_of(cl[i])];
+  }
+  __device__ int64_t time(int64_t i) const { return t[i]; }
+  __host__ __device__ int nclass() const { return C; }
+};
+
+// Markers keyed by (gpu, level, empty): non-empty markers of a (gpu, level)
+// come first; markers with an invalid gpu or level go to the last class.
+struct KeyMarker {
+  const uint8_t* gpu;
+  const uint8_t* level;
+  const int64_t* ms;
+  const int64_t* me;
+  int G, D;
+  __device__ uint32_t cls(int64_t i) const {
+    uint32_t g = gpu[i], l = level[i];
+    if ((int)g >= G || (int)l >= D) return (uint32_t)(G * D * 2);
+    return (g * (uint32_t)D + l) * 2u + (me[i] <= ms[i] ? 1u : 0u);
+  }
+  __device__ int64_t time(int64_t i) const { return ms[i]; }
+  __host__ __device__ int nclass() const { return G * D * 2 + 1; }
+};
+
+struct ClassSortLayout {
+  int64_t n = 0;
+  int C = 0;
+  int64_t ntiles = 0;
+  uint32_t* tilehist = nullptr;
+  uint32_t* tileoff = nullptr;
+  uint32_t* scantmp = nullptr;
+  uint32_t* total = nullptr;
+  uint32_t* flag = nullptr;
+  int64_t* mm = nullptr;
+  uint64_t* key0 = nullptr;
+  uint64_t* key1 = nullptr;
+  uint32_t* val0 = nullptr;
+  uint32_t* val1 = nullptr;
+};
+
+int64_t sort_tiles(int64_t n);
+// Sized for up to c_max classes.
+ClassSortLayout class_sort_layout(Scratch& sc, int64_t n, int c_max);
+
+// out[n]: stable permutation by (class, time); coff[C + 1]: first position of
+// every class and n.  range_error: the packed key would need more than 64
+// bits (only possible on the general path).  May synchronize `s`.
+template <typename Acc>
+int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
+               uint32_t* coff, bool* range_error, hipStream_t s);
+
+__global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v);
+__global__ void k_status_set(uint32_t bits, uint32_t* status);
+
+}  // namespace chopper

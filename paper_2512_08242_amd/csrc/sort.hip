@@ -1,0 +1,408 @@
+// Stable sorts of items by (class, time) for gfx950.
+//
+// Fast path: a stable counting-sort pass by class (class ids are dense, at
+// most 256) followed by a check that every class run of the output is
+// non-decreasing in time.  When the input already lists each class in time
+// order -- what a profiler emits per GPU and stream -- that single pass is
+// the complete stable sort.
+//
+// General path: LSD radix sort of packed 64-bit keys (class << T | time -
+// tmin) with 8-bit digits.  Every pass: per-tile digit histograms in LDS, a
+// device-wide exclusive scan of the digit-major histogram table, then a
+// stable scatter whose in-tile ranks come from wave64 ballots (eight
+// __ballot calls match lanes with equal digits, popcount of the lower lanes
+// gives the rank) and per-wave digit counts in LDS.  Each tile is first
+// reordered in LDS so that the global writes of one digit bucket are
+// contiguous.
+#include "sort.h"
+
+namespace chopper {
+
+constexpr int kSortIpt = 8;
+constexpr int kSortTile = kBlock * kSortIpt;
+
+int64_t sort_tiles(int64_t n) { return ceil_div(n, kSortTile); }
+
+// ---------------------------------------------------------------------------
+// In-tile stable ranking of up to 256 digit values.
+// Items are striped: item j of thread t is tile position j * kBlock + t.
+// On return s_count[d] = number of valid items with digit d in the tile,
+// s_start[d] = exclusive prefix of s_count, rank[j] = stable position of the
+// item among equal digits.
+// ---------------------------------------------------------------------------
+struct RankShared {
+  uint32_t wave[kWavesPerBlock][256];
+  uint32_t count[256];
+  uint32_t start[256];
+};
+
+__device__ inline void tile_rank(const uint32_t (&dig)[kSortIpt],
+                                 const bool (&valid)[kSortIpt],
+                                 uint32_t (&rank)[kSortIpt], RankShared& sh) {
+  const int t = threadIdx.x;
+  const int lane = t & (kWave - 1);
+  const int w = t / kWave;
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int q = 0; q < kWavesPerBlock; ++q) sh.wave[q][t] = 0;
+  sh.count[t] = 0;
+  __syncthreads();
+  for (int j = 0; j < kSortIpt; ++j) {
+    const uint32_t d = dig[j];
+    const bool v = valid[j];
+    uint64_t peers = __ballot(v);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const uint64_t bb = __ballot(bit);
+      peers &= bit ? bb : ~bb;
+    }
+    const uint32_t rin = __popcll(peers & lt);
+    if (v && rin == 0) sh.wave[w][d] = __popcll(peers);
+    __syncthreads();
+    if (v) {
+      uint32_t pre = sh.count[d];
+      for (int q = 0; q < w; ++q) pre += sh.wave[q][d];
+      rank[j] = pre + rin;
+    }
+    __syncthreads();
+    uint32_t add = 0;
+    for (int q = 0; q < kWavesPerBlock; ++q) {
+      add += sh.wave[q][t];
+      sh.wave[q][t] = 0;
+    }
+    sh.count[t] += add;
+    __syncthreads();
+  }
+  uint32_t tot;
+  sh.start[t] = block_exclusive(sh.count[t], OpAdd(), 0u, &tot);
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// Class-partition fast path
+// ---------------------------------------------------------------------------
+template <typename Acc>
+__global__ __launch_bounds__(kBlock) void k_class_hist(Acc acc, int64_t n,
+                                                       int64_t ntiles,
+                                                       uint32_t* tilehist) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  for (int j = 0; j < kSortIpt; ++j) {
+    int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
+    if (i < n) atomicAdd(&h[acc.cls(i)], 1u);
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < acc.nclass())
+    tilehist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
+}
+
+template <typename Acc>
+__global__ __launch_bounds__(kBlock) void k_class_partition(
+    Acc acc, int64_t n, int64_t ntiles, const uint32_t* tileoff,
+    uint32_t* out) {
+  __shared__ RankShared sh;
+  __shared__ uint32_t s_val[kSortTile];
+  __shared__ uint8_t s_dig[kSortTile];
+  __shared__ uint32_t s_gbase[256];
+  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  uint32_t dig[kSortIpt], rank[kSortIpt];
+  bool valid[kSortIpt];
+  for (int j = 0; j < kSortIpt; ++j) {
+    int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
+    valid[j] = i < n;
+    dig[j] = valid[j] ? acc.cls(i) : 0u;
+  }
+  tile_rank(dig, valid, rank, sh);
+  if ((int)threadIdx.x < acc.nclass())
+    s_gbase[threadIdx.x] =
+        tileoff[(int64_t)threadIdx.x * ntiles + blockIdx.x];
+  for (int j = 0; j < kSortIpt; ++j) {
+    if (!valid[j]) continue;
+    uint32_t lp = sh.start[dig[j]] + rank[j];
+    s_val[lp] = (uint32_t)(base + (int64_t)j * kBlock + threadIdx.x);
+    s_dig[lp] = (uint8_t)dig[j];
+  }
+  __syncthreads();
+  const int64_t tile_n = (n - base) < kSortTile ? (n - base) : kSortTile;
+  for (int j = 0; j < kSortIpt; ++j) {
+    int q = j * kBlock + threadIdx.x;
+    if (q >= tile_n) continue;
+    uint32_t d = s_dig[q];
+    out[(int64_t)s_gbase[d] + (q - sh.start[d])] = s_val[q];
+  }
+}
+
+template <typename Acc>
+__global__ __launch_bounds__(kBlock) void k_class_verify(Acc acc, int64_t n,
+                                                         const uint32_t* perm,
+                                                         uint32_t* unsorted) {
+  int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  bool bad = false;
+  if (p + 1 < n) {
+    uint32_t a = perm[p], b = perm[p + 1];
+    bad = acc.cls(a) == acc.cls(b) && acc.time(b) < acc.time(a);
+  }
+  if (__ballot(bad) != 0 && (threadIdx.x & (kWave - 1)) == 0)
+    atomicOr(unsorted, 1u);
+}
+
+// class start offsets from the scanned table: coff[c] = first position of
+// class c, coff[C] = n
+__global__ void k_class_offsets(const uint32_t* tileoff, int64_t ntiles,
+                                int C, int64_t n, uint32_t* coff) {
+  int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c < C) coff[c] = ntiles > 0 ? tileoff[(int64_t)c * ntiles] : 0u;
+  if (c == C) coff[C] = (uint32_t)n;
+}
+
+// ---------------------------------------------------------------------------
+// General path: packed keys + LSD radix passes
+// ---------------------------------------------------------------------------
+template <typename Acc>
+__global__ __launch_bounds__(kBlock) void k_time_minmax(Acc acc, int64_t n,
+                                                        int64_t* mm) {
+  int64_t lo = kI64Max, hi = kI64Min;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kBlock) {
+    int64_t t = acc.time(i);
+    lo = t < lo ? t : lo;
+    hi = t > hi ? t : hi;
+  }
+  for (int d = kWave / 2; d > 0; d >>= 1) {
+    int64_t a = __shfl_xor(lo, d, kWave), b = __shfl_xor(hi, d, kWave);
+    lo = a < lo ? a : lo;
+    hi = b > hi ? b : hi;
+  }
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    atomicMin((long long*)&mm[0], (long long)lo);
+    atomicMax((long long*)&mm[1], (long long)hi);
+  }
+}
+
+__global__ void k_init_minmax(int64_t* mm) {
+  mm[0] = kI64Max;
+  mm[1] = kI64Min;
+}
+
+template <typename Acc>
+__global__ __launch_bounds__(kBlock) void k_make_keys(Acc acc, int64_t n,
+                                                      const int64_t* mm,
+                                                      int tbits, uint64_t* key,
+                                                      uint32_t* val) {
+  int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i >= n) return;
+  uint64_t t = (uint64_t)(acc.time(i) - mm[0]);
+  uint64_t c = acc.cls(i);
+  key[i] = (tbits >= 64 ? 0ull : (c << tbits)) | t;
+  val[i] = (uint32_t)i;
+}
+
+__global__ __launch_bounds__(kBlock) void k_digit_hist(const uint64_t* key,
+                                                       int64_t n, int shift,
+                                                       int64_t ntiles,
+                                                       uint32_t* tilehist) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  for (int j = 0; j < kSortIpt; ++j) {
+    int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
+    if (i < n) atomicAdd(&h[(uint32_t)(key[i] >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  tilehist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
+}
+
+__global__ __launch_bounds__(kBlock) void k_digit_scatter(
+    const uint64_t* key_in, const uint32_t* val_in, int64_t n, int shift,
+    int64_t ntiles, const uint32_t* tileoff, uint64_t* key_out,
+    uint32_t* val_out) {
+  __shared__ RankShared sh;
+  __shared__ uint64_t s_key[kSortTile];
+  __shared__ uint32_t s_val[kSortTile];
+  __shared__ uint32_t s_gbase[256];
+  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  uint32_t dig[kSortIpt], rank[kSortIpt];
+  bool valid[kSortIpt];
+  uint64_t k[kSortIpt];
+  uint32_t v[kSortIpt];
+  for (int j = 0; j < kSortIpt; ++j) {
+    int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
+    valid[j] = i < n;
+    k[j] = valid[j] ? key_in[i] : 0ull;
+    v[j] = valid[j] ? val_in[i] : 0u;
+    dig[j] = (uint32_t)(k[j] >> shift) & 255u;
+  }
+  tile_rank(dig, valid, rank, sh);
+  s_gbase[threadIdx.x] = tileoff[(int64_t)threadIdx.x * ntiles + blockIdx.x];
+  for (int j = 0; j < kSortIpt; ++j) {
+    if (!valid[j]) continue;
+    uint32_t lp = sh.start[dig[j]] + rank[j];
+    s_key[lp] = k[j];
+    s_val[lp] = v[j];
+  }
+  __syncthreads();
+  const int64_t tile_n = (n - base) < kSortTile ? (n - base) : kSortTile;
+  for (int j = 0; j < kSortIpt; ++j) {
+    int q = j * kBlock + threadIdx.x;
+    if (q >= tile_n) continue;
+    uint64_t kk = s_key[q];
+    uint32_t d = (uint32_t)(kk >> shift) & 255u;
+    int64_t pos = (int64_t)s_gbase[d] + (q - sh.start[d]);
+    if (key_out) key_out[pos] = kk;
+    val_out[pos] = s_val[q];
+  }
+}
+
+// class histogram for more than 256 classes (general path only)
+template <typename Acc>
+__global__ __launch_bounds__(kBlock) void k_class_count_global(
+    Acc acc, int64_t n, uint32_t* counts) {
+  int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i < n) atomicAdd(&counts[acc.cls(i)], 1u);
+}
+
+__global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+__global__ void k_status_set(uint32_t bits, uint32_t* status) {
+  atomicOr(status, bits);
+}
+
+// ---------------------------------------------------------------------------
+// Host driver
+// ---------------------------------------------------------------------------
+static int bitlen_u64(uint64_t x) {
+  int b = 0;
+  while (x) { ++b; x >>= 1; }
+  return b;
+}
+
+ClassSortLayout class_sort_layout(Scratch& sc, int64_t n, int C) {
+  ClassSortLayout L;
+  L.n = n;
+  L.C = C;   // maximum number of classes the tables are sized for
+  L.ntiles = sort_tiles(n);
+  int64_t hist_elems = (int64_t)(C > 256 ? 256 : C) * L.ntiles;
+  int64_t radix_elems = 256 * L.ntiles;
+  int64_t tab = hist_elems > radix_elems ? hist_elems : radix_elems;
+  if (C > 256 && C > tab) tab = C;
+  L.tilehist = sc.take<uint32_t>(tab);
+  L.tileoff = sc.take<uint32_t>(tab);
+  L.scantmp = sc.take<uint32_t>(scan_scratch_elems(tab));
+  L.total = sc.take<uint32_t>(4);
+  L.flag = sc.take<uint32_t>(4);
+  L.mm = sc.take<int64_t>(2);
+  L.key0 = sc.take<uint64_t>(n);
+  L.key1 = sc.take<uint64_t>(n);
+  L.val0 = sc.take<uint32_t>(n);
+  L.val1 = sc.take<uint32_t>(n);
+  return L;
+}
+
+template <typename Acc>
+int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
+               uint32_t* coff, bool* range_error, hipStream_t s) {
+  const int64_t n = L.n;
+  const int C = acc.nclass();
+  const int64_t T = L.ntiles;
+  if (C > L.C) return CHOPPER_EINVAL;
+  *range_error = false;
+  if (n == 0) {
+    CHOPPER_HIP(launch("sort_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
+                       coff, (int64_t)(C + 1), 0u));
+    return CHOPPER_OK;
+  }
+  bool sorted = false;
+  if (C <= 256) {
+    CHOPPER_HIP(launch("sort_class_hist", k_class_hist<Acc>, dim3((unsigned)T),
+                       dim3(kBlock), s, acc, n, T, L.tilehist));
+    CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, L.tileoff, (int64_t)C * T,
+                                         L.scantmp, L.total, s));
+    CHOPPER_HIP(launch("sort_class_offsets", k_class_offsets,
+                       grid_for(C + 1, kBlock), dim3(kBlock), s,
+                       (const uint32_t*)L.tileoff, T, C, n, coff));
+    CHOPPER_HIP(launch("sort_class_partition", k_class_partition<Acc>,
+                       dim3((unsigned)T), dim3(kBlock), s, acc, n, T,
+                       (const uint32_t*)L.tileoff, out));
+    CHOPPER_HIP(launch("sort_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
+                       L.flag, (int64_t)1, 0u));
+    CHOPPER_HIP(launch("sort_class_verify", k_class_verify<Acc>,
+                       grid_for(n, kBlock), dim3(kBlock), s, acc, n,
+                       (const uint32_t*)out, L.flag));
+    uint32_t unsorted = 1;
+    CHOPPER_HIP(hipMemcpyAsync(&unsorted, L.flag, sizeof(uint32_t),
+                               hipMemcpyDeviceToHost, s));
+    CHOPPER_HIP(hipStreamSynchronize(s));
+    sorted = (unsorted == 0);
+  } else {
+    CHOPPER_HIP(launch("sort_fill", k_fill_u32, grid_for(C, kBlock),
+                       dim3(kBlock), s, L.tilehist, (int64_t)C, 0u));
+    CHOPPER_HIP(launch("sort_class_count", k_class_count_global<Acc>,
+                       grid_for(n, kBlock), dim3(kBlock), s, acc, n,
+                       L.tilehist));
+    CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, coff, (int64_t)C,
+                                         L.scantmp, coff + C, s));
+  }
+  if (sorted) return CHOPPER_OK;
+
+  // general path
+  CHOPPER_HIP(launch("sort_init_minmax", k_init_minmax, dim3(1), dim3(1), s,
+                     L.mm));
+  CHOPPER_HIP(launch("sort_time_minmax", k_time_minmax<Acc>,
+                     dim3((unsigned)(T < 1024 ? T : 1024)), dim3(kBlock), s,
+                     acc, n, L.mm));
+  int64_t mm[2];
+  CHOPPER_HIP(hipMemcpyAsync(mm, L.mm, sizeof(mm), hipMemcpyDeviceToHost, s));
+  CHOPPER_HIP(hipStreamSynchronize(s));
+  const int tbits = bitlen_u64((uint64_t)(mm[1] - mm[0]));
+  const int cbits = bitlen_u64((uint64_t)(C > 1 ? C - 1 : 0));
+  if (tbits + cbits > 64) {
+    *range_error = true;
+    return CHOPPER_OK;
+  }
+  CHOPPER_HIP(launch("sort_make_keys", k_make_keys<Acc>, grid_for(n, kBlock),
+                     dim3(kBlock), s, acc, n, (const int64_t*)L.mm, tbits,
+                     L.key0, L.val0));
+  const int bits = tbits + cbits;
+  const int passes = bits == 0 ? 0 : (bits + 7) / 8;
+  uint64_t* kin = L.key0;
+  uint64_t* kout = L.key1;
+  uint32_t* vin = L.val0;
+  uint32_t* vout = L.val1;
+  for (int p = 0; p < passes; ++p) {
+    const int shift = 8 * p;
+    const bool last = (p == passes - 1);
+    CHOPPER_HIP(launch("sort_digit_hist", k_digit_hist, dim3((unsigned)T),
+                       dim3(kBlock), s, (const uint64_t*)kin, n, shift, T,
+                       L.tilehist));
+    CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, L.tileoff, 256 * T,
+                                         L.scantmp, L.total, s));
+    CHOPPER_HIP(launch("sort_digit_scatter", k_digit_scatter,
+                       dim3((unsigned)T), dim3(kBlock), s,
+                       (const uint64_t*)kin, (const uint32_t*)vin, n, shift, T,
+                       (const uint32_t*)L.tileoff, last ? nullptr : kout,
+                       last ? out : vout));
+    uint64_t* tk = kin; kin = kout; kout = tk;
+    uint32_t* tv = vin; vin = vout; vout = tv;
+  }
+  if (passes == 0) {
+    CHOPPER_HIP(hipMemcpyAsync(out, L.val0, sizeof(uint32_t) * n,
+                               hipMemcpyDeviceToDevice, s));
+  }
+  return CHOPPER_OK;
+}
+
+template int class_sort<KeyRecStream>(const KeyRecStream&,
+                                      const ClassSortLayout&, uint32_t*,
+                                      uint32_t*, bool*, hipStream_t);
+template int class_sort<KeyRecKind>(const KeyRecKind&, const ClassSortLayout&,
+                                    uint32_t*, uint32_t*, bool*, hipStream_t);
+template int class_sort<KeyMarker>(const KeyMarker&, const ClassSortLayout&,
+                                   uint32_t*, uint32_t*, bool*, hipStream_t);
+
+}  // namespace chopper

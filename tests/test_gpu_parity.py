@@ -1,0 +1,208 @@
+"""Parity of the HIP pipeline with the CPU oracle, element by element, through
+the C ABI.  Integer outputs must be bit-exact; derived doubles must be equal
+(NaN matching NaN), which is within the 1e-12 relative tolerance required for
+them since both sides perform the same IEEE operations."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+REC_KEYS = ("start", "end", "mstart", "mend", "order", "korder", "idx", "ovl",
+            "gap", "mwin", "gwin")
+ROW_KEYS = ("path", "gpu", "kind", "n", "dur", "gap", "ovl", "tmin", "tmax",
+            "first", "ctr")
+
+
+@pytest.fixture(scope="module")
+def ch():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    import paper_2512_08242_amd as m
+    return m
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run_gpu(ch, tr, level=255, filt=None):
+    pipe = ch.Pipeline(ch.DeviceTrace(tr, "cuda"), level=level, filt=filt)
+    pipe.status.zero_()
+    pipe.step()
+    return pipe.results()
+
+
+def assert_same_float(a, b, what):
+    a, b = np.asarray(a), np.asarray(b)
+    assert a.shape == b.shape, what
+    same = (a == b) | (np.isnan(a) & np.isnan(b))
+    if not same.all():
+        i = np.nonzero(~same.reshape(-1))[0][0]
+        raise AssertionError(f"{what}: first difference at {i}: "
+                             f"{a.reshape(-1)[i]!r} vs {b.reshape(-1)[i]!r}")
+
+
+def assert_parity(got, ref, rows=True, name=""):
+    assert got["status"] == ref["status"], (name, got["status"], ref["status"])
+    for k in ("x0", "c", "d"):
+        assert np.array_equal(got[k], ref[k]), (name, k)
+    for k in REC_KEYS:
+        g, r = np.asarray(got[k]), np.asarray(ref[k])
+        assert g.shape == r.shape, (name, k, g.shape, r.shape)
+        if not np.array_equal(g, r):
+            diff = np.nonzero((g != r).reshape(-1))[0]
+            raise AssertionError(f"{name}: {k}: {diff.size} differences, "
+                                 f"first at {diff[0]}: {g.reshape(-1)[diff[0]]} "
+                                 f"vs {r.reshape(-1)[diff[0]]}")
+    if not rows:
+        return
+    gr, rr = got["rows"], ref["rows"]
+    assert np.array_equal(gr["level_offset"], rr["level_offset"]), (
+        name, gr["level_offset"], rr["level_offset"])
+    for k in ROW_KEYS:
+        if not np.array_equal(gr[k], rr[k]):
+            diff = np.nonzero((np.asarray(gr[k]) != np.asarray(rr[k])
+                               ).reshape(-1))[0]
+            raise AssertionError(f"{name}: rows.{k}: {diff.size} differences,"
+                                 f" first at {diff[0]}")
+    assert_same_float(got["ratios"], ref["ratios"], f"{name}: ratios")
+    assert_same_float(got["wfrac"], ref["wfrac"], f"{name}: window fractions")
+
+
+MICRO = [dict(n_gpus=1, n_kernels=40, n_streams=1, depth=2),
+         dict(n_gpus=2, n_kernels=120, n_streams=3, depth=3, n_counters=16,
+              anchors=5),
+         dict(n_gpus=3, n_kernels=300, n_streams=4, depth=4, n_counters=3,
+              anchors=2),
+         dict(n_gpus=4, n_kernels=600, n_streams=2, depth=5, n_counters=16,
+              anchors=8, mixed_stream_kinds=False),
+         dict(n_gpus=2, n_kernels=5000, n_streams=3, depth=4, n_counters=16,
+              anchors=9, span=60000)]
+
+
+@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("shape", range(len(MICRO)))
+def test_micro_nested(ch, seed, shape):
+    tr = tg.make_micro(seed * 7 + shape, **MICRO[shape])
+    say("micro nested", seed, shape, tr.n, tr.n_markers)
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_micro_unnested(ch, seed):
+    """Arbitrary marker intervals: attribution and overlap stay exact; rows
+    only when no path conflict is reported."""
+    tr = tg.make_micro(500 + seed, n_gpus=2, n_kernels=200, n_streams=3,
+                       depth=3, nested=False, n_counters=2)
+    say("micro unnested", seed)
+    got, ref = run_gpu(ch, tr), oracle.run(tr)
+    conflict = bool(ref["status"] & oracle.PATH_CONFLICT)
+    assert_parity(got, ref, rows=not conflict, name=tr.name)
+
+
+@pytest.mark.parametrize("cid", [0, 1, 2])
+def test_config_full_parity(ch, cid):
+    tr = tg.make_config(cid)
+    say("config", cid, tr.n, tr.n_markers)
+    ref = oracle.run(tr)
+    got = run_gpu(ch, tr)
+    assert_parity(got, ref, name=f"config{cid}")
+
+
+@pytest.mark.parametrize("level", [0, 1, 2, 100, 101])
+def test_single_level_requests(ch, level):
+    tr = tg.make_micro(77, n_gpus=3, n_kernels=400, depth=3, n_counters=4,
+                       anchors=3)
+    say("level", level)
+    assert_parity(run_gpu(ch, tr, level=level), oracle.run(tr, level=level),
+                  name=f"level{level}")
+
+
+def test_filter(ch):
+    tr = tg.make_config(0)
+    say("filter")
+    f_or = oracle.make_filter(gpus=[0], classes=[0, 1, 2, 5], iters=(1, 1))
+    f_ch = ch.make_filter(gpus=[0], classes=[0, 1, 2, 5], iters=(1, 1))
+    assert_parity(run_gpu(ch, tr, filt=f_ch), oracle.run(tr, filt=f_or),
+                  name="filter")
+    tr = tg.make_micro(12, n_gpus=3, n_kernels=300, depth=3, n_counters=2)
+    f_or = oracle.make_filter(gpus=[0, 2], classes=[0, 3, 5, 6, 7])
+    f_ch = ch.make_filter(gpus=[0, 2], classes=[0, 3, 5, 6, 7])
+    assert_parity(run_gpu(ch, tr, filt=f_ch), oracle.run(tr, filt=f_or),
+                  name="filter2")
+
+
+def _tiny(n, m=3, G=1, depth=2, mlen=400):
+    rng = np.random.default_rng(n)
+    s = np.sort(rng.integers(0, 1000, size=n)).astype(np.int64)
+    return tg.Trace(
+        n_gpus=G, depth=depth, gpu=np.zeros(n, np.uint8),
+        stream=(np.arange(n) % 2).astype(np.uint8), start=s,
+        end=s + rng.integers(0, 50, size=n), cls=(np.arange(n) % 7
+                                                   ).astype(np.uint8),
+        op_id=np.zeros(n, np.uint32), counters=None,
+        m_gpu=np.zeros(m, np.uint8), m_level=(np.arange(m) % depth
+                                              ).astype(np.uint8),
+        m_start=np.arange(m, dtype=np.int64) * 300,
+        m_end=np.arange(m, dtype=np.int64) * 300 + mlen,
+        m_label=np.arange(m, dtype=np.uint32), a_gpu=np.zeros(0, np.uint8),
+        a_local=np.zeros(0, np.int64), a_ref=np.zeros(0, np.int64),
+        name=f"tiny{n}")
+
+
+@pytest.mark.parametrize("n", [0, 1, 2, 3, 2047, 2048, 2049, 4097])
+def test_edge_sizes(ch, n):
+    tr = _tiny(n)
+    say("edge", n)
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+
+
+def test_no_markers(ch):
+    tr = _tiny(100, m=0)
+    say("no markers")
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name="nomarkers")
+
+
+def test_overflowing_marker_sets_flag(ch):
+    tr = _tiny(300, m=6, depth=2, mlen=700)   # same-level markers overlap
+    say("marker overlap")
+    got, ref = run_gpu(ch, tr), oracle.run(tr)
+    assert ref["status"] & oracle.MARKER_OVERLAP
+    conflict = bool(ref["status"] & oracle.PATH_CONFLICT)
+    assert_parity(got, ref, rows=not conflict, name="overlap")
+
+
+def test_bad_inputs_set_status(ch):
+    tr = tg.make_micro(5, n_gpus=2, n_kernels=100, depth=2)
+    tr.gpu[3] = 7          # beyond n_gpus
+    tr.cls[4] = 9          # unknown class
+    tr.end[5] = tr.start[5] - 10
+    tr.m_level[0] = 5      # beyond depth
+    say("bad inputs")
+    got, ref = run_gpu(ch, tr), oracle.run(tr)
+    for bit in (oracle.BAD_GPU, oracle.BAD_CLASS, oracle.NEG_DURATION,
+                oracle.BAD_LEVEL):
+        assert got["status"] & bit and ref["status"] & bit, bit
+
+
+def test_repeated_steps_are_identical(ch):
+    tr = tg.make_config(1)
+    say("repeat")
+    pipe = ch.Pipeline(ch.DeviceTrace(tr, "cuda"))
+    pipe.status.zero_()
+    pipe.step()
+    a = pipe.results()
+    for _ in range(3):
+        pipe.step()
+    b = pipe.results()
+    for k in REC_KEYS:
+        assert np.array_equal(a[k], b[k]), k
+    for k in ROW_KEYS:
+        assert np.array_equal(a["rows"][k], b["rows"][k]), k

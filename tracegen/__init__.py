@@ -702,7 +702,7 @@ def make_micro(seed: int, n_gpus: int = 2, n_kernels: int = 48,
     a_gpu, a_local, a_ref = [], [], []
     for g in range(G):
         off = int(rng.integers(-300, 301))
-        drift = float(rng.uniform(-0.01, 0.01))
+        drift = float(rng.uniform(-5e-4, 5e-4))
         for _ in range(anchors):
             y = base + int(rng.integers(0, span))
             x = y + off + int(round(drift * (y - base))) + int(
