@@ -237,6 +237,11 @@ __global__ __launch_bounds__(kBlock) void k_agg_assign(
     for (int j = 0; j < kAggIpt; ++j) {
       if (!mine[j]) continue;
       const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
+      if (li == S.D + 1) {
+        // workload rows span GPUs: ordered by kind alone
+        row = tilebase[(int64_t)li * ntiles] +
+              ((it[j].kind == 1u && own[li][0] != kNone) ? 1u : 0u);
+      }
       rowof[li][key[j]] = row;
       if ((int64_t)row < R.cap) {
         for (int l = 0; l < S.D; ++l)
@@ -244,7 +249,8 @@ __global__ __launch_bounds__(kBlock) void k_agg_assign(
               (li < S.D && l <= li) ? it[j].p[l] : kNone;
         R.gpu[row] = (li == S.D + 1) ? (uint8_t)0xFF : (uint8_t)it[j].g;
         R.kind[row] = (uint8_t)it[j].kind;
-        R.first[row] = it[j].r;
+        // workload rows: fixed after the reduction (k_agg_workload_first)
+        R.first[row] = (li == S.D + 1) ? kNone : it[j].r;
         R.firstpos[row] = (uint32_t)pos;
         if ((atomic_levels >> li) & 1u) {
           R.n[row] = 0;
@@ -336,6 +342,7 @@ struct FromRecords {
     for (int l = 0; l < S.D; ++l) p[l] = S.idx[(int64_t)l * S.n + r];
     fpos = (uint32_t)i;
   }
+  __device__ uint32_t first_of(uint32_t r) const { return r; }
   __device__ uint64_t field(int f, uint32_t r) const {
     switch (f) {
       case 0: return 1ull;
@@ -368,6 +375,7 @@ struct FromRows {
     for (int l = 0; l < R.D; ++l) p[l] = R.path[(int64_t)l * R.cap + r];
     fpos = R.firstpos[r];
   }
+  __device__ uint32_t first_of(uint32_t r) const { return R.first[r]; }
   __device__ uint64_t field(int f, uint32_t r) const {
     switch (f) {
       case 0: return R.n[r];
@@ -505,6 +513,24 @@ __global__ __launch_bounds__(kBlock) void k_agg_reduce(
       else if (slot[j] != kNone) ovf.val[(int64_t)f * ovf.cap + slot[j]] = x[j];
     }
   }
+}
+
+// first record of a workload row: the smallest input index among the records
+// (or GPU rows) whose start equals the row's tmin
+template <typename Src>
+__global__ __launch_bounds__(kBlock) void k_agg_workload_first(
+    Src src, int D, int64_t M, const uint32_t* rowof, RowsDev R) {
+  const int64_t cnt = src.count();
+  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i >= cnt) return;
+  uint32_t r, p[8], g, kind, fpos;
+  bool ok;
+  src.load(i, r, ok, p, g, kind, fpos);
+  if (!ok) return;
+  const uint32_t row = rowof[kind];
+  if ((int64_t)row >= R.cap) return;
+  if ((int64_t)src.field(4, r) == R.tmin[row])
+    atomicMin(&R.first[row], src.first_of(r));
 }
 
 __global__ __launch_bounds__(kBlock) void k_agg_apply_overflow(
@@ -756,6 +782,20 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
       CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
                          grid_for(L.ovf_cap, kBlock), dim3(kBlock), s, ovf, R,
                          nfields));
+    if (li == D + 1) {
+      if (finer < 0) {
+        FromRecords src{S};
+        CHOPPER_HIP(launch("agg_workload_first",
+                           k_agg_workload_first<FromRecords>,
+                           grid_for(n, kBlock), dim3(kBlock), s, src, D, M,
+                           (const uint32_t*)L.rowof[li], R));
+      } else {
+        FromRows src{R, 0, 0, rows->level_offset, finer};
+        CHOPPER_HIP(launch("agg_workload_first", k_agg_workload_first<FromRows>,
+                           grid_for(n, kBlock), dim3(kBlock), s, src, D, M,
+                           (const uint32_t*)L.rowof[li], R));
+      }
+    }
     return CHOPPER_OK;
   };
   int order_levels[kMaxLevels];

@@ -25,7 +25,8 @@ static const char* const kKernelNames[] = {
     "agg_reduce_records", "agg_reduce_rows", "agg_apply_overflow",
     "agg_zero_rows", "agg_zero", "scan_reduce", "scan_spine", "scan_down",
     "ratios_rows", "ratios_windows", "sort_fill", "sort_init_minmax",
-    "sort_class_count", "status_set", "ov_fill", "ov_init_gminmax"};
+    "sort_class_count", "status_set", "ov_fill", "ov_init_gminmax",
+    "agg_workload_first"};
 
 __global__ __launch_bounds__(kBlock) void k_ratios(
     const int64_t* level_offset, int depth, int64_t cap, const uint64_t* n,

@@ -92,7 +92,9 @@ MICRO = [dict(n_gpus=1, n_kernels=40, n_streams=1, depth=2),
 def test_micro_nested(ch, seed, shape):
     tr = tg.make_micro(seed * 7 + shape, **MICRO[shape])
     say("micro nested", seed, shape, tr.n, tr.n_markers)
-    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+    ref = oracle.run(tr)
+    assert not ref["status"] & oracle.PATH_CONFLICT
+    assert_parity(run_gpu(ch, tr), ref, name=tr.name)
 
 
 @pytest.mark.parametrize("seed", range(8))
@@ -139,19 +141,31 @@ def test_filter(ch):
                   name="filter2")
 
 
-def _tiny(n, m=3, G=1, depth=2, mlen=400):
+def _tiny(n, m=3, G=1, depth=2, overlapping=False):
+    """n records in [0, 1000) on one GPU; markers: one level-0 marker over
+    everything and m - 1 level-1 markers tiling it (nested), or m markers of
+    alternating levels and length 700 every 300 ns (overlapping)."""
     rng = np.random.default_rng(n)
     s = np.sort(rng.integers(0, 1000, size=n)).astype(np.int64)
+    if overlapping:
+        lev = (np.arange(m) % depth).astype(np.uint8)
+        ms = np.arange(m, dtype=np.int64) * 300
+        me = ms + 700
+    elif m > 0:
+        cuts = np.linspace(0, 1000, m).astype(np.int64)
+        lev = np.array([0] + [1] * (m - 1), np.uint8)
+        ms = np.concatenate([[0], cuts[:-1]]).astype(np.int64)
+        me = np.concatenate([[1000], cuts[1:]]).astype(np.int64)
+    else:
+        lev, ms, me = (np.zeros(0, np.uint8), np.zeros(0, np.int64),
+                       np.zeros(0, np.int64))
     return tg.Trace(
         n_gpus=G, depth=depth, gpu=np.zeros(n, np.uint8),
         stream=(np.arange(n) % 2).astype(np.uint8), start=s,
         end=s + rng.integers(0, 50, size=n), cls=(np.arange(n) % 7
                                                    ).astype(np.uint8),
         op_id=np.zeros(n, np.uint32), counters=None,
-        m_gpu=np.zeros(m, np.uint8), m_level=(np.arange(m) % depth
-                                              ).astype(np.uint8),
-        m_start=np.arange(m, dtype=np.int64) * 300,
-        m_end=np.arange(m, dtype=np.int64) * 300 + mlen,
+        m_gpu=np.zeros(m, np.uint8), m_level=lev, m_start=ms, m_end=me,
         m_label=np.arange(m, dtype=np.uint32), a_gpu=np.zeros(0, np.uint8),
         a_local=np.zeros(0, np.int64), a_ref=np.zeros(0, np.int64),
         name=f"tiny{n}")
@@ -159,9 +173,11 @@ def _tiny(n, m=3, G=1, depth=2, mlen=400):
 
 @pytest.mark.parametrize("n", [0, 1, 2, 3, 2047, 2048, 2049, 4097])
 def test_edge_sizes(ch, n):
-    tr = _tiny(n)
+    tr = _tiny(n, m=5)
     say("edge", n)
-    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+    ref = oracle.run(tr)
+    assert ref["status"] == 0
+    assert_parity(run_gpu(ch, tr), ref, name=tr.name)
 
 
 def test_no_markers(ch):
@@ -171,7 +187,7 @@ def test_no_markers(ch):
 
 
 def test_overflowing_marker_sets_flag(ch):
-    tr = _tiny(300, m=6, depth=2, mlen=700)   # same-level markers overlap
+    tr = _tiny(300, m=6, depth=2, overlapping=True)
     say("marker overlap")
     got, ref = run_gpu(ch, tr), oracle.run(tr)
     assert ref["status"] & oracle.MARKER_OVERLAP
