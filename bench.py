@@ -1,0 +1,173 @@
+"""Throughput of the trace pipeline on one MI355X.
+
+One step = chopper_align + chopper_attribute + chopper_overlap +
+chopper_aggregate(all levels) + derived ratios over the whole synthetic trace
+of 8 GPUs x 800 iterations x 32 layers with 16 counters per record (the
+Llama-3-8B FSDP trace shape), inputs resident in HBM.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--config 3]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("kernel records/sec end-to-end (align+attribute+overlap+aggregate);"
+          " % HBM peak")
+HBM_PEAK_GBS = 8000.0
+# the kernel whose roofline is reported: it reads every record's counters
+ROOF_KERNEL = "agg_reduce_records"
+
+
+def algorithmic_bytes(n, nm, rows, depth, nc, n_rows_finest):
+    """Bytes that must cross HBM once: every input read once, every output
+    written once (records, markers, aggregated rows, derived ratios)."""
+    rec_in = n * (1 + 1 + 8 + 8 + 1 + 8 * nc)          # gpu stream start end cls ctr
+    rec_out = n * (8 + 8 + 4 + 4 + 4 * depth + 8 + 8)  # start' end' order korder idx gap ovl
+    mk = nm * (1 + 1 + 8 + 8) + nm * (8 + 8 + 32 + 32)  # in; start' end' CO..ID fractions
+    row = 4 * depth + 1 + 1 + 8 + 5 * 8 + 4 + 8 * nc + 6 * 8
+    return rec_in + rec_out + mk + rows * row
+
+
+def roof_kernel_bytes(n, depth, nc, n_rows_finest):
+    """Algorithmic bytes of one launch of the finest-level reduction: per
+    record korder, gpu, cls, path, start, end, gap, ovl and counters read
+    once; per finest row its sums and counters written once."""
+    per_rec = 4 + 1 + 1 + 4 * depth + 8 * 4 + 8 * nc
+    per_row = 8 * (6 + nc)
+    return n * per_rec + n_rows_finest * per_row
+
+
+def cpu_baseline(cid, iters):
+    """The CPU oracle, as it stands, on a bounded sample of the workload."""
+    import oracle
+    import tracegen as tg
+    tr = tg.make_config(cid, iters=iters, with_truth=False)
+    t0 = time.perf_counter()
+    oracle.run(tr)
+    dt = time.perf_counter() - t0
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count()
+    return {"value": tr.n / dt, "unit": "records/s", "cores": 1,
+            "host_cores_available": cores, "kind": "oracle",
+            "seconds": dt,
+            "sample": f"config-{cid} trace shape with {iters} iterations "
+                      f"({tr.n} records, {tr.n_markers} markers), "
+                      "single-threaded C oracle, whole pipeline"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-iters", type=int, default=200)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the traces of all ranks are "
+              "input data to a single device (see DESIGN.md for how the path "
+              "would shard).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import tracegen as tg
+    import paper_2512_08242_amd as ch
+
+    def log(*a):
+        print(*a, file=sys.stderr, flush=True)
+
+    cid = args.config
+    t0 = time.perf_counter()
+    tr = tg.make_config(cid, with_truth=False)
+    log(f"[bench] generated config {cid}: {tr.n} records, {tr.n_markers} "
+        f"markers in {time.perf_counter() - t0:.1f}s")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dt = ch.DeviceTrace(tr, dev)
+    n, nm, depth, nc = tr.n, tr.n_markers, tr.depth, tr.n_counters
+    del tr
+    torch.cuda.synchronize()
+    pipe = ch.Pipeline(dt)
+    for _ in range(max(args.warmup, 1)):
+        pipe.step()
+    torch.cuda.synchronize()
+    lo = pipe.rows.level_offset.cpu().numpy()
+    rows_total = int(lo[-1])
+    rows_finest = int(lo[depth] - lo[depth - 1])
+    log(f"[bench] warmup done; rows: {rows_total} (finest level "
+        f"{rows_finest})")
+
+    K = args.steps
+    kev = [(torch.cuda.Event(enable_timing=True),
+            torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for k in range(K):
+        ch.time_kernel(ROOF_KERNEL, kev[k][0], kev[k][1])
+        pipe.step()
+    e1.record()
+    torch.cuda.synchronize()
+    ch.time_kernel(None)
+    ms = e0.elapsed_time(e1) / K
+    kms = float(np.mean([a.elapsed_time(b) for a, b in kev]))
+    status = int(pipe.status.item()) & 0xFFFFFFFF
+    log(f"[bench] {ms:.3f} ms/step, {ROOF_KERNEL} {kms:.3f} ms, "
+        f"status {status}")
+
+    value = n / (ms * 1e-3)
+    bmin = algorithmic_bytes(n, nm, rows_total, depth, nc, rows_finest)
+    kb = roof_kernel_bytes(n, depth, nc, rows_finest)
+    achieved = kb / (kms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "records/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {
+            "workload": f"config {cid}: {tg.CONFIG_NAMES[cid]}",
+            "records": n, "markers": nm, "depth": depth, "counters": nc,
+            "rows": rows_total,
+        },
+        "hbm_frac_end_to_end": bmin / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "algorithmic_bytes_per_step": bmin,
+        "roofline": {
+            "kernel": ROOF_KERNEL,
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None,
+            "kernel_ms": kms,
+            "bytes_per_launch": kb,
+        },
+        "status": status,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(cid, args.cpu_iters)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -153,6 +153,9 @@ def time_kernel(name: Optional[str], start=None, stop=None):
     if name is None:
         _check(lib.chopper_time_kernel(None, None, None), "time_kernel")
         return
+    for ev in (start, stop):
+        if not ev.cuda_event:      # torch creates the HIP event lazily
+            ev.record()
     _check(lib.chopper_time_kernel(name.encode(),
                                    ctypes.c_void_p(start.cuda_event),
                                    ctypes.c_void_p(stop.cuda_event)),
@@ -327,6 +330,7 @@ class Pipeline:
         self._scr["aggregate"] = _scratch(
             lambda s, b: self._call("aggregate", s, b), dev)
         self.ratios = e(6, max(need, 1), dt_=torch.float64)
+        self.status.zero_()       # drop the sizing call's ROWS_OVERFLOW
 
     # raw entry points -------------------------------------------------------
     def _call(self, name, scratch, sbytes):

@@ -180,3 +180,75 @@ def aggregate_brute(gpu, cls, s, e, idx, gap, ovl, counters, depth,
         rows.sort(key=lambda r: (r["gpu"], r["kind"], r["tmin"], r["first"]))
         out[lev] = rows
     return out
+
+
+def aggregate_numpy(gpu, cls, s, e, idx, gap, ovl, counters, depth, levels,
+                    sel=None):
+    """Vectorized grouping for large traces: one sort of the records by
+    (gpu, kind, path...), group boundaries per level from key changes,
+    np.*.reduceat for sums, minima and maxima, first = smallest index at the
+    group's minimum start, rows ordered by (gpu, kind, tmin, first).
+    Returns {level: dict of row columns}."""
+    n = len(gpu)
+    keep = np.arange(n) if sel is None else np.nonzero(sel)[0]
+    g = gpu[keep].astype(np.int64)
+    kind = np.isin(cls[keep], (5, 6)).astype(np.int64)
+    st = s[keep]
+    paths = [idx[l][keep].astype(np.int64) for l in range(depth)]
+    keys = paths[::-1] + [kind, g]
+    o = np.lexsort(keys)
+    rec = keep[o]
+    g, kind, st = g[o], kind[o], st[o]
+    paths = [p[o] for p in paths]
+    en = e[rec]
+    cols = dict(n=np.ones(len(rec), np.uint64),
+                dur=(en - st).astype(np.int64), gap=gap[rec].astype(np.int64),
+                ovl=ovl[rec].astype(np.int64))
+    ctr = None if counters is None else counters[:, rec]
+    out = {}
+    base = dict(rec=rec, g=g, kind=kind, st=st, en=en, paths=paths, cols=cols,
+                ctr=ctr)
+    for lev in levels:
+        if len(rec) == 0:
+            out[lev] = None
+            continue
+        if lev == 101:
+            # workload groups span GPUs: regroup by kind alone
+            ko = np.argsort(base["kind"], kind="stable")
+            rec, g, kind = base["rec"][ko], base["g"][ko], base["kind"][ko]
+            st, en = base["st"][ko], base["en"][ko]
+            cols = {k: v[ko] for k, v in base["cols"].items()}
+            ctr = None if base["ctr"] is None else base["ctr"][:, ko]
+            diff = kind[1:] != kind[:-1]
+        else:
+            diff = (g[1:] != g[:-1]) | (kind[1:] != kind[:-1])
+            if lev < 100:
+                for l in range(lev + 1):
+                    diff |= paths[l][1:] != paths[l][:-1]
+        b = np.concatenate([[0], np.nonzero(diff)[0] + 1])
+        rows = {}
+        for k, v in cols.items():
+            rows[k] = np.add.reduceat(v, b)
+        tmin = np.minimum.reduceat(st, b)
+        gid = np.repeat(np.arange(len(b)), np.diff(np.append(b, len(rec))))
+        at_min = np.where(st == tmin[gid], rec, np.int64(1) << 40)
+        first = np.minimum.reduceat(at_min, b).astype(np.uint32)
+        tmax = np.maximum.reduceat(en, b)
+        rg = (np.full(len(b), 0xFF, np.int64) if lev == 101 else g[b])
+        rk = kind[b]
+        order = np.lexsort((first, tmin, rk, rg))
+        r = dict(gpu=rg[order].astype(np.uint8), kind=rk[order].astype(np.uint8),
+                 tmin=tmin[order], tmax=tmax[order], first=first[order])
+        for k in cols:
+            r[k] = rows[k][order]
+        path = np.full((depth, len(b)), NONE, np.uint32)
+        if lev < 100:
+            for l in range(lev + 1):
+                path[l] = paths[l][b].astype(np.uint32)
+        r["path"] = path[:, order]
+        if ctr is not None:
+            r["ctr"] = np.add.reduceat(ctr, b, axis=1)[:, order]
+        else:
+            r["ctr"] = np.zeros((0, len(b)), np.uint64)
+        out[lev] = r
+    return out

@@ -1,0 +1,112 @@
+"""Full-size parity (the 20M-record headline trace and the 50M-record
+adversarial trace), in the launch configuration bench.py times.
+
+Clocks, alignment, attribution, overlap and bubbles are compared with the C
+oracle over every record and marker; the two orders with numpy's stable
+lexsort; the aggregated rows of every level with the vectorized brute-force
+grouping of tests/brute.py (pinned to the oracle on CPU); the derived ratios
+by recomputing the same IEEE divisions in numpy."""
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import brute
+import oracle
+import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ch():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    import paper_2512_08242_amd as m
+    return m
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def same(a, b, what):
+    a, b = np.asarray(a), np.asarray(b)
+    assert a.shape == b.shape, (what, a.shape, b.shape)
+    if not np.array_equal(a, b):
+        d = np.nonzero((a != b).reshape(-1))[0]
+        raise AssertionError(f"{what}: {d.size} differences, first at {d[0]}")
+
+
+@pytest.mark.parametrize("cid", [3, 4])
+def test_full_size_parity(ch, cid):
+    t0 = time.time()
+    tr = tg.make_config(cid, with_truth=False)
+    say(f"config {cid}: {tr.n} records {tr.n_markers} markers "
+        f"({time.time() - t0:.0f}s)")
+    pipe = ch.Pipeline(ch.DeviceTrace(tr, "cuda"))
+    pipe.status.zero_()
+    pipe.step()
+    got = pipe.results()
+    assert got["status"] == 0, got["status"]
+    say(f"gpu done ({time.time() - t0:.0f}s)")
+    G = tr.n_gpus
+    x0, c, d, rc = oracle.fit(tr.a_gpu, tr.a_local, tr.a_ref, G)
+    assert rc == 0
+    same(got["x0"], x0, "x0")
+    same(got["c"], c, "c")
+    same(got["d"], d, "d")
+    s, _ = oracle.transform(tr.gpu, tr.start, G, x0, c, d)
+    e, _ = oracle.transform(tr.gpu, tr.end, G, x0, c, d)
+    ms, _ = oracle.transform(tr.m_gpu, tr.m_start, G, x0, c, d)
+    me, _ = oracle.transform(tr.m_gpu, tr.m_end, G, x0, c, d)
+    same(got["start"], s, "start")
+    same(got["end"], e, "end")
+    same(got["mstart"], ms, "mstart")
+    same(got["mend"], me, "mend")
+    n = tr.n
+    ar = np.arange(n)
+    kind = np.isin(tr.cls, [5, 6]).astype(np.int64)
+    same(got["order"], np.lexsort((ar, s, tr.stream.astype(np.int64),
+                                   tr.gpu.astype(np.int64))), "order")
+    same(got["korder"], np.lexsort((ar, s, kind, tr.gpu.astype(np.int64))),
+         "korder")
+    say(f"align ok ({time.time() - t0:.0f}s)")
+    idx, st = oracle.attribute(tr.gpu, s, tr.m_gpu, tr.m_level, ms, me,
+                               tr.depth, G)
+    assert st == 0
+    same(got["idx"], idx, "idx")
+    say(f"attribute ok ({time.time() - t0:.0f}s)")
+    ov = oracle.overlap(tr.gpu, tr.stream, tr.cls, s, e, tr.m_gpu, ms, me, G)
+    for k in ("ovl", "gap", "mwin", "gwin"):
+        same(got[k], ov[k], k)
+    say(f"overlap ok ({time.time() - t0:.0f}s)")
+    levels = list(range(tr.depth)) + [100, 101]
+    ref = brute.aggregate_numpy(tr.gpu, tr.cls, s, e, idx, ov["gap"],
+                                ov["ovl"], tr.counters, tr.depth, levels)
+    rows, lo = got["rows"], got["rows"]["level_offset"]
+    for li, lev in enumerate(levels):
+        sl = slice(lo[li], lo[li + 1])
+        for k in ("gpu", "kind", "n", "dur", "gap", "ovl", "tmin", "tmax",
+                  "first"):
+            same(rows[k][sl], ref[lev][k], f"level {lev} {k}")
+        same(rows["path"][:, sl], ref[lev]["path"], f"level {lev} path")
+        same(rows["ctr"][:, sl], ref[lev]["ctr"], f"level {lev} ctr")
+    say(f"aggregate ok ({time.time() - t0:.0f}s)")
+    # derived ratios: the same IEEE operations in numpy
+    f = lambda a: np.asarray(a).astype(np.float64)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        dur = f(rows["dur"])
+        cyc = f(rows["ctr"][0])
+        dpeak = cyc * 1000.0 / 2100.0
+        want = np.stack([f(rows["ovl"]) / dur,
+                         f(rows["ctr"][4] + rows["ctr"][5]) / dur,
+                         f(rows["ctr"][13]) / f(rows["n"]),
+                         f(rows["ctr"][1]) / cyc, dpeak, dur / dpeak])
+    gotr = got["ratios"]
+    ok = (gotr == want) | (np.isnan(gotr) & np.isnan(want))
+    assert ok.all(), "ratios"
+    say(f"done ({time.time() - t0:.0f}s)")

@@ -510,3 +510,26 @@ def test_ratios_are_single_ieee_divisions():
                     assert rat[1, i] == float((c[4] + c[5]) % 2**64) / d
             else:
                 assert np.isnan(rat[1:, i]).all()
+
+
+@pytest.mark.parametrize("case", ["config1", "micro"])
+def test_numpy_aggregation_matches_oracle(case):
+    """The vectorized brute-force grouping used for full-size checks agrees
+    with the oracle row for row."""
+    if case == "config1":
+        tr = tg.make_config(1)
+    else:
+        tr = tg.make_micro(9, n_gpus=3, n_kernels=400, depth=3, n_counters=5)
+    r = oracle.run(tr)
+    levels = list(range(tr.depth)) + [100, 101]
+    ref = brute.aggregate_numpy(tr.gpu, tr.cls, r["start"], r["end"], r["idx"],
+                                r["gap"], r["ovl"], tr.counters, tr.depth,
+                                levels)
+    rows, lo = r["rows"], r["rows"]["level_offset"]
+    for li, lev in enumerate(levels):
+        sl = slice(lo[li], lo[li + 1])
+        for k in ("n", "dur", "gap", "ovl", "tmin", "tmax", "first", "gpu",
+                  "kind"):
+            assert np.array_equal(ref[lev][k], rows[k][sl]), (lev, k)
+        assert np.array_equal(ref[lev]["path"], rows["path"][:, sl]), lev
+        assert np.array_equal(ref[lev]["ctr"], rows["ctr"][:, sl]), lev

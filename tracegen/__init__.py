@@ -545,6 +545,9 @@ def make_config(cid: int, iters: Optional[int] = None,
         if cfg["drop_frac"] > 0:
             keep = rng.random(lv.shape[0]) >= cfg["drop_frac"]
             lv, ms, me, ml = lv[keep], ms[keep], me[keep], ml[keep]
+        # profiler order: ranges in the order they open (start, outer first)
+        mo = np.lexsort((lv, ms))
+        lv, ms, me, ml = lv[mo], ms[mo], me[mo], ml[mo]
         mks["gpu"].append(np.full(lv.shape, g, np.uint8))
         mks["level"].append(lv)
         mks["start"].append(_to_local(ms, off, drift, t0))
