@@ -22,7 +22,7 @@ METRIC = ("kernel records/sec end-to-end (align+attribute+overlap+aggregate);"
           " % HBM peak")
 HBM_PEAK_GBS = 8000.0
 # the kernel whose roofline is reported: it reads every record's counters
-ROOF_KERNEL = "agg_reduce_records"
+ROOF_KERNEL = "agg_fast_reduce_records"
 
 
 def algorithmic_bytes(n, nm, rows, depth, nc, n_rows_finest):

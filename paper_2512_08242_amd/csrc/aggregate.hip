@@ -328,6 +328,30 @@ __device__ inline void seg_scan(const bool (&head)[kAggIpt],
   }
 }
 
+struct FieldRef {
+  const uint64_t* a;
+  const uint64_t* b;
+  int mode;
+  __device__ uint64_t get(uint32_t r) const {
+    if (mode == 0) return 1ull;
+    if (mode == 1) return a[r] - b[r];
+    return a[r];
+  }
+};
+
+// column of row field f (same bits for the signed columns)
+__device__ inline uint64_t* row_column(const RowsDev& R, int f) {
+  switch (f) {
+    case 0: return R.n;
+    case 1: return (uint64_t*)R.dur;
+    case 2: return (uint64_t*)R.gap;
+    case 3: return (uint64_t*)R.ovl;
+    case 4: return (uint64_t*)R.tmin;
+    case 5: return (uint64_t*)R.tmax;
+    default: return R.ctr + (int64_t)(f - 6) * R.cap;
+  }
+}
+
 // Item sources for the reduction: records in korder, or rows of a finer
 // level.  Fields: 0 n, 1 dur, 2 gap, 3 ovl, 4 tmin, 5 tmax, 6.. counters.
 struct FromRecords {
@@ -343,6 +367,34 @@ struct FromRecords {
     fpos = (uint32_t)i;
   }
   __device__ uint32_t first_of(uint32_t r) const { return r; }
+  __device__ uint32_t index(int64_t i) const { return S.korder[i]; }
+  __device__ bool ok(uint32_t r) const { return rec_pass(S, r); }
+  __device__ uint32_t pathv(uint32_t r, int l) const {
+    return S.idx[(int64_t)l * S.n + r];
+  }
+  __device__ uint32_t gpuv(uint32_t r) const { return S.gpu[r]; }
+  __device__ uint32_t kindv(uint32_t r) const {
+    return (uint32_t)kind_of(S.cls[r]);
+  }
+  __device__ uint32_t keyof(uint32_t r, int li) const {
+    if (!rec_pass(S, r)) return kNone;
+    uint32_t p[8];
+    for (int l = 0; l < S.D; ++l) p[l] = pathv(r, l);
+    return group_key(p, S.D, S.M, li, gpuv(r), kindv(r));
+  }
+  // column of field f, resolved once per field: mode 0 constant 1,
+  // 1 a[r] - b[r], 2 a[r]
+  __device__ FieldRef fref(int f) const {
+    switch (f) {
+      case 0: return FieldRef{nullptr, nullptr, 0};
+      case 1: return FieldRef{(const uint64_t*)S.end, (const uint64_t*)S.start, 1};
+      case 2: return FieldRef{(const uint64_t*)S.gap, nullptr, 2};
+      case 3: return FieldRef{(const uint64_t*)S.ovl, nullptr, 2};
+      case 4: return FieldRef{(const uint64_t*)S.start, nullptr, 2};
+      case 5: return FieldRef{(const uint64_t*)S.end, nullptr, 2};
+      default: return FieldRef{S.ctr + (int64_t)(f - 6) * S.n, nullptr, 2};
+    }
+  }
   __device__ uint64_t field(int f, uint32_t r) const {
     switch (f) {
       case 0: return 1ull;
@@ -358,7 +410,7 @@ struct FromRecords {
 
 struct FromRows {
   RowsDev R;
-  int64_t lo, hi;   // rows of the finer level
+  int64_t M;        // number of markers (key space)
   const int64_t* level_offset;
   int lo_slot;      // level_offset index of the finer level
   __device__ int64_t count() const {
@@ -376,6 +428,23 @@ struct FromRows {
     fpos = R.firstpos[r];
   }
   __device__ uint32_t first_of(uint32_t r) const { return R.first[r]; }
+  __device__ uint32_t index(int64_t i) const {
+    return (uint32_t)(level_offset[lo_slot] + i);
+  }
+  __device__ bool ok(uint32_t) const { return true; }
+  __device__ uint32_t pathv(uint32_t r, int l) const {
+    return R.path[(int64_t)l * R.cap + r];
+  }
+  __device__ uint32_t gpuv(uint32_t r) const { return R.gpu[r]; }
+  __device__ uint32_t kindv(uint32_t r) const { return R.kind[r]; }
+  __device__ uint32_t keyof(uint32_t r, int li) const {
+    uint32_t p[8];
+    for (int l = 0; l < R.D; ++l) p[l] = pathv(r, l);
+    return group_key(p, R.D, M, li, gpuv(r), kindv(r));
+  }
+  __device__ FieldRef fref(int f) const {
+    return FieldRef{(const uint64_t*)row_column(R, f), nullptr, 2};
+  }
   __device__ uint64_t field(int f, uint32_t r) const {
     switch (f) {
       case 0: return R.n[r];
@@ -515,6 +584,358 @@ __global__ __launch_bounds__(kBlock) void k_agg_reduce(
   }
 }
 
+// ------------------------------------------------------------------ fast path
+// When every group is one run of consecutive items -- the keys met at piece
+// boundaries strictly increase inside each (gpu, kind) segment, which holds
+// when markers are numbered in the order they open -- rows are simply the
+// pieces in item order: no owner tables, rows numbered by counting piece
+// heads.
+constexpr int kHeadIpt = 4;
+constexpr int kHeadTile = kBlock * kHeadIpt;
+
+// Per tile of items: number of piece heads at every level in [0, D] whose bit
+// is set in `act` (tilecnt[(li - lv0) * ntiles + tile], zeros elsewhere up
+// to level D + 1); flags[0] |= 1 when a key does not increase inside its
+// segment, flags[1] |= 1 << kind for the kinds present; PATH_CONFLICT when
+// two neighbours share a key but not the path.
+template <typename Src>
+__global__ __launch_bounds__(kBlock) void k_agg_heads(
+    Src src, uint32_t act, int lv0, int lv1, int D, int64_t M, int64_t ntiles,
+    uint32_t* tilecnt, uint32_t* flags, uint32_t* status) {
+  __shared__ uint32_t s_path[8][kHeadTile];
+  __shared__ uint16_t s_gk[kHeadTile];
+  __shared__ uint32_t s_ppath[8];
+  __shared__ uint32_t s_pgk;
+  const int t = threadIdx.x;
+  const int64_t cnt = src.count();
+  const int64_t base = (int64_t)blockIdx.x * kHeadTile;
+  if (base >= cnt) {
+    if (t <= lv1 - lv0) tilecnt[(int64_t)t * ntiles + blockIdx.x] = 0;
+    return;
+  }
+  const int tile_n = (int)((cnt - base) < kHeadTile ? (cnt - base) : kHeadTile);
+  for (int j = 0; j < kHeadIpt; ++j) {
+    const int q = j * kBlock + t;
+    if (q >= tile_n) continue;
+    const uint32_t r = src.index(base + q);
+    for (int l = 0; l < D; ++l) s_path[l][q] = src.pathv(r, l);
+    s_gk[q] = src.ok(r) ? (uint16_t)(src.gpuv(r) * 2u + src.kindv(r))
+                        : (uint16_t)0xFFFF;
+  }
+  if (t == 0) {
+    s_pgk = 0xFFFEu;     // no previous item
+    if (base > 0) {
+      const uint32_t r = src.index(base - 1);
+      for (int l = 0; l < D; ++l) s_ppath[l] = src.pathv(r, l);
+      s_pgk = src.ok(r) ? src.gpuv(r) * 2u + src.kindv(r) : 0xFFFFu;
+    }
+  }
+  __syncthreads();
+  uint32_t c[kMaxLevels];
+  for (int li = 0; li < kMaxLevels; ++li) c[li] = 0;
+  bool notinc = false, conflict = false;
+  uint32_t kinds = 0;
+  for (int j = 0; j < kHeadIpt; ++j) {
+    const int q = j * kBlock + t;
+    if (q >= tile_n) continue;
+    uint32_t p[8], pp[8];
+    for (int l = 0; l < D; ++l) {
+      p[l] = s_path[l][q];
+      pp[l] = q > 0 ? s_path[l][q - 1] : s_ppath[l];
+    }
+    const uint32_t gk = s_gk[q];
+    const uint32_t pgk = q > 0 ? (uint32_t)s_gk[q - 1] : s_pgk;
+    if (gk == 0xFFFFu) {          // filtered item: no fast path
+      notinc = true;
+      continue;
+    }
+    const bool pvalid = pgk < 0xFFFEu;
+    for (int li = lv0; li <= lv1; ++li) {
+      if (!((act >> li) & 1u) || li > D) continue;
+      const uint32_t key = group_key(p, D, M, li, gk >> 1, gk & 1u);
+      const uint32_t pkey =
+          pvalid ? group_key(pp, D, M, li, pgk >> 1, pgk & 1u) : kNone;
+      if (key != pkey && key != kNone) {
+        ++c[li];
+        // inside a segment the no-marker group may only come first, so it
+        // orders before every marker key in this test
+        const int64_t ok = (li < D && key >= 2 * M) ? -1 : (int64_t)key;
+        const int64_t opk = (li < D && pkey >= 2 * M) ? -1 : (int64_t)pkey;
+        if (pvalid && pgk == gk && ok <= opk) notinc = true;
+        if (li == D) kinds |= 1u << (gk & 1u);
+      } else if (li < D) {
+        for (int l = 0; l <= li; ++l)
+          if (p[l] != pp[l]) conflict = true;
+      }
+    }
+  }
+  for (int li = lv0; li <= lv1; ++li) {
+    uint32_t tot;
+    block_exclusive(c[li], OpAdd(), 0u, &tot);
+    if (t == 0) tilecnt[(int64_t)(li - lv0) * ntiles + blockIdx.x] = tot;
+  }
+  const int lane = t & (kWave - 1);
+  if (__ballot(notinc) != 0 && lane == 0) atomicOr(&flags[0], 1u);
+  if (__ballot(conflict) != 0 && lane == 0)
+    atomicOr(status, (uint32_t)CHOPPER_ST_PATH_CONFLICT);
+  for (int d = kWave / 2; d > 0; d >>= 1) kinds |= __shfl_xor(kinds, d, kWave);
+  if (lane == 0 && kinds) atomicOr(&flags[1], kinds);
+}
+
+// Fast-path level offsets: the level-major scan gives every level but the
+// workload level, whose rows are the kinds present.
+__global__ void k_agg_offsets_fast(int L, int64_t ntiles,
+                                   const uint32_t* tilebase,
+                                   const uint32_t* total, const uint32_t* flags,
+                                   bool workload, int64_t cap,
+                                   int64_t* level_offset, uint32_t* status) {
+  if (threadIdx.x != 0) return;
+  for (int li = 0; li < L; ++li)
+    level_offset[li] = ntiles > 0 ? tilebase[(int64_t)li * ntiles] : 0;
+  const int64_t tot =
+      (int64_t)*total + (workload ? __popc(flags[1] & 3u) : 0);
+  level_offset[L] = tot;
+  // the counts are the row counts only when the fast path applies
+  if (flags[0] == 0 && tot > cap)
+    atomicOr(status, (uint32_t)CHOPPER_ST_ROWS_OVERFLOW);
+}
+
+// Combine of the fast reduction: 0 sum, 1 min, 2 max (signed).
+__device__ inline uint64_t comb_op(int op, uint64_t a, uint64_t b) {
+  if (op == 1) return (int64_t)a < (int64_t)b ? a : b;
+  if (op == 2) return (int64_t)a > (int64_t)b ? a : b;
+  return a + b;
+}
+
+struct OpSegRt {
+  int op;
+  __device__ FV<uint64_t> operator()(FV<uint64_t> a, FV<uint64_t> b) const {
+    return FV<uint64_t>{a.f | b.f, b.f ? b.v : comb_op(op, a.v, b.v)};
+  }
+};
+
+// segmented inclusive scan over the tile, blocked items, bit j of `heads`
+// starts a segment
+__device__ inline void seg_scan_rt(uint32_t heads, uint64_t (&x)[kAggIpt],
+                                   uint64_t ident, int op) {
+  FV<uint64_t> acc{0u, ident};
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    if ((heads >> j) & 1u) acc = FV<uint64_t>{1u, x[j]};
+    else acc.v = comb_op(op, acc.v, x[j]);
+    x[j] = acc.v;
+  }
+  FV<uint64_t> tot;
+  FV<uint64_t> pre =
+      block_exclusive(acc, OpSegRt{op}, FV<uint64_t>{0u, ident}, &tot);
+  const uint32_t before = heads ? (uint32_t)(__ffs(heads) - 1) : kAggIpt;
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j)
+    if ((uint32_t)j < before) x[j] = comb_op(op, pre.v, x[j]);
+}
+
+__device__ inline uint64_t field_ident(int f) {
+  return f == 4 ? (uint64_t)kI64Max : f == 5 ? (uint64_t)kI64Min : 0ull;
+}
+
+// Reduction of one level when groups are runs: rows numbered by counting
+// real piece heads (key differs from the previous item's); items staged
+// through LDS so that every global load is coalesced, then reduced in a
+// blocked arrangement by segmented scans, the loads of the next field in
+// flight while the current one is scanned.  The piece that starts a row
+// stores it and writes its header; a piece continuing a row from the
+// previous tile goes to the overflow list.
+template <typename Src>
+__global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
+    Src src, int li, int D, int64_t M, const uint32_t* tilebase,
+    const int64_t* row0, RowsDev R, Overflow ovf, int nfields) {
+  __shared__ uint32_t s_r[kAggTile];
+  __shared__ uint32_t s_key[kAggTile];
+  __shared__ uint64_t s_v[kAggTile];
+  __shared__ uint32_t s_head0[kBlock];
+  __shared__ uint32_t s_prevkey;
+  const int t = threadIdx.x;
+  const int64_t cnt = src.count();
+  const int64_t base = (int64_t)blockIdx.x * kAggTile;
+  if (base >= cnt) return;
+  const int tile_n = (int)((cnt - base) < kAggTile ? (cnt - base) : kAggTile);
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int q = j * kBlock + t;
+    if (q >= tile_n) continue;
+    const uint32_t r = src.index(base + q);
+    s_r[q] = r;
+    s_key[q] = src.keyof(r, li);
+  }
+  if (t == 0)
+    s_prevkey = base > 0 ? src.keyof(src.index(base - 1), li) : kNone;
+  // first field in flight while the pieces are worked out
+  uint64_t pf[kAggIpt];
+  __syncthreads();
+  {
+    const uint64_t id0 = field_ident(0);
+    const FieldRef fr = src.fref(0);
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) {
+      const int q = j * kBlock + t;
+      pf[j] = (q < tile_n && s_key[q] != kNone) ? fr.get(s_r[q]) : id0;
+    }
+  }
+  uint32_t m_item = 0, m_real = 0, m_head = 0, m_last = 0;
+  uint32_t c = 0;
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int q = t * kAggIpt + j;
+    const bool valid = q < tile_n;
+    const uint32_t key = valid ? s_key[q] : kNone;
+    const uint32_t prev = q == 0 ? s_prevkey : s_key[q - 1];
+    if (valid && key != kNone) m_item |= 1u << j;
+    if (valid && key != kNone && key != prev) m_real |= 1u << j;
+    if (!valid || q == 0 || key != prev) m_head |= 1u << j;
+    c += (m_real >> j) & 1u;
+  }
+  uint32_t tot;
+  const uint32_t ex = block_exclusive(c, OpAdd(), 0u, &tot);
+  int64_t running = (row0 ? *row0 : 0) +
+                    (int64_t)tilebase[base / kHeadTile] + ex;
+  uint32_t row[kAggIpt];
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    running += (m_real >> j) & 1u;
+    row[j] = ((m_item >> j) & 1u) ? (uint32_t)(running - 1) : kNone;
+  }
+  s_head0[t] = m_head & 1u;
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    const bool next_head = j + 1 < kAggIpt ? ((m_head >> (j + 1)) & 1u)
+                          : (t + 1 < kBlock ? s_head0[t + 1] != 0 : true);
+    if (((m_item >> j) & 1u) && next_head) m_last |= 1u << j;
+  }
+  // headers of the rows that start here
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    if (!((m_real >> j) & 1u) || (int64_t)row[j] >= R.cap) continue;
+    const uint32_t r = s_r[t * kAggIpt + j], w = row[j];
+    for (int l = 0; l < D; ++l)
+      R.path[(int64_t)l * R.cap + w] = (li < D && l <= li) ? src.pathv(r, l)
+                                                           : kNone;
+    R.gpu[w] = (uint8_t)src.gpuv(r);
+    R.kind[w] = (uint8_t)src.kindv(r);
+    R.first[w] = src.first_of(r);
+  }
+  // does the piece start a row?  (propagated from its first item)
+  uint32_t m_own = 0;
+  {
+    uint64_t ob[kAggIpt];
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) ob[j] = (m_real >> j) & 1u;
+    seg_scan_rt(m_head, ob, 0ull, 0);
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) m_own |= (ob[j] ? 1u : 0u) << j;
+  }
+  uint32_t slot[kAggIpt];
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    slot[j] = kNone;
+    if (((m_last & ~m_own) >> j) & 1u && (int64_t)row[j] < R.cap) {
+      const uint32_t e = atomicAdd(ovf.count, 1u);
+      if ((int64_t)e < ovf.cap) {
+        slot[j] = e;
+        ovf.row[e] = row[j];
+      } else {
+        atomicOr(ovf.lost, 1u);
+      }
+    }
+  }
+  for (int f = 0; f < nfields; ++f) {
+    const uint64_t ident = field_ident(f);
+    const int op = f == 4 ? 1 : f == 5 ? 2 : 0;
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) {
+      const int q = j * kBlock + t;
+      if (q < tile_n) s_v[q] = pf[j];
+    }
+    __syncthreads();
+    if (f + 1 < nfields) {
+      const uint64_t idn = field_ident(f + 1);
+      const FieldRef fr = src.fref(f + 1);
+#pragma unroll
+      for (int j = 0; j < kAggIpt; ++j) {
+        const int q = j * kBlock + t;
+        pf[j] = (q < tile_n && s_key[q] != kNone) ? fr.get(s_r[q]) : idn;
+      }
+    }
+    uint64_t x[kAggIpt];
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) {
+      const int q = t * kAggIpt + j;
+      x[j] = q < tile_n ? s_v[q] : ident;
+    }
+    // the scan's barriers also order these reads before the next field's
+    // writes to s_v
+    seg_scan_rt(m_head, x, ident, op);
+    uint64_t* col = row_column(R, f);
+    uint64_t* ocol = ovf.val + (int64_t)f * ovf.cap;
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) {
+      if (!((m_last >> j) & 1u) || (int64_t)row[j] >= R.cap) continue;
+      if ((m_own >> j) & 1u) col[row[j]] = x[j];
+      else if (slot[j] != kNone) ocol[slot[j]] = x[j];
+    }
+  }
+}
+
+// Workload rows (one per kind present) from the GPU rows, in kind order.
+__global__ void k_agg_workload_from_gpu(const int64_t* level_offset, int D,
+                                        RowsDev R, int nfields) {
+  const int64_t g0 = level_offset[D], g1 = level_offset[D + 1];
+  const int64_t w0 = level_offset[D + 1], w1 = level_offset[D + 2];
+  const int f = threadIdx.x;
+  for (int64_t w = w0; w < w1 && w < R.cap; ++w) {
+    // kind of this workload row: 0 first when present
+    const uint32_t kind = (w1 - w0 == 2) ? (uint32_t)(w - w0) : 2u;
+    uint32_t kd = kind;
+    if (kd == 2u) {   // a single row: the only kind present
+      kd = 0u;
+      for (int64_t r = g0; r < g1 && r < R.cap; ++r)
+        if (R.kind[r] == 1u) kd = 1u;
+    }
+    if (f < nfields) {
+      uint64_t acc = f == 4 ? (uint64_t)kI64Max
+                     : f == 5 ? (uint64_t)kI64Min : 0ull;
+      for (int64_t r = g0; r < g1 && r < R.cap; ++r) {
+        if (R.kind[r] != kd) continue;
+        uint64_t v;
+        switch (f) {
+          case 0: v = R.n[r]; break;
+          case 1: v = (uint64_t)R.dur[r]; break;
+          case 2: v = (uint64_t)R.gap[r]; break;
+          case 3: v = (uint64_t)R.ovl[r]; break;
+          case 4: v = (uint64_t)R.tmin[r]; break;
+          case 5: v = (uint64_t)R.tmax[r]; break;
+          default: v = R.ctr[(int64_t)(f - 6) * R.cap + r]; break;
+        }
+        if (f == 4) acc = (int64_t)v < (int64_t)acc ? v : acc;
+        else if (f == 5) acc = (int64_t)v > (int64_t)acc ? v : acc;
+        else acc += v;
+      }
+      store_field(R, f, (uint32_t)w, acc);
+    }
+    __syncthreads();
+    if (f == 0) {
+      for (int l = 0; l < D; ++l) R.path[(int64_t)l * R.cap + w] = kNone;
+      R.gpu[w] = 0xFF;
+      R.kind[w] = (uint8_t)kd;
+      uint32_t first = kNone;
+      for (int64_t r = g0; r < g1 && r < R.cap; ++r)
+        if (R.kind[r] == kd && R.tmin[r] == R.tmin[w] && R.first[r] < first)
+          first = R.first[r];
+      R.first[w] = first;
+    }
+    __syncthreads();
+  }
+}
+
 // first record of a workload row: the smallest input index among the records
 // (or GPU rows) whose start equals the row's tmin
 template <typename Src>
@@ -594,6 +1015,16 @@ struct AggLayout {
   uint32_t* ovf_row;
   uint64_t* ovf_val;
   int64_t ovf_cap;
+  // fast path: head counts per tile of kHeadTile items
+  int64_t ntiles_h;
+  uint32_t* htc;          // [L][ntiles_h]
+  uint32_t* htb;
+  uint32_t* hscan;
+  uint32_t* htotal;
+  uint32_t* hflags;       // [0] keys not increasing, [1] kinds present
+  uint32_t* htc2;         // one level over rows
+  uint32_t* htb2;
+  uint32_t* hflags2;
 };
 
 static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
@@ -618,6 +1049,15 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
   L.ovf_count = sc.take<uint32_t>(2);
   L.ovf_row = sc.take<uint32_t>(L.ovf_cap);
   L.ovf_val = sc.take<uint64_t>((int64_t)kMaxFields * L.ovf_cap);
+  L.ntiles_h = ceil_div(n, kHeadTile);
+  L.htc = sc.take<uint32_t>((int64_t)L.L * L.ntiles_h);
+  L.htb = sc.take<uint32_t>((int64_t)L.L * L.ntiles_h);
+  L.hscan = sc.take<uint32_t>(scan_scratch_elems((int64_t)L.L * L.ntiles_h));
+  L.htotal = sc.take<uint32_t>(2);
+  L.hflags = sc.take<uint32_t>(2);
+  L.htc2 = sc.take<uint32_t>(L.ntiles_h);
+  L.htb2 = sc.take<uint32_t>(L.ntiles_h);
+  L.hflags2 = sc.take<uint32_t>(2);
   return L;
 }
 
@@ -716,6 +1156,88 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
   R.D = D;
   R.nc = nc;
 
+  Overflow ovf{L.ovf_count, L.ovf_count + 1, L.ovf_row, L.ovf_val, L.ovf_cap};
+  const bool want_workload = (act >> (D + 1)) & 1u;
+
+  // ---- fast path: every group is one run of consecutive records
+  if (n > 0 && !filter && level != CHOPPER_LEVEL_WORKLOAD) {
+    const int64_t Th = L.ntiles_h;
+    FromRecords fr{S};
+    CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s, L.hflags,
+                       2));
+    CHOPPER_HIP(launch("agg_heads_records", k_agg_heads<FromRecords>,
+                       dim3((unsigned)Th), dim3(kBlock), s, fr, act, 0,
+                       Lv - 1, D, M, Th, L.htc, L.hflags, status));
+    CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc, L.htb, (int64_t)Lv * Th,
+                                         L.hscan, L.htotal, s));
+    CHOPPER_HIP(launch("agg_offsets", k_agg_offsets_fast, dim3(1), dim3(64),
+                       s, Lv, Th, (const uint32_t*)L.htb,
+                       (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
+                       want_workload, rows->cap, rows->level_offset, status));
+    uint32_t hf[2] = {1u, 0u};
+    CHOPPER_HIP(hipMemcpyAsync(hf, L.hflags, sizeof(hf), hipMemcpyDeviceToHost,
+                               s));
+    CHOPPER_HIP(hipStreamSynchronize(s));
+    if (hf[0] == 0) {
+      auto fast_level = [&](int li, int finer) -> int {
+        CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
+                           L.ovf_count, 1));
+        if (finer < 0) {
+          CHOPPER_HIP(launch("agg_fast_reduce_records",
+                             k_agg_fast_reduce<FromRecords>,
+                             dim3((unsigned)T), dim3(kBlock), s, fr, li, D, M,
+                             (const uint32_t*)(L.htb + (int64_t)li * Th),
+                             (const int64_t*)nullptr, R, ovf, nfields));
+        } else {
+          FromRows src{R, M, rows->level_offset, finer};
+          CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
+                             L.hflags2, 2));
+          CHOPPER_HIP(launch("agg_heads_rows", k_agg_heads<FromRows>,
+                             dim3((unsigned)Th), dim3(kBlock), s, src,
+                             1u << li, li, li, D, M, Th, L.htc2, L.hflags2,
+                             status));
+          CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc2, L.htb2, Th, L.hscan,
+                                               L.htotal + 1, s));
+          CHOPPER_HIP(launch("agg_fast_reduce_rows",
+                             k_agg_fast_reduce<FromRows>, dim3((unsigned)T),
+                             dim3(kBlock), s, src, li, D, M,
+                             (const uint32_t*)L.htb2,
+                             (const int64_t*)(rows->level_offset + li), R, ovf,
+                             nfields));
+        }
+        CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
+                           grid_for(L.ovf_cap, kBlock), dim3(kBlock), s, ovf,
+                           R, nfields));
+        return CHOPPER_OK;
+      };
+      if (level == CHOPPER_LEVEL_ALL) {
+        rc = fast_level(D > 0 ? D - 1 : D, -1);
+        if (rc != CHOPPER_OK) return rc;
+        for (int li = D - 2; li >= 0; --li) {
+          rc = fast_level(li, li + 1);
+          if (rc != CHOPPER_OK) return rc;
+        }
+        if (D > 0) {
+          rc = fast_level(D, 0);
+          if (rc != CHOPPER_OK) return rc;
+        }
+        CHOPPER_HIP(launch("agg_workload_from_gpu", k_agg_workload_from_gpu,
+                           dim3(1), dim3(64), s,
+                           (const int64_t*)rows->level_offset, D, R, nfields));
+      } else {
+        rc = fast_level(level == CHOPPER_LEVEL_GPU ? D : level, -1);
+        if (rc != CHOPPER_OK) return rc;
+      }
+      uint32_t lost = 0;
+      CHOPPER_HIP(hipMemcpyAsync(&lost, L.ovf_count + 1, sizeof(uint32_t),
+                                 hipMemcpyDeviceToHost, s));
+      CHOPPER_HIP(hipStreamSynchronize(s));
+      if (!lost) return CHOPPER_OK;
+      // an overflow list that did not fit: use the general path below
+    }
+  }
+
+  // ---- general path: per-level owner election
   // pointer tables for the per-level owner / row maps
   CHOPPER_HIP(hipMemcpyAsync(L.own_tab, L.own, sizeof(L.own),
                              hipMemcpyHostToDevice, s));
@@ -748,7 +1270,6 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
                      L.rowof_tab, T, (const uint32_t*)L.tilebase, R));
   CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
                      L.ovf_count, 2));
-  Overflow ovf{L.ovf_count, L.ovf_count + 1, L.ovf_row, L.ovf_val, L.ovf_cap};
 
   // order of work: finest marker level from records, coarser marker levels
   // from the rows below, GPU rows from level-0 rows, workload from GPU rows
@@ -770,7 +1291,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
                          (const uint32_t*)L.rowof[li], R, ovf, nfields,
                          status));
     } else {
-      FromRows src{R, 0, 0, rows->level_offset, finer};
+      FromRows src{R, M, rows->level_offset, finer};
       // rows of the finer level never outnumber the records
       CHOPPER_HIP(launch("agg_reduce_rows", k_agg_reduce<FromRows>,
                          dim3((unsigned)T), dim3(kBlock), s, src, li, D, M,
@@ -790,7 +1311,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
                            grid_for(n, kBlock), dim3(kBlock), s, src, D, M,
                            (const uint32_t*)L.rowof[li], R));
       } else {
-        FromRows src{R, 0, 0, rows->level_offset, finer};
+        FromRows src{R, M, rows->level_offset, finer};
         CHOPPER_HIP(launch("agg_workload_first", k_agg_workload_first<FromRows>,
                            grid_for(n, kBlock), dim3(kBlock), s, src, D, M,
                            (const uint32_t*)L.rowof[li], R));

@@ -130,15 +130,28 @@ __device__ inline void status_or(uint32_t* status, uint32_t bits) {
   if ((threadIdx.x & (kWave - 1)) == 0 && v) atomicOr(status, v);
 }
 
+// Presence of (gpu, stream) and (gpu, kind) pairs as byte flags written with
+// plain stores (no read-modify-write on the few hot lines); within a wave
+// only the lanes whose pair differs from the previous lane's store.
+__device__ inline void mark_present(uint8_t* flags, uint32_t idx) {
+  const uint32_t prev = __shfl_up(idx, 1, kWave);
+  const int lane = threadIdx.x & (kWave - 1);
+  if (lane == 0 || prev != idx) flags[idx] = 1;
+}
+
 __global__ __launch_bounds__(kBlock) void k_transform_records(
     int64_t n, int n_gpus, const uint8_t* gpu, const uint8_t* stream,
     const uint8_t* cls, const int64_t* start, const int64_t* end,
-    const ClockDev* clk, int64_t* s_out, int64_t* e_out, uint32_t* pres_s,
-    uint32_t* pres_k, uint32_t* status) {
+    const ClockDev* clk, int64_t* s_out, int64_t* e_out, uint8_t* pres_s,
+    uint8_t* pres_k, uint32_t* unsorted, uint32_t* status) {
   const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  const int lane = threadIdx.x & (kWave - 1);
   uint32_t st = 0;
+  uint32_t g = 0;
+  int64_t s2 = 0;
+  bool bad_order = false;
   if (i < n) {
-    const uint32_t g = gpu[i];
+    g = gpu[i];
     const uint32_t c = cls[i];
     const int64_t s = start[i], e = end[i];
     ClockDev k{0, 0, 0};
@@ -146,15 +159,35 @@ __global__ __launch_bounds__(kBlock) void k_transform_records(
     else st |= CHOPPER_ST_BAD_GPU;
     if (c >= 8) st |= CHOPPER_ST_BAD_CLASS;
     if (e < s) st |= CHOPPER_ST_NEG_DURATION;
-    const int64_t s2 = align_time(s, k), e2 = align_time(e, k);
+    s2 = align_time(s, k);
+    const int64_t e2 = align_time(e, k);
     if (out_of_range(s) || out_of_range(e) || out_of_range(s2) ||
         out_of_range(e2))
       st |= CHOPPER_ST_RANGE;
     s_out[i] = s2;
     e_out[i] = e2;
-    pres_s[g * 256u + stream[i]] = 1u;
-    pres_k[g * 2u + (uint32_t)kind_of(c)] = 1u;
   }
+  {
+    // every lane takes part in the shuffles of mark_present
+    const bool v = i < n;
+    const uint32_t ks = v ? g * 256u + stream[i] : 0xFFFFFFFFu;
+    const uint32_t kk = v ? g * 2u + (uint32_t)kind_of(cls[i]) : 0xFFFFFFFFu;
+    const uint32_t ps = __shfl_up(ks, 1, kWave), pk = __shfl_up(kk, 1, kWave);
+    if (v && (lane == 0 || ps != ks)) pres_s[ks] = 1;
+    if (v && (lane == 0 || pk != kk)) pres_k[kk] = 1;
+  }
+  // is the input ordered by (gpu, start')?  Then every (gpu, stream) and
+  // (gpu, kind) subsequence is time-ordered and one stable class pass sorts.
+  uint32_t pg = __shfl_up(g, 1, kWave);
+  int64_t ps = __shfl_up(s2, 1, kWave);
+  if (lane == 0 && i > 0 && i < n) {
+    pg = gpu[i - 1];
+    ClockDev k{0, 0, 0};
+    if ((int)pg < n_gpus) k = clk[pg];
+    ps = align_time(start[i - 1], k);
+  }
+  if (i > 0 && i < n) bad_order = pg > g || (pg == g && ps > s2);
+  if (__ballot(bad_order) != 0 && lane == 0) atomicOr(unsorted, 1u);
   status_or(status, st);
 }
 
@@ -182,28 +215,39 @@ __global__ __launch_bounds__(kBlock) void k_transform_markers(
   status_or(status, st);
 }
 
-// Dense class ids in (gpu, stream) and (gpu, kind) order from presence flags.
+// Dense class ids in (gpu, stream) and (gpu, kind) order from the presence
+// flags (65536 + 512 bytes): every thread counts the flags of 256
+// consecutive pairs, one block scan, then every thread numbers its own.
 __global__ __launch_bounds__(kBlock) void k_dense_classes(
-    const uint32_t* pres_s, uint16_t* cmap_s, const uint32_t* pres_k,
+    const uint8_t* pres_s, uint16_t* cmap_s, const uint8_t* pres_k,
     uint16_t* cmap_k, uint32_t* counts) {
-  uint32_t carry = 0;
-  for (int base = 0; base < 65536; base += kBlock) {
-    uint32_t p = pres_s[base + threadIdx.x];
-    uint32_t tot;
-    uint32_t ex = block_exclusive(p, OpAdd(), 0u, &tot) + carry;
-    cmap_s[base + threadIdx.x] = (uint16_t)(p ? ex : 0u);
-    carry += tot;
+  const uint32_t* w = reinterpret_cast<const uint32_t*>(pres_s) +
+                      threadIdx.x * 64;
+  uint32_t c = 0;
+  for (int q = 0; q < 64; ++q) {
+    const uint32_t x = w[q];
+    c += (x & 0xFFu ? 1u : 0u) + (x & 0xFF00u ? 1u : 0u) +
+         (x & 0xFF0000u ? 1u : 0u) + (x & 0xFF000000u ? 1u : 0u);
   }
-  if (threadIdx.x == 0) counts[0] = carry;
-  carry = 0;
-  for (int base = 0; base < 512; base += kBlock) {
-    uint32_t p = pres_k[base + threadIdx.x];
-    uint32_t tot;
-    uint32_t ex = block_exclusive(p, OpAdd(), 0u, &tot) + carry;
-    cmap_k[base + threadIdx.x] = (uint16_t)(p ? ex : 0u);
-    carry += tot;
+  uint32_t tot;
+  uint32_t id = block_exclusive(c, OpAdd(), 0u, &tot);
+  const uint8_t* f = pres_s + threadIdx.x * 256;
+  uint16_t* out = cmap_s + threadIdx.x * 256;
+  for (int b = 0; b < 256; ++b) {
+    const bool on = f[b] != 0;
+    out[b] = (uint16_t)(on ? id : 0u);
+    id += on ? 1u : 0u;
   }
-  if (threadIdx.x == 0) counts[1] = carry;
+  if (threadIdx.x == 0) counts[0] = tot;
+  if (threadIdx.x == 0) {
+    uint32_t k = 0;
+    for (int b = 0; b < 512; ++b) {
+      const bool on = pres_k[b] != 0;
+      cmap_k[b] = (uint16_t)(on ? k : 0u);
+      k += on ? 1u : 0u;
+    }
+    counts[1] = k;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -211,8 +255,8 @@ __global__ __launch_bounds__(kBlock) void k_dense_classes(
 // ---------------------------------------------------------------------------
 struct AlignLayout {
   ClockDev* clk;
-  uint32_t* pres_s;   // 65536 + 512, cleared together
-  uint32_t* pres_k;
+  uint8_t* pres_s;    // 65536 + 512 byte flags, cleared together
+  uint8_t* pres_k;
   uint16_t* cmap_s;
   uint16_t* cmap_k;
   uint32_t* counts;
@@ -223,7 +267,7 @@ struct AlignLayout {
 static AlignLayout align_layout(Scratch& sc, int64_t n, int n_gpus) {
   AlignLayout L;
   L.clk = sc.take<ClockDev>(n_gpus);
-  L.pres_s = sc.take<uint32_t>(65536 + 512);
+  L.pres_s = sc.take<uint8_t>(65536 + 512);
   L.pres_k = L.pres_s ? L.pres_s + 65536 : nullptr;
   L.cmap_s = sc.take<uint16_t>(65536);
   L.cmap_k = sc.take<uint16_t>(512);
@@ -306,26 +350,31 @@ extern "C" int chopper_align(const chopper_records* rec,
                        (const ClockDev*)L.clk, mstart_out, mend_out, status));
   }
   if (n == 0) return CHOPPER_OK;
-  CHOPPER_HIP(launch("align_fill", k_fill_u32, grid_for(65536 + 512, kBlock),
-                     dim3(kBlock), s, L.pres_s, (int64_t)(65536 + 512), 0u));
+  CHOPPER_HIP(launch("align_fill", k_fill_u32, grid_for(16384 + 128, kBlock),
+                     dim3(kBlock), s, reinterpret_cast<uint32_t*>(L.pres_s),
+                     (int64_t)(16384 + 128), 0u));
+  CHOPPER_HIP(launch("align_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
+                     L.counts, (int64_t)4, 0u));
   CHOPPER_HIP(launch("align_transform_records", k_transform_records,
                      grid_for(n, kBlock), dim3(kBlock), s, n, G, rec->gpu,
                      rec->stream, rec->cls, rec->start_ns, rec->end_ns,
                      (const ClockDev*)L.clk, start_out, end_out, L.pres_s,
-                     L.pres_k, status));
+                     L.pres_k, L.counts + 2, status));
   CHOPPER_HIP(launch("align_dense_classes", k_dense_classes, dim3(1),
-                     dim3(kBlock), s, (const uint32_t*)L.pres_s, L.cmap_s,
-                     (const uint32_t*)L.pres_k, L.cmap_k, L.counts));
-  uint32_t counts[2];
+                     dim3(kBlock), s, (const uint8_t*)L.pres_s, L.cmap_s,
+                     (const uint8_t*)L.pres_k, L.cmap_k, L.counts));
+  uint32_t counts[3];
   CHOPPER_HIP(hipMemcpyAsync(counts, L.counts, sizeof(counts),
                              hipMemcpyDeviceToHost, s));
   CHOPPER_HIP(hipStreamSynchronize(s));
+  // counts[2] != 0: the input is not ordered by (gpu, start')
+  const int known = counts[2] ? -1 : 1;
   bool range_err = false, r2 = false;
   KeyRecStream ks{rec->gpu, rec->stream, start_out, L.cmap_s, (int)counts[0]};
-  rc = class_sort(ks, L.sort, order_out, L.coff, &range_err, s);
+  rc = class_sort(ks, L.sort, order_out, L.coff, &range_err, s, known);
   if (rc != CHOPPER_OK) return rc;
   KeyRecKind kk{rec->gpu, rec->cls, start_out, L.cmap_k, (int)counts[1]};
-  rc = class_sort(kk, L.sort, korder_out, L.coff, &r2, s);
+  rc = class_sort(kk, L.sort, korder_out, L.coff, &r2, s, known);
   if (rc != CHOPPER_OK) return rc;
   if (range_err || r2) {
     // fold the host-detected condition into the device status word

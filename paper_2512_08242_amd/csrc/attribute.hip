@@ -167,7 +167,7 @@ extern "C" int chopper_attribute(const chopper_records* rec,
   AttrLayout L = attr_layout(sc, nm, G, D);
   KeyMarker km{mk->gpu, mk->level, mstart_al, mend_al, G, D};
   bool range_err = false;
-  rc = class_sort(km, L.sort, L.mord, L.coff, &range_err, s);
+  rc = class_sort(km, L.sort, L.mord, L.coff, &range_err, s, -1);
   if (rc != CHOPPER_OK) return rc;
   if (range_err)
     CHOPPER_HIP(launch("status_set", k_status_set, dim3(1), dim3(1), s,

@@ -229,39 +229,19 @@ __global__ __launch_bounds__(kBlock) void k_runs_comm_overlap(
 // ---------------- queries ----------------------------------------------------
 __global__ __launch_bounds__(kBlock) void k_overlap_records(
     int64_t n, int G, const uint8_t* gpu, const uint8_t* cls,
-    const int64_t* start, const int64_t* end, Runs R, int64_t* ovl,
-    int64_t* gmin, int64_t* gmax) {
+    const int64_t* start, const int64_t* end, Runs R, int64_t* ovl) {
   const int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  const bool v = k < n;
-  uint32_t g = v ? gpu[k] : 0u;
-  int64_t s = v ? start[k] : kI64Max;
-  int64_t e = v ? end[k] : kI64Min;
-  if (v) {
-    int64_t o = 0;
-    if (e > s && (int)g < G) {
-      uint32_t other = g * 2u + (kind_of(cls[k]) ? 0u : 1u);
-      o = F_active(R, other, e) - F_active(R, other, s);
-    }
-    ovl[k] = o;
+  if (k >= n) return;
+  const uint32_t g = gpu[k];
+  const int64_t s = start[k], e = end[k];
+  int64_t o = 0;
+  if (e > s && (int)g < G) {
+    // a compute kernel's overlapped time is the comm-active time inside it
+    // and vice versa
+    const uint32_t other = g * 2u + (kind_of(cls[k]) ? 0u : 1u);
+    o = F_active(R, other, e) - F_active(R, other, s);
   }
-  // per-GPU window bounds: reduce across the wave when it holds one GPU
-  const uint32_t g0 = __shfl(g, 0, kWave);
-  const bool uniform = __ballot(v && g != g0) == 0;
-  if (uniform) {
-    int64_t lo = s, hi = e;
-    for (int d = kWave / 2; d > 0; d >>= 1) {
-      int64_t a = __shfl_xor(lo, d, kWave), b = __shfl_xor(hi, d, kWave);
-      lo = a < lo ? a : lo;
-      hi = b > hi ? b : hi;
-    }
-    if ((threadIdx.x & (kWave - 1)) == 0 && lo != kI64Max && (int)g0 < G) {
-      atomicMin((long long*)&gmin[g0], (long long)lo);
-      atomicMax((long long*)&gmax[g0], (long long)hi);
-    }
-  } else if (v && (int)g < G) {
-    atomicMin((long long*)&gmin[g], (long long)s);
-    atomicMax((long long*)&gmax[g], (long long)e);
-  }
+  ovl[k] = o;
 }
 
 __device__ inline void window(const Runs& R, uint32_t g, int64_t a, int64_t b,
@@ -290,11 +270,19 @@ __global__ __launch_bounds__(kBlock) void k_overlap_markers(
   for (int z = 0; z < 4; ++z) mwin[4 * j + z] = w[z];
 }
 
-__global__ void k_overlap_gpus(int G, const int64_t* gmin, const int64_t* gmax,
-                               Runs R, int64_t* gwin) {
+// GPU window: the first run of a (gpu, kind) segment starts at its smallest
+// start', the last run ends at its largest end'
+__global__ void k_overlap_gpus(int G, Runs R, int64_t* gwin) {
   const int g = blockIdx.x * blockDim.x + threadIdx.x;
   if (g >= G) return;
-  int64_t a = gmin[g], b = gmax[g];
+  int64_t a = kI64Max, b = kI64Min;
+  for (uint32_t seg = g * 2u; seg < g * 2u + 2u; ++seg) {
+    const uint32_t rb = R.rbeg[seg], re = R.rend[seg];
+    if (re > rb) {
+      a = R.rs[rb] < a ? R.rs[rb] : a;
+      b = R.re[re - 1] > b ? R.re[re - 1] : b;
+    }
+  }
   if (a == kI64Max) a = b = 0;
   int64_t w[4];
   window(R, (uint32_t)g, a, b, w);
@@ -303,80 +291,32 @@ __global__ void k_overlap_gpus(int G, const int64_t* gmin, const int64_t* gmax,
   for (int z = 0; z < 4; ++z) gwin[6 * g + 2 + z] = w[z];
 }
 
-__global__ void k_init_gminmax(int G, int64_t* gmin, int64_t* gmax) {
-  const int g = blockIdx.x * blockDim.x + threadIdx.x;
-  if (g < G) {
-    gmin[g] = kI64Max;
-    gmax[g] = kI64Min;
-  }
-}
-
 // ---------------- bubbles ----------------------------------------------------
-// running maximum of the positions of compute records in (gpu, stream) order
-__global__ __launch_bounds__(kBlock) void k_gap_tile_max(int64_t n,
-                                                         const uint32_t* order,
-                                                         const uint8_t* cls,
-                                                         int64_t* tile_agg) {
-  const int64_t base = (int64_t)blockIdx.x * kOvTile;
-  int64_t acc = -1;
-  for (int j = 0; j < kOvIpt; ++j) {
-    int64_t p = base + (int64_t)threadIdx.x * kOvIpt + j;
-    if (p < n && !kind_of(cls[order[p]])) acc = p;
-  }
-  int64_t tot;
-  block_exclusive(acc, OpMax(), (int64_t)-1, &tot);
-  if (threadIdx.x == 0) tile_agg[blockIdx.x] = tot;
-}
-
-__global__ __launch_bounds__(kBlock) void k_gap_spine(int64_t* tile_agg,
-                                                      int64_t ntiles) {
-  int64_t carry = -1;
-  for (int64_t base = 0; base < ntiles; base += kBlock) {
-    int64_t i = base + threadIdx.x;
-    int64_t v = i < ntiles ? tile_agg[i] : -1;
-    int64_t tot;
-    int64_t ex = block_exclusive(v, OpMax(), (int64_t)-1, &tot);
-    if (i < ntiles) tile_agg[i] = ex > carry ? ex : carry;
-    carry = tot > carry ? tot : carry;
-  }
-}
-
-__global__ __launch_bounds__(kBlock) void k_gap_write(
+// In (gpu, stream, start') order the previous compute record of a compute
+// record is found by walking back over communication records of the same
+// (gpu, stream).  Each communication record is walked over by at most one
+// compute record (the next one), so the total work is linear.
+__global__ __launch_bounds__(kBlock) void k_gap(
     int64_t n, const uint32_t* order, const uint8_t* gpu, const uint8_t* stream,
     const uint8_t* cls, const int64_t* start, const int64_t* end,
-    const int64_t* tile_pre, int64_t* gap) {
-  const int64_t base = (int64_t)blockIdx.x * kOvTile;
-  uint32_t r[kOvIpt];
-  bool comp[kOvIpt], valid[kOvIpt];
-  int64_t loc[kOvIpt];
-  int64_t acc = -1;
-  for (int j = 0; j < kOvIpt; ++j) {
-    int64_t p = base + (int64_t)threadIdx.x * kOvIpt + j;
-    valid[j] = p < n;
-    r[j] = valid[j] ? order[p] : 0u;
-    comp[j] = valid[j] && !kind_of(cls[r[j]]);
-    loc[j] = acc;
-    if (comp[j]) acc = p;
-  }
-  int64_t tot;
-  int64_t pre = block_exclusive(acc, OpMax(), (int64_t)-1, &tot);
-  int64_t tp = tile_pre[blockIdx.x];
-  pre = pre > tp ? pre : tp;
-  for (int j = 0; j < kOvIpt; ++j) {
-    if (!valid[j]) continue;
-    int64_t g = 0;
-    if (comp[j]) {
-      int64_t q = loc[j] > pre ? loc[j] : pre;
-      if (q >= 0) {
-        uint32_t rq = order[q];
-        if (gpu[rq] == gpu[r[j]] && stream[rq] == stream[r[j]]) {
-          int64_t b = start[r[j]] - end[rq];
-          g = b > 0 ? b : 0;
-        }
+    int64_t* gap) {
+  const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (p >= n) return;
+  const uint32_t r = order[p];
+  int64_t gv = 0;
+  if (!kind_of(cls[r])) {
+    const uint8_t g = gpu[r], st = stream[r];
+    for (int64_t q = p - 1; q >= 0; --q) {
+      const uint32_t rq = order[q];
+      if (gpu[rq] != g || stream[rq] != st) break;
+      if (!kind_of(cls[rq])) {
+        const int64_t b = start[r] - end[rq];
+        gv = b > 0 ? b : 0;
+        break;
       }
     }
-    gap[r[j]] = g;
   }
+  gap[r] = gv;
 }
 
 // ---------------------------------------------------------------------------
@@ -400,9 +340,6 @@ struct OverlapLayout {
   int64_t* fcrs;
   int64_t* scan_i64;
   int64_t* tot_i64;
-  int64_t* gmin;
-  int64_t* gmax;
-  int64_t* gap_tiles;
 };
 
 static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
@@ -426,9 +363,6 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   L.fcrs = sc.take<int64_t>(n);
   L.scan_i64 = sc.take<int64_t>(scan_scratch_elems(n));
   L.tot_i64 = sc.take<int64_t>(2);
-  L.gmin = sc.take<int64_t>(G);
-  L.gmax = sc.take<int64_t>(G);
-  L.gap_tiles = sc.take<int64_t>(L.ntiles);
   return L;
 }
 
@@ -467,8 +401,6 @@ extern "C" int chopper_overlap(const chopper_records* rec,
 
   CHOPPER_HIP(launch("ov_fill", k_fill_u32, grid_for(2 * kSegs, kBlock),
                      dim3(kBlock), s, L.rbeg, (int64_t)(2 * kSegs), 0u));
-  CHOPPER_HIP(launch("ov_init_gminmax", k_init_gminmax, grid_for(G, kBlock),
-                     dim3(kBlock), s, G, L.gmin, L.gmax));
   if (n > 0) {
     // union runs of every (gpu, kind)
     CHOPPER_HIP(launch("ov_runs_tile_max", k_runs_tile_max, dim3(T),
@@ -502,23 +434,18 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                                         L.tot_i64 + 1, s));
     CHOPPER_HIP(launch("ov_records", k_overlap_records, grid_for(n, kBlock),
                        dim3(kBlock), s, n, G, rec->gpu, rec->cls, start_al,
-                       end_al, R, ovl_out, L.gmin, L.gmax));
+                       end_al, R, ovl_out));
   }
   if (nm > 0)
     CHOPPER_HIP(launch("ov_markers", k_overlap_markers, grid_for(nm, kBlock),
                        dim3(kBlock), s, nm, G, mk->gpu, mstart_al, mend_al, R,
                        mwin_out));
   CHOPPER_HIP(launch("ov_gpus", k_overlap_gpus, grid_for(G, kBlock),
-                     dim3(kBlock), s, G, (const int64_t*)L.gmin,
-                     (const int64_t*)L.gmax, R, gwin_out));
+                     dim3(kBlock), s, G, R, gwin_out));
   if (n > 0) {
-    CHOPPER_HIP(launch("ov_gap_tile_max", k_gap_tile_max, dim3(T),
-                       dim3(kBlock), s, n, order, rec->cls, L.gap_tiles));
-    CHOPPER_HIP(launch("ov_gap_spine", k_gap_spine, dim3(1), dim3(kBlock), s,
-                       L.gap_tiles, L.ntiles));
-    CHOPPER_HIP(launch("ov_gap_write", k_gap_write, dim3(T), dim3(kBlock), s,
+    CHOPPER_HIP(launch("ov_gap", k_gap, grid_for(n, kBlock), dim3(kBlock), s,
                        n, order, rec->gpu, rec->stream, rec->cls, start_al,
-                       end_al, (const int64_t*)L.gap_tiles, gap_out));
+                       end_al, gap_out));
   }
   return CHOPPER_OK;
 }

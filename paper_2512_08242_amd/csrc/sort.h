@@ -17,6 +17,7 @@ struct KeyRecStream {
     return cmap[(uint32_t)gpu[i] * 256u + stream[i]];
   }
   __device__ int64_t time(int64_t i) const { return t[i]; }
+  __device__ uint32_t major(int64_t i) const { return gpu[i]; }
   __host__ __device__ int nclass() const { return C; }
 };
 
@@ -31,6 +32,7 @@ struct KeyRecKind {
     return cmap[(uint32_t)gpu[i] * 2u + (uint32_t)kind_of(cl[i])];
   }
   __device__ int64_t time(int64_t i) const { return t[i]; }
+  __device__ uint32_t major(int64_t i) const { return gpu[i]; }
   __host__ __device__ int nclass() const { return C; }
 };
 
@@ -48,6 +50,7 @@ struct KeyMarker {
     return (g * (uint32_t)D + l) * 2u + (me[i] <= ms[i] ? 1u : 0u);
   }
   __device__ int64_t time(int64_t i) const { return ms[i]; }
+  __device__ uint32_t major(int64_t i) const { return gpu[i]; }
   __host__ __device__ int nclass() const { return G * D * 2 + 1; }
 };
 
@@ -73,10 +76,14 @@ ClassSortLayout class_sort_layout(Scratch& sc, int64_t n, int c_max);
 
 // out[n]: stable permutation by (class, time); coff[C + 1]: first position of
 // every class and n.  range_error: the packed key would need more than 64
-// bits (only possible on the general path).  May synchronize `s`.
+// bits (only possible on the general path).  known_sorted = 1: the caller
+// knows the input is ordered by (major, time) -- the gpu of every accessor
+// leads its class order -- so each class subsequence is already
+// time-ordered; -1: unknown, checked here.  May synchronize `s`.
 template <typename Acc>
 int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
-               uint32_t* coff, bool* range_error, hipStream_t s);
+               uint32_t* coff, bool* range_error, hipStream_t s,
+               int known_sorted);
 
 __global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v);
 __global__ void k_status_set(uint32_t bits, uint32_t* status);

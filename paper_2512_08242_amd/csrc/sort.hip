@@ -148,6 +148,20 @@ __global__ __launch_bounds__(kBlock) void k_class_verify(Acc acc, int64_t n,
     atomicOr(unsorted, 1u);
 }
 
+// is the input ordered by (major, time)?
+template <typename Acc>
+__global__ __launch_bounds__(kBlock) void k_major_sorted(Acc acc, int64_t n,
+                                                         uint32_t* unsorted) {
+  int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  bool bad = false;
+  if (p + 1 < n) {
+    const uint32_t a = acc.major(p), b = acc.major(p + 1);
+    bad = a > b || (a == b && acc.time(p + 1) < acc.time(p));
+  }
+  if (__ballot(bad) != 0 && (threadIdx.x & (kWave - 1)) == 0)
+    atomicOr(unsorted, 1u);
+}
+
 // class start offsets from the scanned table: coff[c] = first position of
 // class c, coff[C] = n
 __global__ void k_class_offsets(const uint32_t* tileoff, int64_t ntiles,
@@ -306,7 +320,8 @@ ClassSortLayout class_sort_layout(Scratch& sc, int64_t n, int C) {
 
 template <typename Acc>
 int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
-               uint32_t* coff, bool* range_error, hipStream_t s) {
+               uint32_t* coff, bool* range_error, hipStream_t s,
+               int known_sorted) {
   const int64_t n = L.n;
   const int C = acc.nclass();
   const int64_t T = L.ntiles;
@@ -319,6 +334,19 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
   }
   bool sorted = false;
   if (C <= 256) {
+    if (known_sorted < 0) {
+      // cheap sufficient test on the input: ordered by (major, time)
+      CHOPPER_HIP(launch("sort_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
+                         L.flag, (int64_t)1, 0u));
+      CHOPPER_HIP(launch("sort_major_sorted", k_major_sorted<Acc>,
+                         grid_for(n, kBlock), dim3(kBlock), s, acc, n,
+                         L.flag));
+      uint32_t unsorted = 1;
+      CHOPPER_HIP(hipMemcpyAsync(&unsorted, L.flag, sizeof(uint32_t),
+                                 hipMemcpyDeviceToHost, s));
+      CHOPPER_HIP(hipStreamSynchronize(s));
+      if (unsorted == 0) known_sorted = 1;
+    }
     CHOPPER_HIP(launch("sort_class_hist", k_class_hist<Acc>, dim3((unsigned)T),
                        dim3(kBlock), s, acc, n, T, L.tilehist));
     CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, L.tileoff, (int64_t)C * T,
@@ -329,16 +357,22 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
     CHOPPER_HIP(launch("sort_class_partition", k_class_partition<Acc>,
                        dim3((unsigned)T), dim3(kBlock), s, acc, n, T,
                        (const uint32_t*)L.tileoff, out));
-    CHOPPER_HIP(launch("sort_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
-                       L.flag, (int64_t)1, 0u));
-    CHOPPER_HIP(launch("sort_class_verify", k_class_verify<Acc>,
-                       grid_for(n, kBlock), dim3(kBlock), s, acc, n,
-                       (const uint32_t*)out, L.flag));
-    uint32_t unsorted = 1;
-    CHOPPER_HIP(hipMemcpyAsync(&unsorted, L.flag, sizeof(uint32_t),
-                               hipMemcpyDeviceToHost, s));
-    CHOPPER_HIP(hipStreamSynchronize(s));
-    sorted = (unsorted == 0);
+    if (known_sorted == 1) {
+      sorted = true;
+    } else {
+      // the partition may still be the sorted order (e.g. input already in
+      // class order): verify the class runs of the output
+      CHOPPER_HIP(launch("sort_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
+                         L.flag, (int64_t)1, 0u));
+      CHOPPER_HIP(launch("sort_class_verify", k_class_verify<Acc>,
+                         grid_for(n, kBlock), dim3(kBlock), s, acc, n,
+                         (const uint32_t*)out, L.flag));
+      uint32_t unsorted = 1;
+      CHOPPER_HIP(hipMemcpyAsync(&unsorted, L.flag, sizeof(uint32_t),
+                                 hipMemcpyDeviceToHost, s));
+      CHOPPER_HIP(hipStreamSynchronize(s));
+      sorted = (unsorted == 0);
+    }
   } else {
     CHOPPER_HIP(launch("sort_fill", k_fill_u32, grid_for(C, kBlock),
                        dim3(kBlock), s, L.tilehist, (int64_t)C, 0u));
@@ -399,10 +433,12 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
 
 template int class_sort<KeyRecStream>(const KeyRecStream&,
                                       const ClassSortLayout&, uint32_t*,
-                                      uint32_t*, bool*, hipStream_t);
+                                      uint32_t*, bool*, hipStream_t, int);
 template int class_sort<KeyRecKind>(const KeyRecKind&, const ClassSortLayout&,
-                                    uint32_t*, uint32_t*, bool*, hipStream_t);
+                                    uint32_t*, uint32_t*, bool*, hipStream_t,
+                                    int);
 template int class_sort<KeyMarker>(const KeyMarker&, const ClassSortLayout&,
-                                   uint32_t*, uint32_t*, bool*, hipStream_t);
+                                   uint32_t*, uint32_t*, bool*, hipStream_t,
+                                   int);
 
 }  // namespace chopper
