@@ -22,6 +22,7 @@
 // level reads the rows of the level below.  GPU and workload rows, which
 // are few, accumulate with atomics.
 #include "sort.h"
+#include "wave.h"
 
 namespace chopper {
 
@@ -589,97 +590,149 @@ __global__ __launch_bounds__(kBlock) void k_agg_reduce(
 // boundaries strictly increase inside each (gpu, kind) segment, which holds
 // when markers are numbered in the order they open -- rows are simply the
 // pieces in item order: no owner tables, rows numbered by counting piece
-// heads.
-constexpr int kHeadIpt = 4;
-constexpr int kHeadTile = kBlock * kHeadIpt;
+// heads.  Each wavefront works alone on a tile of kWaveTile consecutive
+// items (eight per lane); nothing is shared between the waves of a block.
+// The fast path runs only without a record filter.
+static_assert(kAggIpt == kTileIpt, "wave tiles hold eight items per lane");
 
-// Per tile of items: number of piece heads at every level in [0, D] whose bit
-// is set in `act` (tilecnt[(li - lv0) * ntiles + tile], zeros elsewhere up
-// to level D + 1); flags[0] |= 1 when a key does not increase inside its
-// segment, flags[1] |= 1 << kind for the kinds present; PATH_CONFLICT when
-// two neighbours share a key but not the path.
-template <typename Src>
+// group key from the deepest non-NONE slot
+__device__ inline uint32_t slot_key(uint32_t slot, int64_t M, uint32_t gk) {
+  if (slot == kNone) return (uint32_t)((M + (gk >> 1)) * 2 + (gk & 1u));
+  if ((int64_t)slot >= M) return kNone;
+  return slot * 2u + (gk & 1u);
+}
+
+// key of an item at level li (marker levels, then the GPU level)
+template <int MaxD>
+__device__ inline uint32_t level_key(const uint32_t (&p)[MaxD], uint32_t gk,
+                                     int li, int D, int64_t M) {
+  if (li >= D) return gk;
+  uint32_t slot = kNone;
+#pragma unroll
+  for (int l = 0; l < MaxD; ++l)
+    if (l <= li && p[l] != kNone) slot = p[l];
+  return slot_key(slot, M, gk);
+}
+
+// One item's source index, gpu * 2 + kind and path (levels >= D are NONE),
+// loaded without branches so that all loads of a tile are in flight at once.
+template <int MaxD, typename Src>
+__device__ inline void gather_item(const Src& src, int64_t i, int D,
+                                   uint32_t& r, uint32_t& gk,
+                                   uint32_t (&p)[MaxD]) {
+  r = src.index(i);
+  gk = src.gpuv(r) * 2u + src.kindv(r);
+  if (D > 0) {        // uniform; without levels there is no path column
+#pragma unroll
+    for (int l = 0; l < MaxD; ++l) {
+      const uint32_t v = src.pathv(r, l < D ? l : D - 1);
+      p[l] = l < D ? v : kNone;
+    }
+  } else {
+#pragma unroll
+    for (int l = 0; l < MaxD; ++l) p[l] = kNone;
+  }
+}
+
+// Per wave tile: number of piece heads at every level in [lv0, lv1] whose
+// bit is set in `act` (tilecnt[(li - lv0) * nwt + tile]); flags[0] |= 1 when
+// a key does not increase inside its segment, flags[1] |= 1 << kind for the
+// kinds present; PATH_CONFLICT when two neighbours share a key but not the
+// path.  Items are striped (item j * 64 + lane of the tile in lane `lane`);
+// the previous item comes from the lane below by a DPP rotate.
+template <int MaxD, typename Src>
 __global__ __launch_bounds__(kBlock) void k_agg_heads(
-    Src src, uint32_t act, int lv0, int lv1, int D, int64_t M, int64_t ntiles,
+    Src src, uint32_t act, int lv0, int lv1, int D, int64_t M, int64_t nwt,
     uint32_t* tilecnt, uint32_t* flags, uint32_t* status) {
-  __shared__ uint32_t s_path[8][kHeadTile];
-  __shared__ uint16_t s_gk[kHeadTile];
-  __shared__ uint32_t s_ppath[8];
-  __shared__ uint32_t s_pgk;
-  const int t = threadIdx.x;
+  const int lane = lane_id();
+  const int64_t w =
+      (int64_t)blockIdx.x * kWavesPerBlock + (int64_t)(threadIdx.x / kWave);
+  if (w >= nwt) return;
   const int64_t cnt = src.count();
-  const int64_t base = (int64_t)blockIdx.x * kHeadTile;
+  const int64_t base = w * kWaveTile;
   if (base >= cnt) {
-    if (t <= lv1 - lv0) tilecnt[(int64_t)t * ntiles + blockIdx.x] = 0;
+    if (lane <= lv1 - lv0) tilecnt[(int64_t)lane * nwt + w] = 0;
     return;
   }
-  const int tile_n = (int)((cnt - base) < kHeadTile ? (cnt - base) : kHeadTile);
-  for (int j = 0; j < kHeadIpt; ++j) {
-    const int q = j * kBlock + t;
-    if (q >= tile_n) continue;
-    const uint32_t r = src.index(base + q);
-    for (int l = 0; l < D; ++l) s_path[l][q] = src.pathv(r, l);
-    s_gk[q] = src.ok(r) ? (uint16_t)(src.gpuv(r) * 2u + src.kindv(r))
-                        : (uint16_t)0xFFFF;
+  const int tile_n =
+      (int)((cnt - base) < kWaveTile ? (cnt - base) : (int64_t)kWaveTile);
+  uint32_t r[kAggIpt], gk[kAggIpt], p[kAggIpt][MaxD];
+  uint32_t cr, cgk, cp[MaxD];      // the item before the tile
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int q = j * kWave + lane;
+    gather_item<MaxD>(src, base + (q < tile_n ? q : 0), D, r[j], gk[j], p[j]);
   }
-  if (t == 0) {
-    s_pgk = 0xFFFEu;     // no previous item
-    if (base > 0) {
-      const uint32_t r = src.index(base - 1);
-      for (int l = 0; l < D; ++l) s_ppath[l] = src.pathv(r, l);
-      s_pgk = src.ok(r) ? src.gpuv(r) * 2u + src.kindv(r) : 0xFFFFu;
-    }
-  }
-  __syncthreads();
-  uint32_t c[kMaxLevels];
-  for (int li = 0; li < kMaxLevels; ++li) c[li] = 0;
+  gather_item<MaxD>(src, base > 0 ? base - 1 : 0, D, cr, cgk, cp);
+  (void)cr;
+  bool cvalid = base > 0;          // lane 0's previous item exists
+  uint64_t cpk = 0;                // 4-bit head counts per level, packed
   bool notinc = false, conflict = false;
   uint32_t kinds = 0;
-  for (int j = 0; j < kHeadIpt; ++j) {
-    const int q = j * kBlock + t;
-    if (q >= tile_n) continue;
-    uint32_t p[8], pp[8];
-    for (int l = 0; l < D; ++l) {
-      p[l] = s_path[l][q];
-      pp[l] = q > 0 ? s_path[l][q - 1] : s_ppath[l];
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    // previous item: lane below; lane 0 the last lane of the previous row
+    uint32_t pp[MaxD], pgk;
+#pragma unroll
+    for (int l = 0; l < MaxD; ++l) {
+      const uint32_t x = wave_ror1_u32(p[j][l]);
+      pp[l] = lane == 0 ? cp[l] : x;
+      cp[l] = x;
     }
-    const uint32_t gk = s_gk[q];
-    const uint32_t pgk = q > 0 ? (uint32_t)s_gk[q - 1] : s_pgk;
-    if (gk == 0xFFFFu) {          // filtered item: no fast path
-      notinc = true;
-      continue;
+    {
+      const uint32_t x = wave_ror1_u32(gk[j]);
+      pgk = lane == 0 ? cgk : x;
+      cgk = x;
     }
-    const bool pvalid = pgk < 0xFFFEu;
-    for (int li = lv0; li <= lv1; ++li) {
-      if (!((act >> li) & 1u) || li > D) continue;
-      const uint32_t key = group_key(p, D, M, li, gk >> 1, gk & 1u);
-      const uint32_t pkey =
-          pvalid ? group_key(pp, D, M, li, pgk >> 1, pgk & 1u) : kNone;
+    const bool pvalid = lane != 0 || cvalid;
+    cvalid = true;
+    const bool valid = j * kWave + lane < tile_n;
+    uint32_t slot = kNone, pslot = kNone;
+    bool eq = true;
+#pragma unroll
+    for (int li = 0; li < MaxD; ++li) {
+      slot = p[j][li] != kNone ? p[j][li] : slot;
+      pslot = pp[li] != kNone ? pp[li] : pslot;
+      eq = eq && p[j][li] == pp[li];
+      if (li >= D || li < lv0 || li > lv1 || !((act >> li) & 1u)) continue;
+      const uint32_t key = slot_key(slot, M, gk[j]);
+      const uint32_t pkey = pvalid ? slot_key(pslot, M, pgk) : kNone;
       if (key != pkey && key != kNone) {
-        ++c[li];
+        cpk += (valid ? 1ull : 0ull) << (4 * li);
         // inside a segment the no-marker group may only come first, so it
         // orders before every marker key in this test
-        const int64_t ok = (li < D && key >= 2 * M) ? -1 : (int64_t)key;
-        const int64_t opk = (li < D && pkey >= 2 * M) ? -1 : (int64_t)pkey;
-        if (pvalid && pgk == gk && ok <= opk) notinc = true;
-        if (li == D) kinds |= 1u << (gk & 1u);
-      } else if (li < D) {
-        for (int l = 0; l <= li; ++l)
-          if (p[l] != pp[l]) conflict = true;
+        const int64_t ok = key >= 2 * M ? -1 : (int64_t)key;
+        const int64_t opk = pkey >= 2 * M ? -1 : (int64_t)pkey;
+        if (valid && pvalid && pgk == gk[j] && ok <= opk) notinc = true;
+      } else if (valid && pvalid && key == pkey && key != kNone && !eq) {
+        conflict = true;
       }
     }
+    if (valid && D >= lv0 && D <= lv1 && ((act >> D) & 1u) &&
+        (!pvalid || gk[j] != pgk)) {
+      cpk += 1ull << (4 * D);
+      kinds |= 1u << (gk[j] & 1u);
+    }
   }
+  // wave totals from bit planes of the per-lane counts (each at most 8)
   for (int li = lv0; li <= lv1; ++li) {
-    uint32_t tot;
-    block_exclusive(c[li], OpAdd(), 0u, &tot);
-    if (t == 0) tilecnt[(int64_t)(li - lv0) * ntiles + blockIdx.x] = tot;
+    const uint32_t c = (uint32_t)(cpk >> (4 * li)) & 15u;
+    uint32_t tot = 0;
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      tot += (uint32_t)__popcll(__ballot((c >> b) & 1u)) << b;
+    if (lane == 0) tilecnt[(int64_t)(li - lv0) * nwt + w] = tot;
   }
-  const int lane = t & (kWave - 1);
   if (__ballot(notinc) != 0 && lane == 0) atomicOr(&flags[0], 1u);
   if (__ballot(conflict) != 0 && lane == 0)
     atomicOr(status, (uint32_t)CHOPPER_ST_PATH_CONFLICT);
-  for (int d = kWave / 2; d > 0; d >>= 1) kinds |= __shfl_xor(kinds, d, kWave);
-  if (lane == 0 && kinds) atomicOr(&flags[1], kinds);
+  // kinds present: the shared word is zeroed before the launch and only
+  // gains bits, so a bit read as set here was set by this launch
+  const uint32_t kk = (__ballot(kinds & 1u) != 0 ? 1u : 0u) |
+                      (__ballot(kinds & 2u) != 0 ? 2u : 0u);
+  if (lane == 0 && kk &&
+      (__atomic_load_n(&flags[1], __ATOMIC_RELAXED) & kk) != kk)
+    atomicOr(&flags[1], kk);
 }
 
 // Fast-path level offsets: the level-major scan gives every level but the
@@ -700,188 +753,200 @@ __global__ void k_agg_offsets_fast(int L, int64_t ntiles,
     atomicOr(status, (uint32_t)CHOPPER_ST_ROWS_OVERFLOW);
 }
 
-// Combine of the fast reduction: 0 sum, 1 min, 2 max (signed).
-__device__ inline uint64_t comb_op(int op, uint64_t a, uint64_t b) {
-  if (op == 1) return (int64_t)a < (int64_t)b ? a : b;
-  if (op == 2) return (int64_t)a > (int64_t)b ? a : b;
-  return a + b;
-}
-
-struct OpSegRt {
-  int op;
-  __device__ FV<uint64_t> operator()(FV<uint64_t> a, FV<uint64_t> b) const {
-    return FV<uint64_t>{a.f | b.f, b.f ? b.v : comb_op(op, a.v, b.v)};
-  }
+// Per-tile state of the fast reduction, in the blocked arrangement (lane
+// holds items lane * 8 + j).
+struct PieceState {
+  uint32_t row[kAggIpt];   // row of the item's group (valid where m_item)
+  uint32_t m_head;         // item starts a piece
+  uint32_t m_last;         // item ends a piece that is a real group
+  uint32_t m_own;          // that piece starts its row
+  uint32_t before;         // items of the lane's first piece (no head yet)
+  WaveSegMasks masks;      // segment flags of the wave scan of lane tails
 };
 
-// segmented inclusive scan over the tile, blocked items, bit j of `heads`
-// starts a segment
-__device__ inline void seg_scan_rt(uint32_t heads, uint64_t (&x)[kAggIpt],
-                                   uint64_t ident, int op) {
-  FV<uint64_t> acc{0u, ident};
+// One field over the tile: striped values go through the wave's LDS slice
+// into the blocked arrangement, a serial segmented pass per lane and one
+// segmented wave scan of the lane tails give every piece's total at its
+// last item, which the row's first piece stores and a continuation piece
+// (only the tile's first piece can be one) leaves in the tile's overflow
+// slot.
+template <typename C>
+__device__ inline void fast_field(const PieceState& st, uint64_t* sv,
+                                  const uint64_t (&p)[kAggIpt], int lane,
+                                  uint64_t* col, uint64_t* oslot, int64_t cap) {
+  C c;
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) sv[pad8(j * kWave + lane)] = p[j];
+  wave_sync();
+  uint64_t x[kAggIpt];
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) x[j] = sv[pad8(lane * kAggIpt + j)];
+  wave_sync();
+  uint64_t acc = x[0];
+#pragma unroll
+  for (int j = 1; j < kAggIpt; ++j) {
+    acc = ((st.m_head >> j) & 1u) ? x[j] : c(acc, x[j]);
+    x[j] = acc;
+  }
+  const uint64_t incl = wave_seg_incl<C>(st.masks, acc);
+  const uint64_t carry = wave_shr1(C::ident, incl);
 #pragma unroll
   for (int j = 0; j < kAggIpt; ++j) {
-    if ((heads >> j) & 1u) acc = FV<uint64_t>{1u, x[j]};
-    else acc.v = comb_op(op, acc.v, x[j]);
-    x[j] = acc.v;
+    if (!((st.m_last >> j) & 1u) || (int64_t)st.row[j] >= cap) continue;
+    const uint64_t v = (uint32_t)j < st.before ? c(carry, x[j]) : x[j];
+    if ((st.m_own >> j) & 1u) col[st.row[j]] = v;
+    else *oslot = v;
   }
-  FV<uint64_t> tot;
-  FV<uint64_t> pre =
-      block_exclusive(acc, OpSegRt{op}, FV<uint64_t>{0u, ident}, &tot);
-  const uint32_t before = heads ? (uint32_t)(__ffs(heads) - 1) : kAggIpt;
-#pragma unroll
-  for (int j = 0; j < kAggIpt; ++j)
-    if ((uint32_t)j < before) x[j] = comb_op(op, pre.v, x[j]);
 }
 
-__device__ inline uint64_t field_ident(int f) {
-  return f == 4 ? (uint64_t)kI64Max : f == 5 ? (uint64_t)kI64Min : 0ull;
-}
-
-// Reduction of one level when groups are runs: rows numbered by counting
-// real piece heads (key differs from the previous item's); items staged
-// through LDS so that every global load is coalesced, then reduced in a
-// blocked arrangement by segmented scans, the loads of the next field in
-// flight while the current one is scanned.  The piece that starts a row
-// stores it and writes its header; a piece continuing a row from the
-// previous tile goes to the overflow list.
-template <typename Src>
+// Reduction of one level when groups are runs.  Rows are numbered from the
+// tile's head count (level-major exclusive scan of the heads pass) plus the
+// real heads of the lanes below; the piece that starts a row writes its
+// header.  Field loads are striped and coalesced, two fields in flight.
+template <int MaxD, typename Src>
 __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     Src src, int li, int D, int64_t M, const uint32_t* tilebase,
-    const int64_t* row0, RowsDev R, Overflow ovf, int nfields) {
-  __shared__ uint32_t s_r[kAggTile];
-  __shared__ uint32_t s_key[kAggTile];
-  __shared__ uint64_t s_v[kAggTile];
-  __shared__ uint32_t s_head0[kBlock];
-  __shared__ uint32_t s_prevkey;
-  const int t = threadIdx.x;
+    const int64_t* row0, RowsDev R, Overflow ovf, int nfields, int64_t nwt) {
+  __shared__ uint64_t s_v[kWavesPerBlock][kSlice];
+  const int lane = lane_id();
+  const int wv = (int)(threadIdx.x / kWave);
+  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wv;
+  if (w >= nwt) return;
   const int64_t cnt = src.count();
-  const int64_t base = (int64_t)blockIdx.x * kAggTile;
-  if (base >= cnt) return;
-  const int tile_n = (int)((cnt - base) < kAggTile ? (cnt - base) : kAggTile);
-  for (int j = 0; j < kAggIpt; ++j) {
-    const int q = j * kBlock + t;
-    if (q >= tile_n) continue;
-    const uint32_t r = src.index(base + q);
-    s_r[q] = r;
-    s_key[q] = src.keyof(r, li);
+  const int64_t base = w * kWaveTile;
+  if (base >= cnt) {
+    if (lane == 0) ovf.row[w] = kNone;
+    return;
   }
-  if (t == 0)
-    s_prevkey = base > 0 ? src.keyof(src.index(base - 1), li) : kNone;
-  // first field in flight while the pieces are worked out
-  uint64_t pf[kAggIpt];
-  __syncthreads();
+  const int tile_n =
+      (int)((cnt - base) < kWaveTile ? (cnt - base) : (int64_t)kWaveTile);
+  uint64_t* sv = s_v[wv];
+  uint32_t* sk = (uint32_t*)sv;
+  // striped items: source index, gpu * 2 + kind, path, key
+  uint32_t rs[kAggIpt], gk[kAggIpt], p[kAggIpt][MaxD];
+  uint32_t tile_prev;
   {
-    const uint64_t id0 = field_ident(0);
-    const FieldRef fr = src.fref(0);
 #pragma unroll
     for (int j = 0; j < kAggIpt; ++j) {
-      const int q = j * kBlock + t;
-      pf[j] = (q < tile_n && s_key[q] != kNone) ? fr.get(s_r[q]) : id0;
+      const int q = j * kWave + lane;
+      gather_item<MaxD>(src, base + (q < tile_n ? q : 0), D, rs[j], gk[j],
+                        p[j]);
+    }
+    uint32_t cr, cgk, cp[MaxD];
+    gather_item<MaxD>(src, base > 0 ? base - 1 : 0, D, cr, cgk, cp);
+    tile_prev = base > 0 ? level_key<MaxD>(cp, cgk, li, D, M) : kNone;
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) {
+      const int q = j * kWave + lane;
+      sk[pad8(q)] = q < tile_n ? level_key<MaxD>(p[j], gk[j], li, D, M)
+                               : kNone;
     }
   }
-  uint32_t m_item = 0, m_real = 0, m_head = 0, m_last = 0;
-  uint32_t c = 0;
+  wave_sync();
+  uint32_t key[kAggIpt];
 #pragma unroll
-  for (int j = 0; j < kAggIpt; ++j) {
-    const int q = t * kAggIpt + j;
-    const bool valid = q < tile_n;
-    const uint32_t key = valid ? s_key[q] : kNone;
-    const uint32_t prev = q == 0 ? s_prevkey : s_key[q - 1];
-    if (valid && key != kNone) m_item |= 1u << j;
-    if (valid && key != kNone && key != prev) m_real |= 1u << j;
-    if (!valid || q == 0 || key != prev) m_head |= 1u << j;
-    c += (m_real >> j) & 1u;
-  }
-  uint32_t tot;
-  const uint32_t ex = block_exclusive(c, OpAdd(), 0u, &tot);
-  int64_t running = (row0 ? *row0 : 0) +
-                    (int64_t)tilebase[base / kHeadTile] + ex;
-  uint32_t row[kAggIpt];
-#pragma unroll
-  for (int j = 0; j < kAggIpt; ++j) {
-    running += (m_real >> j) & 1u;
-    row[j] = ((m_item >> j) & 1u) ? (uint32_t)(running - 1) : kNone;
-  }
-  s_head0[t] = m_head & 1u;
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < kAggIpt; ++j) {
-    const bool next_head = j + 1 < kAggIpt ? ((m_head >> (j + 1)) & 1u)
-                          : (t + 1 < kBlock ? s_head0[t + 1] != 0 : true);
-    if (((m_item >> j) & 1u) && next_head) m_last |= 1u << j;
-  }
-  // headers of the rows that start here
-#pragma unroll
-  for (int j = 0; j < kAggIpt; ++j) {
-    if (!((m_real >> j) & 1u) || (int64_t)row[j] >= R.cap) continue;
-    const uint32_t r = s_r[t * kAggIpt + j], w = row[j];
-    for (int l = 0; l < D; ++l)
-      R.path[(int64_t)l * R.cap + w] = (li < D && l <= li) ? src.pathv(r, l)
-                                                           : kNone;
-    R.gpu[w] = (uint8_t)src.gpuv(r);
-    R.kind[w] = (uint8_t)src.kindv(r);
-    R.first[w] = src.first_of(r);
-  }
-  // does the piece start a row?  (propagated from its first item)
-  uint32_t m_own = 0;
+  for (int j = 0; j < kAggIpt; ++j) key[j] = sk[pad8(lane * kAggIpt + j)];
+  wave_sync();
+  PieceState st;
+  uint32_t m_item = 0, m_real = 0, m_head = 0;
   {
-    uint64_t ob[kAggIpt];
+    uint32_t prev = wave_shr1_u32(tile_prev, key[kAggIpt - 1]);
 #pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) ob[j] = (m_real >> j) & 1u;
-    seg_scan_rt(m_head, ob, 0ull, 0);
-#pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) m_own |= (ob[j] ? 1u : 0u) << j;
+    for (int j = 0; j < kAggIpt; ++j) {
+      const int q = lane * kAggIpt + j;
+      const bool valid = q < tile_n;
+      const uint32_t k = key[j];
+      if (valid && k != kNone) m_item |= 1u << j;
+      if (valid && k != kNone && k != prev) m_real |= 1u << j;
+      if (!valid || q == 0 || k != prev) m_head |= 1u << j;
+      prev = k;
+    }
   }
-  uint32_t slot[kAggIpt];
+  st.m_head = m_head;
+  // rows: tile base + real heads of the lanes below + those before j here
+  {
+    int64_t running = (row0 ? *row0 : 0) + (int64_t)tilebase[w] +
+                      wave_prefix_small<4>((uint32_t)__popc(m_real));
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) {
+      running += (m_real >> j) & 1u;
+      st.row[j] = (uint32_t)(running - 1);
+    }
+  }
+  // last item of a piece: the next item starts one (the tile's end does)
+  {
+    const uint64_t h0 = __ballot(m_head & 1u);
+    const uint32_t next0 =
+        lane == kWave - 1 ? 1u : (uint32_t)((h0 >> (lane + 1)) & 1u);
+    st.m_last = m_item & ((m_head >> 1) | (next0 << (kAggIpt - 1)));
+  }
+  // does the piece start its row?  The lane's first piece continues the
+  // last piece of the nearest lane below that has a head.
+  {
+    const uint64_t ha = __ballot(m_head != 0);
+    const bool last_real =
+        m_head != 0 && ((m_real >> (31 - __clz(m_head))) & 1u);
+    const uint64_t lr = __ballot(last_real);
+    const uint64_t below = ha & ((1ull << lane) - 1ull);
+    uint32_t own = below ? (uint32_t)((lr >> (63 - __clzll(below))) & 1ull)
+                         : 0u;
+    uint32_t m_own = 0;
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) {
+      if ((m_head >> j) & 1u) own = (m_real >> j) & 1u;
+      m_own |= own << j;
+    }
+    st.m_own = m_own;
+  }
+  st.before = m_head ? (uint32_t)(__ffs(m_head) - 1) : (uint32_t)kAggIpt;
+  st.masks = wave_seg_masks(m_head != 0);
+  // headers of the rows that start here, written from the striped items:
+  // the row of every real head goes back through LDS
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j)
+    sk[pad8(lane * kAggIpt + j)] = ((m_real >> j) & 1u) ? st.row[j] : kNone;
+  wave_sync();
 #pragma unroll
   for (int j = 0; j < kAggIpt; ++j) {
-    slot[j] = kNone;
-    if (((m_last & ~m_own) >> j) & 1u && (int64_t)row[j] < R.cap) {
-      const uint32_t e = atomicAdd(ovf.count, 1u);
-      if ((int64_t)e < ovf.cap) {
-        slot[j] = e;
-        ovf.row[e] = row[j];
-      } else {
-        atomicOr(ovf.lost, 1u);
-      }
-    }
+    const uint32_t wr = sk[pad8(j * kWave + lane)];
+    if (wr == kNone || (int64_t)wr >= R.cap) continue;
+#pragma unroll
+    for (int l = 0; l < MaxD; ++l)
+      if (l < D)
+        R.path[(int64_t)l * R.cap + wr] = (li < D && l <= li) ? p[j][l] : kNone;
+    R.gpu[wr] = (uint8_t)(gk[j] >> 1);
+    R.kind[wr] = (uint8_t)(gk[j] & 1u);
+    R.first[wr] = src.first_of(rs[j]);
   }
-  for (int f = 0; f < nfields; ++f) {
-    const uint64_t ident = field_ident(f);
-    const int op = f == 4 ? 1 : f == 5 ? 2 : 0;
+  wave_sync();
+  // the tile's first piece continues a row of an earlier tile
+  if (lane == 0)
+    ovf.row[w] = ((m_item & ~m_real) & 1u) && (int64_t)st.row[0] < R.cap
+                     ? st.row[0]
+                     : kNone;
+  uint64_t pa[kAggIpt], pb[kAggIpt];
+  auto load = [&](int f, uint64_t (&v)[kAggIpt]) {
+    if (f >= nfields) return;
+    const FieldRef fr = src.fref(f);
 #pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) {
-      const int q = j * kBlock + t;
-      if (q < tile_n) s_v[q] = pf[j];
-    }
-    __syncthreads();
-    if (f + 1 < nfields) {
-      const uint64_t idn = field_ident(f + 1);
-      const FieldRef fr = src.fref(f + 1);
-#pragma unroll
-      for (int j = 0; j < kAggIpt; ++j) {
-        const int q = j * kBlock + t;
-        pf[j] = (q < tile_n && s_key[q] != kNone) ? fr.get(s_r[q]) : idn;
-      }
-    }
-    uint64_t x[kAggIpt];
-#pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) {
-      const int q = t * kAggIpt + j;
-      x[j] = q < tile_n ? s_v[q] : ident;
-    }
-    // the scan's barriers also order these reads before the next field's
-    // writes to s_v
-    seg_scan_rt(m_head, x, ident, op);
+    for (int j = 0; j < kAggIpt; ++j) v[j] = fr.get(rs[j]);
+  };
+  auto step = [&](int f, uint64_t (&v)[kAggIpt]) {
     uint64_t* col = row_column(R, f);
-    uint64_t* ocol = ovf.val + (int64_t)f * ovf.cap;
+    uint64_t* oslot = ovf.val + (int64_t)f * ovf.cap + w;
+    uint64_t cur[kAggIpt];
 #pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) {
-      if (!((m_last >> j) & 1u) || (int64_t)row[j] >= R.cap) continue;
-      if ((m_own >> j) & 1u) col[row[j]] = x[j];
-      else if (slot[j] != kNone) ocol[slot[j]] = x[j];
-    }
+    for (int j = 0; j < kAggIpt; ++j) cur[j] = v[j];
+    load(f + 2, v);
+    if (f == 4) fast_field<CMin>(st, sv, cur, lane, col, oslot, R.cap);
+    else if (f == 5) fast_field<CMax>(st, sv, cur, lane, col, oslot, R.cap);
+    else fast_field<CSum>(st, sv, cur, lane, col, oslot, R.cap);
+  };
+  load(0, pa);
+  load(1, pb);
+  for (int f = 0; f < nfields; f += 2) {
+    step(f, pa);
+    if (f + 1 < nfields) step(f + 1, pb);
   }
 }
 
@@ -954,13 +1019,16 @@ __global__ __launch_bounds__(kBlock) void k_agg_workload_first(
     atomicMin(&R.first[row], src.first_of(r));
 }
 
+// Entries [0, nslots), or [0, *count) when nslots < 0; a slot holding
+// kNone is empty.
 __global__ __launch_bounds__(kBlock) void k_agg_apply_overflow(
-    Overflow ovf, RowsDev R, int nfields) {
+    Overflow ovf, RowsDev R, int nfields, int64_t nslots) {
   const int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  int64_t cnt = *ovf.count;
+  int64_t cnt = nslots >= 0 ? nslots : (int64_t)*ovf.count;
   if (cnt > ovf.cap) cnt = ovf.cap;
   if (e >= cnt) return;
   const uint32_t row = ovf.row[e];
+  if (row == kNone || (int64_t)row >= R.cap) return;
   for (int f = 0; f < nfields; ++f)
     atomic_field(R, f, row, ovf.val[(int64_t)f * ovf.cap + e]);
 }
@@ -1015,7 +1083,7 @@ struct AggLayout {
   uint32_t* ovf_row;
   uint64_t* ovf_val;
   int64_t ovf_cap;
-  // fast path: head counts per tile of kHeadTile items
+  // fast path: head counts per wave tile of kWaveTile items
   int64_t ntiles_h;
   uint32_t* htc;          // [L][ntiles_h]
   uint32_t* htb;
@@ -1049,7 +1117,7 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
   L.ovf_count = sc.take<uint32_t>(2);
   L.ovf_row = sc.take<uint32_t>(L.ovf_cap);
   L.ovf_val = sc.take<uint64_t>((int64_t)kMaxFields * L.ovf_cap);
-  L.ntiles_h = ceil_div(n, kHeadTile);
+  L.ntiles_h = ceil_div(n, kWaveTile);
   L.htc = sc.take<uint32_t>((int64_t)L.L * L.ntiles_h);
   L.htb = sc.take<uint32_t>((int64_t)L.L * L.ntiles_h);
   L.hscan = sc.take<uint32_t>(scan_scratch_elems((int64_t)L.L * L.ntiles_h));
@@ -1064,6 +1132,86 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
 }  // namespace chopper
 
 using namespace chopper;
+
+// Fast path over all requested levels (MaxD >= depth); returns 1 when the
+// groups are not runs and the general path must be used.
+template <int kMD>
+static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
+                    const Overflow& ovf, int64_t T, int Lv, uint32_t act,
+                    int D, int64_t M, int nfields, chopper_rows* rows,
+                    int level, bool want_workload, uint32_t* status,
+                    hipStream_t s) {
+  int rc = CHOPPER_OK;
+  const int64_t Th = L.ntiles_h;
+  FromRecords fr{S};
+  CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s, L.hflags,
+                     2));
+  const unsigned gh = (unsigned)ceil_div(Th, (int64_t)kWavesPerBlock);
+  CHOPPER_HIP(launch("agg_heads_records", k_agg_heads<kMD, FromRecords>,
+                     dim3(gh), dim3(kBlock), s, fr, act, 0,
+                     Lv - 1, D, M, Th, L.htc, L.hflags, status));
+  CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc, L.htb, (int64_t)Lv * Th,
+                                       L.hscan, L.htotal, s));
+  CHOPPER_HIP(launch("agg_offsets", k_agg_offsets_fast, dim3(1), dim3(64),
+                     s, Lv, Th, (const uint32_t*)L.htb,
+                     (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
+                     want_workload, rows->cap, rows->level_offset, status));
+  uint32_t hf[2] = {1u, 0u};
+  CHOPPER_HIP(hipMemcpyAsync(hf, L.hflags, sizeof(hf), hipMemcpyDeviceToHost,
+                             s));
+  CHOPPER_HIP(hipStreamSynchronize(s));
+  if (hf[0] == 0) {
+    auto fast_level = [&](int li, int finer) -> int {
+      if (finer < 0) {
+        CHOPPER_HIP(launch("agg_fast_reduce_records",
+                           k_agg_fast_reduce<kMD, FromRecords>,
+                           dim3((unsigned)T), dim3(kBlock), s, fr, li, D, M,
+                           (const uint32_t*)(L.htb + (int64_t)li * Th),
+                           (const int64_t*)nullptr, R, ovf, nfields, Th));
+      } else {
+        FromRows src{R, M, rows->level_offset, finer};
+        CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
+                           L.hflags2, 2));
+        CHOPPER_HIP(launch("agg_heads_rows", k_agg_heads<kMD, FromRows>,
+                           dim3(gh), dim3(kBlock), s, src,
+                           1u << li, li, li, D, M, Th, L.htc2, L.hflags2,
+                           status));
+        CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc2, L.htb2, Th, L.hscan,
+                                             L.htotal + 1, s));
+        CHOPPER_HIP(launch("agg_fast_reduce_rows",
+                           k_agg_fast_reduce<kMD, FromRows>, dim3((unsigned)T),
+                           dim3(kBlock), s, src, li, D, M,
+                           (const uint32_t*)L.htb2,
+                           (const int64_t*)(rows->level_offset + li), R, ovf,
+                           nfields, Th));
+      }
+      CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
+                         grid_for(Th, kBlock), dim3(kBlock), s, ovf, R,
+                         nfields, Th));
+      return CHOPPER_OK;
+    };
+    if (level == CHOPPER_LEVEL_ALL) {
+      rc = fast_level(D > 0 ? D - 1 : D, -1);
+      if (rc != CHOPPER_OK) return rc;
+      for (int li = D - 2; li >= 0; --li) {
+        rc = fast_level(li, li + 1);
+        if (rc != CHOPPER_OK) return rc;
+      }
+      if (D > 0) {
+        rc = fast_level(D, 0);
+        if (rc != CHOPPER_OK) return rc;
+      }
+      CHOPPER_HIP(launch("agg_workload_from_gpu", k_agg_workload_from_gpu,
+                         dim3(1), dim3(64), s,
+                         (const int64_t*)rows->level_offset, D, R, nfields));
+    } else {
+      rc = fast_level(level == CHOPPER_LEVEL_GPU ? D : level, -1);
+      if (rc != CHOPPER_OK) return rc;
+    }
+    return CHOPPER_OK;
+  }
+  return 1;
+}
 
 extern "C" int chopper_aggregate(const chopper_records* rec,
                                  const int64_t* start_al,
@@ -1161,80 +1309,11 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
 
   // ---- fast path: every group is one run of consecutive records
   if (n > 0 && !filter && level != CHOPPER_LEVEL_WORKLOAD) {
-    const int64_t Th = L.ntiles_h;
-    FromRecords fr{S};
-    CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s, L.hflags,
-                       2));
-    CHOPPER_HIP(launch("agg_heads_records", k_agg_heads<FromRecords>,
-                       dim3((unsigned)Th), dim3(kBlock), s, fr, act, 0,
-                       Lv - 1, D, M, Th, L.htc, L.hflags, status));
-    CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc, L.htb, (int64_t)Lv * Th,
-                                         L.hscan, L.htotal, s));
-    CHOPPER_HIP(launch("agg_offsets", k_agg_offsets_fast, dim3(1), dim3(64),
-                       s, Lv, Th, (const uint32_t*)L.htb,
-                       (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
-                       want_workload, rows->cap, rows->level_offset, status));
-    uint32_t hf[2] = {1u, 0u};
-    CHOPPER_HIP(hipMemcpyAsync(hf, L.hflags, sizeof(hf), hipMemcpyDeviceToHost,
-                               s));
-    CHOPPER_HIP(hipStreamSynchronize(s));
-    if (hf[0] == 0) {
-      auto fast_level = [&](int li, int finer) -> int {
-        CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
-                           L.ovf_count, 1));
-        if (finer < 0) {
-          CHOPPER_HIP(launch("agg_fast_reduce_records",
-                             k_agg_fast_reduce<FromRecords>,
-                             dim3((unsigned)T), dim3(kBlock), s, fr, li, D, M,
-                             (const uint32_t*)(L.htb + (int64_t)li * Th),
-                             (const int64_t*)nullptr, R, ovf, nfields));
-        } else {
-          FromRows src{R, M, rows->level_offset, finer};
-          CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
-                             L.hflags2, 2));
-          CHOPPER_HIP(launch("agg_heads_rows", k_agg_heads<FromRows>,
-                             dim3((unsigned)Th), dim3(kBlock), s, src,
-                             1u << li, li, li, D, M, Th, L.htc2, L.hflags2,
-                             status));
-          CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc2, L.htb2, Th, L.hscan,
-                                               L.htotal + 1, s));
-          CHOPPER_HIP(launch("agg_fast_reduce_rows",
-                             k_agg_fast_reduce<FromRows>, dim3((unsigned)T),
-                             dim3(kBlock), s, src, li, D, M,
-                             (const uint32_t*)L.htb2,
-                             (const int64_t*)(rows->level_offset + li), R, ovf,
-                             nfields));
-        }
-        CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
-                           grid_for(L.ovf_cap, kBlock), dim3(kBlock), s, ovf,
-                           R, nfields));
-        return CHOPPER_OK;
-      };
-      if (level == CHOPPER_LEVEL_ALL) {
-        rc = fast_level(D > 0 ? D - 1 : D, -1);
-        if (rc != CHOPPER_OK) return rc;
-        for (int li = D - 2; li >= 0; --li) {
-          rc = fast_level(li, li + 1);
-          if (rc != CHOPPER_OK) return rc;
-        }
-        if (D > 0) {
-          rc = fast_level(D, 0);
-          if (rc != CHOPPER_OK) return rc;
-        }
-        CHOPPER_HIP(launch("agg_workload_from_gpu", k_agg_workload_from_gpu,
-                           dim3(1), dim3(64), s,
-                           (const int64_t*)rows->level_offset, D, R, nfields));
-      } else {
-        rc = fast_level(level == CHOPPER_LEVEL_GPU ? D : level, -1);
-        if (rc != CHOPPER_OK) return rc;
-      }
-      uint32_t lost = 0;
-      CHOPPER_HIP(hipMemcpyAsync(&lost, L.ovf_count + 1, sizeof(uint32_t),
-                                 hipMemcpyDeviceToHost, s));
-      CHOPPER_HIP(hipStreamSynchronize(s));
-      if (!lost) return CHOPPER_OK;
-      // an overflow list that did not fit: use the general path below
-    }
+    rc = D <= 4 ? agg_fast<4>(L, S, R, ovf, T, Lv, act, D, M, nfields, rows,
+                              level, want_workload, status, s)
+                : agg_fast<8>(L, S, R, ovf, T, Lv, act, D, M, nfields, rows,
+                              level, want_workload, status, s);
+    if (rc != 1) return rc;
   }
 
   // ---- general path: per-level owner election
@@ -1302,7 +1381,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
     if (!atomic_mode)
       CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
                          grid_for(L.ovf_cap, kBlock), dim3(kBlock), s, ovf, R,
-                         nfields));
+                         nfields, (int64_t)-1));
     if (li == D + 1) {
       if (finer < 0) {
         FromRecords src{S};

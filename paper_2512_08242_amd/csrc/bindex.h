@@ -1,0 +1,84 @@
+// Bucket index over a segmented sorted key array.
+//
+// Every segment [sb, se) of non-decreasing int64 keys gets a table of
+// power-of-two time buckets: entry b is the first position whose key is at
+// least lo + (b << shift), entry nb is se.  The number of buckets is about
+// a quarter of the keys, so a search for the last key <= t reads the
+// segment's parameters, two adjacent table entries and then binary-searches
+// the few keys of one bucket; a skewed key distribution only makes some
+// buckets wider, never worse than a plain binary search of the segment.
+#pragma once
+
+#include "common.h"
+
+namespace chopper {
+
+struct BSeg {
+  int64_t lo;        // first key of the segment
+  uint32_t sb, se;   // positions of the segment's keys
+  uint32_t shift;    // log2 of the bucket width
+  uint32_t nb;       // buckets; 0: no table, search the whole segment
+  uint32_t toff;     // first table entry of the segment
+  uint32_t pad;
+};
+
+struct BIndex {
+  const int64_t* key;
+  const BSeg* seg;
+  const uint32_t* table;
+};
+
+// first position in [lo, hi) with key > t
+__device__ inline int64_t bi_bsearch(const int64_t* key, int64_t lo,
+                                     int64_t hi, int64_t t) {
+  while (lo < hi) {
+    const int64_t mid = lo + ((hi - lo) >> 1);
+    if (key[mid] <= t) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Search range of t in segment P: the answer (first position with key > t)
+// lies in [*lo, *hi].
+__device__ inline void bi_range(const BIndex& X, const BSeg& P, int64_t t,
+                                int64_t* lo, int64_t* hi) {
+  if (P.se <= P.sb || t < P.lo) {
+    *lo = *hi = P.sb;
+    return;
+  }
+  if (P.nb == 0) {
+    *lo = P.sb;
+    *hi = P.se;
+    return;
+  }
+  const uint64_t b = ((uint64_t)t - (uint64_t)P.lo) >> P.shift;
+  if (b >= P.nb) {
+    *lo = *hi = P.se;
+    return;
+  }
+  *lo = X.table[P.toff + b];
+  *hi = X.table[P.toff + b + 1];
+}
+
+// first position of segment s with key > t (the segment's start if none)
+__device__ inline int64_t bi_upper(const BIndex& X, uint32_t s, int64_t t) {
+  const BSeg P = X.seg[s];
+  int64_t lo, hi;
+  bi_range(X, P, t, &lo, &hi);
+  return bi_bsearch(X.key, lo, hi, t);
+}
+
+// Scratch: segment parameters and the table for nkeys keys in nseg segments.
+int64_t bindex_table_cap(int64_t nkeys, int64_t nseg);
+
+// Builds the index.  Segment s spans [sbeg[s * stride], send[s * stride]);
+// keyseg[i] is the segment of key i or kNone; *nkeys_dev (device) bounds the
+// keys actually present when non-null.  `tmp` holds nseg + 1 uint32.
+hipError_t bindex_build(const int64_t* key, const uint32_t* keyseg,
+                        int64_t nkeys, const uint32_t* nkeys_dev,
+                        const uint32_t* sbeg, const uint32_t* send, int stride,
+                        int nseg, BSeg* segs, uint32_t* table,
+                        int64_t table_cap, uint32_t* tmp, hipStream_t s);
+
+}  // namespace chopper

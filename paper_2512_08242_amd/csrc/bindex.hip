@@ -1,0 +1,184 @@
+// Construction of the bucket index (see bindex.h).
+//
+//   1. per segment: first key, bucket width (smallest power of two with at
+//      most ceil(count / 4) buckets over the key span), bucket count;
+//   2. one block scans the table sizes into offsets;
+//   3. every key writes the entries of the buckets that start in the gap
+//      after the previous key (at most kFillRun of them, so no thread stalls
+//      on a long gap), the last key also the entries after it;
+//   4. entries still unset (long gaps only) are found by binary search.
+#include "bindex.h"
+#include "wave.h"
+
+namespace chopper {
+
+constexpr int kKeysPerBucket = 4;
+constexpr int kFillRun = 32;
+constexpr uint32_t kUnset = 0xFFFFFFFFu;
+
+int64_t bindex_table_cap(int64_t nkeys, int64_t nseg) {
+  return nkeys / kKeysPerBucket + 2 * nseg + 2;
+}
+
+__global__ __launch_bounds__(kBlock) void k_bi_params(
+    const int64_t* key, const uint32_t* sbeg, const uint32_t* send, int stride,
+    int nseg, BSeg* segs, uint32_t* entries) {
+  const int sidx = blockIdx.x * kBlock + threadIdx.x;
+  if (sidx >= nseg) return;
+  BSeg P;
+  P.sb = sbeg[(int64_t)sidx * stride];
+  P.se = send[(int64_t)sidx * stride];
+  P.lo = 0;
+  P.shift = 0;
+  P.nb = 0;
+  P.toff = 0;
+  P.pad = 0;
+  uint32_t ent = 0;
+  if (P.se > P.sb) {
+    const int64_t cnt = (int64_t)P.se - P.sb;
+    P.lo = key[P.sb];
+    const int64_t d = (int64_t)((uint64_t)key[P.se - 1] - (uint64_t)P.lo);
+    const uint64_t span = d > 0 ? (uint64_t)d : 0;   // keys sorted
+    const uint64_t target =
+        (uint64_t)((cnt + kKeysPerBucket - 1) / kKeysPerBucket);
+    uint32_t k = 0;
+    while (k < 63 && (span >> k) + 1 > target) ++k;
+    P.shift = k;
+    P.nb = (uint32_t)((span >> k) + 1);
+    ent = P.nb + 1;
+  }
+  segs[sidx] = P;
+  entries[sidx] = ent;
+}
+
+// exclusive scan of the entry counts (one block); segments that would not
+// fit keep no table and are searched whole
+__global__ __launch_bounds__(1024) void k_bi_offsets(int nseg, BSeg* segs,
+                                                     const uint32_t* entries,
+                                                     int64_t cap,
+                                                     uint32_t* total) {
+  __shared__ uint32_t s_w[1024 / kWave];
+  const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
+  uint64_t carry = 0;
+  for (int base = 0; base < nseg; base += 1024) {
+    const int i = base + (int)threadIdx.x;
+    const uint32_t v = i < nseg ? entries[i] : 0u;
+    const uint32_t incl = wave_incl(v, OpAdd(), 0u);
+    if (lane == kWave - 1) s_w[w] = incl;
+    __syncthreads();
+    uint64_t pre = carry, tot = carry;
+    for (int q = 0; q < 1024 / kWave; ++q) {
+      if (q < w) pre += s_w[q];
+      tot += s_w[q];
+    }
+    pre += incl - v;
+    if (i < nseg) {
+      // offsets are stored for every segment, so they never decrease
+      segs[i].toff = (uint32_t)(pre < (uint64_t)cap ? pre : cap);
+      if (pre + v > (uint64_t)cap) segs[i].nb = 0;
+    }
+    carry = tot;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *total = (uint32_t)(carry < (uint64_t)cap ? carry : cap);
+}
+
+__global__ __launch_bounds__(kBlock) void k_bi_clear(uint32_t* table,
+                                                     const uint32_t* total) {
+  const int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (e < (int64_t)*total) table[e] = kUnset;
+}
+
+__global__ __launch_bounds__(kBlock) void k_bi_fill(
+    const int64_t* key, const uint32_t* keyseg, int64_t nkeys,
+    const uint32_t* nkeys_dev, const BSeg* segs, uint32_t* table) {
+  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i >= nkeys || (nkeys_dev && i >= (int64_t)*nkeys_dev)) return;
+  const uint32_t sidx = keyseg[i];
+  if (sidx == kNone) return;
+  const BSeg P = segs[sidx];
+  if (P.nb == 0 || i < P.sb || i >= P.se) return;
+  // bucket of a key, clamped to the table (keys are sorted, so the clamp
+  // only guards against inputs that are not)
+  auto bucket = [&](int64_t k) -> int64_t {
+    const uint64_t d = (uint64_t)k - (uint64_t)P.lo;
+    if ((int64_t)d < 0) return 0;
+    const uint64_t b = d >> P.shift;
+    return b < (uint64_t)P.nb ? (int64_t)b : (int64_t)P.nb - 1;
+  };
+  const int64_t bi = bucket(key[i]);
+  const int64_t bp = i == P.sb ? -1 : bucket(key[i - 1]);
+  uint32_t* tb = table + P.toff;
+  const int64_t hi1 = bi < bp + kFillRun ? bi : bp + kFillRun;
+  for (int64_t b = bp + 1; b <= hi1; ++b) tb[b] = (uint32_t)i;
+  if (i == (int64_t)P.se - 1) {
+    const int64_t hi2 =
+        (int64_t)P.nb < bi + kFillRun ? (int64_t)P.nb : bi + kFillRun;
+    for (int64_t b = bi + 1; b <= hi2; ++b) tb[b] = P.se;
+  }
+}
+
+// entries inside long gaps: lower bound of the bucket start by search
+__global__ __launch_bounds__(kBlock) void k_bi_fixup(const int64_t* key,
+                                                     const BSeg* segs, int nseg,
+                                                     uint32_t* table,
+                                                     const uint32_t* total) {
+  const int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (e >= (int64_t)*total || table[e] != kUnset) return;
+  // owner of entry e: the last segment whose table starts at or before e
+  // (a segment without entries shares its offset with the next one)
+  int lo = 0, hi = nseg;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if ((int64_t)segs[mid].toff <= e) lo = mid + 1;
+    else hi = mid;
+  }
+  const int sidx = lo - 1;
+  if (sidx < 0 || segs[sidx].nb == 0) return;
+  const BSeg P = segs[sidx];
+  const int64_t b = e - P.toff;
+  if (b > (int64_t)P.nb) return;
+  uint32_t v = P.se;
+  if (b < (int64_t)P.nb) {
+    const int64_t B = (int64_t)((uint64_t)P.lo + ((uint64_t)b << P.shift));
+    // first position with key >= B
+    int64_t l = P.sb, h = P.se;
+    while (l < h) {
+      const int64_t mid = l + ((h - l) >> 1);
+      if (key[mid] < B) l = mid + 1;
+      else h = mid;
+    }
+    v = (uint32_t)l;
+  }
+  table[e] = v;
+}
+
+hipError_t bindex_build(const int64_t* key, const uint32_t* keyseg,
+                        int64_t nkeys, const uint32_t* nkeys_dev,
+                        const uint32_t* sbeg, const uint32_t* send, int stride,
+                        int nseg, BSeg* segs, uint32_t* table,
+                        int64_t table_cap, uint32_t* tmp, hipStream_t s) {
+  if (nseg <= 0) return hipSuccess;
+  uint32_t* entries = tmp;
+  uint32_t* total = tmp + nseg;
+  hipError_t e;
+  e = launch("bi_params", k_bi_params, grid_for(nseg, kBlock), dim3(kBlock), s,
+             key, sbeg, send, stride, nseg, segs, entries);
+  if (e != hipSuccess) return e;
+  e = launch("bi_offsets", k_bi_offsets, dim3(1), dim3(1024), s, nseg, segs,
+             (const uint32_t*)entries, table_cap, total);
+  if (e != hipSuccess) return e;
+  e = launch("bi_clear", k_bi_clear, grid_for(table_cap, kBlock), dim3(kBlock),
+             s, table, (const uint32_t*)total);
+  if (e != hipSuccess) return e;
+  if (nkeys > 0) {
+    e = launch("bi_fill", k_bi_fill, grid_for(nkeys, kBlock), dim3(kBlock), s,
+               key, keyseg, nkeys, nkeys_dev, (const BSeg*)segs, table);
+    if (e != hipSuccess) return e;
+  }
+  return launch("bi_fixup", k_bi_fixup, grid_for(table_cap, kBlock),
+                dim3(kBlock), s, key, (const BSeg*)segs, nseg, table,
+                (const uint32_t*)total);
+}
+
+}  // namespace chopper

@@ -12,6 +12,8 @@
 // communication run, so every window (kernel, marker, GPU) costs a few
 // binary searches and no per-window sweep.
 #include "sort.h"
+#include "wave.h"
+#include "bindex.h"
 
 namespace chopper {
 
@@ -21,205 +23,459 @@ bool validate_markers(const chopper_markers* m);
 constexpr int kOvIpt = 8;
 constexpr int kOvTile = kBlock * kOvIpt;
 constexpr int kSegs = 512;            // gpu * 2 + kind
+static_assert(kOvTile == kWavesPerBlock * kWaveTile, "tile = block = 4 waves");
 
 struct Runs {
   const int64_t* rs;      // run start
   const int64_t* re;      // run end
-  const int64_t* pl;      // exclusive prefix of run lengths
+  const int64_t* pl;      // active time of the segment before the run
   const int64_t* pov;     // exclusive prefix of overlapped time (comm runs)
   const int64_t* fcrs;    // compute-active time before each comm run start
-  const uint32_t* rbeg;   // [kSegs] first run of a segment
-  const uint32_t* rend;   // [kSegs] one past its last run
+  BIndex X;               // bucket index of the run starts per segment
 };
+
+// Active time of a segment strictly before t, given the first run of the
+// segment whose start is > t (so j = up - 1 is the run holding or preceding
+// t).
+__device__ inline int64_t F_at(const Runs& R, const BSeg& P, int64_t up,
+                               int64_t t) {
+  const int64_t j = up - 1;
+  if (j < (int64_t)P.sb) return 0;
+  const int64_t e = R.re[j] < t ? R.re[j] : t;
+  return R.pl[j] + (e - R.rs[j]);
+}
+
+// K searches in lockstep, so that their loads overlap: on return lo[k] is
+// the first position in [lo[k], hi[k]) with key > t[k].
+template <int K>
+__device__ inline void bsearch_k(const int64_t* key, int64_t (&lo)[K],
+                                 int64_t (&hi)[K], const int64_t (&t)[K]) {
+  for (;;) {
+    bool act = false;
+    int64_t mid[K], v[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      mid[k] = lo[k] + ((hi[k] - lo[k]) >> 1);
+      if (lo[k] < hi[k]) {
+        act = true;
+        v[k] = key[mid[k]];
+      }
+    }
+    if (!act) break;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (lo[k] < hi[k]) {
+        if (v[k] <= t[k]) lo[k] = mid[k] + 1;
+        else hi[k] = mid[k];
+      }
+    }
+  }
+}
 
 // active time of segment seg strictly before t
 __device__ inline int64_t F_active(const Runs& R, uint32_t seg, int64_t t) {
-  int64_t b = R.rbeg[seg], e = R.rend[seg];
-  int64_t lo = b, hi = e;
-  while (lo < hi) {
-    int64_t mid = lo + ((hi - lo) >> 1);
-    if (R.rs[mid] <= t) lo = mid + 1;
-    else hi = mid;
-  }
-  int64_t j = lo - 1;
-  if (j < b) return 0;
-  int64_t end = R.re[j] < t ? R.re[j] : t;
-  return R.pl[j] - R.pl[b] + (end - R.rs[j]);
+  const BSeg P = R.X.seg[seg];
+  int64_t lo[1], hi[1];
+  const int64_t tt[1] = {t};
+  bi_range(R.X, P, t, &lo[0], &hi[0]);
+  bsearch_k<1>(R.rs, lo, hi, tt);
+  return F_at(R, P, lo[0], t);
 }
 
-// time before t where both kinds are active on gpu g
-__device__ inline int64_t F_both(const Runs& R, uint32_t g, int64_t t) {
-  const uint32_t seg = g * 2u + 1u;
-  int64_t b = R.rbeg[seg], e = R.rend[seg];
-  int64_t lo = b, hi = e;
-  while (lo < hi) {
-    int64_t mid = lo + ((hi - lo) >> 1);
-    if (R.rs[mid] <= t) lo = mid + 1;
-    else hi = mid;
+// CO, MO, OV, ID of [a, b) on gpu g (Section V-C): compute-active time c,
+// comm-active time m and the time where both are, o; both-active time
+// before t is the overlap of the comm runs before t plus, inside the comm
+// run holding t, the compute-active time up to t.
+__device__ inline void window(const Runs& R, uint32_t g, int64_t a, int64_t b,
+                              int64_t* out) {
+  if (b <= a) {
+    out[0] = out[1] = out[2] = out[3] = 0;
+    return;
   }
-  int64_t j = lo - 1;
-  if (j < b) return 0;
-  int64_t end = R.re[j] < t ? R.re[j] : t;
-  return R.pov[j] - R.pov[b] + F_active(R, g * 2u, end) - R.fcrs[j];
-}
-
-struct KItem {
-  uint32_t seg;
-  int64_t s, e;
-};
-
-__device__ inline KItem korder_item(const uint32_t* korder, const uint8_t* gpu,
-                                    const uint8_t* cls, const int64_t* start,
-                                    const int64_t* end, int64_t p) {
-  uint32_t r = korder[p];
-  KItem it;
-  it.seg = (uint32_t)gpu[r] * 2u + (uint32_t)kind_of(cls[r]);
-  it.s = start[r];
-  int64_t e = end[r];
-  it.e = e > it.s ? e : it.s;
-  return it;
+  const BSeg Pc = R.X.seg[g * 2u], Pm = R.X.seg[g * 2u + 1u];
+  // compute and comm searches at both ends
+  int64_t lo[4], hi[4];
+  const int64_t t[4] = {a, b, a, b};
+  bi_range(R.X, Pc, a, &lo[0], &hi[0]);
+  bi_range(R.X, Pc, b, &lo[1], &hi[1]);
+  bi_range(R.X, Pm, a, &lo[2], &hi[2]);
+  bi_range(R.X, Pm, b, &lo[3], &hi[3]);
+  bsearch_k<4>(R.rs, lo, hi, t);
+  const int64_t ca = F_at(R, Pc, lo[0], a), cb = F_at(R, Pc, lo[1], b);
+  const int64_t ma = F_at(R, Pm, lo[2], a), mb = F_at(R, Pm, lo[3], b);
+  // both-active time before a and before b
+  int64_t qlo[2], qhi[2], qt[2], base[2];
+  bool some[2];
+  for (int k = 0; k < 2; ++k) {
+    const int64_t jm = lo[2 + k] - 1;
+    const int64_t tk = k ? b : a;
+    some[k] = jm >= (int64_t)Pm.sb;    // a comm run starts at or before t
+    base[k] = 0;
+    qt[k] = tk;
+    qlo[k] = qhi[k] = Pc.sb;
+    if (!some[k]) continue;
+    const int64_t end = R.re[jm] < tk ? R.re[jm] : tk;
+    base[k] = R.pov[jm] - R.pov[Pm.sb] - R.fcrs[jm];
+    qt[k] = end;
+    bi_range(R.X, Pc, end, &qlo[k], &qhi[k]);
+  }
+  bsearch_k<2>(R.rs, qlo, qhi, qt);
+  int64_t ob[2];
+  for (int k = 0; k < 2; ++k)
+    ob[k] = some[k] ? base[k] + F_at(R, Pc, qlo[k], qt[k]) : 0;
+  const int64_t c = cb - ca, m = mb - ma, o = ob[1] - ob[0];
+  out[0] = c - o;
+  out[1] = m - o;
+  out[2] = o;
+  out[3] = (b - a) - c - m + o;
 }
 
 // ---------------- union runs -----------------------------------------------
+// Tiles of kOvTile korder positions, one block each; the block's four waves
+// take kWaveTile consecutive positions apiece.  Loads are striped, and the
+// ordered scans run on the blocked arrangement after an LDS transpose.
+
+// Running sum restricted to the last segment; seg == kNone is the empty
+// value (a two-sided identity).
+struct SegSum {
+  uint32_t seg;
+  uint32_t pad;
+  int64_t sum;
+};
+struct OpSegSum {
+  __device__ SegSum operator()(SegSum a, SegSum b) const {
+    if (b.seg == kNone) return a;
+    if (a.seg == kNone || a.seg != b.seg) return b;
+    return SegSum{b.seg, 0u, a.sum + b.sum};
+  }
+};
+__device__ inline SegSum segsum_ident() { return SegSum{kNone, 0u, 0}; }
+__device__ inline SegMax segmax_ident() { return SegMax{0u, kI64Min}; }
+
+__device__ inline void korder_gather(const uint32_t* korder, const uint8_t* gpu,
+                                     const uint8_t* cls, const int64_t* start,
+                                     const int64_t* end, int64_t p,
+                                     uint32_t& seg, int64_t& s, int64_t& e) {
+  const uint32_t r = korder[p];
+  seg = (uint32_t)gpu[r] * 2u + (uint32_t)kind_of(cls[r]);
+  s = start[r];
+  const int64_t x = end[r];
+  e = x > s ? x : s;
+}
+
+// Tile aggregate of (seg, end) under the lexicographic max: the last segment
+// of the tile and the largest end among its items.  Order does not matter.
 __global__ __launch_bounds__(kBlock) void k_runs_tile_max(
     int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
     const int64_t* start, const int64_t* end, SegMax* tile_agg) {
   const int64_t base = (int64_t)blockIdx.x * kOvTile;
-  SegMax acc{0u, kI64Min};
   OpSegMax op;
+  SegMax acc = segmax_ident();
+#pragma unroll
   for (int j = 0; j < kOvIpt; ++j) {
-    int64_t p = base + (int64_t)threadIdx.x * kOvIpt + j;
+    const int64_t p = base + (int64_t)j * kBlock + threadIdx.x;
     if (p < n) {
-      KItem it = korder_item(korder, gpu, cls, start, end, p);
-      acc = op(acc, SegMax{it.seg, it.e});
+      uint32_t seg;
+      int64_t s, e;
+      korder_gather(korder, gpu, cls, start, end, p, seg, s, e);
+      acc = op(acc, SegMax{seg, e});
     }
   }
-  SegMax tot;
-  block_exclusive(acc, op, SegMax{0u, kI64Min}, &tot);
-  if (threadIdx.x == 0) tile_agg[blockIdx.x] = tot;
-}
-
-// exclusive scan of the tile maxima in one block; also the grand total
-__global__ __launch_bounds__(kBlock) void k_runs_spine(SegMax* tile_agg,
-                                                       int64_t ntiles,
-                                                       SegMax* grand) {
-  OpSegMax op;
-  SegMax carry{0u, kI64Min};
-  for (int64_t base = 0; base < ntiles; base += kBlock) {
-    int64_t i = base + threadIdx.x;
-    SegMax v = i < ntiles ? tile_agg[i] : SegMax{0u, kI64Min};
-    SegMax tot;
-    SegMax ex = block_exclusive(v, op, SegMax{0u, kI64Min}, &tot);
-    if (i < ntiles) tile_agg[i] = op(carry, ex);
-    carry = op(carry, tot);
+  acc = wave_incl(acc, op, segmax_ident());
+  __shared__ SegMax s_w[kWavesPerBlock];
+  if (lane_id() == kWave - 1) s_w[threadIdx.x / kWave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    SegMax t = s_w[0];
+    for (int i = 1; i < kWavesPerBlock; ++i) t = op(t, s_w[i]);
+    tile_agg[blockIdx.x] = t;
   }
-  if (threadIdx.x == 0) *grand = carry;
 }
 
-// Per-item exclusive running maximum; returns head flags for the tile's items.
-__device__ inline void runs_tile_scan(int64_t n, const uint32_t* korder,
-                                      const uint8_t* gpu, const uint8_t* cls,
-                                      const int64_t* start, const int64_t* end,
-                                      const SegMax* tile_pre, KItem (&it)[kOvIpt],
-                                      SegMax (&ex)[kOvIpt],
-                                      bool (&head)[kOvIpt], bool (&valid)[kOvIpt]) {
-  const int64_t base = (int64_t)blockIdx.x * kOvTile;
+// In-place exclusive scan of per-tile values in one block; also the total.
+template <typename T, typename Op>
+__global__ __launch_bounds__(1024) void k_tile_spine(T* tile, int64_t ntiles,
+                                                     T ident, T* total) {
+  constexpr int kIpt = 8;
+  constexpr int kT = 1024;
+  __shared__ T s_w[kT / kWave];
+  Op op;
+  T carry = ident;
+  const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
+  for (int64_t base = 0; base < ntiles; base += (int64_t)kT * kIpt) {
+    T v[kIpt];
+    T acc = ident;
+#pragma unroll
+    for (int j = 0; j < kIpt; ++j) {
+      const int64_t i = base + (int64_t)threadIdx.x * kIpt + j;
+      v[j] = i < ntiles ? tile[i] : ident;
+      acc = op(acc, v[j]);
+    }
+    const T incl = wave_incl(acc, op, ident);
+    if (lane == kWave - 1) s_w[w] = incl;
+    __syncthreads();
+    T pre = carry, tot = carry;
+    for (int i = 0; i < kT / kWave; ++i) {
+      if (i < w) pre = op(pre, s_w[i]);
+      tot = op(tot, s_w[i]);
+    }
+    pre = op(pre, wave_shr1_any(ident, incl));
+#pragma unroll
+    for (int j = 0; j < kIpt; ++j) {
+      const int64_t i = base + (int64_t)threadIdx.x * kIpt + j;
+      if (i < ntiles) tile[i] = pre;
+      pre = op(pre, v[j]);
+    }
+    carry = tot;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0 && total) *total = carry;
+}
+
+// Per-item view of a tile in the blocked arrangement: segment, start, end,
+// exclusive running (seg, end) maximum, run-head flag and the length the
+// item adds to the union of its segment.
+struct RunItems {
+  uint32_t seg[kTileIpt];
+  int64_t s[kTileIpt];
+  int64_t mx[kTileIpt];     // exclusive running max of the same segment
+  int64_t inc[kTileIpt];
+  uint32_t m_valid, m_head, m_newseg;
+  uint32_t pseg0;           // segment of the item before the lane's first
+};
+
+__device__ inline void run_items(int64_t n, const uint32_t* korder,
+                                 const uint8_t* gpu, const uint8_t* cls,
+                                 const int64_t* start, const int64_t* end,
+                                 const SegMax* tile_pre, int64_t* slice,
+                                 RunItems& it) {
+  const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
+  const int64_t wbase = (int64_t)blockIdx.x * kOvTile + (int64_t)wv * kWaveTile;
+  uint32_t seg[kTileIpt];
+  int64_t s[kTileIpt], e[kTileIpt];
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    const int64_t p = wbase + (int64_t)j * kWave + lane;
+    if (p < n) {
+      korder_gather(korder, gpu, cls, start, end, p, seg[j], s[j], e[j]);
+    } else {
+      seg[j] = kNone;
+      s[j] = e[j] = 0;
+    }
+  }
+  wave_to_blocked(slice, s, lane);
+  wave_to_blocked(slice, e, lane);
+  wave_to_blocked((uint32_t*)slice, seg, lane);
   OpSegMax op;
-  SegMax acc{0u, kI64Min};
-  SegMax loc[kOvIpt];
-  for (int j = 0; j < kOvIpt; ++j) {
-    int64_t p = base + (int64_t)threadIdx.x * kOvIpt + j;
-    valid[j] = p < n;
-    if (valid[j]) it[j] = korder_item(korder, gpu, cls, start, end, p);
-    else it[j] = KItem{0u, 0, 0};
+  SegMax acc = segmax_ident();
+  SegMax loc[kTileIpt];
+  uint32_t m_valid = 0;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
     loc[j] = acc;
-    if (valid[j]) acc = op(acc, SegMax{it[j].seg, it[j].e});
+    if (seg[j] != kNone) {
+      m_valid |= 1u << j;
+      acc = op(acc, SegMax{seg[j], e[j]});
+    }
   }
-  SegMax tot;
-  SegMax pre = block_exclusive(acc, op, SegMax{0u, kI64Min}, &tot);
-  pre = op(tile_pre[blockIdx.x], pre);
-  for (int j = 0; j < kOvIpt; ++j) {
-    ex[j] = op(pre, loc[j]);
-    const int64_t p = base + (int64_t)threadIdx.x * kOvIpt + j;
-    head[j] = valid[j] &&
-              (p == 0 || ex[j].seg != it[j].seg || it[j].s > ex[j].val);
+  // lane tails scanned over the wave, then the waves of the block in order
+  const SegMax incl = wave_incl(acc, op, segmax_ident());
+  __shared__ SegMax s_w[kWavesPerBlock];
+  if (lane == kWave - 1) s_w[wv] = incl;
+  __syncthreads();
+  SegMax pre = tile_pre[blockIdx.x];
+  for (int i = 0; i < kWavesPerBlock; ++i)
+    if (i < wv) pre = op(pre, s_w[i]);
+  pre = op(pre, wave_shr1_any(segmax_ident(), incl));
+  const bool first_lane_of_all =
+      blockIdx.x == 0 && wv == 0 && lane == 0;
+  it.pseg0 = first_lane_of_all ? kNone : pre.seg;
+  uint32_t m_head = 0, m_newseg = 0;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    const SegMax ex = op(pre, loc[j]);
+    const bool first = first_lane_of_all && j == 0;
+    const bool newseg = first || ex.seg != seg[j];
+    const bool head = newseg || s[j] > ex.val;
+    it.seg[j] = seg[j];
+    it.s[j] = s[j];
+    it.mx[j] = ex.val;
+    if ((m_valid >> j) & 1u) {
+      if (head) m_head |= 1u << j;
+      if (newseg) m_newseg |= 1u << j;
+      it.inc[j] = head ? e[j] - s[j] : (e[j] > ex.val ? e[j] - ex.val : 0);
+    } else {
+      it.inc[j] = 0;
+    }
   }
+  it.m_valid = m_valid;
+  it.m_head = m_head;
+  it.m_newseg = m_newseg;
 }
 
+// Number of runs (heads) and the segmented sum of union increments per tile.
 __global__ __launch_bounds__(kBlock) void k_runs_count(
     int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
     const int64_t* start, const int64_t* end, const SegMax* tile_pre,
-    uint32_t* tile_heads) {
-  KItem it[kOvIpt];
-  SegMax ex[kOvIpt];
-  bool head[kOvIpt], valid[kOvIpt];
-  runs_tile_scan(n, korder, gpu, cls, start, end, tile_pre, it, ex, head,
-                 valid);
-  uint32_t c = 0;
-  for (int j = 0; j < kOvIpt; ++j) c += head[j] ? 1u : 0u;
-  uint32_t tot;
-  block_exclusive(c, OpAdd(), 0u, &tot);
-  if (threadIdx.x == 0) tile_heads[blockIdx.x] = tot;
-}
-
-__global__ __launch_bounds__(kBlock) void k_runs_write(
-    int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
-    const int64_t* start, const int64_t* end, const SegMax* tile_pre,
-    const uint32_t* tile_run0, const uint32_t* nruns, const SegMax* grand,
-    int64_t* rs, int64_t* re, uint32_t* rseg, uint32_t* rbeg, uint32_t* rend) {
-  KItem it[kOvIpt];
-  SegMax ex[kOvIpt];
-  bool head[kOvIpt], valid[kOvIpt];
-  runs_tile_scan(n, korder, gpu, cls, start, end, tile_pre, it, ex, head,
-                 valid);
-  uint32_t c = 0;
-  for (int j = 0; j < kOvIpt; ++j) c += head[j] ? 1u : 0u;
-  uint32_t tot;
-  uint32_t r = block_exclusive(c, OpAdd(), 0u, &tot) + tile_run0[blockIdx.x];
-  const int64_t base = (int64_t)blockIdx.x * kOvTile;
-  for (int j = 0; j < kOvIpt; ++j) {
-    const int64_t p = base + (int64_t)threadIdx.x * kOvIpt + j;
-    if (head[j]) {
-      rs[r] = it[j].s;
-      rseg[r] = it[j].seg;
-      const bool new_seg = (p == 0) || ex[j].seg != it[j].seg;
-      if (p > 0) re[r - 1] = ex[j].val;   // the previous run ends here
-      if (new_seg) {
-        rbeg[it[j].seg] = r;
-        if (p > 0) rend[ex[j].seg] = r;
-      }
-      ++r;
+    uint32_t* tile_heads, SegSum* tile_inc) {
+  __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
+  RunItems it;
+  run_items(n, korder, gpu, cls, start, end, tile_pre,
+            s_slice[threadIdx.x / kWave], it);
+  OpSegSum op;
+  SegSum acc = segsum_ident();
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j)
+    if ((it.m_valid >> j) & 1u) acc = op(acc, SegSum{it.seg[j], 0u, it.inc[j]});
+  acc = wave_incl(acc, op, segsum_ident());
+  uint32_t c = (uint32_t)__popc(it.m_head);
+  for (int d = kWave / 2; d > 0; d >>= 1) c += __shfl_xor(c, d, kWave);
+  __shared__ SegSum s_w[kWavesPerBlock];
+  __shared__ uint32_t s_c[kWavesPerBlock];
+  const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
+  if (lane == kWave - 1) {
+    s_w[wv] = acc;
+    s_c[wv] = c;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    SegSum t = s_w[0];
+    uint32_t tc = s_c[0];
+    for (int i = 1; i < kWavesPerBlock; ++i) {
+      t = op(t, s_w[i]);
+      tc += s_c[i];
     }
-    if (valid[j] && p == n - 1) {
-      const uint32_t R = *nruns;
-      re[R - 1] = grand->val;
-      rend[it[j].seg] = R;
-    }
+    tile_heads[blockIdx.x] = tc;
+    tile_inc[blockIdx.x] = t;
   }
 }
 
-__global__ __launch_bounds__(kBlock) void k_runs_len(const uint32_t* nruns,
-                                                     const int64_t* rs,
-                                                     const int64_t* re,
-                                                     int64_t* len, int64_t cap) {
-  int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (r >= cap) return;
-  len[r] = r < (int64_t)*nruns ? re[r] - rs[r] : 0;
+// Writes the runs: start, segment and union length before the run (the
+// prefix of the segment's run lengths); every head closes the previous run
+// at the running maximum, and segment starts record the run ranges.
+__global__ __launch_bounds__(kBlock) void k_runs_write(
+    int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
+    const int64_t* start, const int64_t* end, const SegMax* tile_pre,
+    const uint32_t* tile_run0, const SegSum* tile_inc0, const uint32_t* nruns,
+    const SegMax* grand, int64_t* rs, int64_t* re, int64_t* pl,
+    uint32_t* rseg, uint32_t* rbeg, uint32_t* rend) {
+  __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
+  RunItems it;
+  run_items(n, korder, gpu, cls, start, end, tile_pre,
+            s_slice[threadIdx.x / kWave], it);
+  const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
+  OpSegSum op;
+  SegSum acc = segsum_ident();
+  SegSum loc[kTileIpt];
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    loc[j] = acc;
+    if ((it.m_valid >> j) & 1u) acc = op(acc, SegSum{it.seg[j], 0u, it.inc[j]});
+  }
+  const SegSum incl = wave_incl(acc, op, segsum_ident());
+  const uint32_t c = (uint32_t)__popc(it.m_head);
+  const uint32_t cex = wave_prefix_small<4>(c);
+  __shared__ SegSum s_w[kWavesPerBlock];
+  __shared__ uint32_t s_c[kWavesPerBlock];
+  if (lane == kWave - 1) {
+    s_w[wv] = incl;
+    s_c[wv] = cex + c;
+  }
+  __syncthreads();
+  SegSum pre = tile_inc0[blockIdx.x];
+  uint32_t r = tile_run0[blockIdx.x] + cex;
+  for (int i = 0; i < kWavesPerBlock; ++i)
+    if (i < wv) {
+      pre = op(pre, s_w[i]);
+      r += s_c[i];
+    }
+  pre = op(pre, wave_shr1_any(segsum_ident(), incl));
+  const int64_t wbase = (int64_t)blockIdx.x * kOvTile + (int64_t)wv * kWaveTile;
+  // the wave's runs are r0 .. r0 + H - 1; head k of the wave is run r0 + k
+  const uint32_t r0 = r - cex;
+  const uint32_t H = (uint32_t)__builtin_amdgcn_readlane((int)(cex + c), 63);
+  uint32_t k[kTileIpt];
+  int64_t vpl[kTileIpt];
+  {
+    uint32_t kk = cex;
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      k[j] = kk;
+      kk += (it.m_head >> j) & 1u;
+      const SegSum u = op(pre, loc[j]);
+      vpl[j] = (u.seg == it.seg[j]) ? u.sum : 0;
+    }
+  }
+  // segment ranges and the very last run (rare, scattered)
+  uint32_t pseg = it.pseg0;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    const int64_t p = wbase + (int64_t)lane * kTileIpt + j;
+    if (((it.m_newseg >> j) & 1u)) {
+      rbeg[it.seg[j]] = r0 + k[j];
+      if (p > 0) rend[pseg] = r0 + k[j];
+    }
+    if (((it.m_valid >> j) & 1u) && p == n - 1) {
+      const uint32_t R = *nruns;
+      re[R - 1] = grand->val;
+      rend[it.seg[j]] = R;
+    }
+    if ((it.m_valid >> j) & 1u) pseg = it.seg[j];
+  }
+  // run columns, compacted through the wave's LDS slice so that the stores
+  // of consecutive lanes go to consecutive runs
+  int64_t* sl = s_slice[wv];
+  auto emit = [&](const int64_t (&v)[kTileIpt], int64_t* dst) {
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j)
+      if ((it.m_head >> j) & 1u) sl[k[j]] = v[j];
+    wave_sync();
+    for (uint32_t q = lane; q < H; q += kWave) dst[q] = sl[q];
+    wave_sync();
+  };
+  emit(it.s, rs + r0);
+  emit(vpl, pl + r0);
+  {
+    // every head closes the previous run at the running maximum; the
+    // first run of all has no predecessor
+    int64_t* sl2 = sl;
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j)
+      if ((it.m_head >> j) & 1u) sl2[k[j]] = it.mx[j];
+    wave_sync();
+    for (uint32_t q = lane; q < H; q += kWave)
+      if (r0 + q > 0) re[r0 + q - 1] = sl2[q];
+    wave_sync();
+  }
+  {
+    uint32_t* su = (uint32_t*)sl;
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j)
+      if ((it.m_head >> j) & 1u) su[k[j]] = it.seg[j];
+    wave_sync();
+    for (uint32_t q = lane; q < H; q += kWave) rseg[r0 + q] = su[q];
+    wave_sync();
+  }
 }
 
 // overlapped time inside each comm run: compute-active time within it
 __global__ __launch_bounds__(kBlock) void k_runs_comm_overlap(
     const uint32_t* nruns, Runs R, const uint32_t* rseg, int64_t* ovc,
     int64_t* fcrs, int64_t cap) {
-  int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  const int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (r >= cap) return;
   int64_t v = 0, f = 0;
   if (r < (int64_t)*nruns) {
-    uint32_t seg = rseg[r];
+    const uint32_t seg = rseg[r];
     if (seg & 1u) {
-      uint32_t cseg = seg - 1u;
-      f = F_active(R, cseg, R.rs[r]);
-      v = F_active(R, cseg, R.re[r]) - f;
+      const BSeg P = R.X.seg[seg - 1u];
+      const int64_t t[2] = {R.rs[r], R.re[r]};
+      int64_t lo[2], hi[2];
+      bi_range(R.X, P, t[0], &lo[0], &hi[0]);
+      bi_range(R.X, P, t[1], &lo[1], &hi[1]);
+      bsearch_k<2>(R.rs, lo, hi, t);
+      f = F_at(R, P, lo[0], t[0]);
+      v = F_at(R, P, lo[1], t[1]) - f;
     }
   }
   ovc[r] = v;
@@ -239,24 +495,15 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
     // a compute kernel's overlapped time is the comm-active time inside it
     // and vice versa
     const uint32_t other = g * 2u + (kind_of(cls[k]) ? 0u : 1u);
-    o = F_active(R, other, e) - F_active(R, other, s);
+    const BSeg P = R.X.seg[other];
+    const int64_t t[2] = {s, e};
+    int64_t lo[2], hi[2];
+    bi_range(R.X, P, s, &lo[0], &hi[0]);
+    bi_range(R.X, P, e, &lo[1], &hi[1]);
+    bsearch_k<2>(R.rs, lo, hi, t);
+    o = F_at(R, P, lo[1], e) - F_at(R, P, lo[0], s);
   }
   ovl[k] = o;
-}
-
-__device__ inline void window(const Runs& R, uint32_t g, int64_t a, int64_t b,
-                              int64_t* out) {
-  if (b <= a) {
-    out[0] = out[1] = out[2] = out[3] = 0;
-    return;
-  }
-  const int64_t c = F_active(R, g * 2u, b) - F_active(R, g * 2u, a);
-  const int64_t m = F_active(R, g * 2u + 1u, b) - F_active(R, g * 2u + 1u, a);
-  const int64_t o = F_both(R, g, b) - F_both(R, g, a);
-  out[0] = c - o;
-  out[1] = m - o;
-  out[2] = o;
-  out[3] = (b - a) - c - m + o;
 }
 
 __global__ __launch_bounds__(kBlock) void k_overlap_markers(
@@ -277,10 +524,10 @@ __global__ void k_overlap_gpus(int G, Runs R, int64_t* gwin) {
   if (g >= G) return;
   int64_t a = kI64Max, b = kI64Min;
   for (uint32_t seg = g * 2u; seg < g * 2u + 2u; ++seg) {
-    const uint32_t rb = R.rbeg[seg], re = R.rend[seg];
-    if (re > rb) {
-      a = R.rs[rb] < a ? R.rs[rb] : a;
-      b = R.re[re - 1] > b ? R.re[re - 1] : b;
+    const BSeg P = R.X.seg[seg];
+    if (P.se > P.sb) {
+      a = R.rs[P.sb] < a ? R.rs[P.sb] : a;
+      b = R.re[P.se - 1] > b ? R.re[P.se - 1] : b;
     }
   }
   if (a == kI64Max) a = b = 0;
@@ -325,6 +572,8 @@ struct OverlapLayout {
   SegMax* tile_agg;
   SegMax* grand;
   uint32_t* tile_heads;
+  SegSum* tile_inc;
+  SegSum* inc_total;
   uint32_t* tile_run0;
   uint32_t* nruns;
   uint32_t* scan_u32;
@@ -333,13 +582,16 @@ struct OverlapLayout {
   uint32_t* rseg;
   uint32_t* rbeg;     // kSegs, then rend kSegs
   uint32_t* rend;
-  int64_t* len;
   int64_t* pl;
   int64_t* ovc;
   int64_t* pov;
   int64_t* fcrs;
   int64_t* scan_i64;
   int64_t* tot_i64;
+  BSeg* bsegs;
+  uint32_t* btable;
+  int64_t btable_cap;
+  uint32_t* btmp;
 };
 
 static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
@@ -348,6 +600,8 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   L.tile_agg = sc.take<SegMax>(L.ntiles);
   L.grand = sc.take<SegMax>(1);
   L.tile_heads = sc.take<uint32_t>(L.ntiles);
+  L.tile_inc = sc.take<SegSum>(L.ntiles);
+  L.inc_total = sc.take<SegSum>(1);
   L.tile_run0 = sc.take<uint32_t>(L.ntiles);
   L.nruns = sc.take<uint32_t>(1);
   L.scan_u32 = sc.take<uint32_t>(scan_scratch_elems(L.ntiles));
@@ -356,13 +610,16 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   L.rseg = sc.take<uint32_t>(n);
   L.rbeg = sc.take<uint32_t>(2 * kSegs);
   L.rend = L.rbeg ? L.rbeg + kSegs : nullptr;
-  L.len = sc.take<int64_t>(n);
   L.pl = sc.take<int64_t>(n);
   L.ovc = sc.take<int64_t>(n);
   L.pov = sc.take<int64_t>(n);
   L.fcrs = sc.take<int64_t>(n);
   L.scan_i64 = sc.take<int64_t>(scan_scratch_elems(n));
   L.tot_i64 = sc.take<int64_t>(2);
+  L.bsegs = sc.take<BSeg>(kSegs);
+  L.btable_cap = bindex_table_cap(n, kSegs);
+  L.btable = sc.take<uint32_t>(L.btable_cap);
+  L.btmp = sc.take<uint32_t>(kSegs + 1);
   return L;
 }
 
@@ -406,25 +663,29 @@ extern "C" int chopper_overlap(const chopper_records* rec,
     CHOPPER_HIP(launch("ov_runs_tile_max", k_runs_tile_max, dim3(T),
                        dim3(kBlock), s, n, korder, rec->gpu, rec->cls,
                        start_al, end_al, L.tile_agg));
-    CHOPPER_HIP(launch("ov_runs_spine", k_runs_spine, dim3(1), dim3(kBlock), s,
-                       L.tile_agg, L.ntiles, L.grand));
+    CHOPPER_HIP(launch("ov_runs_spine", k_tile_spine<SegMax, OpSegMax>,
+                       dim3(1), dim3(1024), s, L.tile_agg, L.ntiles,
+                       SegMax{0u, kI64Min}, L.grand));
     CHOPPER_HIP(launch("ov_runs_count", k_runs_count, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
-                       (const SegMax*)L.tile_agg, L.tile_heads));
+                       (const SegMax*)L.tile_agg, L.tile_heads, L.tile_inc));
     CHOPPER_HIP(exclusive_scan<uint32_t>(L.tile_heads, L.tile_run0, L.ntiles,
                                          L.scan_u32, L.nruns, s));
+    CHOPPER_HIP(launch("ov_runs_inc_spine", k_tile_spine<SegSum, OpSegSum>,
+                       dim3(1), dim3(1024), s, L.tile_inc, L.ntiles,
+                       SegSum{kNone, 0u, 0}, L.inc_total));
     CHOPPER_HIP(launch("ov_runs_write", k_runs_write, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
                        (const SegMax*)L.tile_agg, (const uint32_t*)L.tile_run0,
-                       (const uint32_t*)L.nruns, (const SegMax*)L.grand, L.rs,
-                       L.re, L.rseg, L.rbeg, L.rend));
-    CHOPPER_HIP(launch("ov_runs_len", k_runs_len, grid_for(n, kBlock),
-                       dim3(kBlock), s, (const uint32_t*)L.nruns,
-                       (const int64_t*)L.rs, (const int64_t*)L.re, L.len, n));
-    CHOPPER_HIP(exclusive_scan<int64_t>(L.len, L.pl, n, L.scan_i64, L.tot_i64,
-                                        s));
+                       (const SegSum*)L.tile_inc, (const uint32_t*)L.nruns,
+                       (const SegMax*)L.grand, L.rs, L.re, L.pl, L.rseg,
+                       L.rbeg, L.rend));
   }
-  Runs R{L.rs, L.re, L.pl, L.pov, L.fcrs, L.rbeg, L.rend};
+  // bucket index of the run starts of every (gpu, kind)
+  CHOPPER_HIP(bindex_build(L.rs, L.rseg, n, L.nruns, L.rbeg, L.rend, 1, kSegs,
+                           L.bsegs, L.btable, L.btable_cap, L.btmp, s));
+  Runs R{L.rs, L.re, L.pl, L.pov, L.fcrs,
+         BIndex{L.rs, L.bsegs, L.btable}};
   if (n > 0) {
     CHOPPER_HIP(launch("ov_runs_comm_overlap", k_runs_comm_overlap,
                        grid_for(n, kBlock), dim3(kBlock), s,

@@ -19,7 +19,7 @@ static const char* const kKernelNames[] = {
     "sort_digit_scatter", "sort_make_keys", "sort_time_minmax",
     "attr_marker_gather", "attr_marker_links", "attr_records",
     "ov_runs_tile_max", "ov_runs_spine", "ov_runs_count", "ov_runs_write",
-    "ov_runs_len", "ov_runs_comm_overlap", "ov_records", "ov_markers",
+    "ov_runs_inc_spine", "ov_runs_comm_overlap", "ov_records", "ov_markers",
     "ov_gpus", "ov_gap",
     "agg_fill_owner", "agg_elect", "agg_count", "agg_offsets", "agg_assign",
     "agg_reduce_records", "agg_reduce_rows", "agg_apply_overflow",
@@ -28,7 +28,8 @@ static const char* const kKernelNames[] = {
     "sort_class_count", "status_set", "ov_fill",
     "agg_workload_first", "sort_major_sorted", "agg_heads_records",
     "agg_heads_rows", "agg_fast_reduce_records", "agg_fast_reduce_rows",
-    "agg_workload_from_gpu"};
+    "agg_workload_from_gpu", "bi_params", "bi_offsets", "bi_clear", "bi_fill",
+    "bi_fixup"};
 
 __global__ __launch_bounds__(kBlock) void k_ratios(
     const int64_t* level_offset, int depth, int64_t cap, const uint64_t* n,
