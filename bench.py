@@ -72,6 +72,9 @@ def main():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-iters", type=int, default=200)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run plain device copies of this many MiB (the "
+                         "reference kernel for scaling HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the traces of all ranks are "
@@ -80,6 +83,15 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_calibration > 0:
+        nb = args.copy_calibration << 20
+        a = torch.ones(nb, dtype=torch.uint8, device="cuda:0")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": nb, "copies": 3}), flush=True)
+        return
     import tracegen as tg
     import paper_2512_08242_amd as ch
 

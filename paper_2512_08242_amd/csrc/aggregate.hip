@@ -356,7 +356,19 @@ __device__ inline uint64_t* row_column(const RowsDev& R, int f) {
 // Item sources for the reduction: records in korder, or rows of a finer
 // level.  Fields: 0 n, 1 dur, 2 gap, 3 ovl, 4 tmin, 5 tmax, 6.. counters.
 struct FromRecords {
+  static constexpr bool kRecords = true;
   RecSrc S;
+  // columns of the fast reduction: start and end give n (no load), dur,
+  // tmin and tmax; the plain sums are gap, ovl and the counters
+  __device__ const int64_t* start_col() const { return S.start; }
+  __device__ const int64_t* end_col() const { return S.end; }
+  __device__ int nsum() const { return 2 + S.nc; }
+  __device__ const uint64_t* sum_col(int i) const {
+    if (i == 0) return (const uint64_t*)S.gap;
+    if (i == 1) return (const uint64_t*)S.ovl;
+    return S.ctr + (int64_t)(i - 2) * S.n;
+  }
+  __device__ int sum_dst(int i) const { return i < 2 ? 2 + i : 6 + (i - 2); }
   __device__ int64_t count() const { return S.n; }
   __device__ void load(int64_t i, uint32_t& r, bool& ok, uint32_t* p,
                        uint32_t& g, uint32_t& kind, uint32_t& fpos) const {
@@ -410,10 +422,21 @@ struct FromRecords {
 };
 
 struct FromRows {
+  static constexpr bool kRecords = false;
   RowsDev R;
   int64_t M;        // number of markers (key space)
   const int64_t* level_offset;
   int lo_slot;      // level_offset index of the finer level
+  // columns of the fast reduction: tmin and tmax, then the plain sums
+  // n, dur, gap, ovl and the counters
+  __device__ const int64_t* start_col() const { return R.tmin; }
+  __device__ const int64_t* end_col() const { return R.tmax; }
+  __device__ int nsum() const { return 4 + R.nc; }
+  __device__ const uint64_t* sum_col(int i) const {
+    if (i < 4) return (const uint64_t*)row_column(R, i);
+    return R.ctr + (int64_t)(i - 4) * R.cap;
+  }
+  __device__ int sum_dst(int i) const { return i < 4 ? i : 6 + (i - 4); }
   __device__ int64_t count() const {
     int64_t a = level_offset[lo_slot], b = level_offset[lo_slot + 1];
     if (b > R.cap) b = R.cap;
@@ -697,6 +720,7 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads(
       if (li >= D || li < lv0 || li > lv1 || !((act >> li) & 1u)) continue;
       const uint32_t key = slot_key(slot, M, gk[j]);
       const uint32_t pkey = pvalid ? slot_key(pslot, M, pgk) : kNone;
+      if (valid && key == kNone) notinc = true;   // unkeyed item: general path
       if (key != pkey && key != kNone) {
         cpk += (valid ? 1ull : 0ull) << (4 * li);
         // inside a segment the no-marker group may only come first, so it
@@ -753,60 +777,22 @@ __global__ void k_agg_offsets_fast(int L, int64_t ntiles,
     atomicOr(status, (uint32_t)CHOPPER_ST_ROWS_OVERFLOW);
 }
 
-// Per-tile state of the fast reduction, in the blocked arrangement (lane
-// holds items lane * 8 + j).
-struct PieceState {
-  uint32_t row[kAggIpt];   // row of the item's group (valid where m_item)
-  uint32_t m_head;         // item starts a piece
-  uint32_t m_last;         // item ends a piece that is a real group
-  uint32_t m_own;          // that piece starts its row
-  uint32_t before;         // items of the lane's first piece (no head yet)
-  WaveSegMasks masks;      // segment flags of the wave scan of lane tails
-};
-
-// One field over the tile: striped values go through the wave's LDS slice
-// into the blocked arrangement, a serial segmented pass per lane and one
-// segmented wave scan of the lane tails give every piece's total at its
-// last item, which the row's first piece stores and a continuation piece
-// (only the tile's first piece can be one) leaves in the tile's overflow
-// slot.
-template <typename C>
-__device__ inline void fast_field(const PieceState& st, uint64_t* sv,
-                                  const uint64_t (&p)[kAggIpt], int lane,
-                                  uint64_t* col, uint64_t* oslot, int64_t cap) {
-  C c;
-#pragma unroll
-  for (int j = 0; j < kAggIpt; ++j) sv[pad8(j * kWave + lane)] = p[j];
-  wave_sync();
-  uint64_t x[kAggIpt];
-#pragma unroll
-  for (int j = 0; j < kAggIpt; ++j) x[j] = sv[pad8(lane * kAggIpt + j)];
-  wave_sync();
-  uint64_t acc = x[0];
-#pragma unroll
-  for (int j = 1; j < kAggIpt; ++j) {
-    acc = ((st.m_head >> j) & 1u) ? x[j] : c(acc, x[j]);
-    x[j] = acc;
-  }
-  const uint64_t incl = wave_seg_incl<C>(st.masks, acc);
-  const uint64_t carry = wave_shr1(C::ident, incl);
-#pragma unroll
-  for (int j = 0; j < kAggIpt; ++j) {
-    if (!((st.m_last >> j) & 1u) || (int64_t)st.row[j] >= cap) continue;
-    const uint64_t v = (uint32_t)j < st.before ? c(carry, x[j]) : x[j];
-    if ((st.m_own >> j) & 1u) col[st.row[j]] = v;
-    else *oslot = v;
-  }
-}
-
-// Reduction of one level when groups are runs.  Rows are numbered from the
-// tile's head count (level-major exclusive scan of the heads pass) plus the
-// real heads of the lanes below; the piece that starts a row writes its
-// header.  Field loads are striped and coalesced, two fields in flight.
+// Reduction of one level when groups are runs.  Within a wave tile the
+// pieces (maximal runs of equal keys) are numbered in item order; rows are
+// numbered from the tile's head count (level-major exclusive scan of the
+// heads pass).  Every field goes striped -> blocked through the wave's LDS
+// slice; sums take one plain prefix sum over the tile and a piece's total is
+// the difference of the prefix at its last item and at the previous piece's
+// last item (exact modulo 2^64); tmin and tmax take a segmented scan.  The
+// value at each piece's last item is written to LDS at the piece's index, so
+// that the stores of consecutive lanes go to consecutive rows.  The tile's
+// first piece may continue a row of an earlier tile: it goes to the tile's
+// overflow slot.  Every valid item has a key here (the heads pass sends
+// traces with unkeyed items to the general path).
 template <int MaxD, typename Src>
 __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     Src src, int li, int D, int64_t M, const uint32_t* tilebase,
-    const int64_t* row0, RowsDev R, Overflow ovf, int nfields, int64_t nwt) {
+    const int64_t* row0, RowsDev R, Overflow ovf, int64_t nwt) {
   __shared__ uint64_t s_v[kWavesPerBlock][kSlice];
   const int lane = lane_id();
   const int wv = (int)(threadIdx.x / kWave);
@@ -847,8 +833,8 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
 #pragma unroll
   for (int j = 0; j < kAggIpt; ++j) key[j] = sk[pad8(lane * kAggIpt + j)];
   wave_sync();
-  PieceState st;
-  uint32_t m_item = 0, m_real = 0, m_head = 0;
+  // pieces in the blocked arrangement
+  uint32_t m_valid = 0, m_real = 0, m_head = 0;
   {
     uint32_t prev = wave_shr1_u32(tile_prev, key[kAggIpt - 1]);
 #pragma unroll
@@ -856,60 +842,52 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
       const int q = lane * kAggIpt + j;
       const bool valid = q < tile_n;
       const uint32_t k = key[j];
-      if (valid && k != kNone) m_item |= 1u << j;
-      if (valid && k != kNone && k != prev) m_real |= 1u << j;
+      if (valid) m_valid |= 1u << j;
+      if (valid && k != prev) m_real |= 1u << j;
       if (!valid || q == 0 || k != prev) m_head |= 1u << j;
       prev = k;
     }
   }
-  st.m_head = m_head;
-  // rows: tile base + real heads of the lanes below + those before j here
-  {
-    int64_t running = (row0 ? *row0 : 0) + (int64_t)tilebase[w] +
-                      wave_prefix_small<4>((uint32_t)__popc(m_real));
-#pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) {
-      running += (m_real >> j) & 1u;
-      st.row[j] = (uint32_t)(running - 1);
-    }
-  }
   // last item of a piece: the next item starts one (the tile's end does)
+  uint32_t m_last;
   {
     const uint64_t h0 = __ballot(m_head & 1u);
     const uint32_t next0 =
         lane == kWave - 1 ? 1u : (uint32_t)((h0 >> (lane + 1)) & 1u);
-    st.m_last = m_item & ((m_head >> 1) | (next0 << (kAggIpt - 1)));
+    m_last = m_valid & ((m_head >> 1) | (next0 << (kAggIpt - 1)));
   }
-  // does the piece start its row?  The lane's first piece continues the
-  // last piece of the nearest lane below that has a head.
-  {
-    const uint64_t ha = __ballot(m_head != 0);
-    const bool last_real =
-        m_head != 0 && ((m_real >> (31 - __clz(m_head))) & 1u);
-    const uint64_t lr = __ballot(last_real);
-    const uint64_t below = ha & ((1ull << lane) - 1ull);
-    uint32_t own = below ? (uint32_t)((lr >> (63 - __clzll(below))) & 1ull)
-                         : 0u;
-    uint32_t m_own = 0;
+  // piece index of every item; NP pieces in the tile; c0 = 1 when the
+  // first piece continues a row of an earlier tile; rows r0 .. r0 + NP - c0
+  const uint32_t m_hv = m_head & m_valid;
+  const uint32_t pfx = wave_prefix_small<4>((uint32_t)__popc(m_hv));
+  const uint32_t NP = (uint32_t)__builtin_amdgcn_readlane(
+      (int)(pfx + (uint32_t)__popc(m_hv)), kWave - 1);
+  const uint32_t c0 =
+      __ballot(lane == 0 && !(m_real & 1u)) != 0 ? 1u : 0u;
+  const int64_t r0 = (row0 ? *row0 : 0) + (int64_t)tilebase[w];
+  int slot[kAggIpt];
 #pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) {
-      if ((m_head >> j) & 1u) own = (m_real >> j) & 1u;
-      m_own |= own << j;
-    }
-    st.m_own = m_own;
+  for (int j = 0; j < kAggIpt; ++j) {
+    const uint32_t idx = pfx + (uint32_t)__popc(m_hv & ((2u << j) - 1u)) - 1u;
+    slot[j] = ((m_last >> j) & 1u) ? (int)idx : kWaveTile + lane;
   }
-  st.before = m_head ? (uint32_t)(__ffs(m_head) - 1) : (uint32_t)kAggIpt;
-  st.masks = wave_seg_masks(m_head != 0);
   // headers of the rows that start here, written from the striped items:
   // the row of every real head goes back through LDS
+  {
+    uint32_t run = pfx;   // pieces before the item, then its index
 #pragma unroll
-  for (int j = 0; j < kAggIpt; ++j)
-    sk[pad8(lane * kAggIpt + j)] = ((m_real >> j) & 1u) ? st.row[j] : kNone;
+    for (int j = 0; j < kAggIpt; ++j) {
+      run += (m_hv >> j) & 1u;
+      const int64_t row = r0 + (int64_t)run - 1 - c0;
+      sk[pad8(lane * kAggIpt + j)] =
+          ((m_real >> j) & 1u) && row < R.cap ? (uint32_t)row : kNone;
+    }
+  }
   wave_sync();
 #pragma unroll
   for (int j = 0; j < kAggIpt; ++j) {
     const uint32_t wr = sk[pad8(j * kWave + lane)];
-    if (wr == kNone || (int64_t)wr >= R.cap) continue;
+    if (wr == kNone) continue;
 #pragma unroll
     for (int l = 0; l < MaxD; ++l)
       if (l < D)
@@ -919,34 +897,104 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     R.first[wr] = src.first_of(rs[j]);
   }
   wave_sync();
-  // the tile's first piece continues a row of an earlier tile
   if (lane == 0)
-    ovf.row[w] = ((m_item & ~m_real) & 1u) && (int64_t)st.row[0] < R.cap
-                     ? st.row[0]
-                     : kNone;
-  uint64_t pa[kAggIpt], pb[kAggIpt];
-  auto load = [&](int f, uint64_t (&v)[kAggIpt]) {
-    if (f >= nfields) return;
-    const FieldRef fr = src.fref(f);
+    ovf.row[w] = c0 && r0 >= 1 && r0 - 1 < R.cap ? (uint32_t)(r0 - 1) : kNone;
+  const WaveSegMasks masks = wave_seg_masks(m_head != 0);
+  const uint32_t before =
+      m_head ? (uint32_t)(__ffs(m_head) - 1) : (uint32_t)kAggIpt;
+  // byte offsets of the striped items (sizes are below 2^29 here)
+  uint32_t off[kAggIpt];
 #pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) v[j] = fr.get(rs[j]);
-  };
-  auto step = [&](int f, uint64_t (&v)[kAggIpt]) {
+  for (int j = 0; j < kAggIpt; ++j) off[j] = rs[j] << 3;
+
+  // piece values at the slots -> rows (and the overflow slot)
+  auto store_pieces = [&](int f, bool diff) {
     uint64_t* col = row_column(R, f);
     uint64_t* oslot = ovf.val + (int64_t)f * ovf.cap + w;
-    uint64_t cur[kAggIpt];
-#pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) cur[j] = v[j];
-    load(f + 2, v);
-    if (f == 4) fast_field<CMin>(st, sv, cur, lane, col, oslot, R.cap);
-    else if (f == 5) fast_field<CMax>(st, sv, cur, lane, col, oslot, R.cap);
-    else fast_field<CSum>(st, sv, cur, lane, col, oslot, R.cap);
+    wave_sync();
+    for (uint32_t q = lane; q < NP; q += kWave) {
+      uint64_t v = sv[q];
+      if (diff && q > 0) v -= sv[q - 1];
+      if (q < c0) {
+        *oslot = v;
+      } else {
+        const int64_t row = r0 + (int64_t)(q - c0);
+        if (row < R.cap) col[row] = v;
+      }
+    }
+    wave_sync();
   };
-  load(0, pa);
-  load(1, pb);
-  for (int f = 0; f < nfields; f += 2) {
-    step(f, pa);
-    if (f + 1 < nfields) step(f + 1, pb);
+  auto do_sum = [&](const uint64_t (&v)[kAggIpt], int f) {
+    uint64_t x[kAggIpt];
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) x[j] = v[j];
+    wave_to_blocked(sv, x, lane);
+#pragma unroll
+    for (int j = 1; j < kAggIpt; ++j) x[j] += x[j - 1];
+    const uint64_t incl = wave_incl(x[kAggIpt - 1], OpAdd(), (uint64_t)0);
+    const uint64_t carry = wave_shr1(0ull, incl);
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) sv[slot[j]] = x[j] + carry;
+    store_pieces(f, true);
+  };
+  auto do_seg = [&](const uint64_t (&v)[kAggIpt], int f, auto cmb) {
+    using C = decltype(cmb);
+    uint64_t x[kAggIpt];
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) x[j] = v[j];
+    wave_to_blocked(sv, x, lane);
+    uint64_t acc = x[0];
+#pragma unroll
+    for (int j = 1; j < kAggIpt; ++j) {
+      acc = ((m_head >> j) & 1u) ? x[j] : cmb(acc, x[j]);
+      x[j] = acc;
+    }
+    const uint64_t incl = wave_seg_incl<C>(masks, acc);
+    const uint64_t carry = wave_shr1(C::ident, incl);
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j)
+      sv[slot[j]] = (uint32_t)j < before ? cmb(carry, x[j]) : x[j];
+    store_pieces(f, false);
+  };
+  auto load = [&](const uint64_t* col, uint64_t (&v)[kAggIpt]) {
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j)
+      v[j] = *(const uint64_t*)((const char*)col + off[j]);
+  };
+
+  const int ns = src.nsum();
+  uint64_t va[kAggIpt], vb[kAggIpt];
+  {
+    // the two plain-sum prefetches are staggered between the special
+    // fields to bound the live registers
+    uint64_t ts[kAggIpt], te[kAggIpt];
+    load((const uint64_t*)src.start_col(), ts);
+    load((const uint64_t*)src.end_col(), te);
+    if constexpr (Src::kRecords) {
+      // n: the prefix of ones at a piece's last item is its position + 1
+#pragma unroll
+      for (int j = 0; j < kAggIpt; ++j)
+        sv[slot[j]] = (uint64_t)(lane * kAggIpt + j + 1);
+      store_pieces(0, true);
+      uint64_t du[kAggIpt];
+#pragma unroll
+      for (int j = 0; j < kAggIpt; ++j) du[j] = te[j] - ts[j];
+      if (ns > 0) load(src.sum_col(0), va);
+      do_sum(du, 1);
+    } else {
+      if (ns > 0) load(src.sum_col(0), va);
+    }
+    do_seg(ts, 4, CMin());
+    if (ns > 1) load(src.sum_col(1), vb);
+    do_seg(te, 5, CMax());
+  }
+  for (int i = 0; i < ns; i += 2) {
+    do_sum(va, src.sum_dst(i));
+    if (i + 2 < ns) load(src.sum_col(i + 2), va);
+    if (i + 1 < ns) {
+      do_sum(vb, src.sum_dst(i + 1));
+      if (i + 3 < ns) load(src.sum_col(i + 3), vb);
+    }
   }
 }
 
@@ -1167,7 +1215,7 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                            k_agg_fast_reduce<kMD, FromRecords>,
                            dim3((unsigned)T), dim3(kBlock), s, fr, li, D, M,
                            (const uint32_t*)(L.htb + (int64_t)li * Th),
-                           (const int64_t*)nullptr, R, ovf, nfields, Th));
+                           (const int64_t*)nullptr, R, ovf, Th));
       } else {
         FromRows src{R, M, rows->level_offset, finer};
         CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
@@ -1183,7 +1231,7 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                            dim3(kBlock), s, src, li, D, M,
                            (const uint32_t*)L.htb2,
                            (const int64_t*)(rows->level_offset + li), R, ovf,
-                           nfields, Th));
+                           Th));
       }
       CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
                          grid_for(Th, kBlock), dim3(kBlock), s, ovf, R,
@@ -1308,7 +1356,9 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
   const bool want_workload = (act >> (D + 1)) & 1u;
 
   // ---- fast path: every group is one run of consecutive records
-  if (n > 0 && !filter && level != CHOPPER_LEVEL_WORKLOAD) {
+  // (the fast path addresses columns with 32-bit byte offsets)
+  if (n > 0 && !filter && level != CHOPPER_LEVEL_WORKLOAD &&
+      n < ((int64_t)1 << 29) && rows->cap < ((int64_t)1 << 29)) {
     rc = D <= 4 ? agg_fast<4>(L, S, R, ovf, T, Lv, act, D, M, nfields, rows,
                               level, want_workload, status, s)
                 : agg_fast<8>(L, S, R, ovf, T, Lv, act, D, M, nfields, rows,

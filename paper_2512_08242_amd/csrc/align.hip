@@ -6,6 +6,7 @@
 #include <vector>
 
 #include "sort.h"
+#include "wave.h"
 
 namespace chopper {
 
@@ -216,38 +217,60 @@ __global__ __launch_bounds__(kBlock) void k_transform_markers(
 }
 
 // Dense class ids in (gpu, stream) and (gpu, kind) order from the presence
-// flags (65536 + 512 bytes): every thread counts the flags of 256
-// consecutive pairs, one block scan, then every thread numbers its own.
-__global__ __launch_bounds__(kBlock) void k_dense_classes(
+// flags (65536 + 512 bytes), one block of 1024 threads: every thread counts
+// 64 consecutive (gpu, stream) flags (and at most one (gpu, kind) flag), a
+// block scan numbers them, and every thread writes its own ids with
+// 16-byte stores.
+constexpr int kDenseThreads = 1024;
+
+__device__ inline uint32_t block1024_exclusive(uint32_t v, uint32_t* s_w,
+                                               uint32_t* total) {
+  const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
+  const uint32_t incl = wave_incl(v, OpAdd(), 0u);
+  if (lane == kWave - 1) s_w[w] = incl;
+  __syncthreads();
+  uint32_t pre = 0, tot = 0;
+  for (int q = 0; q < kDenseThreads / kWave; ++q) {
+    if (q < w) pre += s_w[q];
+    tot += s_w[q];
+  }
+  __syncthreads();
+  *total = tot;
+  return pre + incl - v;
+}
+
+__global__ __launch_bounds__(kDenseThreads) void k_dense_classes(
     const uint8_t* pres_s, uint16_t* cmap_s, const uint8_t* pres_k,
     uint16_t* cmap_k, uint32_t* counts) {
-  const uint32_t* w = reinterpret_cast<const uint32_t*>(pres_s) +
-                      threadIdx.x * 64;
+  __shared__ uint32_t s_w[kDenseThreads / kWave];
+  const int t = threadIdx.x;
+  uint4 f[4];
+  const uint4* src = reinterpret_cast<const uint4*>(pres_s) + t * 4;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) f[q] = src[q];
+  const uint8_t* fb = reinterpret_cast<const uint8_t*>(f);
   uint32_t c = 0;
-  for (int q = 0; q < 64; ++q) {
-    const uint32_t x = w[q];
-    c += (x & 0xFFu ? 1u : 0u) + (x & 0xFF00u ? 1u : 0u) +
-         (x & 0xFF0000u ? 1u : 0u) + (x & 0xFF000000u ? 1u : 0u);
-  }
+#pragma unroll
+  for (int b = 0; b < 64; ++b) c += fb[b] ? 1u : 0u;
   uint32_t tot;
-  uint32_t id = block_exclusive(c, OpAdd(), 0u, &tot);
-  const uint8_t* f = pres_s + threadIdx.x * 256;
-  uint16_t* out = cmap_s + threadIdx.x * 256;
-  for (int b = 0; b < 256; ++b) {
-    const bool on = f[b] != 0;
-    out[b] = (uint16_t)(on ? id : 0u);
-    id += on ? 1u : 0u;
+  uint32_t id = block1024_exclusive(c, s_w, &tot);
+  uint16_t ids[64];
+#pragma unroll
+  for (int b = 0; b < 64; ++b) {
+    ids[b] = (uint16_t)(fb[b] ? id : 0u);
+    id += fb[b] ? 1u : 0u;
   }
-  if (threadIdx.x == 0) counts[0] = tot;
-  if (threadIdx.x == 0) {
-    uint32_t k = 0;
-    for (int b = 0; b < 512; ++b) {
-      const bool on = pres_k[b] != 0;
-      cmap_k[b] = (uint16_t)(on ? k : 0u);
-      k += on ? 1u : 0u;
-    }
-    counts[1] = k;
-  }
+  uint4* dst = reinterpret_cast<uint4*>(cmap_s) + t * 8;
+  const uint4* iv = reinterpret_cast<const uint4*>(ids);
+#pragma unroll
+  for (int q = 0; q < 8; ++q) dst[q] = iv[q];
+  if (t == 0) counts[0] = tot;
+  // (gpu, kind) flags: one per thread
+  const uint32_t on = t < 512 && pres_k[t] ? 1u : 0u;
+  uint32_t totk;
+  const uint32_t k = block1024_exclusive(on, s_w, &totk);
+  if (t < 512) cmap_k[t] = (uint16_t)(on ? k : 0u);
+  if (t == 0) counts[1] = totk;
 }
 
 // ---------------------------------------------------------------------------
@@ -361,7 +384,7 @@ extern "C" int chopper_align(const chopper_records* rec,
                      (const ClockDev*)L.clk, start_out, end_out, L.pres_s,
                      L.pres_k, L.counts + 2, status));
   CHOPPER_HIP(launch("align_dense_classes", k_dense_classes, dim3(1),
-                     dim3(kBlock), s, (const uint8_t*)L.pres_s, L.cmap_s,
+                     dim3(kDenseThreads), s, (const uint8_t*)L.pres_s, L.cmap_s,
                      (const uint8_t*)L.pres_k, L.cmap_k, L.counts));
   uint32_t counts[3];
   CHOPPER_HIP(hipMemcpyAsync(counts, L.counts, sizeof(counts),

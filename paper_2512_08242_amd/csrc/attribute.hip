@@ -4,88 +4,66 @@
 // iterations).
 //
 // Markers are sorted by (gpu, level, empty, start') into contiguous
-// per-(gpu, level) segments of non-empty markers.  Each non-empty marker
-// also records the range of next-level markers that start inside it; the
-// search for level l+1 then runs only over that range (plus the single
-// marker just before it, which is the only other candidate), so a record
-// pays log2 of the child count per level instead of log2 of the segment.
-// The narrowed answer equals the full-segment answer for any sorted marker
-// set, nested or not.
+// per-(gpu, level) segments of non-empty markers, and a bucket index over
+// each segment's starts narrows every search to a few markers.  The answer
+// at a level is the last marker of the record's (gpu, level) segment whose
+// start is <= the record's start, if the record starts before its end; the
+// levels are independent, so a record searches all of them in lockstep.
 #include "sort.h"
+#include "bindex.h"
 
 namespace chopper {
 
 bool validate_records(const chopper_records* r);
 bool validate_markers(const chopper_markers* m);
 
-// first index in [lo, hi) with a[i] > x
-__device__ inline int64_t upper_bound_i64(const int64_t* a, int64_t lo,
-                                          int64_t hi, int64_t x) {
-  while (lo < hi) {
-    int64_t mid = lo + ((hi - lo) >> 1);
-    if (a[mid] <= x) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
-// first index in [lo, hi) with a[i] >= x
-__device__ inline int64_t lower_bound_i64(const int64_t* a, int64_t lo,
-                                          int64_t hi, int64_t x) {
-  while (lo < hi) {
-    int64_t mid = lo + ((hi - lo) >> 1);
-    if (a[mid] < x) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
-// sorted marker columns
+// sorted marker columns and the (gpu, level) segment of every non-empty
+// marker (kNone for empty or invalid ones)
 __global__ __launch_bounds__(kBlock) void k_marker_gather(
-    int64_t nm, const uint32_t* mord, const int64_t* ms, const int64_t* me,
-    int64_t* sms, int64_t* sme, uint32_t* sid) {
+    int64_t nm, KeyMarker km, const uint32_t* mord, const int64_t* ms,
+    const int64_t* me, int64_t* sms, int64_t* sme, uint32_t* sid,
+    uint32_t* sseg) {
   int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (p >= nm) return;
   uint32_t j = mord[p];
   sms[p] = ms[j];
   sme[p] = me[j];
   sid[p] = j;
+  const uint32_t c = km.cls(j);
+  sseg[p] = ((c & 1u) || c >= (uint32_t)(km.G * km.D * 2)) ? kNone : c >> 1;
 }
 
-// overlap check between neighbours of a (gpu, level) segment, and the
-// child range of every non-empty marker at the next level
+// overlap check between neighbours of a (gpu, level) segment
 __global__ __launch_bounds__(kBlock) void k_marker_links(
     int G, int D, const uint32_t* coff, const int64_t* sms, const int64_t* sme,
-    uint32_t* clo, uint32_t* chi, uint32_t* status) {
+    uint32_t* status) {
   // one block column per (gpu, level) segment
   const int seg = blockIdx.y;          // g * D + l
-  const int g = seg / D, l = seg % D;
   const uint32_t cls = (uint32_t)seg * 2u;
   const int64_t b = coff[cls], e = coff[cls + 1];
-  int64_t cb = 0, ce = 0;
-  if (l + 1 < D) {
-    cb = coff[cls + 2];
-    ce = coff[cls + 3];
-  }
-  (void)g;
+  (void)G;
+  (void)D;
   bool ov = false;
   for (int64_t p = b + (int64_t)blockIdx.x * kBlock + threadIdx.x; p < e;
        p += (int64_t)gridDim.x * kBlock) {
     if (p + 1 < e && sme[p] > sms[p + 1]) ov = true;
-    if (l + 1 < D) {
-      clo[p] = (uint32_t)lower_bound_i64(sms, cb, ce, sms[p]);
-      chi[p] = (uint32_t)lower_bound_i64(sms, cb, ce, sme[p]);
-    }
   }
   if (__ballot(ov) != 0 && (threadIdx.x & (kWave - 1)) == 0)
     atomicOr(status, (uint32_t)CHOPPER_ST_MARKER_OVERLAP);
 }
 
+// segment parameters held in LDS when there are at most this many
+constexpr int kLdsSegs = 512;
+
+template <int MaxD, bool kLds>
 __global__ __launch_bounds__(kBlock) void k_attribute_records(
     int64_t n, int G, int D, const uint8_t* gpu, const int64_t* start,
-    const uint32_t* coff, const int64_t* sms, const int64_t* sme,
-    const uint32_t* sid, const uint32_t* clo, const uint32_t* chi,
-    uint32_t* idx) {
+    BIndex X, const int64_t* sme, const uint32_t* sid, uint32_t* idx) {
+  __shared__ BSeg s_seg[kLds ? kLdsSegs : 1];
+  if (kLds) {
+    for (int i = threadIdx.x; i < G * D; i += kBlock) s_seg[i] = X.seg[i];
+    __syncthreads();
+  }
   const int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (k >= n) return;
   const int g = gpu[k];
@@ -94,23 +72,24 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
     return;
   }
   const int64_t s = start[k];
-  int64_t parent = -1;
-  for (int l = 0; l < D; ++l) {
-    const uint32_t cls = (uint32_t)(g * D + l) * 2u;
-    const int64_t sb = coff[cls], se = coff[cls + 1];
-    int64_t lo = sb, hi = se;
-    if (parent >= 0) {
-      lo = clo[parent];
-      hi = chi[parent];
+  BSeg P[MaxD];
+  int64_t lo[MaxD], hi[MaxD], t[MaxD];
+#pragma unroll
+  for (int l = 0; l < MaxD; ++l) {
+    t[l] = s;
+    lo[l] = hi[l] = 0;
+    if (l < D) {
+      P[l] = kLds ? s_seg[g * D + l] : X.seg[g * D + l];
+      bi_range(X, P[l], s, &lo[l], &hi[l]);
     }
-    int64_t j = upper_bound_i64(sms, lo, hi, s) - 1;
-    if (j < lo) j = (lo > sb) ? lo - 1 : -1;
+  }
+  bsearch_k<MaxD>(X.key, lo, hi, t);
+#pragma unroll
+  for (int l = 0; l < MaxD; ++l) {
+    if (l >= D) break;
+    const int64_t j = lo[l] - 1;
     uint32_t out = kNone;
-    parent = -1;
-    if (j >= 0 && s < sme[j]) {
-      out = sid[j];
-      parent = j;
-    }
+    if (j >= (int64_t)P[l].sb && s < sme[j]) out = sid[j];
     idx[(int64_t)l * n + k] = out;
   }
 }
@@ -121,8 +100,11 @@ struct AttrLayout {
   int64_t* sms;
   int64_t* sme;
   uint32_t* sid;
-  uint32_t* clo;
-  uint32_t* chi;
+  uint32_t* sseg;
+  BSeg* bsegs;
+  uint32_t* btable;
+  int64_t btable_cap;
+  uint32_t* btmp;
   ClassSortLayout sort;
 };
 
@@ -134,8 +116,11 @@ static AttrLayout attr_layout(Scratch& sc, int64_t nm, int G, int D) {
   L.sms = sc.take<int64_t>(nm);
   L.sme = sc.take<int64_t>(nm);
   L.sid = sc.take<uint32_t>(nm);
-  L.clo = sc.take<uint32_t>(nm);
-  L.chi = sc.take<uint32_t>(nm);
+  L.sseg = sc.take<uint32_t>(nm);
+  L.bsegs = sc.take<BSeg>((int64_t)G * D);
+  L.btable_cap = bindex_table_cap(nm, (int64_t)G * D);
+  L.btable = sc.take<uint32_t>(L.btable_cap);
+  L.btmp = sc.take<uint32_t>((int64_t)G * D + 1);
   L.sort = class_sort_layout(sc, nm, C);
   return L;
 }
@@ -174,9 +159,9 @@ extern "C" int chopper_attribute(const chopper_records* rec,
                        (uint32_t)CHOPPER_ST_RANGE, status));
   if (nm > 0) {
     CHOPPER_HIP(launch("attr_marker_gather", k_marker_gather,
-                       grid_for(nm, kBlock), dim3(kBlock), s, nm,
+                       grid_for(nm, kBlock), dim3(kBlock), s, nm, km,
                        (const uint32_t*)L.mord, mstart_al, mend_al, L.sms,
-                       L.sme, L.sid));
+                       L.sme, L.sid, L.sseg));
     const int64_t per_seg = ceil_div(nm, (int64_t)G * D);
     unsigned gx = (unsigned)ceil_div(per_seg, kBlock);
     if (gx < 1) gx = 1;
@@ -184,13 +169,25 @@ extern "C" int chopper_attribute(const chopper_records* rec,
     CHOPPER_HIP(launch("attr_marker_links", k_marker_links,
                        dim3(gx, (unsigned)(G * D)), dim3(kBlock), s, G, D,
                        (const uint32_t*)L.coff, (const int64_t*)L.sms,
-                       (const int64_t*)L.sme, L.clo, L.chi, status));
+                       (const int64_t*)L.sme, status));
   }
-  if (n == 0) return CHOPPER_OK;
-  CHOPPER_HIP(launch("attr_records", k_attribute_records, grid_for(n, kBlock),
-                     dim3(kBlock), s, n, G, D, rec->gpu, start_al,
-                     (const uint32_t*)L.coff, (const int64_t*)L.sms,
-                     (const int64_t*)L.sme, (const uint32_t*)L.sid,
-                     (const uint32_t*)L.clo, (const uint32_t*)L.chi, idx_out));
+  if (n == 0 || D == 0) return CHOPPER_OK;
+  // bucket index of the non-empty marker starts of every (gpu, level)
+  CHOPPER_HIP(bindex_build(L.sms, L.sseg, nm, nullptr, L.coff, L.coff + 1, 2,
+                           G * D, L.bsegs, L.btable, L.btable_cap, L.btmp, s));
+  const BIndex X{L.sms, L.bsegs, L.btable};
+  auto run = [&](auto kern) -> int {
+    CHOPPER_HIP(launch("attr_records", kern, grid_for(n, kBlock),
+                       dim3(kBlock), s, n, G, D, rec->gpu, start_al, X,
+                       (const int64_t*)L.sme, (const uint32_t*)L.sid,
+                       idx_out));
+    return CHOPPER_OK;
+  };
+  const bool lds = G * D <= kLdsSegs;
+  if (D <= 4)
+    return lds ? run(k_attribute_records<4, true>)
+               : run(k_attribute_records<4, false>);
+  return lds ? run(k_attribute_records<8, true>)
+             : run(k_attribute_records<8, false>);
   return CHOPPER_OK;
 }

@@ -39,6 +39,33 @@ __device__ inline int64_t bi_bsearch(const int64_t* key, int64_t lo,
   return lo;
 }
 
+// K searches in lockstep, so that their loads overlap: on return lo[k] is
+// the first position in [lo[k], hi[k]) with key > t[k].
+template <int K>
+__device__ inline void bsearch_k(const int64_t* key, int64_t (&lo)[K],
+                                 int64_t (&hi)[K], const int64_t (&t)[K]) {
+  for (;;) {
+    bool act = false;
+    int64_t mid[K], v[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      mid[k] = lo[k] + ((hi[k] - lo[k]) >> 1);
+      if (lo[k] < hi[k]) {
+        act = true;
+        v[k] = key[mid[k]];
+      }
+    }
+    if (!act) break;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (lo[k] < hi[k]) {
+        if (v[k] <= t[k]) lo[k] = mid[k] + 1;
+        else hi[k] = mid[k];
+      }
+    }
+  }
+}
+
 // Search range of t in segment P: the answer (first position with key > t)
 // lies in [*lo, *hi].
 __device__ inline void bi_range(const BIndex& X, const BSeg& P, int64_t t,

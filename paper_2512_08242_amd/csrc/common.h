@@ -170,6 +170,10 @@ int64_t scan_scratch_elems(int64_t n);   // number of T slots needed
 template <typename T>
 hipError_t exclusive_scan(const T* in, T* out, int64_t n, T* tmp, T* total,
                           hipStream_t s);
+// the same over the first min(n, *n_dev) elements (n_dev on the device)
+template <typename T>
+hipError_t exclusive_scan(const T* in, T* out, int64_t n, const uint32_t* n_dev,
+                          T* tmp, T* total, hipStream_t s);
 
 // Sorts (key u64) stably and writes the permutation of 0..n-1.
 // Implemented in sort.hip.

@@ -29,8 +29,10 @@ struct Runs {
   const int64_t* rs;      // run start
   const int64_t* re;      // run end
   const int64_t* pl;      // active time of the segment before the run
-  const int64_t* pov;     // exclusive prefix of overlapped time (comm runs)
-  const int64_t* fcrs;    // compute-active time before each comm run start
+  // comm runs only, at dense index voff[g] + (j - first comm run of g):
+  const int64_t* pov;     // exclusive prefix of overlapped time
+  const int64_t* fcrs;    // compute-active time before the run's start
+  const uint32_t* voff;   // [G + 1] first dense index of every gpu
   BIndex X;               // bucket index of the run starts per segment
 };
 
@@ -45,54 +47,23 @@ __device__ inline int64_t F_at(const Runs& R, const BSeg& P, int64_t up,
   return R.pl[j] + (e - R.rs[j]);
 }
 
-// K searches in lockstep, so that their loads overlap: on return lo[k] is
-// the first position in [lo[k], hi[k]) with key > t[k].
-template <int K>
-__device__ inline void bsearch_k(const int64_t* key, int64_t (&lo)[K],
-                                 int64_t (&hi)[K], const int64_t (&t)[K]) {
-  for (;;) {
-    bool act = false;
-    int64_t mid[K], v[K];
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      mid[k] = lo[k] + ((hi[k] - lo[k]) >> 1);
-      if (lo[k] < hi[k]) {
-        act = true;
-        v[k] = key[mid[k]];
-      }
-    }
-    if (!act) break;
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      if (lo[k] < hi[k]) {
-        if (v[k] <= t[k]) lo[k] = mid[k] + 1;
-        else hi[k] = mid[k];
-      }
-    }
-  }
-}
-
-// active time of segment seg strictly before t
-__device__ inline int64_t F_active(const Runs& R, uint32_t seg, int64_t t) {
-  const BSeg P = R.X.seg[seg];
-  int64_t lo[1], hi[1];
-  const int64_t tt[1] = {t};
-  bi_range(R.X, P, t, &lo[0], &hi[0]);
-  bsearch_k<1>(R.rs, lo, hi, tt);
-  return F_at(R, P, lo[0], t);
+// the segment parameters of the first nseg segments, copied to LDS by the
+// whole block (call before any thread leaves)
+__device__ inline void segs_to_lds(BSeg* s_seg, const BSeg* segs, int nseg) {
+  for (int i = threadIdx.x; i < nseg; i += blockDim.x) s_seg[i] = segs[i];
+  __syncthreads();
 }
 
 // CO, MO, OV, ID of [a, b) on gpu g (Section V-C): compute-active time c,
 // comm-active time m and the time where both are, o; both-active time
 // before t is the overlap of the comm runs before t plus, inside the comm
 // run holding t, the compute-active time up to t.
-__device__ inline void window(const Runs& R, uint32_t g, int64_t a, int64_t b,
-                              int64_t* out) {
+__device__ inline void window(const Runs& R, const BSeg& Pc, const BSeg& Pm,
+                              uint32_t vg, int64_t a, int64_t b, int64_t* out) {
   if (b <= a) {
     out[0] = out[1] = out[2] = out[3] = 0;
     return;
   }
-  const BSeg Pc = R.X.seg[g * 2u], Pm = R.X.seg[g * 2u + 1u];
   // compute and comm searches at both ends
   int64_t lo[4], hi[4];
   const int64_t t[4] = {a, b, a, b};
@@ -115,7 +86,8 @@ __device__ inline void window(const Runs& R, uint32_t g, int64_t a, int64_t b,
     qlo[k] = qhi[k] = Pc.sb;
     if (!some[k]) continue;
     const int64_t end = R.re[jm] < tk ? R.re[jm] : tk;
-    base[k] = R.pov[jm] - R.pov[Pm.sb] - R.fcrs[jm];
+    const int64_t v = (int64_t)vg + (jm - (int64_t)Pm.sb);
+    base[k] = R.pov[v] - R.pov[vg] - R.fcrs[v];
     qt[k] = end;
     bi_range(R.X, Pc, end, &qlo[k], &qhi[k]);
   }
@@ -459,61 +431,167 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
 }
 
 // overlapped time inside each comm run: compute-active time within it
+// dense index of the first comm run of every gpu, and their total
+__global__ void k_comm_voff(int G, const BSeg* segs, uint32_t* voff) {
+  if (threadIdx.x != 0) return;
+  uint32_t acc = 0;
+  for (int g = 0; g < G; ++g) {
+    voff[g] = acc;
+    const BSeg& P = segs[2 * g + 1];
+    acc += P.se > P.sb ? P.se - P.sb : 0u;
+  }
+  voff[G] = acc;
+}
+
+// overlapped time inside each comm run (compute-active time within it) and
+// the compute-active time before it, at the run's dense index
 __global__ __launch_bounds__(kBlock) void k_runs_comm_overlap(
     const uint32_t* nruns, Runs R, const uint32_t* rseg, int64_t* ovc,
-    int64_t* fcrs, int64_t cap) {
+    int64_t* fcrs, int64_t cap, int nseg) {
+  __shared__ BSeg s_seg[kSegs];
+  segs_to_lds(s_seg, R.X.seg, nseg);
   const int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (r >= cap) return;
-  int64_t v = 0, f = 0;
-  if (r < (int64_t)*nruns) {
-    const uint32_t seg = rseg[r];
-    if (seg & 1u) {
-      const BSeg P = R.X.seg[seg - 1u];
-      const int64_t t[2] = {R.rs[r], R.re[r]};
-      int64_t lo[2], hi[2];
-      bi_range(R.X, P, t[0], &lo[0], &hi[0]);
-      bi_range(R.X, P, t[1], &lo[1], &hi[1]);
-      bsearch_k<2>(R.rs, lo, hi, t);
-      f = F_at(R, P, lo[0], t[0]);
-      v = F_at(R, P, lo[1], t[1]) - f;
-    }
-  }
-  ovc[r] = v;
-  fcrs[r] = f;
+  if (r >= cap || r >= (int64_t)*nruns) return;
+  const uint32_t seg = rseg[r];
+  if (!(seg & 1u)) return;
+  const BSeg P = s_seg[seg - 1u];
+  const int64_t t[2] = {R.rs[r], R.re[r]};
+  int64_t lo[2], hi[2];
+  bi_range(R.X, P, t[0], &lo[0], &hi[0]);
+  bi_range(R.X, P, t[1], &lo[1], &hi[1]);
+  bsearch_k<2>(R.rs, lo, hi, t);
+  const int64_t f = F_at(R, P, lo[0], t[0]);
+  const int64_t v = (int64_t)R.voff[seg >> 1] + (r - (int64_t)s_seg[seg].sb);
+  ovc[v] = F_at(R, P, lo[1], t[1]) - f;
+  fcrs[v] = f;
 }
 
 // ---------------- queries ----------------------------------------------------
+// Overlapped time of every record, in korder tiles of kWaveTile positions
+// per wave.  Within a (gpu, kind) segment the starts are sorted, so the
+// runs of the other kind that the tile's records can meet form one window:
+// from the run holding the first start to the last run starting before the
+// largest end.  One lane finds it through the bucket index, the wave stages
+// it in LDS (coalesced), and every record searches LDS.  Records of another
+// segment than the tile's first one, or tiles whose window is wider than
+// kRunWin runs, search the bucket index directly.
+constexpr int kRunWin = 256;
+
 __global__ __launch_bounds__(kBlock) void k_overlap_records(
-    int64_t n, int G, const uint8_t* gpu, const uint8_t* cls,
-    const int64_t* start, const int64_t* end, Runs R, int64_t* ovl) {
-  const int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (k >= n) return;
-  const uint32_t g = gpu[k];
-  const int64_t s = start[k], e = end[k];
-  int64_t o = 0;
-  if (e > s && (int)g < G) {
-    // a compute kernel's overlapped time is the comm-active time inside it
-    // and vice versa
-    const uint32_t other = g * 2u + (kind_of(cls[k]) ? 0u : 1u);
-    const BSeg P = R.X.seg[other];
-    const int64_t t[2] = {s, e};
-    int64_t lo[2], hi[2];
-    bi_range(R.X, P, s, &lo[0], &hi[0]);
-    bi_range(R.X, P, e, &lo[1], &hi[1]);
-    bsearch_k<2>(R.rs, lo, hi, t);
-    o = F_at(R, P, lo[1], e) - F_at(R, P, lo[0], s);
+    int64_t n, int G, const uint32_t* korder, const uint8_t* gpu,
+    const uint8_t* cls, const int64_t* start, const int64_t* end, Runs R,
+    int64_t* ovl) {
+  __shared__ BSeg s_seg[kSegs];
+  __shared__ int64_t s_win[kWavesPerBlock][3][kRunWin];
+  segs_to_lds(s_seg, R.X.seg, 2 * G);
+  const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
+  const int64_t base =
+      ((int64_t)blockIdx.x * kWavesPerBlock + wv) * (int64_t)kWaveTile;
+  if (base >= n) return;
+  uint32_t r[kTileIpt], seg[kTileIpt];
+  int64_t s[kTileIpt], e[kTileIpt];
+  uint32_t m_in = 0, m_valid = 0;   // position exists / and gpu < G
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    const int64_t p = base + (int64_t)j * kWave + lane;
+    const bool in = p < n;
+    r[j] = korder[in ? p : base];
+    seg[j] = (uint32_t)gpu[r[j]] * 2u + (uint32_t)kind_of(cls[r[j]]);
+    s[j] = start[r[j]];
+    e[j] = end[r[j]];
+    if (in) m_in |= 1u << j;
+    if (in && (int)(seg[j] >> 1) < G) m_valid |= 1u << j;
   }
-  ovl[k] = o;
+  // the tile's main segment and the window of the other kind's runs
+  const uint32_t seg0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)seg[0]);
+  int64_t emax = kI64Min;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j)
+    if (((m_valid >> j) & 1u) && seg[j] == seg0 && e[j] > emax) emax = e[j];
+  emax = wave_incl(emax, OpMax(), kI64Min);
+  emax = lane63(emax);
+  const int64_t smin = (int64_t)(
+      (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)s[0]) |
+      ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(
+           (int)(uint32_t)((uint64_t)s[0] >> 32)) << 32));
+  const bool main_ok = (int)(seg0 >> 1) < G;
+  const BSeg Q = s_seg[main_ok ? (seg0 ^ 1u) : 0u];
+  int64_t wlo = 0, whi = 0;
+  if (main_ok && lane == 0) {
+    int64_t lo[2], hi[2];
+    const int64_t t[2] = {smin, emax};
+    bi_range(R.X, Q, smin, &lo[0], &hi[0]);
+    bi_range(R.X, Q, emax, &lo[1], &hi[1]);
+    bsearch_k<2>(R.rs, lo, hi, t);
+    wlo = lo[0] - 1 > (int64_t)Q.sb ? lo[0] - 1 : (int64_t)Q.sb;
+    whi = lo[1];
+  }
+  // run positions fit 32 bits
+  wlo = (int64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)wlo);
+  whi = (int64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)whi);
+  const int K = (int)(whi - wlo);
+  const bool win = main_ok && K >= 0 && K <= kRunWin;
+  int64_t* wrs = s_win[wv][0];
+  int64_t* wre = s_win[wv][1];
+  int64_t* wpl = s_win[wv][2];
+  if (win) {
+    for (int q = lane; q < K; q += kWave) {
+      wrs[q] = R.rs[wlo + q];
+      wre[q] = R.re[wlo + q];
+      wpl[q] = R.pl[wlo + q];
+    }
+  }
+  wave_sync();
+  // window searches for the main segment, bucket searches for the rest
+  int64_t o[kTileIpt];
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    o[j] = 0;
+    if (!((m_valid >> j) & 1u) || e[j] <= s[j]) continue;
+    if (win && seg[j] == seg0) {
+      int64_t F[2];
+#pragma unroll
+      for (int z = 0; z < 2; ++z) {
+        const int64_t t = z ? e[j] : s[j];
+        int lo = 0, hi = K;
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (wrs[mid] <= t) lo = mid + 1;
+          else hi = mid;
+        }
+        const int q = lo - 1;
+        F[z] = q < 0 ? 0
+                     : wpl[q] + ((wre[q] < t ? wre[q] : t) - wrs[q]);
+      }
+      o[j] = F[1] - F[0];
+    } else {
+      // a compute kernel's overlapped time is the comm-active time inside
+      // it and vice versa
+      const BSeg P = s_seg[seg[j] ^ 1u];
+      const int64_t t[2] = {s[j], e[j]};
+      int64_t lo[2], hi[2];
+      bi_range(R.X, P, s[j], &lo[0], &hi[0]);
+      bi_range(R.X, P, e[j], &lo[1], &hi[1]);
+      bsearch_k<2>(R.rs, lo, hi, t);
+      o[j] = F_at(R, P, lo[1], e[j]) - F_at(R, P, lo[0], s[j]);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j)
+    if ((m_in >> j) & 1u) ovl[r[j]] = o[j];
 }
 
 __global__ __launch_bounds__(kBlock) void k_overlap_markers(
     int64_t nm, int G, const uint8_t* mgpu, const int64_t* ms,
     const int64_t* me, Runs R, int64_t* mwin) {
+  __shared__ BSeg s_seg[kSegs];
+  segs_to_lds(s_seg, R.X.seg, 2 * G);
   const int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (j >= nm) return;
   int64_t w[4] = {0, 0, 0, 0};
   const uint32_t g = mgpu[j];
-  if ((int)g < G) window(R, g, ms[j], me[j], w);
+  if ((int)g < G)
+    window(R, s_seg[g * 2u], s_seg[g * 2u + 1u], R.voff[g], ms[j], me[j], w);
   for (int z = 0; z < 4; ++z) mwin[4 * j + z] = w[z];
 }
 
@@ -532,38 +610,120 @@ __global__ void k_overlap_gpus(int G, Runs R, int64_t* gwin) {
   }
   if (a == kI64Max) a = b = 0;
   int64_t w[4];
-  window(R, (uint32_t)g, a, b, w);
+  window(R, R.X.seg[g * 2], R.X.seg[g * 2 + 1], R.voff[g], a, b, w);
   gwin[6 * g + 0] = a;
   gwin[6 * g + 1] = b;
   for (int z = 0; z < 4; ++z) gwin[6 * g + 2 + z] = w[z];
 }
 
 // ---------------- bubbles ----------------------------------------------------
-// In (gpu, stream, start') order the previous compute record of a compute
-// record is found by walking back over communication records of the same
-// (gpu, stream).  Each communication record is walked over by at most one
-// compute record (the next one), so the total work is linear.
+// In (gpu, stream, start') order the bubble before a compute record is the
+// time from the end of the previous compute record of the same (gpu,
+// stream) to its start.  Per wave tile of `order` positions, the previous
+// compute record comes from an exclusive "last compute record" scan in the
+// blocked arrangement; the tile's first (gpu, stream) takes its carry by
+// walking back before the tile over communication records, only when the
+// tile holds a compute record of it (so each communication record is walked
+// over at most once and the total work is linear).
+struct LastComp {
+  uint32_t key;     // (gpu, stream) of the last item; kNone: empty
+  uint32_t has;     // a compute item of that key was seen
+  int64_t end;      // its end
+};
+struct OpLastComp {
+  __device__ LastComp operator()(LastComp a, LastComp b) const {
+    if (b.key == kNone) return a;
+    if (b.has || a.key != b.key) return b;
+    return LastComp{b.key, a.has, a.end};
+  }
+};
+
 __global__ __launch_bounds__(kBlock) void k_gap(
     int64_t n, const uint32_t* order, const uint8_t* gpu, const uint8_t* stream,
     const uint8_t* cls, const int64_t* start, const int64_t* end,
     int64_t* gap) {
-  const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (p >= n) return;
-  const uint32_t r = order[p];
-  int64_t gv = 0;
-  if (!kind_of(cls[r])) {
-    const uint8_t g = gpu[r], st = stream[r];
-    for (int64_t q = p - 1; q >= 0; --q) {
+  __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
+  const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
+  const int64_t base =
+      ((int64_t)blockIdx.x * kWavesPerBlock + wv) * (int64_t)kWaveTile;
+  if (base >= n) return;
+  int64_t* sl = s_slice[wv];
+  uint32_t r[kTileIpt], key[kTileIpt], comp[kTileIpt];
+  int64_t s[kTileIpt], e[kTileIpt];
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    const int64_t p = base + (int64_t)j * kWave + lane;
+    const bool in = p < n;
+    r[j] = order[in ? p : base];
+    key[j] = in ? (uint32_t)gpu[r[j]] * 256u + stream[r[j]] : kNone;
+    comp[j] = in && !kind_of(cls[r[j]]) ? 1u : 0u;
+    s[j] = start[r[j]];
+    e[j] = end[r[j]];
+  }
+  // carry into the tile for its first key
+  const uint32_t key0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)key[0]);
+  bool need = false;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) need = need || (comp[j] && key[j] == key0);
+  LastComp carry{key0, 0u, 0};
+  if (__ballot(need) != 0 && lane == 0) {
+    for (int64_t q = base - 1; q >= 0; --q) {
       const uint32_t rq = order[q];
-      if (gpu[rq] != g || stream[rq] != st) break;
+      if ((uint32_t)gpu[rq] * 256u + stream[rq] != key0) break;
       if (!kind_of(cls[rq])) {
-        const int64_t b = start[r] - end[rq];
-        gv = b > 0 ? b : 0;
+        carry.has = 1u;
+        carry.end = end[rq];
         break;
       }
     }
   }
-  gap[r] = gv;
+  carry.has = (uint32_t)__builtin_amdgcn_readfirstlane((int)carry.has);
+  carry.end = (int64_t)(
+      (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)carry.end) |
+      ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(
+           (int)(uint32_t)((uint64_t)carry.end >> 32)) << 32));
+  // blocked arrangement
+  int64_t eb[kTileIpt];
+  uint32_t kb[kTileIpt], cb[kTileIpt];
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    eb[j] = e[j];
+    kb[j] = key[j];
+    cb[j] = comp[j];
+  }
+  wave_to_blocked(sl, eb, lane);
+  wave_to_blocked((uint32_t*)sl, kb, lane);
+  wave_to_blocked((uint32_t*)sl, cb, lane);
+  OpLastComp op;
+  const LastComp ident{kNone, 0u, 0};
+  LastComp agg = ident;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j)
+    agg = op(agg, LastComp{kb[j], cb[j], eb[j]});
+  const LastComp incl = wave_incl(agg, op, ident);
+  LastComp cur = op(carry, wave_shr1_any(ident, incl));
+  // end of the previous compute record of the same key, per item (blocked)
+  int64_t pe[kTileIpt];
+  uint32_t ph[kTileIpt];
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    ph[j] = (cur.key == kb[j] && cur.has) ? 1u : 0u;
+    pe[j] = cur.end;
+    cur = op(cur, LastComp{kb[j], cb[j], eb[j]});
+  }
+  wave_to_striped(sl, pe, lane);
+  wave_to_striped((uint32_t*)sl, ph, lane);
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    const int64_t p = base + (int64_t)j * kWave + lane;
+    if (p >= n) continue;
+    int64_t gv = 0;
+    if (comp[j] && ph[j]) {
+      const int64_t b = s[j] - pe[j];
+      gv = b > 0 ? b : 0;
+    }
+    gap[r[j]] = gv;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -588,6 +748,7 @@ struct OverlapLayout {
   int64_t* fcrs;
   int64_t* scan_i64;
   int64_t* tot_i64;
+  uint32_t* voff;
   BSeg* bsegs;
   uint32_t* btable;
   int64_t btable_cap;
@@ -616,6 +777,7 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   L.fcrs = sc.take<int64_t>(n);
   L.scan_i64 = sc.take<int64_t>(scan_scratch_elems(n));
   L.tot_i64 = sc.take<int64_t>(2);
+  L.voff = sc.take<uint32_t>(G + 1);
   L.bsegs = sc.take<BSeg>(kSegs);
   L.btable_cap = bindex_table_cap(n, kSegs);
   L.btable = sc.take<uint32_t>(L.btable_cap);
@@ -684,18 +846,22 @@ extern "C" int chopper_overlap(const chopper_records* rec,
   // bucket index of the run starts of every (gpu, kind)
   CHOPPER_HIP(bindex_build(L.rs, L.rseg, n, L.nruns, L.rbeg, L.rend, 1, kSegs,
                            L.bsegs, L.btable, L.btable_cap, L.btmp, s));
-  Runs R{L.rs, L.re, L.pl, L.pov, L.fcrs,
+  Runs R{L.rs, L.re, L.pl, L.pov, L.fcrs, L.voff,
          BIndex{L.rs, L.bsegs, L.btable}};
+  CHOPPER_HIP(launch("ov_comm_voff", k_comm_voff, dim3(1), dim3(64), s, G,
+                     (const BSeg*)L.bsegs, L.voff));
   if (n > 0) {
     CHOPPER_HIP(launch("ov_runs_comm_overlap", k_runs_comm_overlap,
                        grid_for(n, kBlock), dim3(kBlock), s,
                        (const uint32_t*)L.nruns, R, (const uint32_t*)L.rseg,
-                       L.ovc, L.fcrs, n));
-    CHOPPER_HIP(exclusive_scan<int64_t>(L.ovc, L.pov, n, L.scan_i64,
-                                        L.tot_i64 + 1, s));
-    CHOPPER_HIP(launch("ov_records", k_overlap_records, grid_for(n, kBlock),
-                       dim3(kBlock), s, n, G, rec->gpu, rec->cls, start_al,
-                       end_al, R, ovl_out));
+                       L.ovc, L.fcrs, n, 2 * G));
+    CHOPPER_HIP(exclusive_scan<int64_t>(L.ovc, L.pov, n,
+                                        (const uint32_t*)(L.voff + G),
+                                        L.scan_i64, L.tot_i64 + 1, s));
+    CHOPPER_HIP(launch("ov_records", k_overlap_records,
+                       dim3((unsigned)ceil_div(n, (int64_t)kOvTile)),
+                       dim3(kBlock), s, n, G, korder, rec->gpu, rec->cls,
+                       start_al, end_al, R, ovl_out));
   }
   if (nm > 0)
     CHOPPER_HIP(launch("ov_markers", k_overlap_markers, grid_for(nm, kBlock),
@@ -704,7 +870,9 @@ extern "C" int chopper_overlap(const chopper_records* rec,
   CHOPPER_HIP(launch("ov_gpus", k_overlap_gpus, grid_for(G, kBlock),
                      dim3(kBlock), s, G, R, gwin_out));
   if (n > 0) {
-    CHOPPER_HIP(launch("ov_gap", k_gap, grid_for(n, kBlock), dim3(kBlock), s,
+    CHOPPER_HIP(launch("ov_gap", k_gap,
+                       dim3((unsigned)ceil_div(n, (int64_t)kOvTile)),
+                       dim3(kBlock), s,
                        n, order, rec->gpu, rec->stream, rec->cls, start_al,
                        end_al, gap_out));
   }

@@ -13,10 +13,23 @@ constexpr int kScanTile = kBlock * kScanIpt;
 
 int64_t scan_scratch_elems(int64_t n) { return ceil_div(n, kScanTile) + 1; }
 
+// n_dev (optional): the element count held on the device, at most n
+__device__ inline int64_t scan_len(int64_t n, const uint32_t* n_dev) {
+  if (!n_dev) return n;
+  const int64_t m = (int64_t)*n_dev;
+  return m < n ? m : n;
+}
+
 template <typename T>
 __global__ __launch_bounds__(kBlock) void k_scan_reduce(const T* in, int64_t n,
+                                                        const uint32_t* n_dev,
                                                         T* tile_sum) {
+  n = scan_len(n, n_dev);
   const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  if (base >= n) {               // whole block: an empty tile
+    if (threadIdx.x == 0) tile_sum[blockIdx.x] = 0;
+    return;
+  }
   T acc = 0;
   for (int j = 0; j < kScanIpt; ++j) {
     int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
@@ -55,8 +68,11 @@ __global__ __launch_bounds__(kBlock) void k_scan_spine(T* tile_sum,
 template <typename T>
 __global__ __launch_bounds__(kBlock) void k_scan_down(const T* in, T* out,
                                                       int64_t n,
+                                                      const uint32_t* n_dev,
                                                       const T* tile_pre) {
+  n = scan_len(n, n_dev);
   const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  if (base >= n) return;
   T v[kScanIpt];
   T acc = 0;
   for (int j = 0; j < kScanIpt; ++j) {
@@ -76,6 +92,12 @@ __global__ __launch_bounds__(kBlock) void k_scan_down(const T* in, T* out,
 template <typename T>
 hipError_t exclusive_scan(const T* in, T* out, int64_t n, T* tmp, T* total,
                           hipStream_t s) {
+  return exclusive_scan<T>(in, out, n, nullptr, tmp, total, s);
+}
+
+template <typename T>
+hipError_t exclusive_scan(const T* in, T* out, int64_t n, const uint32_t* n_dev,
+                          T* tmp, T* total, hipStream_t s) {
   int64_t ntiles = ceil_div(n, kScanTile);
   hipError_t e;
   if (n <= 0) {
@@ -85,15 +107,18 @@ hipError_t exclusive_scan(const T* in, T* out, int64_t n, T* tmp, T* total,
     return e;
   }
   e = launch("scan_reduce", k_scan_reduce<T>, dim3((unsigned)ntiles),
-             dim3(kBlock), s, in, n, tmp);
+             dim3(kBlock), s, in, n, n_dev, tmp);
   if (e != hipSuccess) return e;
   e = launch("scan_spine", k_scan_spine<T>, dim3(1), dim3(kBlock), s, tmp,
              ntiles, total);
   if (e != hipSuccess) return e;
   return launch("scan_down", k_scan_down<T>, dim3((unsigned)ntiles),
-                dim3(kBlock), s, in, out, n, (const T*)tmp);
+                dim3(kBlock), s, in, out, n, n_dev, (const T*)tmp);
 }
 
+template hipError_t exclusive_scan<int64_t>(const int64_t*, int64_t*, int64_t,
+                                            const uint32_t*, int64_t*,
+                                            int64_t*, hipStream_t);
 template hipError_t exclusive_scan<uint32_t>(const uint32_t*, uint32_t*,
                                              int64_t, uint32_t*, uint32_t*,
                                              hipStream_t);
