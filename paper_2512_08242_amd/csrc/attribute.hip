@@ -11,6 +11,7 @@
 // levels are independent, so a record searches all of them in lockstep.
 #include "sort.h"
 #include "bindex.h"
+#include "wave.h"
 
 namespace chopper {
 
@@ -54,43 +55,167 @@ __global__ __launch_bounds__(kBlock) void k_marker_links(
 
 // segment parameters held in LDS when there are at most this many
 constexpr int kLdsSegs = 512;
+// LDS pool of marker starts per wave, shared by the levels' windows
+constexpr int kMarkWin = 512;
 
+// Records in natural order, wave tiles of kWaveTile, each lane owning eight
+// consecutive records (vector loads and stores).  For the tile's first gpu,
+// lane l finds the window of level-l markers that the tile's starts can
+// fall in (from the marker holding the smallest start to the last one
+// starting at or before the largest); the windows that fit the wave's LDS
+// pool are staged there.  A lane searches a window for its first record
+// and advances from there for the next ones, whose starts usually follow;
+// records of other gpus and levels whose window does not fit search the
+// bucket index.  The input order only affects speed.
 template <int MaxD, bool kLds>
 __global__ __launch_bounds__(kBlock) void k_attribute_records(
     int64_t n, int G, int D, const uint8_t* gpu, const int64_t* start,
     BIndex X, const int64_t* sme, const uint32_t* sid, uint32_t* idx) {
-  __shared__ BSeg s_seg[kLds ? kLdsSegs : 1];
+  __shared__ BSeg s_lds[kLds ? kLdsSegs : 1];
+  __shared__ int64_t s_pool[kWavesPerBlock][kMarkWin];
   if (kLds) {
-    for (int i = threadIdx.x; i < G * D; i += kBlock) s_seg[i] = X.seg[i];
+    for (int i = threadIdx.x; i < G * D; i += kBlock) s_lds[i] = X.seg[i];
     __syncthreads();
   }
-  const int64_t k = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (k >= n) return;
-  const int g = gpu[k];
-  if (g >= G) {
-    for (int l = 0; l < D; ++l) idx[(int64_t)l * n + k] = kNone;
-    return;
-  }
-  const int64_t s = start[k];
-  BSeg P[MaxD];
-  int64_t lo[MaxD], hi[MaxD], t[MaxD];
+  const BSeg* s_seg = kLds ? s_lds : X.seg;
+  const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
+  const int64_t base =
+      ((int64_t)blockIdx.x * kWavesPerBlock + wv) * (int64_t)kWaveTile;
+  if (base >= n) return;
+  int64_t* pool = s_pool[wv];
+  const int64_t k0 = base + (int64_t)lane * kTileIpt;   // lane's first record
+  const bool full = base + kWaveTile <= n;                // uniform
+  // vector loads only from suitably aligned columns
+  const bool vload = full && ((uintptr_t)gpu & 7) == 0 &&
+                     ((uintptr_t)start & 15) == 0;
+  uint32_t g[kTileIpt];
+  int64_t s[kTileIpt];
+  if (vload) {
+    const uint2 gv = *reinterpret_cast<const uint2*>(gpu + k0);
+    const uint8_t* gb = reinterpret_cast<const uint8_t*>(&gv);
+    const int4* sp = reinterpret_cast<const int4*>(start + k0);
+    int64_t sv[kTileIpt];
 #pragma unroll
-  for (int l = 0; l < MaxD; ++l) {
-    t[l] = s;
-    lo[l] = hi[l] = 0;
-    if (l < D) {
-      P[l] = kLds ? s_seg[g * D + l] : X.seg[g * D + l];
-      bi_range(X, P[l], s, &lo[l], &hi[l]);
+    for (int q = 0; q < kTileIpt / 2; ++q)
+      *reinterpret_cast<int4*>(&sv[2 * q]) = sp[q];
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      g[j] = gb[j];
+      s[j] = sv[j];
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      const int64_t k = k0 + j;
+      g[j] = k < n ? gpu[k] : 0xFFFFFFFFu;
+      s[j] = k < n ? start[k] : 0;
     }
   }
-  bsearch_k<MaxD>(X.key, lo, hi, t);
+  // a record is searched when it exists and its gpu is in range; records
+  // past n (partial last tile) carry g = 0xFFFFFFFF and are never searched
+  uint32_t m_ok = 0;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j)
+    if (k0 + j < n && g[j] < (uint32_t)G) m_ok |= 1u << j;
+  const uint32_t g0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)g[0]);
+  const bool g0ok = g0 < (uint32_t)G;
+  int64_t smin = kI64Max, smax = kI64Min;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j)
+    if (((m_ok >> j) & 1u) && g[j] == g0) {
+      smin = s[j] < smin ? s[j] : smin;
+      smax = s[j] > smax ? s[j] : smax;
+    }
+  smin = lane63(wave_incl(smin, OpMin(), kI64Max));
+  smax = lane63(wave_incl(smax, OpMax(), kI64Min));
+  // lane l < D: window of level l
+  int64_t wlo = 0, wk = 0;
+  if (g0ok && lane < D) {
+    const BSeg P = s_seg[g0 * D + lane];
+    int64_t lo[2], hi[2];
+    const int64_t t[2] = {smin, smax};
+    bi_range(X, P, smin, &lo[0], &hi[0]);
+    bi_range(X, P, smax, &lo[1], &hi[1]);
+    bsearch_k<2>(X.key, lo, hi, t);
+    wlo = lo[0] - 1 > (int64_t)P.sb ? lo[0] - 1 : (int64_t)P.sb;
+    wk = lo[1] - wlo;
+  }
+  // pool offsets: levels in order while they fit
+  const int64_t woff = wave_incl(wk, OpAdd(), (int64_t)0) - wk;
+  const bool fits = g0ok && lane < D && woff + wk <= kMarkWin;
+  int64_t wl[MaxD], wn[MaxD], wo[MaxD];
+#pragma unroll
+  for (int l = 0; l < MaxD; ++l) {
+    wl[l] = __shfl(wlo, l, kWave);
+    wo[l] = __shfl(woff, l, kWave);
+    wn[l] = __shfl(fits ? wk : (int64_t)-1, l, kWave);
+  }
+#pragma unroll
+  for (int l = 0; l < MaxD; ++l) {
+    if (l >= D || wn[l] < 0) continue;
+    for (int64_t q = lane; q < wn[l]; q += kWave)
+      pool[wo[l] + q] = X.key[wl[l] + q];
+  }
+  wave_sync();
+  // per level: the window position of each record, then its marker
 #pragma unroll
   for (int l = 0; l < MaxD; ++l) {
     if (l >= D) break;
-    const int64_t j = lo[l] - 1;
-    uint32_t out = kNone;
-    if (j >= (int64_t)P[l].sb && s < sme[j]) out = sid[j];
-    idx[(int64_t)l * n + k] = out;
+    int64_t qq[kTileIpt], sb[kTileIpt];
+    const int64_t* w = pool + wo[l];
+    const int nw = (int)wn[l];
+    int a = -1;             // window index of the last key <= previous start
+    int64_t prev = kI64Max;
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      qq[j] = -1;
+      sb[j] = 0;
+      if (!((m_ok >> j) & 1u)) continue;
+      sb[j] = s_seg[g[j] * D + l].sb;
+      if (g[j] == g0 && nw >= 0) {
+        if (a < 0 || s[j] < prev) {
+          int lo = 0, hi = nw;
+          while (lo < hi) {
+            const int m = (lo + hi) >> 1;
+            if (w[m] <= s[j]) lo = m + 1;
+            else hi = m;
+          }
+          a = lo - 1;
+        } else {
+          while (a + 1 < nw && w[a + 1] <= s[j]) ++a;
+        }
+        prev = s[j];
+        qq[j] = wl[l] + a;
+      } else {
+        // another gpu, or a window that did not fit (rare)
+        qq[j] = bi_upper(X, g[j] * D + l, s[j]) - 1;
+      }
+    }
+    // marker ends and ids, all loads in flight before any is used
+    int64_t me[kTileIpt];
+    uint32_t id[kTileIpt];
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      const int64_t q = qq[j] >= sb[j] && qq[j] >= 0 ? qq[j] : 0;
+      me[j] = sme[q];
+      id[j] = sid[q];
+    }
+    uint32_t out[kTileIpt];
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j)
+      out[j] = (((m_ok >> j) & 1u) && qq[j] >= sb[j] && s[j] < me[j])
+                   ? id[j]
+                   : kNone;
+    uint32_t* dst = idx + (int64_t)l * n + k0;
+    if (full && ((uintptr_t)dst & 15) == 0) {
+      uint4* d4 = reinterpret_cast<uint4*>(dst);
+      d4[0] = make_uint4(out[0], out[1], out[2], out[3]);
+      d4[1] = make_uint4(out[4], out[5], out[6], out[7]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < kTileIpt; ++j)
+        if (k0 + j < n) dst[j] = out[j];
+    }
   }
 }
 
@@ -176,11 +301,11 @@ extern "C" int chopper_attribute(const chopper_records* rec,
   CHOPPER_HIP(bindex_build(L.sms, L.sseg, nm, nullptr, L.coff, L.coff + 1, 2,
                            G * D, L.bsegs, L.btable, L.btable_cap, L.btmp, s));
   const BIndex X{L.sms, L.bsegs, L.btable};
+  const unsigned grid = (unsigned)ceil_div(n, (int64_t)kWaveTile * kWavesPerBlock);
   auto run = [&](auto kern) -> int {
-    CHOPPER_HIP(launch("attr_records", kern, grid_for(n, kBlock),
-                       dim3(kBlock), s, n, G, D, rec->gpu, start_al, X,
-                       (const int64_t*)L.sme, (const uint32_t*)L.sid,
-                       idx_out));
+    CHOPPER_HIP(launch("attr_records", kern, dim3(grid), dim3(kBlock), s, n,
+                       G, D, rec->gpu, start_al, X, (const int64_t*)L.sme,
+                       (const uint32_t*)L.sid, idx_out));
     return CHOPPER_OK;
   };
   const bool lds = G * D <= kLdsSegs;
@@ -189,5 +314,4 @@ extern "C" int chopper_attribute(const chopper_records* rec,
                : run(k_attribute_records<4, false>);
   return lds ? run(k_attribute_records<8, true>)
              : run(k_attribute_records<8, false>);
-  return CHOPPER_OK;
 }

@@ -35,6 +35,10 @@ struct OpAdd {
   template <typename T>
   __device__ T operator()(T a, T b) const { return a + b; }
 };
+struct OpMin {
+  template <typename T>
+  __device__ T operator()(T a, T b) const { return a < b ? a : b; }
+};
 struct OpMax {
   template <typename T>
   __device__ T operator()(T a, T b) const { return a > b ? a : b; }
