@@ -38,10 +38,36 @@ def algorithmic_bytes(n, nm, rows, depth, nc, n_rows_finest):
 def roof_kernel_bytes(n, depth, nc, n_rows_finest):
     """Algorithmic bytes of one launch of the finest-level reduction: per
     record korder, gpu, cls, path, start, end, gap, ovl and counters read
-    once; per finest row its sums and counters written once."""
+    once; per finest row its header (path, gpu, kind, first record) and its
+    sums and counters written once."""
     per_rec = 4 + 1 + 1 + 4 * depth + 8 * 4 + 8 * nc
-    per_row = 8 * (6 + nc)
+    per_row = 4 * depth + 1 + 1 + 4 + 8 * (6 + nc)
     return n * per_rec + n_rows_finest * per_row
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter record
+    (FETCH_SIZE and WRITE_SIZE scaled by a plain copy of known size), or
+    None when there is none or the kernel's sources changed since."""
+    import glob
+    import hashlib
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*_traffic.json")):
+        try:
+            rec = json.load(open(path))
+        except (OSError, ValueError):
+            continue
+        if rec.get("kernel") != kernel:
+            continue
+        h = hashlib.sha256()
+        try:
+            for f in rec["source_files"]:
+                h.update(open(os.path.join(ROOT, f), "rb").read())
+        except OSError:
+            return None
+        if h.hexdigest() != rec.get("source_sha256"):
+            return None
+        return float(rec["traffic_bytes_per_dispatch"])
+    return None
 
 
 def cpu_baseline(cid, iters):
@@ -156,7 +182,7 @@ def main():
         "dtype": "int64",
         "data": "synthetic",
         "config": {
-            "workload": f"config {cid}: {tg.CONFIG_NAMES[cid]}",
+            "workload": tg.CONFIG_NAMES[cid],
             "records": n, "markers": nm, "depth": depth, "counters": nc,
             "rows": rows_total,
         },
@@ -169,7 +195,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": measured_traffic(ROOF_KERNEL),
             "kernel_ms": kms,
             "bytes_per_launch": kb,
         },
