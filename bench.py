@@ -35,14 +35,14 @@ def algorithmic_bytes(n, nm, rows, depth, nc, n_rows_finest):
     return rec_in + rec_out + mk + rows * row
 
 
-def roof_kernel_bytes(n, depth, nc, n_rows_finest):
-    """Algorithmic bytes of one launch of the finest-level reduction: per
-    record korder, gpu, cls, path, start, end, gap, ovl and counters read
-    once; per finest row its header (path, gpu, kind, first record) and its
-    sums and counters written once."""
+def roof_kernel_bytes(n, depth, nc, rows_written):
+    """Algorithmic bytes of one launch of the records reduction: per record
+    korder, gpu, cls, path, start, end, gap, ovl and counters read once; per
+    row it produces (the two finest levels) its header (path, gpu, kind,
+    first record) and its sums and counters written once."""
     per_rec = 4 + 1 + 1 + 4 * depth + 8 * 4 + 8 * nc
     per_row = 4 * depth + 1 + 1 + 4 + 8 * (6 + nc)
-    return n * per_rec + n_rows_finest * per_row
+    return n * per_rec + rows_written * per_row
 
 
 def measured_traffic(kernel):
@@ -142,6 +142,8 @@ def main():
     lo = pipe.rows.level_offset.cpu().numpy()
     rows_total = int(lo[-1])
     rows_finest = int(lo[depth] - lo[depth - 1])
+    # the records reduction writes the two finest levels
+    rows_records = int(lo[depth] - lo[max(depth - 2, 0)])
     log(f"[bench] warmup done; rows: {rows_total} (finest level "
         f"{rows_finest})")
 
@@ -166,7 +168,7 @@ def main():
 
     value = n / (ms * 1e-3)
     bmin = algorithmic_bytes(n, nm, rows_total, depth, nc, rows_finest)
-    kb = roof_kernel_bytes(n, depth, nc, rows_finest)
+    kb = roof_kernel_bytes(n, depth, nc, rows_records)
     achieved = kb / (kms * 1e-3) / 1e9
     out = {
         "metric": METRIC,

@@ -777,22 +777,80 @@ __global__ void k_agg_offsets_fast(int L, int64_t ntiles,
     atomicOr(status, (uint32_t)CHOPPER_ST_ROWS_OVERFLOW);
 }
 
-// Reduction of one level when groups are runs.  Within a wave tile the
-// pieces (maximal runs of equal keys) are numbered in item order; rows are
-// numbered from the tile's head count (level-major exclusive scan of the
-// heads pass).  Every field goes striped -> blocked through the wave's LDS
-// slice; sums take one plain prefix sum over the tile and a piece's total is
-// the difference of the prefix at its last item and at the previous piece's
-// last item (exact modulo 2^64); tmin and tmax take a segmented scan.  The
-// value at each piece's last item is written to LDS at the piece's index, so
-// that the stores of consecutive lanes go to consecutive rows.  The tile's
-// first piece may continue a row of an earlier tile: it goes to the tile's
-// overflow slot.  Every valid item has a key here (the heads pass sends
-// traces with unkeyed items to the general path).
-template <int MaxD, typename Src>
+// Piece structure of one level over a wave tile (blocked arrangement: lane
+// holds items lane * 8 + j).  Pieces are maximal runs of equal keys; the
+// tile's first piece may continue a row of an earlier tile (c0 = 1).
+struct LevelTile {
+  uint32_t m_head;    // item starts a piece (tile start and invalid items too)
+  uint32_t m_hv;      // ... and is valid
+  uint32_t m_last;    // valid item ends a piece
+  uint32_t m_real;    // valid item starts a group (key differs from previous)
+  uint32_t pfx;       // pieces started in the lanes below
+  uint32_t NP;        // pieces in the tile
+  uint32_t c0;        // the first piece continues an earlier row
+  int64_t r0;         // row of the tile's first new group
+  uint32_t before;    // items of the lane before its first piece head
+  WaveSegMasks masks; // lane segment flags for wave scans
+};
+
+// slot[j]: LDS slot of item j's value -- its piece index when it ends a
+// piece, else a junk slot of its own lane
+__device__ inline void level_tile(const uint32_t (&key)[kAggIpt],
+                                  uint32_t tile_prev, int tile_n, int lane,
+                                  int64_t r0, LevelTile& T,
+                                  uint32_t (&slot)[kAggIpt]) {
+  uint32_t m_valid = 0, m_real = 0, m_head = 0;
+  uint32_t prev = wave_shr1_u32(tile_prev, key[kAggIpt - 1]);
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int q = lane * kAggIpt + j;
+    const bool valid = q < tile_n;
+    const uint32_t k = key[j];
+    if (valid) m_valid |= 1u << j;
+    if (valid && k != prev) m_real |= 1u << j;
+    if (!valid || q == 0 || k != prev) m_head |= 1u << j;
+    prev = k;
+  }
+  const uint64_t h0 = __ballot(m_head & 1u);
+  const uint32_t next0 =
+      lane == kWave - 1 ? 1u : (uint32_t)((h0 >> (lane + 1)) & 1u);
+  T.m_head = m_head;
+  T.m_hv = m_head & m_valid;
+  T.m_real = m_real;
+  T.m_last = m_valid & ((m_head >> 1) | (next0 << (kAggIpt - 1)));
+  T.pfx = wave_prefix_small<4>((uint32_t)__popc(T.m_hv));
+  T.NP = (uint32_t)__builtin_amdgcn_readlane(
+      (int)(T.pfx + (uint32_t)__popc(T.m_hv)), kWave - 1);
+  T.c0 = __ballot(lane == 0 && !(m_real & 1u)) != 0 ? 1u : 0u;
+  T.r0 = r0;
+  T.before = m_head ? (uint32_t)(__ffs(m_head) - 1) : (uint32_t)kAggIpt;
+  T.masks = wave_seg_masks(m_head != 0);
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    const uint32_t idx =
+        T.pfx + (uint32_t)__popc(T.m_hv & ((2u << j) - 1u)) - 1u;
+    slot[j] = ((T.m_last >> j) & 1u) ? idx : (uint32_t)(kWaveTile + lane);
+  }
+}
+
+// Reduction of one level -- with kTwo also the next coarser one -- when
+// groups are runs.  Within a wave tile, rows are numbered from the tile's
+// head count (level-major exclusive scan of the heads pass).  Every field
+// goes striped -> blocked through the wave's LDS slice; sums take one plain
+// prefix sum over the tile and a piece's total is the difference of the
+// prefix at its last item and at the previous piece's last item (exact
+// modulo 2^64), for both levels from the same prefix; tmin and tmax take a
+// segmented scan per level.  Piece values are written to LDS at the piece's
+// index, so that the stores of consecutive lanes go to consecutive rows.  A
+// tile's first piece may continue a row of an earlier tile: it goes to the
+// tile's overflow slot of its level (level li: slot w, level li - 1: slot
+// nwt + w).  Every valid item has a key here (the heads pass sends traces
+// with unkeyed items to the general path).
+template <int MaxD, typename Src, bool kTwo>
 __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     Src src, int li, int D, int64_t M, const uint32_t* tilebase,
-    const int64_t* row0, RowsDev R, Overflow ovf, int64_t nwt) {
+    const uint32_t* tilebase2, const int64_t* row0, RowsDev R, Overflow ovf,
+    int64_t nwt) {
   __shared__ uint64_t s_v[kWavesPerBlock][kSlice];
   const int lane = lane_id();
   const int wv = (int)(threadIdx.x / kWave);
@@ -801,16 +859,21 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
   const int64_t cnt = src.count();
   const int64_t base = w * kWaveTile;
   if (base >= cnt) {
-    if (lane == 0) ovf.row[w] = kNone;
+    if (lane == 0) {
+      ovf.row[w] = kNone;
+      if (kTwo) ovf.row[nwt + w] = kNone;
+    }
     return;
   }
   const int tile_n =
       (int)((cnt - base) < kWaveTile ? (cnt - base) : (int64_t)kWaveTile);
+  const int li2 = li - 1;
   uint64_t* sv = s_v[wv];
   uint32_t* sk = (uint32_t*)sv;
-  // striped items: source index, gpu * 2 + kind, path, key
+  // striped items: source index, gpu * 2 + kind, path, keys
   uint32_t rs[kAggIpt], gk[kAggIpt], p[kAggIpt][MaxD];
-  uint32_t tile_prev;
+  uint32_t key[kAggIpt], key2[kAggIpt];
+  uint32_t tprev, tprev2 = kNone;
   {
 #pragma unroll
     for (int j = 0; j < kAggIpt; ++j) {
@@ -820,109 +883,86 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     }
     uint32_t cr, cgk, cp[MaxD];
     gather_item<MaxD>(src, base > 0 ? base - 1 : 0, D, cr, cgk, cp);
-    tile_prev = base > 0 ? level_key<MaxD>(cp, cgk, li, D, M) : kNone;
+    tprev = base > 0 ? level_key<MaxD>(cp, cgk, li, D, M) : kNone;
+    if (kTwo) tprev2 = base > 0 ? level_key<MaxD>(cp, cgk, li2, D, M) : kNone;
 #pragma unroll
     for (int j = 0; j < kAggIpt; ++j) {
       const int q = j * kWave + lane;
-      sk[pad8(q)] = q < tile_n ? level_key<MaxD>(p[j], gk[j], li, D, M)
-                               : kNone;
+      key[j] = q < tile_n ? level_key<MaxD>(p[j], gk[j], li, D, M) : kNone;
+      key2[j] = kTwo && q < tile_n ? level_key<MaxD>(p[j], gk[j], li2, D, M)
+                                   : kNone;
     }
   }
-  wave_sync();
-  uint32_t key[kAggIpt];
-#pragma unroll
-  for (int j = 0; j < kAggIpt; ++j) key[j] = sk[pad8(lane * kAggIpt + j)];
-  wave_sync();
-  // pieces in the blocked arrangement
-  uint32_t m_valid = 0, m_real = 0, m_head = 0;
-  {
-    uint32_t prev = wave_shr1_u32(tile_prev, key[kAggIpt - 1]);
-#pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) {
-      const int q = lane * kAggIpt + j;
-      const bool valid = q < tile_n;
-      const uint32_t k = key[j];
-      if (valid) m_valid |= 1u << j;
-      if (valid && k != prev) m_real |= 1u << j;
-      if (!valid || q == 0 || k != prev) m_head |= 1u << j;
-      prev = k;
-    }
-  }
-  // last item of a piece: the next item starts one (the tile's end does)
-  uint32_t m_last;
-  {
-    const uint64_t h0 = __ballot(m_head & 1u);
-    const uint32_t next0 =
-        lane == kWave - 1 ? 1u : (uint32_t)((h0 >> (lane + 1)) & 1u);
-    m_last = m_valid & ((m_head >> 1) | (next0 << (kAggIpt - 1)));
-  }
-  // piece index of every item; NP pieces in the tile; c0 = 1 when the
-  // first piece continues a row of an earlier tile; rows r0 .. r0 + NP - c0
-  const uint32_t m_hv = m_head & m_valid;
-  const uint32_t pfx = wave_prefix_small<4>((uint32_t)__popc(m_hv));
-  const uint32_t NP = (uint32_t)__builtin_amdgcn_readlane(
-      (int)(pfx + (uint32_t)__popc(m_hv)), kWave - 1);
-  const uint32_t c0 =
-      __ballot(lane == 0 && !(m_real & 1u)) != 0 ? 1u : 0u;
-  const int64_t r0 = (row0 ? *row0 : 0) + (int64_t)tilebase[w];
-  int slot[kAggIpt];
-#pragma unroll
-  for (int j = 0; j < kAggIpt; ++j) {
-    const uint32_t idx = pfx + (uint32_t)__popc(m_hv & ((2u << j) - 1u)) - 1u;
-    slot[j] = ((m_last >> j) & 1u) ? (int)idx : kWaveTile + lane;
-  }
+  wave_to_blocked(sk, key, lane);
+  if (kTwo) wave_to_blocked(sk, key2, lane);
+  LevelTile T1, T2;
+  uint32_t slot[kAggIpt], slot2[kAggIpt];
+  level_tile(key, tprev, tile_n, lane,
+             (row0 ? *row0 : 0) + (int64_t)tilebase[w], T1, slot);
+  if (kTwo)
+    level_tile(key2, tprev2, tile_n, lane, (int64_t)tilebase2[w], T2, slot2);
+
   // headers of the rows that start here, written from the striped items:
-  // the row of every real head goes back through LDS
-  {
-    uint32_t run = pfx;   // pieces before the item, then its index
+  // the row of every group head goes back through LDS
+  auto headers = [&](const LevelTile& T, int lv) {
+    uint32_t rw[kAggIpt];
 #pragma unroll
     for (int j = 0; j < kAggIpt; ++j) {
-      run += (m_hv >> j) & 1u;
-      const int64_t row = r0 + (int64_t)run - 1 - c0;
-      sk[pad8(lane * kAggIpt + j)] =
-          ((m_real >> j) & 1u) && row < R.cap ? (uint32_t)row : kNone;
+      const uint32_t idx =
+          T.pfx + (uint32_t)__popc(T.m_hv & ((2u << j) - 1u)) - 1u;
+      const int64_t row = T.r0 + (int64_t)idx - (int64_t)T.c0;
+      rw[j] = ((T.m_real >> j) & 1u) && row < R.cap ? (uint32_t)row : kNone;
     }
-  }
-  wave_sync();
+    wave_to_striped(sk, rw, lane);
 #pragma unroll
-  for (int j = 0; j < kAggIpt; ++j) {
-    const uint32_t wr = sk[pad8(j * kWave + lane)];
-    if (wr == kNone) continue;
+    for (int j = 0; j < kAggIpt; ++j) {
+      const uint32_t wr = rw[j];
+      if (wr == kNone) continue;
 #pragma unroll
-    for (int l = 0; l < MaxD; ++l)
-      if (l < D)
-        R.path[(int64_t)l * R.cap + wr] = (li < D && l <= li) ? p[j][l] : kNone;
-    R.gpu[wr] = (uint8_t)(gk[j] >> 1);
-    R.kind[wr] = (uint8_t)(gk[j] & 1u);
-    R.first[wr] = src.first_of(rs[j]);
+      for (int l = 0; l < MaxD; ++l)
+        if (l < D)
+          R.path[(int64_t)l * R.cap + wr] =
+              (lv < D && l <= lv) ? p[j][l] : kNone;
+      R.gpu[wr] = (uint8_t)(gk[j] >> 1);
+      R.kind[wr] = (uint8_t)(gk[j] & 1u);
+      R.first[wr] = src.first_of(rs[j]);
+    }
+  };
+  headers(T1, li);
+  if (kTwo) headers(T2, li2);
+  if (lane == 0) {
+    ovf.row[w] = T1.c0 && T1.r0 >= 1 && T1.r0 - 1 < R.cap
+                     ? (uint32_t)(T1.r0 - 1) : kNone;
+    if (kTwo)
+      ovf.row[nwt + w] = T2.c0 && T2.r0 >= 1 && T2.r0 - 1 < R.cap
+                             ? (uint32_t)(T2.r0 - 1) : kNone;
   }
-  wave_sync();
-  if (lane == 0)
-    ovf.row[w] = c0 && r0 >= 1 && r0 - 1 < R.cap ? (uint32_t)(r0 - 1) : kNone;
-  const WaveSegMasks masks = wave_seg_masks(m_head != 0);
-  const uint32_t before =
-      m_head ? (uint32_t)(__ffs(m_head) - 1) : (uint32_t)kAggIpt;
   // byte offsets of the striped items (sizes are below 2^29 here)
   uint32_t off[kAggIpt];
 #pragma unroll
   for (int j = 0; j < kAggIpt; ++j) off[j] = rs[j] << 3;
 
   // piece values at the slots -> rows (and the overflow slot)
-  auto store_pieces = [&](int f, bool diff) {
+  auto store_pieces = [&](const LevelTile& T, int64_t obase, int f,
+                          bool diff) {
     uint64_t* col = row_column(R, f);
-    uint64_t* oslot = ovf.val + (int64_t)f * ovf.cap + w;
+    uint64_t* oslot = ovf.val + (int64_t)f * ovf.cap + obase + w;
     wave_sync();
-    for (uint32_t q = lane; q < NP; q += kWave) {
+    for (uint32_t q = lane; q < T.NP; q += kWave) {
       uint64_t v = sv[q];
       if (diff && q > 0) v -= sv[q - 1];
-      if (q < c0) {
+      if (q < T.c0) {
         *oslot = v;
       } else {
-        const int64_t row = r0 + (int64_t)(q - c0);
+        const int64_t row = T.r0 + (int64_t)(q - T.c0);
         if (row < R.cap) col[row] = v;
       }
     }
     wave_sync();
+  };
+  auto put = [&](const uint32_t (&sl)[kAggIpt], const uint64_t (&x)[kAggIpt]) {
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) sv[sl[j]] = x[j];
   };
   auto do_sum = [&](const uint64_t (&v)[kAggIpt], int f) {
     uint64_t x[kAggIpt];
@@ -934,27 +974,40 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     const uint64_t incl = wave_incl(x[kAggIpt - 1], OpAdd(), (uint64_t)0);
     const uint64_t carry = wave_shr1(0ull, incl);
 #pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) sv[slot[j]] = x[j] + carry;
-    store_pieces(f, true);
+    for (int j = 0; j < kAggIpt; ++j) x[j] += carry;
+    put(slot, x);
+    store_pieces(T1, 0, f, true);
+    if (kTwo) {
+      put(slot2, x);
+      store_pieces(T2, nwt, f, true);
+    }
+  };
+  auto seg_pass = [&](const LevelTile& T, const uint32_t (&sl)[kAggIpt],
+                      const uint64_t (&xin)[kAggIpt], int64_t obase, int f,
+                      auto cmb) {
+    using C = decltype(cmb);
+    uint64_t x[kAggIpt];
+    uint64_t acc = xin[0];
+    x[0] = acc;
+#pragma unroll
+    for (int j = 1; j < kAggIpt; ++j) {
+      acc = ((T.m_head >> j) & 1u) ? xin[j] : cmb(acc, xin[j]);
+      x[j] = acc;
+    }
+    const uint64_t incl = wave_seg_incl<C>(T.masks, acc);
+    const uint64_t carry = wave_shr1(C::ident, incl);
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j)
+      sv[sl[j]] = (uint32_t)j < T.before ? cmb(carry, x[j]) : x[j];
+    store_pieces(T, obase, f, false);
   };
   auto do_seg = [&](const uint64_t (&v)[kAggIpt], int f, auto cmb) {
-    using C = decltype(cmb);
     uint64_t x[kAggIpt];
 #pragma unroll
     for (int j = 0; j < kAggIpt; ++j) x[j] = v[j];
     wave_to_blocked(sv, x, lane);
-    uint64_t acc = x[0];
-#pragma unroll
-    for (int j = 1; j < kAggIpt; ++j) {
-      acc = ((m_head >> j) & 1u) ? x[j] : cmb(acc, x[j]);
-      x[j] = acc;
-    }
-    const uint64_t incl = wave_seg_incl<C>(masks, acc);
-    const uint64_t carry = wave_shr1(C::ident, incl);
-#pragma unroll
-    for (int j = 0; j < kAggIpt; ++j)
-      sv[slot[j]] = (uint32_t)j < before ? cmb(carry, x[j]) : x[j];
-    store_pieces(f, false);
+    seg_pass(T1, slot, x, 0, f, cmb);
+    if (kTwo) seg_pass(T2, slot2, x, nwt, f, cmb);
   };
   auto load = [&](const uint64_t* col, uint64_t (&v)[kAggIpt]) {
 #pragma unroll
@@ -972,10 +1025,16 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     load((const uint64_t*)src.end_col(), te);
     if constexpr (Src::kRecords) {
       // n: the prefix of ones at a piece's last item is its position + 1
+      uint64_t pos[kAggIpt];
 #pragma unroll
       for (int j = 0; j < kAggIpt; ++j)
-        sv[slot[j]] = (uint64_t)(lane * kAggIpt + j + 1);
-      store_pieces(0, true);
+        pos[j] = (uint64_t)(lane * kAggIpt + j + 1);
+      put(slot, pos);
+      store_pieces(T1, 0, 0, true);
+      if (kTwo) {
+        put(slot2, pos);
+        store_pieces(T2, nwt, 0, true);
+      }
       uint64_t du[kAggIpt];
 #pragma unroll
       for (int j = 0; j < kAggIpt; ++j) du[j] = te[j] - ts[j];
@@ -1204,56 +1263,88 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                      s, Lv, Th, (const uint32_t*)L.htb,
                      (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
                      want_workload, rows->cap, rows->level_offset, status));
+  // the fast-path flags and the level offsets (row counts per level size
+  // the launches of the coarser levels)
   uint32_t hf[2] = {1u, 0u};
+  int64_t lo_h[kMaxLevels + 1];
   CHOPPER_HIP(hipMemcpyAsync(hf, L.hflags, sizeof(hf), hipMemcpyDeviceToHost,
                              s));
+  CHOPPER_HIP(hipMemcpyAsync(lo_h, rows->level_offset,
+                             sizeof(int64_t) * (size_t)(Lv + 1),
+                             hipMemcpyDeviceToHost, s));
   CHOPPER_HIP(hipStreamSynchronize(s));
+  auto level_rows = [&](int li) -> int64_t {
+    int64_t a = lo_h[li], b = lo_h[li + 1];
+    if (b > rows->cap) b = rows->cap;
+    return b > a ? b - a : 0;
+  };
   if (hf[0] == 0) {
-    auto fast_level = [&](int li, int finer) -> int {
+    // finer < 0: from the records (two levels, li and li - 1, when `two`)
+    auto fast_level = [&](int li, int finer, bool two) -> int {
       if (finer < 0) {
-        CHOPPER_HIP(launch("agg_fast_reduce_records",
-                           k_agg_fast_reduce<kMD, FromRecords>,
-                           dim3((unsigned)T), dim3(kBlock), s, fr, li, D, M,
-                           (const uint32_t*)(L.htb + (int64_t)li * Th),
-                           (const int64_t*)nullptr, R, ovf, Th));
+        const uint32_t* tb = L.htb + (int64_t)li * Th;
+        if (two)
+          CHOPPER_HIP(launch("agg_fast_reduce_records",
+                             k_agg_fast_reduce<kMD, FromRecords, true>,
+                             dim3((unsigned)T), dim3(kBlock), s, fr, li, D, M,
+                             tb, (const uint32_t*)(tb - Th),
+                             (const int64_t*)nullptr, R, ovf, Th));
+        else
+          CHOPPER_HIP(launch("agg_fast_reduce_records",
+                             k_agg_fast_reduce<kMD, FromRecords, false>,
+                             dim3((unsigned)T), dim3(kBlock), s, fr, li, D, M,
+                             tb, (const uint32_t*)nullptr,
+                             (const int64_t*)nullptr, R, ovf, Th));
+        const int64_t ns = two ? 2 * Th : Th;
+        CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
+                           grid_for(ns, kBlock), dim3(kBlock), s, ovf, R,
+                           nfields, ns));
       } else {
+        // launches sized by the finer level's row count
+        const int64_t cnt = level_rows(finer);
+        if (cnt == 0) return CHOPPER_OK;
+        const int64_t nw = ceil_div(cnt, (int64_t)kWaveTile);
+        const unsigned gr = (unsigned)ceil_div(nw, (int64_t)kWavesPerBlock);
         FromRows src{R, M, rows->level_offset, finer};
         CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
                            L.hflags2, 2));
         CHOPPER_HIP(launch("agg_heads_rows", k_agg_heads<kMD, FromRows>,
-                           dim3(gh), dim3(kBlock), s, src,
-                           1u << li, li, li, D, M, Th, L.htc2, L.hflags2,
+                           dim3(gr), dim3(kBlock), s, src,
+                           1u << li, li, li, D, M, nw, L.htc2, L.hflags2,
                            status));
-        CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc2, L.htb2, Th, L.hscan,
+        CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc2, L.htb2, nw, L.hscan,
                                              L.htotal + 1, s));
         CHOPPER_HIP(launch("agg_fast_reduce_rows",
-                           k_agg_fast_reduce<kMD, FromRows>, dim3((unsigned)T),
+                           k_agg_fast_reduce<kMD, FromRows, false>, dim3(gr),
                            dim3(kBlock), s, src, li, D, M,
-                           (const uint32_t*)L.htb2,
+                           (const uint32_t*)L.htb2, (const uint32_t*)nullptr,
                            (const int64_t*)(rows->level_offset + li), R, ovf,
-                           Th));
+                           nw));
+        CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
+                           grid_for(nw, kBlock), dim3(kBlock), s, ovf, R,
+                           nfields, nw));
       }
-      CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
-                         grid_for(Th, kBlock), dim3(kBlock), s, ovf, R,
-                         nfields, Th));
       return CHOPPER_OK;
     };
     if (level == CHOPPER_LEVEL_ALL) {
-      rc = fast_level(D > 0 ? D - 1 : D, -1);
+      // the records give the two finest levels, each coarser one comes from
+      // the rows of the level below
+      const bool two = D >= 2;
+      rc = fast_level(D > 0 ? D - 1 : D, -1, two);
       if (rc != CHOPPER_OK) return rc;
-      for (int li = D - 2; li >= 0; --li) {
-        rc = fast_level(li, li + 1);
+      for (int li = D - (two ? 3 : 2); li >= 0; --li) {
+        rc = fast_level(li, li + 1, false);
         if (rc != CHOPPER_OK) return rc;
       }
       if (D > 0) {
-        rc = fast_level(D, 0);
+        rc = fast_level(D, 0, false);
         if (rc != CHOPPER_OK) return rc;
       }
       CHOPPER_HIP(launch("agg_workload_from_gpu", k_agg_workload_from_gpu,
                          dim3(1), dim3(64), s,
                          (const int64_t*)rows->level_offset, D, R, nfields));
     } else {
-      rc = fast_level(level == CHOPPER_LEVEL_GPU ? D : level, -1);
+      rc = fast_level(level == CHOPPER_LEVEL_GPU ? D : level, -1, false);
       if (rc != CHOPPER_OK) return rc;
     }
     return CHOPPER_OK;

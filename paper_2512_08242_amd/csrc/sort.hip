@@ -25,57 +25,78 @@ int64_t sort_tiles(int64_t n) { return ceil_div(n, kSortTile); }
 
 // ---------------------------------------------------------------------------
 // In-tile stable ranking of up to 256 digit values.
-// Items are striped: item j of thread t is tile position j * kBlock + t.
-// On return s_count[d] = number of valid items with digit d in the tile,
-// s_start[d] = exclusive prefix of s_count, rank[j] = stable position of the
+// Items are striped: item j of thread t is tile position j * kBlock + t, so
+// tile order is (row j, wave, lane).  Every wave-row counts its digits with
+// `nbits` ballots (lanes with equal digits find each other; the lowest one
+// records the count), one pass turns the counts of the 8 x 4 (row, wave)
+// cells into per-digit exclusive prefixes, and an item's rank is its cell's
+// prefix plus the number of equal lanes below it.
+// On return count[d] = number of valid items with digit d in the tile,
+// start[d] = exclusive prefix of count, rank[j] = stable position of the
 // item among equal digits.
 // ---------------------------------------------------------------------------
 struct RankShared {
-  uint32_t wave[kWavesPerBlock][256];
+  uint16_t cell[kSortIpt][kWavesPerBlock][256];   // counts, then prefixes
   uint32_t count[256];
   uint32_t start[256];
 };
 
 __device__ inline void tile_rank(const uint32_t (&dig)[kSortIpt],
                                  const bool (&valid)[kSortIpt],
-                                 uint32_t (&rank)[kSortIpt], RankShared& sh) {
+                                 uint32_t (&rank)[kSortIpt], RankShared& sh,
+                                 int nbits) {
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1);
   const int w = t / kWave;
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int q = 0; q < kWavesPerBlock; ++q) sh.wave[q][t] = 0;
-  sh.count[t] = 0;
+  {
+    uint4* z = reinterpret_cast<uint4*>(&sh.cell[0][0][0]);
+    constexpr int kZ = (int)(sizeof(sh.cell) / sizeof(uint4));
+    for (int i = t; i < kZ; i += kBlock) z[i] = make_uint4(0u, 0u, 0u, 0u);
+  }
   __syncthreads();
+  uint32_t rin[kSortIpt];
+#pragma unroll
   for (int j = 0; j < kSortIpt; ++j) {
     const uint32_t d = dig[j];
     const bool v = valid[j];
     uint64_t peers = __ballot(v);
-#pragma unroll
-    for (int b = 0; b < 8; ++b) {
+    for (int b = 0; b < nbits; ++b) {
       const bool bit = (d >> b) & 1u;
       const uint64_t bb = __ballot(bit);
       peers &= bit ? bb : ~bb;
     }
-    const uint32_t rin = __popcll(peers & lt);
-    if (v && rin == 0) sh.wave[w][d] = __popcll(peers);
-    __syncthreads();
-    if (v) {
-      uint32_t pre = sh.count[d];
-      for (int q = 0; q < w; ++q) pre += sh.wave[q][d];
-      rank[j] = pre + rin;
-    }
-    __syncthreads();
-    uint32_t add = 0;
-    for (int q = 0; q < kWavesPerBlock; ++q) {
-      add += sh.wave[q][t];
-      sh.wave[q][t] = 0;
-    }
-    sh.count[t] += add;
-    __syncthreads();
+    rin[j] = __popcll(peers & lt);
+    if (v && rin[j] == 0) sh.cell[j][w][d] = (uint16_t)__popcll(peers);
   }
+  __syncthreads();
+  {
+    // digit t: exclusive prefix over the cells in tile order
+    uint32_t acc = 0;
+#pragma unroll
+    for (int j = 0; j < kSortIpt; ++j)
+#pragma unroll
+      for (int q = 0; q < kWavesPerBlock; ++q) {
+        const uint32_t c = sh.cell[j][q][t];
+        sh.cell[j][q][t] = (uint16_t)acc;
+        acc += c;
+      }
+    sh.count[t] = acc;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j)
+    if (valid[j]) rank[j] = sh.cell[j][w][dig[j]] + rin[j];
   uint32_t tot;
   sh.start[t] = block_exclusive(sh.count[t], OpAdd(), 0u, &tot);
   __syncthreads();
+}
+
+// number of ballots that separate c classes
+__host__ __device__ inline int class_bits(int c) {
+  int b = 0;
+  while (b < 8 && (1 << b) < c) ++b;
+  return b;
 }
 
 // ---------------------------------------------------------------------------
@@ -88,10 +109,29 @@ __global__ __launch_bounds__(kBlock) void k_class_hist(Acc acc, int64_t n,
   __shared__ uint32_t h[256];
   h[threadIdx.x] = 0;
   __syncthreads();
+  const int nbits = class_bits(acc.nclass());
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  uint32_t d[kSortIpt];
+  bool v[kSortIpt];
+#pragma unroll
   for (int j = 0; j < kSortIpt; ++j) {
-    int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
-    if (i < n) atomicAdd(&h[acc.cls(i)], 1u);
+    const int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
+    v[j] = i < n;
+    d[j] = v[j] ? acc.cls(i) : 0u;
+  }
+  // one LDS add per distinct class of every wave-row
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j) {
+    uint64_t peers = __ballot(v[j]);
+    for (int b = 0; b < nbits; ++b) {
+      const bool bit = (d[j] >> b) & 1u;
+      const uint64_t bb = __ballot(bit);
+      peers &= bit ? bb : ~bb;
+    }
+    if (v[j] && __popcll(peers & lt) == 0)
+      atomicAdd(&h[d[j]], (uint32_t)__popcll(peers));
   }
   __syncthreads();
   if ((int)threadIdx.x < acc.nclass())
@@ -114,7 +154,7 @@ __global__ __launch_bounds__(kBlock) void k_class_partition(
     valid[j] = i < n;
     dig[j] = valid[j] ? acc.cls(i) : 0u;
   }
-  tile_rank(dig, valid, rank, sh);
+  tile_rank(dig, valid, rank, sh, class_bits(acc.nclass()));
   if ((int)threadIdx.x < acc.nclass())
     s_gbase[threadIdx.x] =
         tileoff[(int64_t)threadIdx.x * ntiles + blockIdx.x];
@@ -249,7 +289,7 @@ __global__ __launch_bounds__(kBlock) void k_digit_scatter(
     v[j] = valid[j] ? val_in[i] : 0u;
     dig[j] = (uint32_t)(k[j] >> shift) & 255u;
   }
-  tile_rank(dig, valid, rank, sh);
+  tile_rank(dig, valid, rank, sh, 8);
   s_gbase[threadIdx.x] = tileoff[(int64_t)threadIdx.x * ntiles + blockIdx.x];
   for (int j = 0; j < kSortIpt; ++j) {
     if (!valid[j]) continue;
