@@ -145,50 +145,118 @@ __global__ __launch_bounds__(kBlock) void k_transform_records(
     const uint8_t* cls, const int64_t* start, const int64_t* end,
     const ClockDev* clk, int64_t* s_out, int64_t* e_out, uint8_t* pres_s,
     uint8_t* pres_k, uint32_t* unsorted, uint32_t* status) {
-  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  const int lane = threadIdx.x & (kWave - 1);
-  uint32_t st = 0;
-  uint32_t g = 0;
-  int64_t s2 = 0;
-  bool bad_order = false;
-  if (i < n) {
-    g = gpu[i];
-    const uint32_t c = cls[i];
-    const int64_t s = start[i], e = end[i];
-    ClockDev k{0, 0, 0};
-    if ((int)g < n_gpus) k = clk[g];
-    else st |= CHOPPER_ST_BAD_GPU;
-    if (c >= 8) st |= CHOPPER_ST_BAD_CLASS;
-    if (e < s) st |= CHOPPER_ST_NEG_DURATION;
-    s2 = align_time(s, k);
-    const int64_t e2 = align_time(e, k);
-    if (out_of_range(s) || out_of_range(e) || out_of_range(s2) ||
-        out_of_range(e2))
-      st |= CHOPPER_ST_RANGE;
-    s_out[i] = s2;
-    e_out[i] = e2;
+  // each lane owns eight consecutive records (a wave 512)
+  const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
+  const int64_t base =
+      ((int64_t)blockIdx.x * kWavesPerBlock + wv) * (int64_t)kWaveTile;
+  if (base >= n) return;
+  const int64_t k0 = base + (int64_t)lane * kTileIpt;
+  const bool full = base + kWaveTile <= n;
+  const bool vec = full && (((uintptr_t)gpu | (uintptr_t)stream |
+                             (uintptr_t)cls) & 7) == 0 &&
+                   (((uintptr_t)start | (uintptr_t)end | (uintptr_t)s_out |
+                     (uintptr_t)e_out) & 15) == 0;
+  uint8_t g8[kTileIpt], st8[kTileIpt], c8[kTileIpt];
+  int64_t s[kTileIpt], e[kTileIpt];
+  if (vec) {
+    *reinterpret_cast<uint2*>(g8) = *reinterpret_cast<const uint2*>(gpu + k0);
+    *reinterpret_cast<uint2*>(st8) =
+        *reinterpret_cast<const uint2*>(stream + k0);
+    *reinterpret_cast<uint2*>(c8) = *reinterpret_cast<const uint2*>(cls + k0);
+#pragma unroll
+    for (int q = 0; q < kTileIpt / 2; ++q) {
+      *reinterpret_cast<int4*>(&s[2 * q]) =
+          reinterpret_cast<const int4*>(start + k0)[q];
+      *reinterpret_cast<int4*>(&e[2 * q]) =
+          reinterpret_cast<const int4*>(end + k0)[q];
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      const int64_t k = k0 + j;
+      const bool v = k < n;
+      g8[j] = v ? gpu[k] : 0;
+      st8[j] = v ? stream[k] : 0;
+      c8[j] = v ? cls[k] : 0;
+      s[j] = v ? start[k] : 0;
+      e[j] = v ? end[k] : 0;
+    }
   }
+  uint32_t st = 0;
+  int64_t s2[kTileIpt], e2[kTileIpt];
+  uint32_t gl = 0xFFFFFFFFu;     // gpu of the clock held
+  ClockDev kc{0, 0, 0};
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    const uint32_t g = g8[j];
+    if (k0 + j >= n) {
+      s2[j] = e2[j] = 0;
+      continue;
+    }
+    if (g != gl) {
+      gl = g;
+      kc = (int)g < n_gpus ? clk[g] : ClockDev{0, 0, 0};
+    }
+    if ((int)g >= n_gpus) st |= CHOPPER_ST_BAD_GPU;
+    if (c8[j] >= 8) st |= CHOPPER_ST_BAD_CLASS;
+    if (e[j] < s[j]) st |= CHOPPER_ST_NEG_DURATION;
+    s2[j] = align_time(s[j], kc);
+    e2[j] = align_time(e[j], kc);
+    if (out_of_range(s[j]) || out_of_range(e[j]) || out_of_range(s2[j]) ||
+        out_of_range(e2[j]))
+      st |= CHOPPER_ST_RANGE;
+  }
+  if (vec) {
+#pragma unroll
+    for (int q = 0; q < kTileIpt / 2; ++q) {
+      reinterpret_cast<int4*>(s_out + k0)[q] =
+          *reinterpret_cast<const int4*>(&s2[2 * q]);
+      reinterpret_cast<int4*>(e_out + k0)[q] =
+          *reinterpret_cast<const int4*>(&e2[2 * q]);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j)
+      if (k0 + j < n) {
+        s_out[k0 + j] = s2[j];
+        e_out[k0 + j] = e2[j];
+      }
+  }
+  // presence of (gpu, stream) and (gpu, kind): one plain byte store per run
+  // of equal pairs in the lane
   {
-    // every lane takes part in the shuffles of mark_present
-    const bool v = i < n;
-    const uint32_t ks = v ? g * 256u + stream[i] : 0xFFFFFFFFu;
-    const uint32_t kk = v ? g * 2u + (uint32_t)kind_of(cls[i]) : 0xFFFFFFFFu;
-    const uint32_t ps = __shfl_up(ks, 1, kWave), pk = __shfl_up(kk, 1, kWave);
-    if (v && (lane == 0 || ps != ks)) pres_s[ks] = 1;
-    if (v && (lane == 0 || pk != kk)) pres_k[kk] = 1;
+    uint32_t ps = 0xFFFFFFFFu, pk = 0xFFFFFFFFu;
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      if (k0 + j >= n) break;
+      const uint32_t ks = (uint32_t)g8[j] * 256u + st8[j];
+      const uint32_t kk = (uint32_t)g8[j] * 2u + (uint32_t)kind_of(c8[j]);
+      if (ks != ps) pres_s[ks] = 1;
+      if (kk != pk) pres_k[kk] = 1;
+      ps = ks;
+      pk = kk;
+    }
   }
   // is the input ordered by (gpu, start')?  Then every (gpu, stream) and
   // (gpu, kind) subsequence is time-ordered and one stable class pass sorts.
-  uint32_t pg = __shfl_up(g, 1, kWave);
-  int64_t ps = __shfl_up(s2, 1, kWave);
-  if (lane == 0 && i > 0 && i < n) {
-    pg = gpu[i - 1];
-    ClockDev k{0, 0, 0};
-    if ((int)pg < n_gpus) k = clk[pg];
-    ps = align_time(start[i - 1], k);
+  bool bad = false;
+#pragma unroll
+  for (int j = 1; j < kTileIpt; ++j)
+    if (k0 + j < n)
+      bad = bad || g8[j - 1] > g8[j] || (g8[j - 1] == g8[j] && s2[j - 1] > s2[j]);
+  // the lane below's last record (lane 0: the record before the tile)
+  uint32_t pg = wave_shr1_u32(0u, (uint32_t)g8[kTileIpt - 1]);
+  int64_t pst = wave_shr1((uint64_t)0, (uint64_t)s2[kTileIpt - 1]);
+  bool have = lane > 0;
+  if (lane == 0 && base > 0) {
+    pg = gpu[base - 1];
+    const ClockDev kp = (int)pg < n_gpus ? clk[pg] : ClockDev{0, 0, 0};
+    pst = align_time(start[base - 1], kp);
+    have = true;
   }
-  if (i > 0 && i < n) bad_order = pg > g || (pg == g && ps > s2);
-  if (__ballot(bad_order) != 0 && lane == 0) atomicOr(unsorted, 1u);
+  if (have && k0 < n)
+    bad = bad || pg > g8[0] || (pg == g8[0] && pst > s2[0]);
+  if (__ballot(bad) != 0 && lane == 0) atomicOr(unsorted, 1u);
   status_or(status, st);
 }
 
@@ -379,7 +447,9 @@ extern "C" int chopper_align(const chopper_records* rec,
   CHOPPER_HIP(launch("align_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
                      L.counts, (int64_t)4, 0u));
   CHOPPER_HIP(launch("align_transform_records", k_transform_records,
-                     grid_for(n, kBlock), dim3(kBlock), s, n, G, rec->gpu,
+                     dim3((unsigned)ceil_div(n, (int64_t)kWaveTile *
+                                                    kWavesPerBlock)),
+                     dim3(kBlock), s, n, G, rec->gpu,
                      rec->stream, rec->cls, rec->start_ns, rec->end_ns,
                      (const ClockDev*)L.clk, start_out, end_out, L.pres_s,
                      L.pres_k, L.counts + 2, status));
