@@ -31,6 +31,7 @@ struct Runs {
   const int64_t* pl;      // active time of the segment before the run
   // comm runs only, at dense index voff[g] + (j - first comm run of g):
   const int64_t* pov;     // exclusive prefix of overlapped time
+  const int64_t* ovc;     // overlapped time inside the run
   const int64_t* fcrs;    // compute-active time before the run's start
   const uint32_t* voff;   // [G + 1] first dense index of every gpu
   BIndex X;               // bucket index of the run starts per segment
@@ -58,49 +59,58 @@ __device__ inline void segs_to_lds(BSeg* s_seg, const BSeg* segs, int nseg) {
 // comm-active time m and the time where both are, o; both-active time
 // before t is the overlap of the comm runs before t plus, inside the comm
 // run holding t, the compute-active time up to t.
-__device__ inline void window(const Runs& R, const BSeg& Pc, const BSeg& Pm,
-                              uint32_t vg, int64_t a, int64_t b, int64_t* out) {
-  if (b <= a) {
-    out[0] = out[1] = out[2] = out[3] = 0;
-    return;
+template <int K>
+__device__ inline void window_k(const Runs& R, const BSeg (&Pc)[K],
+                                const BSeg (&Pm)[K], const uint32_t (&vg)[K],
+                                const int64_t (&a)[K], const int64_t (&b)[K],
+                                int64_t (&out)[K][4]) {
+  // compute and comm searches at both ends of every window, in lockstep
+  int64_t lo[4 * K], hi[4 * K], t[4 * K];
+#pragma unroll
+  for (int q = 0; q < K; ++q) {
+    t[4 * q + 0] = a[q];
+    t[4 * q + 1] = b[q];
+    t[4 * q + 2] = a[q];
+    t[4 * q + 3] = b[q];
+    bi_range(R.X, Pc[q], a[q], &lo[4 * q + 0], &hi[4 * q + 0]);
+    bi_range(R.X, Pc[q], b[q], &lo[4 * q + 1], &hi[4 * q + 1]);
+    bi_range(R.X, Pm[q], a[q], &lo[4 * q + 2], &hi[4 * q + 2]);
+    bi_range(R.X, Pm[q], b[q], &lo[4 * q + 3], &hi[4 * q + 3]);
   }
-  // compute and comm searches at both ends
-  int64_t lo[4], hi[4];
-  const int64_t t[4] = {a, b, a, b};
-  bi_range(R.X, Pc, a, &lo[0], &hi[0]);
-  bi_range(R.X, Pc, b, &lo[1], &hi[1]);
-  bi_range(R.X, Pm, a, &lo[2], &hi[2]);
-  bi_range(R.X, Pm, b, &lo[3], &hi[3]);
-  bsearch_k<4>(R.rs, lo, hi, t);
-  const int64_t ca = F_at(R, Pc, lo[0], a), cb = F_at(R, Pc, lo[1], b);
-  const int64_t ma = F_at(R, Pm, lo[2], a), mb = F_at(R, Pm, lo[3], b);
-  // both-active time before a and before b
-  int64_t qlo[2], qhi[2], qt[2], base[2];
-  bool some[2];
-  for (int k = 0; k < 2; ++k) {
-    const int64_t jm = lo[2 + k] - 1;
-    const int64_t tk = k ? b : a;
-    some[k] = jm >= (int64_t)Pm.sb;    // a comm run starts at or before t
-    base[k] = 0;
-    qt[k] = tk;
-    qlo[k] = qhi[k] = Pc.sb;
-    if (!some[k]) continue;
-    const int64_t end = R.re[jm] < tk ? R.re[jm] : tk;
-    const int64_t v = (int64_t)vg + (jm - (int64_t)Pm.sb);
-    base[k] = R.pov[v] - R.pov[vg] - R.fcrs[v];
-    qt[k] = end;
-    bi_range(R.X, Pc, end, &qlo[k], &qhi[k]);
+  bsearch_k<4 * K>(R.rs, lo, hi, t);
+#pragma unroll
+  for (int q = 0; q < K; ++q) {
+    const int64_t* l = lo + 4 * q;
+    const int64_t ca = F_at(R, Pc[q], l[0], a[q]), cb = F_at(R, Pc[q], l[1], b[q]);
+    const int64_t ma = F_at(R, Pm[q], l[2], a[q]), mb = F_at(R, Pm[q], l[3], b[q]);
+    // both-active time before t: the overlap of the comm runs before the
+    // one holding t, plus inside it either its whole overlap (t past its
+    // end) or the compute-active time from its start to t -- F_c(t), known
+    // above
+    int64_t ob[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int64_t jm = l[2 + k] - 1;
+      const int64_t tk = k ? b[q] : a[q];
+      ob[k] = 0;
+      if (jm < (int64_t)Pm[q].sb) continue;   // no comm run at or before t
+      const int64_t v = (int64_t)vg[q] + (jm - (int64_t)Pm[q].sb);
+      const int64_t before = R.pov[v] - R.pov[vg[q]];
+      ob[k] = before +
+              (tk < R.re[jm] ? (k ? cb : ca) - R.fcrs[v] : R.ovc[v]);
+    }
+    const int64_t c = cb - ca, m = mb - ma, o = ob[1] - ob[0];
+    if (b[q] <= a[q]) {
+      out[q][0] = out[q][1] = out[q][2] = out[q][3] = 0;
+    } else {
+      out[q][0] = c - o;
+      out[q][1] = m - o;
+      out[q][2] = o;
+      out[q][3] = (b[q] - a[q]) - c - m + o;
+    }
   }
-  bsearch_k<2>(R.rs, qlo, qhi, qt);
-  int64_t ob[2];
-  for (int k = 0; k < 2; ++k)
-    ob[k] = some[k] ? base[k] + F_at(R, Pc, qlo[k], qt[k]) : 0;
-  const int64_t c = cb - ca, m = mb - ma, o = ob[1] - ob[0];
-  out[0] = c - o;
-  out[1] = m - o;
-  out[2] = o;
-  out[3] = (b - a) - c - m + o;
 }
+
 
 // ---------------- union runs -----------------------------------------------
 // Tiles of kOvTile korder positions, one block each; the block's four waves
@@ -581,18 +591,41 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
     if ((m_in >> j) & 1u) ovl[r[j]] = o[j];
 }
 
+// Window values of every marker, one per thread (more markers per thread
+// in lockstep measured slower).
+constexpr int kMarkPerThread = 1;
+
 __global__ __launch_bounds__(kBlock) void k_overlap_markers(
     int64_t nm, int G, const uint8_t* mgpu, const int64_t* ms,
     const int64_t* me, Runs R, int64_t* mwin) {
   __shared__ BSeg s_seg[kSegs];
   segs_to_lds(s_seg, R.X.seg, 2 * G);
-  const int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (j >= nm) return;
-  int64_t w[4] = {0, 0, 0, 0};
-  const uint32_t g = mgpu[j];
-  if ((int)g < G)
-    window(R, s_seg[g * 2u], s_seg[g * 2u + 1u], R.voff[g], ms[j], me[j], w);
-  for (int z = 0; z < 4; ++z) mwin[4 * j + z] = w[z];
+  const int64_t j0 =
+      (int64_t)blockIdx.x * kBlock * kMarkPerThread + threadIdx.x;
+  BSeg Pc[kMarkPerThread], Pm[kMarkPerThread];
+  uint32_t vg[kMarkPerThread];
+  int64_t a[kMarkPerThread], b[kMarkPerThread];
+  bool use[kMarkPerThread];
+#pragma unroll
+  for (int q = 0; q < kMarkPerThread; ++q) {
+    const int64_t j = j0 + (int64_t)q * kBlock;
+    const uint32_t g = j < nm ? mgpu[j] : 0xFFFFFFFFu;
+    use[q] = j < nm && g < (uint32_t)G;
+    const uint32_t gg = use[q] ? g : 0u;
+    Pc[q] = s_seg[gg * 2u];
+    Pm[q] = s_seg[gg * 2u + 1u];
+    vg[q] = R.voff[gg];
+    a[q] = use[q] ? ms[j] : 0;
+    b[q] = use[q] ? me[j] : 0;     // empty window when unused
+  }
+  int64_t w[kMarkPerThread][4];
+  window_k<kMarkPerThread>(R, Pc, Pm, vg, a, b, w);
+#pragma unroll
+  for (int q = 0; q < kMarkPerThread; ++q) {
+    const int64_t j = j0 + (int64_t)q * kBlock;
+    if (j >= nm) continue;
+    for (int z = 0; z < 4; ++z) mwin[4 * j + z] = use[q] ? w[q][z] : 0;
+  }
 }
 
 // GPU window: the first run of a (gpu, kind) segment starts at its smallest
@@ -609,11 +642,14 @@ __global__ void k_overlap_gpus(int G, Runs R, int64_t* gwin) {
     }
   }
   if (a == kI64Max) a = b = 0;
-  int64_t w[4];
-  window(R, R.X.seg[g * 2], R.X.seg[g * 2 + 1], R.voff[g], a, b, w);
+  const BSeg Pc[1] = {R.X.seg[g * 2]}, Pm[1] = {R.X.seg[g * 2 + 1]};
+  const uint32_t vg[1] = {R.voff[g]};
+  const int64_t aa[1] = {a}, bb[1] = {b};
+  int64_t w[1][4];
+  window_k<1>(R, Pc, Pm, vg, aa, bb, w);
   gwin[6 * g + 0] = a;
   gwin[6 * g + 1] = b;
-  for (int z = 0; z < 4; ++z) gwin[6 * g + 2 + z] = w[z];
+  for (int z = 0; z < 4; ++z) gwin[6 * g + 2 + z] = w[0][z];
 }
 
 // ---------------- bubbles ----------------------------------------------------
@@ -846,7 +882,7 @@ extern "C" int chopper_overlap(const chopper_records* rec,
   // bucket index of the run starts of every (gpu, kind)
   CHOPPER_HIP(bindex_build(L.rs, L.rseg, n, L.nruns, L.rbeg, L.rend, 1, kSegs,
                            L.bsegs, L.btable, L.btable_cap, L.btmp, s));
-  Runs R{L.rs, L.re, L.pl, L.pov, L.fcrs, L.voff,
+  Runs R{L.rs, L.re, L.pl, L.pov, L.ovc, L.fcrs, L.voff,
          BIndex{L.rs, L.bsegs, L.btable}};
   CHOPPER_HIP(launch("ov_comm_voff", k_comm_voff, dim3(1), dim3(64), s, G,
                      (const BSeg*)L.bsegs, L.voff));
@@ -864,7 +900,8 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                        start_al, end_al, R, ovl_out));
   }
   if (nm > 0)
-    CHOPPER_HIP(launch("ov_markers", k_overlap_markers, grid_for(nm, kBlock),
+    CHOPPER_HIP(launch("ov_markers", k_overlap_markers,
+                       grid_for(nm, kBlock * kMarkPerThread),
                        dim3(kBlock), s, nm, G, mk->gpu, mstart_al, mend_al, R,
                        mwin_out));
   CHOPPER_HIP(launch("ov_gpus", k_overlap_gpus, grid_for(G, kBlock),
