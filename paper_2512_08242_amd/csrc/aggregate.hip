@@ -772,14 +772,449 @@ __global__ void k_agg_offsets_fast(int L, int64_t ntiles,
   const int64_t tot =
       (int64_t)*total + (workload ? __popc(flags[1] & 3u) : 0);
   level_offset[L] = tot;
-  // the counts are the row counts only when the fast path applies
-  if (flags[0] == 0 && tot > cap)
+  // the counts are the row counts only when the fast path applies (and,
+  // for the natural tiles, when the input order qualified)
+  if (flags[0] == 0 && flags[2] == 0 && tot > cap)
     atomicOr(status, (uint32_t)CHOPPER_ST_ROWS_OVERFLOW);
 }
 
+// ------------------------------------------------------------ input order
+// A profiler writes each GPU's records together and in start order.  For
+// such input the (gpu, kind, start') order is the input order with every
+// GPU's communication records moved after its compute records, so the fast
+// path can read all columns in input order instead of through korder, where
+// each sparse communication record would pull a whole cache line of every
+// column.  A wave tile then covers consecutive input positions of one GPU
+// and regroups its items by kind in LDS (compute first, order kept), which
+// yields per (gpu, kind) exactly the item sequence of the korder tiles.
+//
+// Tiles: the natural tiles of kWaveTile positions, cut at GPU boundaries;
+// GPU g owns tiles tb[g] .. tb[g + 1] - 1.  Head counts of a level are laid
+// out as (gpu, kind, tile), so one exclusive scan numbers the rows in
+// (gpu, kind, first record) order, as on the korder tiles.
+struct NatGeom {
+  const uint32_t* tb;   // [G + 1] first tile of every GPU; tb[G] = tiles
+  const uint8_t* tg;    // [tiles] GPU of every tile
+  const uint32_t* gs;   // [G] first input position of the GPU, kNone: none
+  const uint32_t* ge;   // [G] one past its last position
+  const int32_t* lp;    // [2][lps] last kind-k position before natural
+                        // tile t, -1 if none
+  const uint32_t* bad;  // nonzero: the input order does not qualify
+  int64_t nnt;          // natural tiles
+  int64_t lps;          // row stride of lp (nnt rounded up to kLpChunk)
+  int G;
+};
+
+struct NatTile {
+  uint32_t g;
+  int64_t base;
+  int tile_n;
+  int64_t prev[2];      // last kind-k position of the GPU before the tile
+  uint32_t tbg, cg, tl; // GPU's first tile, its tile count, tile - tbg
+};
+
+// Geometry of tile tt; false past the last tile.
+__device__ inline bool nat_tile(const NatGeom& N, int64_t tt, NatTile& T) {
+  if (tt >= (int64_t)N.tb[N.G]) return false;
+  const uint32_t g = N.tg[tt];
+  const int64_t gs = N.gs[g], ge = N.ge[g];
+  T.g = g;
+  T.tbg = N.tb[g];
+  T.cg = N.tb[g + 1] - T.tbg;
+  T.tl = (uint32_t)(tt - T.tbg);
+  const int64_t nt = gs / kWaveTile + T.tl;
+  const int64_t a = nt * kWaveTile;
+  T.base = a > gs ? a : gs;
+  const int64_t e = a + kWaveTile < ge ? a + kWaveTile : ge;
+  T.tile_n = (int)(e - T.base);
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    int64_t pv = -1;
+    if (T.base > gs) {
+      pv = N.lp[(int64_t)k * N.lps + nt];
+      if (pv < gs) pv = -1;
+    }
+    T.prev[k] = pv;
+  }
+  return true;
+}
+
+// Kind regrouping of a tile: item q (striped) goes to LDS slot dst[j]
+// (padded), compute items first; n0 = compute items.
+__device__ inline void nat_regroup(const bool (&valid)[kAggIpt],
+                                   const uint32_t (&kind)[kAggIpt], int lane,
+                                   uint32_t (&dst)[kAggIpt], int* n0_out) {
+  uint64_t m0[kAggIpt], m1[kAggIpt];
+  uint32_t n0 = 0;
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    m0[j] = __ballot(valid[j] && kind[j] == 0u);
+    m1[j] = __ballot(valid[j] && kind[j] != 0u);
+    n0 += (uint32_t)__popcll(m0[j]);
+  }
+  uint32_t c0 = 0, c1 = n0;
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    uint32_t d = (uint32_t)(j * kWave + lane);
+    if (valid[j]) d = kind[j] == 0u ? c0 + lanes_below(m0[j])
+                                    : c1 + lanes_below(m1[j]);
+    dst[j] = (uint32_t)pad8((int)d);
+    c0 += (uint32_t)__popcll(m0[j]);
+    c1 += (uint32_t)__popcll(m1[j]);
+  }
+  *n0_out = (int)n0;
+}
+
+template <typename T>
+__device__ inline void wave_regroup_to_blocked(T* slice, T (&v)[kAggIpt],
+                                               const uint32_t (&dst)[kAggIpt],
+                                               int lane) {
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) slice[dst[j]] = v[j];
+  wave_sync();
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) v[j] = slice[pad8(lane * kAggIpt + j)];
+  wave_sync();
+}
+
+template <typename T>
+__device__ inline void wave_blocked_to_regrouped(
+    T* slice, T (&v)[kAggIpt], const uint32_t (&dst)[kAggIpt], int lane) {
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) slice[pad8(lane * kAggIpt + j)] = v[j];
+  wave_sync();
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) v[j] = slice[dst[j]];
+  wave_sync();
+}
+
+// Per natural tile: last position of each kind, the first position of every
+// GPU, and whether the order qualifies (GPU ids never decrease, start'
+// never decreases inside a GPU, every id below G).  Lane l reads positions
+// 8l .. 8l + 7 of the tile, with vector loads when the columns allow.
+__global__ __launch_bounds__(kBlock) void k_nat_pre(
+    int64_t n, int G, const uint8_t* gpu, const uint8_t* cls,
+    const int64_t* start, int64_t nnt, int64_t lps, int32_t* lpraw,
+    uint32_t* gs, uint32_t* bad) {
+  const int lane = lane_id();
+  const int64_t nt =
+      (int64_t)blockIdx.x * kWavesPerBlock + (int64_t)(threadIdx.x / kWave);
+  if (nt >= nnt) return;
+  const int64_t base = nt * kWaveTile;
+  const int64_t p0 = base + (int64_t)lane * kAggIpt;
+  uint32_t g[kAggIpt], k[kAggIpt];
+  int64_t s[kAggIpt];
+  const bool vec = base + kWaveTile <= n && ((uintptr_t)gpu & 7) == 0 &&
+                   ((uintptr_t)cls & 7) == 0 && ((uintptr_t)start & 15) == 0;
+  if (vec) {
+    const uint64_t gw = *(const uint64_t*)(gpu + p0);
+    const uint64_t cw = *(const uint64_t*)(cls + p0);
+#pragma unroll
+    for (int j = 0; j < kAggIpt; j += 2) {
+      const longlong2 v = *(const longlong2*)(start + p0 + j);
+      s[j] = v.x;
+      s[j + 1] = v.y;
+    }
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) {
+      g[j] = (uint32_t)(gw >> (8 * j)) & 0xFFu;
+      k[j] = (uint32_t)kind_of((uint32_t)(cw >> (8 * j)) & 0xFFu);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) {
+      const int64_t p = p0 + j;
+      g[j] = p < n ? (uint32_t)gpu[p] : 0u;
+      k[j] = p < n ? (uint32_t)kind_of(cls[p]) : 0u;
+      s[j] = p < n ? start[p] : 0;
+    }
+  }
+  // the item before each lane's first: the lane below, or the tile's
+  // predecessor for lane 0
+  uint32_t pg = wave_shr1_u32(0u, g[kAggIpt - 1]);
+  int64_t ps = dpp_any<kDppWaveShr1, 0xF>((int64_t)0, s[kAggIpt - 1]);
+  if (lane == 0 && base > 0) {
+    pg = gpu[base - 1];
+    ps = start[base - 1];
+  }
+  bool wrong = false;
+  int32_t last[2] = {-1, -1};
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int64_t p = p0 + j;
+    if (p < n) {
+      if (g[j] >= (uint32_t)G) wrong = true;
+      if (p > 0 && (g[j] < pg || (g[j] == pg && s[j] < ps))) wrong = true;
+      if ((p == 0 || g[j] != pg) && g[j] < (uint32_t)G) gs[g[j]] = (uint32_t)p;
+      last[k[j] ? 1 : 0] = (int32_t)p;
+    }
+    pg = g[j];
+    ps = s[j];
+  }
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const uint64_t m = __ballot(last[q] >= 0);
+    const int32_t v =
+        m ? __builtin_amdgcn_readlane(last[q], 63 - __clzll((long long)m))
+          : -1;
+    if (lane == 0) lpraw[(int64_t)q * lps + nt] = v;
+  }
+  if (__ballot(wrong) != 0 && lane == 0) atomicOr(bad, 1u);
+}
+
+// One block: GPU ranges, tile offsets and the GPU of every tile, and the
+// exclusive running maximum of the last-position table.
+constexpr int kLpChunk = 32;      // table entries per thread and pass
+__global__ __launch_bounds__(1024) void k_nat_tiles(
+    int64_t n, int G, int64_t nnt, int64_t lps, const int32_t* lpraw,
+    int32_t* lp, const uint32_t* gs, uint32_t* ge, uint32_t* tb, uint8_t* tg,
+    const uint32_t* bad) {
+  if (*bad) return;
+  __shared__ uint32_t s_c[256];
+  __shared__ uint32_t s_tb[257];
+  __shared__ int32_t s_w[2][1024 / kWave];
+  const int t = (int)threadIdx.x, lane = lane_id(), w = t / kWave;
+  if (t < G) {
+    const uint32_t a = gs[t];
+    uint32_t e = (uint32_t)n;
+    if (a != kNone) {
+      for (int h = t + 1; h < G; ++h) {
+        const uint32_t b = gs[h];
+        if (b != kNone) {
+          e = b;
+          break;
+        }
+      }
+    }
+    ge[t] = a == kNone ? kNone : e;
+    s_c[t] = a == kNone ? 0u
+                        : (e - 1u) / (uint32_t)kWaveTile -
+                              a / (uint32_t)kWaveTile + 1u;
+  }
+  __syncthreads();
+  if (w == 0) {
+    uint32_t carry = 0;
+    for (int b0 = 0; b0 < G; b0 += kWave) {
+      const uint32_t v = b0 + lane < G ? s_c[b0 + lane] : 0u;
+      const uint32_t incl = wave_incl(v, OpAdd(), 0u);
+      if (b0 + lane < G) {
+        tb[b0 + lane] = carry + incl - v;
+        s_tb[b0 + lane] = carry + incl - v;
+      }
+      carry += (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+    }
+    if (lane == 0) {
+      tb[G] = carry;
+      s_tb[G] = carry;
+    }
+  }
+  __syncthreads();
+  for (int g = 0; g < G; ++g)
+    for (uint32_t i = s_tb[g] + (uint32_t)t; i < s_tb[g + 1]; i += 1024)
+      tg[i] = (uint8_t)g;
+  // both kinds at once; kLpChunk consecutive entries per thread
+  OpMax op;
+  int32_t carry[2] = {-1, -1};
+  for (int64_t b0 = 0; b0 < nnt; b0 += 1024 * kLpChunk) {
+    const int64_t i0 = b0 + (int64_t)t * kLpChunk;
+    int32_t v[2][kLpChunk];
+    int32_t acc[2] = {-1, -1};
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+#pragma unroll
+      for (int j = 0; j < kLpChunk; j += 4) {
+        int4 x = make_int4(-1, -1, -1, -1);
+        if (i0 + j < nnt) x = *(const int4*)(lpraw + (int64_t)q * lps + i0 + j);
+        v[q][j] = i0 + j < nnt ? x.x : -1;
+        v[q][j + 1] = i0 + j + 1 < nnt ? x.y : -1;
+        v[q][j + 2] = i0 + j + 2 < nnt ? x.z : -1;
+        v[q][j + 3] = i0 + j + 3 < nnt ? x.w : -1;
+      }
+#pragma unroll
+      for (int j = 0; j < kLpChunk; ++j) acc[q] = op(acc[q], v[q][j]);
+    }
+    int32_t incl[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      incl[q] = wave_incl(acc[q], op, (int32_t)-1);
+      if (lane == kWave - 1) s_w[q][w] = incl[q];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      int32_t pre = carry[q], tot = carry[q];
+      for (int r = 0; r < 1024 / kWave; ++r) {
+        if (r < w) pre = op(pre, s_w[q][r]);
+        tot = op(tot, s_w[q][r]);
+      }
+      pre = op(pre, wave_shr1_any((int32_t)-1, incl[q]));
+#pragma unroll
+      for (int j = 0; j < kLpChunk; j += 4) {
+        int4 x;
+        x.x = pre;
+        pre = op(pre, v[q][j]);
+        x.y = pre;
+        pre = op(pre, v[q][j + 1]);
+        x.z = pre;
+        pre = op(pre, v[q][j + 2]);
+        x.w = pre;
+        pre = op(pre, v[q][j + 3]);
+        if (i0 + j < nnt) *(int4*)(lp + (int64_t)q * lps + i0 + j) = x;
+      }
+      carry[q] = tot;
+    }
+    __syncthreads();
+  }
+}
+
+// Item of the natural tiles: gpu * 2 + kind and path of input position i.
+template <int MaxD>
+__device__ inline void nat_item(const RecSrc& S, int64_t i, uint32_t g, int D,
+                                uint32_t& gk, uint32_t (&p)[MaxD]) {
+  gk = g * 2u + (uint32_t)kind_of(S.cls[i]);
+#pragma unroll
+  for (int l = 0; l < MaxD; ++l) {
+    const int ll = l < D ? l : (D > 0 ? D - 1 : 0);
+    const uint32_t v = D > 0 ? S.idx[(int64_t)ll * S.n + i] : kNone;
+    p[l] = l < D ? v : kNone;
+  }
+}
+
+// Heads pass over the natural tiles: per level and kind the groups that
+// start in the tile, at tilecnt[(li - lv0) * stride + 2 * tbg + k * cg + tl];
+// entries past the last tile are zeroed.  Flags as in k_agg_heads.
+template <int MaxD>
+__global__ __launch_bounds__(kBlock) void k_agg_heads_nat(
+    RecSrc S, NatGeom N, uint32_t act, int lv0, int lv1, int D, int64_t M,
+    int64_t stride, uint32_t* tilecnt, uint32_t* flags, uint32_t* status) {
+  __shared__ uint32_t s_k[kWavesPerBlock][kSlice];
+  if (*N.bad) return;
+  const int lane = lane_id();
+  const int wv = (int)(threadIdx.x / kWave);
+  const int64_t tt = (int64_t)blockIdx.x * kWavesPerBlock + wv;
+  if (tt >= N.nnt + N.G) return;
+  NatTile T;
+  if (!nat_tile(N, tt, T)) {
+    if (lane <= lv1 - lv0) {
+      tilecnt[(int64_t)lane * stride + 2 * tt] = 0;
+      tilecnt[(int64_t)lane * stride + 2 * tt + 1] = 0;
+    }
+    return;
+  }
+  uint32_t* sk = s_k[wv];
+  uint32_t gk[kAggIpt], p[kAggIpt][MaxD], kind[kAggIpt], dst[kAggIpt];
+  bool valid[kAggIpt];
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int q = j * kWave + lane;
+    valid[j] = q < T.tile_n;
+    nat_item<MaxD>(S, T.base + (valid[j] ? q : 0), T.g, D, gk[j], p[j]);
+    kind[j] = gk[j] & 1u;
+  }
+  int n0;
+  nat_regroup(valid, kind, lane, dst, &n0);
+  wave_regroup_to_blocked(sk, gk, dst, lane);
+#pragma unroll
+  for (int l = 0; l < MaxD; ++l) {
+    uint32_t x[kAggIpt];
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) x[j] = p[j][l];
+    wave_regroup_to_blocked(sk, x, dst, lane);
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) p[j][l] = x[j];
+  }
+  // the items before the tile, one per kind (same GPU)
+  uint32_t qgk[2], qp[2][MaxD];
+  bool qv[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    qv[k] = T.prev[k] >= 0;
+    nat_item<MaxD>(S, qv[k] ? T.prev[k] : T.base, T.g, D, qgk[k], qp[k]);
+  }
+  uint64_t cpk[2] = {0, 0};   // 4-bit head counts per level, per kind
+  bool notinc = false, conflict = false;
+  uint32_t kinds = 0;
+  // previous item in the regrouped order: lane below for j == 0
+  uint32_t cp[MaxD], cgk;
+#pragma unroll
+  for (int l = 0; l < MaxD; ++l) cp[l] = wave_shr1_u32(0u, p[kAggIpt - 1][l]);
+  cgk = wave_shr1_u32(0u, gk[kAggIpt - 1]);
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int v = lane * kAggIpt + j;
+    const bool vv = v < T.tile_n;
+    const uint32_t kd = v < n0 ? 0u : 1u;
+    uint32_t pp[MaxD], pgk;
+    bool pvalid = true;
+    if (v == n0 || v == 0) {
+      const int k = v == n0 ? 1 : 0;
+      pvalid = qv[k];
+#pragma unroll
+      for (int l = 0; l < MaxD; ++l) pp[l] = qp[k][l];
+      pgk = qgk[k];
+    } else {
+#pragma unroll
+      for (int l = 0; l < MaxD; ++l) pp[l] = cp[l];
+      pgk = cgk;
+    }
+#pragma unroll
+    for (int l = 0; l < MaxD; ++l) cp[l] = p[j][l];
+    cgk = gk[j];
+    uint32_t slot = kNone, pslot = kNone;
+    bool eq = true;
+#pragma unroll
+    for (int li = 0; li < MaxD; ++li) {
+      slot = p[j][li] != kNone ? p[j][li] : slot;
+      pslot = pp[li] != kNone ? pp[li] : pslot;
+      eq = eq && p[j][li] == pp[li];
+      if (li >= D || li < lv0 || li > lv1 || !((act >> li) & 1u)) continue;
+      const uint32_t key = slot_key(slot, M, gk[j]);
+      const uint32_t pkey = pvalid ? slot_key(pslot, M, pgk) : kNone;
+      if (vv && key == kNone) notinc = true;
+      if (key != pkey && key != kNone) {
+        cpk[kd] += (vv ? 1ull : 0ull) << (4 * li);
+        const int64_t ok = key >= 2 * M ? -1 : (int64_t)key;
+        const int64_t opk = pkey >= 2 * M ? -1 : (int64_t)pkey;
+        if (vv && pvalid && pgk == gk[j] && ok <= opk) notinc = true;
+      } else if (vv && pvalid && key == pkey && key != kNone && !eq) {
+        conflict = true;
+      }
+    }
+    if (vv && D >= lv0 && D <= lv1 && ((act >> D) & 1u) &&
+        (!pvalid || gk[j] != pgk)) {
+      cpk[kd] += 1ull << (4 * D);
+      kinds |= 1u << kd;
+    }
+  }
+  for (int li = lv0; li <= lv1; ++li) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const uint32_t c = (uint32_t)(cpk[k] >> (4 * li)) & 15u;
+      uint32_t tot = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        tot += (uint32_t)__popcll(__ballot((c >> b) & 1u)) << b;
+      if (lane == 0)
+        tilecnt[(int64_t)(li - lv0) * stride + 2 * (int64_t)T.tbg +
+                (int64_t)k * T.cg + T.tl] = tot;
+    }
+  }
+  if (__ballot(notinc) != 0 && lane == 0) atomicOr(&flags[0], 1u);
+  if (__ballot(conflict) != 0 && lane == 0)
+    atomicOr(status, (uint32_t)CHOPPER_ST_PATH_CONFLICT);
+  const uint32_t kk = (__ballot(kinds & 1u) != 0 ? 1u : 0u) |
+                      (__ballot(kinds & 2u) != 0 ? 2u : 0u);
+  if (lane == 0 && kk &&
+      (__atomic_load_n(&flags[1], __ATOMIC_RELAXED) & kk) != kk)
+    atomicOr(&flags[1], kk);
+}
+
 // Piece structure of one level over a wave tile (blocked arrangement: lane
-// holds items lane * 8 + j).  Pieces are maximal runs of equal keys; the
-// tile's first piece may continue a row of an earlier tile (c0 = 1).
+// holds items lane * 8 + j).  Pieces are maximal runs of equal keys.  Items
+// [0, n0) and [n0, tile_n) are two separate runs of rows (the two kinds of
+// a natural tile; n0 = tile_n on korder tiles): rows r0 + i for the pieces
+// of the first, r1 + i for the second.  The first piece of each may continue
+// a row of an earlier tile (c0, c1).
 struct LevelTile {
   uint32_t m_head;    // item starts a piece (tile start and invalid items too)
   uint32_t m_hv;      // ... and is valid
@@ -787,28 +1222,31 @@ struct LevelTile {
   uint32_t m_real;    // valid item starts a group (key differs from previous)
   uint32_t pfx;       // pieces started in the lanes below
   uint32_t NP;        // pieces in the tile
-  uint32_t c0;        // the first piece continues an earlier row
-  int64_t r0;         // row of the tile's first new group
+  uint32_t NP0;       // pieces of the first run
+  uint32_t c0, c1;    // the run's first piece continues an earlier row
+  int64_t r0, r1;     // row of the run's first new group
   uint32_t before;    // items of the lane before its first piece head
   WaveSegMasks masks; // lane segment flags for wave scans
 };
 
 // slot[j]: LDS slot of item j's value -- its piece index when it ends a
-// piece, else a junk slot of its own lane
+// piece, else a junk slot of its own lane.  prev0 / prev1: keys of the items
+// before each run (kNone: none).
 __device__ inline void level_tile(const uint32_t (&key)[kAggIpt],
-                                  uint32_t tile_prev, int tile_n, int lane,
-                                  int64_t r0, LevelTile& T,
-                                  uint32_t (&slot)[kAggIpt]) {
+                                  uint32_t prev0, uint32_t prev1, int n0,
+                                  int tile_n, int lane, int64_t r0, int64_t r1,
+                                  LevelTile& T, uint32_t (&slot)[kAggIpt]) {
   uint32_t m_valid = 0, m_real = 0, m_head = 0;
-  uint32_t prev = wave_shr1_u32(tile_prev, key[kAggIpt - 1]);
+  uint32_t prev = wave_shr1_u32(prev0, key[kAggIpt - 1]);
 #pragma unroll
   for (int j = 0; j < kAggIpt; ++j) {
     const int q = lane * kAggIpt + j;
     const bool valid = q < tile_n;
     const uint32_t k = key[j];
+    if (q == n0) prev = prev1;
     if (valid) m_valid |= 1u << j;
     if (valid && k != prev) m_real |= 1u << j;
-    if (!valid || q == 0 || k != prev) m_head |= 1u << j;
+    if (!valid || q == 0 || q == n0 || k != prev) m_head |= 1u << j;
     prev = k;
   }
   const uint64_t h0 = __ballot(m_head & 1u);
@@ -818,11 +1256,26 @@ __device__ inline void level_tile(const uint32_t (&key)[kAggIpt],
   T.m_hv = m_head & m_valid;
   T.m_real = m_real;
   T.m_last = m_valid & ((m_head >> 1) | (next0 << (kAggIpt - 1)));
-  T.pfx = wave_prefix_small<4>((uint32_t)__popc(T.m_hv));
-  T.NP = (uint32_t)__builtin_amdgcn_readlane(
-      (int)(T.pfx + (uint32_t)__popc(T.m_hv)), kWave - 1);
-  T.c0 = __ballot(lane == 0 && !(m_real & 1u)) != 0 ? 1u : 0u;
+  const uint32_t hc = (uint32_t)__popc(T.m_hv);
+  T.pfx = wave_prefix_small<4>(hc);
+  T.NP = (uint32_t)__builtin_amdgcn_readlane((int)(T.pfx + hc), kWave - 1);
+  if (n0 >= tile_n) {
+    T.NP0 = T.NP;
+    T.c1 = 0;
+  } else {
+    // pieces that start below position n0, and whether the item there is
+    // a new group
+    const int ln = n0 / kAggIpt, jn = n0 % kAggIpt;
+    const uint32_t below =
+        T.pfx + (uint32_t)__popc(T.m_hv & ((1u << jn) - 1u));
+    T.NP0 = (uint32_t)__builtin_amdgcn_readlane((int)below, ln);
+    const uint32_t real_n =
+        (uint32_t)__builtin_amdgcn_readlane((int)((m_real >> jn) & 1u), ln);
+    T.c1 = real_n ? 0u : 1u;
+  }
+  T.c0 = n0 > 0 && __ballot(lane == 0 && !(m_real & 1u)) != 0 ? 1u : 0u;
   T.r0 = r0;
+  T.r1 = r1;
   T.before = m_head ? (uint32_t)(__ffs(m_head) - 1) : (uint32_t)kAggIpt;
   T.masks = wave_seg_masks(m_head != 0);
 #pragma unroll
@@ -831,6 +1284,15 @@ __device__ inline void level_tile(const uint32_t (&key)[kAggIpt],
         T.pfx + (uint32_t)__popc(T.m_hv & ((2u << j) - 1u)) - 1u;
     slot[j] = ((T.m_last >> j) & 1u) ? idx : (uint32_t)(kWaveTile + lane);
   }
+}
+
+// Row of piece q, or -1 when it continues a row of an earlier tile.
+__device__ inline int64_t piece_row(const LevelTile& T, uint32_t q) {
+  const bool second = q >= T.NP0;
+  const uint32_t qi = second ? q - T.NP0 : q;
+  const uint32_t cc = second ? T.c1 : T.c0;
+  if (qi < cc) return -1;
+  return (second ? T.r1 : T.r0) + (int64_t)(qi - cc);
 }
 
 // Reduction of one level -- with kTwo also the next coarser one -- when
@@ -842,13 +1304,15 @@ __device__ inline void level_tile(const uint32_t (&key)[kAggIpt],
 // modulo 2^64), for both levels from the same prefix; tmin and tmax take a
 // segmented scan per level.  Piece values are written to LDS at the piece's
 // index, so that the stores of consecutive lanes go to consecutive rows.  A
-// tile's first piece may continue a row of an earlier tile: it goes to the
-// tile's overflow slot of its level (level li: slot w, level li - 1: slot
-// nwt + w).  Every valid item has a key here (the heads pass sends traces
-// with unkeyed items to the general path).
-template <int MaxD, typename Src, bool kTwo>
+// run's first piece may continue a row of an earlier tile: it goes to the
+// tile's overflow slot of its level (korder tiles: slot w of level li,
+// nwt + w of level li - 1; natural tiles: 2w + kind and 2nwt + 2w + kind).
+// Every valid item has a key here (the heads pass sends traces with unkeyed
+// items to the general path).  kNat: the natural tiles, items read in input
+// order and regrouped by kind on the way to the blocked arrangement.
+template <int MaxD, typename Src, bool kTwo, bool kNat>
 __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
-    Src src, int li, int D, int64_t M, const uint32_t* tilebase,
+    Src src, NatGeom N, int li, int D, int64_t M, const uint32_t* tilebase,
     const uint32_t* tilebase2, const int64_t* row0, RowsDev R, Overflow ovf,
     int64_t nwt) {
   __shared__ uint64_t s_v[kWavesPerBlock][kSlice];
@@ -856,51 +1320,108 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
   const int wv = (int)(threadIdx.x / kWave);
   const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wv;
   if (w >= nwt) return;
-  const int64_t cnt = src.count();
-  const int64_t base = w * kWaveTile;
-  if (base >= cnt) {
-    if (lane == 0) {
-      ovf.row[w] = kNone;
-      if (kTwo) ovf.row[nwt + w] = kNone;
+  int64_t base;
+  int tile_n;
+  NatTile NT;
+  if constexpr (kNat) {
+    if (!nat_tile(N, w, NT)) {
+      if (lane < 2) {
+        ovf.row[2 * w + lane] = kNone;
+        if (kTwo) ovf.row[2 * nwt + 2 * w + lane] = kNone;
+      }
+      return;
     }
-    return;
+    base = NT.base;
+    tile_n = NT.tile_n;
+  } else {
+    const int64_t cnt = src.count();
+    base = w * kWaveTile;
+    if (base >= cnt) {
+      if (lane == 0) {
+        ovf.row[w] = kNone;
+        if (kTwo) ovf.row[nwt + w] = kNone;
+      }
+      return;
+    }
+    tile_n =
+        (int)((cnt - base) < kWaveTile ? (cnt - base) : (int64_t)kWaveTile);
   }
-  const int tile_n =
-      (int)((cnt - base) < kWaveTile ? (cnt - base) : (int64_t)kWaveTile);
   const int li2 = li - 1;
   uint64_t* sv = s_v[wv];
   uint32_t* sk = (uint32_t*)sv;
   // striped items: source index, gpu * 2 + kind, path, keys
   uint32_t rs[kAggIpt], gk[kAggIpt], p[kAggIpt][MaxD];
-  uint32_t key[kAggIpt], key2[kAggIpt];
-  uint32_t tprev, tprev2 = kNone;
-  {
+  uint32_t key[kAggIpt], key2[kAggIpt], dst[kAggIpt];
+  uint32_t tprev[2] = {kNone, kNone}, tprev2[2] = {kNone, kNone};
+  int n0 = tile_n;
+  int64_t r0 = 0, r1 = 0, q0 = 0, q1 = 0;
+  if constexpr (kNat) {
+    bool valid[kAggIpt];
+    uint32_t kind[kAggIpt];
+#pragma unroll
+    for (int j = 0; j < kAggIpt; ++j) {
+      const int q = j * kWave + lane;
+      valid[j] = q < tile_n;
+      rs[j] = (uint32_t)(base + (valid[j] ? q : 0));
+      nat_item<MaxD>(src.S, rs[j], NT.g, D, gk[j], p[j]);
+      kind[j] = gk[j] & 1u;
+    }
+    nat_regroup(valid, kind, lane, dst, &n0);
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      if (NT.prev[k] < 0) continue;
+      uint32_t cgk, cp[MaxD];
+      nat_item<MaxD>(src.S, NT.prev[k], NT.g, D, cgk, cp);
+      tprev[k] = level_key<MaxD>(cp, cgk, li, D, M);
+      if (kTwo) tprev2[k] = level_key<MaxD>(cp, cgk, li2, D, M);
+    }
+    const int64_t e0 = 2 * (int64_t)NT.tbg + NT.tl;
+    const int64_t e1 = e0 + NT.cg;
+    r0 = tilebase[e0];
+    r1 = tilebase[e1];
+    if (kTwo) {
+      q0 = tilebase2[e0];
+      q1 = tilebase2[e1];
+    }
+  } else {
 #pragma unroll
     for (int j = 0; j < kAggIpt; ++j) {
       const int q = j * kWave + lane;
       gather_item<MaxD>(src, base + (q < tile_n ? q : 0), D, rs[j], gk[j],
                         p[j]);
+      dst[j] = 0;
     }
     uint32_t cr, cgk, cp[MaxD];
     gather_item<MaxD>(src, base > 0 ? base - 1 : 0, D, cr, cgk, cp);
-    tprev = base > 0 ? level_key<MaxD>(cp, cgk, li, D, M) : kNone;
-    if (kTwo) tprev2 = base > 0 ? level_key<MaxD>(cp, cgk, li2, D, M) : kNone;
-#pragma unroll
-    for (int j = 0; j < kAggIpt; ++j) {
-      const int q = j * kWave + lane;
-      key[j] = q < tile_n ? level_key<MaxD>(p[j], gk[j], li, D, M) : kNone;
-      key2[j] = kTwo && q < tile_n ? level_key<MaxD>(p[j], gk[j], li2, D, M)
-                                   : kNone;
-    }
+    tprev[0] = base > 0 ? level_key<MaxD>(cp, cgk, li, D, M) : kNone;
+    if (kTwo)
+      tprev2[0] = base > 0 ? level_key<MaxD>(cp, cgk, li2, D, M) : kNone;
+    r0 = (row0 ? *row0 : 0) + (int64_t)tilebase[w];
+    if (kTwo) q0 = (int64_t)tilebase2[w];
   }
-  wave_to_blocked(sk, key, lane);
-  if (kTwo) wave_to_blocked(sk, key2, lane);
+#pragma unroll
+  for (int j = 0; j < kAggIpt; ++j) {
+    const int q = j * kWave + lane;
+    key[j] = q < tile_n ? level_key<MaxD>(p[j], gk[j], li, D, M) : kNone;
+    key2[j] = kTwo && q < tile_n ? level_key<MaxD>(p[j], gk[j], li2, D, M)
+                                 : kNone;
+  }
+  auto blk32 = [&](uint32_t (&x)[kAggIpt]) {
+    if constexpr (kNat) wave_regroup_to_blocked(sk, x, dst, lane);
+    else wave_to_blocked(sk, x, lane);
+  };
+  auto blk64 = [&](uint64_t (&x)[kAggIpt]) {
+    if constexpr (kNat) wave_regroup_to_blocked(sv, x, dst, lane);
+    else wave_to_blocked(sv, x, lane);
+  };
+  blk32(key);
+  if (kTwo) blk32(key2);
   LevelTile T1, T2;
   uint32_t slot[kAggIpt], slot2[kAggIpt];
-  level_tile(key, tprev, tile_n, lane,
-             (row0 ? *row0 : 0) + (int64_t)tilebase[w], T1, slot);
+  level_tile(key, tprev[0], tprev[1], n0, tile_n, lane, r0, r1, T1, slot);
   if (kTwo)
-    level_tile(key2, tprev2, tile_n, lane, (int64_t)tilebase2[w], T2, slot2);
+    level_tile(key2, tprev2[0], tprev2[1], n0, tile_n, lane, q0, q1, T2,
+               slot2);
 
   // headers of the rows that start here, written from the striped items:
   // the row of every group head goes back through LDS
@@ -910,10 +1431,12 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     for (int j = 0; j < kAggIpt; ++j) {
       const uint32_t idx =
           T.pfx + (uint32_t)__popc(T.m_hv & ((2u << j) - 1u)) - 1u;
-      const int64_t row = T.r0 + (int64_t)idx - (int64_t)T.c0;
-      rw[j] = ((T.m_real >> j) & 1u) && row < R.cap ? (uint32_t)row : kNone;
+      const int64_t row = piece_row(T, idx);
+      rw[j] = ((T.m_real >> j) & 1u) && row >= 0 && row < R.cap
+                  ? (uint32_t)row : kNone;
     }
-    wave_to_striped(sk, rw, lane);
+    if constexpr (kNat) wave_blocked_to_regrouped(sk, rw, dst, lane);
+    else wave_to_striped(sk, rw, lane);
 #pragma unroll
     for (int j = 0; j < kAggIpt; ++j) {
       const uint32_t wr = rw[j];
@@ -930,32 +1453,42 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
   };
   headers(T1, li);
   if (kTwo) headers(T2, li2);
+  auto cont_row = [&](uint32_t c, int64_t r) -> uint32_t {
+    return c && r >= 1 && r - 1 < R.cap ? (uint32_t)(r - 1) : kNone;
+  };
   if (lane == 0) {
-    ovf.row[w] = T1.c0 && T1.r0 >= 1 && T1.r0 - 1 < R.cap
-                     ? (uint32_t)(T1.r0 - 1) : kNone;
-    if (kTwo)
-      ovf.row[nwt + w] = T2.c0 && T2.r0 >= 1 && T2.r0 - 1 < R.cap
-                             ? (uint32_t)(T2.r0 - 1) : kNone;
+    if constexpr (kNat) {
+      ovf.row[2 * w] = cont_row(T1.c0, T1.r0);
+      ovf.row[2 * w + 1] = cont_row(T1.c1, T1.r1);
+      if (kTwo) {
+        ovf.row[2 * nwt + 2 * w] = cont_row(T2.c0, T2.r0);
+        ovf.row[2 * nwt + 2 * w + 1] = cont_row(T2.c1, T2.r1);
+      }
+    } else {
+      ovf.row[w] = cont_row(T1.c0, T1.r0);
+      if (kTwo) ovf.row[nwt + w] = cont_row(T2.c0, T2.r0);
+    }
   }
   // byte offsets of the striped items (sizes are below 2^29 here)
   uint32_t off[kAggIpt];
 #pragma unroll
   for (int j = 0; j < kAggIpt; ++j) off[j] = rs[j] << 3;
 
-  // piece values at the slots -> rows (and the overflow slot)
+  // piece values at the slots -> rows (and the overflow slots)
   auto store_pieces = [&](const LevelTile& T, int64_t obase, int f,
                           bool diff) {
     uint64_t* col = row_column(R, f);
-    uint64_t* oslot = ovf.val + (int64_t)f * ovf.cap + obase + w;
+    uint64_t* oslot = ovf.val + (int64_t)f * ovf.cap + obase +
+                      (kNat ? 2 * w : w);
     wave_sync();
     for (uint32_t q = lane; q < T.NP; q += kWave) {
       uint64_t v = sv[q];
       if (diff && q > 0) v -= sv[q - 1];
-      if (q < T.c0) {
-        *oslot = v;
-      } else {
-        const int64_t row = T.r0 + (int64_t)(q - T.c0);
-        if (row < R.cap) col[row] = v;
+      const int64_t row = piece_row(T, q);
+      if (row < 0) {
+        oslot[q >= T.NP0 ? 1 : 0] = v;
+      } else if (row < R.cap) {
+        col[row] = v;
       }
     }
     wave_sync();
@@ -964,11 +1497,12 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
 #pragma unroll
     for (int j = 0; j < kAggIpt; ++j) sv[sl[j]] = x[j];
   };
+  const int64_t ob2 = kNat ? 2 * nwt : nwt;
   auto do_sum = [&](const uint64_t (&v)[kAggIpt], int f) {
     uint64_t x[kAggIpt];
 #pragma unroll
     for (int j = 0; j < kAggIpt; ++j) x[j] = v[j];
-    wave_to_blocked(sv, x, lane);
+    blk64(x);
 #pragma unroll
     for (int j = 1; j < kAggIpt; ++j) x[j] += x[j - 1];
     const uint64_t incl = wave_incl(x[kAggIpt - 1], OpAdd(), (uint64_t)0);
@@ -979,7 +1513,7 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     store_pieces(T1, 0, f, true);
     if (kTwo) {
       put(slot2, x);
-      store_pieces(T2, nwt, f, true);
+      store_pieces(T2, ob2, f, true);
     }
   };
   auto seg_pass = [&](const LevelTile& T, const uint32_t (&sl)[kAggIpt],
@@ -1005,9 +1539,9 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     uint64_t x[kAggIpt];
 #pragma unroll
     for (int j = 0; j < kAggIpt; ++j) x[j] = v[j];
-    wave_to_blocked(sv, x, lane);
+    blk64(x);
     seg_pass(T1, slot, x, 0, f, cmb);
-    if (kTwo) seg_pass(T2, slot2, x, nwt, f, cmb);
+    if (kTwo) seg_pass(T2, slot2, x, ob2, f, cmb);
   };
   auto load = [&](const uint64_t* col, uint64_t (&v)[kAggIpt]) {
 #pragma unroll
@@ -1033,7 +1567,7 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
       store_pieces(T1, 0, 0, true);
       if (kTwo) {
         put(slot2, pos);
-        store_pieces(T2, nwt, 0, true);
+        store_pieces(T2, ob2, 0, true);
       }
       uint64_t du[kAggIpt];
 #pragma unroll
@@ -1166,6 +1700,12 @@ __global__ void k_fill_u32_many(uint32_t** p, const int64_t* counts, int L,
     p[li][i] = 0xFFFFFFFFu;
 }
 
+__global__ void k_nat_init(uint32_t* flags, uint32_t* gs, int G) {
+  const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (i < 3) flags[i] = 0;
+  if (i < G) gs[i] = kNone;
+}
+
 __global__ void k_zero_u32(uint32_t* p, int n) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = 0;
@@ -1196,14 +1736,28 @@ struct AggLayout {
   uint32_t* htb;
   uint32_t* hscan;
   uint32_t* htotal;
-  uint32_t* hflags;       // [0] keys not increasing, [1] kinds present
+  uint32_t* hflags;       // [0] keys not increasing, [1] kinds present,
+                          // [2] input order unfit for the natural tiles
   uint32_t* htc2;         // one level over rows
   uint32_t* htb2;
   uint32_t* hflags2;
+  // natural tiles
+  int G;
+  int64_t nstride;        // 2 * (natural tiles + G): counts per level
+  uint32_t* ntc;          // [L][nstride]
+  uint32_t* ntb;
+  uint32_t* nscan;
+  int64_t lps;            // ntiles_h rounded up to kLpChunk
+  int32_t* lpraw;         // [2][lps]
+  int32_t* lp;
+  uint8_t* tg;            // [ntiles_h + G]
+  uint32_t* gs;           // [G]
+  uint32_t* ge;
+  uint32_t* gtb;          // [G + 1]
 };
 
 static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
-                            int64_t cap, uint32_t act) {
+                            int64_t cap, uint32_t act, int G) {
   AggLayout L;
   L.L = D + 2;
   L.ntiles = ceil_div(n, kAggTile);
@@ -1220,19 +1774,32 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
   L.scantmp = sc.take<uint32_t>(scan_scratch_elems((int64_t)L.L * L.ntiles));
   L.total = sc.take<uint32_t>(1);
   L.firstpos = sc.take<uint32_t>(cap);
+  L.ntiles_h = ceil_div(n, kWaveTile);
+  L.nstride = 2 * (L.ntiles_h + G);
   L.ovf_cap = n / 64 > 65536 ? n / 64 : 65536;
+  if (L.ovf_cap < 2 * L.nstride) L.ovf_cap = 2 * L.nstride;
   L.ovf_count = sc.take<uint32_t>(2);
   L.ovf_row = sc.take<uint32_t>(L.ovf_cap);
   L.ovf_val = sc.take<uint64_t>((int64_t)kMaxFields * L.ovf_cap);
-  L.ntiles_h = ceil_div(n, kWaveTile);
   L.htc = sc.take<uint32_t>((int64_t)L.L * L.ntiles_h);
   L.htb = sc.take<uint32_t>((int64_t)L.L * L.ntiles_h);
   L.hscan = sc.take<uint32_t>(scan_scratch_elems((int64_t)L.L * L.ntiles_h));
   L.htotal = sc.take<uint32_t>(2);
-  L.hflags = sc.take<uint32_t>(2);
+  L.hflags = sc.take<uint32_t>(3);
   L.htc2 = sc.take<uint32_t>(L.ntiles_h);
   L.htb2 = sc.take<uint32_t>(L.ntiles_h);
-  L.hflags2 = sc.take<uint32_t>(2);
+  L.hflags2 = sc.take<uint32_t>(3);
+  L.G = G;
+  L.ntc = sc.take<uint32_t>((int64_t)L.L * L.nstride);
+  L.ntb = sc.take<uint32_t>((int64_t)L.L * L.nstride);
+  L.nscan = sc.take<uint32_t>(scan_scratch_elems((int64_t)L.L * L.nstride));
+  L.lps = ceil_div(L.ntiles_h, (int64_t)kLpChunk) * kLpChunk;
+  L.lpraw = sc.take<int32_t>(2 * L.lps);
+  L.lp = sc.take<int32_t>(2 * L.lps);
+  L.tg = sc.take<uint8_t>(L.ntiles_h + G);
+  L.gs = sc.take<uint32_t>(G);
+  L.ge = sc.take<uint32_t>(G);
+  L.gtb = sc.take<uint32_t>(G + 1);
   return L;
 }
 
@@ -1241,7 +1808,9 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
 using namespace chopper;
 
 // Fast path over all requested levels (MaxD >= depth); returns 1 when the
-// groups are not runs and the general path must be used.
+// groups are not runs and the general path must be used.  The natural tiles
+// are tried first; when the input order does not qualify, the korder tiles
+// count the heads again.
 template <int kMD>
 static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                     const Overflow& ovf, int64_t T, int Lv, uint32_t act,
@@ -1250,106 +1819,157 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                     hipStream_t s) {
   int rc = CHOPPER_OK;
   const int64_t Th = L.ntiles_h;
+  const int G = L.G;
+  const int64_t NW = Th + G;          // natural tile slots
   FromRecords fr{S};
-  CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s, L.hflags,
-                     2));
-  const unsigned gh = (unsigned)ceil_div(Th, (int64_t)kWavesPerBlock);
-  CHOPPER_HIP(launch("agg_heads_records", k_agg_heads<kMD, FromRecords>,
-                     dim3(gh), dim3(kBlock), s, fr, act, 0,
-                     Lv - 1, D, M, Th, L.htc, L.hflags, status));
-  CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc, L.htb, (int64_t)Lv * Th,
-                                       L.hscan, L.htotal, s));
-  CHOPPER_HIP(launch("agg_offsets", k_agg_offsets_fast, dim3(1), dim3(64),
-                     s, Lv, Th, (const uint32_t*)L.htb,
-                     (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
-                     want_workload, rows->cap, rows->level_offset, status));
+  const NatGeom N{L.gtb, L.tg, L.gs, L.ge, L.lp, L.hflags + 2, Th, L.lps, G};
+  const NatGeom none{};
   // the fast-path flags and the level offsets (row counts per level size
   // the launches of the coarser levels)
-  uint32_t hf[2] = {1u, 0u};
+  uint32_t hf[3] = {1u, 0u, 1u};
   int64_t lo_h[kMaxLevels + 1];
-  CHOPPER_HIP(hipMemcpyAsync(hf, L.hflags, sizeof(hf), hipMemcpyDeviceToHost,
-                             s));
-  CHOPPER_HIP(hipMemcpyAsync(lo_h, rows->level_offset,
-                             sizeof(int64_t) * (size_t)(Lv + 1),
-                             hipMemcpyDeviceToHost, s));
-  CHOPPER_HIP(hipStreamSynchronize(s));
+  auto read_back = [&]() -> int {
+    CHOPPER_HIP(hipMemcpyAsync(hf, L.hflags, sizeof(hf),
+                               hipMemcpyDeviceToHost, s));
+    CHOPPER_HIP(hipMemcpyAsync(lo_h, rows->level_offset,
+                               sizeof(int64_t) * (size_t)(Lv + 1),
+                               hipMemcpyDeviceToHost, s));
+    CHOPPER_HIP(hipStreamSynchronize(s));
+    return CHOPPER_OK;
+  };
+  CHOPPER_HIP(launch("agg_nat_init", k_nat_init, dim3(1), dim3(kBlock), s,
+                     L.hflags, L.gs, G));
+  CHOPPER_HIP(launch("agg_nat_pre", k_nat_pre,
+                     dim3((unsigned)ceil_div(Th, (int64_t)kWavesPerBlock)),
+                     dim3(kBlock), s, S.n, G, S.gpu, S.cls, S.start, Th,
+                     L.lps, L.lpraw, L.gs, L.hflags + 2));
+  CHOPPER_HIP(launch("agg_nat_tiles", k_nat_tiles, dim3(1), dim3(1024), s,
+                     S.n, G, Th, L.lps, (const int32_t*)L.lpraw, L.lp,
+                     (const uint32_t*)L.gs, L.ge, L.gtb, L.tg,
+                     (const uint32_t*)(L.hflags + 2)));
+  CHOPPER_HIP(launch("agg_heads_nat", k_agg_heads_nat<kMD>,
+                     dim3((unsigned)ceil_div(NW, (int64_t)kWavesPerBlock)),
+                     dim3(kBlock), s, S, N, act, 0, Lv - 1, D, M, L.nstride,
+                     L.ntc, L.hflags, status));
+  CHOPPER_HIP(exclusive_scan<uint32_t>(L.ntc, L.ntb, (int64_t)Lv * L.nstride,
+                                       L.nscan, L.htotal, s));
+  CHOPPER_HIP(launch("agg_offsets", k_agg_offsets_fast, dim3(1), dim3(64),
+                     s, Lv, L.nstride, (const uint32_t*)L.ntb,
+                     (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
+                     want_workload, rows->cap, rows->level_offset, status));
+  rc = read_back();
+  if (rc != CHOPPER_OK) return rc;
+  const bool nat = hf[2] == 0;
+  if (!nat) {
+    CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
+                       L.hflags, 3));
+    CHOPPER_HIP(launch("agg_heads_records", k_agg_heads<kMD, FromRecords>,
+                       dim3((unsigned)ceil_div(Th, (int64_t)kWavesPerBlock)),
+                       dim3(kBlock), s, fr, act, 0, Lv - 1, D, M, Th, L.htc,
+                       L.hflags, status));
+    CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc, L.htb, (int64_t)Lv * Th,
+                                         L.hscan, L.htotal, s));
+    CHOPPER_HIP(launch("agg_offsets", k_agg_offsets_fast, dim3(1), dim3(64),
+                       s, Lv, Th, (const uint32_t*)L.htb,
+                       (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
+                       want_workload, rows->cap, rows->level_offset, status));
+    rc = read_back();
+    if (rc != CHOPPER_OK) return rc;
+  }
   auto level_rows = [&](int li) -> int64_t {
     int64_t a = lo_h[li], b = lo_h[li + 1];
     if (b > rows->cap) b = rows->cap;
     return b > a ? b - a : 0;
   };
-  if (hf[0] == 0) {
-    // finer < 0: from the records (two levels, li and li - 1, when `two`)
-    auto fast_level = [&](int li, int finer, bool two) -> int {
-      if (finer < 0) {
+  if (hf[0] != 0) return 1;
+  // finer < 0: from the records (two levels, li and li - 1, when `two`)
+  auto fast_level = [&](int li, int finer, bool two) -> int {
+    if (finer < 0) {
+      int64_t ns;
+      if (nat) {
+        const uint32_t* tb = L.ntb + (int64_t)li * L.nstride;
+        const dim3 grid((unsigned)ceil_div(NW, (int64_t)kWavesPerBlock));
+        if (two)
+          CHOPPER_HIP(launch("agg_fast_reduce_records",
+                             k_agg_fast_reduce<kMD, FromRecords, true, true>,
+                             grid, dim3(kBlock), s, fr, N, li, D, M, tb,
+                             (const uint32_t*)(tb - L.nstride),
+                             (const int64_t*)nullptr, R, ovf, NW));
+        else
+          CHOPPER_HIP(launch("agg_fast_reduce_records",
+                             k_agg_fast_reduce<kMD, FromRecords, false, true>,
+                             grid, dim3(kBlock), s, fr, N, li, D, M, tb,
+                             (const uint32_t*)nullptr,
+                             (const int64_t*)nullptr, R, ovf, NW));
+        ns = (two ? 4 : 2) * NW;
+      } else {
         const uint32_t* tb = L.htb + (int64_t)li * Th;
         if (two)
           CHOPPER_HIP(launch("agg_fast_reduce_records",
-                             k_agg_fast_reduce<kMD, FromRecords, true>,
-                             dim3((unsigned)T), dim3(kBlock), s, fr, li, D, M,
-                             tb, (const uint32_t*)(tb - Th),
+                             k_agg_fast_reduce<kMD, FromRecords, true, false>,
+                             dim3((unsigned)T), dim3(kBlock), s, fr, none, li,
+                             D, M, tb, (const uint32_t*)(tb - Th),
                              (const int64_t*)nullptr, R, ovf, Th));
         else
           CHOPPER_HIP(launch("agg_fast_reduce_records",
-                             k_agg_fast_reduce<kMD, FromRecords, false>,
-                             dim3((unsigned)T), dim3(kBlock), s, fr, li, D, M,
-                             tb, (const uint32_t*)nullptr,
+                             k_agg_fast_reduce<kMD, FromRecords, false, false>,
+                             dim3((unsigned)T), dim3(kBlock), s, fr, none, li,
+                             D, M, tb, (const uint32_t*)nullptr,
                              (const int64_t*)nullptr, R, ovf, Th));
-        const int64_t ns = two ? 2 * Th : Th;
-        CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
-                           grid_for(ns, kBlock), dim3(kBlock), s, ovf, R,
-                           nfields, ns));
-      } else {
-        // launches sized by the finer level's row count
-        const int64_t cnt = level_rows(finer);
-        if (cnt == 0) return CHOPPER_OK;
-        const int64_t nw = ceil_div(cnt, (int64_t)kWaveTile);
-        const unsigned gr = (unsigned)ceil_div(nw, (int64_t)kWavesPerBlock);
-        FromRows src{R, M, rows->level_offset, finer};
-        CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
-                           L.hflags2, 2));
-        CHOPPER_HIP(launch("agg_heads_rows", k_agg_heads<kMD, FromRows>,
-                           dim3(gr), dim3(kBlock), s, src,
-                           1u << li, li, li, D, M, nw, L.htc2, L.hflags2,
-                           status));
-        CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc2, L.htb2, nw, L.hscan,
-                                             L.htotal + 1, s));
-        CHOPPER_HIP(launch("agg_fast_reduce_rows",
-                           k_agg_fast_reduce<kMD, FromRows, false>, dim3(gr),
-                           dim3(kBlock), s, src, li, D, M,
-                           (const uint32_t*)L.htb2, (const uint32_t*)nullptr,
-                           (const int64_t*)(rows->level_offset + li), R, ovf,
-                           nw));
-        CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
-                           grid_for(nw, kBlock), dim3(kBlock), s, ovf, R,
-                           nfields, nw));
+        ns = two ? 2 * Th : Th;
       }
-      return CHOPPER_OK;
-    };
-    if (level == CHOPPER_LEVEL_ALL) {
-      // the records give the two finest levels, each coarser one comes from
-      // the rows of the level below
-      const bool two = D >= 2;
-      rc = fast_level(D > 0 ? D - 1 : D, -1, two);
-      if (rc != CHOPPER_OK) return rc;
-      for (int li = D - (two ? 3 : 2); li >= 0; --li) {
-        rc = fast_level(li, li + 1, false);
-        if (rc != CHOPPER_OK) return rc;
-      }
-      if (D > 0) {
-        rc = fast_level(D, 0, false);
-        if (rc != CHOPPER_OK) return rc;
-      }
-      CHOPPER_HIP(launch("agg_workload_from_gpu", k_agg_workload_from_gpu,
-                         dim3(1), dim3(64), s,
-                         (const int64_t*)rows->level_offset, D, R, nfields));
+      CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
+                         grid_for(ns, kBlock), dim3(kBlock), s, ovf, R,
+                         nfields, ns));
     } else {
-      rc = fast_level(level == CHOPPER_LEVEL_GPU ? D : level, -1, false);
-      if (rc != CHOPPER_OK) return rc;
+      // launches sized by the finer level's row count
+      const int64_t cnt = level_rows(finer);
+      if (cnt == 0) return CHOPPER_OK;
+      const int64_t nw = ceil_div(cnt, (int64_t)kWaveTile);
+      const unsigned gr = (unsigned)ceil_div(nw, (int64_t)kWavesPerBlock);
+      FromRows src{R, M, rows->level_offset, finer};
+      CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
+                         L.hflags2, 3));
+      CHOPPER_HIP(launch("agg_heads_rows", k_agg_heads<kMD, FromRows>,
+                         dim3(gr), dim3(kBlock), s, src,
+                         1u << li, li, li, D, M, nw, L.htc2, L.hflags2,
+                         status));
+      CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc2, L.htb2, nw, L.hscan,
+                                           L.htotal + 1, s));
+      CHOPPER_HIP(launch("agg_fast_reduce_rows",
+                         k_agg_fast_reduce<kMD, FromRows, false, false>,
+                         dim3(gr), dim3(kBlock), s, src, none, li, D, M,
+                         (const uint32_t*)L.htb2, (const uint32_t*)nullptr,
+                         (const int64_t*)(rows->level_offset + li), R, ovf,
+                         nw));
+      CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
+                         grid_for(nw, kBlock), dim3(kBlock), s, ovf, R,
+                         nfields, nw));
     }
     return CHOPPER_OK;
+  };
+  if (level == CHOPPER_LEVEL_ALL) {
+    // the records give the two finest levels, each coarser one comes from
+    // the rows of the level below
+    const bool two = D >= 2;
+    rc = fast_level(D > 0 ? D - 1 : D, -1, two);
+    if (rc != CHOPPER_OK) return rc;
+    for (int li = D - (two ? 3 : 2); li >= 0; --li) {
+      rc = fast_level(li, li + 1, false);
+      if (rc != CHOPPER_OK) return rc;
+    }
+    if (D > 0) {
+      rc = fast_level(D, 0, false);
+      if (rc != CHOPPER_OK) return rc;
+    }
+    CHOPPER_HIP(launch("agg_workload_from_gpu", k_agg_workload_from_gpu,
+                       dim3(1), dim3(64), s,
+                       (const int64_t*)rows->level_offset, D, R, nfields));
+  } else {
+    rc = fast_level(level == CHOPPER_LEVEL_GPU ? D : level, -1, false);
+    if (rc != CHOPPER_OK) return rc;
   }
-  return 1;
+  return CHOPPER_OK;
 }
 
 extern "C" int chopper_aggregate(const chopper_records* rec,
@@ -1390,13 +2010,13 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
   else return CHOPPER_EINVAL;
 
   Scratch probe(nullptr);
-  agg_layout(probe, n, D, M, rows->cap, act);
+  agg_layout(probe, n, D, M, rows->cap, act, rec->n_gpus);
   int rc = scratch_check(scratch, scratch_bytes, probe.used);
   if (rc != 0) return rc > 0 ? CHOPPER_OK : rc;
   if (!status) return CHOPPER_EINVAL;
   hipStream_t s = (hipStream_t)stream;
   Scratch sc(scratch);
-  AggLayout L = agg_layout(sc, n, D, M, rows->cap, act);
+  AggLayout L = agg_layout(sc, n, D, M, rows->cap, act, rec->n_gpus);
   const int Lv = L.L;
   const int64_t T = L.ntiles;
   const int nc = rec->n_counters;

@@ -2,6 +2,7 @@
 the C ABI.  Integer outputs must be bit-exact; derived doubles must be equal
 (NaN matching NaN), which is within the 1e-12 relative tolerance required for
 them since both sides perform the same IEEE operations."""
+import dataclasses
 import sys
 
 import numpy as np
@@ -139,6 +140,77 @@ def test_filter(ch):
     f_ch = ch.make_filter(gpus=[0, 2], classes=[0, 3, 5, 6, 7])
     assert_parity(run_gpu(ch, tr, filt=f_ch), oracle.run(tr, filt=f_or),
                   name="filter2")
+
+
+# ---------------------------------------------------------------------------
+# Input grouped by GPU and in start order inside each GPU (the order a
+# profiler writes): the aggregation then reads the records in input order.
+# ---------------------------------------------------------------------------
+def natural_order(tr, gpu_map=None, n_gpus=None):
+    """The records stably sorted by (gpu, start); optionally GPU ids renamed
+    through gpu_map (records, markers and anchors alike)."""
+    if gpu_map is not None:
+        gm = np.asarray(gpu_map, np.uint8)
+        tr = dataclasses.replace(tr, gpu=gm[tr.gpu], m_gpu=gm[tr.m_gpu],
+                                 a_gpu=gm[tr.a_gpu], n_gpus=n_gpus)
+    p = np.lexsort((tr.start, tr.gpu))
+    return dataclasses.replace(
+        tr, gpu=tr.gpu[p], stream=tr.stream[p], start=tr.start[p],
+        end=tr.end[p], cls=tr.cls[p], op_id=tr.op_id[p],
+        counters=None if tr.counters is None else tr.counters[:, p].copy(),
+        name=tr.name + "/natural")
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("shape", range(len(MICRO)))
+def test_natural_order_micro(ch, seed, shape):
+    tr = natural_order(tg.make_micro(900 + seed * 7 + shape, **MICRO[shape]))
+    say("natural micro", seed, shape, tr.n)
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_natural_order_many_small_gpus(ch, seed):
+    """Forty GPUs of about fifty records: most tiles hold several GPUs."""
+    tr = natural_order(tg.make_micro(950 + seed, n_gpus=40, n_kernels=2000,
+                                     n_streams=3, depth=3, n_counters=16,
+                                     span=3000))
+    say("natural many gpus", seed, tr.n)
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+
+
+def test_natural_order_sparse_gpu_ids(ch):
+    """GPUs 1, 4 and 6 of 8 have records; the others none."""
+    tr = natural_order(tg.make_micro(960, n_gpus=3, n_kernels=3000,
+                                     n_streams=3, depth=4, n_counters=16,
+                                     anchors=4, span=40000),
+                       gpu_map=[1, 4, 6], n_gpus=8)
+    say("natural sparse gpus", tr.n)
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+
+
+@pytest.mark.parametrize("level", [0, 2, 100])
+def test_natural_order_single_level(ch, level):
+    tr = natural_order(tg.make_micro(970, n_gpus=2, n_kernels=3000,
+                                     depth=3, n_counters=4, span=30000))
+    say("natural level", level)
+    assert_parity(run_gpu(ch, tr, level=level), oracle.run(tr, level=level),
+                  name=f"natural level{level}")
+
+
+def test_natural_order_broken_inside_a_gpu(ch):
+    """Two records of one GPU out of start order: the korder tiles apply."""
+    tr = natural_order(tg.make_micro(980, n_gpus=2, n_kernels=3000,
+                                     depth=3, n_counters=16, span=30000))
+    g0 = np.nonzero(tr.gpu == tr.gpu[1000])[0]
+    i = int(g0[g0 > 1000][0])
+    j = next(int(k) for k in g0[g0 > i] if tr.start[k] != tr.start[i])
+    for a in ("gpu", "stream", "start", "end", "cls", "op_id"):
+        v = getattr(tr, a)
+        v[[i, j]] = v[[j, i]]
+    tr.counters[:, [i, j]] = tr.counters[:, [j, i]]
+    say("natural broken", i, j)
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name="natural broken")
 
 
 def _tiny(n, m=3, G=1, depth=2, overlapping=False):
