@@ -1396,8 +1396,12 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
     tprev[0] = base > 0 ? level_key<MaxD>(cp, cgk, li, D, M) : kNone;
     if (kTwo)
       tprev2[0] = base > 0 ? level_key<MaxD>(cp, cgk, li2, D, M) : kNone;
-    r0 = (row0 ? *row0 : 0) + (int64_t)tilebase[w];
-    if (kTwo) q0 = (int64_t)tilebase2[w];
+    // rows: the level offset (row0, when the scan covers this level only)
+    // plus the scanned head count; row0[-1] is the second level's offset
+    r0 = (row0 ? row0[0] - (int64_t)tilebase[0] : 0) + (int64_t)tilebase[w];
+    if (kTwo)
+      q0 = (row0 ? row0[-1] - (int64_t)tilebase2[0] : 0) +
+           (int64_t)tilebase2[w];
   }
 #pragma unroll
   for (int j = 0; j < kAggIpt; ++j) {
@@ -1591,54 +1595,163 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
   }
 }
 
-// Workload rows (one per kind present) from the GPU rows, in kind order.
-__global__ void k_agg_workload_from_gpu(const int64_t* level_offset, int D,
-                                        RowsDev R, int nfields) {
-  const int64_t g0 = level_offset[D], g1 = level_offset[D + 1];
-  const int64_t w0 = level_offset[D + 1], w1 = level_offset[D + 2];
-  const int f = threadIdx.x;
-  for (int64_t w = w0; w < w1 && w < R.cap; ++w) {
-    // kind of this workload row: 0 first when present
-    const uint32_t kind = (w1 - w0 == 2) ? (uint32_t)(w - w0) : 2u;
-    uint32_t kd = kind;
-    if (kd == 2u) {   // a single row: the only kind present
-      kd = 0u;
-      for (int64_t r = g0; r < g1 && r < R.cap; ++r)
-        if (R.kind[r] == 1u) kd = 1u;
-    }
-    if (f < nfields) {
-      uint64_t acc = f == 4 ? (uint64_t)kI64Max
-                     : f == 5 ? (uint64_t)kI64Min : 0ull;
-      for (int64_t r = g0; r < g1 && r < R.cap; ++r) {
-        if (R.kind[r] != kd) continue;
-        uint64_t v;
-        switch (f) {
-          case 0: v = R.n[r]; break;
-          case 1: v = (uint64_t)R.dur[r]; break;
-          case 2: v = (uint64_t)R.gap[r]; break;
-          case 3: v = (uint64_t)R.ovl[r]; break;
-          case 4: v = (uint64_t)R.tmin[r]; break;
-          case 5: v = (uint64_t)R.tmax[r]; break;
-          default: v = R.ctr[(int64_t)(f - 6) * R.cap + r]; break;
-        }
-        if (f == 4) acc = (int64_t)v < (int64_t)acc ? v : acc;
-        else if (f == 5) acc = (int64_t)v > (int64_t)acc ? v : acc;
-        else acc += v;
-      }
-      store_field(R, f, (uint32_t)w, acc);
-    }
+// GPU rows from the level-0 rows (with no marker level, the GPU rows
+// themselves): the level-0 rows of one (gpu, kind) are consecutive and
+// ordered by (tmin, first), and every record is in exactly one of them.
+// Block b sums the rows of the pair gpu * 2 + kind = b into slot b of
+// `pair` (fields, then tmin, first and a presence flag); a single block
+// then numbers the pairs present, writes the GPU rows and adds them up into
+// the workload rows (one per kind present, kind 0 first).
+constexpr int kPairW = kMaxFields + 3;
+
+// First row in [a0, a1) whose pair is >= k, for every thread of the block:
+// a search with kBlock probes per round.
+__device__ inline int64_t block_pair_lower(const RowsDev& R, int64_t a0,
+                                           int64_t a1, uint32_t k,
+                                           uint32_t* s_cnt) {
+  int64_t lo = a0, hi = a1;           // answer in [lo, hi]
+  while (hi > lo) {
+    const int64_t step = (hi - lo + kBlock - 1) / kBlock;
+    const int64_t p = lo + (int64_t)threadIdx.x * step;
+    const bool below =
+        p < hi && (uint32_t)R.gpu[p] * 2u + R.kind[p] < k;
+    const uint64_t m = __ballot(below);
     __syncthreads();
-    if (f == 0) {
-      for (int l = 0; l < D; ++l) R.path[(int64_t)l * R.cap + w] = kNone;
+    if (lane_id() == 0) s_cnt[threadIdx.x / kWave] = (uint32_t)__popcll(m);
+    __syncthreads();
+    uint32_t c = 0;
+    for (int i = 0; i < kWavesPerBlock; ++i) c += s_cnt[i];
+    // probes 0 .. c - 1 are below k (rows are sorted by pair)
+    if (c == 0) return lo;
+    const int64_t nlo = lo + (int64_t)(c - 1) * step + 1;
+    const int64_t nhi = lo + (int64_t)c * step;
+    lo = nlo;
+    hi = nhi < hi ? nhi : hi;
+  }
+  return lo;
+}
+
+__global__ __launch_bounds__(kBlock) void k_agg_gpu_sums(
+    const int64_t* level_offset, RowsDev R, int nfields, uint64_t* pair) {
+  __shared__ uint32_t s_cnt[kWavesPerBlock];
+  __shared__ uint64_t s_f[kWavesPerBlock][kMaxFields];
+  const uint32_t b = blockIdx.x;
+  uint64_t* slot = pair + (int64_t)b * kPairW;
+  int64_t a0 = level_offset[0], a1 = level_offset[1];
+  if (a1 > R.cap) a1 = R.cap;
+  if (a0 > a1) a0 = a1;
+  const int64_t lo = block_pair_lower(R, a0, a1, b, s_cnt);
+  const int64_t hi = block_pair_lower(R, lo, a1, b + 1, s_cnt);
+  if (lo >= hi) {
+    if (threadIdx.x == 0) slot[kMaxFields + 2] = 0;
+    return;
+  }
+  uint64_t acc[kMaxFields];
+#pragma unroll
+  for (int f = 0; f < kMaxFields; ++f)
+    acc[f] = f == 5 ? (uint64_t)kI64Min : 0ull;
+  for (int64_t r = lo + threadIdx.x; r < hi; r += kBlock) {
+#pragma unroll
+    for (int f = 0; f < kMaxFields; ++f) {
+      if (f == 4 || f >= nfields) continue;
+      const uint64_t x = row_column(R, f)[r];
+      acc[f] = f == 5 ? ((int64_t)x > (int64_t)acc[f] ? x : acc[f])
+                      : acc[f] + x;
+    }
+  }
+#pragma unroll
+  for (int f = 0; f < kMaxFields; ++f) {
+    uint64_t v = acc[f];
+    for (int d = kWave / 2; d > 0; d >>= 1) {
+      const uint64_t o = __shfl_xor(v, d, kWave);
+      v = f == 5 ? ((int64_t)o > (int64_t)v ? o : v) : v + o;
+    }
+    if (lane_id() == 0) s_f[threadIdx.x / kWave][f] = v;
+  }
+  __syncthreads();
+  const int f = (int)threadIdx.x;
+  if (f < nfields && f != 4) {
+    uint64_t t = s_f[0][f];
+    for (int i = 1; i < kWavesPerBlock; ++i)
+      t = f == 5 ? ((int64_t)s_f[i][f] > (int64_t)t ? s_f[i][f] : t)
+                 : t + s_f[i][f];
+    slot[f] = t;
+  }
+  if (f == 0) {
+    // the pair's first row has the smallest (tmin, first)
+    slot[4] = (uint64_t)R.tmin[lo];
+    slot[kMaxFields] = (uint64_t)R.tmin[lo];
+    slot[kMaxFields + 1] = R.first[lo];
+    slot[kMaxFields + 2] = 1;
+  }
+}
+
+__global__ __launch_bounds__(1024) void k_agg_gpu_finish(
+    const int64_t* level_offset, int D, RowsDev R, int nfields, int npairs,
+    const uint64_t* pair) {
+  __shared__ uint32_t s_rank[513];
+  const int t = (int)threadIdx.x;
+  if (t == 0) {
+    uint32_t c = 0;
+    for (int q = 0; q < npairs; ++q) {
+      s_rank[q] = c;
+      c += (uint32_t)pair[(int64_t)q * kPairW + kMaxFields + 2];
+    }
+    s_rank[npairs] = c;
+  }
+  __syncthreads();
+  const int64_t g0 = level_offset[D];
+  // GPU rows: one thread per (pair, field) of the pairs present
+  for (int i = t; i < npairs * kPairW; i += 1024) {
+    const int q = i / kPairW, f = i % kPairW;
+    const uint64_t* slot = pair + (int64_t)q * kPairW;
+    if (!slot[kMaxFields + 2]) continue;
+    const int64_t row = g0 + s_rank[q];
+    if (row >= R.cap) continue;
+    if (f < nfields) {
+      row_column(R, f)[row] = slot[f];
+    } else if (f == kMaxFields) {
+      R.first[row] = (uint32_t)slot[kMaxFields + 1];
+      R.gpu[row] = (uint8_t)(q >> 1);
+      R.kind[row] = (uint8_t)(q & 1);
+      for (int l = 0; l < D; ++l) R.path[(int64_t)l * R.cap + row] = kNone;
+    }
+  }
+  // workload rows: kind 0 first when present
+  const int64_t w0 = level_offset[D + 1], w1 = level_offset[D + 2];
+  for (int i = t; i < 2 * kPairW; i += 1024) {
+    const uint32_t kd = (uint32_t)(i / kPairW);
+    const int f = i % kPairW;
+    bool any = false;
+    uint64_t acc = f == 5 ? (uint64_t)kI64Min : 0ull;
+    int64_t bt = kI64Max;
+    uint32_t bf = kNone;
+    for (int q = (int)kd; q < npairs; q += 2) {
+      const uint64_t* slot = pair + (int64_t)q * kPairW;
+      if (!slot[kMaxFields + 2]) continue;
+      any = true;
+      const uint64_t x = slot[f < kMaxFields ? f : 0];
+      acc = f == 5 ? ((int64_t)x > (int64_t)acc ? x : acc) : acc + x;
+      const int64_t tq = (int64_t)slot[kMaxFields];
+      const uint32_t fq = (uint32_t)slot[kMaxFields + 1];
+      if (tq < bt || (tq == bt && fq < bf)) {
+        bt = tq;
+        bf = fq;
+      }
+    }
+    if (!any) continue;
+    const int64_t w = w0 + (w1 - w0 == 2 ? (int64_t)kd : 0);
+    if (w >= w1 || w >= R.cap) continue;
+    if (f < nfields && f != 4) {
+      row_column(R, f)[w] = acc;
+    } else if (f == 4) {
+      R.tmin[w] = bt;
+    } else if (f == kMaxFields) {
+      R.first[w] = bf;
       R.gpu[w] = 0xFF;
       R.kind[w] = (uint8_t)kd;
-      uint32_t first = kNone;
-      for (int64_t r = g0; r < g1 && r < R.cap; ++r)
-        if (R.kind[r] == kd && R.tmin[r] == R.tmin[w] && R.first[r] < first)
-          first = R.first[r];
-      R.first[w] = first;
+      for (int l = 0; l < D; ++l) R.path[(int64_t)l * R.cap + w] = kNone;
     }
-    __syncthreads();
   }
 }
 
@@ -1738,7 +1851,7 @@ struct AggLayout {
   uint32_t* htotal;
   uint32_t* hflags;       // [0] keys not increasing, [1] kinds present,
                           // [2] input order unfit for the natural tiles
-  uint32_t* htc2;         // one level over rows
+  uint32_t* htc2;         // one or two levels over rows
   uint32_t* htb2;
   uint32_t* hflags2;
   // natural tiles
@@ -1751,6 +1864,7 @@ struct AggLayout {
   int32_t* lpraw;         // [2][lps]
   int32_t* lp;
   uint8_t* tg;            // [ntiles_h + G]
+  uint64_t* pair;         // [2G][kPairW] GPU row sums
   uint32_t* gs;           // [G]
   uint32_t* ge;
   uint32_t* gtb;          // [G + 1]
@@ -1786,8 +1900,8 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
   L.hscan = sc.take<uint32_t>(scan_scratch_elems((int64_t)L.L * L.ntiles_h));
   L.htotal = sc.take<uint32_t>(2);
   L.hflags = sc.take<uint32_t>(3);
-  L.htc2 = sc.take<uint32_t>(L.ntiles_h);
-  L.htb2 = sc.take<uint32_t>(L.ntiles_h);
+  L.htc2 = sc.take<uint32_t>(2 * L.ntiles_h);
+  L.htb2 = sc.take<uint32_t>(2 * L.ntiles_h);
   L.hflags2 = sc.take<uint32_t>(3);
   L.G = G;
   L.ntc = sc.take<uint32_t>((int64_t)L.L * L.nstride);
@@ -1797,6 +1911,7 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
   L.lpraw = sc.take<int32_t>(2 * L.lps);
   L.lp = sc.take<int32_t>(2 * L.lps);
   L.tg = sc.take<uint8_t>(L.ntiles_h + G);
+  L.pair = sc.take<uint64_t>((int64_t)2 * G * kPairW);
   L.gs = sc.take<uint32_t>(G);
   L.ge = sc.take<uint32_t>(G);
   L.gtb = sc.take<uint32_t>(G + 1);
@@ -1922,49 +2037,61 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                          grid_for(ns, kBlock), dim3(kBlock), s, ovf, R,
                          nfields, ns));
     } else {
-      // launches sized by the finer level's row count
+      // launches sized by the finer level's row count; with `two` also the
+      // level li - 1 (heads of li - 1 first in the table, then li)
       const int64_t cnt = level_rows(finer);
       if (cnt == 0) return CHOPPER_OK;
       const int64_t nw = ceil_div(cnt, (int64_t)kWaveTile);
       const unsigned gr = (unsigned)ceil_div(nw, (int64_t)kWavesPerBlock);
       FromRows src{R, M, rows->level_offset, finer};
+      const int lv0 = two ? li - 1 : li;
+      const uint32_t lact = two ? (3u << (li - 1)) : (1u << li);
       CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
                          L.hflags2, 3));
       CHOPPER_HIP(launch("agg_heads_rows", k_agg_heads<kMD, FromRows>,
-                         dim3(gr), dim3(kBlock), s, src,
-                         1u << li, li, li, D, M, nw, L.htc2, L.hflags2,
-                         status));
-      CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc2, L.htb2, nw, L.hscan,
+                         dim3(gr), dim3(kBlock), s, src, lact, lv0, li, D, M,
+                         nw, L.htc2, L.hflags2, status));
+      CHOPPER_HIP(exclusive_scan<uint32_t>(L.htc2, L.htb2,
+                                           (two ? 2 : 1) * nw, L.hscan,
                                            L.htotal + 1, s));
-      CHOPPER_HIP(launch("agg_fast_reduce_rows",
-                         k_agg_fast_reduce<kMD, FromRows, false, false>,
-                         dim3(gr), dim3(kBlock), s, src, none, li, D, M,
-                         (const uint32_t*)L.htb2, (const uint32_t*)nullptr,
-                         (const int64_t*)(rows->level_offset + li), R, ovf,
-                         nw));
+      const int64_t* r0 = rows->level_offset + li;
+      if (two)
+        CHOPPER_HIP(launch("agg_fast_reduce_rows",
+                           k_agg_fast_reduce<kMD, FromRows, true, false>,
+                           dim3(gr), dim3(kBlock), s, src, none, li, D, M,
+                           (const uint32_t*)(L.htb2 + nw),
+                           (const uint32_t*)L.htb2, r0, R, ovf, nw));
+      else
+        CHOPPER_HIP(launch("agg_fast_reduce_rows",
+                           k_agg_fast_reduce<kMD, FromRows, false, false>,
+                           dim3(gr), dim3(kBlock), s, src, none, li, D, M,
+                           (const uint32_t*)L.htb2, (const uint32_t*)nullptr,
+                           r0, R, ovf, nw));
+      const int64_t ns = (two ? 2 : 1) * nw;
       CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
-                         grid_for(nw, kBlock), dim3(kBlock), s, ovf, R,
-                         nfields, nw));
+                         grid_for(ns, kBlock), dim3(kBlock), s, ovf, R,
+                         nfields, ns));
     }
     return CHOPPER_OK;
   };
   if (level == CHOPPER_LEVEL_ALL) {
-    // the records give the two finest levels, each coarser one comes from
-    // the rows of the level below
+    // the records give the two finest levels, coarser marker levels come
+    // in pairs from the rows of the level below, the GPU rows from the
+    // level-0 rows
     const bool two = D >= 2;
     rc = fast_level(D > 0 ? D - 1 : D, -1, two);
     if (rc != CHOPPER_OK) return rc;
-    for (int li = D - (two ? 3 : 2); li >= 0; --li) {
-      rc = fast_level(li, li + 1, false);
+    for (int li = D - (two ? 3 : 2); li >= 0; li -= 2) {
+      rc = fast_level(li, li + 1, li >= 1);
       if (rc != CHOPPER_OK) return rc;
     }
-    if (D > 0) {
-      rc = fast_level(D, 0, false);
-      if (rc != CHOPPER_OK) return rc;
-    }
-    CHOPPER_HIP(launch("agg_workload_from_gpu", k_agg_workload_from_gpu,
-                       dim3(1), dim3(64), s,
-                       (const int64_t*)rows->level_offset, D, R, nfields));
+    CHOPPER_HIP(launch("agg_gpu_rows", k_agg_gpu_sums,
+                       dim3((unsigned)(2 * L.G)), dim3(kBlock), s,
+                       (const int64_t*)rows->level_offset, R, nfields,
+                       L.pair));
+    CHOPPER_HIP(launch("agg_workload_from_gpu", k_agg_gpu_finish, dim3(1),
+                       dim3(1024), s, (const int64_t*)rows->level_offset, D,
+                       R, nfields, 2 * L.G, (const uint64_t*)L.pair));
   } else {
     rc = fast_level(level == CHOPPER_LEVEL_GPU ? D : level, -1, false);
     if (rc != CHOPPER_OK) return rc;

@@ -53,9 +53,9 @@ __global__ __launch_bounds__(kBlock) void k_marker_links(
     atomicOr(status, (uint32_t)CHOPPER_ST_MARKER_OVERLAP);
 }
 
-// segment parameters held in LDS when there are at most this many
-constexpr int kLdsSegs = 512;
-// LDS pool of marker starts per wave, shared by the levels' windows
+// LDS pool per wave of marker starts, ends and ids, shared by the levels'
+// windows (a wave tile of the finest level of a training trace spans a few
+// hundred operation markers)
 constexpr int kMarkWin = 512;
 
 // Records in natural order, wave tiles of kWaveTile, each lane owning eight
@@ -63,26 +63,25 @@ constexpr int kMarkWin = 512;
 // lane l finds the window of level-l markers that the tile's starts can
 // fall in (from the marker holding the smallest start to the last one
 // starting at or before the largest); the windows that fit the wave's LDS
-// pool are staged there.  A lane searches a window for its first record
-// and advances from there for the next ones, whose starts usually follow;
-// records of other gpus and levels whose window does not fit search the
-// bucket index.  The input order only affects speed.
-template <int MaxD, bool kLds>
+// pool are staged there with the markers' ends and ids.  A lane searches a
+// window for its first record and advances from there for the next ones,
+// whose starts usually follow; records of other gpus and levels whose
+// window does not fit search the bucket index.  The input order only
+// affects speed.
+template <int MaxD>
 __global__ __launch_bounds__(kBlock) void k_attribute_records(
     int64_t n, int G, int D, const uint8_t* gpu, const int64_t* start,
     BIndex X, const int64_t* sme, const uint32_t* sid, uint32_t* idx) {
-  __shared__ BSeg s_lds[kLds ? kLdsSegs : 1];
-  __shared__ int64_t s_pool[kWavesPerBlock][kMarkWin];
-  if (kLds) {
-    for (int i = threadIdx.x; i < G * D; i += kBlock) s_lds[i] = X.seg[i];
-    __syncthreads();
-  }
-  const BSeg* s_seg = kLds ? s_lds : X.seg;
+  __shared__ int64_t s_ps[kWavesPerBlock][kMarkWin];
+  __shared__ int64_t s_pe[kWavesPerBlock][kMarkWin];
+  __shared__ uint32_t s_pi[kWavesPerBlock][kMarkWin];
   const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
   const int64_t base =
       ((int64_t)blockIdx.x * kWavesPerBlock + wv) * (int64_t)kWaveTile;
   if (base >= n) return;
-  int64_t* pool = s_pool[wv];
+  int64_t* ps = s_ps[wv];
+  int64_t* pe = s_pe[wv];
+  uint32_t* pi = s_pi[wv];
   const int64_t k0 = base + (int64_t)lane * kTileIpt;   // lane's first record
   const bool full = base + kWaveTile <= n;                // uniform
   // vector loads only from suitably aligned columns
@@ -131,7 +130,7 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
   // lane l < D: window of level l
   int64_t wlo = 0, wk = 0;
   if (g0ok && lane < D) {
-    const BSeg P = s_seg[g0 * D + lane];
+    const BSeg P = X.seg[g0 * D + lane];
     int64_t lo[2], hi[2];
     const int64_t t[2] = {smin, smax};
     bi_range(X, P, smin, &lo[0], &hi[0]);
@@ -153,25 +152,26 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
 #pragma unroll
   for (int l = 0; l < MaxD; ++l) {
     if (l >= D || wn[l] < 0) continue;
-    for (int64_t q = lane; q < wn[l]; q += kWave)
-      pool[wo[l] + q] = X.key[wl[l] + q];
+    for (int64_t q = lane; q < wn[l]; q += kWave) {
+      ps[wo[l] + q] = X.key[wl[l] + q];
+      pe[wo[l] + q] = sme[wl[l] + q];
+      pi[wo[l] + q] = sid[wl[l] + q];
+    }
   }
   wave_sync();
   // per level: the window position of each record, then its marker
 #pragma unroll
   for (int l = 0; l < MaxD; ++l) {
     if (l >= D) break;
-    int64_t qq[kTileIpt], sb[kTileIpt];
-    const int64_t* w = pool + wo[l];
+    const int64_t* w = ps + wo[l];
     const int nw = (int)wn[l];
     int a = -1;             // window index of the last key <= previous start
     int64_t prev = kI64Max;
+    uint32_t out[kTileIpt];
 #pragma unroll
     for (int j = 0; j < kTileIpt; ++j) {
-      qq[j] = -1;
-      sb[j] = 0;
+      out[j] = kNone;
       if (!((m_ok >> j) & 1u)) continue;
-      sb[j] = s_seg[g[j] * D + l].sb;
       if (g[j] == g0 && nw >= 0) {
         if (a < 0 || s[j] < prev) {
           int lo = 0, hi = nw;
@@ -185,27 +185,16 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
           while (a + 1 < nw && w[a + 1] <= s[j]) ++a;
         }
         prev = s[j];
-        qq[j] = wl[l] + a;
+        // a < 0: the record starts before the segment's first marker (the
+        // window then begins at that marker)
+        if (a >= 0 && s[j] < pe[wo[l] + a]) out[j] = pi[wo[l] + a];
       } else {
         // another gpu, or a window that did not fit (rare)
-        qq[j] = bi_upper(X, g[j] * D + l, s[j]) - 1;
+        const uint32_t sg = g[j] * D + l;
+        const int64_t q = bi_upper(X, sg, s[j]) - 1;
+        if (q >= (int64_t)X.seg[sg].sb && s[j] < sme[q]) out[j] = sid[q];
       }
     }
-    // marker ends and ids, all loads in flight before any is used
-    int64_t me[kTileIpt];
-    uint32_t id[kTileIpt];
-#pragma unroll
-    for (int j = 0; j < kTileIpt; ++j) {
-      const int64_t q = qq[j] >= sb[j] && qq[j] >= 0 ? qq[j] : 0;
-      me[j] = sme[q];
-      id[j] = sid[q];
-    }
-    uint32_t out[kTileIpt];
-#pragma unroll
-    for (int j = 0; j < kTileIpt; ++j)
-      out[j] = (((m_ok >> j) & 1u) && qq[j] >= sb[j] && s[j] < me[j])
-                   ? id[j]
-                   : kNone;
     uint32_t* dst = idx + (int64_t)l * n + k0;
     if (full && ((uintptr_t)dst & 15) == 0) {
       uint4* d4 = reinterpret_cast<uint4*>(dst);
@@ -308,10 +297,6 @@ extern "C" int chopper_attribute(const chopper_records* rec,
                        (const uint32_t*)L.sid, idx_out));
     return CHOPPER_OK;
   };
-  const bool lds = G * D <= kLdsSegs;
-  if (D <= 4)
-    return lds ? run(k_attribute_records<4, true>)
-               : run(k_attribute_records<4, false>);
-  return lds ? run(k_attribute_records<8, true>)
-             : run(k_attribute_records<8, false>);
+  if (D <= 4) return run(k_attribute_records<4>);
+  return run(k_attribute_records<8>);
 }
