@@ -35,12 +35,14 @@ def algorithmic_bytes(n, nm, rows, depth, nc, n_rows_finest):
     return rec_in + rec_out + mk + rows * row
 
 
-def roof_kernel_bytes(n, depth, nc, rows_written):
+def roof_kernel_bytes(n, depth, nc, rows_written, input_order):
     """Algorithmic bytes of one launch of the records reduction: per record
-    korder, gpu, cls, path, start, end, gap, ovl and counters read once; per
-    row it produces (the two finest levels) its header (path, gpu, kind,
-    first record) and its sums and counters written once."""
-    per_rec = 4 + 1 + 1 + 4 * depth + 8 * 4 + 8 * nc
+    gpu, cls, path, start, end, gap, ovl and counters read once (and korder
+    when the input is not grouped by GPU in start order, so that the
+    reduction reads through it); per row it produces (the two finest levels)
+    its header (path, gpu, kind, first record) and its sums and counters
+    written once."""
+    per_rec = (0 if input_order else 4) + 1 + 1 + 4 * depth + 8 * 4 + 8 * nc
     per_row = 4 * depth + 1 + 1 + 4 + 8 * (6 + nc)
     return n * per_rec + rows_written * per_row
 
@@ -97,7 +99,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-iters", type=int, default=200)
+    ap.add_argument("--cpu-iters", type=int, default=500)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run plain device copies of this many MiB (the "
                          "reference kernel for scaling HBM byte counters)")
@@ -133,7 +135,12 @@ def main():
     torch.cuda.set_device(dev)
     dt = ch.DeviceTrace(tr, dev)
     n, nm, depth, nc = tr.n, tr.n_markers, tr.depth, tr.n_counters
-    del tr
+    # records grouped by GPU and in start order inside each GPU: the
+    # reduction then reads them in input order
+    g = tr.gpu.astype(np.int64)
+    input_order = bool(np.all(np.diff(g) >= 0) and np.all(
+        (np.diff(g) != 0) | (np.diff(tr.start) >= 0)))
+    del tr, g
     torch.cuda.synchronize()
     pipe = ch.Pipeline(dt)
     for _ in range(max(args.warmup, 1)):
@@ -168,7 +175,7 @@ def main():
 
     value = n / (ms * 1e-3)
     bmin = algorithmic_bytes(n, nm, rows_total, depth, nc, rows_finest)
-    kb = roof_kernel_bytes(n, depth, nc, rows_records)
+    kb = roof_kernel_bytes(n, depth, nc, rows_records, input_order)
     achieved = kb / (kms * 1e-3) / 1e9
     out = {
         "metric": METRIC,
@@ -200,6 +207,7 @@ def main():
             "traffic": measured_traffic(ROOF_KERNEL),
             "kernel_ms": kms,
             "bytes_per_launch": kb,
+            "input_order": input_order,
         },
         "status": status,
     }
