@@ -761,17 +761,25 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads(
 
 // Fast-path level offsets: the level-major scan gives every level but the
 // workload level, whose rows are the kinds present.
+// `stage` receives the three flags and the L + 1 offsets, so that the host
+// reads them with one copy.
 __global__ void k_agg_offsets_fast(int L, int64_t ntiles,
                                    const uint32_t* tilebase,
                                    const uint32_t* total, const uint32_t* flags,
                                    bool workload, int64_t cap,
-                                   int64_t* level_offset, uint32_t* status) {
+                                   int64_t* level_offset, int64_t* stage,
+                                   uint32_t* status) {
   if (threadIdx.x != 0) return;
-  for (int li = 0; li < L; ++li)
-    level_offset[li] = ntiles > 0 ? tilebase[(int64_t)li * ntiles] : 0;
+  for (int li = 0; li < L; ++li) {
+    const int64_t v = ntiles > 0 ? tilebase[(int64_t)li * ntiles] : 0;
+    level_offset[li] = v;
+    stage[3 + li] = v;
+  }
   const int64_t tot =
       (int64_t)*total + (workload ? __popc(flags[1] & 3u) : 0);
   level_offset[L] = tot;
+  stage[3 + L] = tot;
+  for (int i = 0; i < 3; ++i) stage[i] = flags[i];
   // the counts are the row counts only when the fast path applies (and,
   // for the natural tiles, when the input order qualified)
   if (flags[0] == 0 && flags[2] == 0 && tot > cap)
@@ -1865,6 +1873,7 @@ struct AggLayout {
   int32_t* lp;
   uint8_t* tg;            // [ntiles_h + G]
   uint64_t* pair;         // [2G][kPairW] GPU row sums
+  int64_t* stage;         // flags and level offsets for the host
   uint32_t* gs;           // [G]
   uint32_t* ge;
   uint32_t* gtb;          // [G + 1]
@@ -1912,6 +1921,7 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
   L.lp = sc.take<int32_t>(2 * L.lps);
   L.tg = sc.take<uint8_t>(L.ntiles_h + G);
   L.pair = sc.take<uint64_t>((int64_t)2 * G * kPairW);
+  L.stage = sc.take<int64_t>(3 + kMaxLevels + 1);
   L.gs = sc.take<uint32_t>(G);
   L.ge = sc.take<uint32_t>(G);
   L.gtb = sc.take<uint32_t>(G + 1);
@@ -1944,12 +1954,13 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
   uint32_t hf[3] = {1u, 0u, 1u};
   int64_t lo_h[kMaxLevels + 1];
   auto read_back = [&]() -> int {
-    CHOPPER_HIP(hipMemcpyAsync(hf, L.hflags, sizeof(hf),
-                               hipMemcpyDeviceToHost, s));
-    CHOPPER_HIP(hipMemcpyAsync(lo_h, rows->level_offset,
-                               sizeof(int64_t) * (size_t)(Lv + 1),
+    int64_t st[3 + kMaxLevels + 1];
+    CHOPPER_HIP(hipMemcpyAsync(st, L.stage,
+                               sizeof(int64_t) * (size_t)(3 + Lv + 1),
                                hipMemcpyDeviceToHost, s));
     CHOPPER_HIP(hipStreamSynchronize(s));
+    for (int i = 0; i < 3; ++i) hf[i] = (uint32_t)st[i];
+    for (int i = 0; i <= Lv; ++i) lo_h[i] = st[3 + i];
     return CHOPPER_OK;
   };
   CHOPPER_HIP(launch("agg_nat_init", k_nat_init, dim3(1), dim3(kBlock), s,
@@ -1971,7 +1982,8 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
   CHOPPER_HIP(launch("agg_offsets", k_agg_offsets_fast, dim3(1), dim3(64),
                      s, Lv, L.nstride, (const uint32_t*)L.ntb,
                      (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
-                     want_workload, rows->cap, rows->level_offset, status));
+                     want_workload, rows->cap, rows->level_offset, L.stage,
+                     status));
   rc = read_back();
   if (rc != CHOPPER_OK) return rc;
   const bool nat = hf[2] == 0;
@@ -1987,7 +1999,8 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
     CHOPPER_HIP(launch("agg_offsets", k_agg_offsets_fast, dim3(1), dim3(64),
                        s, Lv, Th, (const uint32_t*)L.htb,
                        (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
-                       want_workload, rows->cap, rows->level_offset, status));
+                       want_workload, rows->cap, rows->level_offset, L.stage,
+                       status));
     rc = read_back();
     if (rc != CHOPPER_OK) return rc;
   }
