@@ -464,11 +464,19 @@ extern "C" int chopper_align(const chopper_records* rec,
   const int known = counts[2] ? -1 : 1;
   bool range_err = false, r2 = false;
   KeyRecStream ks{rec->gpu, rec->stream, start_out, L.cmap_s, (int)counts[0]};
-  rc = class_sort(ks, L.sort, order_out, L.coff, &range_err, s, known);
-  if (rc != CHOPPER_OK) return rc;
   KeyRecKind kk{rec->gpu, rec->cls, start_out, L.cmap_k, (int)counts[1]};
-  rc = class_sort(kk, L.sort, korder_out, L.coff, &r2, s, known);
-  if (rc != CHOPPER_OK) return rc;
+  if (known == 1 && counts[0] + counts[1] <= 256) {
+    // input in (gpu, start') order: both orders are class partitions,
+    // computed together
+    rc = class_sort2(ks, kk, L.sort, order_out, L.coff, korder_out,
+                     L.coff + counts[0] + 1, s);
+    if (rc != CHOPPER_OK) return rc;
+  } else {
+    rc = class_sort(ks, L.sort, order_out, L.coff, &range_err, s, known);
+    if (rc != CHOPPER_OK) return rc;
+    rc = class_sort(kk, L.sort, korder_out, L.coff, &r2, s, known);
+    if (rc != CHOPPER_OK) return rc;
+  }
   if (range_err || r2) {
     // fold the host-detected condition into the device status word
     CHOPPER_HIP(launch("status_set", k_status_set, dim3(1), dim3(1), s,

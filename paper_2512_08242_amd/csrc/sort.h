@@ -85,6 +85,14 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
                uint32_t* coff, bool* range_error, hipStream_t s,
                int known_sorted);
 
+// Both class partitions of the same n > 0 items at once, for input ordered
+// by (major, time) (so the partitions are the stable sorts); needs
+// a.nclass() + b.nclass() <= 256.
+template <typename AccA, typename AccB>
+int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
+                uint32_t* outA, uint32_t* coffA, uint32_t* outB,
+                uint32_t* coffB, hipStream_t s);
+
 __global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v);
 __global__ void k_status_set(uint32_t bits, uint32_t* status);
 

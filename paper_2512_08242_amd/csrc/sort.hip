@@ -471,6 +471,140 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
   return CHOPPER_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Two class partitions of the same items, for input already ordered by
+// (major, time): one histogram pass fills both tables (A's classes, then
+// B's), one scan covers both, one pass writes both permutations.
+// ---------------------------------------------------------------------------
+template <typename AccA, typename AccB>
+__global__ __launch_bounds__(kBlock) void k_class_hist2(AccA a, AccB b,
+                                                        int64_t n,
+                                                        int64_t ntiles,
+                                                        uint32_t* tilehist) {
+  __shared__ uint32_t h[2][256];
+  h[0][threadIdx.x] = 0;
+  h[1][threadIdx.x] = 0;
+  __syncthreads();
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  const int nb[2] = {class_bits(a.nclass()), class_bits(b.nclass())};
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j) {
+    const int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
+    const bool v = i < n;
+    const uint32_t d[2] = {v ? a.cls(i) : 0u, v ? b.cls(i) : 0u};
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      uint64_t peers = __ballot(v);
+      for (int bb = 0; bb < nb[q]; ++bb) {
+        const bool bit = (d[q] >> bb) & 1u;
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+      }
+      if (v && __popcll(peers & lt) == 0)
+        atomicAdd(&h[q][d[q]], (uint32_t)__popcll(peers));
+    }
+  }
+  __syncthreads();
+  const int CA = a.nclass();
+  if ((int)threadIdx.x < CA)
+    tilehist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[0][threadIdx.x];
+  if ((int)threadIdx.x < b.nclass())
+    tilehist[(int64_t)(CA + threadIdx.x) * ntiles + blockIdx.x] =
+        h[1][threadIdx.x];
+}
+
+template <typename AccA, typename AccB>
+__global__ __launch_bounds__(kBlock) void k_class_partition2(
+    AccA a, AccB b, int64_t n, int64_t ntiles, const uint32_t* tileoff,
+    uint32_t* outA, uint32_t* outB) {
+  __shared__ RankShared sh;
+  __shared__ uint32_t s_val[kSortTile];
+  __shared__ uint8_t s_dig[kSortTile];
+  __shared__ uint32_t s_gbase[256];
+  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  const int64_t tile_n = (n - base) < kSortTile ? (n - base) : kSortTile;
+  uint32_t da[kSortIpt], db[kSortIpt], rank[kSortIpt];
+  bool valid[kSortIpt];
+  for (int j = 0; j < kSortIpt; ++j) {
+    const int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
+    valid[j] = i < n;
+    da[j] = valid[j] ? a.cls(i) : 0u;
+    db[j] = valid[j] ? b.cls(i) : 0u;
+  }
+  const int CA = a.nclass();
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const uint32_t(&dig)[kSortIpt] = q == 0 ? da : db;
+    const int C = q == 0 ? CA : b.nclass();
+    tile_rank(dig, valid, rank, sh, class_bits(C));
+    // B's rows of the table follow A's; its scanned values include A's n
+    const int64_t row0 = q == 0 ? 0 : CA;
+    const uint32_t sub = q == 0 ? 0u : (uint32_t)n;
+    if ((int)threadIdx.x < C)
+      s_gbase[threadIdx.x] =
+          tileoff[(row0 + threadIdx.x) * ntiles + blockIdx.x] - sub;
+    for (int j = 0; j < kSortIpt; ++j) {
+      if (!valid[j]) continue;
+      const uint32_t lp = sh.start[dig[j]] + rank[j];
+      s_val[lp] = (uint32_t)(base + (int64_t)j * kBlock + threadIdx.x);
+      s_dig[lp] = (uint8_t)dig[j];
+    }
+    __syncthreads();
+    uint32_t* out = q == 0 ? outA : outB;
+    for (int j = 0; j < kSortIpt; ++j) {
+      const int qq = j * kBlock + threadIdx.x;
+      if (qq >= tile_n) continue;
+      const uint32_t d = s_dig[qq];
+      out[(int64_t)s_gbase[d] + (qq - sh.start[d])] = s_val[qq];
+    }
+    __syncthreads();
+  }
+}
+
+// class start offsets of both sorts from the scanned table
+__global__ void k_class_offsets2(const uint32_t* tileoff, int64_t ntiles,
+                                 int CA, int CB, int64_t n, uint32_t* coffA,
+                                 uint32_t* coffB) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c < CA) coffA[c] = ntiles > 0 ? tileoff[(int64_t)c * ntiles] : 0u;
+  if (c == CA) coffA[CA] = (uint32_t)n;
+  if (c < CB)
+    coffB[c] = ntiles > 0 ? tileoff[(int64_t)(CA + c) * ntiles] - (uint32_t)n
+                          : 0u;
+  if (c == CB) coffB[CB] = (uint32_t)n;
+}
+
+template <typename AccA, typename AccB>
+int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
+                uint32_t* outA, uint32_t* coffA, uint32_t* outB,
+                uint32_t* coffB, hipStream_t s) {
+  const int64_t n = L.n;
+  const int CA = a.nclass(), CB = b.nclass();
+  const int64_t T = L.ntiles;
+  if (n == 0 || CA > 256 || CB > 256 || CA + CB > 256)
+    return CHOPPER_EINVAL;
+  CHOPPER_HIP(launch("sort_class_hist", k_class_hist2<AccA, AccB>,
+                     dim3((unsigned)T), dim3(kBlock), s, a, b, n, T,
+                     L.tilehist));
+  CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, L.tileoff,
+                                       (int64_t)(CA + CB) * T, L.scantmp,
+                                       L.total, s));
+  CHOPPER_HIP(launch("sort_class_offsets", k_class_offsets2,
+                     grid_for((CA > CB ? CA : CB) + 1, kBlock), dim3(kBlock),
+                     s, (const uint32_t*)L.tileoff, T, CA, CB, n, coffA,
+                     coffB));
+  CHOPPER_HIP(launch("sort_class_partition", k_class_partition2<AccA, AccB>,
+                     dim3((unsigned)T), dim3(kBlock), s, a, b, n, T,
+                     (const uint32_t*)L.tileoff, outA, outB));
+  return CHOPPER_OK;
+}
+
+template int class_sort2<KeyRecStream, KeyRecKind>(
+    const KeyRecStream&, const KeyRecKind&, const ClassSortLayout&, uint32_t*,
+    uint32_t*, uint32_t*, uint32_t*, hipStream_t);
+
 template int class_sort<KeyRecStream>(const KeyRecStream&,
                                       const ClassSortLayout&, uint32_t*,
                                       uint32_t*, bool*, hipStream_t, int);
