@@ -1562,13 +1562,14 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
   };
 
   const int ns = src.nsum();
-  uint64_t va[kAggIpt], vb[kAggIpt];
+  // three plain-sum columns in flight: each is loaded three fields ahead of
+  // its use (the first ones staggered between the special fields)
+  uint64_t va[kAggIpt], vb[kAggIpt], vc[kAggIpt];
   {
-    // the two plain-sum prefetches are staggered between the special
-    // fields to bound the live registers
     uint64_t ts[kAggIpt], te[kAggIpt];
     load((const uint64_t*)src.start_col(), ts);
     load((const uint64_t*)src.end_col(), te);
+    if (ns > 0) load(src.sum_col(0), va);
     if constexpr (Src::kRecords) {
       // n: the prefix of ones at a piece's last item is its position + 1
       uint64_t pos[kAggIpt];
@@ -1584,21 +1585,25 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
       uint64_t du[kAggIpt];
 #pragma unroll
       for (int j = 0; j < kAggIpt; ++j) du[j] = te[j] - ts[j];
-      if (ns > 0) load(src.sum_col(0), va);
+      if (ns > 1) load(src.sum_col(1), vb);
       do_sum(du, 1);
     } else {
-      if (ns > 0) load(src.sum_col(0), va);
+      if (ns > 1) load(src.sum_col(1), vb);
     }
     do_seg(ts, 4, CMin());
-    if (ns > 1) load(src.sum_col(1), vb);
+    if (ns > 2) load(src.sum_col(2), vc);
     do_seg(te, 5, CMax());
   }
-  for (int i = 0; i < ns; i += 2) {
+  for (int i = 0; i < ns; i += 3) {
     do_sum(va, src.sum_dst(i));
-    if (i + 2 < ns) load(src.sum_col(i + 2), va);
+    if (i + 3 < ns) load(src.sum_col(i + 3), va);
     if (i + 1 < ns) {
       do_sum(vb, src.sum_dst(i + 1));
-      if (i + 3 < ns) load(src.sum_col(i + 3), vb);
+      if (i + 4 < ns) load(src.sum_col(i + 4), vb);
+    }
+    if (i + 2 < ns) {
+      do_sum(vc, src.sum_dst(i + 2));
+      if (i + 5 < ns) load(src.sum_col(i + 5), vc);
     }
   }
 }
