@@ -972,7 +972,7 @@ __global__ __launch_bounds__(kBlock) void k_nat_pre(
 
 // One block: GPU ranges, tile offsets and the GPU of every tile, and the
 // exclusive running maximum of the last-position table.
-constexpr int kLpChunk = 32;      // table entries per thread and pass
+constexpr int kLpChunk = 48;      // table entries per thread and pass
 __global__ __launch_bounds__(1024) void k_nat_tiles(
     int64_t n, int G, int64_t nnt, int64_t lps, const int32_t* lpraw,
     int32_t* lp, const uint32_t* gs, uint32_t* ge, uint32_t* tb, uint8_t* tg,

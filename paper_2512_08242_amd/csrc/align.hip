@@ -341,6 +341,14 @@ __global__ __launch_bounds__(kDenseThreads) void k_dense_classes(
   if (t == 0) counts[1] = totk;
 }
 
+// presence flags (65536 + 512 bytes) and the class counts to zero
+__global__ __launch_bounds__(kBlock) void k_align_clear(uint32_t* pres,
+                                                        uint32_t* counts) {
+  const int i = (int)(blockIdx.x * kBlock + threadIdx.x);
+  if (i < 16384 + 128) pres[i] = 0;
+  if (i < 4) counts[i] = 0;
+}
+
 // ---------------------------------------------------------------------------
 // Entry point
 // ---------------------------------------------------------------------------
@@ -441,11 +449,9 @@ extern "C" int chopper_align(const chopper_records* rec,
                        (const ClockDev*)L.clk, mstart_out, mend_out, status));
   }
   if (n == 0) return CHOPPER_OK;
-  CHOPPER_HIP(launch("align_fill", k_fill_u32, grid_for(16384 + 128, kBlock),
-                     dim3(kBlock), s, reinterpret_cast<uint32_t*>(L.pres_s),
-                     (int64_t)(16384 + 128), 0u));
-  CHOPPER_HIP(launch("align_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
-                     L.counts, (int64_t)4, 0u));
+  CHOPPER_HIP(launch("align_fill", k_align_clear,
+                     grid_for(16384 + 128, kBlock), dim3(kBlock), s,
+                     reinterpret_cast<uint32_t*>(L.pres_s), L.counts));
   CHOPPER_HIP(launch("align_transform_records", k_transform_records,
                      dim3((unsigned)ceil_div(n, (int64_t)kWaveTile *
                                                     kWavesPerBlock)),

@@ -178,7 +178,7 @@ __global__ __launch_bounds__(kBlock) void k_runs_tile_max(
 template <typename T, typename Op>
 __global__ __launch_bounds__(1024) void k_tile_spine(T* tile, int64_t ntiles,
                                                      T ident, T* total) {
-  constexpr int kIpt = 8;
+  constexpr int kIpt = 16;   // one pass up to 16384 tiles (33.5M records)
   constexpr int kT = 1024;
   __shared__ T s_w[kT / kWave];
   Op op;
