@@ -145,35 +145,6 @@ __device__ inline void korder_gather(const uint32_t* korder, const uint8_t* gpu,
   e = x > s ? x : s;
 }
 
-// Tile aggregate of (seg, end) under the lexicographic max: the last segment
-// of the tile and the largest end among its items.  Order does not matter.
-__global__ __launch_bounds__(kBlock) void k_runs_tile_max(
-    int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
-    const int64_t* start, const int64_t* end, SegMax* tile_agg) {
-  const int64_t base = (int64_t)blockIdx.x * kOvTile;
-  OpSegMax op;
-  SegMax acc = segmax_ident();
-#pragma unroll
-  for (int j = 0; j < kOvIpt; ++j) {
-    const int64_t p = base + (int64_t)j * kBlock + threadIdx.x;
-    if (p < n) {
-      uint32_t seg;
-      int64_t s, e;
-      korder_gather(korder, gpu, cls, start, end, p, seg, s, e);
-      acc = op(acc, SegMax{seg, e});
-    }
-  }
-  acc = wave_incl(acc, op, segmax_ident());
-  __shared__ SegMax s_w[kWavesPerBlock];
-  if (lane_id() == kWave - 1) s_w[threadIdx.x / kWave] = acc;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    SegMax t = s_w[0];
-    for (int i = 1; i < kWavesPerBlock; ++i) t = op(t, s_w[i]);
-    tile_agg[blockIdx.x] = t;
-  }
-}
-
 // In-place exclusive scan of per-tile values in one block; also the total.
 template <typename T, typename Op>
 __global__ __launch_bounds__(1024) void k_tile_spine(T* tile, int64_t ntiles,
@@ -224,6 +195,7 @@ struct RunItems {
   int64_t inc[kTileIpt];
   uint32_t m_valid, m_head, m_newseg;
   uint32_t pseg0;           // segment of the item before the lane's first
+  SegMax wagg;              // (segment, end) maximum of the wave's items
 };
 
 __device__ inline void run_items(int64_t n, const uint32_t* korder,
@@ -262,10 +234,11 @@ __device__ inline void run_items(int64_t n, const uint32_t* korder,
   }
   // lane tails scanned over the wave, then the waves of the block in order
   const SegMax incl = wave_incl(acc, op, segmax_ident());
+  it.wagg = lane63(incl);
   __shared__ SegMax s_w[kWavesPerBlock];
   if (lane == kWave - 1) s_w[wv] = incl;
   __syncthreads();
-  SegMax pre = tile_pre[blockIdx.x];
+  SegMax pre = tile_pre ? tile_pre[blockIdx.x] : segmax_ident();
   for (int i = 0; i < kWavesPerBlock; ++i)
     if (i < wv) pre = op(pre, s_w[i]);
   pre = op(pre, wave_shr1_any(segmax_ident(), incl));
@@ -296,11 +269,22 @@ __device__ inline void run_items(int64_t n, const uint32_t* korder,
 }
 
 // Number of runs (heads) and the segmented sum of union increments per tile.
+// First pass (tile_pre null): counted as if no earlier item reached into
+// the tile, and also the tile's (segment, end) maximum and its first item
+// (segment, start).  Fix-up pass (tile_pre = exclusive maxima): only tiles
+// whose carry has their first item's segment and reaches its start count
+// again; for the others the first count is exact, since every item of the
+// first segment then starts after the carry.
 __global__ __launch_bounds__(kBlock) void k_runs_count(
     int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
     const int64_t* start, const int64_t* end, const SegMax* tile_pre,
-    uint32_t* tile_heads, SegSum* tile_inc) {
+    SegMax* tile_agg, SegMax* tile_first, uint32_t* tile_heads,
+    SegSum* tile_inc) {
   __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
+  if (tile_pre) {
+    const SegMax c = tile_pre[blockIdx.x], f = tile_first[blockIdx.x];
+    if (!(c.seg == f.seg && c.val >= f.val)) return;   // block-uniform
+  }
   RunItems it;
   run_items(n, korder, gpu, cls, start, end, tile_pre,
             s_slice[threadIdx.x / kWave], it);
@@ -312,24 +296,35 @@ __global__ __launch_bounds__(kBlock) void k_runs_count(
   acc = wave_incl(acc, op, segsum_ident());
   uint32_t c = (uint32_t)__popc(it.m_head);
   for (int d = kWave / 2; d > 0; d >>= 1) c += __shfl_xor(c, d, kWave);
+  // the tile's (segment, end) maximum from the waves' ones
+  OpSegMax om;
+  const SegMax mx = it.wagg;
   __shared__ SegSum s_w[kWavesPerBlock];
   __shared__ uint32_t s_c[kWavesPerBlock];
+  __shared__ SegMax s_m[kWavesPerBlock];
   const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
   if (lane == kWave - 1) {
     s_w[wv] = acc;
     s_c[wv] = c;
+    s_m[wv] = mx;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     SegSum t = s_w[0];
     uint32_t tc = s_c[0];
+    SegMax tm = s_m[0];
     for (int i = 1; i < kWavesPerBlock; ++i) {
       t = op(t, s_w[i]);
       tc += s_c[i];
+      tm = om(tm, s_m[i]);
     }
     tile_heads[blockIdx.x] = tc;
     tile_inc[blockIdx.x] = t;
+    if (!tile_pre) tile_agg[blockIdx.x] = tm;
   }
+  // the tile's first item (blocked arrangement: lane 0, item 0 of wave 0)
+  if (!tile_pre && threadIdx.x == 0)
+    tile_first[blockIdx.x] = SegMax{it.seg[0], it.s[0]};
 }
 
 // Writes the runs: start, segment and union length before the run (the
@@ -766,6 +761,7 @@ __global__ __launch_bounds__(kBlock) void k_gap(
 struct OverlapLayout {
   int64_t ntiles;
   SegMax* tile_agg;
+  SegMax* tile_first;   // first item of every tile: (segment, start)
   SegMax* grand;
   uint32_t* tile_heads;
   SegSum* tile_inc;
@@ -795,6 +791,7 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   OverlapLayout L;
   L.ntiles = ceil_div(n, kOvTile);
   L.tile_agg = sc.take<SegMax>(L.ntiles);
+  L.tile_first = sc.take<SegMax>(L.ntiles);
   L.grand = sc.take<SegMax>(1);
   L.tile_heads = sc.take<uint32_t>(L.ntiles);
   L.tile_inc = sc.take<SegSum>(L.ntiles);
@@ -858,15 +855,17 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                      dim3(kBlock), s, L.rbeg, (int64_t)(2 * kSegs), 0u));
   if (n > 0) {
     // union runs of every (gpu, kind)
-    CHOPPER_HIP(launch("ov_runs_tile_max", k_runs_tile_max, dim3(T),
-                       dim3(kBlock), s, n, korder, rec->gpu, rec->cls,
-                       start_al, end_al, L.tile_agg));
+    CHOPPER_HIP(launch("ov_runs_count", k_runs_count, dim3(T), dim3(kBlock), s,
+                       n, korder, rec->gpu, rec->cls, start_al, end_al,
+                       (const SegMax*)nullptr, L.tile_agg, L.tile_first,
+                       L.tile_heads, L.tile_inc));
     CHOPPER_HIP(launch("ov_runs_spine", k_tile_spine<SegMax, OpSegMax>,
                        dim3(1), dim3(1024), s, L.tile_agg, L.ntiles,
                        SegMax{0u, kI64Min}, L.grand));
-    CHOPPER_HIP(launch("ov_runs_count", k_runs_count, dim3(T), dim3(kBlock), s,
+    CHOPPER_HIP(launch("ov_runs_fixup", k_runs_count, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
-                       (const SegMax*)L.tile_agg, L.tile_heads, L.tile_inc));
+                       (const SegMax*)L.tile_agg, (SegMax*)nullptr,
+                       L.tile_first, L.tile_heads, L.tile_inc));
     CHOPPER_HIP(exclusive_scan<uint32_t>(L.tile_heads, L.tile_run0, L.ntiles,
                                          L.scan_u32, L.nruns, s));
     CHOPPER_HIP(launch("ov_runs_inc_spine", k_tile_spine<SegSum, OpSegSum>,

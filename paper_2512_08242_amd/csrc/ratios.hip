@@ -18,7 +18,7 @@ static const char* const kKernelNames[] = {
     "sort_class_verify", "sort_class_offsets", "sort_digit_hist",
     "sort_digit_scatter", "sort_make_keys", "sort_time_minmax",
     "attr_marker_gather", "attr_marker_links", "attr_records",
-    "ov_runs_tile_max", "ov_runs_spine", "ov_runs_count", "ov_runs_write",
+    "ov_runs_fixup", "ov_runs_spine", "ov_runs_count", "ov_runs_write",
     "ov_runs_inc_spine", "ov_runs_comm_overlap", "ov_records", "ov_markers",
     "ov_gpus", "ov_gap",
     "agg_fill_owner", "agg_elect", "agg_count", "agg_offsets", "agg_assign",
