@@ -89,32 +89,76 @@ __global__ __launch_bounds__(kBlock) void k_bi_clear(uint32_t* table,
   if (e < (int64_t)*total) table[e] = kUnset;
 }
 
+// Eight consecutive keys per thread (vector loads when the chunk is whole
+// and aligned); the segment parameters come from LDS when they fit.
+constexpr int kFillIpt = 8;
+constexpr int kFillLdsSegs = 512;
 __global__ __launch_bounds__(kBlock) void k_bi_fill(
     const int64_t* key, const uint32_t* keyseg, int64_t nkeys,
-    const uint32_t* nkeys_dev, const BSeg* segs, uint32_t* table) {
-  const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (i >= nkeys || (nkeys_dev && i >= (int64_t)*nkeys_dev)) return;
-  const uint32_t sidx = keyseg[i];
-  if (sidx == kNone) return;
-  const BSeg P = segs[sidx];
-  if (P.nb == 0 || i < P.sb || i >= P.se) return;
-  // bucket of a key, clamped to the table (keys are sorted, so the clamp
-  // only guards against inputs that are not)
-  auto bucket = [&](int64_t k) -> int64_t {
-    const uint64_t d = (uint64_t)k - (uint64_t)P.lo;
-    if ((int64_t)d < 0) return 0;
-    const uint64_t b = d >> P.shift;
-    return b < (uint64_t)P.nb ? (int64_t)b : (int64_t)P.nb - 1;
-  };
-  const int64_t bi = bucket(key[i]);
-  const int64_t bp = i == P.sb ? -1 : bucket(key[i - 1]);
-  uint32_t* tb = table + P.toff;
-  const int64_t hi1 = bi < bp + kFillRun ? bi : bp + kFillRun;
-  for (int64_t b = bp + 1; b <= hi1; ++b) tb[b] = (uint32_t)i;
-  if (i == (int64_t)P.se - 1) {
-    const int64_t hi2 =
-        (int64_t)P.nb < bi + kFillRun ? (int64_t)P.nb : bi + kFillRun;
-    for (int64_t b = bi + 1; b <= hi2; ++b) tb[b] = P.se;
+    const uint32_t* nkeys_dev, const BSeg* segs, int nseg, uint32_t* table) {
+  __shared__ BSeg s_seg[kFillLdsSegs];
+  const bool lds = nseg <= kFillLdsSegs;
+  if (lds) {
+    for (int i = threadIdx.x; i < nseg; i += kBlock) s_seg[i] = segs[i];
+    __syncthreads();
+  }
+  int64_t nk = nkeys;
+  if (nkeys_dev && (int64_t)*nkeys_dev < nk) nk = (int64_t)*nkeys_dev;
+  const int64_t i0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kFillIpt;
+  if (i0 >= nk) return;
+  int64_t k[kFillIpt + 1];
+  uint32_t sg[kFillIpt];
+  const bool whole = i0 + kFillIpt <= nk && ((uintptr_t)key & 15) == 0 &&
+                     ((uintptr_t)keyseg & 15) == 0;
+  if (whole) {
+#pragma unroll
+    for (int j = 0; j < kFillIpt; j += 2) {
+      const longlong2 v = *(const longlong2*)(key + i0 + j);
+      k[j + 1] = v.x;
+      k[j + 2] = v.y;
+    }
+#pragma unroll
+    for (int j = 0; j < kFillIpt; j += 4) {
+      const uint4 v = *(const uint4*)(keyseg + i0 + j);
+      sg[j] = v.x;
+      sg[j + 1] = v.y;
+      sg[j + 2] = v.z;
+      sg[j + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kFillIpt; ++j) {
+      const bool in = i0 + j < nk;
+      k[j + 1] = in ? key[i0 + j] : 0;
+      sg[j] = in ? keyseg[i0 + j] : kNone;
+    }
+  }
+  k[0] = i0 > 0 ? key[i0 - 1] : 0;
+#pragma unroll
+  for (int j = 0; j < kFillIpt; ++j) {
+    const int64_t i = i0 + j;
+    const uint32_t sidx = sg[j];
+    if (sidx == kNone || sidx >= (uint32_t)nseg) continue;
+    const BSeg P = lds ? s_seg[sidx] : segs[sidx];
+    if (P.nb == 0 || i < P.sb || i >= P.se) continue;
+    // bucket of a key, clamped to the table (keys are sorted, so the clamp
+    // only guards against inputs that are not)
+    auto bucket = [&](int64_t kv) -> int64_t {
+      const uint64_t d = (uint64_t)kv - (uint64_t)P.lo;
+      if ((int64_t)d < 0) return 0;
+      const uint64_t b = d >> P.shift;
+      return b < (uint64_t)P.nb ? (int64_t)b : (int64_t)P.nb - 1;
+    };
+    const int64_t bi = bucket(k[j + 1]);
+    const int64_t bp = i == P.sb ? -1 : bucket(k[j]);
+    uint32_t* tb = table + P.toff;
+    const int64_t hi1 = bi < bp + kFillRun ? bi : bp + kFillRun;
+    for (int64_t b = bp + 1; b <= hi1; ++b) tb[b] = (uint32_t)i;
+    if (i == (int64_t)P.se - 1) {
+      const int64_t hi2 =
+          (int64_t)P.nb < bi + kFillRun ? (int64_t)P.nb : bi + kFillRun;
+      for (int64_t b = bi + 1; b <= hi2; ++b) tb[b] = P.se;
+    }
   }
 }
 
@@ -172,8 +216,9 @@ hipError_t bindex_build(const int64_t* key, const uint32_t* keyseg,
              s, table, (const uint32_t*)total);
   if (e != hipSuccess) return e;
   if (nkeys > 0) {
-    e = launch("bi_fill", k_bi_fill, grid_for(nkeys, kBlock), dim3(kBlock), s,
-               key, keyseg, nkeys, nkeys_dev, (const BSeg*)segs, table);
+    e = launch("bi_fill", k_bi_fill, grid_for(nkeys, kBlock * kFillIpt),
+               dim3(kBlock), s, key, keyseg, nkeys, nkeys_dev,
+               (const BSeg*)segs, nseg, table);
     if (e != hipSuccess) return e;
   }
   return launch("bi_fixup", k_bi_fixup, grid_for(table_cap, kBlock),
