@@ -449,26 +449,36 @@ __global__ void k_comm_voff(int G, const BSeg* segs, uint32_t* voff) {
 }
 
 // overlapped time inside each comm run (compute-active time within it) and
-// the compute-active time before it, at the run's dense index
+// the compute-active time before it, at the run's dense index; a fixed grid
+// strides over the dense indices of all GPUs
+constexpr int kCommGrid = 2048;
 __global__ __launch_bounds__(kBlock) void k_runs_comm_overlap(
-    const uint32_t* nruns, Runs R, const uint32_t* rseg, int64_t* ovc,
-    int64_t* fcrs, int64_t cap, int nseg) {
+    Runs R, int G, int64_t* ovc, int64_t* fcrs) {
   __shared__ BSeg s_seg[kSegs];
-  segs_to_lds(s_seg, R.X.seg, nseg);
-  const int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (r >= cap || r >= (int64_t)*nruns) return;
-  const uint32_t seg = rseg[r];
-  if (!(seg & 1u)) return;
-  const BSeg P = s_seg[seg - 1u];
-  const int64_t t[2] = {R.rs[r], R.re[r]};
-  int64_t lo[2], hi[2];
-  bi_range(R.X, P, t[0], &lo[0], &hi[0]);
-  bi_range(R.X, P, t[1], &lo[1], &hi[1]);
-  bsearch_k<2>(R.rs, lo, hi, t);
-  const int64_t f = F_at(R, P, lo[0], t[0]);
-  const int64_t v = (int64_t)R.voff[seg >> 1] + (r - (int64_t)s_seg[seg].sb);
-  ovc[v] = F_at(R, P, lo[1], t[1]) - f;
-  fcrs[v] = f;
+  __shared__ uint32_t s_voff[kSegs / 2 + 1];
+  for (int i = threadIdx.x; i <= G; i += kBlock) s_voff[i] = R.voff[i];
+  segs_to_lds(s_seg, R.X.seg, 2 * G);
+  const int64_t total = s_voff[G];
+  for (int64_t v = (int64_t)blockIdx.x * kBlock + threadIdx.x; v < total;
+       v += (int64_t)gridDim.x * kBlock) {
+    // gpu of dense index v: the last g with voff[g] <= v
+    int lo = 0, hi = G;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if ((int64_t)s_voff[mid] <= v) lo = mid;
+      else hi = mid;
+    }
+    const BSeg P = s_seg[2 * lo];
+    const int64_t r = (int64_t)s_seg[2 * lo + 1].sb + (v - s_voff[lo]);
+    const int64_t t[2] = {R.rs[r], R.re[r]};
+    int64_t l2[2], h2[2];
+    bi_range(R.X, P, t[0], &l2[0], &h2[0]);
+    bi_range(R.X, P, t[1], &l2[1], &h2[1]);
+    bsearch_k<2>(R.rs, l2, h2, t);
+    const int64_t f = F_at(R, P, l2[0], t[0]);
+    ovc[v] = F_at(R, P, l2[1], t[1]) - f;
+    fcrs[v] = f;
+  }
 }
 
 // ---------------- queries ----------------------------------------------------
@@ -886,10 +896,10 @@ extern "C" int chopper_overlap(const chopper_records* rec,
   CHOPPER_HIP(launch("ov_comm_voff", k_comm_voff, dim3(1), dim3(64), s, G,
                      (const BSeg*)L.bsegs, L.voff));
   if (n > 0) {
+    const int64_t cg = ceil_div(n, (int64_t)kBlock);
     CHOPPER_HIP(launch("ov_runs_comm_overlap", k_runs_comm_overlap,
-                       grid_for(n, kBlock), dim3(kBlock), s,
-                       (const uint32_t*)L.nruns, R, (const uint32_t*)L.rseg,
-                       L.ovc, L.fcrs, n, 2 * G));
+                       dim3((unsigned)(cg < kCommGrid ? cg : kCommGrid)),
+                       dim3(kBlock), s, R, G, L.ovc, L.fcrs));
     CHOPPER_HIP(exclusive_scan<int64_t>(L.ovc, L.pov, n,
                                         (const uint32_t*)(L.voff + G),
                                         L.scan_i64, L.tot_i64 + 1, s));
