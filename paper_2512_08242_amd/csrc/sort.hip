@@ -35,6 +35,30 @@ int64_t sort_tiles(int64_t n) { return ceil_div(n, kSortTile); }
 // start[d] = exclusive prefix of count, rank[j] = stable position of the
 // item among equal digits.
 // ---------------------------------------------------------------------------
+// Lanes among those with v that hold the same digit as this lane.  Rows of
+// one or two distinct digits -- the usual case for classes of consecutive
+// records -- take two or three ballots; other rows match bit by bit.
+__device__ inline uint64_t digit_peers(uint32_t d, bool v, int nbits) {
+  const uint64_t vm = __ballot(v);
+  if (vm == 0) return 0;
+  const uint32_t d0 = (uint32_t)__shfl((int)d, __ffsll((long long)vm) - 1,
+                                       kWave);
+  const uint64_t m0 = __ballot(v && d == d0);
+  if (m0 == vm) return vm;
+  const uint64_t rest = vm & ~m0;
+  const uint32_t d1 = (uint32_t)__shfl((int)d, __ffsll((long long)rest) - 1,
+                                       kWave);
+  const uint64_t m1 = __ballot(v && d == d1);
+  if ((m0 | m1) == vm) return d == d0 ? m0 : m1;
+  uint64_t peers = vm;
+  for (int b = 0; b < nbits; ++b) {
+    const bool bit = (d >> b) & 1u;
+    const uint64_t bb = __ballot(bit);
+    peers &= bit ? bb : ~bb;
+  }
+  return peers;
+}
+
 struct RankShared {
   uint16_t cell[kSortIpt][kWavesPerBlock][256];   // counts, then prefixes
   uint32_t count[256];
@@ -60,12 +84,7 @@ __device__ inline void tile_rank(const uint32_t (&dig)[kSortIpt],
   for (int j = 0; j < kSortIpt; ++j) {
     const uint32_t d = dig[j];
     const bool v = valid[j];
-    uint64_t peers = __ballot(v);
-    for (int b = 0; b < nbits; ++b) {
-      const bool bit = (d >> b) & 1u;
-      const uint64_t bb = __ballot(bit);
-      peers &= bit ? bb : ~bb;
-    }
+    const uint64_t peers = digit_peers(d, v, nbits);
     rin[j] = __popcll(peers & lt);
     if (v && rin[j] == 0) sh.cell[j][w][d] = (uint16_t)__popcll(peers);
   }
@@ -124,12 +143,7 @@ __global__ __launch_bounds__(kBlock) void k_class_hist(Acc acc, int64_t n,
   // one LDS add per distinct class of every wave-row
 #pragma unroll
   for (int j = 0; j < kSortIpt; ++j) {
-    uint64_t peers = __ballot(v[j]);
-    for (int b = 0; b < nbits; ++b) {
-      const bool bit = (d[j] >> b) & 1u;
-      const uint64_t bb = __ballot(bit);
-      peers &= bit ? bb : ~bb;
-    }
+    const uint64_t peers = digit_peers(d[j], v[j], nbits);
     if (v[j] && __popcll(peers & lt) == 0)
       atomicAdd(&h[d[j]], (uint32_t)__popcll(peers));
   }
@@ -496,12 +510,7 @@ __global__ __launch_bounds__(kBlock) void k_class_hist2(AccA a, AccB b,
     const uint32_t d[2] = {v ? a.cls(i) : 0u, v ? b.cls(i) : 0u};
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      uint64_t peers = __ballot(v);
-      for (int bb = 0; bb < nb[q]; ++bb) {
-        const bool bit = (d[q] >> bb) & 1u;
-        const uint64_t m = __ballot(bit);
-        peers &= bit ? m : ~m;
-      }
+      const uint64_t peers = digit_peers(d[q], v, nb[q]);
       if (v && __popcll(peers & lt) == 0)
         atomicAdd(&h[q][d[q]], (uint32_t)__popcll(peers));
     }
