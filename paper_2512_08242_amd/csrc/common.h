@@ -161,6 +161,21 @@ inline hipError_t launch(const char* name, Kern kern, dim3 grid, dim3 block,
   return e;
 }
 
+// the same with `shm` bytes of dynamic LDS
+template <typename Kern, typename... Args>
+inline hipError_t launch_shm(const char* name, Kern kern, dim3 grid,
+                             dim3 block, size_t shm, hipStream_t s,
+                             Args... args) {
+  if (grid.x == 0 || grid.y == 0 || grid.z == 0) return hipSuccess;
+  TimerHook& h = timer_hook();
+  bool timed = h.name && strcmp(h.name, name) == 0;
+  if (timed) (void)hipEventRecord(h.start, s);
+  hipLaunchKernelGGL(kern, grid, block, shm, s, args...);
+  hipError_t e = hipGetLastError();
+  if (timed) (void)hipEventRecord(h.stop, s);
+  return e;
+}
+
 inline dim3 grid_for(int64_t items, int per_block) {
   int64_t b = ceil_div(items, per_block);
   return dim3((unsigned)(b > 0 ? b : 0));

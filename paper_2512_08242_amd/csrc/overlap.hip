@@ -454,7 +454,7 @@ __global__ void k_comm_voff(int G, const BSeg* segs, uint32_t* voff) {
 constexpr int kCommGrid = 2048;
 __global__ __launch_bounds__(kBlock) void k_runs_comm_overlap(
     Runs R, int G, int64_t* ovc, int64_t* fcrs) {
-  __shared__ BSeg s_seg[kSegs];
+  extern __shared__ BSeg s_seg[];   // 2G entries (dynamic LDS)
   __shared__ uint32_t s_voff[kSegs / 2 + 1];
   for (int i = threadIdx.x; i <= G; i += kBlock) s_voff[i] = R.voff[i];
   segs_to_lds(s_seg, R.X.seg, 2 * G);
@@ -496,7 +496,7 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
     int64_t n, int G, const uint32_t* korder, const uint8_t* gpu,
     const uint8_t* cls, const int64_t* start, const int64_t* end, Runs R,
     int64_t* ovl) {
-  __shared__ BSeg s_seg[kSegs];
+  extern __shared__ BSeg s_seg[];   // 2G entries (dynamic LDS)
   __shared__ int64_t s_win[kWavesPerBlock][3][kRunWin];
   segs_to_lds(s_seg, R.X.seg, 2 * G);
   const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
@@ -603,7 +603,7 @@ constexpr int kMarkPerThread = 1;
 __global__ __launch_bounds__(kBlock) void k_overlap_markers(
     int64_t nm, int G, const uint8_t* mgpu, const int64_t* ms,
     const int64_t* me, Runs R, int64_t* mwin) {
-  __shared__ BSeg s_seg[kSegs];
+  extern __shared__ BSeg s_seg[];   // 2G entries (dynamic LDS)
   segs_to_lds(s_seg, R.X.seg, 2 * G);
   const int64_t j0 =
       (int64_t)blockIdx.x * kBlock * kMarkPerThread + threadIdx.x;
@@ -893,26 +893,29 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                            L.bsegs, L.btable, L.btable_cap, L.btmp, s));
   Runs R{L.rs, L.re, L.pl, L.pov, L.ovc, L.fcrs, L.voff,
          BIndex{L.rs, L.bsegs, L.btable}};
+  // the query kernels hold the 2G segment parameters in LDS
+  const size_t segs_bytes = sizeof(BSeg) * (size_t)(2 * G);
   CHOPPER_HIP(launch("ov_comm_voff", k_comm_voff, dim3(1), dim3(64), s, G,
                      (const BSeg*)L.bsegs, L.voff));
   if (n > 0) {
     const int64_t cg = ceil_div(n, (int64_t)kBlock);
-    CHOPPER_HIP(launch("ov_runs_comm_overlap", k_runs_comm_overlap,
-                       dim3((unsigned)(cg < kCommGrid ? cg : kCommGrid)),
-                       dim3(kBlock), s, R, G, L.ovc, L.fcrs));
+    CHOPPER_HIP(launch_shm("ov_runs_comm_overlap", k_runs_comm_overlap,
+                           dim3((unsigned)(cg < kCommGrid ? cg : kCommGrid)),
+                           dim3(kBlock), segs_bytes, s, R, G, L.ovc, L.fcrs));
     CHOPPER_HIP(exclusive_scan<int64_t>(L.ovc, L.pov, n,
                                         (const uint32_t*)(L.voff + G),
                                         L.scan_i64, L.tot_i64 + 1, s));
-    CHOPPER_HIP(launch("ov_records", k_overlap_records,
+    CHOPPER_HIP(launch_shm("ov_records", k_overlap_records,
                        dim3((unsigned)ceil_div(n, (int64_t)kOvTile)),
-                       dim3(kBlock), s, n, G, korder, rec->gpu, rec->cls,
+                       dim3(kBlock), segs_bytes, s, n, G, korder, rec->gpu,
+                       rec->cls,
                        start_al, end_al, R, ovl_out));
   }
   if (nm > 0)
-    CHOPPER_HIP(launch("ov_markers", k_overlap_markers,
-                       grid_for(nm, kBlock * kMarkPerThread),
-                       dim3(kBlock), s, nm, G, mk->gpu, mstart_al, mend_al, R,
-                       mwin_out));
+    CHOPPER_HIP(launch_shm("ov_markers", k_overlap_markers,
+                           grid_for(nm, kBlock * kMarkPerThread),
+                           dim3(kBlock), segs_bytes, s, nm, G, mk->gpu,
+                           mstart_al, mend_al, R, mwin_out));
   CHOPPER_HIP(launch("ov_gpus", k_overlap_gpus, grid_for(G, kBlock),
                      dim3(kBlock), s, G, R, gwin_out));
   if (n > 0) {
