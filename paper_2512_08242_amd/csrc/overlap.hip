@@ -390,12 +390,17 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
     const int64_t p = wbase + (int64_t)lane * kTileIpt + j;
     if (((it.m_newseg >> j) & 1u)) {
       rbeg[it.seg[j]] = r0 + k[j];
-      if (p > 0) rend[pseg] = r0 + k[j];
+      rbeg[2 * kSegs + it.seg[j]] = (uint32_t)p;     // korder positions
+      if (p > 0) {
+        rend[pseg] = r0 + k[j];
+        rend[2 * kSegs + pseg] = (uint32_t)p;
+      }
     }
     if (((it.m_valid >> j) & 1u) && p == n - 1) {
       const uint32_t R = *nruns;
       re[R - 1] = grand->val;
       rend[it.seg[j]] = R;
+      rend[2 * kSegs + it.seg[j]] = (uint32_t)n;
     }
     if ((it.m_valid >> j) & 1u) pseg = it.seg[j];
   }
@@ -437,15 +442,59 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
 
 // overlapped time inside each comm run: compute-active time within it
 // dense index of the first comm run of every gpu, and their total
-__global__ void k_comm_voff(int G, const BSeg* segs, uint32_t* voff) {
+// and (roff) of the communication records: korder positions kbeg .. kend
+// of each gpu's communication segment
+__global__ void k_comm_voff(int G, const BSeg* segs, const uint32_t* kbeg,
+                            const uint32_t* kend, uint32_t* voff,
+                            uint32_t* roff) {
   if (threadIdx.x != 0) return;
-  uint32_t acc = 0;
+  uint32_t acc = 0, racc = 0;
   for (int g = 0; g < G; ++g) {
     voff[g] = acc;
+    roff[g] = racc;
     const BSeg& P = segs[2 * g + 1];
     acc += P.se > P.sb ? P.se - P.sb : 0u;
+    const uint32_t b = kbeg[2 * g + 1], e = kend[2 * g + 1];
+    racc += e > b ? e - b : 0u;
   }
   voff[G] = acc;
+  roff[G] = racc;
+}
+
+// Overlapped time of the communication records (the compute-active time
+// inside each), one thread per record over the dense indices of all GPUs;
+// the korder tiles leave these records out, so that no tile mixes the
+// window searches of compute records with these wide ones.
+__global__ __launch_bounds__(kBlock) void k_comm_records(
+    int G, const uint32_t* korder, const uint32_t* kbeg, const uint32_t* roff,
+    const int64_t* start, const int64_t* end, Runs R, int64_t* ovl) {
+  extern __shared__ BSeg s_seg[];   // 2G entries (dynamic LDS)
+  __shared__ uint32_t s_roff[kSegs / 2 + 1];
+  for (int i = threadIdx.x; i <= G; i += kBlock) s_roff[i] = roff[i];
+  segs_to_lds(s_seg, R.X.seg, 2 * G);
+  const int64_t total = s_roff[G];
+  for (int64_t v = (int64_t)blockIdx.x * kBlock + threadIdx.x; v < total;
+       v += (int64_t)gridDim.x * kBlock) {
+    int lo = 0, hi = G;            // the last g with roff[g] <= v
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if ((int64_t)s_roff[mid] <= v) lo = mid;
+      else hi = mid;
+    }
+    const uint32_t r = korder[(int64_t)kbeg[2 * lo + 1] + (v - s_roff[lo])];
+    const int64_t s = start[r], e0 = end[r];
+    int64_t o = 0;
+    if (e0 > s) {
+      const BSeg P = s_seg[2 * lo];
+      const int64_t t[2] = {s, e0};
+      int64_t l2[2], h2[2];
+      bi_range(R.X, P, s, &l2[0], &h2[0]);
+      bi_range(R.X, P, e0, &l2[1], &h2[1]);
+      bsearch_k<2>(R.rs, l2, h2, t);
+      o = F_at(R, P, l2[1], e0) - F_at(R, P, l2[0], s);
+    }
+    ovl[r] = o;
+  }
 }
 
 // overlapped time inside each comm run (compute-active time within it) and
@@ -517,19 +566,31 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
     if (in) m_in |= 1u << j;
     if (in && (int)(seg[j] >> 1) < G) m_valid |= 1u << j;
   }
-  // the tile's main segment and the window of the other kind's runs
-  const uint32_t seg0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)seg[0]);
-  int64_t emax = kI64Min;
+  // communication records are done by k_comm_records
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j)
-    if (((m_valid >> j) & 1u) && seg[j] == seg0 && e[j] > emax) emax = e[j];
-  emax = wave_incl(emax, OpMax(), kI64Min);
-  emax = lane63(emax);
-  const int64_t smin = (int64_t)(
-      (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)s[0]) |
-      ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(
-           (int)(uint32_t)((uint64_t)s[0] >> 32)) << 32));
-  const bool main_ok = (int)(seg0 >> 1) < G;
+    if (seg[j] & 1u) m_valid &= ~(1u << j);
+  // the tile's main segment (its first compute item's) and the window of
+  // the communication runs of that gpu
+  uint32_t seg0 = kNone;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    const uint64_t m = __ballot((m_valid >> j) & 1u);
+    if (seg0 == kNone && m)
+      seg0 = (uint32_t)__builtin_amdgcn_readlane((int)seg[j],
+                                                 __ffsll((long long)m) - 1);
+  }
+  int64_t emax = kI64Min, smin = kI64Max;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j)
+    if (((m_valid >> j) & 1u) && seg[j] == seg0) {
+      emax = e[j] > emax ? e[j] : emax;
+      smin = s[j] < smin ? s[j] : smin;
+    }
+  emax = lane63(wave_incl(emax, OpMax(), kI64Min));
+  smin = lane63(wave_incl(smin, OpMin(), kI64Max));
+  // seg0 = kNone: no compute record here
+  const bool main_ok = seg0 != kNone && (int)(seg0 >> 1) < G;
   const BSeg Q = s_seg[main_ok ? (seg0 ^ 1u) : 0u];
   int64_t wlo = 0, whi = 0;
   if (main_ok && lane == 0) {
@@ -591,9 +652,12 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
       o[j] = F_at(R, P, lo[1], e[j]) - F_at(R, P, lo[0], s[j]);
     }
   }
+  // every position but the communication records of valid gpus (written
+  // by k_comm_records)
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j)
-    if ((m_in >> j) & 1u) ovl[r[j]] = o[j];
+    if (((m_in >> j) & 1u) && !((seg[j] & 1u) && (int)(seg[j] >> 1) < G))
+      ovl[r[j]] = o[j];
 }
 
 // Window values of every marker, one per thread (more markers per thread
@@ -791,6 +855,7 @@ struct OverlapLayout {
   int64_t* scan_i64;
   int64_t* tot_i64;
   uint32_t* voff;
+  uint32_t* roff;     // dense offsets of every gpu's communication records
   BSeg* bsegs;
   uint32_t* btable;
   int64_t btable_cap;
@@ -812,7 +877,7 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   L.rs = sc.take<int64_t>(n);
   L.re = sc.take<int64_t>(n);
   L.rseg = sc.take<uint32_t>(n);
-  L.rbeg = sc.take<uint32_t>(2 * kSegs);
+  L.rbeg = sc.take<uint32_t>(4 * kSegs);   // run and korder ranges
   L.rend = L.rbeg ? L.rbeg + kSegs : nullptr;
   L.pl = sc.take<int64_t>(n);
   L.ovc = sc.take<int64_t>(n);
@@ -821,6 +886,7 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   L.scan_i64 = sc.take<int64_t>(scan_scratch_elems(n));
   L.tot_i64 = sc.take<int64_t>(2);
   L.voff = sc.take<uint32_t>(G + 1);
+  L.roff = sc.take<uint32_t>(G + 1);
   L.bsegs = sc.take<BSeg>(kSegs);
   L.btable_cap = bindex_table_cap(n, kSegs);
   L.btable = sc.take<uint32_t>(L.btable_cap);
@@ -861,8 +927,8 @@ extern "C" int chopper_overlap(const chopper_records* rec,
   OverlapLayout L = overlap_layout(sc, n, G);
   const unsigned T = (unsigned)L.ntiles;
 
-  CHOPPER_HIP(launch("ov_fill", k_fill_u32, grid_for(2 * kSegs, kBlock),
-                     dim3(kBlock), s, L.rbeg, (int64_t)(2 * kSegs), 0u));
+  CHOPPER_HIP(launch("ov_fill", k_fill_u32, grid_for(4 * kSegs, kBlock),
+                     dim3(kBlock), s, L.rbeg, (int64_t)(4 * kSegs), 0u));
   if (n > 0) {
     // union runs of every (gpu, kind)
     CHOPPER_HIP(launch("ov_runs_count", k_runs_count, dim3(T), dim3(kBlock), s,
@@ -896,7 +962,8 @@ extern "C" int chopper_overlap(const chopper_records* rec,
   // the query kernels hold the 2G segment parameters in LDS
   const size_t segs_bytes = sizeof(BSeg) * (size_t)(2 * G);
   CHOPPER_HIP(launch("ov_comm_voff", k_comm_voff, dim3(1), dim3(64), s, G,
-                     (const BSeg*)L.bsegs, L.voff));
+                     (const BSeg*)L.bsegs, (const uint32_t*)(L.rbeg + 2 * kSegs),
+                     (const uint32_t*)(L.rbeg + 3 * kSegs), L.voff, L.roff));
   if (n > 0) {
     const int64_t cg = ceil_div(n, (int64_t)kBlock);
     CHOPPER_HIP(launch_shm("ov_runs_comm_overlap", k_runs_comm_overlap,
@@ -910,6 +977,12 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                        dim3(kBlock), segs_bytes, s, n, G, korder, rec->gpu,
                        rec->cls,
                        start_al, end_al, R, ovl_out));
+    CHOPPER_HIP(launch_shm("ov_comm_records", k_comm_records,
+                           dim3((unsigned)(cg < kCommGrid ? cg : kCommGrid)),
+                           dim3(kBlock), segs_bytes, s, G, korder,
+                           (const uint32_t*)(L.rbeg + 2 * kSegs),
+                           (const uint32_t*)L.roff, start_al, end_al, R,
+                           ovl_out));
   }
   if (nm > 0)
     CHOPPER_HIP(launch_shm("ov_markers", k_overlap_markers,
