@@ -1788,9 +1788,11 @@ __global__ __launch_bounds__(kBlock) void k_agg_workload_first(
 
 // Entries [0, nslots), or [0, *count) when nslots < 0; a slot holding
 // kNone is empty.
+// `clear` (optional): three flag words zeroed for the next heads pass
 __global__ __launch_bounds__(kBlock) void k_agg_apply_overflow(
-    Overflow ovf, RowsDev R, int nfields, int64_t nslots) {
+    Overflow ovf, RowsDev R, int nfields, int64_t nslots, uint32_t* clear) {
   const int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (clear && e < 3) clear[e] = 0;
   int64_t cnt = nslots >= 0 ? nslots : (int64_t)*ovf.count;
   if (cnt > ovf.cap) cnt = ovf.cap;
   if (e >= cnt) return;
@@ -2053,7 +2055,7 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
       }
       CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
                          grid_for(ns, kBlock), dim3(kBlock), s, ovf, R,
-                         nfields, ns));
+                         nfields, ns, L.hflags2));
     } else {
       // launches sized by the finer level's row count; with `two` also the
       // level li - 1 (heads of li - 1 first in the table, then li)
@@ -2064,8 +2066,7 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
       FromRows src{R, M, rows->level_offset, finer};
       const int lv0 = two ? li - 1 : li;
       const uint32_t lact = two ? (3u << (li - 1)) : (1u << li);
-      CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
-                         L.hflags2, 3));
+      // (the flags were zeroed by the previous overflow pass)
       CHOPPER_HIP(launch("agg_heads_rows", k_agg_heads<kMD, FromRows>,
                          dim3(gr), dim3(kBlock), s, src, lact, lv0, li, D, M,
                          nw, L.htc2, L.hflags2, status));
@@ -2088,7 +2089,7 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
       const int64_t ns = (two ? 2 : 1) * nw;
       CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
                          grid_for(ns, kBlock), dim3(kBlock), s, ovf, R,
-                         nfields, ns));
+                         nfields, ns, L.hflags2));
     }
     return CHOPPER_OK;
   };
@@ -2287,7 +2288,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
     if (!atomic_mode)
       CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
                          grid_for(L.ovf_cap, kBlock), dim3(kBlock), s, ovf, R,
-                         nfields, (int64_t)-1));
+                         nfields, (int64_t)-1, (uint32_t*)nullptr));
     if (li == D + 1) {
       if (finer < 0) {
         FromRecords src{S};

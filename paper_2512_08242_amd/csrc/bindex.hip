@@ -1,8 +1,8 @@
 // Construction of the bucket index (see bindex.h).
 //
-//   1. per segment: first key, bucket width (smallest power of two with at
-//      most ceil(count / 4) buckets over the key span), bucket count;
-//   2. one block scans the table sizes into offsets;
+//   1-2. one block: per segment the first key, the bucket width (smallest
+//      power of two with at most ceil(count / 4) buckets over the key span)
+//      and the bucket count, and the scan of the table sizes into offsets;
 //   3. every key writes the entries of the buckets that start in the gap
 //      after the previous key (at most kFillRun of them, so no thread stalls
 //      on a long gap), the last key also the entries after it;
@@ -20,50 +20,44 @@ int64_t bindex_table_cap(int64_t nkeys, int64_t nseg) {
   return nkeys / kKeysPerBucket + 2 * nseg + 2;
 }
 
-__global__ __launch_bounds__(kBlock) void k_bi_params(
+// One block: every segment's parameters (first key, bucket width: the
+// smallest power of two with at most ceil(count / 4) buckets over the key
+// span, bucket count) and the exclusive scan of the table sizes; segments
+// that would not fit the table keep no table and are searched whole.
+__global__ __launch_bounds__(1024) void k_bi_params(
     const int64_t* key, const uint32_t* sbeg, const uint32_t* send, int stride,
-    int nseg, BSeg* segs, uint32_t* entries) {
-  const int sidx = blockIdx.x * kBlock + threadIdx.x;
-  if (sidx >= nseg) return;
-  BSeg P;
-  P.sb = sbeg[(int64_t)sidx * stride];
-  P.se = send[(int64_t)sidx * stride];
-  P.lo = 0;
-  P.shift = 0;
-  P.nb = 0;
-  P.toff = 0;
-  P.pad = 0;
-  uint32_t ent = 0;
-  if (P.se > P.sb) {
-    const int64_t cnt = (int64_t)P.se - P.sb;
-    P.lo = key[P.sb];
-    const int64_t d = (int64_t)((uint64_t)key[P.se - 1] - (uint64_t)P.lo);
-    const uint64_t span = d > 0 ? (uint64_t)d : 0;   // keys sorted
-    const uint64_t target =
-        (uint64_t)((cnt + kKeysPerBucket - 1) / kKeysPerBucket);
-    uint32_t k = 0;
-    while (k < 63 && (span >> k) + 1 > target) ++k;
-    P.shift = k;
-    P.nb = (uint32_t)((span >> k) + 1);
-    ent = P.nb + 1;
-  }
-  segs[sidx] = P;
-  entries[sidx] = ent;
-}
-
-// exclusive scan of the entry counts (one block); segments that would not
-// fit keep no table and are searched whole
-__global__ __launch_bounds__(1024) void k_bi_offsets(int nseg, BSeg* segs,
-                                                     const uint32_t* entries,
-                                                     int64_t cap,
-                                                     uint32_t* total) {
+    int nseg, BSeg* segs, int64_t cap, uint32_t* total) {
   __shared__ uint32_t s_w[1024 / kWave];
   const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
   uint64_t carry = 0;
   for (int base = 0; base < nseg; base += 1024) {
-    const int i = base + (int)threadIdx.x;
-    const uint32_t v = i < nseg ? entries[i] : 0u;
-    const uint32_t incl = wave_incl(v, OpAdd(), 0u);
+    const int sidx = base + (int)threadIdx.x;
+    BSeg P;
+    P.lo = 0;
+    P.sb = P.se = 0;
+    P.shift = 0;
+    P.nb = 0;
+    P.toff = 0;
+    P.pad = 0;
+    uint32_t ent = 0;
+    if (sidx < nseg) {
+      P.sb = sbeg[(int64_t)sidx * stride];
+      P.se = send[(int64_t)sidx * stride];
+      if (P.se > P.sb) {
+        const int64_t cnt = (int64_t)P.se - P.sb;
+        P.lo = key[P.sb];
+        const int64_t d = (int64_t)((uint64_t)key[P.se - 1] - (uint64_t)P.lo);
+        const uint64_t span = d > 0 ? (uint64_t)d : 0;   // keys sorted
+        const uint64_t target =
+            (uint64_t)((cnt + kKeysPerBucket - 1) / kKeysPerBucket);
+        uint32_t k = 0;
+        while (k < 63 && (span >> k) + 1 > target) ++k;
+        P.shift = k;
+        P.nb = (uint32_t)((span >> k) + 1);
+        ent = P.nb + 1;
+      }
+    }
+    const uint32_t incl = wave_incl(ent, OpAdd(), 0u);
     if (lane == kWave - 1) s_w[w] = incl;
     __syncthreads();
     uint64_t pre = carry, tot = carry;
@@ -71,11 +65,12 @@ __global__ __launch_bounds__(1024) void k_bi_offsets(int nseg, BSeg* segs,
       if (q < w) pre += s_w[q];
       tot += s_w[q];
     }
-    pre += incl - v;
-    if (i < nseg) {
+    pre += incl - ent;
+    if (sidx < nseg) {
       // offsets are stored for every segment, so they never decrease
-      segs[i].toff = (uint32_t)(pre < (uint64_t)cap ? pre : cap);
-      if (pre + v > (uint64_t)cap) segs[i].nb = 0;
+      P.toff = (uint32_t)(pre < (uint64_t)cap ? pre : cap);
+      if (pre + ent > (uint64_t)cap) P.nb = 0;
+      segs[sidx] = P;
     }
     carry = tot;
     __syncthreads();
@@ -203,14 +198,10 @@ hipError_t bindex_build(const int64_t* key, const uint32_t* keyseg,
                         int nseg, BSeg* segs, uint32_t* table,
                         int64_t table_cap, uint32_t* tmp, hipStream_t s) {
   if (nseg <= 0) return hipSuccess;
-  uint32_t* entries = tmp;
   uint32_t* total = tmp + nseg;
   hipError_t e;
-  e = launch("bi_params", k_bi_params, grid_for(nseg, kBlock), dim3(kBlock), s,
-             key, sbeg, send, stride, nseg, segs, entries);
-  if (e != hipSuccess) return e;
-  e = launch("bi_offsets", k_bi_offsets, dim3(1), dim3(1024), s, nseg, segs,
-             (const uint32_t*)entries, table_cap, total);
+  e = launch("bi_params", k_bi_params, dim3(1), dim3(1024), s, key, sbeg, send,
+             stride, nseg, segs, table_cap, total);
   if (e != hipSuccess) return e;
   e = launch("bi_clear", k_bi_clear, grid_for(table_cap, kBlock), dim3(kBlock),
              s, table, (const uint32_t*)total);

@@ -440,27 +440,6 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
   }
 }
 
-// overlapped time inside each comm run: compute-active time within it
-// dense index of the first comm run of every gpu, and their total
-// and (roff) of the communication records: korder positions kbeg .. kend
-// of each gpu's communication segment
-__global__ void k_comm_voff(int G, const BSeg* segs, const uint32_t* kbeg,
-                            const uint32_t* kend, uint32_t* voff,
-                            uint32_t* roff) {
-  if (threadIdx.x != 0) return;
-  uint32_t acc = 0, racc = 0;
-  for (int g = 0; g < G; ++g) {
-    voff[g] = acc;
-    roff[g] = racc;
-    const BSeg& P = segs[2 * g + 1];
-    acc += P.se > P.sb ? P.se - P.sb : 0u;
-    const uint32_t b = kbeg[2 * g + 1], e = kend[2 * g + 1];
-    racc += e > b ? e - b : 0u;
-  }
-  voff[G] = acc;
-  roff[G] = racc;
-}
-
 // Overlapped time of the communication records (the compute-active time
 // inside each), one thread per record over the dense indices of all GPUs;
 // the korder tiles leave these records out, so that no tile mixes the
@@ -501,12 +480,42 @@ __global__ __launch_bounds__(kBlock) void k_comm_records(
 // the compute-active time before it, at the run's dense index; a fixed grid
 // strides over the dense indices of all GPUs
 constexpr int kCommGrid = 2048;
+// dense offsets (voff) of every gpu's communication runs and (roff) of its
+// communication records (korder positions kbeg .. kend), from the segment
+// table; every block computes them, block 0 also stores them
+__device__ inline void comm_offsets(int G, const BSeg* seg,
+                                    const uint32_t* kbeg, const uint32_t* kend,
+                                    uint32_t* s_voff, uint32_t* s_roff,
+                                    uint32_t* voff, uint32_t* roff) {
+  if (threadIdx.x == 0) {
+    uint32_t acc = 0, racc = 0;
+    for (int g = 0; g < G; ++g) {
+      s_voff[g] = acc;
+      s_roff[g] = racc;
+      const BSeg& P = seg[2 * g + 1];
+      acc += P.se > P.sb ? P.se - P.sb : 0u;
+      const uint32_t b = kbeg[2 * g + 1], e = kend[2 * g + 1];
+      racc += e > b ? e - b : 0u;
+    }
+    s_voff[G] = acc;
+    s_roff[G] = racc;
+  }
+  __syncthreads();
+  if (blockIdx.x == 0)
+    for (int i = threadIdx.x; i <= G; i += kBlock) {
+      voff[i] = s_voff[i];
+      roff[i] = s_roff[i];
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void k_runs_comm_overlap(
-    Runs R, int G, int64_t* ovc, int64_t* fcrs) {
+    Runs R, int G, const uint32_t* kbeg, const uint32_t* kend, uint32_t* voff,
+    uint32_t* roff, int64_t* ovc, int64_t* fcrs) {
   extern __shared__ BSeg s_seg[];   // 2G entries (dynamic LDS)
   __shared__ uint32_t s_voff[kSegs / 2 + 1];
-  for (int i = threadIdx.x; i <= G; i += kBlock) s_voff[i] = R.voff[i];
+  __shared__ uint32_t s_roff[kSegs / 2 + 1];
   segs_to_lds(s_seg, R.X.seg, 2 * G);
+  comm_offsets(G, s_seg, kbeg, kend, s_voff, s_roff, voff, roff);
   const int64_t total = s_voff[G];
   for (int64_t v = (int64_t)blockIdx.x * kBlock + threadIdx.x; v < total;
        v += (int64_t)gridDim.x * kBlock) {
@@ -699,9 +708,7 @@ __global__ __launch_bounds__(kBlock) void k_overlap_markers(
 
 // GPU window: the first run of a (gpu, kind) segment starts at its smallest
 // start', the last run ends at its largest end'
-__global__ void k_overlap_gpus(int G, Runs R, int64_t* gwin) {
-  const int g = blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= G) return;
+__device__ inline void overlap_gpu(int g, const Runs& R, int64_t* gwin) {
   int64_t a = kI64Max, b = kI64Min;
   for (uint32_t seg = g * 2u; seg < g * 2u + 2u; ++seg) {
     const BSeg P = R.X.seg[seg];
@@ -719,6 +726,11 @@ __global__ void k_overlap_gpus(int G, Runs R, int64_t* gwin) {
   gwin[6 * g + 0] = a;
   gwin[6 * g + 1] = b;
   for (int z = 0; z < 4; ++z) gwin[6 * g + 2 + z] = w[0][z];
+}
+
+__global__ void k_overlap_gpus(int G, Runs R, int64_t* gwin) {
+  const int g = blockIdx.x * blockDim.x + threadIdx.x;
+  if (g < G) overlap_gpu(g, R, gwin);
 }
 
 // ---------------- bubbles ----------------------------------------------------
@@ -961,14 +973,18 @@ extern "C" int chopper_overlap(const chopper_records* rec,
          BIndex{L.rs, L.bsegs, L.btable}};
   // the query kernels hold the 2G segment parameters in LDS
   const size_t segs_bytes = sizeof(BSeg) * (size_t)(2 * G);
-  CHOPPER_HIP(launch("ov_comm_voff", k_comm_voff, dim3(1), dim3(64), s, G,
-                     (const BSeg*)L.bsegs, (const uint32_t*)(L.rbeg + 2 * kSegs),
-                     (const uint32_t*)(L.rbeg + 3 * kSegs), L.voff, L.roff));
+  // communication offsets (always, the marker windows read them) and the
+  // overlap inside every communication run
+  int64_t cg = ceil_div(n, (int64_t)kBlock);
+  cg = cg < 1 ? 1 : (cg < kCommGrid ? cg : kCommGrid);
+  CHOPPER_HIP(launch_shm("ov_runs_comm_overlap", k_runs_comm_overlap,
+                         dim3((unsigned)cg), dim3(kBlock), segs_bytes, s, R, G,
+                         (const uint32_t*)(L.rbeg + 2 * kSegs),
+                         (const uint32_t*)(L.rbeg + 3 * kSegs), L.voff, L.roff,
+                         L.ovc, L.fcrs));
+
   if (n > 0) {
-    const int64_t cg = ceil_div(n, (int64_t)kBlock);
-    CHOPPER_HIP(launch_shm("ov_runs_comm_overlap", k_runs_comm_overlap,
-                           dim3((unsigned)(cg < kCommGrid ? cg : kCommGrid)),
-                           dim3(kBlock), segs_bytes, s, R, G, L.ovc, L.fcrs));
+
     CHOPPER_HIP(exclusive_scan<int64_t>(L.ovc, L.pov, n,
                                         (const uint32_t*)(L.voff + G),
                                         L.scan_i64, L.tot_i64 + 1, s));
@@ -978,8 +994,8 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                        rec->cls,
                        start_al, end_al, R, ovl_out));
     CHOPPER_HIP(launch_shm("ov_comm_records", k_comm_records,
-                           dim3((unsigned)(cg < kCommGrid ? cg : kCommGrid)),
-                           dim3(kBlock), segs_bytes, s, G, korder,
+                           dim3((unsigned)cg), dim3(kBlock), segs_bytes, s, G,
+                           korder,
                            (const uint32_t*)(L.rbeg + 2 * kSegs),
                            (const uint32_t*)L.roff, start_al, end_al, R,
                            ovl_out));

@@ -28,8 +28,8 @@ static const char* const kKernelNames[] = {
     "sort_class_count", "status_set", "ov_fill",
     "agg_workload_first", "sort_major_sorted", "agg_heads_records",
     "agg_heads_rows", "agg_fast_reduce_records", "agg_fast_reduce_rows",
-    "agg_workload_from_gpu", "bi_params", "bi_offsets", "bi_clear", "bi_fill",
-    "bi_fixup", "ov_comm_voff", "ov_comm_records", "agg_nat_init", "agg_nat_pre",
+    "agg_workload_from_gpu", "bi_params", "bi_clear", "bi_fill",
+    "bi_fixup", "ov_comm_records", "agg_nat_init", "agg_nat_pre",
     "agg_nat_tiles", "agg_heads_nat", "agg_gpu_rows"};
 
 __global__ __launch_bounds__(kBlock) void k_ratios(

@@ -89,6 +89,43 @@ __global__ __launch_bounds__(kBlock) void k_scan_down(const T* in, T* out,
   }
 }
 
+// Rescan of a tile whose prefix is the sum of the tile sums before it,
+// added up by the block itself (used when there are at most kDirectTiles
+// tiles); the block holding the last element also writes the total.
+constexpr int64_t kDirectTiles = 1024;
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_scan_down_direct(
+    const T* in, T* out, int64_t n, const uint32_t* n_dev, const T* tile_sum,
+    T* total) {
+  n = scan_len(n, n_dev);
+  const int64_t base = (int64_t)blockIdx.x * kScanTile;
+  if (base >= n) {
+    if (blockIdx.x == 0 && threadIdx.x == 0 && total) *total = 0;
+    return;
+  }
+  T p = 0;
+  for (int64_t i = threadIdx.x; i < (int64_t)blockIdx.x; i += kBlock)
+    p += tile_sum[i];
+  T prefix;
+  block_exclusive(p, OpAdd(), (T)0, &prefix);
+  T v[kScanIpt];
+  T acc = 0;
+  for (int j = 0; j < kScanIpt; ++j) {
+    int64_t i = base + (int64_t)threadIdx.x * kScanIpt + j;
+    v[j] = (i < n) ? in[i] : (T)0;
+    acc += v[j];
+  }
+  T tot;
+  T pre = block_exclusive(acc, OpAdd(), (T)0, &tot) + prefix;
+  for (int j = 0; j < kScanIpt; ++j) {
+    int64_t i = base + (int64_t)threadIdx.x * kScanIpt + j;
+    if (i < n) out[i] = pre;
+    pre += v[j];
+  }
+  if (base + kScanTile >= n && threadIdx.x == 0 && total)
+    *total = prefix + tot;
+}
+
 template <typename T>
 hipError_t exclusive_scan(const T* in, T* out, int64_t n, T* tmp, T* total,
                           hipStream_t s) {
@@ -105,6 +142,17 @@ hipError_t exclusive_scan(const T* in, T* out, int64_t n, const uint32_t* n_dev,
     e = launch("scan_spine", k_scan_spine<T>, dim3(1), dim3(kBlock), s, tmp,
                (int64_t)0, total);
     return e;
+  }
+  if (ntiles <= kDirectTiles) {
+    // two passes (one for a single tile): each block adds up the tile sums
+    // before it
+    if (ntiles > 1) {
+      e = launch("scan_reduce", k_scan_reduce<T>, dim3((unsigned)ntiles),
+                 dim3(kBlock), s, in, n, n_dev, tmp);
+      if (e != hipSuccess) return e;
+    }
+    return launch("scan_down", k_scan_down_direct<T>, dim3((unsigned)ntiles),
+                  dim3(kBlock), s, in, out, n, n_dev, (const T*)tmp, total);
   }
   e = launch("scan_reduce", k_scan_reduce<T>, dim3((unsigned)ntiles),
              dim3(kBlock), s, in, n, n_dev, tmp);
