@@ -23,7 +23,9 @@ bool validate_markers(const chopper_markers* m);
 __global__ __launch_bounds__(kBlock) void k_marker_gather(
     int64_t nm, KeyMarker km, const uint32_t* mord, const int64_t* ms,
     const int64_t* me, int64_t* sms, int64_t* sme, uint32_t* sid,
-    uint32_t* sseg) {
+    uint32_t* sseg, uint32_t* btable, int64_t btable_cap) {
+  // the bucket index table, built after the links pass, starts unset
+  bindex_clear(btable, btable_cap, blockIdx.x, gridDim.x);
   int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (p >= nm) return;
   uint32_t j = mord[p];
@@ -275,7 +277,7 @@ extern "C" int chopper_attribute(const chopper_records* rec,
     CHOPPER_HIP(launch("attr_marker_gather", k_marker_gather,
                        grid_for(nm, kBlock), dim3(kBlock), s, nm, km,
                        (const uint32_t*)L.mord, mstart_al, mend_al, L.sms,
-                       L.sme, L.sid, L.sseg));
+                       L.sme, L.sid, L.sseg, L.btable, L.btable_cap));
     const int64_t per_seg = ceil_div(nm, (int64_t)G * D);
     unsigned gx = (unsigned)ceil_div(per_seg, kBlock);
     if (gx < 1) gx = 1;
@@ -288,7 +290,8 @@ extern "C" int chopper_attribute(const chopper_records* rec,
   if (n == 0 || D == 0) return CHOPPER_OK;
   // bucket index of the non-empty marker starts of every (gpu, level)
   CHOPPER_HIP(bindex_build(L.sms, L.sseg, nm, nullptr, L.coff, L.coff + 1, 2,
-                           G * D, L.bsegs, L.btable, L.btable_cap, L.btmp, s));
+                           G * D, L.bsegs, L.btable, L.btable_cap, L.btmp, s,
+                           nm > 0));
   const BIndex X{L.sms, L.bsegs, L.btable};
   const unsigned grid = (unsigned)ceil_div(n, (int64_t)kWaveTile * kWavesPerBlock);
   auto run = [&](auto kern) -> int {

@@ -22,6 +22,9 @@ struct BSeg {
   uint32_t pad;
 };
 
+// table entries that no key wrote (inside a gap longer than the fill run)
+constexpr uint32_t kUnset = 0xFFFFFFFFu;
+
 struct BIndex {
   const int64_t* key;
   const BSeg* seg;
@@ -84,8 +87,11 @@ __device__ inline void bi_range(const BIndex& X, const BSeg& P, int64_t t,
     *lo = *hi = P.se;
     return;
   }
-  *lo = X.table[P.toff + b];
-  *hi = X.table[P.toff + b + 1];
+  // an entry inside a long gap is unset: the range then widens to the
+  // segment's end on that side, which only costs a longer search
+  const uint32_t a = X.table[P.toff + b], c = X.table[P.toff + b + 1];
+  *lo = a != kUnset ? (int64_t)a : (int64_t)P.sb;
+  *hi = c != kUnset ? (int64_t)c : (int64_t)P.se;
 }
 
 // first position of segment s with key > t (the segment's start if none)
@@ -101,11 +107,22 @@ int64_t bindex_table_cap(int64_t nkeys, int64_t nseg);
 
 // Builds the index.  Segment s spans [sbeg[s * stride], send[s * stride]);
 // keyseg[i] is the segment of key i or kNone; *nkeys_dev (device) bounds the
-// keys actually present when non-null.  `tmp` holds nseg + 1 uint32.
+// keys actually present when non-null.  `tmp` holds nseg + 1 uint32.  With
+// `cleared` the caller has already set all table_cap entries to kUnset (an
+// earlier kernel of the same stream, see bindex_clear).
 hipError_t bindex_build(const int64_t* key, const uint32_t* keyseg,
                         int64_t nkeys, const uint32_t* nkeys_dev,
                         const uint32_t* sbeg, const uint32_t* send, int stride,
                         int nseg, BSeg* segs, uint32_t* table,
-                        int64_t table_cap, uint32_t* tmp, hipStream_t s);
+                        int64_t table_cap, uint32_t* tmp, hipStream_t s,
+                        bool cleared = false);
+
+// Part of a grid-stride clear of the table that a kernel of any grid can
+// take on: block b of nb clears its share.
+__device__ inline void bindex_clear(uint32_t* table, int64_t cap, int64_t b,
+                                    int64_t nb) {
+  for (int64_t e = b * kBlock + threadIdx.x; e < cap; e += nb * kBlock)
+    table[e] = kUnset;
+}
 
 }  // namespace chopper

@@ -6,15 +6,15 @@
 //   3. every key writes the entries of the buckets that start in the gap
 //      after the previous key (at most kFillRun of them, so no thread stalls
 //      on a long gap), the last key also the entries after it;
-//   4. entries still unset (long gaps only) are found by binary search.
+//   4. entries left unset (long gaps only) make a search fall back to the
+//      segment's bounds on that side (bi_range).
 #include "bindex.h"
 #include "wave.h"
 
 namespace chopper {
 
 constexpr int kKeysPerBucket = 4;
-constexpr int kFillRun = 32;
-constexpr uint32_t kUnset = 0xFFFFFFFFu;
+constexpr int kFillRun = 256;
 
 int64_t bindex_table_cap(int64_t nkeys, int64_t nseg) {
   return nkeys / kKeysPerBucket + 2 * nseg + 2;
@@ -157,64 +157,30 @@ __global__ __launch_bounds__(kBlock) void k_bi_fill(
   }
 }
 
-// entries inside long gaps: lower bound of the bucket start by search
-__global__ __launch_bounds__(kBlock) void k_bi_fixup(const int64_t* key,
-                                                     const BSeg* segs, int nseg,
-                                                     uint32_t* table,
-                                                     const uint32_t* total) {
-  const int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (e >= (int64_t)*total || table[e] != kUnset) return;
-  // owner of entry e: the last segment whose table starts at or before e
-  // (a segment without entries shares its offset with the next one)
-  int lo = 0, hi = nseg;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if ((int64_t)segs[mid].toff <= e) lo = mid + 1;
-    else hi = mid;
-  }
-  const int sidx = lo - 1;
-  if (sidx < 0 || segs[sidx].nb == 0) return;
-  const BSeg P = segs[sidx];
-  const int64_t b = e - P.toff;
-  if (b > (int64_t)P.nb) return;
-  uint32_t v = P.se;
-  if (b < (int64_t)P.nb) {
-    const int64_t B = (int64_t)((uint64_t)P.lo + ((uint64_t)b << P.shift));
-    // first position with key >= B
-    int64_t l = P.sb, h = P.se;
-    while (l < h) {
-      const int64_t mid = l + ((h - l) >> 1);
-      if (key[mid] < B) l = mid + 1;
-      else h = mid;
-    }
-    v = (uint32_t)l;
-  }
-  table[e] = v;
-}
-
 hipError_t bindex_build(const int64_t* key, const uint32_t* keyseg,
                         int64_t nkeys, const uint32_t* nkeys_dev,
                         const uint32_t* sbeg, const uint32_t* send, int stride,
                         int nseg, BSeg* segs, uint32_t* table,
-                        int64_t table_cap, uint32_t* tmp, hipStream_t s) {
+                        int64_t table_cap, uint32_t* tmp, hipStream_t s,
+                        bool cleared) {
   if (nseg <= 0) return hipSuccess;
   uint32_t* total = tmp + nseg;
   hipError_t e;
   e = launch("bi_params", k_bi_params, dim3(1), dim3(1024), s, key, sbeg, send,
              stride, nseg, segs, table_cap, total);
   if (e != hipSuccess) return e;
-  e = launch("bi_clear", k_bi_clear, grid_for(table_cap, kBlock), dim3(kBlock),
-             s, table, (const uint32_t*)total);
-  if (e != hipSuccess) return e;
+  if (!cleared) {
+    e = launch("bi_clear", k_bi_clear, grid_for(table_cap, kBlock),
+               dim3(kBlock), s, table, (const uint32_t*)total);
+    if (e != hipSuccess) return e;
+  }
   if (nkeys > 0) {
     e = launch("bi_fill", k_bi_fill, grid_for(nkeys, kBlock * kFillIpt),
                dim3(kBlock), s, key, keyseg, nkeys, nkeys_dev,
                (const BSeg*)segs, nseg, table);
     if (e != hipSuccess) return e;
   }
-  return launch("bi_fixup", k_bi_fixup, grid_for(table_cap, kBlock),
-                dim3(kBlock), s, key, (const BSeg*)segs, nseg, table,
-                (const uint32_t*)total);
+  return hipSuccess;
 }
 
 }  // namespace chopper

@@ -185,6 +185,72 @@ __global__ __launch_bounds__(1024) void k_tile_spine(T* tile, int64_t ntiles,
   if (threadIdx.x == 0 && total) *total = carry;
 }
 
+// One block: the exclusive scan of the tiles' run counts (with the total)
+// and, in place, the segmented scan of their union increments.
+__global__ __launch_bounds__(1024) void k_runs_spine2(
+    const uint32_t* heads, uint32_t* run0, uint32_t* nruns, SegSum* inc,
+    SegSum* inc_total, int64_t ntiles) {
+  constexpr int kIpt = 12;
+  constexpr int kT = 1024;
+  __shared__ uint32_t s_h[kT / kWave];
+  __shared__ SegSum s_i[kT / kWave];
+  OpSegSum op;
+  const SegSum ident = segsum_ident();
+  uint32_t hcarry = 0;
+  SegSum icarry = ident;
+  const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
+  for (int64_t base = 0; base < ntiles; base += (int64_t)kT * kIpt) {
+    uint32_t h[kIpt];
+    SegSum v[kIpt];
+    uint32_t hacc = 0;
+    SegSum iacc = ident;
+#pragma unroll
+    for (int j = 0; j < kIpt; ++j) {
+      const int64_t i = base + (int64_t)threadIdx.x * kIpt + j;
+      h[j] = i < ntiles ? heads[i] : 0u;
+      v[j] = i < ntiles ? inc[i] : ident;
+      hacc += h[j];
+      iacc = op(iacc, v[j]);
+    }
+    const uint32_t hin = wave_incl(hacc, OpAdd(), 0u);
+    const SegSum iin = wave_incl(iacc, op, ident);
+    if (lane == kWave - 1) {
+      s_h[w] = hin;
+      s_i[w] = iin;
+    }
+    __syncthreads();
+    uint32_t hp = hcarry, ht = hcarry;
+    SegSum ip = icarry, it = icarry;
+    for (int q = 0; q < kT / kWave; ++q) {
+      if (q < w) {
+        hp += s_h[q];
+        ip = op(ip, s_i[q]);
+      }
+      ht += s_h[q];
+      it = op(it, s_i[q]);
+    }
+    hp += hin - hacc;
+    ip = op(ip, wave_shr1_any(ident, iin));
+#pragma unroll
+    for (int j = 0; j < kIpt; ++j) {
+      const int64_t i = base + (int64_t)threadIdx.x * kIpt + j;
+      if (i < ntiles) {
+        run0[i] = hp;
+        inc[i] = ip;
+      }
+      hp += h[j];
+      ip = op(ip, v[j]);
+    }
+    hcarry = ht;
+    icarry = it;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    *nruns = hcarry;
+    *inc_total = icarry;
+  }
+}
+
 // Per-item view of a tile in the blocked arrangement: segment, start, end,
 // exclusive running (seg, end) maximum, run-head flag and the length the
 // item adds to the union of its segment.
@@ -279,8 +345,11 @@ __global__ __launch_bounds__(kBlock) void k_runs_count(
     int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
     const int64_t* start, const int64_t* end, const SegMax* tile_pre,
     SegMax* tile_agg, SegMax* tile_first, uint32_t* tile_heads,
-    SegSum* tile_inc) {
+    SegSum* tile_inc, uint32_t* ranges) {
   __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
+  // first pass: block 0 clears the segment run and korder ranges
+  if (ranges && blockIdx.x == 0)
+    for (int i = threadIdx.x; i < 4 * kSegs; i += kBlock) ranges[i] = 0;
   if (tile_pre) {
     const SegMax c = tile_pre[blockIdx.x], f = tile_first[blockIdx.x];
     if (!(c.seg == f.seg && c.val >= f.val)) return;   // block-uniform
@@ -335,8 +404,11 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
     const int64_t* start, const int64_t* end, const SegMax* tile_pre,
     const uint32_t* tile_run0, const SegSum* tile_inc0, const uint32_t* nruns,
     const SegMax* grand, int64_t* rs, int64_t* re, int64_t* pl,
-    uint32_t* rseg, uint32_t* rbeg, uint32_t* rend) {
+    uint32_t* rseg, uint32_t* rbeg, uint32_t* rend, uint32_t* btable,
+    int64_t btable_cap) {
   __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
+  // the bucket index table, built right after this pass, starts unset
+  bindex_clear(btable, btable_cap, blockIdx.x, gridDim.x);
   RunItems it;
   run_items(n, korder, gpu, cls, start, end, tile_pre,
             s_slice[threadIdx.x / kWave], it);
@@ -444,13 +516,19 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
 // inside each), one thread per record over the dense indices of all GPUs;
 // the korder tiles leave these records out, so that no tile mixes the
 // window searches of compute records with these wide ones.
+__device__ inline void overlap_gpu(int g, const Runs& R, int64_t* gwin);
+
+// Block 0 also writes the GPU windows.
 __global__ __launch_bounds__(kBlock) void k_comm_records(
     int G, const uint32_t* korder, const uint32_t* kbeg, const uint32_t* roff,
-    const int64_t* start, const int64_t* end, Runs R, int64_t* ovl) {
+    const int64_t* start, const int64_t* end, Runs R, int64_t* ovl,
+    int64_t* gwin) {
   extern __shared__ BSeg s_seg[];   // 2G entries (dynamic LDS)
   __shared__ uint32_t s_roff[kSegs / 2 + 1];
   for (int i = threadIdx.x; i <= G; i += kBlock) s_roff[i] = roff[i];
   segs_to_lds(s_seg, R.X.seg, 2 * G);
+  if (blockIdx.x == 0)
+    for (int g = threadIdx.x; g < G; g += kBlock) overlap_gpu(g, R, gwin);
   const int64_t total = s_roff[G];
   for (int64_t v = (int64_t)blockIdx.x * kBlock + threadIdx.x; v < total;
        v += (int64_t)gridDim.x * kBlock) {
@@ -939,36 +1017,39 @@ extern "C" int chopper_overlap(const chopper_records* rec,
   OverlapLayout L = overlap_layout(sc, n, G);
   const unsigned T = (unsigned)L.ntiles;
 
-  CHOPPER_HIP(launch("ov_fill", k_fill_u32, grid_for(4 * kSegs, kBlock),
-                     dim3(kBlock), s, L.rbeg, (int64_t)(4 * kSegs), 0u));
+  if (n == 0)   // (otherwise the first count pass clears them)
+    CHOPPER_HIP(launch("ov_fill", k_fill_u32, grid_for(4 * kSegs, kBlock),
+                       dim3(kBlock), s, L.rbeg, (int64_t)(4 * kSegs), 0u));
   if (n > 0) {
     // union runs of every (gpu, kind)
     CHOPPER_HIP(launch("ov_runs_count", k_runs_count, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
                        (const SegMax*)nullptr, L.tile_agg, L.tile_first,
-                       L.tile_heads, L.tile_inc));
+                       L.tile_heads, L.tile_inc, L.rbeg));
     CHOPPER_HIP(launch("ov_runs_spine", k_tile_spine<SegMax, OpSegMax>,
                        dim3(1), dim3(1024), s, L.tile_agg, L.ntiles,
                        SegMax{0u, kI64Min}, L.grand));
     CHOPPER_HIP(launch("ov_runs_fixup", k_runs_count, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
                        (const SegMax*)L.tile_agg, (SegMax*)nullptr,
-                       L.tile_first, L.tile_heads, L.tile_inc));
-    CHOPPER_HIP(exclusive_scan<uint32_t>(L.tile_heads, L.tile_run0, L.ntiles,
-                                         L.scan_u32, L.nruns, s));
-    CHOPPER_HIP(launch("ov_runs_inc_spine", k_tile_spine<SegSum, OpSegSum>,
-                       dim3(1), dim3(1024), s, L.tile_inc, L.ntiles,
-                       SegSum{kNone, 0u, 0}, L.inc_total));
+                       L.tile_first, L.tile_heads, L.tile_inc,
+                       (uint32_t*)nullptr));
+    CHOPPER_HIP(launch("ov_runs_inc_spine", k_runs_spine2, dim3(1),
+                       dim3(1024), s, (const uint32_t*)L.tile_heads,
+                       L.tile_run0, L.nruns, L.tile_inc, L.inc_total,
+                       L.ntiles));
     CHOPPER_HIP(launch("ov_runs_write", k_runs_write, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
                        (const SegMax*)L.tile_agg, (const uint32_t*)L.tile_run0,
                        (const SegSum*)L.tile_inc, (const uint32_t*)L.nruns,
                        (const SegMax*)L.grand, L.rs, L.re, L.pl, L.rseg,
-                       L.rbeg, L.rend));
+                       L.rbeg, L.rend, L.btable, L.btable_cap));
   }
-  // bucket index of the run starts of every (gpu, kind)
+  // bucket index of the run starts of every (gpu, kind) (the write pass
+  // cleared its table)
   CHOPPER_HIP(bindex_build(L.rs, L.rseg, n, L.nruns, L.rbeg, L.rend, 1, kSegs,
-                           L.bsegs, L.btable, L.btable_cap, L.btmp, s));
+                           L.bsegs, L.btable, L.btable_cap, L.btmp, s,
+                           n > 0));
   Runs R{L.rs, L.re, L.pl, L.pov, L.ovc, L.fcrs, L.voff,
          BIndex{L.rs, L.bsegs, L.btable}};
   // the query kernels hold the 2G segment parameters in LDS
@@ -998,14 +1079,15 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                            korder,
                            (const uint32_t*)(L.rbeg + 2 * kSegs),
                            (const uint32_t*)L.roff, start_al, end_al, R,
-                           ovl_out));
+                           ovl_out, gwin_out));
   }
   if (nm > 0)
     CHOPPER_HIP(launch_shm("ov_markers", k_overlap_markers,
                            grid_for(nm, kBlock * kMarkPerThread),
                            dim3(kBlock), segs_bytes, s, nm, G, mk->gpu,
                            mstart_al, mend_al, R, mwin_out));
-  CHOPPER_HIP(launch("ov_gpus", k_overlap_gpus, grid_for(G, kBlock),
+  if (n == 0)   // (otherwise the communication-records pass writes them)
+    CHOPPER_HIP(launch("ov_gpus", k_overlap_gpus, grid_for(G, kBlock),
                      dim3(kBlock), s, G, R, gwin_out));
   if (n > 0) {
     CHOPPER_HIP(launch("ov_gap", k_gap,

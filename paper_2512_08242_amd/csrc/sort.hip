@@ -152,10 +152,17 @@ __global__ __launch_bounds__(kBlock) void k_class_hist(Acc acc, int64_t n,
     tilehist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
 }
 
+// Block 0 also writes the class start offsets: coff[c] = first position of
+// class c (the scanned table's first tile), coff[C] = n.
 template <typename Acc>
 __global__ __launch_bounds__(kBlock) void k_class_partition(
     Acc acc, int64_t n, int64_t ntiles, const uint32_t* tileoff,
-    uint32_t* out) {
+    uint32_t* out, uint32_t* coff) {
+  if (blockIdx.x == 0) {
+    const int C = acc.nclass();
+    for (int c = threadIdx.x; c <= C; c += kBlock)
+      coff[c] = c < C ? tileoff[(int64_t)c * ntiles] : (uint32_t)n;
+  }
   __shared__ RankShared sh;
   __shared__ uint32_t s_val[kSortTile];
   __shared__ uint8_t s_dig[kSortTile];
@@ -214,15 +221,6 @@ __global__ __launch_bounds__(kBlock) void k_major_sorted(Acc acc, int64_t n,
   }
   if (__ballot(bad) != 0 && (threadIdx.x & (kWave - 1)) == 0)
     atomicOr(unsorted, 1u);
-}
-
-// class start offsets from the scanned table: coff[c] = first position of
-// class c, coff[C] = n
-__global__ void k_class_offsets(const uint32_t* tileoff, int64_t ntiles,
-                                int C, int64_t n, uint32_t* coff) {
-  int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c < C) coff[c] = ntiles > 0 ? tileoff[(int64_t)c * ntiles] : 0u;
-  if (c == C) coff[C] = (uint32_t)n;
 }
 
 // ---------------------------------------------------------------------------
@@ -405,12 +403,9 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
                        dim3(kBlock), s, acc, n, T, L.tilehist));
     CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, L.tileoff, (int64_t)C * T,
                                          L.scantmp, L.total, s));
-    CHOPPER_HIP(launch("sort_class_offsets", k_class_offsets,
-                       grid_for(C + 1, kBlock), dim3(kBlock), s,
-                       (const uint32_t*)L.tileoff, T, C, n, coff));
     CHOPPER_HIP(launch("sort_class_partition", k_class_partition<Acc>,
                        dim3((unsigned)T), dim3(kBlock), s, acc, n, T,
-                       (const uint32_t*)L.tileoff, out));
+                       (const uint32_t*)L.tileoff, out, coff));
     if (known_sorted == 1) {
       sorted = true;
     } else {
@@ -527,7 +522,16 @@ __global__ __launch_bounds__(kBlock) void k_class_hist2(AccA a, AccB b,
 template <typename AccA, typename AccB>
 __global__ __launch_bounds__(kBlock) void k_class_partition2(
     AccA a, AccB b, int64_t n, int64_t ntiles, const uint32_t* tileoff,
-    uint32_t* outA, uint32_t* outB) {
+    uint32_t* outA, uint32_t* outB, uint32_t* coffA, uint32_t* coffB) {
+  if (blockIdx.x == 0) {
+    // class start offsets of both sorts (B's scanned values include A's n)
+    const int CA = a.nclass(), CB = b.nclass();
+    for (int c = threadIdx.x; c <= CA; c += kBlock)
+      coffA[c] = c < CA ? tileoff[(int64_t)c * ntiles] : (uint32_t)n;
+    for (int c = threadIdx.x; c <= CB; c += kBlock)
+      coffB[c] = c < CB ? tileoff[(int64_t)(CA + c) * ntiles] - (uint32_t)n
+                        : (uint32_t)n;
+  }
   __shared__ RankShared sh;
   __shared__ uint32_t s_val[kSortTile];
   __shared__ uint8_t s_dig[kSortTile];
@@ -572,19 +576,6 @@ __global__ __launch_bounds__(kBlock) void k_class_partition2(
   }
 }
 
-// class start offsets of both sorts from the scanned table
-__global__ void k_class_offsets2(const uint32_t* tileoff, int64_t ntiles,
-                                 int CA, int CB, int64_t n, uint32_t* coffA,
-                                 uint32_t* coffB) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c < CA) coffA[c] = ntiles > 0 ? tileoff[(int64_t)c * ntiles] : 0u;
-  if (c == CA) coffA[CA] = (uint32_t)n;
-  if (c < CB)
-    coffB[c] = ntiles > 0 ? tileoff[(int64_t)(CA + c) * ntiles] - (uint32_t)n
-                          : 0u;
-  if (c == CB) coffB[CB] = (uint32_t)n;
-}
-
 template <typename AccA, typename AccB>
 int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
                 uint32_t* outA, uint32_t* coffA, uint32_t* outB,
@@ -600,13 +591,9 @@ int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
   CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, L.tileoff,
                                        (int64_t)(CA + CB) * T, L.scantmp,
                                        L.total, s));
-  CHOPPER_HIP(launch("sort_class_offsets", k_class_offsets2,
-                     grid_for((CA > CB ? CA : CB) + 1, kBlock), dim3(kBlock),
-                     s, (const uint32_t*)L.tileoff, T, CA, CB, n, coffA,
-                     coffB));
   CHOPPER_HIP(launch("sort_class_partition", k_class_partition2<AccA, AccB>,
                      dim3((unsigned)T), dim3(kBlock), s, a, b, n, T,
-                     (const uint32_t*)L.tileoff, outA, outB));
+                     (const uint32_t*)L.tileoff, outA, outB, coffA, coffB));
   return CHOPPER_OK;
 }
 
