@@ -809,7 +809,7 @@ struct NatGeom {
                         // tile t, -1 if none
   const uint32_t* bad;  // nonzero: the input order does not qualify
   int64_t nnt;          // natural tiles
-  int64_t lps;          // row stride of lp (nnt rounded up to kLpChunk)
+  int64_t lps;          // row stride of lp (nnt rounded up to kLpIpt)
   int G;
 };
 
@@ -970,9 +970,12 @@ __global__ __launch_bounds__(kBlock) void k_nat_pre(
   if (__ballot(wrong) != 0 && lane == 0) atomicOr(bad, 1u);
 }
 
-// One block: GPU ranges, tile offsets and the GPU of every tile, and the
-// exclusive running maximum of the last-position table.
-constexpr int kLpChunk = 48;      // table entries per thread and pass
+// Block 0: GPU ranges, tile offsets and the GPU of every tile.  Blocks
+// 1 ..: the exclusive running maximum of the last-position table over
+// kLpSpan entries of each kind, each block taking the maximum of the entries
+// before its span itself.
+constexpr int kLpIpt = 4;                      // entries per thread and kind
+constexpr int64_t kLpSpan = 1024 * kLpIpt;     // entries per block and kind
 __global__ __launch_bounds__(1024) void k_nat_tiles(
     int64_t n, int G, int64_t nnt, int64_t lps, const int32_t* lpraw,
     int32_t* lp, const uint32_t* gs, uint32_t* ge, uint32_t* tb, uint8_t* tg,
@@ -981,97 +984,98 @@ __global__ __launch_bounds__(1024) void k_nat_tiles(
   __shared__ uint32_t s_c[256];
   __shared__ uint32_t s_tb[257];
   __shared__ int32_t s_w[2][1024 / kWave];
+  __shared__ int32_t s_p[2][1024 / kWave];
   const int t = (int)threadIdx.x, lane = lane_id(), w = t / kWave;
-  if (t < G) {
-    const uint32_t a = gs[t];
-    uint32_t e = (uint32_t)n;
-    if (a != kNone) {
-      for (int h = t + 1; h < G; ++h) {
-        const uint32_t b = gs[h];
-        if (b != kNone) {
-          e = b;
-          break;
+  if (blockIdx.x == 0) {
+    if (t < G) {
+      const uint32_t a = gs[t];
+      uint32_t e = (uint32_t)n;
+      if (a != kNone) {
+        for (int h = t + 1; h < G; ++h) {
+          const uint32_t b = gs[h];
+          if (b != kNone) {
+            e = b;
+            break;
+          }
         }
       }
+      ge[t] = a == kNone ? kNone : e;
+      s_c[t] = a == kNone ? 0u
+                          : (e - 1u) / (uint32_t)kWaveTile -
+                                a / (uint32_t)kWaveTile + 1u;
     }
-    ge[t] = a == kNone ? kNone : e;
-    s_c[t] = a == kNone ? 0u
-                        : (e - 1u) / (uint32_t)kWaveTile -
-                              a / (uint32_t)kWaveTile + 1u;
-  }
-  __syncthreads();
-  if (w == 0) {
-    uint32_t carry = 0;
-    for (int b0 = 0; b0 < G; b0 += kWave) {
-      const uint32_t v = b0 + lane < G ? s_c[b0 + lane] : 0u;
-      const uint32_t incl = wave_incl(v, OpAdd(), 0u);
-      if (b0 + lane < G) {
-        tb[b0 + lane] = carry + incl - v;
-        s_tb[b0 + lane] = carry + incl - v;
+    __syncthreads();
+    if (w == 0) {
+      uint32_t carry = 0;
+      for (int b0 = 0; b0 < G; b0 += kWave) {
+        const uint32_t v = b0 + lane < G ? s_c[b0 + lane] : 0u;
+        const uint32_t incl = wave_incl(v, OpAdd(), 0u);
+        if (b0 + lane < G) {
+          tb[b0 + lane] = carry + incl - v;
+          s_tb[b0 + lane] = carry + incl - v;
+        }
+        carry += (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
       }
-      carry += (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+      if (lane == 0) {
+        tb[G] = carry;
+        s_tb[G] = carry;
+      }
     }
-    if (lane == 0) {
-      tb[G] = carry;
-      s_tb[G] = carry;
-    }
+    __syncthreads();
+    for (int g = 0; g < G; ++g)
+      for (uint32_t i = s_tb[g] + (uint32_t)t; i < s_tb[g + 1]; i += 1024)
+        tg[i] = (uint8_t)g;
+    return;
   }
-  __syncthreads();
-  for (int g = 0; g < G; ++g)
-    for (uint32_t i = s_tb[g] + (uint32_t)t; i < s_tb[g + 1]; i += 1024)
-      tg[i] = (uint8_t)g;
-  // both kinds at once; kLpChunk consecutive entries per thread
   OpMax op;
-  int32_t carry[2] = {-1, -1};
-  for (int64_t b0 = 0; b0 < nnt; b0 += 1024 * kLpChunk) {
-    const int64_t i0 = b0 + (int64_t)t * kLpChunk;
-    int32_t v[2][kLpChunk];
-    int32_t acc[2] = {-1, -1};
+  const int64_t b0 = (int64_t)(blockIdx.x - 1) * kLpSpan;
+  const int64_t i0 = b0 + (int64_t)t * kLpIpt;
+  int32_t pre[2] = {-1, -1}, v[2][kLpIpt], acc[2] = {-1, -1};
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-#pragma unroll
-      for (int j = 0; j < kLpChunk; j += 4) {
-        int4 x = make_int4(-1, -1, -1, -1);
-        if (i0 + j < nnt) x = *(const int4*)(lpraw + (int64_t)q * lps + i0 + j);
-        v[q][j] = i0 + j < nnt ? x.x : -1;
-        v[q][j + 1] = i0 + j + 1 < nnt ? x.y : -1;
-        v[q][j + 2] = i0 + j + 2 < nnt ? x.z : -1;
-        v[q][j + 3] = i0 + j + 3 < nnt ? x.w : -1;
-      }
-#pragma unroll
-      for (int j = 0; j < kLpChunk; ++j) acc[q] = op(acc[q], v[q][j]);
+  for (int q = 0; q < 2; ++q) {
+    const int32_t* row = lpraw + (int64_t)q * lps;
+    for (int64_t i = (int64_t)t * kLpIpt; i < b0; i += kLpSpan) {
+      const int4 x = *(const int4*)(row + i);
+      pre[q] = op(pre[q], op(op(x.x, x.y), op(x.z, x.w)));
     }
-    int32_t incl[2];
+    int4 x = make_int4(-1, -1, -1, -1);
+    if (i0 < nnt) x = *(const int4*)(row + i0);
+    v[q][0] = x.x;
+    v[q][1] = i0 + 1 < nnt ? x.y : -1;
+    v[q][2] = i0 + 2 < nnt ? x.z : -1;
+    v[q][3] = i0 + 3 < nnt ? x.w : -1;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      incl[q] = wave_incl(acc[q], op, (int32_t)-1);
-      if (lane == kWave - 1) s_w[q][w] = incl[q];
+    for (int j = 0; j < kLpIpt; ++j) acc[q] = op(acc[q], v[q][j]);
+  }
+  int32_t incl[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    incl[q] = wave_incl(acc[q], op, (int32_t)-1);
+    const int32_t pw = lane63(wave_incl(pre[q], op, (int32_t)-1));
+    if (lane == kWave - 1) {
+      s_w[q][w] = incl[q];
+      s_p[q][w] = pw;
     }
-    __syncthreads();
+  }
+  __syncthreads();
+  if (i0 >= nnt) return;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      int32_t pre = carry[q], tot = carry[q];
-      for (int r = 0; r < 1024 / kWave; ++r) {
-        if (r < w) pre = op(pre, s_w[q][r]);
-        tot = op(tot, s_w[q][r]);
-      }
-      pre = op(pre, wave_shr1_any((int32_t)-1, incl[q]));
-#pragma unroll
-      for (int j = 0; j < kLpChunk; j += 4) {
-        int4 x;
-        x.x = pre;
-        pre = op(pre, v[q][j]);
-        x.y = pre;
-        pre = op(pre, v[q][j + 1]);
-        x.z = pre;
-        pre = op(pre, v[q][j + 2]);
-        x.w = pre;
-        pre = op(pre, v[q][j + 3]);
-        if (i0 + j < nnt) *(int4*)(lp + (int64_t)q * lps + i0 + j) = x;
-      }
-      carry[q] = tot;
+  for (int q = 0; q < 2; ++q) {
+    int32_t p = -1;
+    for (int r = 0; r < 1024 / kWave; ++r) {
+      p = op(p, s_p[q][r]);
+      if (r < w) p = op(p, s_w[q][r]);
     }
-    __syncthreads();
+    p = op(p, wave_shr1_any((int32_t)-1, incl[q]));
+    int4 x;
+    x.x = p;
+    p = op(p, v[q][0]);
+    x.y = p;
+    p = op(p, v[q][1]);
+    x.z = p;
+    p = op(p, v[q][2]);
+    x.w = p;
+    *(int4*)(lp + (int64_t)q * lps + i0) = x;
   }
 }
 
@@ -1875,7 +1879,7 @@ struct AggLayout {
   uint32_t* ntc;          // [L][nstride]
   uint32_t* ntb;
   uint32_t* nscan;
-  int64_t lps;            // ntiles_h rounded up to kLpChunk
+  int64_t lps;            // ntiles_h rounded up to kLpIpt
   int32_t* lpraw;         // [2][lps]
   int32_t* lp;
   uint8_t* tg;            // [ntiles_h + G]
@@ -1923,7 +1927,7 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
   L.ntc = sc.take<uint32_t>((int64_t)L.L * L.nstride);
   L.ntb = sc.take<uint32_t>((int64_t)L.L * L.nstride);
   L.nscan = sc.take<uint32_t>(scan_scratch_elems((int64_t)L.L * L.nstride));
-  L.lps = ceil_div(L.ntiles_h, (int64_t)kLpChunk) * kLpChunk;
+  L.lps = ceil_div(L.ntiles_h, (int64_t)kLpIpt) * kLpIpt;
   L.lpraw = sc.take<int32_t>(2 * L.lps);
   L.lp = sc.take<int32_t>(2 * L.lps);
   L.tg = sc.take<uint8_t>(L.ntiles_h + G);
@@ -1976,7 +1980,8 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                      dim3((unsigned)ceil_div(Th, (int64_t)kWavesPerBlock)),
                      dim3(kBlock), s, S.n, G, S.gpu, S.cls, S.start, Th,
                      L.lps, L.lpraw, L.gs, L.hflags + 2));
-  CHOPPER_HIP(launch("agg_nat_tiles", k_nat_tiles, dim3(1), dim3(1024), s,
+  CHOPPER_HIP(launch("agg_nat_tiles", k_nat_tiles,
+                     dim3((unsigned)(1 + ceil_div(Th, kLpSpan))), dim3(1024), s,
                      S.n, G, Th, L.lps, (const int32_t*)L.lpraw, L.lp,
                      (const uint32_t*)L.gs, L.ge, L.gtb, L.tg,
                      (const uint32_t*)(L.hflags + 2)));
