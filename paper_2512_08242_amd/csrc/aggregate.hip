@@ -1964,12 +1964,10 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
   // the launches of the coarser levels)
   uint32_t hf[3] = {1u, 0u, 1u};
   int64_t lo_h[kMaxLevels + 1];
-  auto read_back = [&]() -> int {
+  auto fetch_stage = [&]() -> int {
     int64_t st[3 + kMaxLevels + 1];
-    CHOPPER_HIP(hipMemcpyAsync(st, L.stage,
-                               sizeof(int64_t) * (size_t)(3 + Lv + 1),
-                               hipMemcpyDeviceToHost, s));
-    CHOPPER_HIP(hipStreamSynchronize(s));
+    CHOPPER_HIP(read_back(L.stage, st,
+                          sizeof(int64_t) * (size_t)(3 + Lv + 1), s));
     for (int i = 0; i < 3; ++i) hf[i] = (uint32_t)st[i];
     for (int i = 0; i <= Lv; ++i) lo_h[i] = st[3 + i];
     return CHOPPER_OK;
@@ -1996,7 +1994,7 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                      (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
                      want_workload, rows->cap, rows->level_offset, L.stage,
                      status));
-  rc = read_back();
+  rc = fetch_stage();
   if (rc != CHOPPER_OK) return rc;
   const bool nat = hf[2] == 0;
   if (!nat) {
@@ -2013,7 +2011,7 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                        (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
                        want_workload, rows->cap, rows->level_offset, L.stage,
                        status));
-    rc = read_back();
+    rc = fetch_stage();
     if (rc != CHOPPER_OK) return rc;
   }
   auto level_rows = [&](int li) -> int64_t {
@@ -2323,9 +2321,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
   }
   // an overflow list that did not fit: redo the marker levels with atomics
   uint32_t lost = 0;
-  CHOPPER_HIP(hipMemcpyAsync(&lost, L.ovf_count + 1, sizeof(uint32_t),
-                             hipMemcpyDeviceToHost, s));
-  CHOPPER_HIP(hipStreamSynchronize(s));
+  CHOPPER_HIP(read_back(L.ovf_count + 1, &lost, sizeof(uint32_t), s));
   if (lost) {
     for (int q = 0; q < nl; ++q) {
       const int li = order_levels[q];

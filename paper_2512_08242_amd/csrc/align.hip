@@ -463,9 +463,7 @@ extern "C" int chopper_align(const chopper_records* rec,
                      dim3(kDenseThreads), s, (const uint8_t*)L.pres_s, L.cmap_s,
                      (const uint8_t*)L.pres_k, L.cmap_k, L.counts));
   uint32_t counts[3];
-  CHOPPER_HIP(hipMemcpyAsync(counts, L.counts, sizeof(counts),
-                             hipMemcpyDeviceToHost, s));
-  CHOPPER_HIP(hipStreamSynchronize(s));
+  CHOPPER_HIP(read_back(L.counts, counts, sizeof(counts), s));
   // counts[2] != 0: the input is not ordered by (gpu, start')
   const int known = counts[2] ? -1 : 1;
   bool range_err = false, r2 = false;

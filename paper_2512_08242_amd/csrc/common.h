@@ -161,7 +161,15 @@ inline hipError_t launch(const char* name, Kern kern, dim3 grid, dim3 block,
   return e;
 }
 
-// the same with `shm` bytes of dynamic LDS
+// Copies `bytes` (a multiple of 4, at most 4 KiB) of device memory at `dev`
+// to `host` once the work queued on `s` before it is done, and returns when
+// they are there.  A one-block kernel stores them into pinned memory of the
+// calling host thread (allocated on its first use, kept for the life of the
+// process) and the host polls the stream, which avoids a copy launch and the
+// runtime's blocking wait.  Callers on one host thread are serialized by it.
+hipError_t read_back(const void* dev, void* host, size_t bytes, hipStream_t s);
+
+// the same as launch() with `shm` bytes of dynamic LDS
 template <typename Kern, typename... Args>
 inline hipError_t launch_shm(const char* name, Kern kern, dim3 grid,
                              dim3 block, size_t shm, hipStream_t s,

@@ -394,9 +394,7 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
                          grid_for(n, kBlock), dim3(kBlock), s, acc, n,
                          L.flag));
       uint32_t unsorted = 1;
-      CHOPPER_HIP(hipMemcpyAsync(&unsorted, L.flag, sizeof(uint32_t),
-                                 hipMemcpyDeviceToHost, s));
-      CHOPPER_HIP(hipStreamSynchronize(s));
+      CHOPPER_HIP(read_back(L.flag, &unsorted, sizeof(uint32_t), s));
       if (unsorted == 0) known_sorted = 1;
     }
     CHOPPER_HIP(launch("sort_class_hist", k_class_hist<Acc>, dim3((unsigned)T),
@@ -417,9 +415,7 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
                          grid_for(n, kBlock), dim3(kBlock), s, acc, n,
                          (const uint32_t*)out, L.flag));
       uint32_t unsorted = 1;
-      CHOPPER_HIP(hipMemcpyAsync(&unsorted, L.flag, sizeof(uint32_t),
-                                 hipMemcpyDeviceToHost, s));
-      CHOPPER_HIP(hipStreamSynchronize(s));
+      CHOPPER_HIP(read_back(L.flag, &unsorted, sizeof(uint32_t), s));
       sorted = (unsorted == 0);
     }
   } else {
@@ -440,8 +436,7 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
                      dim3((unsigned)(T < 1024 ? T : 1024)), dim3(kBlock), s,
                      acc, n, L.mm));
   int64_t mm[2];
-  CHOPPER_HIP(hipMemcpyAsync(mm, L.mm, sizeof(mm), hipMemcpyDeviceToHost, s));
-  CHOPPER_HIP(hipStreamSynchronize(s));
+  CHOPPER_HIP(read_back(L.mm, mm, sizeof(mm), s));
   const int tbits = bitlen_u64((uint64_t)(mm[1] - mm[0]));
   const int cbits = bitlen_u64((uint64_t)(C > 1 ? C - 1 : 0));
   if (tbits + cbits > 64) {
