@@ -145,109 +145,88 @@ __device__ inline void korder_gather(const uint32_t* korder, const uint8_t* gpu,
   e = x > s ? x : s;
 }
 
-// In-place exclusive scan of per-tile values in one block; also the total.
+// Exclusive scans of per-tile values over many blocks of 1024 threads:
+// block b scans tiles [1024 b, 1024 b + 1024), one per thread, after
+// folding every tile before them itself (thread t the b consecutive tiles
+// from t b on, so the fold keeps the tile order); the block of the last
+// tile also writes the total.
+constexpr int kSpineSpan = 1024;
+
+// Ordered fold of one value per thread over the block: the exclusive
+// prefix of the thread and the block total.  `s_w` holds one value per
+// wave and the total; wave 0 scans the wave totals.
+constexpr int kSpineWaves = kSpineSpan / kWave;
 template <typename T, typename Op>
-__global__ __launch_bounds__(1024) void k_tile_spine(T* tile, int64_t ntiles,
-                                                     T ident, T* total) {
-  constexpr int kIpt = 16;   // one pass up to 16384 tiles (33.5M records)
-  constexpr int kT = 1024;
-  __shared__ T s_w[kT / kWave];
-  Op op;
-  T carry = ident;
+__device__ inline T block_excl_ordered(T v, Op op, T ident, T* s_w, T* tot) {
   const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
-  for (int64_t base = 0; base < ntiles; base += (int64_t)kT * kIpt) {
-    T v[kIpt];
-    T acc = ident;
-#pragma unroll
-    for (int j = 0; j < kIpt; ++j) {
-      const int64_t i = base + (int64_t)threadIdx.x * kIpt + j;
-      v[j] = i < ntiles ? tile[i] : ident;
-      acc = op(acc, v[j]);
-    }
-    const T incl = wave_incl(acc, op, ident);
-    if (lane == kWave - 1) s_w[w] = incl;
-    __syncthreads();
-    T pre = carry, tot = carry;
-    for (int i = 0; i < kT / kWave; ++i) {
-      if (i < w) pre = op(pre, s_w[i]);
-      tot = op(tot, s_w[i]);
-    }
-    pre = op(pre, wave_shr1_any(ident, incl));
-#pragma unroll
-    for (int j = 0; j < kIpt; ++j) {
-      const int64_t i = base + (int64_t)threadIdx.x * kIpt + j;
-      if (i < ntiles) tile[i] = pre;
-      pre = op(pre, v[j]);
-    }
-    carry = tot;
-    __syncthreads();
+  const T incl = wave_incl(v, op, ident);
+  if (lane == kWave - 1) s_w[w] = incl;
+  __syncthreads();
+  if (w == 0) {
+    const T x = lane < kSpineWaves ? s_w[lane] : ident;
+    const T xi = wave_incl(x, op, ident);
+    const T xe = wave_shr1_any(ident, xi);
+    if (lane < kSpineWaves) s_w[lane] = xe;
+    if (lane == kWave - 1) s_w[kSpineWaves] = xi;
   }
-  if (threadIdx.x == 0 && total) *total = carry;
+  __syncthreads();
+  *tot = s_w[kSpineWaves];
+  const T pre = s_w[w];
+  __syncthreads();
+  return op(pre, wave_shr1_any(ident, incl));
 }
 
-// One block: the exclusive scan of the tiles' run counts (with the total)
-// and, in place, the segmented scan of their union increments.
-__global__ __launch_bounds__(1024) void k_runs_spine2(
-    const uint32_t* heads, uint32_t* run0, uint32_t* nruns, SegSum* inc,
-    SegSum* inc_total, int64_t ntiles) {
-  constexpr int kIpt = 12;
-  constexpr int kT = 1024;
-  __shared__ uint32_t s_h[kT / kWave];
-  __shared__ SegSum s_i[kT / kWave];
+template <typename T, typename Op>
+__device__ inline T fold_before(const T* in, Op op, T ident, T* s_w) {
+  const int64_t c = blockIdx.x, t = threadIdx.x;
+  T p = ident;
+  for (int64_t k = 0; k < c; ++k) p = op(p, in[t * c + k]);
+  T tot;
+  (void)block_excl_ordered(p, op, ident, s_w, &tot);
+  return tot;
+}
+
+template <typename T, typename Op>
+__global__ __launch_bounds__(kSpineSpan) void k_tile_spine(
+    const T* in, T* out, int64_t ntiles, T ident, T* total) {
+  __shared__ T s_w[kSpineWaves + 1];
+  Op op;
+  const T before = fold_before(in, op, ident, s_w);
+  const int64_t i = (int64_t)blockIdx.x * kSpineSpan + threadIdx.x;
+  const T v = i < ntiles ? in[i] : ident;
+  T tot;
+  const T pre = op(before, block_excl_ordered(v, op, ident, s_w, &tot));
+  if (i < ntiles) out[i] = pre;
+  if (total && threadIdx.x == 0 &&
+      (int64_t)(blockIdx.x + 1) * kSpineSpan >= ntiles)
+    *total = op(before, tot);
+}
+
+// The exclusive scan of the tiles' run counts (with the total) and the
+// segmented scan of their union increments (with the total).
+__global__ __launch_bounds__(kSpineSpan) void k_runs_spine2(
+    const uint32_t* heads, uint32_t* run0, uint32_t* nruns,
+    const SegSum* inc, SegSum* inc_pre, SegSum* inc_total, int64_t ntiles) {
+  __shared__ uint32_t s_h[kSpineWaves + 1];
+  __shared__ SegSum s_i[kSpineWaves + 1];
   OpSegSum op;
   const SegSum ident = segsum_ident();
-  uint32_t hcarry = 0;
-  SegSum icarry = ident;
-  const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
-  for (int64_t base = 0; base < ntiles; base += (int64_t)kT * kIpt) {
-    uint32_t h[kIpt];
-    SegSum v[kIpt];
-    uint32_t hacc = 0;
-    SegSum iacc = ident;
-#pragma unroll
-    for (int j = 0; j < kIpt; ++j) {
-      const int64_t i = base + (int64_t)threadIdx.x * kIpt + j;
-      h[j] = i < ntiles ? heads[i] : 0u;
-      v[j] = i < ntiles ? inc[i] : ident;
-      hacc += h[j];
-      iacc = op(iacc, v[j]);
-    }
-    const uint32_t hin = wave_incl(hacc, OpAdd(), 0u);
-    const SegSum iin = wave_incl(iacc, op, ident);
-    if (lane == kWave - 1) {
-      s_h[w] = hin;
-      s_i[w] = iin;
-    }
-    __syncthreads();
-    uint32_t hp = hcarry, ht = hcarry;
-    SegSum ip = icarry, it = icarry;
-    for (int q = 0; q < kT / kWave; ++q) {
-      if (q < w) {
-        hp += s_h[q];
-        ip = op(ip, s_i[q]);
-      }
-      ht += s_h[q];
-      it = op(it, s_i[q]);
-    }
-    hp += hin - hacc;
-    ip = op(ip, wave_shr1_any(ident, iin));
-#pragma unroll
-    for (int j = 0; j < kIpt; ++j) {
-      const int64_t i = base + (int64_t)threadIdx.x * kIpt + j;
-      if (i < ntiles) {
-        run0[i] = hp;
-        inc[i] = ip;
-      }
-      hp += h[j];
-      ip = op(ip, v[j]);
-    }
-    hcarry = ht;
-    icarry = it;
-    __syncthreads();
+  const uint32_t hb = fold_before(heads, OpAdd(), 0u, s_h);
+  const SegSum ib = fold_before(inc, op, ident, s_i);
+  const int64_t i = (int64_t)blockIdx.x * kSpineSpan + threadIdx.x;
+  const uint32_t h = i < ntiles ? heads[i] : 0u;
+  const SegSum v = i < ntiles ? inc[i] : ident;
+  uint32_t ht;
+  SegSum it;
+  const uint32_t hp = hb + block_excl_ordered(h, OpAdd(), 0u, s_h, &ht);
+  const SegSum ip = op(ib, block_excl_ordered(v, op, ident, s_i, &it));
+  if (i < ntiles) {
+    run0[i] = hp;
+    inc_pre[i] = ip;
   }
-  if (threadIdx.x == 0) {
-    *nruns = hcarry;
-    *inc_total = icarry;
+  if (threadIdx.x == 0 && (int64_t)(blockIdx.x + 1) * kSpineSpan >= ntiles) {
+    *nruns = hb + ht;
+    *inc_total = op(ib, it);
   }
 }
 
@@ -925,10 +904,12 @@ __global__ __launch_bounds__(kBlock) void k_gap(
 struct OverlapLayout {
   int64_t ntiles;
   SegMax* tile_agg;
+  SegMax* tile_pre;     // exclusive scan of tile_agg
   SegMax* tile_first;   // first item of every tile: (segment, start)
   SegMax* grand;
   uint32_t* tile_heads;
   SegSum* tile_inc;
+  SegSum* tile_incp;    // exclusive segmented scan of tile_inc
   SegSum* inc_total;
   uint32_t* tile_run0;
   uint32_t* nruns;
@@ -956,10 +937,12 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   OverlapLayout L;
   L.ntiles = ceil_div(n, kOvTile);
   L.tile_agg = sc.take<SegMax>(L.ntiles);
+  L.tile_pre = sc.take<SegMax>(L.ntiles);
   L.tile_first = sc.take<SegMax>(L.ntiles);
   L.grand = sc.take<SegMax>(1);
   L.tile_heads = sc.take<uint32_t>(L.ntiles);
   L.tile_inc = sc.take<SegSum>(L.ntiles);
+  L.tile_incp = sc.take<SegSum>(L.ntiles);
   L.inc_total = sc.take<SegSum>(1);
   L.tile_run0 = sc.take<uint32_t>(L.ntiles);
   L.nruns = sc.take<uint32_t>(1);
@@ -1026,22 +1009,23 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
                        (const SegMax*)nullptr, L.tile_agg, L.tile_first,
                        L.tile_heads, L.tile_inc, L.rbeg));
-    CHOPPER_HIP(launch("ov_runs_spine", k_tile_spine<SegMax, OpSegMax>,
-                       dim3(1), dim3(1024), s, L.tile_agg, L.ntiles,
-                       SegMax{0u, kI64Min}, L.grand));
+    const dim3 sg((unsigned)ceil_div(L.ntiles, (int64_t)kSpineSpan));
+    CHOPPER_HIP(launch("ov_runs_spine", k_tile_spine<SegMax, OpSegMax>, sg,
+                       dim3(kSpineSpan), s, (const SegMax*)L.tile_agg,
+                       L.tile_pre, L.ntiles, SegMax{0u, kI64Min}, L.grand));
     CHOPPER_HIP(launch("ov_runs_fixup", k_runs_count, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
-                       (const SegMax*)L.tile_agg, (SegMax*)nullptr,
+                       (const SegMax*)L.tile_pre, (SegMax*)nullptr,
                        L.tile_first, L.tile_heads, L.tile_inc,
                        (uint32_t*)nullptr));
-    CHOPPER_HIP(launch("ov_runs_inc_spine", k_runs_spine2, dim3(1),
-                       dim3(1024), s, (const uint32_t*)L.tile_heads,
-                       L.tile_run0, L.nruns, L.tile_inc, L.inc_total,
-                       L.ntiles));
+    CHOPPER_HIP(launch("ov_runs_inc_spine", k_runs_spine2, sg,
+                       dim3(kSpineSpan), s, (const uint32_t*)L.tile_heads,
+                       L.tile_run0, L.nruns, (const SegSum*)L.tile_inc,
+                       L.tile_incp, L.inc_total, L.ntiles));
     CHOPPER_HIP(launch("ov_runs_write", k_runs_write, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
-                       (const SegMax*)L.tile_agg, (const uint32_t*)L.tile_run0,
-                       (const SegSum*)L.tile_inc, (const uint32_t*)L.nruns,
+                       (const SegMax*)L.tile_pre, (const uint32_t*)L.tile_run0,
+                       (const SegSum*)L.tile_incp, (const uint32_t*)L.nruns,
                        (const SegMax*)L.grand, L.rs, L.re, L.pl, L.rseg,
                        L.rbeg, L.rend, L.btable, L.btable_cap));
   }
