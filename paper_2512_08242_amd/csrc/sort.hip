@@ -493,16 +493,23 @@ __global__ __launch_bounds__(kBlock) void k_class_hist2(AccA a, AccB b,
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   const int64_t base = (int64_t)blockIdx.x * kSortTile;
   const int nb[2] = {class_bits(a.nclass()), class_bits(b.nclass())};
+  // every class id of the tile first (all loads in flight), then the counts
+  uint32_t d[kSortIpt][2];
+  bool v[kSortIpt];
 #pragma unroll
   for (int j = 0; j < kSortIpt; ++j) {
     const int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
-    const bool v = i < n;
-    const uint32_t d[2] = {v ? a.cls(i) : 0u, v ? b.cls(i) : 0u};
+    v[j] = i < n;
+    d[j][0] = v[j] ? a.cls(i) : 0u;
+    d[j][1] = v[j] ? b.cls(i) : 0u;
+  }
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j) {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const uint64_t peers = digit_peers(d[q], v, nb[q]);
-      if (v && __popcll(peers & lt) == 0)
-        atomicAdd(&h[q][d[q]], (uint32_t)__popcll(peers));
+      const uint64_t peers = digit_peers(d[j][q], v[j], nb[q]);
+      if (v[j] && __popcll(peers & lt) == 0)
+        atomicAdd(&h[q][d[j][q]], (uint32_t)__popcll(peers));
     }
   }
   __syncthreads();
