@@ -120,6 +120,10 @@ def _load():
     lib.orc_ratios.restype = None
     lib.orc_window_fractions.argtypes = [i64, P, P]
     lib.orc_window_fractions.restype = None
+    lib.orc_views.argtypes = [i64, P, P, P, P, i32, P, P, i64, P, P, i32, i32,
+                              i32, i32, i32, i32, ctypes.c_uint32, i64, P, P,
+                              P, P, P, P, P, P, P, P, P, P]
+    lib.orc_views.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -251,6 +255,43 @@ def window_fractions(w: np.ndarray) -> np.ndarray:
     w = _c(w, np.int64).reshape(-1, 4)
     out = np.empty(w.shape, np.float64)
     lib.orc_window_fractions(w.shape[0], _p(w), _p(out))
+    return out
+
+
+def views(cls, s, e, idx, gap, ovl, m_level, m_label, iter_level=0,
+          phase_level=1, op_level=3, n_phases=3, n_ops=64, n_iters=1,
+          warmup=0) -> Dict:
+    """Re-keyed views and medians (Fig. end_to_end, V-B / Fig.
+    operation_time, warm-up iterations of IV); definitions in oracle.c."""
+    lib = _load()
+    n = int(np.asarray(s).shape[0])
+    nm = int(np.asarray(m_level).shape[0])
+    idx = _c(idx, np.uint32).reshape(-1)
+    depth = idx.shape[0] // n if n else 0
+    U = int((np.asarray(m_level) == iter_level).sum())
+    P, O, NI = int(n_phases), int(n_ops), int(n_iters)
+    out = dict(
+        n_units=np.zeros(1, np.int64), unit_marker=np.zeros(U, np.uint32),
+        cls_tab=np.zeros((3, U * P * 8), np.uint64),
+        op_tab=np.zeros((4, U * P * O * 2), np.uint64),
+        busy=np.zeros(U, np.int64), iter_max=np.zeros(NI, np.int64),
+        cls_med=np.zeros((3, P * 8)), cls_cnt=np.zeros(P * 8, np.int64),
+        op_med=np.zeros((3, P * O * 2)), op_cnt=np.zeros(P * O * 2, np.int64),
+        iter_med=np.zeros(1), iter_cnt=np.zeros(1, np.int64))
+    a = [_c(cls, np.uint8), _c(s, np.int64), _c(e, np.int64), idx,
+         _c(gap, np.int64), _c(ovl, np.int64), _c(m_level, np.uint8),
+         _c(m_label, np.uint32)]
+    rc = lib.orc_views(n, _p(a[0]), _p(a[1]), _p(a[2]), _p(a[3]), depth,
+                       _p(a[4]), _p(a[5]), nm, _p(a[6]), _p(a[7]), iter_level,
+                       phase_level, op_level, P, O, NI, warmup, U,
+                       *[_p(out[k]) for k in (
+                           "n_units", "unit_marker", "cls_tab", "op_tab",
+                           "busy", "iter_max", "cls_med", "cls_cnt", "op_med",
+                           "op_cnt", "iter_med", "iter_cnt")])
+    assert rc == 0
+    out["n_units"] = int(out["n_units"][0])
+    out["iter_med"] = float(out["iter_med"][0])
+    out["iter_cnt"] = int(out["iter_cnt"][0])
     return out
 
 

@@ -723,3 +723,143 @@ void orc_window_fractions(int64_t nw, const int64_t* w, double* out) {
       out[4 * j + z] = (double)w[4 * j + z] / (double)len;
   }
 }
+
+/* ------------------------------------------------------------------------
+ * Re-keyed views and their statistics.
+ *
+ * Figure "end_to_end": per phase and kernel class, duration = sum of kernel
+ * durations and launch overhead = sum of bubbles, median values across
+ * iterations and GPUs; throughput from the largest duration plus launch
+ * overhead across GPUs.  Section V-B and Figure "operation_time": operation
+ * duration summed across layers with the bubbles between its kernels, one
+ * data point per iteration and GPU.  Section IV: the first iterations are
+ * warm-up and are not sampled.
+ *
+ * A unit is one marker of level iter_level (one GPU's iteration), numbered
+ * in marker input order.  A record belongs to the unit of its level
+ * iter_level marker, to the phase labelled by its level phase_level marker
+ * and to the operation labelled by its level op_level marker (NONE: none).
+ * Tables (sums wrap modulo 2^64 like every other sum here):
+ *   cls_tab [3][U * P * 8]     n, dur, gap by (unit, phase label, class)
+ *   op_tab  [4][U * P * O * 2] n, dur, gap, ovl by (unit, phase label,
+ *                              operation label, kind)
+ *   busy    [U]                sum of dur + gap of the unit's compute records
+ *   iter_max [NI]              max of busy over the units whose iteration
+ *                              label is i, -1 if there is none
+ * A record counts in cls_tab when it has a unit and a phase label < P, in
+ * op_tab when also its operation label < O; busy needs only the unit.
+ * Medians (st = dur, gap, dur + gap): over the units whose iteration label
+ * is >= warmup and whose table entry has n > 0, the middle values lo =
+ * v[(m - 1) / 2] and hi = v[m / 2] of the m sorted values, median =
+ * ((double)lo + (double)hi) / 2 (NaN when m = 0).  iter_med: the same over
+ * iter_max[i] >= 0 for warmup <= i < NI.
+ * ------------------------------------------------------------------------ */
+static int cmp_i64(const void* x, const void* y) {
+  const int64_t a = *(const int64_t*)x, b = *(const int64_t*)y;
+  return a < b ? -1 : a > b;
+}
+
+static double median_of(int64_t* v, int64_t m) {
+  if (m == 0) return __builtin_nan("");
+  qsort(v, (size_t)m, sizeof(int64_t), cmp_i64);
+  return ((double)v[(m - 1) / 2] + (double)v[m / 2]) / 2.0;
+}
+
+int orc_views(int64_t n, const uint8_t* cls, const int64_t* s,
+              const int64_t* e, const uint32_t* idx, int depth,
+              const int64_t* gap, const int64_t* ovl, int64_t nm,
+              const uint8_t* m_level, const uint32_t* m_label, int iter_level,
+              int phase_level, int op_level, int P, int O, int NI,
+              uint32_t warmup, int64_t unit_cap, int64_t* n_units,
+              uint32_t* unit_marker, uint64_t* cls_tab, uint64_t* op_tab,
+              int64_t* busy, int64_t* iter_max, double* cls_med,
+              int64_t* cls_cnt, double* op_med, int64_t* op_cnt,
+              double* iter_med, int64_t* iter_cnt) {
+  /* units: the iteration markers in input order */
+  int64_t U = 0;
+  uint32_t* unit_of = (uint32_t*)malloc(sizeof(uint32_t) * (size_t)(nm + 1));
+  for (int64_t m = 0; m < nm; ++m) {
+    unit_of[m] = ORC_NONE;
+    if (m_level[m] == (uint8_t)iter_level) {
+      if (U < unit_cap) unit_marker[U] = (uint32_t)m;
+      unit_of[m] = (uint32_t)U;
+      ++U;
+    }
+  }
+  *n_units = U;
+  if (U > unit_cap) {
+    free(unit_of);
+    return -1;
+  }
+  const int64_t nc = U * P * 8, no = U * P * O * 2;
+  memset(cls_tab, 0, sizeof(uint64_t) * (size_t)(3 * nc));
+  memset(op_tab, 0, sizeof(uint64_t) * (size_t)(4 * no));
+  for (int64_t u = 0; u < U; ++u) busy[u] = 0;
+  /* one pass over the records */
+  for (int64_t r = 0; r < n; ++r) {
+    const uint32_t mi = idx[(int64_t)iter_level * n + r];
+    if (mi == ORC_NONE) continue;
+    const int64_t u = unit_of[mi];
+    const int64_t dur = e[r] - s[r];
+    const int kd = kind_of(cls[r]);
+    if (kd == 0)
+      busy[u] = (int64_t)((uint64_t)busy[u] + (uint64_t)dur + (uint64_t)gap[r]);
+    const uint32_t mp = idx[(int64_t)phase_level * n + r];
+    if (mp == ORC_NONE || m_label[mp] >= (uint32_t)P) continue;
+    const int64_t p = m_label[mp];
+    if (cls[r] < 8) {
+      const int64_t k = (u * P + p) * 8 + cls[r];
+      cls_tab[k] += 1;
+      cls_tab[nc + k] += (uint64_t)dur;
+      cls_tab[2 * nc + k] += (uint64_t)gap[r];
+    }
+    const uint32_t mo = idx[(int64_t)op_level * n + r];
+    if (mo == ORC_NONE || m_label[mo] >= (uint32_t)O) continue;
+    const int64_t k = ((u * P + p) * O + m_label[mo]) * 2 + kd;
+    op_tab[k] += 1;
+    op_tab[no + k] += (uint64_t)dur;
+    op_tab[2 * no + k] += (uint64_t)gap[r];
+    op_tab[3 * no + k] += (uint64_t)ovl[r];
+  }
+  for (int i = 0; i < NI; ++i) iter_max[i] = -1;
+  for (int64_t u = 0; u < U; ++u) {
+    const uint32_t lab = m_label[unit_marker[u]];
+    if (lab < (uint32_t)NI && busy[u] > iter_max[lab]) iter_max[lab] = busy[u];
+  }
+  /* medians over the kept units */
+  int64_t* v = (int64_t*)malloc(sizeof(int64_t) * (size_t)(U + NI + 1));
+  for (int g = 0; g < P * 8; ++g) {
+    for (int st = 0; st < 3; ++st) {
+      int64_t m = 0;
+      for (int64_t u = 0; u < U; ++u) {
+        const int64_t k = u * P * 8 + g;
+        if (m_label[unit_marker[u]] < warmup || cls_tab[k] == 0) continue;
+        const uint64_t d = cls_tab[nc + k], b = cls_tab[2 * nc + k];
+        v[m++] = (int64_t)(st == 0 ? d : st == 1 ? b : d + b);
+      }
+      cls_cnt[g] = m;
+      cls_med[(int64_t)st * P * 8 + g] = median_of(v, m);
+    }
+  }
+  for (int64_t g = 0; g < (int64_t)P * O * 2; ++g) {
+    for (int st = 0; st < 3; ++st) {
+      int64_t m = 0;
+      for (int64_t u = 0; u < U; ++u) {
+        const int64_t k = u * P * O * 2 + g;
+        if (m_label[unit_marker[u]] < warmup || op_tab[k] == 0) continue;
+        const uint64_t d = op_tab[no + k], b = op_tab[2 * no + k];
+        v[m++] = (int64_t)(st == 0 ? d : st == 1 ? b : d + b);
+      }
+      op_cnt[g] = m;
+      op_med[(int64_t)st * P * O * 2 + g] = median_of(v, m);
+    }
+  }
+  int64_t m = 0;
+  for (int i = (int)warmup; i < NI; ++i)
+    if (i >= 0 && iter_max[i] >= 0) v[m++] = iter_max[i];
+  *iter_cnt = m;
+  *iter_med = median_of(v, m);
+  free(v);
+  free(unit_of);
+  return 0;
+}
