@@ -17,6 +17,9 @@
  *                      granularity, optionally filtered by GPU / class /
  *                      iteration                  (Section III-C)
  *   chopper_ratios     derived metrics per aggregated row (III-C; eq. 10)
+ *   chopper_views      per-phase/class and per-operation views with medians
+ *                      over iterations and GPUs, iteration throughput
+ *                      (Fig. end_to_end, Fig. operation_time)
  *
  * Memory.  Every pointer is a DEVICE pointer unless marked [host].  The caller
  * owns every buffer.  The library allocates no device memory, frees nothing
@@ -300,6 +303,81 @@ int chopper_ratios(const chopper_rows* rows, int32_t depth, int32_t n_counters,
  */
 int chopper_window_fractions(int64_t n, const int64_t* win, double* out,
                              void* stream);
+
+/*
+ * chopper_views -- re-keyed views of the aggregated run and their statistics
+ * (caption of Fig. end_to_end: duration = sum of kernel durations, launch
+ * overhead = sum of bubbles, per phase and kernel class, median values
+ * across iterations and GPUs, throughput from the largest duration plus
+ * launch overhead across GPUs; Section V-B and Fig. operation_time:
+ * operation duration summed across layers including the bubbles between its
+ * kernels, one data point per iteration and GPU; Section IV: the first
+ * iterations are warm-up and not sampled).
+ *
+ * A unit is one marker of level spec->iter_level (one GPU's iteration),
+ * numbered in marker input order; out->unit_marker[u] is its marker index
+ * and *out->n_units the number of units.  A record belongs to the unit of
+ * its level iter_level marker, to the phase labelled by its level
+ * phase_level marker and to the operation labelled by its level op_level
+ * marker (no marker: none).  With P = n_phases, O = n_ops, C = unit_cap:
+ *   cls_tab [3][C * P * 8]      n, dur, gap summed by (unit, phase label,
+ *                               class), index (u * P + p) * 8 + class
+ *   op_tab  [4][C * P * O * 2]  n, dur, gap, ovl summed by (unit, phase
+ *                               label, operation label, kind), index
+ *                               ((u * P + p) * O + o) * 2 + kind
+ *   busy    [C]                 sum of dur + gap of the unit's compute
+ *                               records (whatever their phase)
+ *   iter_max [n_iters]          the largest busy among the units whose
+ *                               iteration label is i, -1 if none
+ * Records without a unit, or with a phase label >= P, are in neither table;
+ * op_tab also needs an operation label < O.  Sums wrap modulo 2^64.
+ *   cls_med [3][P * 8], op_med [3][P * O * 2]: for dur, gap and dur + gap,
+ *   the median over the units whose iteration label is >= warmup and whose
+ *   entry has n > 0: with the m values sorted, ((double)v[(m-1)/2] +
+ *   (double)v[m/2]) / 2, NaN when m = 0; cls_cnt / op_cnt hold m.
+ *   iter_med [1], iter_cnt [1]: the same over iter_max[i] >= 0 for
+ *   warmup <= i < n_iters (throughput = tokens per iteration / iter_med).
+ * Inputs: start_al / end_al / idx / gap from chopper_align, chopper_attribute
+ * and chopper_overlap; rows from chopper_aggregate of the same records
+ * without a filter, at level op_level or CHOPPER_LEVEL_ALL (op_tab is the
+ * re-keyed level op_level rows).  Levels < depth <= markers->depth;
+ * 1 <= n_phases <= 16, 1 <= n_ops <= 128, n_iters >= 0, unit_cap * n_phases
+ * < 2^32.  More units than unit_cap: ROWS_OVERFLOW, *n_units holds the
+ * count, outputs unspecified.  Every output array is written.
+ */
+typedef struct {
+  int32_t iter_level;
+  int32_t phase_level;
+  int32_t op_level;
+  int32_t n_phases;
+  int32_t n_ops;
+  int32_t n_iters;
+  uint32_t warmup;
+  int32_t reserved;
+} chopper_view_spec;
+
+typedef struct {
+  int64_t unit_cap;
+  int64_t* n_units;
+  uint32_t* unit_marker;
+  uint64_t* cls_tab;
+  uint64_t* op_tab;
+  int64_t* busy;
+  int64_t* iter_max;
+  double* cls_med;
+  int64_t* cls_cnt;
+  double* op_med;
+  int64_t* op_cnt;
+  double* iter_med;
+  int64_t* iter_cnt;
+} chopper_view_out;
+
+int chopper_views(const chopper_records* records, const int64_t* start_al,
+                  const int64_t* end_al, const uint32_t* idx, int32_t depth,
+                  const int64_t* gap, const chopper_markers* markers,
+                  const chopper_rows* rows, const chopper_view_spec* spec,
+                  const chopper_view_out* out, void* scratch,
+                  size_t* scratch_bytes, uint32_t* status, void* stream);
 
 /* Text for a return code. */
 const char* chopper_strerror(int code);

@@ -61,6 +61,22 @@ class Rows(ctypes.Structure):
                 ("ctr", P)]
 
 
+class ViewSpec(ctypes.Structure):
+    _fields_ = [("iter_level", ctypes.c_int32), ("phase_level", ctypes.c_int32),
+                ("op_level", ctypes.c_int32), ("n_phases", ctypes.c_int32),
+                ("n_ops", ctypes.c_int32), ("n_iters", ctypes.c_int32),
+                ("warmup", ctypes.c_uint32), ("reserved", ctypes.c_int32)]
+
+
+_VIEW_OUT = ("n_units", "unit_marker", "cls_tab", "op_tab", "busy",
+             "iter_max", "cls_med", "cls_cnt", "op_med", "op_cnt", "iter_med",
+             "iter_cnt")
+
+
+class ViewOut(ctypes.Structure):
+    _fields_ = [("unit_cap", ctypes.c_int64)] + [(k, P) for k in _VIEW_OUT]
+
+
 def make_filter(gpus=None, classes=None, iters=None) -> Filter:
     f = Filter()
     mask = [0, 0, 0, 0]
@@ -104,6 +120,11 @@ def _load():
     lib.chopper_ratios.argtypes = [ctypes.POINTER(Rows), i32, i32,
                                    ctypes.c_double, P, P]
     lib.chopper_window_fractions.argtypes = [i64, P, P, P]
+    lib.chopper_views.argtypes = [ctypes.POINTER(Records), P, P, P, i32, P,
+                                  ctypes.POINTER(Markers),
+                                  ctypes.POINTER(Rows),
+                                  ctypes.POINTER(ViewSpec),
+                                  ctypes.POINTER(ViewOut), P, SZ, P, P]
     lib.chopper_strerror.argtypes = [ctypes.c_int]
     lib.chopper_strerror.restype = ctypes.c_char_p
     lib.chopper_version.restype = ctypes.c_int
@@ -113,7 +134,7 @@ def _load():
     for name in ("chopper_align", "chopper_attribute", "chopper_overlap",
                  "chopper_aggregate", "chopper_ratios",
                  "chopper_window_fractions", "chopper_version",
-                 "chopper_time_kernel"):
+                 "chopper_time_kernel", "chopper_views"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -423,3 +444,68 @@ class Pipeline:
             ratios=u(self.ratios[:, :nr], np.float64).reshape(6, nr),
             wfrac=u(self.wfrac[:nm], np.float64).reshape(nm, 4),
             status=int(self.status.item()) & 0xFFFFFFFF)
+
+
+class Views:
+    """Re-keyed views of a Pipeline's run (chopper_views): per (iteration
+    unit, phase, class) and (unit, phase, operation, kind) sums, busy time
+    per unit, its maximum per iteration, and medians over the units."""
+
+    def __init__(self, pipe: Pipeline, iter_level: int = 0,
+                 phase_level: int = 1, op_level: int = 3, n_phases: int = 3,
+                 n_ops: int = 64, n_iters: int = 1, warmup: int = 0):
+        self.pipe = pipe
+        dt = pipe.dt
+        dev = dt.start.device
+        self.spec = ViewSpec(iter_level, phase_level, op_level, n_phases,
+                             n_ops, n_iters, warmup, 0)
+        U = int((dt.m_level == iter_level).sum().item()) if dt.n_markers else 0
+        Pn, O, NI = n_phases, n_ops, n_iters
+        e = lambda n, dt_: torch.empty(max(n, 1), dtype=dt_, device=dev)
+        self.U, self.P, self.O, self.NI = U, Pn, O, NI
+        self.t = dict(
+            n_units=e(1, torch.int64), unit_marker=e(U, torch.int32),
+            cls_tab=e(3 * U * Pn * 8, torch.int64),
+            op_tab=e(4 * U * Pn * O * 2, torch.int64),
+            busy=e(U, torch.int64), iter_max=e(NI, torch.int64),
+            cls_med=e(3 * Pn * 8, torch.float64),
+            cls_cnt=e(Pn * 8, torch.int64),
+            op_med=e(3 * Pn * O * 2, torch.float64),
+            op_cnt=e(Pn * O * 2, torch.int64),
+            iter_med=e(1, torch.float64), iter_cnt=e(1, torch.int64))
+        self.out = ViewOut()
+        self.out.unit_cap = U
+        for k in _VIEW_OUT:
+            setattr(self.out, k, _ptr(self.t[k]))
+        self._scr = _scratch(lambda s, b: self._call(s, b), dev)
+
+    def _call(self, scratch, sbytes):
+        pp, dt = self.pipe, self.pipe.dt
+        rows = pp.rows.struct()
+        self._rows = rows
+        return lib.chopper_views(
+            ctypes.byref(pp._rec), _ptr(pp.start), _ptr(pp.end), _ptr(pp.idx),
+            dt.depth, _ptr(pp.gap), ctypes.byref(pp._mk), ctypes.byref(rows),
+            ctypes.byref(self.spec), ctypes.byref(self.out), scratch, sbytes,
+            _ptr(pp.status), _stream())
+
+    def run(self):
+        scr, sb = _aligned(self._scr)
+        _check(self._call(scr, ctypes.byref(sb)), "views")
+
+    def results(self) -> Dict:
+        torch.cuda.synchronize()
+        U, Pn, O, NI = self.U, self.P, self.O, self.NI
+        u = lambda k, n, dt_: self.t[k][:n].cpu().numpy().view(dt_)
+        return dict(
+            n_units=int(self.t["n_units"][0].item()),
+            unit_marker=u("unit_marker", U, np.uint32),
+            cls_tab=u("cls_tab", 3 * U * Pn * 8, np.uint64).reshape(3, -1),
+            op_tab=u("op_tab", 4 * U * Pn * O * 2, np.uint64).reshape(4, -1),
+            busy=u("busy", U, np.int64), iter_max=u("iter_max", NI, np.int64),
+            cls_med=u("cls_med", 3 * Pn * 8, np.float64).reshape(3, -1),
+            cls_cnt=u("cls_cnt", Pn * 8, np.int64),
+            op_med=u("op_med", 3 * Pn * O * 2, np.float64).reshape(3, -1),
+            op_cnt=u("op_cnt", Pn * O * 2, np.int64),
+            iter_med=float(self.t["iter_med"][0].item()),
+            iter_cnt=int(self.t["iter_cnt"][0].item()))

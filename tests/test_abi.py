@@ -33,7 +33,8 @@ def test_header_declares_the_four_steps():
     for n in ("chopper_align", "chopper_attribute", "chopper_overlap",
               "chopper_aggregate", "chopper_ratios",
               "chopper_window_fractions", "chopper_strerror",
-              "chopper_version", "chopper_time_kernel", "chopper_kernel_name"):
+              "chopper_version", "chopper_time_kernel", "chopper_kernel_name",
+              "chopper_views"):
         assert n in names
 
 
@@ -202,3 +203,57 @@ def test_anchor_errors_are_reported_before_gpu_work(ch):
                            ctypes.c_void_p(0x100000), ctypes.byref(sz), status,
                            None)
     assert rc == -3
+
+
+def test_views_scratch_query_and_argument_errors(ch):
+    """chopper_views answers the scratch query without GPU work and rejects
+    bad specs synchronously."""
+    lib, b = ch.lib, ch.binding
+    fake = ctypes.c_void_p(0x1000)
+    rec = b.Records()
+    rec.n, rec.n_gpus, rec.n_counters = 1000, 2, 0
+    rec.gpu = rec.stream = rec.cls = rec.start_ns = rec.end_ns = fake
+    mk = b.Markers()
+    mk.n, mk.depth = 500, 4
+    mk.gpu = mk.level = mk.start_ns = mk.end_ns = mk.label = fake
+    rows = b.Rows()
+    rows.cap = 10
+    for k in ("level_offset", "path", "gpu", "kind", "n", "dur", "gap", "ovl",
+              "tmin", "tmax", "first"):
+        setattr(rows, k, fake)
+    out = b.ViewOut()
+    out.unit_cap = 16
+    for k in b._VIEW_OUT:
+        setattr(out, k, fake)
+
+    def call(spec, out_=out, scratch=None):
+        sz = ctypes.c_size_t(0)
+        rc = lib.chopper_views(ctypes.byref(rec), fake, fake, fake, 4, fake,
+                               ctypes.byref(mk), ctypes.byref(rows),
+                               ctypes.byref(spec), ctypes.byref(out_),
+                               scratch, ctypes.byref(sz), None, None)
+        return rc, sz.value
+
+    good = b.ViewSpec(0, 1, 3, 3, 64, 10, 0, 0)
+    rc, sz = call(good)
+    assert rc == 0 and sz > 0
+    for bad in (b.ViewSpec(0, 1, 4, 3, 64, 10, 0, 0),    # level >= depth
+                b.ViewSpec(-1, 1, 3, 3, 64, 10, 0, 0),
+                b.ViewSpec(0, 1, 3, 0, 64, 10, 0, 0),    # no phase
+                b.ViewSpec(0, 1, 3, 17, 64, 10, 0, 0),   # > 16 phases
+                b.ViewSpec(0, 1, 3, 3, 129, 10, 0, 0),   # > 128 operations
+                b.ViewSpec(0, 1, 3, 3, 64, -1, 0, 0)):
+        assert call(bad)[0] == -1
+    o2 = b.ViewOut()
+    o2.unit_cap = 16
+    for k in b._VIEW_OUT:
+        setattr(o2, k, fake)
+    o2.op_med = None
+    assert call(good, o2)[0] == -1
+    # too small a scratch buffer
+    sz = ctypes.c_size_t(8)
+    assert lib.chopper_views(ctypes.byref(rec), fake, fake, fake, 4, fake,
+                             ctypes.byref(mk), ctypes.byref(rows),
+                             ctypes.byref(good), ctypes.byref(out),
+                             ctypes.c_void_p(0x10000), ctypes.byref(sz), fake,
+                             None) == -2
