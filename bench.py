@@ -3,7 +3,9 @@
 One step = chopper_align + chopper_attribute + chopper_overlap +
 chopper_aggregate(all levels) + derived ratios over the whole synthetic trace
 of 8 GPUs x 800 iterations x 32 layers with 16 counters per record (the
-Llama-3-8B FSDP trace shape), inputs resident in HBM.  Prints one JSON line.
+Llama-3-8B FSDP trace shape), inputs resident in HBM.  After the timed steps
+chopper_views (per-phase/class and per-operation views with their medians)
+is timed on its own over the same run ("views").  Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--config 3]
 """
@@ -45,6 +47,16 @@ def roof_kernel_bytes(n, depth, nc, rows_written, input_order):
     per_rec = (0 if input_order else 4) + 1 + 1 + 4 * depth + 8 * 4 + 8 * nc
     per_row = 4 * depth + 1 + 1 + 4 + 8 * (6 + nc)
     return n * per_rec + rows_written * per_row
+
+
+def views_bytes(n, nm, rows_op, units, P, O):
+    """Algorithmic bytes of chopper_views: per record cls, start', end', gap
+    and its iteration and phase markers read once; per marker its level read
+    and its unit number written; per row of the operation level its three
+    path entries, kind and n / dur / gap / ovl read; the tables, busy times
+    and unit markers written once."""
+    return (n * (1 + 8 + 8 + 8 + 4 + 4) + nm * (1 + 4) + rows_op * (12 + 1 + 32)
+            + units * (8 * (3 * P * 8 + 4 * P * O * 2 + 1) + 4))
 
 
 def measured_traffic(kernel):
@@ -211,6 +223,30 @@ def main():
         },
         "status": status,
     }
+    # the re-keyed views of the same run, timed on their own after the steps
+    iters = tg.CONFIGS[cid]["iters"]
+    P, O = 3, 64
+    views = ch.Views(pipe, n_phases=P, n_ops=O, n_iters=iters,
+                     warmup=10 if iters > 10 else 0)
+    views.run()
+    torch.cuda.synchronize()
+    v0 = torch.cuda.Event(enable_timing=True)
+    v1 = torch.cuda.Event(enable_timing=True)
+    v0.record()
+    for _ in range(K):
+        views.run()
+    v1.record()
+    torch.cuda.synchronize()
+    vms = v0.elapsed_time(v1) / K
+    vb = views_bytes(n, nm, int(lo[min(3, depth - 1) + 1] -
+                                lo[min(3, depth - 1)]), views.U, P, O)
+    out["views"] = {
+        "ms": vms, "units": views.U, "bytes": vb,
+        "achieved": vb / (vms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+        "unit": "GB/s", "frac": vb / (vms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "spec": {"n_phases": P, "n_ops": O, "n_iters": iters,
+                 "warmup": 10 if iters > 10 else 0}}
+    log(f"[bench] views {vms:.3f} ms")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(cid, args.cpu_iters)

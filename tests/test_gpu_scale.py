@@ -41,6 +41,9 @@ def same(a, b, what):
         raise AssertionError(f"{what}: {d.size} differences, first at {d[0]}")
 
 
+ITERS = {3: 800, 4: 2035}     # iterations of the two traces
+
+
 @pytest.mark.parametrize("cid", [3, 4])
 def test_full_size_parity(ch, cid):
     t0 = time.time()
@@ -109,4 +112,25 @@ def test_full_size_parity(ch, cid):
     gotr = got["ratios"]
     ok = (gotr == want) | (np.isnan(gotr) & np.isnan(want))
     assert ok.all(), "ratios"
+    say(f"ratios ok ({time.time() - t0:.0f}s)")
+    # re-keyed views over (iteration, phase, class / operation) and medians
+    # over iterations and GPUs, the first ten iterations as warm-up
+    spec = dict(n_phases=3, n_ops=64, n_iters=ITERS[cid], warmup=10)
+    v = ch.Views(pipe, **spec)
+    v.run()
+    gv = v.results()
+    rv = oracle.views(tr.cls, s, e, idx, ov["gap"], ov["ovl"], tr.m_level,
+                      tr.m_label, **spec)
+    assert gv["n_units"] == rv["n_units"]
+    if cid == 3:      # no marker dropped there
+        assert rv["n_units"] == G * ITERS[cid]
+        assert rv["iter_cnt"] == ITERS[cid] - 10
+    for k in ("unit_marker", "cls_tab", "op_tab", "busy", "iter_max",
+              "cls_cnt", "op_cnt"):
+        same(gv[k], rv[k], f"views {k}")
+    for k in ("cls_med", "op_med"):
+        a, b = gv[k], rv[k]
+        assert ((a == b) | (np.isnan(a) & np.isnan(b))).all(), f"views {k}"
+    assert gv["iter_cnt"] == rv["iter_cnt"]
+    assert gv["iter_med"] == rv["iter_med"]
     say(f"done ({time.time() - t0:.0f}s)")
