@@ -320,11 +320,11 @@ int chopper_window_fractions(int64_t n, const int64_t* win, double* out,
  * its level iter_level marker, to the phase labelled by its level
  * phase_level marker and to the operation labelled by its level op_level
  * marker (no marker: none).  With P = n_phases, O = n_ops, C = unit_cap:
- *   cls_tab [3][C * P * 8]      n, dur, gap summed by (unit, phase label,
- *                               class), index (u * P + p) * 8 + class
- *   op_tab  [4][C * P * O * 2]  n, dur, gap, ovl summed by (unit, phase
- *                               label, operation label, kind), index
- *                               ((u * P + p) * O + o) * 2 + kind
+ *   cls_tab [3][P * 8][C]       n, dur, gap summed by (phase label, class;
+ *                               unit): entry (p * 8 + class) * C + u
+ *   op_tab  [4][P * O * 2][C]   n, dur, gap, ovl summed by (phase label,
+ *                               operation label, kind; unit): entry
+ *                               ((p * O + o) * 2 + kind) * C + u
  *   busy    [C]                 sum of dur + gap of the unit's compute
  *                               records (whatever their phase)
  *   iter_max [n_iters]          the largest busy among the units whose

@@ -739,10 +739,11 @@ void orc_window_fractions(int64_t nw, const int64_t* w, double* out) {
  * in marker input order.  A record belongs to the unit of its level
  * iter_level marker, to the phase labelled by its level phase_level marker
  * and to the operation labelled by its level op_level marker (NONE: none).
- * Tables (sums wrap modulo 2^64 like every other sum here):
- *   cls_tab [3][U * P * 8]     n, dur, gap by (unit, phase label, class)
- *   op_tab  [4][U * P * O * 2] n, dur, gap, ovl by (unit, phase label,
- *                              operation label, kind)
+ * Tables (sums wrap modulo 2^64 like every other sum here), one series over
+ * the units per group:
+ *   cls_tab [3][P * 8][U]      n, dur, gap by (phase label, class; unit)
+ *   op_tab  [4][P * O * 2][U]  n, dur, gap, ovl by (phase label, operation
+ *                              label, kind; unit)
  *   busy    [U]                sum of dur + gap of the unit's compute records
  *   iter_max [NI]              max of busy over the units whose iteration
  *                              label is i, -1 if there is none
@@ -808,14 +809,14 @@ int orc_views(int64_t n, const uint8_t* cls, const int64_t* s,
     if (mp == ORC_NONE || m_label[mp] >= (uint32_t)P) continue;
     const int64_t p = m_label[mp];
     if (cls[r] < 8) {
-      const int64_t k = (u * P + p) * 8 + cls[r];
+      const int64_t k = (p * 8 + cls[r]) * U + u;
       cls_tab[k] += 1;
       cls_tab[nc + k] += (uint64_t)dur;
       cls_tab[2 * nc + k] += (uint64_t)gap[r];
     }
     const uint32_t mo = idx[(int64_t)op_level * n + r];
     if (mo == ORC_NONE || m_label[mo] >= (uint32_t)O) continue;
-    const int64_t k = ((u * P + p) * O + m_label[mo]) * 2 + kd;
+    const int64_t k = ((p * O + m_label[mo]) * 2 + kd) * U + u;
     op_tab[k] += 1;
     op_tab[no + k] += (uint64_t)dur;
     op_tab[2 * no + k] += (uint64_t)gap[r];
@@ -832,7 +833,7 @@ int orc_views(int64_t n, const uint8_t* cls, const int64_t* s,
     for (int st = 0; st < 3; ++st) {
       int64_t m = 0;
       for (int64_t u = 0; u < U; ++u) {
-        const int64_t k = u * P * 8 + g;
+        const int64_t k = g * U + u;
         if (m_label[unit_marker[u]] < warmup || cls_tab[k] == 0) continue;
         const uint64_t d = cls_tab[nc + k], b = cls_tab[2 * nc + k];
         v[m++] = (int64_t)(st == 0 ? d : st == 1 ? b : d + b);
@@ -845,7 +846,7 @@ int orc_views(int64_t n, const uint8_t* cls, const int64_t* s,
     for (int st = 0; st < 3; ++st) {
       int64_t m = 0;
       for (int64_t u = 0; u < U; ++u) {
-        const int64_t k = u * P * O * 2 + g;
+        const int64_t k = g * U + u;
         if (m_label[unit_marker[u]] < warmup || op_tab[k] == 0) continue;
         const uint64_t d = op_tab[no + k], b = op_tab[2 * no + k];
         v[m++] = (int64_t)(st == 0 ? d : st == 1 ? b : d + b);

@@ -28,7 +28,7 @@ constexpr int kViewClasses = 8;
 constexpr int kMaxPhases = 16;
 constexpr int kMaxOps = 128;
 constexpr int kMedThreads = 1024;
-constexpr int kMedIpt = 16;      // items per thread of a group's pass
+constexpr int kMedIpt = 8;       // items per thread held in registers
 constexpr uint64_t kSign = 1ull << 63;
 
 __global__ void k_view_fill(uint64_t* p, int64_t n, uint64_t v) {
@@ -37,54 +37,122 @@ __global__ void k_view_fill(uint64_t* p, int64_t n, uint64_t v) {
     p[i] = v;
 }
 
-__global__ void k_view_zero(uint32_t* p) { *p = 0; }
+constexpr int kRankThreads = 1024;
+constexpr int kRankIpt = 8;
+constexpr int64_t kRankTile = (int64_t)kRankThreads * kRankIpt;
 
-__global__ void k_view_flags(int64_t nm, const uint8_t* level, int iter_level,
-                             uint32_t* flags) {
-  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (m < nm) flags[m] = level[m] == (uint8_t)iter_level ? 1u : 0u;
+// level == iter_level flags of thread t's kRankIpt consecutive markers
+__device__ inline uint32_t unit_bits(const uint8_t* level, int64_t nm,
+                                     int64_t m0, int iter_level) {
+  uint32_t b = 0;
+  if (m0 + kRankIpt <= nm && ((uintptr_t)(level + m0) & 7) == 0) {
+    const uint64_t w = *(const uint64_t*)(level + m0);
+#pragma unroll
+    for (int j = 0; j < kRankIpt; ++j)
+      if (((w >> (8 * j)) & 0xFFu) == (uint64_t)(uint8_t)iter_level)
+        b |= 1u << j;
+  } else {
+#pragma unroll
+    for (int j = 0; j < kRankIpt; ++j)
+      if (m0 + j < nm && level[m0 + j] == (uint8_t)iter_level) b |= 1u << j;
+  }
+  return b;
 }
 
-// unit_marker of every unit that fits and the unit count
-__global__ void k_view_units(int64_t nm, const uint32_t* flags,
-                             const uint32_t* unit_of, const uint32_t* total,
-                             int64_t cap, uint32_t* unit_marker,
-                             int64_t* n_units, uint32_t* status) {
-  const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (m == 0) {
-    *n_units = (int64_t)*total;
-    if ((int64_t)*total > cap) atomicOr(status, CHOPPER_ST_ROWS_OVERFLOW);
+template <typename T>
+__device__ inline T block_sum_1024(T v, T* s_w) {
+  const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
+  v = lane63(wave_incl(v, OpAdd(), (T)0));
+  if (lane == 0) s_w[w] = v;
+  __syncthreads();
+  T s = 0;
+  for (int i = 0; i < kRankThreads / kWave; ++i) s += s_w[i];
+  __syncthreads();
+  return s;
+}
+
+// units per tile of kRankTile markers
+__global__ __launch_bounds__(kRankThreads) void k_view_count(
+    const uint8_t* level, int64_t nm, int iter_level, uint32_t* tilecnt) {
+  __shared__ uint32_t s_w[kRankThreads / kWave];
+  const int64_t m0 = (int64_t)blockIdx.x * kRankTile +
+                     (int64_t)threadIdx.x * kRankIpt;
+  const uint32_t c = (uint32_t)__popc(unit_bits(level, nm, m0, iter_level));
+  const uint32_t tot = block_sum_1024(c, s_w);
+  if (threadIdx.x == 0) tilecnt[blockIdx.x] = tot;
+}
+
+// Unit numbers: block b adds up the counts of the tiles before it itself,
+// then numbers its units in marker order (unit_of is written for the units
+// only); the last block writes the count.
+__global__ __launch_bounds__(kRankThreads) void k_view_rank(
+    const uint8_t* level, int64_t nm, int iter_level, const uint32_t* tilecnt,
+    int64_t cap, uint32_t* unit_of, uint32_t* unit_marker, uint32_t* total,
+    int64_t* n_units, uint32_t* status) {
+  __shared__ uint32_t s_w[kRankThreads / kWave];
+  uint32_t p = 0;
+  for (int64_t i = threadIdx.x; i < (int64_t)blockIdx.x; i += kRankThreads)
+    p += tilecnt[i];
+  const uint32_t before = block_sum_1024(p, s_w);
+  const int64_t m0 = (int64_t)blockIdx.x * kRankTile +
+                     (int64_t)threadIdx.x * kRankIpt;
+  const uint32_t b = unit_bits(level, nm, m0, iter_level);
+  const uint32_t c = (uint32_t)__popc(b);
+  const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
+  const uint32_t incl = wave_incl(c, OpAdd(), 0u);
+  if (lane == kWave - 1) s_w[w] = incl;
+  __syncthreads();
+  uint32_t r = before + incl - c, tot = before;
+  for (int i = 0; i < kRankThreads / kWave; ++i) {
+    if (i < w) r += s_w[i];
+    tot += s_w[i];
   }
-  if (m < nm && flags[m] && (int64_t)unit_of[m] < cap)
-    unit_marker[unit_of[m]] = (uint32_t)m;
+#pragma unroll
+  for (int j = 0; j < kRankIpt; ++j)
+    if ((b >> j) & 1u) {
+      unit_of[m0 + j] = r;
+      if ((int64_t)r < cap) unit_marker[r] = (uint32_t)(m0 + j);
+      ++r;
+    }
+  if (threadIdx.x == 0 && (int64_t)(blockIdx.x + 1) * kRankTile >= nm) {
+    *total = tot;
+    *n_units = (int64_t)tot;
+    if ((int64_t)tot > cap) atomicOr(status, CHOPPER_ST_ROWS_OVERFLOW);
+  }
+}
+
+__global__ void k_view_zero(uint32_t* p, int64_t* n_units) {
+  *p = 0;
+  *n_units = 0;
 }
 
 __device__ inline uint64_t wave_sum(uint64_t v) {
   return lane63(wave_incl(v, OpAdd(), (uint64_t)0));
 }
 
-// Value of a per-lane item array at a lane-varying index (a select chain
-// keeps the array in registers).
-template <typename T>
-__device__ inline T pick(const T (&a)[kTileIpt], int j) {
-  T r = a[0];
-#pragma unroll
-  for (int q = 1; q < kTileIpt; ++q)
-    if (q == j) r = a[q];
-  return r;
-}
-
 // The key of the first pending item of the first lane that has one; every
 // lane then marks its pending items with that key in `hit`.  Returns false
 // when no item is pending.
 __device__ inline bool next_group(uint32_t pend,
-                                  const uint32_t (&key)[kTileIpt],
-                                  uint32_t& k, uint32_t& hit) {
+                                  const uint64_t (&key)[kTileIpt],
+                                  uint64_t& k, uint32_t& hit) {
   const uint64_t act = __ballot(pend != 0u);
   if (act == 0) return false;
   const int leader = __ffsll((long long)act) - 1;
-  const uint32_t mine = pend ? pick(key, __ffs((int)pend) - 1) : 0u;
-  k = (uint32_t)__builtin_amdgcn_readlane((int)mine, leader);
+  // this lane's first pending key (no indexing, so the keys stay in
+  // registers)
+  uint64_t mine = 0;
+  bool found = false;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j)
+    if (!found && ((pend >> j) & 1u)) {
+      mine = key[j];
+      found = true;
+    }
+  k = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)mine,
+                                                    leader) |
+      ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(
+           (int)(uint32_t)(mine >> 32), leader) << 32);
   hit = 0;
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j)
@@ -92,76 +160,118 @@ __device__ inline bool next_group(uint32_t pend,
   return true;
 }
 
+// Unit of an iteration marker m (kNone if m is not one or does not fit).
+__device__ inline uint32_t unit_of_marker(uint32_t m, int64_t nm,
+                                          const uint8_t* level, int iter_level,
+                                          const uint32_t* unit_of,
+                                          int64_t ucap) {
+  if ((int64_t)m >= nm) return kNone;
+  const uint8_t lv = level[m];
+  const uint32_t u = unit_of[m];   // meaningful for iteration markers only
+  return lv == (uint8_t)iter_level && (int64_t)u < ucap ? u : kNone;
+}
+
 // Class view and busy time from the records; one wave per kWaveTile records.
+// Items are grouped by their (iteration marker, phase marker) pair; the unit
+// and the phase label are looked up once per group.
 __global__ __launch_bounds__(kBlock) void k_view_records(
     int64_t n, const uint8_t* cls, const int64_t* start, const int64_t* end,
     const int64_t* gap, const uint32_t* idx_iter, const uint32_t* idx_phase,
-    const uint32_t* unit_of, const uint32_t* label, int64_t nm,
-    const uint32_t* units, int64_t cap, int P, uint64_t* cls_tab,
-    int64_t* busy) {
+    const uint8_t* level, int iter_level, const uint32_t* unit_of,
+    const uint32_t* label, int64_t nm, const uint32_t* units, int64_t cap,
+    int P, uint64_t* cls_tab, int64_t* busy) {
+  __shared__ uint64_t s_acc[kWavesPerBlock][2 * kViewClasses * kWave];
+  __shared__ uint32_t s_cnt[kWavesPerBlock][kViewClasses * kWave];
   const int lane = lane_id();
-  const int64_t w =
-      (int64_t)blockIdx.x * kWavesPerBlock + (int64_t)(threadIdx.x / kWave);
+  const int wv = (int)(threadIdx.x / kWave);
+  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wv;
   const int64_t base = w * kWaveTile;
   if (base >= n) return;
   int64_t ucap = (int64_t)*units;
   ucap = ucap < cap ? ucap : cap;
-  uint32_t ukey[kTileIpt], key[kTileIpt], c[kTileIpt];
-  uint64_t d[kTileIpt], g[kTileIpt];
+  uint64_t ikey[kTileIpt], key[kTileIpt], d[kTileIpt], g[kTileIpt];
+  uint32_t c[kTileIpt];
   uint32_t pb = 0, pc = 0;   // pending items: busy, class view
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j) {
     const int64_t r = base + (int64_t)j * kWave + lane;
     const bool valid = r < n;
     const uint32_t mi = valid ? idx_iter[r] : kNone;
-    uint32_t u = (int64_t)mi < nm ? unit_of[mi] : kNone;
-    if ((int64_t)u >= ucap) u = kNone;
-    const uint32_t mp = u != kNone ? idx_phase[r] : kNone;
-    const uint32_t p = (int64_t)mp < nm ? label[mp] : kNone;
+    const uint32_t mp = valid ? idx_phase[r] : kNone;
     c[j] = valid ? (uint32_t)cls[r] : 255u;
     d[j] = valid ? (uint64_t)(end[r] - start[r]) : 0ull;
     g[j] = valid ? (uint64_t)gap[r] : 0ull;
-    ukey[j] = u;
-    key[j] = (u != kNone && p < (uint32_t)P && c[j] < (uint32_t)kViewClasses)
-                 ? u * (uint32_t)P + p : kNone;
-    if (u != kNone && !kind_of(c[j])) pb |= 1u << j;
-    if (key[j] != kNone) pc |= 1u << j;
+    ikey[j] = mi;
+    key[j] = (uint64_t)mi << 32 | mp;
+    if (mi != kNone && !kind_of(c[j])) pb |= 1u << j;
+    if (mi != kNone && mp != kNone && c[j] < (uint32_t)kViewClasses)
+      pc |= 1u << j;
   }
-  uint32_t k, hit;
-  // busy: compute records by unit
-  while (next_group(pb, ukey, k, hit)) {
+  uint64_t k;
+  uint32_t hit;
+  // busy: compute records by iteration marker
+  while (next_group(pb, ikey, k, hit)) {
+    const uint32_t u = unit_of_marker((uint32_t)k, nm, level, iter_level,
+                                      unit_of, ucap);
     uint64_t x = 0;
 #pragma unroll
     for (int j = 0; j < kTileIpt; ++j)
       if ((hit >> j) & 1u) x += d[j] + g[j];
     x = wave_sum(x);
-    if (lane == 0) atomicAdd((unsigned long long*)&busy[k], x);
+    if (lane == 0 && u != kNone) atomicAdd((unsigned long long*)&busy[u], x);
     pb &= ~hit;
   }
-  // class view by (unit, phase), one class at a time
+  // class view by (iteration marker, phase marker): each lane adds its items
+  // into its own LDS column per class (dur and gap rows, and a count row),
+  // then groups of lanes add the rows up
+  uint64_t* acc = s_acc[wv];
+  uint32_t* cnt = s_cnt[wv];
   const int64_t ncls = cap * P * kViewClasses;
   while (next_group(pc, key, k, hit)) {
-    for (uint32_t cc = 0; cc < (uint32_t)kViewClasses; ++cc) {
-      uint64_t xn = 0, xd = 0, xg = 0;
-#pragma unroll
-      for (int j = 0; j < kTileIpt; ++j)
-        if (((hit >> j) & 1u) && c[j] == cc) {
-          xn += 1;
-          xd += d[j];
-          xg += g[j];
-        }
-      if (__ballot(xn != 0) == 0) continue;
-      xn = wave_sum(xn);
-      xd = wave_sum(xd);
-      xg = wave_sum(xg);
-      const int64_t e = (int64_t)k * kViewClasses + cc;
-      if (lane == 0) {
-        atomicAdd((unsigned long long*)&cls_tab[e], xn);
-        atomicAdd((unsigned long long*)&cls_tab[ncls + e], xd);
-        atomicAdd((unsigned long long*)&cls_tab[2 * ncls + e], xg);
-      }
-    }
+    const uint32_t u = unit_of_marker((uint32_t)(k >> 32), nm, level,
+                                      iter_level, unit_of, ucap);
+    const uint32_t mp = (uint32_t)k;
+    const uint32_t p = (int64_t)mp < nm ? label[mp] : kNone;
     pc &= ~hit;
+    if (u == kNone || p >= (uint32_t)P) continue;
+#pragma unroll
+    for (int r = 0; r < 2 * kViewClasses; ++r) acc[r * kWave + lane] = 0;
+#pragma unroll
+    for (int r = 0; r < kViewClasses; ++r) cnt[r * kWave + lane] = 0;
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j)
+      if ((hit >> j) & 1u) {
+        acc[c[j] * kWave + lane] += d[j];
+        acc[(kViewClasses + c[j]) * kWave + lane] += g[j];
+        cnt[c[j] * kWave + lane] += 1u;
+      }
+    wave_sync();
+    // lanes 4r .. 4r + 3 add up row r of the dur / gap rows, lanes
+    // 8c .. 8c + 7 the count row of class c
+    const int r = lane >> 2, q = lane & 3;
+    uint64_t sv = 0;
+#pragma unroll
+    for (int i = 0; i < kWave / 4; ++i) sv += acc[r * kWave + q * 16 + i];
+    sv += __shfl_xor(sv, 1, kWave);
+    sv += __shfl_xor(sv, 2, kWave);
+    const int cn = lane >> 3, qn = lane & 7;
+    uint32_t sn = 0;
+#pragma unroll
+    for (int i = 0; i < kWave / 8; ++i) sn += cnt[cn * kWave + qn * 8 + i];
+    sn += __shfl_xor(sn, 1, kWave);
+    sn += __shfl_xor(sn, 2, kWave);
+    sn += __shfl_xor(sn, 4, kWave);
+    const int cr = r & (kViewClasses - 1);
+    const uint32_t ncr = (uint32_t)__shfl((int)sn, cr * 8, kWave);
+    const int64_t col = ((int64_t)p * kViewClasses) * cap + u;
+    if (q == 0 && ncr != 0)
+      atomicAdd((unsigned long long*)&cls_tab[(1 + (r >> 3)) * ncls + col +
+                                              (int64_t)cr * cap],
+                sv);
+    if (qn == 0 && sn != 0)
+      atomicAdd((unsigned long long*)&cls_tab[col + (int64_t)cn * cap],
+                (uint64_t)sn);
+    wave_sync();
   }
 }
 
@@ -181,9 +291,9 @@ struct RowCols {
 };
 
 __global__ __launch_bounds__(kBlock) void k_view_rows(
-    RowCols R, int lv_iter, int lv_phase, int lv_op, const uint32_t* unit_of,
-    const uint32_t* label, int64_t nm, const uint32_t* units, int64_t cap,
-    int P, int O, uint64_t* op_tab) {
+    RowCols R, int lv_iter, int lv_phase, int lv_op, const uint8_t* level,
+    const uint32_t* unit_of, const uint32_t* label, int64_t nm,
+    const uint32_t* units, int64_t cap, int P, int O, uint64_t* op_tab) {
   __shared__ uint64_t s_tab[kWavesPerBlock][kMaxOps * 2 * 4];
   const int lane = lane_id();
   const int wv = (int)(threadIdx.x / kWave);
@@ -197,8 +307,8 @@ __global__ __launch_bounds__(kBlock) void k_view_rows(
   ucap = ucap < cap ? ucap : cap;
   uint64_t* tab = s_tab[wv];
   const int ne = O * 2;
-  uint32_t key[kTileIpt], sub[kTileIpt];
-  uint64_t v[kTileIpt][4];
+  uint64_t key[kTileIpt], v[kTileIpt][4];
+  uint32_t sub[kTileIpt];
   uint32_t pend = 0;
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j) {
@@ -209,22 +319,25 @@ __global__ __launch_bounds__(kBlock) void k_view_rows(
     const uint32_t p1 =
         valid ? R.path[(int64_t)lv_phase * R.cap + row] : kNone;
     const uint32_t p3 = valid ? R.path[(int64_t)lv_op * R.cap + row] : kNone;
-    uint32_t u = (int64_t)p0 < nm ? unit_of[p0] : kNone;
-    if ((int64_t)u >= ucap) u = kNone;
-    const uint32_t ph = (int64_t)p1 < nm ? label[p1] : kNone;
     const uint32_t op = (int64_t)p3 < nm ? label[p3] : kNone;
-    key[j] = (u != kNone && ph < (uint32_t)P && op < (uint32_t)O)
-                 ? u * (uint32_t)P + ph : kNone;
-    sub[j] = key[j] != kNone ? op * 2u + (R.kind[row] ? 1u : 0u) : 0u;
-    v[j][0] = key[j] != kNone ? R.n[row] : 0ull;
-    v[j][1] = key[j] != kNone ? (uint64_t)R.dur[row] : 0ull;
-    v[j][2] = key[j] != kNone ? (uint64_t)R.gap[row] : 0ull;
-    v[j][3] = key[j] != kNone ? (uint64_t)R.ovl[row] : 0ull;
-    if (key[j] != kNone) pend |= 1u << j;
+    key[j] = (uint64_t)p0 << 32 | p1;
+    sub[j] = op * 2u + (valid && R.kind[row] ? 1u : 0u);
+    v[j][0] = valid ? R.n[row] : 0ull;
+    v[j][1] = valid ? (uint64_t)R.dur[row] : 0ull;
+    v[j][2] = valid ? (uint64_t)R.gap[row] : 0ull;
+    v[j][3] = valid ? (uint64_t)R.ovl[row] : 0ull;
+    if (p0 != kNone && p1 != kNone && op < (uint32_t)O) pend |= 1u << j;
   }
   const int64_t nop = cap * P * O * 2;
-  uint32_t k, hit;
+  uint64_t k;
+  uint32_t hit;
   while (next_group(pend, key, k, hit)) {
+    pend &= ~hit;
+    const uint32_t u = unit_of_marker((uint32_t)(k >> 32), nm, level,
+                                      lv_iter, unit_of, ucap);
+    const uint32_t mp = (uint32_t)k;
+    const uint32_t ph = (int64_t)mp < nm ? label[mp] : kNone;
+    if (u == kNone || ph >= (uint32_t)P) continue;
     for (int e = lane; e < ne * 4; e += kWave) tab[e] = 0;
     wave_sync();
 #pragma unroll
@@ -235,16 +348,15 @@ __global__ __launch_bounds__(kBlock) void k_view_rows(
           atomicAdd((unsigned long long*)&tab[sub[j] * 4 + f], v[j][f]);
       }
     wave_sync();
-    const int64_t row0 = (int64_t)k * O * 2;
+    const int64_t g0 = (int64_t)ph * O * 2;
     for (int e = lane; e < ne; e += kWave) {
       if (tab[e * 4] == 0) continue;
+      const int64_t at = (g0 + e) * cap + u;
 #pragma unroll
       for (int f = 0; f < 4; ++f)
-        atomicAdd((unsigned long long*)&op_tab[f * nop + row0 + e],
-                  tab[e * 4 + f]);
+        atomicAdd((unsigned long long*)&op_tab[f * nop + at], tab[e * 4 + f]);
     }
     wave_sync();
-    pend &= ~hit;
   }
 }
 
@@ -290,34 +402,12 @@ struct MedSrc {
   int64_t items;
 };
 
-__device__ inline int64_t block_sum_i64(int64_t v, int64_t* s_red) {
-  const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
-  v = (int64_t)wave_sum((uint64_t)v);
-  if (lane == 0) s_red[w] = v;
-  __syncthreads();
-  int64_t t = 0;
-  for (int i = 0; i < kMedThreads / kWave; ++i) t += s_red[i];
-  __syncthreads();
-  return t;
-}
-
-__device__ inline uint64_t block_or_u64(uint64_t v, uint64_t* s_red) {
-  const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
-  v = lane63(wave_incl(v, [](uint64_t a, uint64_t b) { return a | b; },
-                       (uint64_t)0));
-  if (lane == 0) s_red[w] = v;
-  __syncthreads();
-  uint64_t t = 0;
-  for (int i = 0; i < kMedThreads / kWave; ++i) t |= s_red[i];
-  __syncthreads();
-  return t;
-}
-
 __global__ __launch_bounds__(kMedThreads) void k_view_medians(MedArgs A) {
   __shared__ uint32_t s_hist[2][256];
   __shared__ uint64_t s_red[kMedThreads / kWave];
   __shared__ uint64_t s_sel[4];
   const int t = (int)threadIdx.x;
+  const int lane = lane_id(), wv = t / kWave;
   const int64_t gi = blockIdx.x;
   const int64_t ncg = (int64_t)A.P * kViewClasses;
   const int64_t nog = (int64_t)A.P * A.O * 2;
@@ -329,17 +419,17 @@ __global__ __launch_bounds__(kMedThreads) void k_view_medians(MedArgs A) {
   int64_t off, mstride;
   int nstat;
   if (gi < ncg) {
-    const int64_t col = A.cap * ncg;
-    S = MedSrc{A.cls_tab + gi, A.cls_tab + col + gi, A.cls_tab + 2 * col + gi,
-               ncg, U};
+    const int64_t col = A.cap * ncg, at = gi * A.cap;
+    S = MedSrc{A.cls_tab + at, A.cls_tab + col + at, A.cls_tab + 2 * col + at,
+               1, U};
     med = A.cls_med;
     cnt = A.cls_cnt;
     off = gi;
     mstride = ncg;
     nstat = 3;
   } else if (gi < ncg + nog) {
-    const int64_t o = gi - ncg, col = A.cap * nog;
-    S = MedSrc{A.op_tab + o, A.op_tab + col + o, A.op_tab + 2 * col + o, nog,
+    const int64_t o = gi - ncg, col = A.cap * nog, at = o * A.cap;
+    S = MedSrc{A.op_tab + at, A.op_tab + col + at, A.op_tab + 2 * col + at, 1,
                U};
     med = A.op_med;
     cnt = A.op_cnt;
@@ -362,13 +452,15 @@ __global__ __launch_bounds__(kMedThreads) void k_view_medians(MedArgs A) {
     if (!S.n) return i >= (int64_t)A.warmup && (int64_t)S.d[i] >= 0;
     return A.label[A.unit_marker[i]] >= A.warmup && S.n[i * S.stride] != 0;
   };
-  auto value = [&](int64_t i, int st) -> uint64_t {
+  // order-preserving unsigned key of statistic st of item i
+  auto key_of = [&](int64_t i, int st) -> uint64_t {
     const uint64_t d = S.d[i * S.stride];
-    if (st == 0) return d;
+    if (st == 0) return d ^ kSign;
     const uint64_t g = S.g[i * S.stride];
-    return st == 1 ? g : d + g;
+    return (st == 1 ? g : d + g) ^ kSign;
   };
-  // membership of this thread's first kMedIpt items, kept as bits
+  // the first kMedIpt items of each thread are held in registers, items
+  // past kMedIpt * kMedThreads are read again in every pass
   uint32_t mine = 0;
   int64_t m = 0;
 #pragma unroll
@@ -380,81 +472,101 @@ __global__ __launch_bounds__(kMedThreads) void k_view_medians(MedArgs A) {
   for (int64_t i = t + (int64_t)kMedIpt * kMedThreads; i < S.items;
        i += kMedThreads)
     if (member(i)) ++m;
-  m = block_sum_i64(m, (int64_t*)s_red);
+  m = (int64_t)lane63(wave_incl((uint64_t)m, OpAdd(), (uint64_t)0));
+  if (lane == 0) s_red[wv] = (uint64_t)m;
+  __syncthreads();
+  m = 0;
+  for (int i = 0; i < kMedThreads / kWave; ++i) m += (int64_t)s_red[i];
+  __syncthreads();
   if (t == 0) cnt[off] = m;
-  auto is_member = [&](int64_t q, int64_t i) -> bool {
-    return q < kMedIpt ? ((mine >> q) & 1u) != 0 : member(i);
-  };
-  const int64_t nq = (S.items + kMedThreads - 1) / kMedThreads;
   for (int st = 0; st < nstat; ++st) {
     if (m == 0) {
       if (t == 0) med[st * mstride + off] = __builtin_nan("");
       continue;
     }
-    // highest bit in which the members' keys differ from the first one's
-    uint64_t first = 0, diff = 0;
-    bool have = false;
-    for (int64_t q = 0; q < nq; ++q) {
-      const int64_t i = t + q * kMedThreads;
-      if (i < S.items && is_member(q, i)) {
-        first = value(i, st) ^ kSign;
-        have = true;
-        break;
+    uint64_t key[kMedIpt];
+#pragma unroll
+    for (int q = 0; q < kMedIpt; ++q)
+      key[q] = ((mine >> q) & 1u) ? key_of(t + (int64_t)q * kMedThreads, st)
+                                  : 0ull;
+    // fn(key, is_member) for every item slot; whole waves take part
+    auto each = [&](auto&& fn) {
+#pragma unroll
+      for (int q = 0; q < kMedIpt; ++q) fn(key[q], ((mine >> q) & 1u) != 0);
+      for (int64_t i0 = (int64_t)kMedIpt * kMedThreads; i0 < S.items;
+           i0 += kMedThreads) {
+        const int64_t i = i0 + t;
+        const bool ok = member(i);
+        fn(ok ? key_of(i, st) : 0ull, ok);
       }
+    };
+    // smallest and largest key: the bits above the highest one in which
+    // they differ are common to every member
+    uint64_t lo = ~0ull, hi = 0;
+    each([&](uint64_t k, bool ok) {
+      if (!ok) return;
+      lo = k < lo ? k : lo;
+      hi = k > hi ? k : hi;
+    });
+    lo = lane63(wave_incl(
+        lo, [](uint64_t a, uint64_t b) { return a < b ? a : b; },
+        ~(uint64_t)0));
+    hi = lane63(wave_incl(
+        hi, [](uint64_t a, uint64_t b) { return a > b ? a : b; },
+        (uint64_t)0));
+    if (lane == 0) {
+      s_red[wv] = lo;
+      s_hist[0][wv * 2] = (uint32_t)hi;
+      s_hist[0][wv * 2 + 1] = (uint32_t)(hi >> 32);
     }
-    // a common reference: the key of the first member of the lowest thread
-    // that holds one
-    {
-      const uint64_t cand = have ? (uint64_t)t : ~0ull;
-      const int lane = lane_id(), w = t / kWave;
-      uint64_t mn = lane63(wave_incl(
-          cand, [](uint64_t a, uint64_t b) { return a < b ? a : b; },
-          ~(uint64_t)0));
-      if (lane == 0) s_red[w] = mn;
-      __syncthreads();
-      uint64_t best = ~0ull;
-      for (int i = 0; i < kMedThreads / kWave; ++i)
-        best = s_red[i] < best ? s_red[i] : best;
-      __syncthreads();
-      if ((uint64_t)t == best) s_sel[0] = first;
-      __syncthreads();
-      first = s_sel[0];
-      __syncthreads();
+    __syncthreads();
+    lo = ~0ull;
+    hi = 0;
+    for (int i = 0; i < kMedThreads / kWave; ++i) {
+      const uint64_t a = s_red[i];
+      const uint64_t b = (uint64_t)s_hist[0][2 * i] |
+                         ((uint64_t)s_hist[0][2 * i + 1] << 32);
+      lo = a < lo ? a : lo;
+      hi = b > hi ? b : hi;
     }
-    for (int64_t q = 0; q < nq; ++q) {
-      const int64_t i = t + q * kMedThreads;
-      if (i < S.items && is_member(q, i))
-        diff |= (value(i, st) ^ kSign) ^ first;
-    }
-    diff = block_or_u64(diff, s_red);
+    __syncthreads();
     uint64_t res[2];
-    if (diff == 0) {
-      res[0] = res[1] = first;
+    if (lo == hi) {
+      res[0] = res[1] = lo;
     } else {
-      const int top = 63 - __clzll((long long)diff);
+      const int top = 63 - __clzll((long long)(lo ^ hi));
       const int s0 = (top / 8) * 8;
-      // candidates share the bits above s0 + 8 with `first`
       uint64_t pre[2];
       int64_t rank[2] = {(m - 1) / 2, m / 2};
-      pre[0] = pre[1] = s0 + 8 >= 64 ? 0ull : (first >> (s0 + 8)) << (s0 + 8);
+      pre[0] = pre[1] = s0 + 8 >= 64 ? 0ull : (lo >> (s0 + 8)) << (s0 + 8);
       for (int sh = s0; sh >= 0; sh -= 8) {
         for (int b = t; b < 512; b += kMedThreads) (&s_hist[0][0])[b] = 0;
         __syncthreads();
         const int hs = sh + 8;
-        for (int64_t q = 0; q < nq; ++q) {
-          const int64_t i = t + q * kMedThreads;
-          if (!(i < S.items && is_member(q, i))) continue;
-          const uint64_t key = value(i, st) ^ kSign;
-          const uint32_t dig = (uint32_t)(key >> sh) & 255u;
+        each([&](uint64_t k, bool ok) {
+          const uint32_t dig = (uint32_t)(k >> sh) & 255u;
 #pragma unroll
-          for (int r = 0; r < 2; ++r)
-            if (hs >= 64 || (key >> hs) == (pre[r] >> hs))
+          for (int r = 0; r < 2; ++r) {
+            const bool cand = ok && (hs >= 64 || (k >> hs) == (pre[r] >> hs));
+            // one add per wave when its candidates share the digit (the
+            // usual case in the high digits), else one per candidate
+            const uint64_t act = __ballot(cand);
+            if (act == 0) continue;
+            const int ld = __ffsll((long long)act) - 1;
+            const uint32_t d0 =
+                (uint32_t)__builtin_amdgcn_readlane((int)dig, ld);
+            if (__ballot(cand && dig == d0) == act) {
+              if (lane == ld)
+                atomicAdd(&s_hist[r][d0], (uint32_t)__popcll(act));
+            } else if (cand) {
               atomicAdd(&s_hist[r][dig], 1u);
-        }
+            }
+          }
+        });
         __syncthreads();
         if (t < 2 * kWave) {
-          // wave r finds the digit holding rank[r]
-          const int r = t / kWave, lane = lane_id();
+          // wave r finds the digit that holds rank r
+          const int r = t / kWave;
           uint32_t h[4], sum = 0;
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
@@ -462,22 +574,21 @@ __global__ __launch_bounds__(kMedThreads) void k_view_medians(MedArgs A) {
             sum += h[q];
           }
           const uint32_t incl = wave_incl(sum, OpAdd(), 0u);
-          const uint32_t excl = incl - sum;
           const uint64_t past = __ballot((int64_t)incl > rank[r]);
           const int ln = __ffsll((long long)past) - 1;
           if (lane == ln) {
-            int64_t below = excl;
-            int dsel = lane * 4;
+            int64_t below = incl - sum;
+            int dsel = lane * 4 + 3;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              if (below + h[q] > rank[r]) {
+            for (int q = 3; q >= 0; --q)
+              if (below + (int64_t)h[0] + (q > 0 ? h[1] : 0) +
+                      (q > 1 ? h[2] : 0) + (q > 2 ? h[3] : 0) >
+                  rank[r])
                 dsel = lane * 4 + q;
-                break;
-              }
-              below += h[q];
-            }
+            int64_t under = below;
+            for (int q = 0; q < dsel - lane * 4; ++q) under += h[q];
             s_sel[2 * r] = (uint64_t)dsel;
-            s_sel[2 * r + 1] = (uint64_t)below;
+            s_sel[2 * r + 1] = (uint64_t)under;
           }
         }
         __syncthreads();
@@ -492,9 +603,9 @@ __global__ __launch_bounds__(kMedThreads) void k_view_medians(MedArgs A) {
       res[1] = pre[1];
     }
     if (t == 0) {
-      const int64_t lo = (int64_t)(res[0] ^ kSign);
-      const int64_t hi = (int64_t)(res[1] ^ kSign);
-      med[st * mstride + off] = ((double)lo + (double)hi) / 2.0;
+      const int64_t a = (int64_t)(res[0] ^ kSign);
+      const int64_t b = (int64_t)(res[1] ^ kSign);
+      med[st * mstride + off] = ((double)a + (double)b) / 2.0;
     }
   }
 }
@@ -535,37 +646,36 @@ extern "C" int chopper_views(const chopper_records* rec,
       (cap > 0 && (!out->unit_marker || !out->cls_tab || !out->op_tab ||
                    !out->busy)))
     return CHOPPER_EINVAL;
+  const int64_t ntiles = ceil_div(nm, kRankTile);
   Scratch probe(nullptr);
-  auto layout = [&](Scratch& sc, uint32_t*& flags, uint32_t*& unit_of,
-                    uint32_t*& tmp, uint32_t*& total) {
-    flags = sc.take<uint32_t>(nm);
+  auto layout = [&](Scratch& sc, uint32_t*& tilecnt, uint32_t*& unit_of,
+                    uint32_t*& total) {
+    tilecnt = sc.take<uint32_t>(ntiles);
     unit_of = sc.take<uint32_t>(nm);
-    tmp = sc.take<uint32_t>(scan_scratch_elems(nm));
     total = sc.take<uint32_t>(1);
   };
-  uint32_t *flags, *unit_of, *tmp, *total;
-  layout(probe, flags, unit_of, tmp, total);
+  uint32_t *tilecnt, *unit_of, *total;
+  layout(probe, tilecnt, unit_of, total);
   int rc = scratch_check(scratch, scratch_bytes, probe.used);
   if (rc != 0) return rc > 0 ? CHOPPER_OK : rc;
   if (!status) return CHOPPER_EINVAL;
   hipStream_t s = (hipStream_t)stream;
   Scratch sc(scratch);
-  layout(sc, flags, unit_of, tmp, total);
+  layout(sc, tilecnt, unit_of, total);
 
-  // units
+  // units: the iteration markers numbered in marker order
   if (nm > 0) {
-    CHOPPER_HIP(launch("view_flags", k_view_flags, grid_for(nm, kBlock),
-                       dim3(kBlock), s, nm, mk->level, spec->iter_level,
-                       flags));
-    CHOPPER_HIP(exclusive_scan<uint32_t>(flags, unit_of, nm, tmp, total, s));
+    CHOPPER_HIP(launch("view_units", k_view_count, dim3((unsigned)ntiles),
+                       dim3(kRankThreads), s, mk->level, nm, spec->iter_level,
+                       tilecnt));
+    CHOPPER_HIP(launch("view_units", k_view_rank, dim3((unsigned)ntiles),
+                       dim3(kRankThreads), s, mk->level, nm, spec->iter_level,
+                       (const uint32_t*)tilecnt, cap, unit_of,
+                       out->unit_marker, total, out->n_units, status));
   } else {
-    CHOPPER_HIP(launch("view_units", k_view_zero, dim3(1), dim3(1), s, total));
+    CHOPPER_HIP(launch("view_units", k_view_zero, dim3(1), dim3(1), s, total,
+                       out->n_units));
   }
-  CHOPPER_HIP(launch("view_units", k_view_units,
-                     grid_for(nm > 0 ? nm : 1, kBlock), dim3(kBlock), s, nm,
-                     (const uint32_t*)flags, (const uint32_t*)unit_of,
-                     (const uint32_t*)total, cap, out->unit_marker,
-                     out->n_units, status));
   // cleared tables
   const int64_t ncls = cap * P * kViewClasses, nop = cap * P * O * 2;
   auto fill = [&](void* p, int64_t cnt, uint64_t v) -> int {
@@ -587,9 +697,9 @@ extern "C" int chopper_views(const chopper_records* rec,
         dim3((unsigned)ceil_div(n, (int64_t)kWaveTile * kWavesPerBlock)),
         dim3(kBlock), s, n, rec->cls, start_al, end_al, gap,
         idx + (int64_t)spec->iter_level * n,
-        idx + (int64_t)spec->phase_level * n, (const uint32_t*)unit_of,
-        mk->label, nm, (const uint32_t*)total, cap, P, out->cls_tab,
-        out->busy));
+        idx + (int64_t)spec->phase_level * n, mk->level, spec->iter_level,
+        (const uint32_t*)unit_of, mk->label, nm, (const uint32_t*)total, cap,
+        P, out->cls_tab, out->busy));
   }
   // operation view from the rows
   if (rows->cap > 0 && nm > 0 && cap > 0) {
@@ -600,7 +710,7 @@ extern "C" int chopper_views(const chopper_records* rec,
         dim3((unsigned)ceil_div(rows->cap,
                                 (int64_t)kWaveTile * kWavesPerBlock)),
         dim3(kBlock), s, R, spec->iter_level, spec->phase_level,
-        spec->op_level, (const uint32_t*)unit_of, mk->label, nm,
+        spec->op_level, mk->level, (const uint32_t*)unit_of, mk->label, nm,
         (const uint32_t*)total, cap, P, O, out->op_tab));
   }
   if (NI > 0 && cap > 0)

@@ -80,9 +80,11 @@ def test_views_hand_example():
     # class view, phase 0: GEMM (class 0) in units 0, 1, 3 (two kernels,
     # bubble 0), 5; attention in unit 2; RMSNorm in unit 4
     P, C = 1, 8
-    n_tab = v["cls_tab"][0].reshape(6, P, C)
-    d_tab = v["cls_tab"][1].reshape(6, P, C).astype(np.int64)
-    g_tab = v["cls_tab"][2].reshape(6, P, C).astype(np.int64)
+    # tables are [field][group][unit]; viewed here as [unit, phase, class]
+    unit_major = lambda a, *g: np.moveaxis(a.reshape(*g, 6), -1, 0)
+    n_tab = unit_major(v["cls_tab"][0], P, C)
+    d_tab = unit_major(v["cls_tab"][1], P, C).astype(np.int64)
+    g_tab = unit_major(v["cls_tab"][2], P, C).astype(np.int64)
     assert n_tab[:, 0, 0].tolist() == [1, 1, 0, 2, 0, 1]
     assert d_tab[:, 0, 0].tolist() == [20, 10, 0, 30, 0, 10]
     assert n_tab[:, 0, 2].tolist() == [1, 0, 0, 0, 1, 0]
@@ -97,13 +99,13 @@ def test_views_hand_example():
     assert v["cls_med"][2][0] == 35.0
     # operation view: op 5, compute: dur + gap per unit = busy
     O = 8
-    o_n = v["op_tab"][0].reshape(6, P, O, 2)
-    o_d = v["op_tab"][1].reshape(6, P, O, 2).astype(np.int64)
-    o_g = v["op_tab"][2].reshape(6, P, O, 2).astype(np.int64)
+    o_n = unit_major(v["op_tab"][0], P, O, 2)
+    o_d = unit_major(v["op_tab"][1], P, O, 2).astype(np.int64)
+    o_g = unit_major(v["op_tab"][2], P, O, 2).astype(np.int64)
     assert (o_d[:, 0, 5, 0] + o_g[:, 0, 5, 0]).tolist() == v["busy"].tolist()
     assert o_n[:, 0, 5, 1].tolist() == [0, 1, 0, 0, 0, 0]
     # the all_gather [115, 140) overlaps the GEMM [110, 120) for 5 ns
-    assert int(v["op_tab"][3].reshape(6, P, O, 2)[1, 0, 5, 1]) == 5
+    assert int(unit_major(v["op_tab"][3], P, O, 2)[1, 0, 5, 1]) == 5
     g = (0 * O + 5) * 2
     assert v["op_cnt"][g] == 6
     assert v["op_med"][2][g] == 55.0      # {30, 40, 40, 70, 140, 145}
@@ -165,13 +167,14 @@ def test_views_brute_force(seed):
     U = len(units)
     assert v["n_units"] == U and v["unit_marker"].tolist() == units
     ui = {m: u for u, m in enumerate(units)}
-    ct = v["cls_tab"].astype(np.int64).reshape(3, U, P, 8)
+    ct = np.moveaxis(v["cls_tab"].astype(np.int64).reshape(3, P, 8, U), 3, 1)
     got = {}
     for u, p, c in zip(*np.nonzero(ct[0])):
         got[(units[u], int(p), int(c))] = [int(ct[f, u, p, c])
                                            for f in range(3)]
     assert got == cls_d
-    ot = v["op_tab"].astype(np.int64).reshape(4, U, P, O, 2)
+    ot = np.moveaxis(v["op_tab"].astype(np.int64).reshape(4, P, O, 2, U), 4,
+                     1)
     got = {}
     for u, p, o, k in zip(*np.nonzero(ot[0])):
         got[(units[u], int(p), int(o), int(k))] = [int(ot[f, u, p, o, k])
@@ -228,7 +231,8 @@ def test_views_against_rows_config0():
     assert v["busy"].tolist() == b.tolist()
     # operation view: level-3 rows re-keyed by (unit, phase label, operation
     # label, kind) and summed across layers
-    ot = v["op_tab"].astype(np.int64).reshape(4, U, P, O, 2)
+    ot = np.moveaxis(v["op_tab"].astype(np.int64).reshape(4, P, O, 2, U), 4,
+                     1)
     acc = np.zeros_like(ot)
     for i in range(lo[3], lo[4]):
         p0, p1, p3 = (int(rows["path"][l, i]) for l in (0, 1, 3))
@@ -242,7 +246,7 @@ def test_views_against_rows_config0():
             acc[f, ui[p0], ph, op, k] += int(rows[key][i])
     assert np.array_equal(acc, ot)
     # class view summed over classes = level-1 rows (phase) summed over kind
-    ct = v["cls_tab"].astype(np.int64).reshape(3, U, P, 8)
+    ct = np.moveaxis(v["cls_tab"].astype(np.int64).reshape(3, P, 8, U), 3, 1)
     acc = np.zeros((3, U, P), np.int64)
     for i in range(lo[1], lo[2]):
         p0, p1 = int(rows["path"][0, i]), int(rows["path"][1, i])
