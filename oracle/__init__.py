@@ -124,6 +124,8 @@ def _load():
                               i32, i32, i32, i32, ctypes.c_uint32, i64, P, P,
                               P, P, P, P, P, P, P, P, P, P]
     lib.orc_views.restype = ctypes.c_int
+    lib.orc_launch_split.argtypes = [i64, P, P, P, P, P, P, P, P]
+    lib.orc_launch_split.restype = None
     _lib = lib
     return lib
 
@@ -256,6 +258,19 @@ def window_fractions(w: np.ndarray) -> np.ndarray:
     out = np.empty(w.shape, np.float64)
     lib.orc_window_fractions(w.shape[0], _p(w), _p(out))
     return out
+
+
+def launch_split(gpu, stream, cls, s, e, tl):
+    """Preparation and call overhead of every record (V-D eqs. 1-3) from
+    aligned start, end and dispatch times; definitions in oracle.c."""
+    lib = _load()
+    n = int(np.asarray(s).shape[0])
+    a = [_c(gpu, np.uint8), _c(stream, np.uint8), _c(cls, np.uint8),
+         _c(s, np.int64), _c(e, np.int64), _c(tl, np.int64)]
+    prep = np.zeros(n, np.int64)
+    call = np.zeros(n, np.int64)
+    lib.orc_launch_split(n, *[_p(x) for x in a], _p(prep), _p(call))
+    return prep, call
 
 
 def views(cls, s, e, idx, gap, ovl, m_level, m_label, iter_level=0,

@@ -864,3 +864,57 @@ int orc_views(int64_t n, const uint8_t* cls, const int64_t* s,
   free(unit_of);
   return 0;
 }
+
+/* ------------------------------------------------------------------------
+ * Launch overhead split (Section V-D eqs. 1-3).  For a compute record i with
+ * previous compute record p of the same (gpu, stream) in (start', index)
+ * order, with dispatch time tl (aligned):
+ *   O_prep = max(tl - e_p, 0), O_call = min(s_i - tl, s_i - e_p),
+ *   O_launch = O_prep + O_call.
+ * Reading: when the bubble s_i - e_p is not positive (abutting or
+ * overlapping kernels), for the first compute record of a stream and for
+ * communication records both parts are 0; otherwise O_prep is capped at the
+ * bubble and O_call is the rest, which are the equations' values whenever
+ * tl <= s_i.
+ * ------------------------------------------------------------------------ */
+void orc_launch_split(int64_t n, const uint8_t* gpu, const uint8_t* stream,
+                      const uint8_t* cls, const int64_t* s, const int64_t* e,
+                      const int64_t* tl, int64_t* prep, int64_t* call) {
+  uint32_t* ord = (uint32_t*)malloc(sizeof(uint32_t) * (size_t)(n > 0 ? n : 1));
+  orc_order(n, gpu, stream, cls, s, 0, ord);
+  int have = 0;
+  uint32_t cur_g = 0, cur_st = 0;
+  int64_t last_e = 0;
+  for (int64_t q = 0; q < n; ++q) {
+    const uint32_t i = ord[q];
+    if (q == 0 || gpu[i] != cur_g || stream[i] != cur_st) {
+      cur_g = gpu[i];
+      cur_st = stream[i];
+      have = 0;
+    }
+    prep[i] = 0;
+    call[i] = 0;
+    if (kind_of(cls[i])) continue;
+    if (have) {
+      const int64_t ep = last_e;
+      const int64_t bubble = s[i] - ep;
+      if (bubble > 0) {
+        int64_t p = tl[i] - ep;                 /* eq. 1 */
+        if (p < 0) p = 0;
+        int64_t c = s[i] - tl[i];               /* eq. 2 */
+        if (s[i] - ep < c) c = s[i] - ep;
+        /* a dispatch after the start (tl > s_i): the whole bubble is
+           preparation */
+        if (p > bubble) {
+          p = bubble;
+          c = 0;
+        }
+        prep[i] = p;
+        call[i] = c;
+      }
+    }
+    have = 1;
+    last_e = e[i];
+  }
+  free(ord);
+}

@@ -730,3 +730,16 @@ def make_micro(seed: int, n_gpus: int = 2, n_kernels: int = 48,
                  m_label=m_label, a_gpu=np.asarray(a_gpu, np.uint8),
                  a_local=np.asarray(a_local, np.int64),
                  a_ref=np.asarray(a_ref, np.int64), name=f"micro{seed}")
+
+
+def make_launch(tr: Trace, seed: int, max_lead: int,
+                late_frac: float = 0.01) -> np.ndarray:
+    """Host dispatch times of the records of `tr` on each GPU's local clock:
+    start minus a uniform lead in [0, max_lead] ns, a fraction `late_frac`
+    dispatched up to max_lead / 4 ns after the start (clock noise)."""
+    rng = np.random.default_rng(seed)
+    n = tr.n
+    lead = rng.integers(0, max_lead + 1, size=n).astype(np.int64)
+    late = rng.random(n) < late_frac
+    lead[late] = -rng.integers(1, max(2, max_lead // 4), size=int(late.sum()))
+    return tr.start - lead
