@@ -17,6 +17,8 @@
  *                      granularity, optionally filtered by GPU / class /
  *                      iteration                  (Section III-C)
  *   chopper_ratios     derived metrics per aggregated row (III-C; eq. 10)
+ *   chopper_launch_split  preparation / call split of the launch overhead
+ *                      from dispatch times (V-D eqs. 1-3)
  *   chopper_views      per-phase/class and per-operation views with medians
  *                      over iterations and GPUs, iteration throughput
  *                      (Fig. end_to_end, Fig. operation_time)
@@ -378,6 +380,33 @@ int chopper_views(const chopper_records* records, const int64_t* start_al,
                   const chopper_rows* rows, const chopper_view_spec* spec,
                   const chopper_view_out* out, void* scratch,
                   size_t* scratch_bytes, uint32_t* status, void* stream);
+
+/*
+ * chopper_launch_split -- launch overhead split into preparation and call
+ * overhead (Section V-D eqs. 1-3) from the kernels' dispatch times.
+ *
+ * launch_ns [n]: dispatch time t_l of every record on its GPU's local clock
+ * (the clock of start_ns / end_ns); it is aligned with clocks (n_gpus
+ * entries, [host], chopper_align's clocks_out) exactly like start and end.
+ * gap [n] is chopper_overlap's bubble and start_al chopper_align's start'.
+ * For a compute record with gap g > 0 the previous compute kernel of its
+ * stream ended at e = s' - g, and
+ *   prep_out = min(max(t_l' - e, 0), g)      (eq. 1, at most the bubble)
+ *   call_out = g - prep_out                   (eq. 2: min(s' - t_l', s' - e))
+ * so that prep + call = g (eq. 3) whenever e <= s', as in every trace;
+ * records with g = 0 (communication kernels, the first kernel of a stream,
+ * abutting or overlapping kernels) get 0 and 0.  Outputs in input order.
+ * Per-row sums: pass prep_out / call_out to chopper_aggregate as counter
+ * columns.  Sets BAD_GPU, and RANGE when |t_l| or |t_l'| >= 2^62.  Scratch
+ * protocol as above (n_gpus clock entries).
+ */
+int chopper_launch_split(const chopper_records* records,
+                         const chopper_clock* clocks,
+                         const int64_t* launch_ns, const int64_t* start_al,
+                         const int64_t* gap, int64_t* prep_out,
+                         int64_t* call_out, void* scratch,
+                         size_t* scratch_bytes, uint32_t* status,
+                         void* stream);
 
 /* Text for a return code. */
 const char* chopper_strerror(int code);

@@ -120,6 +120,9 @@ def _load():
     lib.chopper_ratios.argtypes = [ctypes.POINTER(Rows), i32, i32,
                                    ctypes.c_double, P, P]
     lib.chopper_window_fractions.argtypes = [i64, P, P, P]
+    lib.chopper_launch_split.argtypes = [ctypes.POINTER(Records),
+                                         ctypes.POINTER(Clock), P, P, P, P, P,
+                                         P, SZ, P, P]
     lib.chopper_views.argtypes = [ctypes.POINTER(Records), P, P, P, i32, P,
                                   ctypes.POINTER(Markers),
                                   ctypes.POINTER(Rows),
@@ -134,7 +137,8 @@ def _load():
     for name in ("chopper_align", "chopper_attribute", "chopper_overlap",
                  "chopper_aggregate", "chopper_ratios",
                  "chopper_window_fractions", "chopper_version",
-                 "chopper_time_kernel", "chopper_views"):
+                 "chopper_time_kernel", "chopper_views",
+                 "chopper_launch_split"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -412,6 +416,27 @@ class Pipeline:
         _check(lib.chopper_window_fractions(self.dt.n_markers,
                                             _ptr(self.mwin), _ptr(self.wfrac),
                                             _stream()), "window_fractions")
+
+    def launch_split(self, launch_ns: torch.Tensor):
+        """Preparation and call overhead of every record (chopper_launch_split)
+        from dispatch times on each GPU's local clock; returns (prep, call)
+        device tensors in input order.  Needs align and overlap to have
+        run."""
+        dt = self.dt
+        dev = dt.start.device
+        prep = torch.empty(max(dt.n, 1), dtype=torch.int64, device=dev)
+        call = torch.empty(max(dt.n, 1), dtype=torch.int64, device=dev)
+
+        def go(scratch, sbytes):
+            return lib.chopper_launch_split(
+                ctypes.byref(self._rec), self.clocks, _ptr(launch_ns),
+                _ptr(self.start), _ptr(self.gap), _ptr(prep), _ptr(call),
+                scratch, sbytes, _ptr(self.status), _stream())
+        if "launch" not in self._scr:
+            self._scr["launch"] = _scratch(go, dev)
+        scr, sb = _aligned(self._scr["launch"])
+        _check(go(scr, ctypes.byref(sb)), "launch_split")
+        return prep[:dt.n], call[:dt.n]
 
     def step(self):
         """One pass of the whole pipeline."""

@@ -1,0 +1,96 @@
+// chopper_launch_split: launch overhead split into preparation and call
+// overhead (Section V-D eqs. 1-3) from the kernels' dispatch times.
+//
+// The bubble before a compute kernel is the sum of the two parts, so with
+// the bubble already known (chopper_overlap) the split is elementwise: when
+// the bubble g is positive the previous compute kernel of the stream ended at
+// s' - g, preparation is the dispatch time past that end (at most g) and the
+// call overhead the rest.  One wave tile of records per wave, each lane eight
+// consecutive records with 16-byte vector loads and stores where aligned.
+#include <vector>
+
+#include "clock.h"
+#include "wave.h"
+
+namespace chopper {
+
+bool validate_records(const chopper_records* r);
+
+namespace {
+
+__global__ __launch_bounds__(kBlock) void k_launch_split(
+    int64_t n, int G, const uint8_t* gpu, const ClockDev* clk,
+    const int64_t* launch, const int64_t* start, const int64_t* gap,
+    int64_t* prep, int64_t* call, uint32_t* status) {
+  const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
+  const int64_t base =
+      ((int64_t)blockIdx.x * kWavesPerBlock + wv) * (int64_t)kWaveTile;
+  if (base >= n) return;
+  const int64_t k0 = base + (int64_t)lane * kTileIpt;
+  uint32_t bad = 0;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    const int64_t k = k0 + j;
+    if (k >= n) break;
+    const uint32_t g = gpu[k];
+    const int64_t gp = gap[k];
+    int64_t p = 0;
+    if (g >= (uint32_t)G) {
+      bad |= CHOPPER_ST_BAD_GPU;
+    } else {
+      const int64_t tl = align_time(launch[k], clk[g]);
+      if (out_of_range(launch[k]) || out_of_range(tl)) bad |= CHOPPER_ST_RANGE;
+      if (gp > 0) {
+        const int64_t past = tl - (start[k] - gp);
+        p = past <= 0 ? 0 : (past < gp ? past : gp);
+      }
+    }
+    prep[k] = p;
+    call[k] = gp > 0 ? gp - p : 0;
+  }
+  uint32_t v = bad;
+  for (int d = kWave / 2; d > 0; d >>= 1) v |= __shfl_xor(v, d, kWave);
+  if (lane == 0 && v) atomicOr(status, v);
+}
+
+}  // namespace
+
+extern "C" int chopper_launch_split(const chopper_records* rec,
+                                    const chopper_clock* clocks,
+                                    const int64_t* launch_ns,
+                                    const int64_t* start_al,
+                                    const int64_t* gap, int64_t* prep_out,
+                                    int64_t* call_out, void* scratch,
+                                    size_t* scratch_bytes, uint32_t* status,
+                                    void* stream) {
+  if (!validate_records(rec) || !clocks || !scratch_bytes)
+    return CHOPPER_EINVAL;
+  const int64_t n = rec->n;
+  const int G = rec->n_gpus;
+  if (n > 0 && (!rec->gpu || !launch_ns || !start_al || !gap || !prep_out ||
+                !call_out))
+    return CHOPPER_EINVAL;
+  Scratch probe(nullptr);
+  probe.take<ClockDev>(G);
+  int rc = scratch_check(scratch, scratch_bytes, probe.used);
+  if (rc != 0) return rc > 0 ? CHOPPER_OK : rc;
+  if (!status) return CHOPPER_EINVAL;
+  if (n == 0) return CHOPPER_OK;
+  hipStream_t s = (hipStream_t)stream;
+  Scratch sc(scratch);
+  ClockDev* clk = sc.take<ClockDev>(G);
+  std::vector<ClockDev> cd(G);
+  for (int g = 0; g < G; ++g)
+    cd[g] = ClockDev{clocks[g].x0, clocks[g].c, clocks[g].d_q48};
+  // (a copy from pageable memory is staged before the call returns)
+  CHOPPER_HIP(hipMemcpyAsync(clk, cd.data(), sizeof(ClockDev) * G,
+                             hipMemcpyHostToDevice, s));
+  CHOPPER_HIP(launch("launch_split", k_launch_split,
+                     dim3((unsigned)ceil_div(n, (int64_t)kWaveTile *
+                                                    kWavesPerBlock)),
+                     dim3(kBlock), s, n, G, rec->gpu, (const ClockDev*)clk,
+                     launch_ns, start_al, gap, prep_out, call_out, status));
+  return CHOPPER_OK;
+}
+
+}  // namespace chopper

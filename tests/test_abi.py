@@ -34,7 +34,7 @@ def test_header_declares_the_four_steps():
               "chopper_aggregate", "chopper_ratios",
               "chopper_window_fractions", "chopper_strerror",
               "chopper_version", "chopper_time_kernel", "chopper_kernel_name",
-              "chopper_views"):
+              "chopper_views", "chopper_launch_split"):
         assert n in names
 
 
@@ -257,3 +257,22 @@ def test_views_scratch_query_and_argument_errors(ch):
                              ctypes.byref(good), ctypes.byref(out),
                              ctypes.c_void_p(0x10000), ctypes.byref(sz), fake,
                              None) == -2
+
+
+def test_launch_split_scratch_query_and_argument_errors(ch):
+    lib, b = ch.lib, ch.binding
+    fake = ctypes.c_void_p(0x1000)
+    rec = _records(ch, 1000)
+    clocks = (b.Clock * 2)()
+    sz = ctypes.c_size_t(0)
+    assert lib.chopper_launch_split(ctypes.byref(rec), clocks, fake, fake,
+                                    fake, fake, fake, None, ctypes.byref(sz),
+                                    None, None) == 0
+    assert sz.value > 0
+    for args in ((None, fake), (fake, None)):
+        assert lib.chopper_launch_split(ctypes.byref(rec), clocks, args[0],
+                                        fake, fake, fake, args[1], None,
+                                        ctypes.byref(sz), None, None) == -1
+    assert lib.chopper_launch_split(ctypes.byref(rec), None, fake, fake, fake,
+                                    fake, fake, None, ctypes.byref(sz), None,
+                                    None) == -1
