@@ -5,7 +5,9 @@ chopper_aggregate(all levels) + derived ratios over the whole synthetic trace
 of 8 GPUs x 800 iterations x 32 layers with 16 counters per record (the
 Llama-3-8B FSDP trace shape), inputs resident in HBM.  After the timed steps
 chopper_views (per-phase/class and per-operation views with their medians)
-is timed on its own over the same run ("views").  Prints one JSON line.
+and chopper_launch_split (preparation / call overhead from seeded dispatch
+times) are timed on their own over the same run ("views", "launch_split").
+Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--config 3]
 """
@@ -152,6 +154,8 @@ def main():
     g = tr.gpu.astype(np.int64)
     input_order = bool(np.all(np.diff(g) >= 0) and np.all(
         (np.diff(g) != 0) | (np.diff(tr.start) >= 0)))
+    # seeded dispatch times (local clocks) for the launch-overhead split
+    launch_host = tg.make_launch(tr, 11, max_lead=20000)
     del tr, g
     torch.cuda.synchronize()
     pipe = ch.Pipeline(dt)
@@ -247,6 +251,22 @@ def main():
         "spec": {"n_phases": P, "n_ops": O, "n_iters": iters,
                  "warmup": 10 if iters > 10 else 0}}
     log(f"[bench] views {vms:.3f} ms")
+    # the launch-overhead split from seeded dispatch times, timed on its own
+    tl = torch.from_numpy(launch_host).to(dev)
+    pipe.launch_split(tl)
+    torch.cuda.synchronize()
+    v0.record()
+    for _ in range(K):
+        pipe.launch_split(tl)
+    v1.record()
+    torch.cuda.synchronize()
+    lms = v0.elapsed_time(v1) / K
+    lb = n * (1 + 8 + 8 + 8 + 8 + 8)
+    out["launch_split"] = {
+        "ms": lms, "bytes": lb, "achieved": lb / (lms * 1e-3) / 1e9,
+        "peak": HBM_PEAK_GBS, "unit": "GB/s",
+        "frac": lb / (lms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    log(f"[bench] launch split {lms:.3f} ms")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(cid, args.cpu_iters)

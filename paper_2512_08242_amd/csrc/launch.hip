@@ -5,8 +5,9 @@
 // the bubble already known (chopper_overlap) the split is elementwise: when
 // the bubble g is positive the previous compute kernel of the stream ended at
 // s' - g, preparation is the dispatch time past that end (at most g) and the
-// call overhead the rest.  One wave tile of records per wave, each lane eight
-// consecutive records with 16-byte vector loads and stores where aligned.
+// call overhead the rest.  One wave tile of records per wave, loads striped
+// across the lanes and all issued before any use; the clock table sits in
+// LDS.
 #include <vector>
 
 #include "clock.h"
@@ -18,35 +19,49 @@ bool validate_records(const chopper_records* r);
 
 namespace {
 
+constexpr int kMaxGpus = 256;
+
 __global__ __launch_bounds__(kBlock) void k_launch_split(
     int64_t n, int G, const uint8_t* gpu, const ClockDev* clk,
     const int64_t* launch, const int64_t* start, const int64_t* gap,
     int64_t* prep, int64_t* call, uint32_t* status) {
+  __shared__ ClockDev s_clk[kMaxGpus];
+  for (int g = (int)threadIdx.x; g < G; g += kBlock) s_clk[g] = clk[g];
+  __syncthreads();
   const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
   const int64_t base =
       ((int64_t)blockIdx.x * kWavesPerBlock + wv) * (int64_t)kWaveTile;
   if (base >= n) return;
-  const int64_t k0 = base + (int64_t)lane * kTileIpt;
+  // striped items (j * 64 + lane): every load of the tile in flight at once
+  uint32_t g[kTileIpt];
+  int64_t tl[kTileIpt], s[kTileIpt], gp[kTileIpt];
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    const int64_t k = base + (int64_t)j * kWave + lane;
+    const bool v = k < n;
+    g[j] = v ? gpu[k] : 0u;
+    tl[j] = v ? launch[k] : 0;
+    s[j] = v ? start[k] : 0;
+    gp[j] = v ? gap[k] : 0;
+  }
   uint32_t bad = 0;
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j) {
-    const int64_t k = k0 + j;
-    if (k >= n) break;
-    const uint32_t g = gpu[k];
-    const int64_t gp = gap[k];
+    const int64_t k = base + (int64_t)j * kWave + lane;
+    if (k >= n) continue;
     int64_t p = 0;
-    if (g >= (uint32_t)G) {
+    if (g[j] >= (uint32_t)G) {
       bad |= CHOPPER_ST_BAD_GPU;
     } else {
-      const int64_t tl = align_time(launch[k], clk[g]);
-      if (out_of_range(launch[k]) || out_of_range(tl)) bad |= CHOPPER_ST_RANGE;
-      if (gp > 0) {
-        const int64_t past = tl - (start[k] - gp);
-        p = past <= 0 ? 0 : (past < gp ? past : gp);
+      const int64_t t2 = align_time(tl[j], s_clk[g[j]]);
+      if (out_of_range(tl[j]) || out_of_range(t2)) bad |= CHOPPER_ST_RANGE;
+      if (gp[j] > 0) {
+        const int64_t past = t2 - (s[j] - gp[j]);
+        p = past <= 0 ? 0 : (past < gp[j] ? past : gp[j]);
       }
     }
     prep[k] = p;
-    call[k] = gp > 0 ? gp - p : 0;
+    call[k] = gp[j] > 0 ? gp[j] - p : 0;
   }
   uint32_t v = bad;
   for (int d = kWave / 2; d > 0; d >>= 1) v |= __shfl_xor(v, d, kWave);

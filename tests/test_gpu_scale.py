@@ -133,4 +133,13 @@ def test_full_size_parity(ch, cid):
         assert ((a == b) | (np.isnan(a) & np.isnan(b))).all(), f"views {k}"
     assert gv["iter_cnt"] == rv["iter_cnt"]
     assert gv["iter_med"] == rv["iter_med"]
+    say(f"views ok ({time.time() - t0:.0f}s)")
+    # launch overhead split from seeded dispatch times
+    import torch
+    tl = tg.make_launch(tr, 11, max_lead=20000)
+    prep, call = pipe.launch_split(torch.from_numpy(tl).cuda())
+    tla, _ = oracle.transform(tr.gpu, tl, G, x0, c, d)
+    rp, rc2 = oracle.launch_split(tr.gpu, tr.stream, tr.cls, s, e, tla)
+    same(prep.cpu().numpy(), rp, "prep")
+    same(call.cpu().numpy(), rc2, "call")
     say(f"done ({time.time() - t0:.0f}s)")
