@@ -126,6 +126,9 @@ def _load():
     lib.orc_views.restype = ctypes.c_int
     lib.orc_launch_split.argtypes = [i64, P, P, P, P, P, P, P, P]
     lib.orc_launch_split.restype = None
+    lib.orc_join.argtypes = [i64, P, P, P, P, P, i32, P, P, P, P, P, P, P, P,
+                             P, P]
+    lib.orc_join.restype = ctypes.c_uint32
     _lib = lib
     return lib
 
@@ -258,6 +261,43 @@ def window_fractions(w: np.ndarray) -> np.ndarray:
     out = np.empty(w.shape, np.float64)
     lib.orc_window_fractions(w.shape[0], _p(w), _p(out))
     return out
+
+
+JOIN_MISS, JOIN_ORDER = 256, 512
+
+
+def join(gpu, stream, cls, s, lab, passes):
+    """Counter-pass join (III-A, III-B): counters [16][n] u64 and the matched
+    pass bits [n] of every record, and the status; definitions in
+    oracle.c.  passes: dicts with gpu, stream, cls, lab ([m] each), values
+    ([c][m] u64) and dst (c destination columns)."""
+    lib = _load()
+    n = int(np.asarray(s).shape[0])
+    P_ = len(passes)
+    keep = []
+    arr = lambda vals, dt: (ctypes.c_void_p * max(P_, 1))(*[
+        _p(v) for v in vals])
+    g = [_c(q["gpu"], np.uint8) for q in passes]
+    st = [_c(q["stream"], np.uint8) for q in passes]
+    cl = [_c(q["cls"], np.uint8) for q in passes]
+    lb = [_c(q["lab"], np.uint32) for q in passes]
+    vl = [_c(q["values"], np.uint64) for q in passes]
+    keep += [g, st, cl, lb, vl]
+    pn = np.array([int(np.asarray(q["gpu"]).shape[0]) for q in passes] or [0],
+                  np.int64)
+    pc = np.array([len(q["dst"]) for q in passes] or [0], np.int32)
+    pd = np.zeros(16 * max(P_, 1), np.int32)
+    for i, q in enumerate(passes):
+        pd[16 * i:16 * i + len(q["dst"])] = q["dst"]
+    counters = np.zeros((16, n), np.uint64)
+    matched = np.zeros(n, np.uint8)
+    a = [_c(gpu, np.uint8), _c(stream, np.uint8), _c(cls, np.uint8),
+         _c(s, np.int64), _c(lab, np.uint32)]
+    st_ = lib.orc_join(n, *[_p(x) for x in a], P_, _p(pn), _p(pc), _p(pd),
+                       arr(g, None), arr(st, None), arr(cl, None),
+                       arr(lb, None), arr(vl, None), _p(counters),
+                       _p(matched))
+    return counters, matched, int(st_)
 
 
 def launch_split(gpu, stream, cls, s, e, tl):

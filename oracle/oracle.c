@@ -918,3 +918,144 @@ void orc_launch_split(int64_t n, const uint8_t* gpu, const uint8_t* stream,
   }
   free(ord);
 }
+
+/* ------------------------------------------------------------------------
+ * Counter-pass join (Section III-A hardware profiling: counters come from
+ * serialized passes of two or three counters each, without valid
+ * timestamps; Section III-B: alignment attaches them to the runtime trace's
+ * kernels).
+ *
+ * A runtime record's key is (gpu, stream, iteration label, ordinal), the
+ * ordinal being the number of records with the same (gpu, stream, label)
+ * and a smaller (start', index); a pass entry's key is (gpu, stream, label,
+ * ordinal), the ordinal counting earlier entries of the pass with the same
+ * (gpu, stream, label).  Record and entry match when the keys are equal and
+ * their classes agree; then each of the pass's value columns goes to its
+ * destination counter column of the record and bit p of matched is set.
+ * Columns no matched entry fills are 0.  Records and entries without an
+ * iteration (label NONE) are never matched.  JOIN_MISS: some record with an
+ * iteration found no matching entry in some pass.  JOIN_ORDER: along
+ * (gpu, stream) in (start', index) order, or along a pass's own order, an
+ * iteration label is smaller than an earlier one (NONE labels aside; the
+ * library then leaves the result unspecified).
+ * ------------------------------------------------------------------------ */
+#define ORC_JOIN_MISS 256u
+#define ORC_JOIN_ORDER 512u
+
+typedef struct {
+  uint32_t g, st, lab;
+  int64_t t;      /* start' (records) or position (entries) */
+  uint32_t k;     /* index */
+  uint32_t ord;
+} jrow_t;
+
+static int cmp_jrow_time(const void* x, const void* y) {
+  const jrow_t* a = (const jrow_t*)x;
+  const jrow_t* b = (const jrow_t*)y;
+  if (a->g != b->g) return a->g < b->g ? -1 : 1;
+  if (a->st != b->st) return a->st < b->st ? -1 : 1;
+  if (a->t != b->t) return a->t < b->t ? -1 : 1;
+  return a->k < b->k ? -1 : a->k > b->k;
+}
+
+static int cmp_jrow_key(const void* x, const void* y) {
+  const jrow_t* a = (const jrow_t*)x;
+  const jrow_t* b = (const jrow_t*)y;
+  if (a->g != b->g) return a->g < b->g ? -1 : 1;
+  if (a->st != b->st) return a->st < b->st ? -1 : 1;
+  if (a->lab != b->lab) return a->lab < b->lab ? -1 : 1;
+  if (a->ord != b->ord) return a->ord < b->ord ? -1 : 1;
+  return a->k < b->k ? -1 : a->k > b->k;
+}
+
+/* ordinals: sort by (g, st, t, k), check the labels, then count within
+   each (g, st, lab) */
+static uint32_t join_ordinals(jrow_t* v, int64_t n) {
+  uint32_t st = 0;
+  qsort(v, (size_t)n, sizeof(jrow_t), cmp_jrow_time);
+  {
+    uint32_t last = ORC_NONE;   /* last label of the current (g, st) */
+    for (int64_t i = 0; i < n; ++i) {
+      if (i == 0 || v[i].g != v[i - 1].g || v[i].st != v[i - 1].st)
+        last = ORC_NONE;
+      if (v[i].lab == ORC_NONE) continue;
+      if (last != ORC_NONE && v[i].lab < last) st |= ORC_JOIN_ORDER;
+      last = v[i].lab;
+    }
+  }
+  /* counts per (g, st, lab) in time order, whatever the label order */
+  for (int64_t i = 0; i < n; ++i) v[i].ord = 0;
+  {
+    /* group equal (g, st, lab) keeping time order: a stable pass over a
+       copy sorted by (g, st, lab, t, k) */
+    jrow_t* w = (jrow_t*)malloc(sizeof(jrow_t) * (size_t)(n > 0 ? n : 1));
+    memcpy(w, v, sizeof(jrow_t) * (size_t)n);
+    for (int64_t i = 0; i < n; ++i) w[i].ord = (uint32_t)i; /* time rank */
+    qsort(w, (size_t)n, sizeof(jrow_t), cmp_jrow_key);
+    /* cmp_jrow_key orders by ord = time rank inside equal (g, st, lab) */
+    uint32_t c = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      if (i > 0 && (w[i].g != w[i - 1].g || w[i].st != w[i - 1].st ||
+                    w[i].lab != w[i - 1].lab))
+        c = 0;
+      v[w[i].ord].ord = c++;
+    }
+    free(w);
+  }
+  return st;
+}
+
+uint32_t orc_join(int64_t n, const uint8_t* gpu, const uint8_t* stream,
+                  const uint8_t* cls, const int64_t* s, const uint32_t* lab,
+                  int32_t n_passes, const int64_t* pn, const int32_t* pcols,
+                  const int32_t* pdst, const uint8_t* const* pgpu,
+                  const uint8_t* const* pstream, const uint8_t* const* pcls,
+                  const uint32_t* const* plab,
+                  const uint64_t* const* pval, uint64_t* counters,
+                  uint8_t* matched) {
+  uint32_t status = 0;
+  memset(counters, 0, sizeof(uint64_t) * 16 * (size_t)n);
+  memset(matched, 0, (size_t)n);
+  jrow_t* R = (jrow_t*)malloc(sizeof(jrow_t) * (size_t)(n > 0 ? n : 1));
+  for (int64_t i = 0; i < n; ++i)
+    R[i] = (jrow_t){gpu[i], stream[i], lab[i], s[i], (uint32_t)i, 0};
+  status |= join_ordinals(R, n);
+  qsort(R, (size_t)n, sizeof(jrow_t), cmp_jrow_key);
+  for (int p = 0; p < n_passes; ++p) {
+    const int64_t m = pn[p];
+    jrow_t* Q = (jrow_t*)malloc(sizeof(jrow_t) * (size_t)(m > 0 ? m : 1));
+    for (int64_t i = 0; i < m; ++i)
+      Q[i] = (jrow_t){pgpu[p][i], pstream[p][i], plab[p][i], i, (uint32_t)i,
+                      0};
+    status |= join_ordinals(Q, m);
+    qsort(Q, (size_t)m, sizeof(jrow_t), cmp_jrow_key);
+    /* merge the two key-sorted lists */
+    int64_t j = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      const jrow_t* a = &R[i];
+      if (a->lab == ORC_NONE) continue;
+      while (j < m) {
+        const jrow_t* b = &Q[j];
+        if (b->g != a->g ? b->g < a->g
+            : b->st != a->st ? b->st < a->st
+            : b->lab != a->lab ? b->lab < a->lab : b->ord < a->ord)
+          ++j;
+        else
+          break;
+      }
+      int hit = 0;
+      if (j < m && Q[j].g == a->g && Q[j].st == a->st && Q[j].lab == a->lab &&
+          Q[j].ord == a->ord && pcls[p][Q[j].k] == cls[a->k]) {
+        hit = 1;
+        for (int c = 0; c < pcols[p]; ++c)
+          counters[(int64_t)pdst[16 * p + c] * n + a->k] =
+              pval[p][(int64_t)c * m + Q[j].k];
+        matched[a->k] |= (uint8_t)(1u << p);
+      }
+      if (!hit) status |= ORC_JOIN_MISS;
+    }
+    free(Q);
+  }
+  free(R);
+  return status;
+}

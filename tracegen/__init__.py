@@ -26,7 +26,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
-from typing import Dict, Optional
+from typing import Dict, List, Optional
 
 import numpy as np
 
@@ -743,3 +743,48 @@ def make_launch(tr: Trace, seed: int, max_lead: int,
     late = rng.random(n) < late_frac
     lead[late] = -rng.integers(1, max(2, max_lead // 4), size=int(late.sum()))
     return tr.start - lead
+
+
+def make_counter_passes(tr: Trace, rec_label: np.ndarray, seed: int,
+                        cols=(3, 3, 2, 2, 2, 2, 2), drop_frac: float = 0.0,
+                        mismatch_frac: float = 0.0,
+                        extra: int = 0) -> List[dict]:
+    """Serialized hardware-counter passes of the records of `tr` (paper
+    III-A: two or three counters per pass, no valid timestamps): pass p
+    lists every record once, grouped by GPU in dispatch (local start) order,
+    with its iteration label rec_label[k] and the values of the counter
+    columns it covers.  Perturbations: a fraction of entries dropped, a
+    fraction given another class, `extra` entries per GPU appended with an
+    iteration label past the last one."""
+    rng = np.random.default_rng(seed)
+    assert tr.counters is not None and sum(cols) <= tr.counters.shape[0]
+    order = np.lexsort((np.arange(tr.n), tr.start, tr.gpu.astype(np.int64)))
+    passes, c0 = [], 0
+    for p, nc in enumerate(cols):
+        k = order.copy()
+        if drop_frac > 0:
+            k = k[rng.random(k.shape[0]) >= drop_frac]
+        cls = tr.cls[k].copy()
+        if mismatch_frac > 0:
+            flip = rng.random(k.shape[0]) < mismatch_frac
+            cls[flip] = (cls[flip] + 1) % 8
+        gpu, stream = tr.gpu[k].copy(), tr.stream[k].copy()
+        lab = np.asarray(rec_label, np.uint32)[k].copy()
+        vals = tr.counters[c0:c0 + nc][:, k].copy()
+        if extra:
+            pos = np.searchsorted(gpu, np.arange(tr.n_gpus), side="right")
+            ins_g = np.repeat(np.arange(tr.n_gpus), extra)
+            at = np.repeat(pos, extra)
+            gpu = np.insert(gpu, at, ins_g.astype(np.uint8))
+            stream = np.insert(stream, at, np.zeros(at.shape, np.uint8))
+            cls = np.insert(cls, at, np.zeros(at.shape, np.uint8))
+            top = np.uint32(lab[lab != 0xFFFFFFFF].max() + 1 if
+                            (lab != 0xFFFFFFFF).any() else 0)
+            lab = np.insert(lab, at, np.full(at.shape, top, np.uint32))
+            vals = np.insert(vals, at, np.zeros((nc, at.shape[0]), np.uint64),
+                             axis=1)
+        passes.append(dict(gpu=gpu, stream=stream, cls=cls, lab=lab,
+                           values=np.ascontiguousarray(vals, np.uint64),
+                           dst=list(range(c0, c0 + nc))))
+        c0 += nc
+    return passes
