@@ -17,6 +17,8 @@
  *                      granularity, optionally filtered by GPU / class /
  *                      iteration                  (Section III-C)
  *   chopper_ratios     derived metrics per aggregated row (III-C; eq. 10)
+ *   chopper_join_counters  counters of serialized profiling passes matched
+ *                      to the runtime kernels (III-A, III-B)
  *   chopper_launch_split  preparation / call split of the launch overhead
  *                      from dispatch times (V-D eqs. 1-3)
  *   chopper_views      per-phase/class and per-operation views with medians
@@ -84,9 +86,14 @@ enum {
   CHOPPER_ST_ROWS_OVERFLOW = 32u,  /* aggregate rows exceed rows->cap; the
                                       level offsets hold the needed counts  */
   CHOPPER_ST_BAD_LEVEL = 64u,      /* marker level >= depth                 */
-  CHOPPER_ST_PATH_CONFLICT = 128u  /* records sharing a deepest marker have
+  CHOPPER_ST_PATH_CONFLICT = 128u, /* records sharing a deepest marker have
                                       different marker paths (markers not
                                       nested); aggregate rows unspecified   */
+  CHOPPER_ST_JOIN_MISS = 256u,     /* a record with an iteration found no
+                                      entry of some counter pass           */
+  CHOPPER_ST_JOIN_ORDER = 512u     /* iteration labels not increasing run by
+                                      run along a (gpu, stream): the join
+                                      is unspecified                       */
 };
 
 /* aggregation levels besides the marker levels 0 .. depth-1 */
@@ -407,6 +414,52 @@ int chopper_launch_split(const chopper_records* records,
                          int64_t* call_out, void* scratch,
                          size_t* scratch_bytes, uint32_t* status,
                          void* stream);
+
+/*
+ * chopper_join_counters -- counters of serialized hardware-profiling passes
+ * attached to the runtime trace's kernels (Section III-A: two or three
+ * counters per pass, kernels serialized, no valid timestamps; Section III-B:
+ * alignment attaches counters to operations, layers and iterations).
+ *
+ * A pass ([host] struct, device arrays) lists kernels in its own order with
+ * gpu, stream, class and iteration label (NONE: none) and n_cols value
+ * columns ([n_cols][n], u64) that go to counter columns dst[0 .. n_cols-1]
+ * (each destination used by at most one pass).  A record's key is
+ * (gpu, stream, label, ordinal): label = label of its level iter_level
+ * marker (idx from chopper_attribute), ordinal = number of records with the
+ * same (gpu, stream, label) before it in (start', index) order (`order` from
+ * chopper_align); an entry's ordinal counts earlier entries of its pass with
+ * the same (gpu, stream, label).  Equal keys and equal classes match:
+ * counters_out [16][n] gets the entry's values in the pass's columns (0 when
+ * nothing matches, and in columns no pass fills), bit p of matched_out [n]
+ * is set for pass p.  Records and entries without an iteration never match.
+ * JOIN_MISS: a record with an iteration found no entry in some pass.
+ * JOIN_ORDER (result unspecified): along a (gpu, stream), in either order,
+ * a label's kernels are not consecutive apart from kernels without an
+ * iteration, or labels do not increase from one label to the next.
+ * n_passes <= 8, at most 256 (gpu, stream) pairs per pass.
+ */
+typedef struct {
+  int64_t n;
+  int32_t n_cols;
+  int32_t reserved;
+  const uint8_t* gpu;
+  const uint8_t* stream;
+  const uint8_t* cls;
+  const uint32_t* label;
+  const uint64_t* values;
+  int32_t dst[16];
+} chopper_counter_pass;
+
+int chopper_join_counters(const chopper_records* records,
+                          const int64_t* start_al, const uint32_t* order,
+                          const uint32_t* idx, int32_t depth,
+                          int32_t iter_level, const chopper_markers* markers,
+                          const chopper_counter_pass* passes,
+                          int32_t n_passes, uint64_t* counters_out,
+                          uint8_t* matched_out, void* scratch,
+                          size_t* scratch_bytes, uint32_t* status,
+                          void* stream);
 
 /* Text for a return code. */
 const char* chopper_strerror(int code);

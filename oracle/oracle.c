@@ -935,9 +935,10 @@ void orc_launch_split(int64_t n, const uint8_t* gpu, const uint8_t* stream,
  * Columns no matched entry fills are 0.  Records and entries without an
  * iteration (label NONE) are never matched.  JOIN_MISS: some record with an
  * iteration found no matching entry in some pass.  JOIN_ORDER: along
- * (gpu, stream) in (start', index) order, or along a pass's own order, an
- * iteration label is smaller than an earlier one (NONE labels aside; the
- * library then leaves the result unspecified).
+ * (gpu, stream) in (start', index) order, or along a pass's own order, a
+ * run of equal labels is not above the previous run with an iteration: a
+ * label's kernels are not consecutive (kernels without an iteration aside)
+ * or labels decrease (the library then leaves the result unspecified).
  * ------------------------------------------------------------------------ */
 #define ORC_JOIN_MISS 256u
 #define ORC_JOIN_ORDER 512u
@@ -974,12 +975,16 @@ static uint32_t join_ordinals(jrow_t* v, int64_t n) {
   uint32_t st = 0;
   qsort(v, (size_t)n, sizeof(jrow_t), cmp_jrow_time);
   {
-    uint32_t last = ORC_NONE;   /* last label of the current (g, st) */
+    /* runs of equal labels along each (g, st): the label of a run must be
+       above that of the previous run with an iteration */
+    uint32_t last = ORC_NONE;   /* label of the last run with an iteration */
     for (int64_t i = 0; i < n; ++i) {
-      if (i == 0 || v[i].g != v[i - 1].g || v[i].st != v[i - 1].st)
-        last = ORC_NONE;
-      if (v[i].lab == ORC_NONE) continue;
-      if (last != ORC_NONE && v[i].lab < last) st |= ORC_JOIN_ORDER;
+      const int first = i == 0 || v[i].g != v[i - 1].g ||
+                        v[i].st != v[i - 1].st;
+      if (first) last = ORC_NONE;
+      const int new_run = first || v[i].lab != v[i - 1].lab;
+      if (v[i].lab == ORC_NONE || !new_run) continue;
+      if (last != ORC_NONE && last >= v[i].lab) st |= ORC_JOIN_ORDER;
       last = v[i].lab;
     }
   }

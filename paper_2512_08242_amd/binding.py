@@ -77,6 +77,13 @@ class ViewOut(ctypes.Structure):
     _fields_ = [("unit_cap", ctypes.c_int64)] + [(k, P) for k in _VIEW_OUT]
 
 
+class CounterPass(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("n_cols", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("gpu", P), ("stream", P),
+                ("cls", P), ("label", P), ("values", P),
+                ("dst", ctypes.c_int32 * 16)]
+
+
 def make_filter(gpus=None, classes=None, iters=None) -> Filter:
     f = Filter()
     mask = [0, 0, 0, 0]
@@ -123,6 +130,10 @@ def _load():
     lib.chopper_launch_split.argtypes = [ctypes.POINTER(Records),
                                          ctypes.POINTER(Clock), P, P, P, P, P,
                                          P, SZ, P, P]
+    lib.chopper_join_counters.argtypes = [ctypes.POINTER(Records), P, P, P,
+                                          i32, i32, ctypes.POINTER(Markers),
+                                          ctypes.POINTER(CounterPass), i32, P,
+                                          P, P, SZ, P, P]
     lib.chopper_views.argtypes = [ctypes.POINTER(Records), P, P, P, i32, P,
                                   ctypes.POINTER(Markers),
                                   ctypes.POINTER(Rows),
@@ -138,7 +149,7 @@ def _load():
                  "chopper_aggregate", "chopper_ratios",
                  "chopper_window_fractions", "chopper_version",
                  "chopper_time_kernel", "chopper_views",
-                 "chopper_launch_split"):
+                 "chopper_launch_split", "chopper_join_counters"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -437,6 +448,40 @@ class Pipeline:
         scr, sb = _aligned(self._scr["launch"])
         _check(go(scr, ctypes.byref(sb)), "launch_split")
         return prep[:dt.n], call[:dt.n]
+
+    def join_counters(self, passes, iter_level: int = 0):
+        """Counters of serialized profiling passes matched to the records
+        (chopper_join_counters).  passes: dicts of device tensors gpu,
+        stream, cls (u8), label (i32 holding u32), values ([c][m] i64
+        holding u64) and the list dst of destination columns.  Returns
+        (counters [16][n], matched [n]) device tensors.  Needs align and
+        attribute to have run."""
+        dt = self.dt
+        dev = dt.start.device
+        n = dt.n
+        arr = (CounterPass * max(len(passes), 1))()
+        for i, q in enumerate(passes):
+            c = arr[i]
+            c.n = int(q["gpu"].numel())
+            c.n_cols = len(q["dst"])
+            c.gpu, c.stream, c.cls = _ptr(q["gpu"]), _ptr(q["stream"]), \
+                _ptr(q["cls"])
+            c.label, c.values = _ptr(q["label"]), _ptr(q["values"])
+            for j, d in enumerate(q["dst"]):
+                c.dst[j] = int(d)
+        ctr = torch.empty(16, max(n, 1), dtype=torch.int64, device=dev)
+        matched = torch.empty(max(n, 1), dtype=torch.uint8, device=dev)
+
+        def go(scratch, sbytes):
+            return lib.chopper_join_counters(
+                ctypes.byref(self._rec), _ptr(self.start), _ptr(self.order),
+                _ptr(self.idx), dt.depth, iter_level, ctypes.byref(self._mk),
+                arr, len(passes), _ptr(ctr), _ptr(matched), scratch, sbytes,
+                _ptr(self.status), _stream())
+        scr = _scratch(go, dev)
+        a, sb = _aligned(scr)
+        _check(go(a, ctypes.byref(sb)), "join_counters")
+        return ctr[:, :n], matched[:n]
 
     def step(self):
         """One pass of the whole pipeline."""

@@ -32,7 +32,9 @@ static const char* const kKernelNames[] = {
     "bi_fixup", "ov_comm_records", "agg_nat_init", "agg_nat_pre",
     "agg_nat_tiles", "agg_heads_nat", "agg_gpu_rows", "read_back",
     "view_flags", "view_units", "view_fill", "view_records", "view_rows",
-    "view_iter_max", "view_medians", "launch_split"};
+    "view_iter_max", "view_medians", "launch_split", "join_fill",
+    "join_labels", "join_heads", "join_runs", "join_order", "join_pass_prep",
+    "join_dense", "join_match", "join_gather"};
 
 __global__ __launch_bounds__(kBlock) void k_ratios(
     const int64_t* level_offset, int depth, int64_t cap, const uint64_t* n,

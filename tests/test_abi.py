@@ -34,7 +34,8 @@ def test_header_declares_the_four_steps():
               "chopper_aggregate", "chopper_ratios",
               "chopper_window_fractions", "chopper_strerror",
               "chopper_version", "chopper_time_kernel", "chopper_kernel_name",
-              "chopper_views", "chopper_launch_split"):
+              "chopper_views", "chopper_launch_split",
+              "chopper_join_counters"):
         assert n in names
 
 

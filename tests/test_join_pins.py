@@ -46,6 +46,13 @@ def test_join_hand_example():
     # a pass whose labels decrease along a stream
     q = dict(p, lab=np.array([8, 7, 7, 7], np.uint32))
     assert oracle.join(gpu, stream, cls, s, lab, [q])[2] & oracle.JOIN_ORDER
+    # records of one label split by a record without an iteration
+    lab2 = np.array([7, 7, NONE, 7, 8], np.uint32)
+    assert oracle.join(gpu, stream, cls, s, lab2, [p])[2] & oracle.JOIN_ORDER
+    # a record without an iteration at the start of a stream is fine
+    lab3 = np.array([NONE, 7, 7, 8, 8], np.uint32)
+    assert not oracle.join(gpu, stream, cls, s, lab3, [p])[2] & \
+        oracle.JOIN_ORDER
 
 
 def _dict_join(tr, s, lab, passes):
