@@ -5,8 +5,10 @@ chopper_aggregate(all levels) + derived ratios over the whole synthetic trace
 of 8 GPUs x 800 iterations x 32 layers with 16 counters per record (the
 Llama-3-8B FSDP trace shape), inputs resident in HBM.  After the timed steps
 chopper_views (per-phase/class and per-operation views with their medians)
-and chopper_launch_split (preparation / call overhead from seeded dispatch
-times) are timed on their own over the same run ("views", "launch_split").
+chopper_launch_split (preparation / call overhead from seeded dispatch
+times) and chopper_join_counters (the counters split into seven serialized
+passes and attached back) are timed on their own over the same run
+("views", "launch_split", "join_counters").
 Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--config 3]
@@ -156,7 +158,8 @@ def main():
         (np.diff(g) != 0) | (np.diff(tr.start) >= 0)))
     # seeded dispatch times (local clocks) for the launch-overhead split
     launch_host = tg.make_launch(tr, 11, max_lead=20000)
-    del tr, g
+    trace_host = tr
+    del g
     torch.cuda.synchronize()
     pipe = ch.Pipeline(dt)
     for _ in range(max(args.warmup, 1)):
@@ -267,6 +270,42 @@ def main():
         "peak": HBM_PEAK_GBS, "unit": "GB/s",
         "frac": lb / (lms * 1e-3) / 1e9 / HBM_PEAK_GBS}
     log(f"[bench] launch split {lms:.3f} ms")
+    # the counter-pass join: the 16 counters split into seven serialized
+    # passes (3, 3, 2, 2, 2, 2, 2 columns) and attached back to the records
+    if trace_host.counters is not None:
+        res = pipe.results()
+        i0 = res["idx"][0]
+        lab = np.full(n, 0xFFFFFFFF, np.uint32)
+        lab[i0 != 0xFFFFFFFF] = trace_host.m_label[i0[i0 != 0xFFFFFFFF]]
+        passes = tg.make_counter_passes(trace_host, lab, 5)
+        tt = lambda a, dt_: torch.from_numpy(
+            np.ascontiguousarray(a).view(dt_)).to(dev)
+        dp = [dict(gpu=tt(q["gpu"], np.uint8), stream=tt(q["stream"], np.uint8),
+                   cls=tt(q["cls"], np.uint8), label=tt(q["lab"], np.int32),
+                   values=tt(q["values"], np.int64), dst=q["dst"])
+              for q in passes]
+        del passes, res
+        pipe.join_counters(dp)
+        torch.cuda.synchronize()
+        v0.record()
+        for _ in range(K):
+            pipe.join_counters(dp)
+        v1.record()
+        torch.cuda.synchronize()
+        jms = v0.elapsed_time(v1) / K
+        # per pass entry gpu, stream, class, label and its columns read; per
+        # record and pass order, gpu, stream, class, label read and its
+        # columns written; matched bits
+        cols = 16
+        jb = (len(dp) * n * (1 + 1 + 1 + 4) + n * 8 * cols
+              + len(dp) * n * (4 + 1 + 1 + 1 + 4) + n * 8 * cols + n)
+        out["join_counters"] = {
+            "ms": jms, "passes": len(dp), "bytes": jb,
+            "achieved": jb / (jms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": jb / (jms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+        log(f"[bench] join counters {jms:.3f} ms")
+        del dp
+    del trace_host
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(cid, args.cpu_iters)

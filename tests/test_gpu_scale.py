@@ -142,4 +142,25 @@ def test_full_size_parity(ch, cid):
     rp, rc2 = oracle.launch_split(tr.gpu, tr.stream, tr.cls, s, e, tla)
     same(prep.cpu().numpy(), rp, "prep")
     same(call.cpu().numpy(), rc2, "call")
+    say(f"launch split ok ({time.time() - t0:.0f}s)")
+    if cid == 3:
+        # counters of seven serialized passes attached back to the records
+        lab = np.full(n, 0xFFFFFFFF, np.uint32)
+        ok = idx[0] != 0xFFFFFFFF
+        lab[ok] = tr.m_label[idx[0][ok]]
+        passes = tg.make_counter_passes(tr, lab, 5, drop_frac=0.001,
+                                        mismatch_frac=0.001, extra=2)
+        t = lambda a, dt: torch.from_numpy(
+            np.ascontiguousarray(a).view(dt)).cuda()
+        dp = [dict(gpu=t(q["gpu"], np.uint8), stream=t(q["stream"], np.uint8),
+                   cls=t(q["cls"], np.uint8), label=t(q["lab"], np.int32),
+                   values=t(q["values"], np.int64), dst=q["dst"])
+              for q in passes]
+        pipe.status.zero_()
+        ctr, matched = pipe.join_counters(dp)
+        st = int(pipe.status.item()) & 0xFFFFFFFF
+        rc3, rm3, rs3 = oracle.join(tr.gpu, tr.stream, tr.cls, s, lab, passes)
+        assert st == rs3 == oracle.JOIN_MISS
+        same(matched.cpu().numpy(), rm3, "join matched")
+        same(ctr.cpu().numpy().view(np.uint64), rc3, "join counters")
     say(f"done ({time.time() - t0:.0f}s)")
