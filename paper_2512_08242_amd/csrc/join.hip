@@ -55,25 +55,29 @@ __global__ void k_join_rec_labels(int64_t n, const uint32_t* idx_iter,
   lab[i] = (int64_t)m < nm ? m_label[m] : kNone;
 }
 
-// the entry index as the pass's time, and its (gpu, stream) pairs present
-__global__ void k_join_pass_prep(int64_t m, const uint8_t* gpu,
-                                 const uint8_t* stream, int64_t* t,
-                                 uint8_t* pres) {
+// the (gpu, stream) pairs of the records
+__global__ void k_join_presence(int64_t n, const uint8_t* gpu,
+                                const uint8_t* stream, uint8_t* pres) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= m) return;
-  t[i] = i;
-  pres[(uint32_t)gpu[i] * 256u + stream[i]] = 1;
+  if (i < n) pres[(uint32_t)gpu[i] * 256u + stream[i]] = 1;
 }
 
-// dense class ids of the (gpu, stream) pairs present, in (gpu, stream)
-// order; count[0] = number of classes
+// Dense class ids of the records' (gpu, stream) pairs in (gpu, stream)
+// order; every other pair gets the id after the last (pass entries of such
+// pairs can match nothing); count[0] = number of records' pairs.
 __global__ __launch_bounds__(kDenseT) void k_join_dense(const uint8_t* pres,
                                                         uint16_t* cmap,
                                                         uint32_t* count) {
-  __shared__ uint32_t s_w[kDenseT / kWave];
+  __shared__ uint32_t s_w[kDenseT / kWave + 1];
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  uint4 f[4];
+  const uint4* src = reinterpret_cast<const uint4*>(pres) + t * 4;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) f[q] = src[q];
+  const uint8_t* fb = reinterpret_cast<const uint8_t*>(f);
   uint32_t c = 0;
-  for (int b = 0; b < 64; ++b) c += pres[t * 64 + b] ? 1u : 0u;
+#pragma unroll
+  for (int b = 0; b < 64; ++b) c += fb[b] ? 1u : 0u;
   const uint32_t incl = wave_incl(c, OpAdd(), 0u);
   if (lane == kWave - 1) s_w[w] = incl;
   __syncthreads();
@@ -82,12 +86,23 @@ __global__ __launch_bounds__(kDenseT) void k_join_dense(const uint8_t* pres,
     if (q < w) id += s_w[q];
     tot += s_w[q];
   }
+  uint16_t ids[64];
+#pragma unroll
   for (int b = 0; b < 64; ++b) {
-    const bool on = pres[t * 64 + b] != 0;
-    cmap[t * 64 + b] = (uint16_t)(on ? id : 0u);
-    id += on ? 1u : 0u;
+    ids[b] = (uint16_t)(fb[b] ? id : tot);
+    id += fb[b] ? 1u : 0u;
   }
+  uint4* dst = reinterpret_cast<uint4*>(cmap) + t * 8;
+  const uint4* iv = reinterpret_cast<const uint4*>(ids);
+#pragma unroll
+  for (int q = 0; q < 8; ++q) dst[q] = iv[q];
   if (t == 0) *count = tot;
+}
+
+// the entry index as the pass's time
+__global__ void k_join_iota(int64_t m, int64_t* t) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < m) t[i] = i;
 }
 
 // Items of a (gpu, stream)-ordered sequence: key = (gpu, stream, label).
@@ -96,9 +111,10 @@ struct Seq {
   const uint8_t* gpu;
   const uint8_t* stream;
   const uint32_t* lab;
+  const uint16_t* cmap;    // (gpu, stream) -> dense class
   int64_t n;
   __device__ uint32_t cls(uint32_t i) const {
-    return (uint32_t)gpu[i] * 256u + stream[i];
+    return cmap[(uint32_t)gpu[i] * 256u + stream[i]];
   }
 };
 
@@ -305,10 +321,21 @@ extern "C" int chopper_join_counters(
                          dim3(kBlock), s, counters_out + (int64_t)c * n, n));
   CHOPPER_HIP(launch("join_fill", k_join_fill_u8, gn, dim3(kBlock), s,
                      matched_out, n, (uint32_t*)nullptr));
+  // dense classes of the records' (gpu, stream) pairs (one read-back)
+  CHOPPER_HIP(launch("join_fill", k_join_fill_u8, dim3(64), dim3(kBlock), s,
+                     (uint8_t*)nullptr, (int64_t)0, (uint32_t*)pres));
+  CHOPPER_HIP(launch("join_pass_prep", k_join_presence, gn, dim3(kBlock), s,
+                     n, rec->gpu, rec->stream, pres));
+  CHOPPER_HIP(launch("join_dense", k_join_dense, dim3(1), dim3(kDenseT), s,
+                     (const uint8_t*)pres, cmap, tot + 2));
+  uint32_t nclass = 0;
+  CHOPPER_HIP(read_back(tot + 2, &nclass, sizeof(uint32_t), s));
+  // (pass entries of other pairs take one more class)
+  if (nclass + 1 > 256) return CHOPPER_EINVAL;
   // the records' runs along `order`
   CHOPPER_HIP(launch("join_labels", k_join_rec_labels, gn, dim3(kBlock), s,
                      n, idx + (int64_t)iter_level * n, nm, mk->label, rlabv));
-  const Seq R{order, rec->gpu, rec->stream, rlabv, n};
+  const Seq R{order, rec->gpu, rec->stream, rlabv, cmap, n};
   CHOPPER_HIP(launch("join_heads", k_join_heads, gn, dim3(kBlock), s, R,
                      head));
   CHOPPER_HIP(exclusive_scan<uint32_t>(head, excl, n, tmp, tot, s));
@@ -323,27 +350,19 @@ extern "C" int chopper_join_counters(
     const int64_t m = P.n;
     PassCols C{P.n_cols, p, {0}};
     for (int c = 0; c < P.n_cols; ++c) C.dst[c] = P.dst[c];
-    uint32_t nclass = 0;
     if (m > 0) {
-      // stable (gpu, stream) partition of the pass in its own order
-      CHOPPER_HIP(launch("join_fill", k_join_fill_u8, dim3(64), dim3(kBlock),
-                         s, (uint8_t*)nullptr, (int64_t)0, (uint32_t*)pres));
-      CHOPPER_HIP(launch("join_pass_prep", k_join_pass_prep,
-                         grid_for(m, kBlock), dim3(kBlock), s, m, P.gpu,
-                         P.stream, ptime, pres));
-      CHOPPER_HIP(launch("join_dense", k_join_dense, dim3(1), dim3(kDenseT),
-                         s, (const uint8_t*)pres, cmap, tot + 2));
-      CHOPPER_HIP(read_back(tot + 2, &nclass, sizeof(uint32_t), s));
-      // (more than 256 (gpu, stream) pairs in one pass is not supported)
-      if (nclass > 256) return CHOPPER_EINVAL;
+      // stable partition of the pass by class, in its own order: with the
+      // entry index as time each class is then in time order already
+      CHOPPER_HIP(launch("join_pass_prep", k_join_iota, grid_for(m, kBlock),
+                         dim3(kBlock), s, m, ptime));
       ClassSortLayout L = SL;
       L.n = m;
       L.ntiles = sort_tiles(m);
       bool range_err = false;
-      KeyRecStream kq{P.gpu, P.stream, ptime, cmap, (int)nclass};
-      rc = class_sort(kq, L, qorder, coff, &range_err, s, -1);
+      KeyRecStream kq{P.gpu, P.stream, ptime, cmap, (int)nclass + 1};
+      rc = class_sort(kq, L, qorder, coff, &range_err, s, 1);
       if (rc != CHOPPER_OK) return rc;
-      const Seq Q{qorder, P.gpu, P.stream, P.label, m};
+      const Seq Q{qorder, P.gpu, P.stream, P.label, cmap, m};
       const dim3 gm = grid_for(m, kBlock);
       CHOPPER_HIP(launch("join_heads", k_join_heads, gm, dim3(kBlock), s, Q,
                          qhead));
@@ -367,7 +386,7 @@ extern "C" int chopper_join_counters(
                        (const uint32_t*)rstart, (const uint32_t*)match,
                        (const uint32_t*)qstart, (const uint32_t*)(tot + 1),
                        m, (const uint32_t*)qorder,
-                       Seq{qorder, P.gpu, P.stream, P.label, m}, P.cls,
+                       Seq{qorder, P.gpu, P.stream, P.label, cmap, m}, P.cls,
                        P.values, C, counters_out, matched_out, status));
   }
   return CHOPPER_OK;
