@@ -38,7 +38,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + f".tmp{os.getpid()}"
         subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-fPIC", "-shared",
-                               "-ffp-contract=off", "-o", tmp, _SRC])
+                               "-ffp-contract=off", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -129,6 +129,10 @@ def _load():
     lib.orc_join.argtypes = [i64, P, P, P, P, P, i32, P, P, P, P, P, P, P, P,
                              P, P]
     lib.orc_join.restype = ctypes.c_uint32
+    lib.orc_op_stats.argtypes = [i64, i64, i64, P, i32, i32, P, P, P, P, P,
+                                 i32, P, i32, i32, ctypes.c_double,
+                                 ctypes.c_double, P, P, P]
+    lib.orc_op_stats.restype = None
     _lib = lib
     return lib
 
@@ -261,6 +265,39 @@ def window_fractions(w: np.ndarray) -> np.ndarray:
     out = np.empty(w.shape, np.float64)
     lib.orc_window_fractions(w.shape[0], _p(w), _p(out))
     return out
+
+
+OP_STATS = ("pearson", "slope", "intercept", "d0", "d50", "q0", "q25",
+            "q50", "q75", "q100", "d_act", "d_peak", "ovr_util", "ovr_inst",
+            "ovr_overlap", "ovr_freq", "d_thr")
+
+
+def op_stats(rows: Dict, m_label, depth, phase_level=1, op_level=3,
+             n_phases=3, n_ops=64, freq_peak_mhz=2100.0, tpt_peak=1.0,
+             f_gemm=None):
+    """Overlap statistics and overhead breakdown per (phase, operation)
+    (Fig. gemm_overlap, Section VI eqs. 6-10) from the rows of the
+    operation level; definitions in oracle.c.  Returns (out [17][P*O],
+    cnt [P*O])."""
+    lib = _load()
+    lo = rows["level_offset"]
+    nr = int(rows["n"].shape[0])
+    path = _c(rows["path"], np.uint32)
+    nc = int(rows["ctr"].shape[0]) if rows["ctr"] is not None else 0
+    ctr = _c(rows["ctr"], np.uint64) if nc else np.zeros(1, np.uint64)
+    P_, O_ = int(n_phases), int(n_ops)
+    out = np.zeros((17, P_ * O_))
+    cnt = np.zeros(P_ * O_, np.int64)
+    fg = None if f_gemm is None else _c(f_gemm, np.float64)
+    a = [path, _c(rows["kind"], np.uint8), _c(rows["dur"], np.int64),
+         _c(rows["gap"], np.int64), _c(rows["ovl"], np.int64), ctr,
+         _c(m_label, np.uint32)]
+    lib.orc_op_stats(int(lo[op_level]), int(lo[op_level + 1]), nr,
+                     _p(a[0]), phase_level, op_level, _p(a[1]), _p(a[2]),
+                     _p(a[3]), _p(a[4]), _p(a[5]), nc, _p(a[6]), P_, O_,
+                     float(freq_peak_mhz), float(tpt_peak), _p(fg), _p(out),
+                     _p(cnt))
+    return out, cnt
 
 
 JOIN_MISS, JOIN_ORDER = 256, 512

@@ -31,6 +31,7 @@
  */
 #include <stdint.h>
 #include <stdlib.h>
+#include <math.h>
 #include <string.h>
 
 typedef __int128 i128;
@@ -1063,4 +1064,146 @@ uint32_t orc_join(int64_t n, const uint8_t* gpu, const uint8_t* stream,
   }
   free(R);
   return status;
+}
+
+/* ------------------------------------------------------------------------
+ * Overlap statistics and overhead breakdown of operations (Fig.
+ * gemm_overlap: overlap ratio against duration of operations, their
+ * correlation, 25-75 % and min-max fills of the overlap ratio; Section VI
+ * duration breakdown, eqs. 6-10).
+ *
+ * Instances: compute rows (kind 0) of the operation level with dur > 0 --
+ * one operation of one layer in one GPU's iteration -- grouped by
+ * g = p * O + o, p and o the labels of the row's phase- and operation-level
+ * markers (p < P, o < O).  Per instance
+ *   x = floor(ovl * 2^30 / dur)    overlap ratio in Q30 (ovl <= dur)
+ *   y = dur + gap                   operation duration with its bubbles (V-B)
+ * Per group with m instances, from exact sums Sx, Sy, Sxx, Syy, Sxy:
+ *   cov = m Sxy - Sx Sy, vx = m Sxx - Sx^2, vy = m Syy - Sy^2 (exact),
+ *   pearson = (double)cov / sqrt((double)vx * (double)vy)   (NaN if m < 2 or
+ *             a variance is 0: constant overlap gives NaN),
+ *   slope = (double)cov / (double)vx (per Q30 unit), intercept
+ *   a = ((double)Sy - slope (double)Sx) / m: the least-squares line of
+ *   duration on overlap; D0 = a, D50 = a + slope 2^29 (duration at 0 % and
+ *   50 % overlap), Ovr_overlap = D50 / D0 (eq. 9);
+ *   quantiles of x / 2^30: v[0], v[(m-1)/4], (v[(m-1)/2] + v[m/2]) / 2,
+ *   v[3(m-1)/4], v[m-1] of the sorted values;
+ *   D_act = Sy / m, D_peak = (sum of ctr[0]) * 1000 / freq_peak / m (ns,
+ *   eq. 10), MFMA_util = sum ctr[1] / sum ctr[0], Ovr_util = 1 / MFMA_util
+ *   (eq. 8), F_perf = sum ctr[11] / m, Ovr_inst = F_perf / F_gemm[o]
+ *   (eq. 7), D_thr = F_gemm[o] / TPT_peak (eq. 6), Ovr_freq = D_act /
+ *   D_peak / Ovr_overlap (eq. 10); F_gemm[o] is given per operation label
+ *   (NaN: not given).  Counter sums wrap modulo 2^64; with fewer than 16
+ *   counters the counter-based values are NaN.
+ * out [17][P * O]: pearson, slope, intercept, D0, D50, q0, q25, q50, q75,
+ * q100, D_act, D_peak, Ovr_util, Ovr_inst, Ovr_overlap, Ovr_freq, D_thr;
+ * cnt [P * O] = m.  Limits: y < 2^34, m < 2^26 per group.
+ * ------------------------------------------------------------------------ */
+typedef unsigned __int128 u128;
+
+static int cmp_u32(const void* x, const void* y) {
+  const uint32_t a = *(const uint32_t*)x, b = *(const uint32_t*)y;
+  return a < b ? -1 : a > b;
+}
+
+void orc_op_stats(int64_t lo, int64_t hi, int64_t cap, const uint32_t* path,
+                  int phase_level, int op_level, const uint8_t* kind,
+                  const int64_t* dur, const int64_t* gap, const int64_t* ovl,
+                  const uint64_t* ctr, int nc, const uint32_t* m_label,
+                  int P, int O, double freq_peak, double tpt_peak,
+                  const double* f_gemm, double* out, int64_t* cnt) {
+  const int G = P * O;
+  const double nan = __builtin_nan("");
+  /* the group of every row (-1: not an instance), then each group's rows */
+  const int64_t nr = hi > lo ? hi - lo : 0;
+  int32_t* grp = (int32_t*)malloc(sizeof(int32_t) * (size_t)(nr + 1));
+  int64_t* start = (int64_t*)calloc((size_t)G + 1, sizeof(int64_t));
+  for (int64_t r = lo; r < hi; ++r) {
+    int32_t gg = -1;
+    if (kind[r] == 0 && dur[r] > 0) {
+      const uint32_t mp = path[(int64_t)phase_level * cap + r];
+      const uint32_t mo = path[(int64_t)op_level * cap + r];
+      if (mp != ORC_NONE && mo != ORC_NONE) {
+        const uint32_t p = m_label[mp], o = m_label[mo];
+        if (p < (uint32_t)P && o < (uint32_t)O) gg = (int32_t)(p * O + o);
+      }
+    }
+    grp[r - lo] = gg;
+    if (gg >= 0) start[gg + 1]++;
+  }
+  for (int g = 0; g < G; ++g) start[g + 1] += start[g];
+  int64_t* rows = (int64_t*)malloc(sizeof(int64_t) * (size_t)(nr + 1));
+  int64_t* fillp = (int64_t*)malloc(sizeof(int64_t) * (size_t)(G + 1));
+  memcpy(fillp, start, sizeof(int64_t) * (size_t)(G + 1));
+  for (int64_t r = lo; r < hi; ++r)
+    if (grp[r - lo] >= 0) rows[fillp[grp[r - lo]]++] = r;
+  for (int g = 0; g < G; ++g) {
+    int64_t m = 0;
+    i128 sx = 0, sy = 0, sxx = 0, syy = 0, sxy = 0;
+    uint64_t cyc = 0, busy = 0, flops = 0;
+    uint32_t* xs =
+        (uint32_t*)malloc(sizeof(uint32_t) * (size_t)(start[g + 1] - start[g] + 1));
+    for (int64_t q = start[g]; q < start[g + 1]; ++q) {
+      const int64_t r = rows[q];
+      const i128 x = ((i128)ovl[r] << 30) / dur[r];
+      const i128 y = (i128)dur[r] + gap[r];
+      xs[m++] = (uint32_t)x;
+      sx += x;
+      sy += y;
+      sxx += x * x;
+      syy += y * y;
+      sxy += x * y;
+      if (nc >= 16) {
+        cyc += ctr[0 * cap + r];
+        busy += ctr[1 * cap + r];
+        flops += ctr[11 * cap + r];
+      }
+    }
+    cnt[g] = m;
+    double* o_ = out;
+    for (int k = 0; k < 17; ++k) o_[(int64_t)k * G + g] = nan;
+    if (m > 0) {
+      const i128 cov = (i128)m * sxy - sx * sy;
+      const i128 vx = (i128)m * sxx - sx * sx;
+      const i128 vy = (i128)m * syy - sy * sy;
+      const double dm = (double)m;
+      if (m >= 2 && vx != 0 && vy != 0)
+        o_[0 * G + g] = (double)cov / sqrt((double)vx * (double)vy);
+      double slope = nan, a = nan;
+      if (vx != 0) {
+        slope = (double)cov / (double)vx;
+        a = ((double)sy - slope * (double)sx) / dm;
+      }
+      o_[1 * G + g] = slope;
+      o_[2 * G + g] = a;
+      const double d0 = a, d50 = a + slope * 536870912.0;
+      o_[3 * G + g] = d0;
+      o_[4 * G + g] = d50;
+      qsort(xs, (size_t)m, sizeof(uint32_t), cmp_u32);
+      const double q = 1.0 / 1073741824.0;
+      o_[5 * G + g] = (double)xs[0] * q;
+      o_[6 * G + g] = (double)xs[(m - 1) / 4] * q;
+      o_[7 * G + g] = ((double)xs[(m - 1) / 2] + (double)xs[m / 2]) / 2.0 * q;
+      o_[8 * G + g] = (double)xs[3 * (m - 1) / 4] * q;
+      o_[9 * G + g] = (double)xs[m - 1] * q;
+      const double dact = (double)sy / dm;
+      o_[10 * G + g] = dact;
+      const double ovr_ov = d50 / d0;
+      o_[14 * G + g] = ovr_ov;
+      if (nc >= 16) {
+        const double dpeak = (double)cyc * 1000.0 / freq_peak / dm;
+        o_[11 * G + g] = dpeak;
+        o_[12 * G + g] = 1.0 / ((double)busy / (double)cyc);
+        const double fg = f_gemm ? f_gemm[g % O] : nan;
+        o_[13 * G + g] = ((double)flops / dm) / fg;
+        o_[15 * G + g] = dact / dpeak / ovr_ov;
+      }
+      o_[16 * G + g] = (f_gemm ? f_gemm[g % O] : nan) / tpt_peak;
+    }
+    free(xs);
+  }
+  free(grp);
+  free(start);
+  free(rows);
+  free(fillp);
 }
