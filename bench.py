@@ -4,11 +4,12 @@ One step = chopper_align + chopper_attribute + chopper_overlap +
 chopper_aggregate(all levels) + derived ratios over the whole synthetic trace
 of 8 GPUs x 800 iterations x 32 layers with 16 counters per record (the
 Llama-3-8B FSDP trace shape), inputs resident in HBM.  After the timed steps
-chopper_views (per-phase/class and per-operation views with their medians)
+chopper_views (per-phase/class and per-operation views with their medians),
+chopper_op_stats (overlap statistics and overhead breakdown per operation),
 chopper_launch_split (preparation / call overhead from seeded dispatch
 times) and chopper_join_counters (the counters split into seven serialized
 passes and attached back) are timed on their own over the same run
-("views", "launch_split", "join_counters").
+("views", "op_stats", "launch_split", "join_counters").
 Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--config 3]
@@ -254,6 +255,26 @@ def main():
         "spec": {"n_phases": P, "n_ops": O, "n_iters": iters,
                  "warmup": 10 if iters > 10 else 0}}
     log(f"[bench] views {vms:.3f} ms")
+    # overlap statistics and overhead breakdown per (phase, operation)
+    fg = np.linspace(2e9, 9e10, O)
+    pipe.op_stats(n_phases=P, n_ops=O, tpt_peak=1.3e6, f_gemm=fg)
+    torch.cuda.synchronize()
+    v0.record()
+    for _ in range(K):
+        pipe.op_stats(n_phases=P, n_ops=O, tpt_peak=1.3e6, f_gemm=fg)
+    v1.record()
+    torch.cuda.synchronize()
+    sms = v0.elapsed_time(v1) / K
+    # per operation-level row: kind, duration, gap, overlap, the phase and
+    # operation path entries, three counters
+    lop = min(3, depth - 1)
+    rows_op = int(lo[lop + 1] - lo[lop])
+    sb = rows_op * (1 + 8 + 8 + 8 + 4 + 4 + (24 if nc >= 16 else 0))
+    out["op_stats"] = {
+        "ms": sms, "rows": rows_op, "bytes": sb,
+        "achieved": sb / (sms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+        "unit": "GB/s", "frac": sb / (sms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    log(f"[bench] op stats {sms:.3f} ms")
     # the launch-overhead split from seeded dispatch times, timed on its own
     tl = torch.from_numpy(launch_host).to(dev)
     pipe.launch_split(tl)

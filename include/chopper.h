@@ -21,6 +21,8 @@
  *                      to the runtime kernels (III-A, III-B)
  *   chopper_launch_split  preparation / call split of the launch overhead
  *                      from dispatch times (V-D eqs. 1-3)
+ *   chopper_op_stats   overlap statistics and overhead breakdown per
+ *                      operation (Fig. gemm_overlap; VI eqs. 6-10)
  *   chopper_views      per-phase/class and per-operation views with medians
  *                      over iterations and GPUs, iteration throughput
  *                      (Fig. end_to_end, Fig. operation_time)
@@ -460,6 +462,53 @@ int chopper_join_counters(const chopper_records* records,
                           uint8_t* matched_out, void* scratch,
                           size_t* scratch_bytes, uint32_t* status,
                           void* stream);
+
+/*
+ * chopper_op_stats -- overlap statistics and overhead breakdown of
+ * operations (Fig. gemm_overlap: overlap ratio against operation duration,
+ * their correlation, 25-75 % and min-max fills of the ratio; Section VI
+ * duration breakdown, eqs. 6-10).
+ *
+ * Instances: compute rows (kind 0, dur > 0) of chopper_aggregate's level
+ * op_level -- one operation of one layer in one GPU's iteration -- in group
+ * g = p * n_ops + o of their phase and operation labels (p < n_phases,
+ * o < n_ops).  Per instance x = floor(ovl * 2^30 / dur) (overlap ratio,
+ * Q30) and y = dur + gap (duration with its bubbles, V-B).  From exact
+ * 128-bit sums Sx, Sy, Sxx, Syy, Sxy of a group of m instances:
+ * cov = m Sxy - Sx Sy, vx = m Sxx - Sx^2, vy = m Syy - Sy^2 (exact), each
+ * converted to the nearest double, and out [17][n_phases * n_ops] =
+ *   0 pearson    cov / sqrt(vx * vy)  (NaN if m < 2 or a variance is 0)
+ *   1 slope      cov / vx  (least-squares duration per Q30 unit of ratio)
+ *   2 intercept  (Sy - slope * Sx) / m
+ *   3 D0 = intercept, 4 D50 = intercept + slope * 2^29  (eq. 9)
+ *   5..9 ratio quantiles v[0], v[(m-1)/4], (v[(m-1)/2] + v[m/2]) / 2,
+ *        v[3(m-1)/4], v[m-1] of the sorted x, times 2^-30
+ *   10 D_act = Sy / m;  11 D_peak = sum ctr[0] * 1000 / freq_peak_mhz / m
+ *   12 Ovr_util = 1 / (sum ctr[1] / sum ctr[0])  (eq. 8)
+ *   13 Ovr_inst = (sum ctr[11] / m) / f_gemm[o]  (eq. 7)
+ *   14 Ovr_overlap = D50 / D0  (eq. 9)
+ *   15 Ovr_freq = D_act / D_peak / Ovr_overlap  (eq. 10)
+ *   16 D_thr = f_gemm[o] / tpt_peak  (eq. 6)
+ * in exactly these IEEE operations; cnt [n_phases * n_ops] = m.  Empty
+ * groups: NaN.  11-13 and 15 need n_counters = 16 (else NaN); f_gemm
+ * ([host], n_ops theoretical FLOP counts, per operation label) may be NULL
+ * (13 and 16 NaN).  Limits: y < 2^34 (else RANGE), m < 2^26 per group.
+ */
+typedef struct {
+  int32_t phase_level;
+  int32_t op_level;
+  int32_t n_phases;   /* 1 .. 16 */
+  int32_t n_ops;      /* 1 .. 128 */
+  double freq_peak_mhz;
+  double tpt_peak;    /* FLOP per ns */
+  const double* f_gemm;
+} chopper_stats_spec;
+
+int chopper_op_stats(const chopper_rows* rows, int32_t depth,
+                     int32_t n_counters, const chopper_markers* markers,
+                     const chopper_stats_spec* spec, double* out,
+                     int64_t* cnt, void* scratch, size_t* scratch_bytes,
+                     uint32_t* status, void* stream);
 
 /* Text for a return code. */
 const char* chopper_strerror(int code);

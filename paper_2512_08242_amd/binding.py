@@ -77,6 +77,14 @@ class ViewOut(ctypes.Structure):
     _fields_ = [("unit_cap", ctypes.c_int64)] + [(k, P) for k in _VIEW_OUT]
 
 
+class StatsSpec(ctypes.Structure):
+    _fields_ = [("phase_level", ctypes.c_int32), ("op_level", ctypes.c_int32),
+                ("n_phases", ctypes.c_int32), ("n_ops", ctypes.c_int32),
+                ("freq_peak_mhz", ctypes.c_double),
+                ("tpt_peak", ctypes.c_double),
+                ("f_gemm", ctypes.POINTER(ctypes.c_double))]
+
+
 class CounterPass(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int64), ("n_cols", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("gpu", P), ("stream", P),
@@ -130,6 +138,10 @@ def _load():
     lib.chopper_launch_split.argtypes = [ctypes.POINTER(Records),
                                          ctypes.POINTER(Clock), P, P, P, P, P,
                                          P, SZ, P, P]
+    lib.chopper_op_stats.argtypes = [ctypes.POINTER(Rows), i32, i32,
+                                     ctypes.POINTER(Markers),
+                                     ctypes.POINTER(StatsSpec), P, P, P, SZ,
+                                     P, P]
     lib.chopper_join_counters.argtypes = [ctypes.POINTER(Records), P, P, P,
                                           i32, i32, ctypes.POINTER(Markers),
                                           ctypes.POINTER(CounterPass), i32, P,
@@ -149,7 +161,8 @@ def _load():
                  "chopper_aggregate", "chopper_ratios",
                  "chopper_window_fractions", "chopper_version",
                  "chopper_time_kernel", "chopper_views",
-                 "chopper_launch_split", "chopper_join_counters"):
+                 "chopper_launch_split", "chopper_join_counters",
+                 "chopper_op_stats"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
 
@@ -448,6 +461,38 @@ class Pipeline:
         scr, sb = _aligned(self._scr["launch"])
         _check(go(scr, ctypes.byref(sb)), "launch_split")
         return prep[:dt.n], call[:dt.n]
+
+    def op_stats(self, phase_level: int = 1, op_level: int = 3,
+                 n_phases: int = 3, n_ops: int = 64,
+                 freq_peak_mhz: float = 2100.0, tpt_peak: float = 1.0,
+                 f_gemm=None):
+        """Overlap statistics and overhead breakdown per (phase, operation)
+        from the aggregated rows (chopper_op_stats); returns device tensors
+        out [17][n_phases * n_ops] and cnt [n_phases * n_ops]."""
+        dt = self.dt
+        dev = dt.start.device
+        G = n_phases * n_ops
+        out = torch.empty(17, G, dtype=torch.float64, device=dev)
+        cnt = torch.empty(G, dtype=torch.int64, device=dev)
+        fg = None
+        if f_gemm is not None:
+            fg = (ctypes.c_double * n_ops)(*[float(v) for v in f_gemm])
+        spec = StatsSpec(phase_level, op_level, n_phases, n_ops,
+                         float(freq_peak_mhz), float(tpt_peak),
+                         ctypes.cast(fg, ctypes.POINTER(ctypes.c_double))
+                         if fg is not None else None)
+        rows = self.rows.struct()
+
+        def go(scratch, sbytes):
+            return lib.chopper_op_stats(
+                ctypes.byref(rows), dt.depth, dt.n_counters,
+                ctypes.byref(self._mk), ctypes.byref(spec), _ptr(out),
+                _ptr(cnt), scratch, sbytes, _ptr(self.status), _stream())
+        if "stats" not in self._scr:
+            self._scr["stats"] = _scratch(go, dev)
+        scr, sb = _aligned(self._scr["stats"])
+        _check(go(scr, ctypes.byref(sb)), "op_stats")
+        return out, cnt
 
     def join_counters(self, passes, iter_level: int = 0):
         """Counters of serialized profiling passes matched to the records

@@ -35,7 +35,7 @@ def test_header_declares_the_four_steps():
               "chopper_window_fractions", "chopper_strerror",
               "chopper_version", "chopper_time_kernel", "chopper_kernel_name",
               "chopper_views", "chopper_launch_split",
-              "chopper_join_counters"):
+              "chopper_join_counters", "chopper_op_stats"):
         assert n in names
 
 

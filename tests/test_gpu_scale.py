@@ -134,6 +134,23 @@ def test_full_size_parity(ch, cid):
     assert gv["iter_cnt"] == rv["iter_cnt"]
     assert gv["iter_med"] == rv["iter_med"]
     say(f"views ok ({time.time() - t0:.0f}s)")
+    # overlap statistics and overhead breakdown per (phase, operation), the
+    # oracle run on the brute-force rows of the operation level
+    fg = np.linspace(2e9, 9e10, 64)
+    pipe.status.zero_()
+    so, sc = pipe.op_stats(freq_peak_mhz=2100.0, tpt_peak=1.3e6, f_gemm=fg)
+    assert int(pipe.status.item()) & 0xFFFFFFFF == 0
+    r3 = ref[3]
+    lofs = np.zeros(tr.depth + 3, np.int64)
+    lofs[4:] = r3["n"].shape[0]
+    ro, rcnt = oracle.op_stats(dict(r3, level_offset=lofs), tr.m_label,
+                               tr.depth, freq_peak_mhz=2100.0, tpt_peak=1.3e6,
+                               f_gemm=fg)
+    same(sc.cpu().numpy(), rcnt, "op stats counts")
+    so = so.cpu().numpy()
+    assert ((so == ro) | (np.isnan(so) & np.isnan(ro))).all(), "op stats"
+    assert rcnt.sum() > 0
+    say(f"op stats ok ({time.time() - t0:.0f}s)")
     # launch overhead split from seeded dispatch times
     import torch
     tl = tg.make_launch(tr, 11, max_lead=20000)

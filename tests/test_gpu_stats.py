@@ -1,0 +1,82 @@
+"""Parity of chopper_op_stats (overlap statistics and overhead breakdown of
+operations: Fig. gemm_overlap, Section VI eqs. 6-10) with the CPU oracle
+through the C ABI: instance counts bit-exact and every statistic equal as a
+double (NaN matching NaN) -- both sides take the same IEEE operations on
+the same exact integer moments and order statistics."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ch():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    import paper_2512_08242_amd as m
+    return m
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def stats_both(ch, tr, **spec):
+    pipe = ch.Pipeline(ch.DeviceTrace(tr, "cuda"))
+    pipe.status.zero_()
+    pipe.step()
+    out, cnt = pipe.op_stats(**spec)
+    got = (out.cpu().numpy(), cnt.cpu().numpy(),
+           int(pipe.status.item()) & 0xFFFFFFFF)
+    ref = oracle.op_stats(oracle.run(tr)["rows"], tr.m_label, tr.depth,
+                          **spec)
+    return got, ref
+
+
+def check(got, ref, name):
+    go, gc, _ = got
+    ro, rc = ref
+    assert np.array_equal(gc, rc), name
+    same = (go == ro) | (np.isnan(go) & np.isnan(ro))
+    if not same.all():
+        k, g = np.argwhere(~same)[0]
+        raise AssertionError(f"{name}: {oracle.OP_STATS[k]} of group {g}: "
+                             f"{go[k, g]!r} vs {ro[k, g]!r}")
+
+
+@pytest.mark.parametrize("cid", [0, 1, 2])
+def test_stats_configs(ch, cid):
+    say(f"op stats: config {cid}")
+    tr = tg.make_config(cid)
+    fg = np.linspace(1e8, 9e9, 64)
+    got, ref = stats_both(ch, tr, n_phases=3, n_ops=64, freq_peak_mhz=2100.0,
+                          tpt_peak=1.3e6, f_gemm=fg)
+    check(got, ref, f"config {cid}")
+    assert got[1].sum() > 0 and np.isfinite(got[0][0]).any()
+
+
+def test_stats_no_gemm_flops(ch):
+    say("op stats: config 2 without per-operation FLOPs")
+    got, ref = stats_both(ch, tg.make_config(2))
+    check(got, ref, "config 2, f_gemm NULL")
+    assert np.isnan(got[0][13]).all() and np.isnan(got[0][16]).all()
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_stats_micro(ch, seed):
+    say(f"op stats: micro seed {seed}")
+    tr = tg.make_micro(seed, n_gpus=3, n_kernels=900, n_streams=3, depth=3,
+                       span=12000, n_counters=16 if seed != 1 else 0)
+    # few labels, so that groups hold several instances
+    tr.m_label = (tr.m_label % (3 + seed)).astype(tr.m_label.dtype)
+    got, ref = stats_both(ch, tr, phase_level=1, op_level=2, n_phases=16,
+                          n_ops=50)
+    check(got, ref, f"micro {seed}")
+    assert got[1].max() >= 2
