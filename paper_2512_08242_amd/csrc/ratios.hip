@@ -35,7 +35,8 @@ static const char* const kKernelNames[] = {
     "view_iter_max", "view_medians", "launch_split", "join_fill",
     "join_labels", "join_heads", "join_runs", "join_order", "join_pass_prep",
     "join_dense", "join_match", "join_gather", "stats_clear", "stats_keys",
-    "stats_offsets", "stats_scatter", "stats_group"};
+    "stats_offsets", "stats_scatter", "stats_pass", "stats_select",
+    "stats_final"};
 
 __global__ __launch_bounds__(kBlock) void k_ratios(
     const int64_t* level_offset, int depth, int64_t cap, const uint64_t* n,

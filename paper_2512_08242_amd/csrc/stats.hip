@@ -4,11 +4,13 @@
 // eqs. 6-10).
 //
 // The instances (compute rows of the operation level) are partitioned by
-// (phase, operation) group; one 1024-thread block per group then adds the
-// exact moments of (overlap ratio in Q30, duration) in 128-bit integers --
-// integer sums do not depend on their order, so the derived doubles are the
-// same IEEE operations on the same values as anywhere else -- and selects
-// the quantiles of the ratio by radix, eight bits per pass.
+// (phase, operation) group into compact columns of the overlap ratio (Q30),
+// the time and three counters.  Blocks of 8192 instances of one group then
+// add the exact moments in 64-bit words (halves of the products that would
+// overflow) -- integer sums do not depend on their order, so the derived
+// doubles are the same IEEE operations on the same values as anywhere else
+// -- and build the histograms of a radix selection of six order statistics
+// of the ratio per group, eight bits per pass, all groups at once.
 #include "common.h"
 #include "wave.h"
 
@@ -20,6 +22,11 @@ namespace {
 
 constexpr int kMaxGroups = 16 * 128;
 constexpr int kStatT = 1024;
+constexpr int kStatIpt = 8;
+constexpr int kRowSpan = kStatT * kStatIpt;   // rows per block
+constexpr int kChunk = kStatT * kStatIpt;     // instances per block
+constexpr int kRanks = 6;                     // order statistics per group
+constexpr int kSums = 11;                     // exact sums per group
 constexpr int kStats = 17;
 typedef __int128 i128;
 typedef unsigned __int128 u128;
@@ -59,73 +66,6 @@ __device__ inline uint32_t group_of(const StatArgs& A, int64_t r) {
   return p * (uint32_t)A.O + o;
 }
 
-__global__ void k_stats_clear(uint32_t* cnt, int G) {
-  const int g = (int)(blockIdx.x * blockDim.x + threadIdx.x);
-  if (g < G) cnt[g] = 0;
-}
-
-// group of every row and the instances per group
-__global__ __launch_bounds__(kBlock) void k_stats_keys(StatArgs A,
-                                                       uint32_t* key,
-                                                       uint32_t* cnt) {
-  __shared__ uint32_t s_h[kMaxGroups];
-  const int G = A.P * A.O;
-  for (int g = threadIdx.x; g < G; g += kBlock) s_h[g] = 0;
-  __syncthreads();
-  int64_t lo, hi;
-  level_range(A, lo, hi);
-  const int64_t r = lo + (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (r < hi) {
-    const uint32_t g = group_of(A, r);
-    key[r - lo] = g;
-    if (g != kNone) atomicAdd(&s_h[g], 1u);
-  }
-  __syncthreads();
-  for (int g = threadIdx.x; g < G; g += kBlock)
-    if (s_h[g]) atomicAdd(&cnt[g], s_h[g]);
-}
-
-// group offsets (one block) and the fill cursors
-__global__ __launch_bounds__(kStatT) void k_stats_offsets(const uint32_t* cnt,
-                                                          int G, uint32_t* off,
-                                                          uint32_t* cur) {
-  __shared__ uint32_t s_w[kStatT / kWave];
-  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
-  uint32_t carry = 0;
-  for (int b0 = 0; b0 < G; b0 += kStatT) {
-    const int g = b0 + t;
-    const uint32_t v = g < G ? cnt[g] : 0u;
-    const uint32_t incl = wave_incl(v, OpAdd(), 0u);
-    if (lane == kWave - 1) s_w[w] = incl;
-    __syncthreads();
-    uint32_t pre = carry, tot = carry;
-    for (int q = 0; q < kStatT / kWave; ++q) {
-      if (q < w) pre += s_w[q];
-      tot += s_w[q];
-    }
-    if (g < G) {
-      off[g] = pre + incl - v;
-      cur[g] = pre + incl - v;
-    }
-    carry = tot;
-    __syncthreads();
-  }
-  if (t == 0) off[G] = carry;
-}
-
-// rows into their group's slots (the order inside a group is immaterial:
-// its sums are exact and its quantiles are order statistics)
-__global__ void k_stats_scatter(StatArgs A, const uint32_t* key,
-                                uint32_t* cur, uint32_t* list) {
-  int64_t lo, hi;
-  level_range(A, lo, hi);
-  const int64_t r = lo + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= hi) return;
-  const uint32_t g = key[r - lo];
-  if (g == kNone) return;
-  list[atomicAdd(&cur[g], 1u)] = (uint32_t)r;
-}
-
 // nearest double to a 128-bit integer (round half to even): a magnitude
 // below 2^63 converts directly; else its top 64 bits with every lower bit
 // folded into the last one (below the double's precision there) convert
@@ -147,18 +87,296 @@ __device__ inline double i128_to_double(i128 v) {
   return neg ? -d : d;
 }
 
-// block-wide sum of a 128-bit value (tree in LDS)
-__device__ inline u128 block_sum_u128(u128 v, u128* s) {
-  const int t = threadIdx.x;
-  s[t] = v;
+// add 1 for every active lane to h[bin] and return the lane's slot among
+// the adds (the old value plus its rank): one LDS atomic per wave when the
+// active lanes share the bin, else one per lane
+__device__ inline uint32_t lds_claim(uint32_t* h, uint32_t bin, bool act) {
+  const uint64_t m = __ballot(act);
+  if (m == 0) return 0;
+  const int ld = __ffsll((long long)m) - 1;
+  const uint32_t b0 = (uint32_t)__builtin_amdgcn_readlane((int)bin, ld);
+  if (__ballot(act && bin == b0) == m) {
+    uint32_t base = 0;
+    if (lane_id() == ld) base = atomicAdd(&h[b0], (uint32_t)__popcll(m));
+    base = (uint32_t)__builtin_amdgcn_readlane((int)base, ld);
+    return base + lanes_below(m);
+  }
+  return act ? atomicAdd(&h[bin], 1u) : 0u;
+}
+
+__global__ void k_stats_clear(uint32_t* cnt, int G, uint32_t* hist,
+                              int64_t nh) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < G) cnt[i] = 0;
+  if (i < nh) hist[i] = 0;
+}
+
+// group of every row of the operation level and the instances per group
+__global__ __launch_bounds__(kStatT) void k_stats_keys(StatArgs A,
+                                                       uint32_t* key,
+                                                       uint32_t* cnt) {
+  __shared__ uint32_t s_h[kMaxGroups];
+  const int G = A.P * A.O;
+  for (int g = threadIdx.x; g < G; g += kStatT) s_h[g] = 0;
   __syncthreads();
-  for (int d = kStatT / 2; d > 0; d >>= 1) {
-    if (t < d) s[t] += s[t + d];
+  int64_t lo, hi;
+  level_range(A, lo, hi);
+  const int64_t r0 = lo + (int64_t)blockIdx.x * kRowSpan + threadIdx.x;
+#pragma unroll
+  for (int k = 0; k < kStatIpt; ++k) {
+    const int64_t r = r0 + (int64_t)k * kStatT;
+    uint32_t g = kNone;
+    if (r < hi) {
+      g = group_of(A, r);
+      key[r - lo] = g;
+    }
+    lds_claim(s_h, g, g != kNone);
+  }
+  __syncthreads();
+  for (int g = threadIdx.x; g < G; g += kStatT)
+    if (s_h[g]) atomicAdd(&cnt[g], s_h[g]);
+}
+
+// group offsets, fill cursors, chunk offsets and the ranks to select (one
+// block)
+__global__ __launch_bounds__(kStatT) void k_stats_offsets(
+    const uint32_t* cnt, int G, uint32_t* off, uint32_t* cur, uint32_t* coff,
+    uint32_t* spre, int64_t* srank) {
+  __shared__ uint32_t s_w[2][kStatT / kWave];
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  uint32_t carry = 0, ccarry = 0;
+  for (int b0 = 0; b0 < G; b0 += kStatT) {
+    const int g = b0 + t;
+    const uint32_t v = g < G ? cnt[g] : 0u;
+    const uint32_t c = (uint32_t)ceil_div(v, kChunk);
+    const uint32_t incl = wave_incl(v, OpAdd(), 0u);
+    const uint32_t cincl = wave_incl(c, OpAdd(), 0u);
+    if (lane == kWave - 1) {
+      s_w[0][w] = incl;
+      s_w[1][w] = cincl;
+    }
+    __syncthreads();
+    uint32_t pre = carry, tot = carry, cpre = ccarry, ctot = ccarry;
+    for (int q = 0; q < kStatT / kWave; ++q) {
+      if (q < w) {
+        pre += s_w[0][q];
+        cpre += s_w[1][q];
+      }
+      tot += s_w[0][q];
+      ctot += s_w[1][q];
+    }
+    if (g < G) {
+      off[g] = pre + incl - v;
+      cur[g] = pre + incl - v;
+      coff[g] = cpre + cincl - c;
+      // v[0], v[(m-1)/4], v[(m-1)/2], v[m/2], v[3(m-1)/4], v[m-1]
+      const int64_t m = v;
+      const int64_t want[kRanks] = {0, (m - 1) / 4, (m - 1) / 2, m / 2,
+                                    3 * (m - 1) / 4, m - 1};
+#pragma unroll
+      for (int r = 0; r < kRanks; ++r) {
+        spre[g * kRanks + r] = 0;
+        srank[g * kRanks + r] = want[r];
+      }
+    }
+    carry = tot;
+    ccarry = ctot;
     __syncthreads();
   }
-  const u128 r = s[0];
+  if (t == 0) {
+    off[G] = carry;
+    coff[G] = ccarry;
+  }
+}
+
+// every instance into its group's slots with its ratio x (Q30), its time y
+// and three counters: a block claims its slots of a group with one atomic
+// (the order inside a group is immaterial: sums are exact and quantiles are
+// order statistics)
+__global__ __launch_bounds__(kStatT) void k_stats_scatter(
+    StatArgs A, const uint32_t* key, uint32_t* cur, uint32_t* xs,
+    uint64_t* ys, uint64_t* cs, int64_t ncap, uint32_t* status) {
+  __shared__ uint32_t s_n[kMaxGroups];
+  __shared__ uint32_t s_base[kMaxGroups];
+  const int G = A.P * A.O;
+  for (int g = threadIdx.x; g < G; g += kStatT) s_n[g] = 0;
   __syncthreads();
-  return r;
+  int64_t lo, hi;
+  level_range(A, lo, hi);
+  const int64_t r0 = lo + (int64_t)blockIdx.x * kRowSpan + threadIdx.x;
+  uint32_t g[kStatIpt], slot[kStatIpt];
+#pragma unroll
+  for (int k = 0; k < kStatIpt; ++k) {
+    const int64_t r = r0 + (int64_t)k * kStatT;
+    g[k] = r < hi ? key[r - lo] : kNone;
+    slot[k] = lds_claim(s_n, g[k], g[k] != kNone);
+  }
+  __syncthreads();
+  for (int q = threadIdx.x; q < G; q += kStatT)
+    if (s_n[q]) s_base[q] = atomicAdd(&cur[q], s_n[q]);
+  __syncthreads();
+  bool big = false;
+#pragma unroll
+  for (int k = 0; k < kStatIpt; ++k) {
+    if (g[k] == kNone) continue;
+    const int64_t r = r0 + (int64_t)k * kStatT;
+    const uint64_t d = (uint64_t)A.dur[r];
+    const uint64_t ov = (uint64_t)A.ovl[r];
+    const uint64_t y = d + (uint64_t)A.gap[r];
+    const uint64_t x = (ov << 30) / d;
+    if ((y >> 34) != 0 || x > (1ull << 30)) big = true;
+    const uint32_t pos = s_base[g[k]] + slot[k];
+    xs[pos] = (uint32_t)x;
+    ys[pos] = y;
+    if (A.nc >= 16) {
+      cs[pos] = A.ctr[0 * A.cap + r];
+      cs[ncap + pos] = A.ctr[1 * A.cap + r];
+      cs[2 * ncap + pos] = A.ctr[11 * A.cap + r];
+    }
+  }
+  if (__ballot(big) != 0 && lane_id() == 0)
+    atomicOr(status, CHOPPER_ST_RANGE);
+}
+
+// the group and chunk of this block (false past the last chunk)
+__device__ inline bool chunk_of(const uint32_t* coff, const uint32_t* off,
+                                int G, int64_t& b, int64_t& e, int& g) {
+  const uint32_t c = blockIdx.x;
+  if (c >= coff[G]) return false;
+  int lo = 0, hi = G;        // the last g with coff[g] <= c
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (coff[mid] <= c) lo = mid;
+    else hi = mid;
+  }
+  g = lo;
+  b = (int64_t)off[g] + (int64_t)(c - coff[g]) * kChunk;
+  e = b + kChunk;
+  if (e > (int64_t)off[g + 1]) e = off[g + 1];
+  return true;
+}
+
+// sum of v over the block into s_part (kSums words), exact in 64 bits
+__device__ inline void block_sums(uint64_t (&v)[kSums],
+                                  uint64_t (*s_w)[kSums], uint64_t* dst) {
+  const int w = threadIdx.x / kWave;
+#pragma unroll
+  for (int k = 0; k < kSums; ++k) {
+    const uint64_t s = lane63(wave_incl(v[k], OpAdd(), (uint64_t)0));
+    if (lane_id() == 0) s_w[w][k] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x < kSums) {
+    uint64_t s = 0;
+    for (int q = 0; q < (int)(blockDim.x / kWave); ++q)
+      s += s_w[q][threadIdx.x];
+    dst[threadIdx.x] = s;
+  }
+}
+
+// One radix pass over a chunk of one group: the histogram of digit
+// (x >> sh) & 255 of the candidates of every rank (those whose higher
+// digits equal the rank's selected prefix) into the group's global
+// histograms.  The first pass has one histogram (no prefix yet) and also
+// writes the chunk's sums of x, y, x^2, y^2, xy (in 32-bit halves where they
+// would overflow) and the three counters.
+template <bool First>
+__global__ __launch_bounds__(kStatT) void k_stats_pass(
+    const uint32_t* off, const uint32_t* coff, int G, const uint32_t* xs,
+    const uint64_t* ys, const uint64_t* cs, int64_t ncap, int nc,
+    const uint32_t* spre, int sh, uint32_t* ghist, uint64_t* part) {
+  __shared__ uint32_t s_h[kRanks * 256];
+  __shared__ uint64_t s_w[kStatT / kWave][kSums];
+  int64_t b, e;
+  int g;
+  if (!chunk_of(coff, off, G, b, e, g)) return;
+  const int t = threadIdx.x;
+  for (int q = t; q < kRanks * 256; q += kStatT) s_h[q] = 0;
+  uint32_t pre[kRanks];
+#pragma unroll
+  for (int r = 0; r < kRanks; ++r) pre[r] = spre[g * kRanks + r];
+  __syncthreads();
+  const int hs = sh + 8;
+  uint64_t acc[kSums];
+#pragma unroll
+  for (int k = 0; k < kSums; ++k) acc[k] = 0;
+#pragma unroll
+  for (int k = 0; k < kStatIpt; ++k) {
+    const int64_t i = b + (int64_t)k * kStatT + t;
+    const bool ok = i < e;
+    const uint32_t x = ok ? xs[i] : 0u;
+    const uint32_t dig = (x >> sh) & 255u;
+    if (First) {
+      lds_claim(s_h, dig, ok);
+      if (ok) {
+        const uint64_t y = ys[i];
+        const uint64_t xx = (uint64_t)x * x;
+        const u128 yy = (u128)y * y;
+        const uint64_t xy = (uint64_t)x * y;
+        acc[0] += x;
+        acc[1] += y;
+        acc[2] += xx & 0xFFFFFFFFull;
+        acc[3] += xx >> 32;
+        acc[4] += (uint64_t)yy & 0xFFFFFFFFull;
+        acc[5] += (uint64_t)(yy >> 32);
+        acc[6] += xy & 0xFFFFFFFFull;
+        acc[7] += xy >> 32;
+        if (nc >= 16) {
+          acc[8] += cs[i];
+          acc[9] += cs[ncap + i];
+          acc[10] += cs[2 * ncap + i];
+        }
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < kRanks; ++r)
+        lds_claim(&s_h[r * 256], dig, ok && (x >> hs) == (pre[r] >> hs));
+    }
+  }
+  if (First) block_sums(acc, s_w, part + (int64_t)blockIdx.x * kSums);
+  __syncthreads();
+  uint32_t* gh = ghist + (int64_t)g * kRanks * 256;
+  for (int q = t; q < (First ? 256 : kRanks * 256); q += kStatT)
+    if (s_h[q]) atomicAdd(&gh[q], s_h[q]);
+}
+
+// the digit of every rank of a group from its histogram; the prefix and
+// the rank within the remaining candidates move on, and the histograms are
+// cleared for the next pass
+__global__ __launch_bounds__(kRanks * kWave) void k_stats_select(
+    const uint32_t* cnt, int sh, bool first, uint32_t* ghist, uint32_t* spre,
+    int64_t* srank) {
+  const int g = blockIdx.x, w = threadIdx.x / kWave, lane = lane_id();
+  if (cnt[g] == 0) return;
+  uint32_t* gh = ghist + (int64_t)g * kRanks * 256;
+  const uint32_t* h4 = gh + (first ? 0 : w * 256) + lane * 4;
+  uint32_t h[4], sum = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    h[q] = h4[q];
+    sum += h[q];
+  }
+  const int64_t rank = srank[g * kRanks + w];
+  const uint32_t incl = wave_incl(sum, OpAdd(), 0u);
+  const uint64_t past = __ballot((int64_t)incl > rank);
+  const int ln = __ffsll((long long)past) - 1;
+  if (lane == ln) {
+    int64_t under = (int64_t)incl - sum;
+    int dsel = lane * 4 + 3;
+    for (int q = 0; q < 4; ++q) {
+      if (under + (int64_t)h[q] > rank) {
+        dsel = lane * 4 + q;
+        break;
+      }
+      under += h[q];
+    }
+    spre[g * kRanks + w] |= (uint32_t)dsel << sh;
+    srank[g * kRanks + w] = rank - under;
+  }
+  __syncthreads();
+  for (int q = threadIdx.x; q < (first ? 256 : kRanks * 256);
+       q += kRanks * kWave)
+    gh[q] = 0;
 }
 
 struct StatOut {
@@ -169,121 +387,42 @@ struct StatOut {
   double f_gemm[128];
 };
 
-__global__ __launch_bounds__(kStatT) void k_stats_group(
-    StatArgs A, const uint32_t* off, const uint32_t* list, uint32_t* xs,
-    StatOut S, uint32_t* status) {
-  __shared__ u128 s_v[kStatT];
-  __shared__ uint32_t s_hist[2][256];
-  __shared__ uint32_t s_sel[4];
-  const int t = threadIdx.x;
-  const int G = A.P * A.O;
-  const int g = blockIdx.x;
-  const int64_t b = off[g], m = (int64_t)off[g + 1] - b;
+// the exact sums of a group from its chunks and the derived values, in the
+// same IEEE operations as their definition
+__global__ __launch_bounds__(kBlock) void k_stats_final(
+    const uint32_t* cnt, const uint32_t* coff, int G, int O, int nc,
+    const uint64_t* part, const uint32_t* spre, StatOut S) {
+  __shared__ uint64_t s_w[kBlock / kWave][kSums];
+  __shared__ uint64_t s_tot[kSums];
+  const int g = blockIdx.x, t = threadIdx.x;
+  const int64_t m = cnt[g];
   const double nan = __builtin_nan("");
+  double* o = S.out;
   if (m == 0) {
-    if (t < kStats) S.out[(int64_t)t * G + g] = nan;
+    if (t < kStats) o[(int64_t)t * G + g] = nan;
     if (t == 0) S.cnt[g] = 0;
     return;
   }
-  // exact moments; the ratio of every instance into xs
-  u128 sx = 0, sy = 0, sxx = 0, syy = 0, sxy = 0;
-  uint64_t cyc = 0, busy = 0, flops = 0;
-  bool big = false;
-  for (int64_t i = t; i < m; i += kStatT) {
-    const uint32_t r = list[b + i];
-    const uint64_t d = (uint64_t)A.dur[r];
-    const uint64_t ov = (uint64_t)A.ovl[r];
-    const uint64_t x = (ov << 30) / d;
-    const uint64_t y = d + (uint64_t)A.gap[r];
-    if (y >> 34) big = true;
-    xs[b + i] = (uint32_t)x;
-    sx += x;
-    sy += y;
-    sxx += (u128)x * x;
-    syy += (u128)y * y;
-    sxy += (u128)x * y;
-    if (A.nc >= 16) {
-      cyc += A.ctr[0 * A.cap + r];
-      busy += A.ctr[1 * A.cap + r];
-      flops += A.ctr[11 * A.cap + r];
-    }
-  }
-  if (__ballot(big) != 0 && lane_id() == 0)
-    atomicOr(status, CHOPPER_ST_RANGE);
-  sx = block_sum_u128(sx, s_v);
-  sy = block_sum_u128(sy, s_v);
-  sxx = block_sum_u128(sxx, s_v);
-  syy = block_sum_u128(syy, s_v);
-  sxy = block_sum_u128(sxy, s_v);
-  cyc = (uint64_t)block_sum_u128(cyc, s_v);
-  busy = (uint64_t)block_sum_u128(busy, s_v);
-  flops = (uint64_t)block_sum_u128(flops, s_v);
-  // order statistics of the ratio: the smallest, v[(m-1)/4], v[(m-1)/2],
-  // v[m/2], v[3(m-1)/4] and the largest, two ranks per radix selection
-  const int64_t want[6] = {0, (m - 1) / 4, (m - 1) / 2, m / 2,
-                           3 * (m - 1) / 4, m - 1};
-  uint32_t got[6];
-  for (int pair = 0; pair < 3; ++pair) {
-    int64_t rank[2] = {want[2 * pair], want[2 * pair + 1]};
-    uint32_t pre[2] = {0, 0};
-    for (int sh = 24; sh >= 0; sh -= 8) {
-      for (int q = t; q < 512; q += kStatT) (&s_hist[0][0])[q] = 0;
-      __syncthreads();
-      const int hs = sh + 8;
-      for (int64_t i = t; i < m; i += kStatT) {
-        const uint32_t k = xs[b + i];
-        const uint32_t dig = (k >> sh) & 255u;
+  uint64_t acc[kSums];
 #pragma unroll
-        for (int rr = 0; rr < 2; ++rr)
-          if (hs >= 32 || (k >> hs) == (pre[rr] >> hs))
-            atomicAdd(&s_hist[rr][dig], 1u);
-      }
-      __syncthreads();
-      if (t < 2 * kWave) {
-        const int rr = t / kWave, lane = lane_id();
-        uint32_t h[4], sum = 0;
+  for (int k = 0; k < kSums; ++k) acc[k] = 0;
+  for (uint32_t c = coff[g] + t; c < coff[g + 1]; c += kBlock)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          h[q] = s_hist[rr][lane * 4 + q];
-          sum += h[q];
-        }
-        const uint32_t incl = wave_incl(sum, OpAdd(), 0u);
-        const uint64_t past = __ballot((int64_t)incl > rank[rr]);
-        const int ln = __ffsll((long long)past) - 1;
-        if (lane == ln) {
-          int64_t under = incl - sum;
-          int dsel = lane * 4 + 3;
-          for (int q = 0; q < 4; ++q) {
-            if (under + (int64_t)h[q] > rank[rr]) {
-              dsel = lane * 4 + q;
-              break;
-            }
-            under += h[q];
-          }
-          s_sel[2 * rr] = (uint32_t)dsel;
-          s_sel[2 * rr + 1] = (uint32_t)under;   // candidates below it
-        }
-      }
-      __syncthreads();
-#pragma unroll
-      for (int rr = 0; rr < 2; ++rr) {
-        pre[rr] |= s_sel[2 * rr] << sh;
-        rank[rr] -= (int64_t)s_sel[2 * rr + 1];
-      }
-      __syncthreads();
-    }
-    got[2 * pair] = pre[0];
-    got[2 * pair + 1] = pre[1];
-  }
+    for (int k = 0; k < kSums; ++k) acc[k] += part[(int64_t)c * kSums + k];
+  block_sums(acc, s_w, s_tot);
+  __syncthreads();
   if (t != 0) return;
-  // the derived values, in the same IEEE operations as their definition
-  double* o = S.out;
   for (int k = 0; k < kStats; ++k) o[(int64_t)k * G + g] = nan;
   S.cnt[g] = m;
+  const i128 sx = (i128)s_tot[0], sy = (i128)s_tot[1];
+  const i128 sxx = ((i128)s_tot[3] << 32) + (i128)s_tot[2];
+  const i128 syy = ((i128)s_tot[5] << 32) + (i128)s_tot[4];
+  const i128 sxy = ((i128)s_tot[7] << 32) + (i128)s_tot[6];
+  const uint64_t cyc = s_tot[8], busy = s_tot[9], flops = s_tot[10];
   const i128 im = (i128)m;
-  const i128 cov = im * (i128)sxy - (i128)sx * (i128)sy;
-  const i128 vx = im * (i128)sxx - (i128)sx * (i128)sx;
-  const i128 vy = im * (i128)syy - (i128)sy * (i128)sy;
+  const i128 cov = im * sxy - sx * sy;
+  const i128 vx = im * sxx - sx * sx;
+  const i128 vy = im * syy - sy * sy;
   const double dm = (double)m;
   if (m >= 2 && vx != 0 && vy != 0)
     o[0 * G + g] = i128_to_double(cov) /
@@ -291,25 +430,26 @@ __global__ __launch_bounds__(kStatT) void k_stats_group(
   double slope = nan, a = nan;
   if (vx != 0) {
     slope = i128_to_double(cov) / i128_to_double(vx);
-    a = (i128_to_double((i128)sy) - slope * i128_to_double((i128)sx)) / dm;
+    a = (i128_to_double(sy) - slope * i128_to_double(sx)) / dm;
   }
   o[1 * G + g] = slope;
   o[2 * G + g] = a;
   const double d0 = a, d50 = a + slope * 536870912.0;
   o[3 * G + g] = d0;
   o[4 * G + g] = d50;
+  const uint32_t* v = spre + g * kRanks;
   const double q = 1.0 / 1073741824.0;
-  o[5 * G + g] = (double)got[0] * q;
-  o[6 * G + g] = (double)got[1] * q;
-  o[7 * G + g] = ((double)got[2] + (double)got[3]) / 2.0 * q;
-  o[8 * G + g] = (double)got[4] * q;
-  o[9 * G + g] = (double)got[5] * q;
-  const double dact = i128_to_double((i128)sy) / dm;
+  o[5 * G + g] = (double)v[0] * q;
+  o[6 * G + g] = (double)v[1] * q;
+  o[7 * G + g] = ((double)v[2] + (double)v[3]) / 2.0 * q;
+  o[8 * G + g] = (double)v[4] * q;
+  o[9 * G + g] = (double)v[5] * q;
+  const double dact = i128_to_double(sy) / dm;
   o[10 * G + g] = dact;
   const double ovr_ov = d50 / d0;
   o[14 * G + g] = ovr_ov;
-  const double fg = S.have_f ? S.f_gemm[g % A.O] : nan;
-  if (A.nc >= 16) {
+  const double fg = S.have_f ? S.f_gemm[g % O] : nan;
+  if (nc >= 16) {
     const double dpeak = (double)cyc * 1000.0 / S.freq_peak / dm;
     o[11 * G + g] = dpeak;
     o[12 * G + g] = 1.0 / ((double)busy / (double)cyc);
@@ -345,43 +485,70 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
   if (mk->n > 0 && !mk->label) return CHOPPER_EINVAL;
   const int G = P * O;
   const int64_t cap = rows->cap;
-  auto layout = [&](Scratch& sc, uint32_t*& key, uint32_t*& gcnt,
-                    uint32_t*& off, uint32_t*& cur, uint32_t*& list,
-                    uint32_t*& xs) {
-    key = sc.take<uint32_t>(cap);
-    gcnt = sc.take<uint32_t>(G);
-    off = sc.take<uint32_t>(G + 1);
-    cur = sc.take<uint32_t>(G);
-    list = sc.take<uint32_t>(cap);
-    xs = sc.take<uint32_t>(cap);
+  const int64_t ncs = n_counters >= 16 ? 3 * cap : 1;
+  const int64_t nchunk = ceil_div(cap, kChunk) + G;
+  const int64_t nh = (int64_t)G * kRanks * 256;
+  struct Bufs {
+    uint32_t *key, *gcnt, *off, *cur, *coff, *xs, *ghist, *spre;
+    uint64_t *ys, *cs, *part;
+    int64_t* srank;
+  } B;
+  auto layout = [&](Scratch& sc) {
+    B.key = sc.take<uint32_t>(cap);
+    B.gcnt = sc.take<uint32_t>(G);
+    B.off = sc.take<uint32_t>(G + 1);
+    B.cur = sc.take<uint32_t>(G);
+    B.coff = sc.take<uint32_t>(G + 1);
+    B.xs = sc.take<uint32_t>(cap);
+    B.ys = sc.take<uint64_t>(cap);
+    B.cs = sc.take<uint64_t>(ncs);
+    B.part = sc.take<uint64_t>(nchunk * kSums);
+    B.ghist = sc.take<uint32_t>(nh);
+    B.spre = sc.take<uint32_t>((int64_t)G * kRanks);
+    B.srank = sc.take<int64_t>((int64_t)G * kRanks);
   };
-  uint32_t *key, *gcnt, *off, *cur, *list, *xs;
   Scratch probe(nullptr);
-  layout(probe, key, gcnt, off, cur, list, xs);
+  layout(probe);
   int rc = scratch_check(scratch, scratch_bytes, probe.used);
   if (rc != 0) return rc > 0 ? CHOPPER_OK : rc;
   if (!status) return CHOPPER_EINVAL;
   hipStream_t s = (hipStream_t)stream;
   Scratch sc(scratch);
-  layout(sc, key, gcnt, off, cur, list, xs);
+  layout(sc);
   StatArgs A{rows->level_offset, rows->path, rows->kind, rows->dur,
              rows->gap, rows->ovl, rows->ctr, cap, n_counters,
              spec->phase_level, spec->op_level, mk->label, mk->n, P, O};
   StatOut S{out, cnt, spec->freq_peak_mhz, spec->tpt_peak,
             spec->f_gemm != nullptr, {0}};
   for (int o = 0; o < O && spec->f_gemm; ++o) S.f_gemm[o] = spec->f_gemm[o];
-  CHOPPER_HIP(launch("stats_clear", k_stats_clear, grid_for(G, kBlock),
-                     dim3(kBlock), s, gcnt, G));
-  const unsigned rb = (unsigned)ceil_div(cap > 0 ? cap : 1, (int64_t)kBlock);
-  CHOPPER_HIP(launch("stats_keys", k_stats_keys, dim3(rb), dim3(kBlock), s,
-                     A, key, gcnt));
-  CHOPPER_HIP(launch("stats_offsets", k_stats_offsets, dim3(1),
-                     dim3(kStatT), s, (const uint32_t*)gcnt, G, off, cur));
-  CHOPPER_HIP(launch("stats_scatter", k_stats_scatter, dim3(rb), dim3(kBlock),
-                     s, A, (const uint32_t*)key, cur, list));
-  CHOPPER_HIP(launch("stats_group", k_stats_group, dim3((unsigned)G),
-                     dim3(kStatT), s, A, (const uint32_t*)off,
-                     (const uint32_t*)list, xs, S, status));
+  CHOPPER_HIP(launch("stats_clear", k_stats_clear, grid_for(nh, kBlock),
+                     dim3(kBlock), s, B.gcnt, G, B.ghist, nh));
+  const dim3 rb((unsigned)ceil_div(cap > 0 ? cap : 1, (int64_t)kRowSpan));
+  CHOPPER_HIP(launch("stats_keys", k_stats_keys, rb, dim3(kStatT), s, A,
+                     B.key, B.gcnt));
+  CHOPPER_HIP(launch("stats_offsets", k_stats_offsets, dim3(1), dim3(kStatT),
+                     s, (const uint32_t*)B.gcnt, G, B.off, B.cur, B.coff,
+                     B.spre, B.srank));
+  CHOPPER_HIP(launch("stats_scatter", k_stats_scatter, rb, dim3(kStatT), s,
+                     A, (const uint32_t*)B.key, B.cur, B.xs, B.ys, B.cs, cap,
+                     status));
+  for (int pass = 0; pass < 4; ++pass) {
+    const int sh = 24 - 8 * pass;
+    CHOPPER_HIP(launch("stats_pass",
+                       pass == 0 ? k_stats_pass<true> : k_stats_pass<false>,
+                       dim3((unsigned)nchunk), dim3(kStatT), s,
+                       (const uint32_t*)B.off, (const uint32_t*)B.coff, G,
+                       (const uint32_t*)B.xs, (const uint64_t*)B.ys,
+                       (const uint64_t*)B.cs, cap, n_counters,
+                       (const uint32_t*)B.spre, sh, B.ghist, B.part));
+    CHOPPER_HIP(launch("stats_select", k_stats_select, dim3((unsigned)G),
+                       dim3(kRanks * kWave), s, (const uint32_t*)B.gcnt, sh,
+                       pass == 0, B.ghist, B.spre, B.srank));
+  }
+  CHOPPER_HIP(launch("stats_final", k_stats_final, dim3((unsigned)G),
+                     dim3(kBlock), s, (const uint32_t*)B.gcnt,
+                     (const uint32_t*)B.coff, G, O, n_counters,
+                     (const uint64_t*)B.part, (const uint32_t*)B.spre, S));
   return CHOPPER_OK;
 }
 
