@@ -99,12 +99,6 @@ __global__ __launch_bounds__(kDenseT) void k_join_dense(const uint8_t* pres,
   if (t == 0) *count = tot;
 }
 
-// the entry index as the pass's time
-__global__ void k_join_iota(int64_t m, int64_t* t) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < m) t[i] = i;
-}
-
 // Items of a (gpu, stream)-ordered sequence: key = (gpu, stream, label).
 struct Seq {
   const uint32_t* idx;     // sequence position -> item
@@ -118,34 +112,92 @@ struct Seq {
   }
 };
 
-// run heads: an item with an iteration whose predecessor differs in
-// (gpu, stream, label) -- items without an iteration belong to no run, and
-// one of them between two items of a label starts a second run of it
-__global__ void k_join_heads(Seq S, uint32_t* head) {
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= S.n) return;
-  const uint32_t b = S.idx[p];
-  uint32_t h = 0;
-  if (S.lab[b] != kNone) {
-    h = 1;
-    if (p > 0) {
-      const uint32_t a = S.idx[p - 1];
-      h = (S.cls(a) != S.cls(b) || S.lab[a] != S.lab[b]) ? 1u : 0u;
-    }
-  }
-  head[p] = h;
+// key of a sequence item: label | class << 32 | pass class << 48
+__device__ inline uint64_t item_key(const Seq& S, const uint8_t* pcls,
+                                    uint32_t i) {
+  return (uint64_t)S.lab[i] | (uint64_t)S.cls(i) << 32 |
+         (pcls ? (uint64_t)pcls[i] << 48 : 0ull);
 }
 
-// run table: start position, (gpu, stream) and label of every run
-__global__ void k_join_runs(Seq S, const uint32_t* head, const uint32_t* excl,
-                            uint32_t* rstart, uint32_t* rcls,
-                            uint32_t* rlab) {
+// run heads: an item with an iteration whose predecessor differs in
+// (gpu, stream, label) -- items without an iteration belong to no run, and
+// one of them between two items of a label starts a second run of it.  The
+// key of every position is kept for the later passes, which then read it
+// in sequence order.
+// The heads of a block of kBlock positions are also counted (tcnt), so that
+// the run numbers come from a scan of the block counts.
+__global__ __launch_bounds__(kBlock) void k_join_heads(Seq S,
+                                                       const uint8_t* pcls,
+                                                       uint32_t* head,
+                                                       uint64_t* key,
+                                                       uint32_t* tcnt) {
+  __shared__ uint32_t s_c[kWavesPerBlock];
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= S.n || !head[p]) return;
-  const uint32_t r = excl[p], i = S.idx[p];
+  const bool ok = p < S.n;
+  const uint64_t kb = ok ? item_key(S, pcls, S.idx[p]) : 0ull;
+  // the predecessor's key from the lane below; lane 0 loads it
+  uint64_t ka = wave_shr1_any((uint64_t)0, kb);
+  if (lane_id() == 0 && ok && p > 0) ka = item_key(S, pcls, S.idx[p - 1]);
+  const uint64_t kMask = 0x0000FFFFFFFFFFFFull;    // class and label
+  uint32_t h = 0;
+  if (ok && (uint32_t)kb != kNone) h = (p == 0 || ((ka ^ kb) & kMask) != 0);
+  if (ok) {
+    head[p] = h;
+    key[p] = kb;
+  }
+  const uint32_t c = (uint32_t)__popcll(__ballot(h != 0));
+  if (lane_id() == 0) s_c[threadIdx.x / kWave] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t sum = 0;
+    for (int w = 0; w < kWavesPerBlock; ++w) sum += s_c[w];
+    tcnt[blockIdx.x] = sum;
+  }
+}
+
+// run table: start position, (gpu, stream) and label of every run, the run
+// number of a head being the heads before it (block prefix tpre + the
+// heads below it in its block); excl (optional) gets that count at every
+// position
+__global__ __launch_bounds__(kBlock) void k_join_runs(
+    int64_t n, const uint32_t* head, const uint32_t* tpre,
+    const uint64_t* key, uint32_t* rstart, uint32_t* rcls, uint32_t* rlab,
+    uint32_t* excl) {
+  __shared__ uint32_t s_c[kWavesPerBlock];
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint32_t h = p < n ? head[p] : 0u;
+  const uint64_t m = __ballot(h != 0);
+  const int w = threadIdx.x / kWave;
+  if (lane_id() == 0) s_c[w] = (uint32_t)__popcll(m);
+  __syncthreads();
+  uint32_t r = tpre[blockIdx.x] + lanes_below(m);
+  for (int q = 0; q < w; ++q) r += s_c[q];
+  if (p >= n) return;
+  if (excl) excl[p] = r;
+  if (!h) return;
+  const uint64_t k = key[p];
   rstart[r] = (uint32_t)p;
-  rcls[r] = S.cls(i);
-  rlab[r] = S.lab[i];
+  rcls[r] = (uint32_t)(k >> 32) & 0xFFFFu;
+  rlab[r] = (uint32_t)k;
+}
+
+// run and ordinal of every record, stored at the record (NONE: no
+// iteration)
+__global__ void k_join_rec_pos(int64_t n, const uint32_t* order,
+                               const uint32_t* head, const uint32_t* excl,
+                               const uint64_t* key, const uint32_t* rstart,
+                               uint32_t* rrun, uint32_t* rord) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n) return;
+  const uint32_t r = order[p];
+  if ((uint32_t)key[p] == kNone) {
+    rrun[r] = kNone;
+    rord[r] = 0;
+    return;
+  }
+  const uint32_t run = excl[p] + head[p] - 1;
+  rrun[r] = run;
+  rord[r] = (uint32_t)p - rstart[run];
 }
 
 // JOIN_ORDER: a run whose label is not above that of the previous run of
@@ -185,40 +237,40 @@ struct PassCols {
   int32_t dst[16];
 };
 
-// every record: its entry in the pass (run start + ordinal), the class
-// check, and the pass's columns (0 where nothing matches)
+// every record, in input order: its entry in the pass (run start +
+// ordinal), the key and class check, and the pass's columns (0 where
+// nothing matches)
 __global__ __launch_bounds__(kBlock) void k_join_gather(
-    Seq R, const uint8_t* cls, const uint32_t* head, const uint32_t* excl,
-    const uint32_t* rstart, const uint32_t* match, const uint32_t* qstart,
-    const uint32_t* nq, int64_t m, const uint32_t* qorder, Seq Q,
-    const uint8_t* pcls, const uint64_t* values, PassCols C,
-    uint64_t* counters, uint8_t* matched, uint32_t* status) {
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t n, const uint32_t* rrun, const uint32_t* rord, const uint8_t* cls,
+    const uint32_t* rcls, const uint32_t* rlab, const uint32_t* match,
+    const uint32_t* qstart, const uint32_t* nq, int64_t m,
+    const uint32_t* qorder, const uint64_t* qkey, const uint64_t* values,
+    PassCols C, uint64_t* counters, uint8_t* matched, uint32_t* status) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   bool miss = false;
-  if (p < R.n) {
-    const uint32_t r = R.idx[p];
+  if (r < n) {
+    const uint32_t run = rrun[r];
     int64_t q = -1;
-    if (R.lab[r] != kNone) {
-      const uint32_t run = excl[p] + head[p] - 1;
+    if (run != kNone) {
       const uint32_t qr = match[run];
       if (qr != kNone) {
-        const int64_t ord = p - (int64_t)rstart[run];
-        const int64_t q0 = qstart[qr];
+        const int64_t pos = (int64_t)qstart[qr] + rord[r];
         const int64_t q1 =
             (int64_t)qr + 1 < (int64_t)*nq ? (int64_t)qstart[qr + 1] : m;
         // the entry at the ordinal is the record's only if it still has the
         // run's key (entries without an iteration may follow the run)
-        if (q0 + ord < q1) {
-          const uint32_t e = qorder[q0 + ord];
-          if (Q.cls(e) == R.cls(r) && Q.lab[e] == R.lab[r] &&
-              pcls[e] == cls[r])
-            q = e;
+        if (pos < q1) {
+          const uint64_t k = qkey[pos];
+          if ((uint32_t)k == rlab[run] &&
+              ((uint32_t)(k >> 32) & 0xFFFFu) == rcls[run] &&
+              (uint32_t)(k >> 48) == cls[r])
+            q = qorder[pos];
         }
       }
       miss = q < 0;
     }
     for (int c = 0; c < C.n_cols; ++c)
-      counters[(int64_t)C.dst[c] * R.n + r] =
+      counters[(int64_t)C.dst[c] * n + r] =
           q >= 0 ? values[(int64_t)c * m + q] : 0ull;
     if (q >= 0) matched[r] |= (uint8_t)(1u << C.bit);
   }
@@ -273,16 +325,19 @@ extern "C" int chopper_join_counters(
     v.push_back(sc.take<uint32_t>(4));             // 7 totals (R, Q, C)
     v.push_back(sc.take<uint32_t>(
         scan_scratch_elems(n > mmax ? n : mmax)));  // 8 scan tmp
-    v.push_back(sc.take<int64_t>(mmax));           // 9 pass times
+    v.push_back(sc.take<uint64_t>(n > mmax ? n : mmax));  // 9 keys
     v.push_back(sc.take<uint8_t>(65536));          // 10 presence
     v.push_back(sc.take<uint16_t>(65536));         // 11 class map
     v.push_back(sc.take<uint32_t>(mmax));          // 12 qorder
     v.push_back(sc.take<uint32_t>(256 + 1));       // 13 class offsets
     v.push_back(sc.take<uint32_t>(mmax));          // 14 q heads
-    v.push_back(sc.take<uint32_t>(mmax));          // 15 q excl
+    v.push_back(sc.take<uint32_t>(
+        2 * (ceil_div(n > mmax ? n : mmax, kBlock) + 1)));  // 15 block heads
     v.push_back(sc.take<uint32_t>(mmax + 1));      // 16 qstart
     v.push_back(sc.take<uint32_t>(mmax + 1));      // 17 qcls
     v.push_back(sc.take<uint32_t>(mmax + 1));      // 18 qlab
+    v.push_back(sc.take<uint32_t>(n));             // 19 run of each record
+    v.push_back(sc.take<uint32_t>(n));             // 20 its ordinal
   };
   std::vector<void*> v;
   Scratch probe(nullptr);
@@ -303,11 +358,14 @@ extern "C" int chopper_join_counters(
            *rlab = (uint32_t*)v[5], *match = (uint32_t*)v[6];
   uint32_t* tot = (uint32_t*)v[7];
   uint32_t* tmp = (uint32_t*)v[8];
-  int64_t* ptime = (int64_t*)v[9];
+  uint64_t* key = (uint64_t*)v[9];
+  uint32_t *rrun = (uint32_t*)v[19], *rord = (uint32_t*)v[20];
   uint8_t* pres = (uint8_t*)v[10];
   uint16_t* cmap = (uint16_t*)v[11];
   uint32_t *qorder = (uint32_t*)v[12], *coff = (uint32_t*)v[13];
-  uint32_t *qhead = (uint32_t*)v[14], *qexcl = (uint32_t*)v[15];
+  uint32_t* qhead = (uint32_t*)v[14];
+  uint32_t* tcnt = (uint32_t*)v[15];
+  uint32_t* tpre = tcnt + ceil_div(n > mmax ? n : mmax, kBlock) + 1;
   uint32_t *qstart = (uint32_t*)v[16], *qcls = (uint32_t*)v[17],
            *qlab = (uint32_t*)v[18];
   const dim3 gn = grid_for(n, kBlock);
@@ -337,39 +395,44 @@ extern "C" int chopper_join_counters(
                      n, idx + (int64_t)iter_level * n, nm, mk->label, rlabv));
   const Seq R{order, rec->gpu, rec->stream, rlabv, cmap, n};
   CHOPPER_HIP(launch("join_heads", k_join_heads, gn, dim3(kBlock), s, R,
-                     head));
-  CHOPPER_HIP(exclusive_scan<uint32_t>(head, excl, n, tmp, tot, s));
-  CHOPPER_HIP(launch("join_runs", k_join_runs, gn, dim3(kBlock), s, R,
-                     (const uint32_t*)head, (const uint32_t*)excl, rstart,
-                     rcls, rlab));
+                     (const uint8_t*)nullptr, head, key, tcnt));
+  CHOPPER_HIP(exclusive_scan<uint32_t>(tcnt, tpre, (int64_t)gn.x, tmp, tot,
+                                       s));
+  CHOPPER_HIP(launch("join_runs", k_join_runs, gn, dim3(kBlock), s, n,
+                     (const uint32_t*)head, (const uint32_t*)tpre,
+                     (const uint64_t*)key, rstart, rcls, rlab, excl));
   CHOPPER_HIP(launch("join_order", k_join_order, gn, dim3(kBlock), s,
                      (const uint32_t*)tot, (const uint32_t*)rcls,
                      (const uint32_t*)rlab, status));
+  CHOPPER_HIP(launch("join_runs", k_join_rec_pos, gn, dim3(kBlock), s, n,
+                     order, (const uint32_t*)head, (const uint32_t*)excl,
+                     (const uint64_t*)key, (const uint32_t*)rstart, rrun,
+                     rord));
   for (int p = 0; p < n_passes; ++p) {
     const chopper_counter_pass& P = passes[p];
     const int64_t m = P.n;
     PassCols C{P.n_cols, p, {0}};
     for (int c = 0; c < P.n_cols; ++c) C.dst[c] = P.dst[c];
     if (m > 0) {
-      // stable partition of the pass by class, in its own order: with the
-      // entry index as time each class is then in time order already
-      CHOPPER_HIP(launch("join_pass_prep", k_join_iota, grid_for(m, kBlock),
-                         dim3(kBlock), s, m, ptime));
+      // stable partition of the pass by class, in its own order (the
+      // pass's order is its time: the partition needs no time key)
       ClassSortLayout L = SL;
       L.n = m;
       L.ntiles = sort_tiles(m);
       bool range_err = false;
-      KeyRecStream kq{P.gpu, P.stream, ptime, cmap, (int)nclass + 1};
+      KeyRecStream kq{P.gpu, P.stream, nullptr, cmap, (int)nclass + 1};
       rc = class_sort(kq, L, qorder, coff, &range_err, s, 1);
       if (rc != CHOPPER_OK) return rc;
       const Seq Q{qorder, P.gpu, P.stream, P.label, cmap, m};
       const dim3 gm = grid_for(m, kBlock);
       CHOPPER_HIP(launch("join_heads", k_join_heads, gm, dim3(kBlock), s, Q,
-                         qhead));
-      CHOPPER_HIP(exclusive_scan<uint32_t>(qhead, qexcl, m, tmp, tot + 1, s));
-      CHOPPER_HIP(launch("join_runs", k_join_runs, gm, dim3(kBlock), s, Q,
-                         (const uint32_t*)qhead, (const uint32_t*)qexcl,
-                         qstart, qcls, qlab));
+                         P.cls, qhead, key, tcnt));
+      CHOPPER_HIP(exclusive_scan<uint32_t>(tcnt, tpre, (int64_t)gm.x, tmp,
+                                           tot + 1, s));
+      CHOPPER_HIP(launch("join_runs", k_join_runs, gm, dim3(kBlock), s, m,
+                         (const uint32_t*)qhead, (const uint32_t*)tpre,
+                         (const uint64_t*)key, qstart, qcls, qlab,
+                         (uint32_t*)nullptr));
       CHOPPER_HIP(launch("join_order", k_join_order, gm, dim3(kBlock), s,
                          (const uint32_t*)(tot + 1), (const uint32_t*)qcls,
                          (const uint32_t*)qlab, status));
@@ -381,12 +444,12 @@ extern "C" int chopper_join_counters(
                        (const uint32_t*)tot, (const uint32_t*)rcls,
                        (const uint32_t*)rlab, (const uint32_t*)(tot + 1),
                        (const uint32_t*)qcls, (const uint32_t*)qlab, match));
-    CHOPPER_HIP(launch("join_gather", k_join_gather, gn, dim3(kBlock), s, R,
-                       rec->cls, (const uint32_t*)head, (const uint32_t*)excl,
-                       (const uint32_t*)rstart, (const uint32_t*)match,
-                       (const uint32_t*)qstart, (const uint32_t*)(tot + 1),
-                       m, (const uint32_t*)qorder,
-                       Seq{qorder, P.gpu, P.stream, P.label, cmap, m}, P.cls,
+    CHOPPER_HIP(launch("join_gather", k_join_gather, gn, dim3(kBlock), s, n,
+                       (const uint32_t*)rrun, (const uint32_t*)rord, rec->cls,
+                       (const uint32_t*)rcls, (const uint32_t*)rlab,
+                       (const uint32_t*)match, (const uint32_t*)qstart,
+                       (const uint32_t*)(tot + 1), m,
+                       (const uint32_t*)qorder, (const uint64_t*)key,
                        P.values, C, counters_out, matched_out, status));
   }
   return CHOPPER_OK;
