@@ -277,3 +277,47 @@ def test_launch_split_scratch_query_and_argument_errors(ch):
     assert lib.chopper_launch_split(ctypes.byref(rec), None, fake, fake, fake,
                                     fake, fake, None, ctypes.byref(sz), None,
                                     None) == -1
+
+
+def test_op_stats_scratch_query_and_argument_errors(ch):
+    """chopper_op_stats answers the scratch query without GPU work, sizes
+    its scratch from the row capacity, and rejects bad specs synchronously."""
+    lib, b = ch.lib, ch.binding
+    fake = ctypes.c_void_p(0x1000)
+    mk = b.Markers()
+    mk.n, mk.depth = 500, 4
+    mk.gpu = mk.level = mk.start_ns = mk.end_ns = mk.label = fake
+    rows = b.Rows()
+    rows.cap = 10
+    for k in ("level_offset", "path", "gpu", "kind", "n", "dur", "gap", "ovl",
+              "tmin", "tmax", "first", "ctr"):
+        setattr(rows, k, fake)
+
+    def call(spec, depth=4, nc=16, out=fake, cap=10):
+        rows.cap = cap
+        sz = ctypes.c_size_t(0)
+        rc = lib.chopper_op_stats(ctypes.byref(rows), depth, nc,
+                                  ctypes.byref(mk), ctypes.byref(spec), out,
+                                  fake, None, ctypes.byref(sz), None, None)
+        return rc, sz.value
+
+    good = b.StatsSpec(1, 3, 3, 64, 2100.0, 1.0, None)
+    rc, sz = call(good)
+    assert rc == 0 and sz > 0
+    rc2, sz2 = call(good, cap=10**6)
+    assert rc2 == 0 and sz2 > sz + 4 * 10**6
+    for bad in (b.StatsSpec(1, 4, 3, 64, 2100.0, 1.0, None),   # level >= depth
+                b.StatsSpec(-1, 3, 3, 64, 2100.0, 1.0, None),
+                b.StatsSpec(1, 3, 0, 64, 2100.0, 1.0, None),   # no phase
+                b.StatsSpec(1, 3, 17, 64, 2100.0, 1.0, None),  # > 16 phases
+                b.StatsSpec(1, 3, 3, 0, 2100.0, 1.0, None),
+                b.StatsSpec(1, 3, 3, 129, 2100.0, 1.0, None)):  # > 128 ops
+        assert call(bad)[0] == -1
+    assert call(good, depth=5)[0] == -1          # deeper than the markers
+    assert call(good, nc=17)[0] == -1
+    assert call(good, out=None)[0] == -1
+    sz = ctypes.c_size_t(8)
+    assert lib.chopper_op_stats(ctypes.byref(rows), 4, 16, ctypes.byref(mk),
+                                ctypes.byref(good), fake, fake,
+                                ctypes.c_void_p(0x10000), ctypes.byref(sz),
+                                fake, None) == -2

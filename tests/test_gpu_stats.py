@@ -80,3 +80,27 @@ def test_stats_micro(ch, seed):
                           n_ops=50)
     check(got, ref, f"micro {seed}")
     assert got[1].max() >= 2
+
+
+def test_stats_max_groups(ch):
+    say("op stats: 16 phases x 128 operations, labels past both limits")
+    tr = tg.make_micro(7, n_gpus=4, n_kernels=3000, n_streams=2, depth=3,
+                       span=30000, n_counters=16)
+    rng = np.random.default_rng(7)
+    top = np.where(tr.m_level == 0, 18, 135)
+    tr.m_label = (rng.random(tr.m_label.shape[0]) * top).astype(
+        tr.m_label.dtype)
+    got, ref = stats_both(ch, tr, phase_level=0, op_level=2, n_phases=16,
+                          n_ops=128, f_gemm=np.arange(1, 129) * 1e9)
+    check(got, ref, "16 x 128")
+    assert got[1].sum() > 0
+
+
+def test_stats_no_instances(ch):
+    say("op stats: every operation label out of range")
+    tr = tg.make_micro(8, n_gpus=2, n_kernels=400, depth=3, span=5000)
+    tr.m_label = np.full_like(tr.m_label, 200)
+    got, ref = stats_both(ch, tr, phase_level=1, op_level=2, n_phases=2,
+                          n_ops=8)
+    check(got, ref, "no instances")
+    assert got[1].sum() == 0 and np.isnan(got[0]).all()
