@@ -5,7 +5,10 @@ Clocks, alignment, attribution, overlap and bubbles are compared with the C
 oracle over every record and marker; the two orders with numpy's stable
 lexsort; the aggregated rows of every level with the vectorized brute-force
 grouping of tests/brute.py (pinned to the oracle on CPU); the derived ratios
-by recomputing the same IEEE divisions in numpy."""
+by recomputing the same IEEE divisions in numpy; the views, the overlap
+statistics, the launch split and (on the 20M-record trace) the counter-pass
+join with the oracle.  One module-scoped run per trace feeds short tests, so
+that none of them is silent for long."""
 import sys
 import time
 
@@ -44,53 +47,101 @@ def same(a, b, what):
 ITERS = {3: 800, 4: 2035}     # iterations of the two traces
 
 
-@pytest.mark.parametrize("cid", [3, 4])
-def test_full_size_parity(ch, cid):
-    t0 = time.time()
-    tr = tg.make_config(cid, with_truth=False)
-    say(f"config {cid}: {tr.n} records {tr.n_markers} markers "
-        f"({time.time() - t0:.0f}s)")
-    pipe = ch.Pipeline(ch.DeviceTrace(tr, "cuda"))
-    pipe.status.zero_()
-    pipe.step()
-    got = pipe.results()
+class Full:
+    """The trace, the GPU run and the oracle's results of one full-size
+    configuration, computed once per module and in pieces, so that each
+    test ends (and reports) within about a minute."""
+
+    def __init__(self, ch, cid):
+        self.ch, self.cid, self.t0 = ch, cid, time.time()
+        tr = tg.make_config(cid, with_truth=False)
+        self.tr = tr
+        say(f"config {cid}: {tr.n} records {tr.n_markers} markers "
+            f"({self.el()}s)")
+        self.pipe = ch.Pipeline(ch.DeviceTrace(tr, "cuda"))
+        self.pipe.status.zero_()
+        self.pipe.step()
+        self.got = self.pipe.results()
+        say(f"gpu done ({self.el()}s)")
+        self._memo = {}
+
+    def el(self):
+        return f"{time.time() - self.t0:.0f}"
+
+    def need(self, what):
+        if what not in self._memo:
+            self._memo[what] = getattr(self, "_" + what)()
+        return self._memo[what]
+
+    def _aligned(self):
+        tr, G = self.tr, self.tr.n_gpus
+        x0, c, d, rc = oracle.fit(tr.a_gpu, tr.a_local, tr.a_ref, G)
+        s, _ = oracle.transform(tr.gpu, tr.start, G, x0, c, d)
+        e, _ = oracle.transform(tr.gpu, tr.end, G, x0, c, d)
+        ms, _ = oracle.transform(tr.m_gpu, tr.m_start, G, x0, c, d)
+        me, _ = oracle.transform(tr.m_gpu, tr.m_end, G, x0, c, d)
+        return dict(x0=x0, c=c, d=d, rc=rc, s=s, e=e, ms=ms, me=me)
+
+    def _idx(self):
+        tr, a = self.tr, self.need("aligned")
+        return oracle.attribute(tr.gpu, a["s"], tr.m_gpu, tr.m_level, a["ms"],
+                                a["me"], tr.depth, tr.n_gpus)
+
+    def _ov(self):
+        tr, a = self.tr, self.need("aligned")
+        return oracle.overlap(tr.gpu, tr.stream, tr.cls, a["s"], a["e"],
+                              tr.m_gpu, a["ms"], a["me"], tr.n_gpus)
+
+    def _rows(self):
+        tr, a = self.tr, self.need("aligned")
+        idx, ov = self.need("idx")[0], self.need("ov")
+        levels = list(range(tr.depth)) + [100, 101]
+        return levels, brute.aggregate_numpy(
+            tr.gpu, tr.cls, a["s"], a["e"], idx, ov["gap"], ov["ovl"],
+            tr.counters, tr.depth, levels)
+
+
+@pytest.fixture(scope="module", params=[3, 4])
+def full(ch, request):
+    return Full(ch, request.param)
+
+
+def test_full_align(full):
+    tr, got, a = full.tr, full.got, full.need("aligned")
     assert got["status"] == 0, got["status"]
-    say(f"gpu done ({time.time() - t0:.0f}s)")
-    G = tr.n_gpus
-    x0, c, d, rc = oracle.fit(tr.a_gpu, tr.a_local, tr.a_ref, G)
-    assert rc == 0
-    same(got["x0"], x0, "x0")
-    same(got["c"], c, "c")
-    same(got["d"], d, "d")
-    s, _ = oracle.transform(tr.gpu, tr.start, G, x0, c, d)
-    e, _ = oracle.transform(tr.gpu, tr.end, G, x0, c, d)
-    ms, _ = oracle.transform(tr.m_gpu, tr.m_start, G, x0, c, d)
-    me, _ = oracle.transform(tr.m_gpu, tr.m_end, G, x0, c, d)
-    same(got["start"], s, "start")
-    same(got["end"], e, "end")
-    same(got["mstart"], ms, "mstart")
-    same(got["mend"], me, "mend")
-    n = tr.n
-    ar = np.arange(n)
+    assert a["rc"] == 0
+    for k in ("x0", "c", "d"):
+        same(got[k], a[k], k)
+    same(got["start"], a["s"], "start")
+    same(got["end"], a["e"], "end")
+    same(got["mstart"], a["ms"], "mstart")
+    same(got["mend"], a["me"], "mend")
+    ar = np.arange(tr.n)
     kind = np.isin(tr.cls, [5, 6]).astype(np.int64)
-    same(got["order"], np.lexsort((ar, s, tr.stream.astype(np.int64),
+    same(got["order"], np.lexsort((ar, a["s"], tr.stream.astype(np.int64),
                                    tr.gpu.astype(np.int64))), "order")
-    same(got["korder"], np.lexsort((ar, s, kind, tr.gpu.astype(np.int64))),
-         "korder")
-    say(f"align ok ({time.time() - t0:.0f}s)")
-    idx, st = oracle.attribute(tr.gpu, s, tr.m_gpu, tr.m_level, ms, me,
-                               tr.depth, G)
+    same(got["korder"], np.lexsort((ar, a["s"], kind,
+                                    tr.gpu.astype(np.int64))), "korder")
+    say(f"align ok ({full.el()}s)")
+
+
+def test_full_attribute(full):
+    idx, st = full.need("idx")
     assert st == 0
-    same(got["idx"], idx, "idx")
-    say(f"attribute ok ({time.time() - t0:.0f}s)")
-    ov = oracle.overlap(tr.gpu, tr.stream, tr.cls, s, e, tr.m_gpu, ms, me, G)
+    same(full.got["idx"], idx, "idx")
+    say(f"attribute ok ({full.el()}s)")
+
+
+def test_full_overlap(full):
+    ov = full.need("ov")
     for k in ("ovl", "gap", "mwin", "gwin"):
-        same(got[k], ov[k], k)
-    say(f"overlap ok ({time.time() - t0:.0f}s)")
-    levels = list(range(tr.depth)) + [100, 101]
-    ref = brute.aggregate_numpy(tr.gpu, tr.cls, s, e, idx, ov["gap"],
-                                ov["ovl"], tr.counters, tr.depth, levels)
-    rows, lo = got["rows"], got["rows"]["level_offset"]
+        same(full.got[k], ov[k], k)
+    say(f"overlap ok ({full.el()}s)")
+
+
+def test_full_aggregate_and_ratios(full):
+    levels, ref = full.need("rows")
+    rows, lo = full.got["rows"], full.got["rows"]["level_offset"]
     for li, lev in enumerate(levels):
         sl = slice(lo[li], lo[li + 1])
         for k in ("gpu", "kind", "n", "dur", "gap", "ovl", "tmin", "tmax",
@@ -98,7 +149,7 @@ def test_full_size_parity(ch, cid):
             same(rows[k][sl], ref[lev][k], f"level {lev} {k}")
         same(rows["path"][:, sl], ref[lev]["path"], f"level {lev} path")
         same(rows["ctr"][:, sl], ref[lev]["ctr"], f"level {lev} ctr")
-    say(f"aggregate ok ({time.time() - t0:.0f}s)")
+    say(f"aggregate ok ({full.el()}s)")
     # derived ratios: the same IEEE operations in numpy
     f = lambda a: np.asarray(a).astype(np.float64)
     with np.errstate(divide="ignore", invalid="ignore"):
@@ -109,18 +160,23 @@ def test_full_size_parity(ch, cid):
                          f(rows["ctr"][4] + rows["ctr"][5]) / dur,
                          f(rows["ctr"][13]) / f(rows["n"]),
                          f(rows["ctr"][1]) / cyc, dpeak, dur / dpeak])
-    gotr = got["ratios"]
+    gotr = full.got["ratios"]
     ok = (gotr == want) | (np.isnan(gotr) & np.isnan(want))
     assert ok.all(), "ratios"
-    say(f"ratios ok ({time.time() - t0:.0f}s)")
+    say(f"ratios ok ({full.el()}s)")
+
+
+def test_full_views(full):
     # re-keyed views over (iteration, phase, class / operation) and medians
     # over iterations and GPUs, the first ten iterations as warm-up
+    tr, cid, G = full.tr, full.cid, full.tr.n_gpus
+    a, idx, ov = full.need("aligned"), full.need("idx")[0], full.need("ov")
     spec = dict(n_phases=3, n_ops=64, n_iters=ITERS[cid], warmup=10)
-    v = ch.Views(pipe, **spec)
+    v = full.ch.Views(full.pipe, **spec)
     v.run()
     gv = v.results()
-    rv = oracle.views(tr.cls, s, e, idx, ov["gap"], ov["ovl"], tr.m_level,
-                      tr.m_label, **spec)
+    rv = oracle.views(tr.cls, a["s"], a["e"], idx, ov["gap"], ov["ovl"],
+                      tr.m_level, tr.m_label, **spec)
     assert gv["n_units"] == rv["n_units"]
     if cid == 3:      # no marker dropped there
         assert rv["n_units"] == G * ITERS[cid]
@@ -129,13 +185,18 @@ def test_full_size_parity(ch, cid):
               "cls_cnt", "op_cnt"):
         same(gv[k], rv[k], f"views {k}")
     for k in ("cls_med", "op_med"):
-        a, b = gv[k], rv[k]
-        assert ((a == b) | (np.isnan(a) & np.isnan(b))).all(), f"views {k}"
+        x, y = gv[k], rv[k]
+        assert ((x == y) | (np.isnan(x) & np.isnan(y))).all(), f"views {k}"
     assert gv["iter_cnt"] == rv["iter_cnt"]
     assert gv["iter_med"] == rv["iter_med"]
-    say(f"views ok ({time.time() - t0:.0f}s)")
+    say(f"views ok ({full.el()}s)")
+
+
+def test_full_op_stats(full):
     # overlap statistics and overhead breakdown per (phase, operation), the
     # oracle run on the brute-force rows of the operation level
+    tr, pipe = full.tr, full.pipe
+    _, ref = full.need("rows")
     fg = np.linspace(2e9, 9e10, 64)
     pipe.status.zero_()
     so, sc = pipe.op_stats(freq_peak_mhz=2100.0, tpt_peak=1.3e6, f_gemm=fg)
@@ -150,34 +211,47 @@ def test_full_size_parity(ch, cid):
     so = so.cpu().numpy()
     assert ((so == ro) | (np.isnan(so) & np.isnan(ro))).all(), "op stats"
     assert rcnt.sum() > 0
-    say(f"op stats ok ({time.time() - t0:.0f}s)")
+    say(f"op stats ok ({full.el()}s)")
+
+
+def test_full_launch_split(full):
     # launch overhead split from seeded dispatch times
     import torch
+    tr, a, G = full.tr, full.need("aligned"), full.tr.n_gpus
     tl = tg.make_launch(tr, 11, max_lead=20000)
-    prep, call = pipe.launch_split(torch.from_numpy(tl).cuda())
-    tla, _ = oracle.transform(tr.gpu, tl, G, x0, c, d)
-    rp, rc2 = oracle.launch_split(tr.gpu, tr.stream, tr.cls, s, e, tla)
+    prep, call = full.pipe.launch_split(torch.from_numpy(tl).cuda())
+    tla, _ = oracle.transform(tr.gpu, tl, G, a["x0"], a["c"], a["d"])
+    rp, rc2 = oracle.launch_split(tr.gpu, tr.stream, tr.cls, a["s"], a["e"],
+                                  tla)
     same(prep.cpu().numpy(), rp, "prep")
     same(call.cpu().numpy(), rc2, "call")
-    say(f"launch split ok ({time.time() - t0:.0f}s)")
-    if cid == 3:
-        # counters of seven serialized passes attached back to the records
-        lab = np.full(n, 0xFFFFFFFF, np.uint32)
-        ok = idx[0] != 0xFFFFFFFF
-        lab[ok] = tr.m_label[idx[0][ok]]
-        passes = tg.make_counter_passes(tr, lab, 5, drop_frac=0.001,
-                                        mismatch_frac=0.001, extra=2)
-        t = lambda a, dt: torch.from_numpy(
-            np.ascontiguousarray(a).view(dt)).cuda()
-        dp = [dict(gpu=t(q["gpu"], np.uint8), stream=t(q["stream"], np.uint8),
-                   cls=t(q["cls"], np.uint8), label=t(q["lab"], np.int32),
-                   values=t(q["values"], np.int64), dst=q["dst"])
-              for q in passes]
-        pipe.status.zero_()
-        ctr, matched = pipe.join_counters(dp)
-        st = int(pipe.status.item()) & 0xFFFFFFFF
-        rc3, rm3, rs3 = oracle.join(tr.gpu, tr.stream, tr.cls, s, lab, passes)
-        assert st == rs3 == oracle.JOIN_MISS
-        same(matched.cpu().numpy(), rm3, "join matched")
-        same(ctr.cpu().numpy().view(np.uint64), rc3, "join counters")
-    say(f"done ({time.time() - t0:.0f}s)")
+    say(f"launch split ok ({full.el()}s)")
+
+
+def test_full_join(full):
+    # counters of seven serialized passes attached back to the records (the
+    # 20M-record trace, which carries the 16 counters the passes split)
+    if full.cid != 3:
+        pytest.skip("the counter passes are built for the headline trace")
+    import torch
+    tr, pipe, n = full.tr, full.pipe, full.tr.n
+    a, idx = full.need("aligned"), full.need("idx")[0]
+    lab = np.full(n, 0xFFFFFFFF, np.uint32)
+    ok = idx[0] != 0xFFFFFFFF
+    lab[ok] = tr.m_label[idx[0][ok]]
+    passes = tg.make_counter_passes(tr, lab, 5, drop_frac=0.001,
+                                    mismatch_frac=0.001, extra=2)
+    t = lambda x, dt: torch.from_numpy(np.ascontiguousarray(x).view(dt)).cuda()
+    dp = [dict(gpu=t(q["gpu"], np.uint8), stream=t(q["stream"], np.uint8),
+               cls=t(q["cls"], np.uint8), label=t(q["lab"], np.int32),
+               values=t(q["values"], np.int64), dst=q["dst"])
+          for q in passes]
+    pipe.status.zero_()
+    ctr, matched = pipe.join_counters(dp)
+    st = int(pipe.status.item()) & 0xFFFFFFFF
+    rc3, rm3, rs3 = oracle.join(tr.gpu, tr.stream, tr.cls, a["s"], lab,
+                                passes)
+    assert st == rs3 == oracle.JOIN_MISS
+    same(matched.cpu().numpy(), rm3, "join matched")
+    same(ctr.cpu().numpy().view(np.uint64), rc3, "join counters")
+    say(f"join ok ({full.el()}s)")
