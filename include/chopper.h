@@ -439,7 +439,10 @@ int chopper_launch_split(const chopper_records* records,
  * JOIN_ORDER (result unspecified): along a (gpu, stream), in either order,
  * a label's kernels are not consecutive apart from kernels without an
  * iteration, or labels do not increase from one label to the next.
- * n_passes <= 8, at most 256 (gpu, stream) pairs per pass.
+ * n_passes <= 8; the records may hold at most 255 (gpu, stream) pairs
+ * (CHOPPER_EINVAL otherwise; entries of other pairs never match).  Scratch
+ * protocol as above (grows with n and the largest pass).  The call waits
+ * once for `stream`: the number of the records' pairs is read back.
  */
 typedef struct {
   int64_t n;
@@ -492,7 +495,19 @@ int chopper_join_counters(const chopper_records* records,
  * in exactly these IEEE operations; cnt [n_phases * n_ops] = m.  Empty
  * groups: NaN.  11-13 and 15 need n_counters = 16 (else NaN); f_gemm
  * ([host], n_ops theoretical FLOP counts, per operation label) may be NULL
- * (13 and 16 NaN).  Limits: y < 2^34 (else RANGE), m < 2^26 per group.
+ * (13 and 16 NaN).  Limits: y < 2^34 and x <= 2^30 (else RANGE, result
+ * unspecified), m < 2^26 per group.
+ *
+ * rows: chopper_aggregate's output (device arrays) for `depth` marker
+ * levels, of which level op_level is read; markers: the same markers
+ * (device; labels read); n_counters: the rows' counter columns (0 .. 16).
+ * out and cnt: device arrays, every element written.  Scratch:
+ * caller-owned device memory, size query with scratch == NULL (grows with
+ * rows->cap and n_phases * n_ops), 256-byte aligned.  status: device word
+ * (RANGE bit).  Enqueued on `stream` without synchronizing.  Returns
+ * CHOPPER_EINVAL for a level outside 0 .. depth-1, depth above the markers'
+ * depth, sizes out of range or a missing pointer, CHOPPER_ESCRATCH for a
+ * short scratch buffer.
  */
 typedef struct {
   int32_t phase_level;
