@@ -231,48 +231,72 @@ __global__ void k_join_match(const uint32_t* nr, const uint32_t* rcls,
   match[r] = hit ? (uint32_t)lo : kNone;
 }
 
-struct PassCols {
+// one pass as the gather sees it
+struct PassView {
+  const uint32_t* match;    // record run -> pass run (NONE: no such run)
+  const uint32_t* qstart;   // pass run -> first position in class order
+  const uint32_t* nq;       // number of pass runs (device)
+  const uint32_t* qorder;   // class-order position -> entry
+  const uint64_t* qkey;     // class-order position -> entry key
+  const uint64_t* values;   // [n_cols][m]
+  int64_t m;
   int32_t n_cols;
-  int32_t bit;
   int32_t dst[16];
 };
 
-// every record, in input order: its entry in the pass (run start +
+struct JoinPasses {
+  int32_t np;
+  PassView p[kMaxPasses];
+};
+
+// every record, in input order, against every pass: its entry (run start +
 // ordinal), the key and class check, and the pass's columns (0 where
-// nothing matches)
+// nothing matches); the matched bits are written once
 __global__ __launch_bounds__(kBlock) void k_join_gather(
     int64_t n, const uint32_t* rrun, const uint32_t* rord, const uint8_t* cls,
-    const uint32_t* rcls, const uint32_t* rlab, const uint32_t* match,
-    const uint32_t* qstart, const uint32_t* nq, int64_t m,
-    const uint32_t* qorder, const uint64_t* qkey, const uint64_t* values,
-    PassCols C, uint64_t* counters, uint8_t* matched, uint32_t* status) {
+    const uint32_t* rcls, const uint32_t* rlab, JoinPasses J,
+    uint64_t* counters, uint8_t* matched, uint32_t* status) {
   const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   bool miss = false;
   if (r < n) {
     const uint32_t run = rrun[r];
-    int64_t q = -1;
+    uint32_t ord = 0, kc = 0, kl = 0, kk = 0;
     if (run != kNone) {
-      const uint32_t qr = match[run];
-      if (qr != kNone) {
-        const int64_t pos = (int64_t)qstart[qr] + rord[r];
-        const int64_t q1 =
-            (int64_t)qr + 1 < (int64_t)*nq ? (int64_t)qstart[qr + 1] : m;
-        // the entry at the ordinal is the record's only if it still has the
-        // run's key (entries without an iteration may follow the run)
-        if (pos < q1) {
-          const uint64_t k = qkey[pos];
-          if ((uint32_t)k == rlab[run] &&
-              ((uint32_t)(k >> 32) & 0xFFFFu) == rcls[run] &&
-              (uint32_t)(k >> 48) == cls[r])
-            q = qorder[pos];
-        }
-      }
-      miss = q < 0;
+      ord = rord[r];
+      kc = rcls[run];
+      kl = rlab[run];
+      kk = cls[r];
     }
-    for (int c = 0; c < C.n_cols; ++c)
-      counters[(int64_t)C.dst[c] * n + r] =
-          q >= 0 ? values[(int64_t)c * m + q] : 0ull;
-    if (q >= 0) matched[r] |= (uint8_t)(1u << C.bit);
+    uint32_t bits = 0;
+#pragma unroll
+    for (int p = 0; p < kMaxPasses; ++p) {
+      if (p >= J.np) break;
+      const PassView& P = J.p[p];
+      int64_t q = -1;
+      if (run != kNone) {
+        const uint32_t qr = P.match[run];
+        if (qr != kNone) {
+          const int64_t pos = (int64_t)P.qstart[qr] + ord;
+          const int64_t q1 = (int64_t)qr + 1 < (int64_t)*P.nq
+                                 ? (int64_t)P.qstart[qr + 1]
+                                 : P.m;
+          // the entry at the ordinal is the record's only if it still has
+          // the run's key (entries without an iteration may follow the run)
+          if (pos < q1) {
+            const uint64_t k = P.qkey[pos];
+            if ((uint32_t)k == kl && ((uint32_t)(k >> 32) & 0xFFFFu) == kc &&
+                (uint32_t)(k >> 48) == kk)
+              q = P.qorder[pos];
+          }
+        }
+        miss |= q < 0;
+      }
+      for (int c = 0; c < P.n_cols; ++c)
+        counters[(int64_t)P.dst[c] * n + r] =
+            q >= 0 ? P.values[(int64_t)c * P.m + q] : 0ull;
+      if (q >= 0) bits |= 1u << p;
+    }
+    matched[r] = (uint8_t)bits;
   }
   if (__ballot(miss) != 0 && lane_id() == 0)
     atomicOr(status, CHOPPER_ST_JOIN_MISS);
@@ -311,37 +335,52 @@ extern "C" int chopper_join_counters(
     }
     mmax = P.n > mmax ? P.n : mmax;
   }
-  // scratch: record labels and runs; per pass (reused): times, class map,
-  // class sort, order, heads and runs
-  auto layout = [&](Scratch& sc, std::vector<void*>& v) {
-    v.clear();
-    v.push_back(sc.take<uint32_t>(n));             // 0 rec labels
-    v.push_back(sc.take<uint32_t>(n));             // 1 heads
-    v.push_back(sc.take<uint32_t>(n));             // 2 excl
-    v.push_back(sc.take<uint32_t>(n + 1));         // 3 rstart
-    v.push_back(sc.take<uint32_t>(n + 1));         // 4 rcls
-    v.push_back(sc.take<uint32_t>(n + 1));         // 5 rlab
-    v.push_back(sc.take<uint32_t>(n + 1));         // 6 match
-    v.push_back(sc.take<uint32_t>(4));             // 7 totals (R, Q, C)
-    v.push_back(sc.take<uint32_t>(
-        scan_scratch_elems(n > mmax ? n : mmax)));  // 8 scan tmp
-    v.push_back(sc.take<uint64_t>(n > mmax ? n : mmax));  // 9 keys
-    v.push_back(sc.take<uint8_t>(65536));          // 10 presence
-    v.push_back(sc.take<uint16_t>(65536));         // 11 class map
-    v.push_back(sc.take<uint32_t>(mmax));          // 12 qorder
-    v.push_back(sc.take<uint32_t>(256 + 1));       // 13 class offsets
-    v.push_back(sc.take<uint32_t>(mmax));          // 14 q heads
-    v.push_back(sc.take<uint32_t>(
-        2 * (ceil_div(n > mmax ? n : mmax, kBlock) + 1)));  // 15 block heads
-    v.push_back(sc.take<uint32_t>(mmax + 1));      // 16 qstart
-    v.push_back(sc.take<uint32_t>(mmax + 1));      // 17 qcls
-    v.push_back(sc.take<uint32_t>(mmax + 1));      // 18 qlab
-    v.push_back(sc.take<uint32_t>(n));             // 19 run of each record
-    v.push_back(sc.take<uint32_t>(n));             // 20 its ordinal
+  // scratch: record labels, runs and keys, the class map, per-pass
+  // temporaries (reused) and what the gather reads of every pass
+  const int64_t nmax = n > mmax ? n : mmax;
+  struct PassBuf {
+    uint32_t *match, *qstart, *qorder;
+    uint64_t* key;
   };
-  std::vector<void*> v;
+  struct Bufs {
+    uint32_t *rlabv, *head, *excl, *rstart, *rcls, *rlab, *tot, *tmp, *coff;
+    uint32_t *qhead, *tcnt, *tpre, *qcls, *qlab, *rrun, *rord;
+    uint64_t* rkey;
+    uint8_t* pres;
+    uint16_t* cmap;
+    PassBuf pb[kMaxPasses];
+  } B;
+  auto layout = [&](Scratch& sc) {
+    B.rlabv = sc.take<uint32_t>(n);
+    B.head = sc.take<uint32_t>(n);
+    B.excl = sc.take<uint32_t>(n);
+    B.rstart = sc.take<uint32_t>(n + 1);
+    B.rcls = sc.take<uint32_t>(n + 1);
+    B.rlab = sc.take<uint32_t>(n + 1);
+    // runs of the records, class count, runs of every pass
+    B.tot = sc.take<uint32_t>(2 + kMaxPasses);
+    B.tmp = sc.take<uint32_t>(scan_scratch_elems(nmax));
+    B.rkey = sc.take<uint64_t>(n);
+    B.pres = sc.take<uint8_t>(65536);
+    B.cmap = sc.take<uint16_t>(65536);
+    B.coff = sc.take<uint32_t>(256 + 1);
+    B.qhead = sc.take<uint32_t>(mmax);
+    B.tcnt = sc.take<uint32_t>(ceil_div(nmax, kBlock) + 1);
+    B.tpre = sc.take<uint32_t>(ceil_div(nmax, kBlock) + 1);
+    B.qcls = sc.take<uint32_t>(mmax + 1);
+    B.qlab = sc.take<uint32_t>(mmax + 1);
+    B.rrun = sc.take<uint32_t>(n);
+    B.rord = sc.take<uint32_t>(n);
+    for (int p = 0; p < n_passes; ++p) {
+      const int64_t m = passes[p].n;
+      B.pb[p].match = sc.take<uint32_t>(n + 1);
+      B.pb[p].qstart = sc.take<uint32_t>(m + 1);
+      B.pb[p].qorder = sc.take<uint32_t>(m);
+      B.pb[p].key = sc.take<uint64_t>(m);
+    }
+  };
   Scratch probe(nullptr);
-  layout(probe, v);
+  layout(probe);
   ClassSortLayout probe_sort = class_sort_layout(probe, mmax, 256);
   (void)probe_sort;
   int rc = scratch_check(scratch, scratch_bytes, probe.used);
@@ -350,69 +389,57 @@ extern "C" int chopper_join_counters(
   if (n == 0) return CHOPPER_OK;
   hipStream_t s = (hipStream_t)stream;
   Scratch sc(scratch);
-  layout(sc, v);
+  layout(sc);
   ClassSortLayout SL = class_sort_layout(sc, mmax, 256);
-  uint32_t* rlabv = (uint32_t*)v[0];
-  uint32_t *head = (uint32_t*)v[1], *excl = (uint32_t*)v[2];
-  uint32_t *rstart = (uint32_t*)v[3], *rcls = (uint32_t*)v[4],
-           *rlab = (uint32_t*)v[5], *match = (uint32_t*)v[6];
-  uint32_t* tot = (uint32_t*)v[7];
-  uint32_t* tmp = (uint32_t*)v[8];
-  uint64_t* key = (uint64_t*)v[9];
-  uint32_t *rrun = (uint32_t*)v[19], *rord = (uint32_t*)v[20];
-  uint8_t* pres = (uint8_t*)v[10];
-  uint16_t* cmap = (uint16_t*)v[11];
-  uint32_t *qorder = (uint32_t*)v[12], *coff = (uint32_t*)v[13];
-  uint32_t* qhead = (uint32_t*)v[14];
-  uint32_t* tcnt = (uint32_t*)v[15];
-  uint32_t* tpre = tcnt + ceil_div(n > mmax ? n : mmax, kBlock) + 1;
-  uint32_t *qstart = (uint32_t*)v[16], *qcls = (uint32_t*)v[17],
-           *qlab = (uint32_t*)v[18];
   const dim3 gn = grid_for(n, kBlock);
 
-  // columns no pass fills are zero; no record matched yet
+  // columns no pass fills are zero
   for (int c = 0; c < 16; ++c)
     if (!((used >> c) & 1u))
       CHOPPER_HIP(launch("join_fill", k_join_fill_u64,
                          dim3((unsigned)std::min<int64_t>(
                              ceil_div(n, (int64_t)kBlock), 4096)),
                          dim3(kBlock), s, counters_out + (int64_t)c * n, n));
-  CHOPPER_HIP(launch("join_fill", k_join_fill_u8, gn, dim3(kBlock), s,
-                     matched_out, n, (uint32_t*)nullptr));
   // dense classes of the records' (gpu, stream) pairs (one read-back)
   CHOPPER_HIP(launch("join_fill", k_join_fill_u8, dim3(64), dim3(kBlock), s,
-                     (uint8_t*)nullptr, (int64_t)0, (uint32_t*)pres));
+                     (uint8_t*)nullptr, (int64_t)0, (uint32_t*)B.pres));
   CHOPPER_HIP(launch("join_pass_prep", k_join_presence, gn, dim3(kBlock), s,
-                     n, rec->gpu, rec->stream, pres));
+                     n, rec->gpu, rec->stream, B.pres));
   CHOPPER_HIP(launch("join_dense", k_join_dense, dim3(1), dim3(kDenseT), s,
-                     (const uint8_t*)pres, cmap, tot + 2));
+                     (const uint8_t*)B.pres, B.cmap, B.tot + 1));
   uint32_t nclass = 0;
-  CHOPPER_HIP(read_back(tot + 2, &nclass, sizeof(uint32_t), s));
+  CHOPPER_HIP(read_back(B.tot + 1, &nclass, sizeof(uint32_t), s));
   // (pass entries of other pairs take one more class)
   if (nclass + 1 > 256) return CHOPPER_EINVAL;
-  // the records' runs along `order`
+  // the records' runs along `order`, then each record's run and ordinal
   CHOPPER_HIP(launch("join_labels", k_join_rec_labels, gn, dim3(kBlock), s,
-                     n, idx + (int64_t)iter_level * n, nm, mk->label, rlabv));
-  const Seq R{order, rec->gpu, rec->stream, rlabv, cmap, n};
+                     n, idx + (int64_t)iter_level * n, nm, mk->label,
+                     B.rlabv));
+  const Seq R{order, rec->gpu, rec->stream, B.rlabv, B.cmap, n};
   CHOPPER_HIP(launch("join_heads", k_join_heads, gn, dim3(kBlock), s, R,
-                     (const uint8_t*)nullptr, head, key, tcnt));
-  CHOPPER_HIP(exclusive_scan<uint32_t>(tcnt, tpre, (int64_t)gn.x, tmp, tot,
-                                       s));
+                     (const uint8_t*)nullptr, B.head, B.rkey, B.tcnt));
+  CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gn.x, B.tmp,
+                                       B.tot, s));
   CHOPPER_HIP(launch("join_runs", k_join_runs, gn, dim3(kBlock), s, n,
-                     (const uint32_t*)head, (const uint32_t*)tpre,
-                     (const uint64_t*)key, rstart, rcls, rlab, excl));
+                     (const uint32_t*)B.head, (const uint32_t*)B.tpre,
+                     (const uint64_t*)B.rkey, B.rstart, B.rcls, B.rlab,
+                     B.excl));
   CHOPPER_HIP(launch("join_order", k_join_order, gn, dim3(kBlock), s,
-                     (const uint32_t*)tot, (const uint32_t*)rcls,
-                     (const uint32_t*)rlab, status));
+                     (const uint32_t*)B.tot, (const uint32_t*)B.rcls,
+                     (const uint32_t*)B.rlab, status));
   CHOPPER_HIP(launch("join_runs", k_join_rec_pos, gn, dim3(kBlock), s, n,
-                     order, (const uint32_t*)head, (const uint32_t*)excl,
-                     (const uint64_t*)key, (const uint32_t*)rstart, rrun,
-                     rord));
+                     order, (const uint32_t*)B.head, (const uint32_t*)B.excl,
+                     (const uint64_t*)B.rkey, (const uint32_t*)B.rstart,
+                     B.rrun, B.rord));
+  // every pass: class order, keys, run table, and the pass run of every
+  // record run
+  JoinPasses J;
+  J.np = n_passes;
   for (int p = 0; p < n_passes; ++p) {
     const chopper_counter_pass& P = passes[p];
+    const PassBuf& Q_ = B.pb[p];
     const int64_t m = P.n;
-    PassCols C{P.n_cols, p, {0}};
-    for (int c = 0; c < P.n_cols; ++c) C.dst[c] = P.dst[c];
+    uint32_t* nq = B.tot + 2 + p;
     if (m > 0) {
       // stable partition of the pass by class, in its own order (the
       // pass's order is its time: the partition needs no time key)
@@ -420,38 +447,46 @@ extern "C" int chopper_join_counters(
       L.n = m;
       L.ntiles = sort_tiles(m);
       bool range_err = false;
-      KeyRecStream kq{P.gpu, P.stream, nullptr, cmap, (int)nclass + 1};
-      rc = class_sort(kq, L, qorder, coff, &range_err, s, 1);
+      KeyRecStream kq{P.gpu, P.stream, nullptr, B.cmap, (int)nclass + 1};
+      rc = class_sort(kq, L, Q_.qorder, B.coff, &range_err, s, 1);
       if (rc != CHOPPER_OK) return rc;
-      const Seq Q{qorder, P.gpu, P.stream, P.label, cmap, m};
+      const Seq Q{Q_.qorder, P.gpu, P.stream, P.label, B.cmap, m};
       const dim3 gm = grid_for(m, kBlock);
       CHOPPER_HIP(launch("join_heads", k_join_heads, gm, dim3(kBlock), s, Q,
-                         P.cls, qhead, key, tcnt));
-      CHOPPER_HIP(exclusive_scan<uint32_t>(tcnt, tpre, (int64_t)gm.x, tmp,
-                                           tot + 1, s));
+                         P.cls, B.qhead, Q_.key, B.tcnt));
+      CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gm.x,
+                                           B.tmp, nq, s));
       CHOPPER_HIP(launch("join_runs", k_join_runs, gm, dim3(kBlock), s, m,
-                         (const uint32_t*)qhead, (const uint32_t*)tpre,
-                         (const uint64_t*)key, qstart, qcls, qlab,
+                         (const uint32_t*)B.qhead, (const uint32_t*)B.tpre,
+                         (const uint64_t*)Q_.key, Q_.qstart, B.qcls, B.qlab,
                          (uint32_t*)nullptr));
       CHOPPER_HIP(launch("join_order", k_join_order, gm, dim3(kBlock), s,
-                         (const uint32_t*)(tot + 1), (const uint32_t*)qcls,
-                         (const uint32_t*)qlab, status));
+                         (const uint32_t*)nq, (const uint32_t*)B.qcls,
+                         (const uint32_t*)B.qlab, status));
     } else {
-      CHOPPER_HIP(launch("join_fill", k_join_zero, dim3(1), dim3(1), s,
-                         tot + 1));
+      CHOPPER_HIP(launch("join_fill", k_join_zero, dim3(1), dim3(1), s, nq));
     }
     CHOPPER_HIP(launch("join_match", k_join_match, gn, dim3(kBlock), s,
-                       (const uint32_t*)tot, (const uint32_t*)rcls,
-                       (const uint32_t*)rlab, (const uint32_t*)(tot + 1),
-                       (const uint32_t*)qcls, (const uint32_t*)qlab, match));
-    CHOPPER_HIP(launch("join_gather", k_join_gather, gn, dim3(kBlock), s, n,
-                       (const uint32_t*)rrun, (const uint32_t*)rord, rec->cls,
-                       (const uint32_t*)rcls, (const uint32_t*)rlab,
-                       (const uint32_t*)match, (const uint32_t*)qstart,
-                       (const uint32_t*)(tot + 1), m,
-                       (const uint32_t*)qorder, (const uint64_t*)key,
-                       P.values, C, counters_out, matched_out, status));
+                       (const uint32_t*)B.tot, (const uint32_t*)B.rcls,
+                       (const uint32_t*)B.rlab, (const uint32_t*)nq,
+                       (const uint32_t*)B.qcls, (const uint32_t*)B.qlab,
+                       Q_.match));
+    PassView& V = J.p[p];
+    V.match = Q_.match;
+    V.qstart = Q_.qstart;
+    V.nq = nq;
+    V.qorder = Q_.qorder;
+    V.qkey = Q_.key;
+    V.values = P.values;
+    V.m = m;
+    V.n_cols = P.n_cols;
+    for (int c = 0; c < 16; ++c) V.dst[c] = c < P.n_cols ? P.dst[c] : 0;
   }
+  CHOPPER_HIP(launch("join_gather", k_join_gather, gn, dim3(kBlock), s, n,
+                     (const uint32_t*)B.rrun, (const uint32_t*)B.rord,
+                     rec->cls, (const uint32_t*)B.rcls,
+                     (const uint32_t*)B.rlab, J, counters_out, matched_out,
+                     status));
   return CHOPPER_OK;
 }
 
