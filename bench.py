@@ -123,8 +123,9 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the traces of all ranks are "
-              "input data to a single device (see DESIGN.md for how the path "
-              "would shard).", file=sys.stderr)
+              "input data to a single device (the path would shard by source "
+              "GPU, each device taking the traces of its ranks).",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
