@@ -55,17 +55,6 @@ __device__ inline void level_range(const StatArgs& A, int64_t& lo,
   if (lo > hi) lo = hi;
 }
 
-// group of an operation-level row, or kNone when it is no instance
-__device__ inline uint32_t group_of(const StatArgs& A, int64_t r) {
-  if (A.kind[r] != 0 || A.dur[r] <= 0) return kNone;
-  const uint32_t mp = A.path[(int64_t)A.lv_phase * A.cap + r];
-  const uint32_t mo = A.path[(int64_t)A.lv_op * A.cap + r];
-  if ((int64_t)mp >= A.nm || (int64_t)mo >= A.nm) return kNone;
-  const uint32_t p = A.label[mp], o = A.label[mo];
-  if (p >= (uint32_t)A.P || o >= (uint32_t)A.O) return kNone;
-  return p * (uint32_t)A.O + o;
-}
-
 // nearest double to a 128-bit integer (round half to even): a magnitude
 // below 2^63 converts directly; else its top 64 bits with every lower bit
 // folded into the last one (below the double's precision there) convert
@@ -111,7 +100,9 @@ __global__ void k_stats_clear(uint32_t* cnt, int G, uint32_t* hist,
   if (i < nh) hist[i] = 0;
 }
 
-// group of every row of the operation level and the instances per group
+// group of every row of the operation level (kNone when it is no
+// instance: not a compute row, zero length, or a label out of range) and
+// the instances per group
 __global__ __launch_bounds__(kStatT) void k_stats_keys(StatArgs A,
                                                        uint32_t* key,
                                                        uint32_t* cnt) {
@@ -122,14 +113,29 @@ __global__ __launch_bounds__(kStatT) void k_stats_keys(StatArgs A,
   int64_t lo, hi;
   level_range(A, lo, hi);
   const int64_t r0 = lo + (int64_t)blockIdx.x * kRowSpan + threadIdx.x;
+  // the rows' fields of all eight rows in flight at once, then the labels
+  uint8_t kd[kStatIpt];
+  int64_t du[kStatIpt];
+  uint32_t mp[kStatIpt], mo[kStatIpt];
+#pragma unroll
+  for (int k = 0; k < kStatIpt; ++k) {
+    const int64_t r = r0 + (int64_t)k * kStatT;
+    const bool ok = r < hi;
+    kd[k] = ok ? A.kind[r] : (uint8_t)1;
+    du[k] = ok ? A.dur[r] : 0;
+    mp[k] = ok ? A.path[(int64_t)A.lv_phase * A.cap + r] : kNone;
+    mo[k] = ok ? A.path[(int64_t)A.lv_op * A.cap + r] : kNone;
+  }
 #pragma unroll
   for (int k = 0; k < kStatIpt; ++k) {
     const int64_t r = r0 + (int64_t)k * kStatT;
     uint32_t g = kNone;
-    if (r < hi) {
-      g = group_of(A, r);
-      key[r - lo] = g;
+    if (kd[k] == 0 && du[k] > 0 && (int64_t)mp[k] < A.nm &&
+        (int64_t)mo[k] < A.nm) {
+      const uint32_t p = A.label[mp[k]], o = A.label[mo[k]];
+      if (p < (uint32_t)A.P && o < (uint32_t)A.O) g = p * (uint32_t)A.O + o;
     }
+    if (r < hi) key[r - lo] = g;
     lds_claim(s_h, g, g != kNone);
   }
   __syncthreads();
@@ -205,12 +211,19 @@ __global__ __launch_bounds__(kStatT) void k_stats_scatter(
   level_range(A, lo, hi);
   const int64_t r0 = lo + (int64_t)blockIdx.x * kRowSpan + threadIdx.x;
   uint32_t g[kStatIpt], slot[kStatIpt];
+  int64_t du[kStatIpt], ol[kStatIpt], gp[kStatIpt];
 #pragma unroll
   for (int k = 0; k < kStatIpt; ++k) {
     const int64_t r = r0 + (int64_t)k * kStatT;
-    g[k] = r < hi ? key[r - lo] : kNone;
-    slot[k] = lds_claim(s_n, g[k], g[k] != kNone);
+    const bool ok = r < hi;
+    g[k] = ok ? key[r - lo] : kNone;
+    du[k] = ok ? A.dur[r] : 1;
+    ol[k] = ok ? A.ovl[r] : 0;
+    gp[k] = ok ? A.gap[r] : 0;
   }
+#pragma unroll
+  for (int k = 0; k < kStatIpt; ++k)
+    slot[k] = lds_claim(s_n, g[k], g[k] != kNone);
   __syncthreads();
   for (int q = threadIdx.x; q < G; q += kStatT)
     if (s_n[q]) s_base[q] = atomicAdd(&cur[q], s_n[q]);
@@ -220,9 +233,9 @@ __global__ __launch_bounds__(kStatT) void k_stats_scatter(
   for (int k = 0; k < kStatIpt; ++k) {
     if (g[k] == kNone) continue;
     const int64_t r = r0 + (int64_t)k * kStatT;
-    const uint64_t d = (uint64_t)A.dur[r];
-    const uint64_t ov = (uint64_t)A.ovl[r];
-    const uint64_t y = d + (uint64_t)A.gap[r];
+    const uint64_t d = (uint64_t)du[k];
+    const uint64_t ov = (uint64_t)ol[k];
+    const uint64_t y = d + (uint64_t)gp[k];
     const uint64_t x = (ov << 30) / d;
     if ((y >> 34) != 0 || x > (1ull << 30)) big = true;
     const uint32_t pos = s_base[g[k]] + slot[k];
