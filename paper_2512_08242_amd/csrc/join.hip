@@ -155,6 +155,54 @@ __global__ __launch_bounds__(kBlock) void k_join_heads(Seq S,
   }
 }
 
+// The same for a pass in class order: the class of a position comes from
+// the class offsets of the partition (coff[0 .. C]), so only the label and
+// the kernel class are read through the permutation.
+__global__ __launch_bounds__(kBlock) void k_join_heads_pass(
+    int64_t m, const uint32_t* qorder, const uint32_t* label,
+    const uint8_t* kcls, const uint32_t* coff, int C, uint32_t* head,
+    uint64_t* key, uint32_t* tcnt) {
+  __shared__ uint32_t s_off[256 + 1];
+  __shared__ uint32_t s_c[kWavesPerBlock];
+  for (int c = threadIdx.x; c <= C; c += kBlock) s_off[c] = coff[c];
+  __syncthreads();
+  // class of position q: the last c < C with s_off[c] <= q
+  auto cls_at = [&](int64_t q) {
+    int lo = 0, hi = C;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if ((int64_t)s_off[mid] <= q) lo = mid;
+      else hi = mid;
+    }
+    return (uint32_t)lo;
+  };
+  auto key_at = [&](int64_t q) {
+    const uint32_t e = qorder[q];
+    return (uint64_t)label[e] | (uint64_t)cls_at(q) << 32 |
+           (uint64_t)kcls[e] << 48;
+  };
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const bool ok = p < m;
+  const uint64_t kb = ok ? key_at(p) : 0ull;
+  uint64_t ka = wave_shr1_any((uint64_t)0, kb);
+  if (lane_id() == 0 && ok && p > 0) ka = key_at(p - 1);
+  const uint64_t kMask = 0x0000FFFFFFFFFFFFull;    // class and label
+  uint32_t h = 0;
+  if (ok && (uint32_t)kb != kNone) h = (p == 0 || ((ka ^ kb) & kMask) != 0);
+  if (ok) {
+    head[p] = h;
+    key[p] = kb;
+  }
+  const uint32_t c = (uint32_t)__popcll(__ballot(h != 0));
+  if (lane_id() == 0) s_c[threadIdx.x / kWave] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t sum = 0;
+    for (int w = 0; w < kWavesPerBlock; ++w) sum += s_c[w];
+    tcnt[blockIdx.x] = sum;
+  }
+}
+
 // run table: start position, (gpu, stream) and label of every run, the run
 // number of a head being the heads before it (block prefix tpre + the
 // heads below it in its block); excl (optional) gets that count at every
@@ -450,10 +498,11 @@ extern "C" int chopper_join_counters(
       KeyRecStream kq{P.gpu, P.stream, nullptr, B.cmap, (int)nclass + 1};
       rc = class_sort(kq, L, Q_.qorder, B.coff, &range_err, s, 1);
       if (rc != CHOPPER_OK) return rc;
-      const Seq Q{Q_.qorder, P.gpu, P.stream, P.label, B.cmap, m};
       const dim3 gm = grid_for(m, kBlock);
-      CHOPPER_HIP(launch("join_heads", k_join_heads, gm, dim3(kBlock), s, Q,
-                         P.cls, B.qhead, Q_.key, B.tcnt));
+      CHOPPER_HIP(launch("join_heads", k_join_heads_pass, gm, dim3(kBlock), s,
+                         m, (const uint32_t*)Q_.qorder, P.label, P.cls,
+                         (const uint32_t*)B.coff, (int)nclass + 1, B.qhead,
+                         Q_.key, B.tcnt));
       CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gm.x,
                                            B.tmp, nq, s));
       CHOPPER_HIP(launch("join_runs", k_join_runs, gm, dim3(kBlock), s, m,
