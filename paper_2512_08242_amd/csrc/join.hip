@@ -251,11 +251,15 @@ __global__ void k_join_rec_pos(int64_t n, const uint32_t* order,
 // JOIN_ORDER: a run whose label is not above that of the previous run of
 // its (gpu, stream); otherwise the run table is sorted by (gpu, stream,
 // label) and every label has one run
+// (run tables are short: a fixed grid strides over them)
 __global__ void k_join_order(const uint32_t* nruns, const uint32_t* rcls,
                              const uint32_t* rlab, uint32_t* status) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r == 0 || r >= (int64_t)*nruns) return;
-  if (rcls[r - 1] == rcls[r] && rlab[r - 1] >= rlab[r])
+  const int64_t nr = (int64_t)*nruns;
+  bool bad = false;
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < nr;
+       r += (int64_t)gridDim.x * blockDim.x)
+    if (r > 0 && rcls[r - 1] == rcls[r] && rlab[r - 1] >= rlab[r]) bad = true;
+  if (__ballot(bad) != 0 && lane_id() == 0)
     atomicOr(status, CHOPPER_ST_JOIN_ORDER);
 }
 
@@ -264,19 +268,21 @@ __global__ void k_join_match(const uint32_t* nr, const uint32_t* rcls,
                              const uint32_t* rlab, const uint32_t* nq,
                              const uint32_t* qcls, const uint32_t* qlab,
                              uint32_t* match) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= (int64_t)*nr) return;
-  const uint64_t key = (uint64_t)rcls[r] << 32 | rlab[r];
-  int64_t lo = 0, hi = (int64_t)*nq;     // first run with key >= ours
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) >> 1;
-    const uint64_t k = (uint64_t)qcls[mid] << 32 | qlab[mid];
-    if (k < key) lo = mid + 1;
-    else hi = mid;
+  const int64_t n_r = (int64_t)*nr, n_q = (int64_t)*nq;
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n_r;
+       r += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t key = (uint64_t)rcls[r] << 32 | rlab[r];
+    int64_t lo = 0, hi = n_q;     // first run with key >= ours
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) >> 1;
+      const uint64_t k = (uint64_t)qcls[mid] << 32 | qlab[mid];
+      if (k < key) lo = mid + 1;
+      else hi = mid;
+    }
+    const bool hit =
+        lo < n_q && ((uint64_t)qcls[lo] << 32 | qlab[lo]) == key;
+    match[r] = hit ? (uint32_t)lo : kNone;
   }
-  const bool hit = lo < (int64_t)*nq &&
-                   ((uint64_t)qcls[lo] << 32 | qlab[lo]) == key;
-  match[r] = hit ? (uint32_t)lo : kNone;
 }
 
 // one pass as the gather sees it
@@ -472,7 +478,8 @@ extern "C" int chopper_join_counters(
                      (const uint32_t*)B.head, (const uint32_t*)B.tpre,
                      (const uint64_t*)B.rkey, B.rstart, B.rcls, B.rlab,
                      B.excl));
-  CHOPPER_HIP(launch("join_order", k_join_order, gn, dim3(kBlock), s,
+  const dim3 gr(std::min<unsigned>(gn.x, 1024u));
+  CHOPPER_HIP(launch("join_order", k_join_order, gr, dim3(kBlock), s,
                      (const uint32_t*)B.tot, (const uint32_t*)B.rcls,
                      (const uint32_t*)B.rlab, status));
   CHOPPER_HIP(launch("join_runs", k_join_rec_pos, gn, dim3(kBlock), s, n,
@@ -509,13 +516,14 @@ extern "C" int chopper_join_counters(
                          (const uint32_t*)B.qhead, (const uint32_t*)B.tpre,
                          (const uint64_t*)Q_.key, Q_.qstart, B.qcls, B.qlab,
                          (uint32_t*)nullptr));
-      CHOPPER_HIP(launch("join_order", k_join_order, gm, dim3(kBlock), s,
+      CHOPPER_HIP(launch("join_order", k_join_order,
+                         dim3(std::min<unsigned>(gm.x, 1024u)), dim3(kBlock), s,
                          (const uint32_t*)nq, (const uint32_t*)B.qcls,
                          (const uint32_t*)B.qlab, status));
     } else {
       CHOPPER_HIP(launch("join_fill", k_join_zero, dim3(1), dim3(1), s, nq));
     }
-    CHOPPER_HIP(launch("join_match", k_join_match, gn, dim3(kBlock), s,
+    CHOPPER_HIP(launch("join_match", k_join_match, gr, dim3(kBlock), s,
                        (const uint32_t*)B.tot, (const uint32_t*)B.rcls,
                        (const uint32_t*)B.rlab, (const uint32_t*)nq,
                        (const uint32_t*)B.qcls, (const uint32_t*)B.qlab,
