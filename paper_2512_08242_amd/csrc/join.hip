@@ -112,11 +112,9 @@ struct Seq {
   }
 };
 
-// key of a sequence item: label | class << 32 | pass class << 48
-__device__ inline uint64_t item_key(const Seq& S, const uint8_t* pcls,
-                                    uint32_t i) {
-  return (uint64_t)S.lab[i] | (uint64_t)S.cls(i) << 32 |
-         (pcls ? (uint64_t)pcls[i] << 48 : 0ull);
+// key of a sequence item: label | class << 32
+__device__ inline uint64_t item_key(const Seq& S, uint32_t i) {
+  return (uint64_t)S.lab[i] | (uint64_t)S.cls(i) << 32;
 }
 
 // run heads: an item with an iteration whose predecessor differs in
@@ -127,17 +125,16 @@ __device__ inline uint64_t item_key(const Seq& S, const uint8_t* pcls,
 // The heads of a block of kBlock positions are also counted (tcnt), so that
 // the run numbers come from a scan of the block counts.
 __global__ __launch_bounds__(kBlock) void k_join_heads(Seq S,
-                                                       const uint8_t* pcls,
                                                        uint32_t* head,
                                                        uint64_t* key,
                                                        uint32_t* tcnt) {
   __shared__ uint32_t s_c[kWavesPerBlock];
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const bool ok = p < S.n;
-  const uint64_t kb = ok ? item_key(S, pcls, S.idx[p]) : 0ull;
+  const uint64_t kb = ok ? item_key(S, S.idx[p]) : 0ull;
   // the predecessor's key from the lane below; lane 0 loads it
   uint64_t ka = wave_shr1_any((uint64_t)0, kb);
-  if (lane_id() == 0 && ok && p > 0) ka = item_key(S, pcls, S.idx[p - 1]);
+  if (lane_id() == 0 && ok && p > 0) ka = item_key(S, S.idx[p - 1]);
   const uint64_t kMask = 0x0000FFFFFFFFFFFFull;    // class and label
   uint32_t h = 0;
   if (ok && (uint32_t)kb != kNone) h = (p == 0 || ((ka ^ kb) & kMask) != 0);
@@ -471,7 +468,7 @@ extern "C" int chopper_join_counters(
                      B.rlabv));
   const Seq R{order, rec->gpu, rec->stream, B.rlabv, B.cmap, n};
   CHOPPER_HIP(launch("join_heads", k_join_heads, gn, dim3(kBlock), s, R,
-                     (const uint8_t*)nullptr, B.head, B.rkey, B.tcnt));
+                     B.head, B.rkey, B.tcnt));
   CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gn.x, B.tmp,
                                        B.tot, s));
   CHOPPER_HIP(launch("join_runs", k_join_runs, gn, dim3(kBlock), s, n,
