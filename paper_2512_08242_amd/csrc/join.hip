@@ -154,15 +154,22 @@ __global__ __launch_bounds__(kBlock) void k_join_heads(Seq S,
 
 // The same for a pass in class order: the class of a position comes from
 // the class offsets of the partition (coff[0 .. C]), so only the label and
-// the kernel class are read through the permutation.
+// the kernel class are read through the permutation.  Each wave takes 256
+// consecutive positions, four per lane (more gathers in flight per wave),
+// and writes the head count of its 256 positions (tcnt is per kBlock
+// positions, as k_join_runs reads it).
+constexpr int kHeadsIpt = 4;
 __global__ __launch_bounds__(kBlock) void k_join_heads_pass(
     int64_t m, const uint32_t* qorder, const uint32_t* label,
     const uint8_t* kcls, const uint32_t* coff, int C, uint32_t* head,
     uint64_t* key, uint32_t* tcnt) {
   __shared__ uint32_t s_off[256 + 1];
-  __shared__ uint32_t s_c[kWavesPerBlock];
   for (int c = threadIdx.x; c <= C; c += kBlock) s_off[c] = coff[c];
   __syncthreads();
+  const int lane = lane_id();
+  const int64_t W = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
+  const int64_t base = W * (kWave * kHeadsIpt);
+  if (base >= m) return;                                   // whole wave
   // class of position q: the last c < C with s_off[c] <= q
   auto cls_at = [&](int64_t q) {
     int lo = 0, hi = C;
@@ -173,31 +180,66 @@ __global__ __launch_bounds__(kBlock) void k_join_heads_pass(
     }
     return (uint32_t)lo;
   };
-  auto key_at = [&](int64_t q) {
-    const uint32_t e = qorder[q];
-    return (uint64_t)label[e] | (uint64_t)cls_at(q) << 32 |
-           (uint64_t)kcls[e] << 48;
-  };
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const bool ok = p < m;
-  const uint64_t kb = ok ? key_at(p) : 0ull;
-  uint64_t ka = wave_shr1_any((uint64_t)0, kb);
-  if (lane_id() == 0 && ok && p > 0) ka = key_at(p - 1);
+  const int64_t p0 = base + (int64_t)lane * kHeadsIpt;
+  uint32_t e[kHeadsIpt];
+  bool ok[kHeadsIpt];
+  if (p0 + kHeadsIpt <= m) {
+    const uint4 v = *reinterpret_cast<const uint4*>(qorder + p0);
+    e[0] = v.x; e[1] = v.y; e[2] = v.z; e[3] = v.w;
+#pragma unroll
+    for (int j = 0; j < kHeadsIpt; ++j) ok[j] = true;
+  } else {
+#pragma unroll
+    for (int j = 0; j < kHeadsIpt; ++j) {
+      ok[j] = p0 + j < m;
+      e[j] = ok[j] ? qorder[p0 + j] : 0u;
+    }
+  }
+  uint64_t k[kHeadsIpt];
+  uint32_t c = ok[0] ? cls_at(p0) : 0u;
+#pragma unroll
+  for (int j = 0; j < kHeadsIpt; ++j) {
+    if (!ok[j]) {
+      k[j] = 0ull;
+      continue;
+    }
+    while ((int)c + 1 < C && (int64_t)s_off[c + 1] <= p0 + j) ++c;
+    k[j] = (uint64_t)label[e[j]] | (uint64_t)c << 32 |
+           (uint64_t)kcls[e[j]] << 48;
+  }
+  // the predecessor of the lane's first position: the lane below's last
+  // key; lane 0 reads it
+  uint64_t ka = wave_shr1_any((uint64_t)0, k[kHeadsIpt - 1]);
+  if (lane == 0 && p0 > 0) {
+    const uint32_t ep = qorder[p0 - 1];
+    ka = (uint64_t)label[ep] | (uint64_t)cls_at(p0 - 1) << 32;
+  }
   const uint64_t kMask = 0x0000FFFFFFFFFFFFull;    // class and label
-  uint32_t h = 0;
-  if (ok && (uint32_t)kb != kNone) h = (p == 0 || ((ka ^ kb) & kMask) != 0);
-  if (ok) {
-    head[p] = h;
-    key[p] = kb;
+  uint32_t h[kHeadsIpt];
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int j = 0; j < kHeadsIpt; ++j) {
+    const uint64_t prev = j == 0 ? ka : k[j - 1];
+    h[j] = (ok[j] && (uint32_t)k[j] != kNone &&
+            (p0 + j == 0 || ((prev ^ k[j]) & kMask) != 0))
+               ? 1u
+               : 0u;
+    cnt += (uint32_t)__popcll(__ballot(h[j] != 0));
   }
-  const uint32_t c = (uint32_t)__popcll(__ballot(h != 0));
-  if (lane_id() == 0) s_c[threadIdx.x / kWave] = c;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t sum = 0;
-    for (int w = 0; w < kWavesPerBlock; ++w) sum += s_c[w];
-    tcnt[blockIdx.x] = sum;
+  if (p0 + kHeadsIpt <= m) {
+    *reinterpret_cast<uint4*>(head + p0) = make_uint4(h[0], h[1], h[2], h[3]);
+    ulonglong2* kp = reinterpret_cast<ulonglong2*>(key + p0);
+    kp[0] = make_ulonglong2(k[0], k[1]);
+    kp[1] = make_ulonglong2(k[2], k[3]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < kHeadsIpt; ++j)
+      if (ok[j]) {
+        head[p0 + j] = h[j];
+        key[p0 + j] = k[j];
+      }
   }
+  if (lane == 0) tcnt[W] = cnt;
 }
 
 // run table: start position, (gpu, stream) and label of every run, the run
@@ -503,7 +545,10 @@ extern "C" int chopper_join_counters(
       rc = class_sort(kq, L, Q_.qorder, B.coff, &range_err, s, 1);
       if (rc != CHOPPER_OK) return rc;
       const dim3 gm = grid_for(m, kBlock);
-      CHOPPER_HIP(launch("join_heads", k_join_heads_pass, gm, dim3(kBlock), s,
+      CHOPPER_HIP(launch("join_heads", k_join_heads_pass,
+                         dim3((unsigned)ceil_div((int64_t)gm.x,
+                                                 (int64_t)kWavesPerBlock)),
+                         dim3(kBlock), s,
                          m, (const uint32_t*)Q_.qorder, P.label, P.cls,
                          (const uint32_t*)B.coff, (int)nclass + 1, B.qhead,
                          Q_.key, B.tcnt));
