@@ -360,34 +360,38 @@ __global__ __launch_bounds__(kBlock) void k_join_gather(
       kl = rlab[run];
       kk = cls[r];
     }
+    // the entry of every pass first (loads only, so that the passes'
+    // dependent chains overlap), then the values and the stores
+    int64_t q[kMaxPasses];
+#pragma unroll
+    for (int p = 0; p < kMaxPasses; ++p) {
+      q[p] = -1;
+      if (p >= J.np || run == kNone) continue;
+      const PassView& P = J.p[p];
+      const uint32_t qr = P.match[run];
+      if (qr == kNone) continue;
+      const int64_t pos = (int64_t)P.qstart[qr] + ord;
+      const int64_t q1 =
+          (int64_t)qr + 1 < (int64_t)*P.nq ? (int64_t)P.qstart[qr + 1] : P.m;
+      // the entry at the ordinal is the record's only if it still has the
+      // run's key (entries without an iteration may follow the run)
+      if (pos < q1) {
+        const uint64_t k = P.qkey[pos];
+        if ((uint32_t)k == kl && ((uint32_t)(k >> 32) & 0xFFFFu) == kc &&
+            (uint32_t)(k >> 48) == kk)
+          q[p] = P.qorder[pos];
+      }
+    }
     uint32_t bits = 0;
 #pragma unroll
     for (int p = 0; p < kMaxPasses; ++p) {
       if (p >= J.np) break;
       const PassView& P = J.p[p];
-      int64_t q = -1;
-      if (run != kNone) {
-        const uint32_t qr = P.match[run];
-        if (qr != kNone) {
-          const int64_t pos = (int64_t)P.qstart[qr] + ord;
-          const int64_t q1 = (int64_t)qr + 1 < (int64_t)*P.nq
-                                 ? (int64_t)P.qstart[qr + 1]
-                                 : P.m;
-          // the entry at the ordinal is the record's only if it still has
-          // the run's key (entries without an iteration may follow the run)
-          if (pos < q1) {
-            const uint64_t k = P.qkey[pos];
-            if ((uint32_t)k == kl && ((uint32_t)(k >> 32) & 0xFFFFu) == kc &&
-                (uint32_t)(k >> 48) == kk)
-              q = P.qorder[pos];
-          }
-        }
-        miss |= q < 0;
-      }
+      if (run != kNone && q[p] < 0) miss = true;
       for (int c = 0; c < P.n_cols; ++c)
         counters[(int64_t)P.dst[c] * n + r] =
-            q >= 0 ? P.values[(int64_t)c * P.m + q] : 0ull;
-      if (q >= 0) bits |= 1u << p;
+            q[p] >= 0 ? P.values[(int64_t)c * P.m + q[p]] : 0ull;
+      if (q[p] >= 0) bits |= 1u << p;
     }
     matched[r] = (uint8_t)bits;
   }
