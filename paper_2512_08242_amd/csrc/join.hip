@@ -121,35 +121,65 @@ __device__ inline uint64_t item_key(const Seq& S, uint32_t i) {
 // (gpu, stream, label) -- items without an iteration belong to no run, and
 // one of them between two items of a label starts a second run of it.  The
 // key of every position is kept for the later passes, which then read it
-// in sequence order.
-// The heads of a block of kBlock positions are also counted (tcnt), so that
-// the run numbers come from a scan of the block counts.
+// in sequence order.  Each wave takes 256 consecutive positions, four per
+// lane (more gathers in flight per wave), and writes the head count of its
+// 256 positions (tcnt is per kBlock positions, as k_join_runs reads it).
+constexpr int kHeadsIpt = 4;
 __global__ __launch_bounds__(kBlock) void k_join_heads(Seq S,
                                                        uint32_t* head,
                                                        uint64_t* key,
                                                        uint32_t* tcnt) {
-  __shared__ uint32_t s_c[kWavesPerBlock];
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const bool ok = p < S.n;
-  const uint64_t kb = ok ? item_key(S, S.idx[p]) : 0ull;
-  // the predecessor's key from the lane below; lane 0 loads it
-  uint64_t ka = wave_shr1_any((uint64_t)0, kb);
-  if (lane_id() == 0 && ok && p > 0) ka = item_key(S, S.idx[p - 1]);
-  const uint64_t kMask = 0x0000FFFFFFFFFFFFull;    // class and label
-  uint32_t h = 0;
-  if (ok && (uint32_t)kb != kNone) h = (p == 0 || ((ka ^ kb) & kMask) != 0);
-  if (ok) {
-    head[p] = h;
-    key[p] = kb;
+  const int lane = lane_id();
+  const int64_t W = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
+  const int64_t base = W * (kWave * kHeadsIpt);
+  if (base >= S.n) return;                                 // whole wave
+  const int64_t p0 = base + (int64_t)lane * kHeadsIpt;
+  uint32_t e[kHeadsIpt];
+  bool ok[kHeadsIpt];
+  // (vector loads only from a 16-byte aligned order)
+  if (p0 + kHeadsIpt <= S.n && ((uintptr_t)S.idx & 15) == 0) {
+    const uint4 v = *reinterpret_cast<const uint4*>(S.idx + p0);
+    e[0] = v.x; e[1] = v.y; e[2] = v.z; e[3] = v.w;
+#pragma unroll
+    for (int j = 0; j < kHeadsIpt; ++j) ok[j] = true;
+  } else {
+#pragma unroll
+    for (int j = 0; j < kHeadsIpt; ++j) {
+      ok[j] = p0 + j < S.n;
+      e[j] = ok[j] ? S.idx[p0 + j] : 0u;
+    }
   }
-  const uint32_t c = (uint32_t)__popcll(__ballot(h != 0));
-  if (lane_id() == 0) s_c[threadIdx.x / kWave] = c;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t sum = 0;
-    for (int w = 0; w < kWavesPerBlock; ++w) sum += s_c[w];
-    tcnt[blockIdx.x] = sum;
+  uint64_t k[kHeadsIpt];
+#pragma unroll
+  for (int j = 0; j < kHeadsIpt; ++j) k[j] = ok[j] ? item_key(S, e[j]) : 0ull;
+  // the predecessor of the lane's first position: the lane below's last
+  // key; lane 0 reads it
+  uint64_t ka = wave_shr1_any((uint64_t)0, k[kHeadsIpt - 1]);
+  if (lane == 0 && p0 > 0) ka = item_key(S, S.idx[p0 - 1]);
+  uint32_t h[kHeadsIpt];
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int j = 0; j < kHeadsIpt; ++j) {
+    const uint64_t prev = j == 0 ? ka : k[j - 1];
+    h[j] = (ok[j] && (uint32_t)k[j] != kNone && (p0 + j == 0 || prev != k[j]))
+               ? 1u
+               : 0u;
+    cnt += (uint32_t)__popcll(__ballot(h[j] != 0));
   }
+  if (p0 + kHeadsIpt <= S.n) {
+    *reinterpret_cast<uint4*>(head + p0) = make_uint4(h[0], h[1], h[2], h[3]);
+    ulonglong2* kp = reinterpret_cast<ulonglong2*>(key + p0);
+    kp[0] = make_ulonglong2(k[0], k[1]);
+    kp[1] = make_ulonglong2(k[2], k[3]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < kHeadsIpt; ++j)
+      if (ok[j]) {
+        head[p0 + j] = h[j];
+        key[p0 + j] = k[j];
+      }
+  }
+  if (lane == 0) tcnt[W] = cnt;
 }
 
 // The same for a pass in class order: the class of a position comes from
@@ -158,7 +188,6 @@ __global__ __launch_bounds__(kBlock) void k_join_heads(Seq S,
 // consecutive positions, four per lane (more gathers in flight per wave),
 // and writes the head count of its 256 positions (tcnt is per kBlock
 // positions, as k_join_runs reads it).
-constexpr int kHeadsIpt = 4;
 __global__ __launch_bounds__(kBlock) void k_join_heads_pass(
     int64_t m, const uint32_t* qorder, const uint32_t* label,
     const uint8_t* kcls, const uint32_t* coff, int C, uint32_t* head,
@@ -513,8 +542,10 @@ extern "C" int chopper_join_counters(
                      n, idx + (int64_t)iter_level * n, nm, mk->label,
                      B.rlabv));
   const Seq R{order, rec->gpu, rec->stream, B.rlabv, B.cmap, n};
-  CHOPPER_HIP(launch("join_heads", k_join_heads, gn, dim3(kBlock), s, R,
-                     B.head, B.rkey, B.tcnt));
+  CHOPPER_HIP(launch("join_heads", k_join_heads,
+                     dim3((unsigned)ceil_div((int64_t)gn.x,
+                                             (int64_t)kWavesPerBlock)),
+                     dim3(kBlock), s, R, B.head, B.rkey, B.tcnt));
   CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gn.x, B.tmp,
                                        B.tot, s));
   CHOPPER_HIP(launch("join_runs", k_join_runs, gn, dim3(kBlock), s, n,
