@@ -4,8 +4,9 @@
 // eqs. 6-10).
 //
 // The instances (compute rows of the operation level) are partitioned by
-// (phase, operation) group into compact columns of the overlap ratio (Q30),
-// the time and three counters.  Blocks of 8192 instances of one group then
+// (phase, operation) group into compact columns of the overlap ratio (Q30)
+// and the time (the grouping pass adds the three counters of every group in
+// LDS on the way).  Blocks of 8192 instances of one group then
 // add the exact moments in 64-bit words (halves of the products that would
 // overflow) -- integer sums do not depend on their order, so the derived
 // doubles are the same IEEE operations on the same values as anywhere else
@@ -26,7 +27,7 @@ constexpr int kStatIpt = 8;
 constexpr int kRowSpan = kStatT * kStatIpt;   // rows per block
 constexpr int kChunk = kStatT * kStatIpt;     // instances per block
 constexpr int kRanks = 6;                     // order statistics per group
-constexpr int kSums = 11;                     // exact sums per group
+constexpr int kSums = 8;                      // exact moment words per group
 constexpr int kStats = 17;
 typedef __int128 i128;
 typedef unsigned __int128 u128;
@@ -94,9 +95,10 @@ __device__ inline uint32_t lds_claim(uint32_t* h, uint32_t bin, bool act) {
 }
 
 __global__ void k_stats_clear(uint32_t* cnt, int G, uint32_t* hist,
-                              int64_t nh) {
+                              int64_t nh, uint64_t* csum) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < G) cnt[i] = 0;
+  if (i < 3 * (int64_t)G) csum[i] = 0;
   if (i < nh) hist[i] = 0;
 }
 
@@ -105,10 +107,16 @@ __global__ void k_stats_clear(uint32_t* cnt, int G, uint32_t* hist,
 // the instances per group
 __global__ __launch_bounds__(kStatT) void k_stats_keys(StatArgs A,
                                                        uint32_t* key,
-                                                       uint32_t* cnt) {
+                                                       uint32_t* cnt,
+                                                       uint64_t* csum) {
   __shared__ uint32_t s_h[kMaxGroups];
+  __shared__ uint64_t s_cs[3][kMaxGroups];   // counter sums (wrap mod 2^64)
   const int G = A.P * A.O;
-  for (int g = threadIdx.x; g < G; g += kStatT) s_h[g] = 0;
+  const bool ctr = A.nc >= 16;
+  for (int g = threadIdx.x; g < G; g += kStatT) {
+    s_h[g] = 0;
+    s_cs[0][g] = s_cs[1][g] = s_cs[2][g] = 0;
+  }
   __syncthreads();
   int64_t lo, hi;
   level_range(A, lo, hi);
@@ -137,10 +145,25 @@ __global__ __launch_bounds__(kStatT) void k_stats_keys(StatArgs A,
     }
     if (r < hi) key[r - lo] = g;
     lds_claim(s_h, g, g != kNone);
+    // GPU cycles, MFMA-busy cycles and FLOPs of the instance (eqs. 7, 8, 10)
+    if (ctr && g != kNone) {
+      atomicAdd((unsigned long long*)&s_cs[0][g],
+                (unsigned long long)A.ctr[0 * A.cap + r]);
+      atomicAdd((unsigned long long*)&s_cs[1][g],
+                (unsigned long long)A.ctr[1 * A.cap + r]);
+      atomicAdd((unsigned long long*)&s_cs[2][g],
+                (unsigned long long)A.ctr[11 * A.cap + r]);
+    }
   }
   __syncthreads();
   for (int g = threadIdx.x; g < G; g += kStatT)
-    if (s_h[g]) atomicAdd(&cnt[g], s_h[g]);
+    if (s_h[g]) {
+      atomicAdd(&cnt[g], s_h[g]);
+      if (ctr)
+        for (int f = 0; f < 3; ++f)
+          atomicAdd((unsigned long long*)&csum[3 * g + f],
+                    (unsigned long long)s_cs[f][g]);
+    }
 }
 
 // group offsets, fill cursors, chunk offsets and the ranks to select (one
@@ -201,7 +224,7 @@ __global__ __launch_bounds__(kStatT) void k_stats_offsets(
 // order statistics)
 __global__ __launch_bounds__(kStatT) void k_stats_scatter(
     StatArgs A, const uint32_t* key, uint32_t* cur, uint32_t* xs,
-    uint64_t* ys, uint64_t* cs, int64_t ncap, uint32_t* status) {
+    uint64_t* ys, uint32_t* status) {
   __shared__ uint32_t s_n[kMaxGroups];
   __shared__ uint32_t s_base[kMaxGroups];
   const int G = A.P * A.O;
@@ -241,11 +264,6 @@ __global__ __launch_bounds__(kStatT) void k_stats_scatter(
     const uint32_t pos = s_base[g[k]] + slot[k];
     xs[pos] = (uint32_t)x;
     ys[pos] = y;
-    if (A.nc >= 16) {
-      cs[pos] = A.ctr[0 * A.cap + r];
-      cs[ncap + pos] = A.ctr[1 * A.cap + r];
-      cs[2 * ncap + pos] = A.ctr[11 * A.cap + r];
-    }
   }
   if (__ballot(big) != 0 && lane_id() == 0)
     atomicOr(status, CHOPPER_ST_RANGE);
@@ -292,11 +310,11 @@ __device__ inline void block_sums(uint64_t (&v)[kSums],
 // digits equal the rank's selected prefix) into the group's global
 // histograms.  The first pass has one histogram (no prefix yet) and also
 // writes the chunk's sums of x, y, x^2, y^2, xy (in 32-bit halves where they
-// would overflow) and the three counters.
+// would overflow); the counter sums come from the grouping pass.
 template <bool First>
 __global__ __launch_bounds__(kStatT) void k_stats_pass(
     const uint32_t* off, const uint32_t* coff, int G, const uint32_t* xs,
-    const uint64_t* ys, const uint64_t* cs, int64_t ncap, int nc,
+    const uint64_t* ys,
     const uint32_t* spre, int sh, uint32_t* ghist, uint64_t* part) {
   __shared__ uint32_t s_h[kRanks * 256];
   __shared__ uint64_t s_w[kStatT / kWave][kSums];
@@ -334,11 +352,6 @@ __global__ __launch_bounds__(kStatT) void k_stats_pass(
         acc[5] += (uint64_t)(yy >> 32);
         acc[6] += xy & 0xFFFFFFFFull;
         acc[7] += xy >> 32;
-        if (nc >= 16) {
-          acc[8] += cs[i];
-          acc[9] += cs[ncap + i];
-          acc[10] += cs[2 * ncap + i];
-        }
       }
     } else {
 #pragma unroll
@@ -404,7 +417,8 @@ struct StatOut {
 // same IEEE operations as their definition
 __global__ __launch_bounds__(kBlock) void k_stats_final(
     const uint32_t* cnt, const uint32_t* coff, int G, int O, int nc,
-    const uint64_t* part, const uint32_t* spre, StatOut S) {
+    const uint64_t* part, const uint64_t* csum, const uint32_t* spre,
+    StatOut S) {
   __shared__ uint64_t s_w[kBlock / kWave][kSums];
   __shared__ uint64_t s_tot[kSums];
   const int g = blockIdx.x, t = threadIdx.x;
@@ -431,7 +445,8 @@ __global__ __launch_bounds__(kBlock) void k_stats_final(
   const i128 sxx = ((i128)s_tot[3] << 32) + (i128)s_tot[2];
   const i128 syy = ((i128)s_tot[5] << 32) + (i128)s_tot[4];
   const i128 sxy = ((i128)s_tot[7] << 32) + (i128)s_tot[6];
-  const uint64_t cyc = s_tot[8], busy = s_tot[9], flops = s_tot[10];
+  const uint64_t cyc = csum[3 * g], busy = csum[3 * g + 1],
+                 flops = csum[3 * g + 2];
   const i128 im = (i128)m;
   const i128 cov = im * sxy - sx * sy;
   const i128 vx = im * sxx - sx * sx;
@@ -498,12 +513,11 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
   if (mk->n > 0 && !mk->label) return CHOPPER_EINVAL;
   const int G = P * O;
   const int64_t cap = rows->cap;
-  const int64_t ncs = n_counters >= 16 ? 3 * cap : 1;
   const int64_t nchunk = ceil_div(cap, kChunk) + G;
   const int64_t nh = (int64_t)G * kRanks * 256;
   struct Bufs {
     uint32_t *key, *gcnt, *off, *cur, *coff, *xs, *ghist, *spre;
-    uint64_t *ys, *cs, *part;
+    uint64_t *ys, *csum, *part;
     int64_t* srank;
   } B;
   auto layout = [&](Scratch& sc) {
@@ -514,7 +528,7 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
     B.coff = sc.take<uint32_t>(G + 1);
     B.xs = sc.take<uint32_t>(cap);
     B.ys = sc.take<uint64_t>(cap);
-    B.cs = sc.take<uint64_t>(ncs);
+    B.csum = sc.take<uint64_t>(3 * (int64_t)G);
     B.part = sc.take<uint64_t>(nchunk * kSums);
     B.ghist = sc.take<uint32_t>(nh);
     B.spre = sc.take<uint32_t>((int64_t)G * kRanks);
@@ -535,16 +549,15 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
             spec->f_gemm != nullptr, {0}};
   for (int o = 0; o < O && spec->f_gemm; ++o) S.f_gemm[o] = spec->f_gemm[o];
   CHOPPER_HIP(launch("stats_clear", k_stats_clear, grid_for(nh, kBlock),
-                     dim3(kBlock), s, B.gcnt, G, B.ghist, nh));
+                     dim3(kBlock), s, B.gcnt, G, B.ghist, nh, B.csum));
   const dim3 rb((unsigned)ceil_div(cap > 0 ? cap : 1, (int64_t)kRowSpan));
   CHOPPER_HIP(launch("stats_keys", k_stats_keys, rb, dim3(kStatT), s, A,
-                     B.key, B.gcnt));
+                     B.key, B.gcnt, B.csum));
   CHOPPER_HIP(launch("stats_offsets", k_stats_offsets, dim3(1), dim3(kStatT),
                      s, (const uint32_t*)B.gcnt, G, B.off, B.cur, B.coff,
                      B.spre, B.srank));
   CHOPPER_HIP(launch("stats_scatter", k_stats_scatter, rb, dim3(kStatT), s,
-                     A, (const uint32_t*)B.key, B.cur, B.xs, B.ys, B.cs, cap,
-                     status));
+                     A, (const uint32_t*)B.key, B.cur, B.xs, B.ys, status));
   for (int pass = 0; pass < 4; ++pass) {
     const int sh = 24 - 8 * pass;
     CHOPPER_HIP(launch("stats_pass",
@@ -552,7 +565,6 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
                        dim3((unsigned)nchunk), dim3(kStatT), s,
                        (const uint32_t*)B.off, (const uint32_t*)B.coff, G,
                        (const uint32_t*)B.xs, (const uint64_t*)B.ys,
-                       (const uint64_t*)B.cs, cap, n_counters,
                        (const uint32_t*)B.spre, sh, B.ghist, B.part));
     CHOPPER_HIP(launch("stats_select", k_stats_select, dim3((unsigned)G),
                        dim3(kRanks * kWave), s, (const uint32_t*)B.gcnt, sh,
@@ -561,7 +573,8 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
   CHOPPER_HIP(launch("stats_final", k_stats_final, dim3((unsigned)G),
                      dim3(kBlock), s, (const uint32_t*)B.gcnt,
                      (const uint32_t*)B.coff, G, O, n_counters,
-                     (const uint64_t*)B.part, (const uint32_t*)B.spre, S));
+                     (const uint64_t*)B.part, (const uint64_t*)B.csum,
+                     (const uint32_t*)B.spre, S));
   return CHOPPER_OK;
 }
 
