@@ -272,29 +272,51 @@ __global__ __launch_bounds__(kBlock) void k_join_heads_pass(
 }
 
 // run table: start position, (gpu, stream) and label of every run, the run
-// number of a head being the heads before it (block prefix tpre + the
-// heads below it in its block); excl (optional) gets that count at every
-// position
+// number of a head being the heads before it (prefix tpre of its 256
+// positions + the heads before it among them); excl (optional) gets that
+// count at every position.  Each wave takes 256 consecutive positions, four
+// per lane, as the heads passes do.
 __global__ __launch_bounds__(kBlock) void k_join_runs(
     int64_t n, const uint32_t* head, const uint32_t* tpre,
     const uint64_t* key, uint32_t* rstart, uint32_t* rcls, uint32_t* rlab,
     uint32_t* excl) {
-  __shared__ uint32_t s_c[kWavesPerBlock];
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const uint32_t h = p < n ? head[p] : 0u;
-  const uint64_t m = __ballot(h != 0);
-  const int w = threadIdx.x / kWave;
-  if (lane_id() == 0) s_c[w] = (uint32_t)__popcll(m);
-  __syncthreads();
-  uint32_t r = tpre[blockIdx.x] + lanes_below(m);
-  for (int q = 0; q < w; ++q) r += s_c[q];
-  if (p >= n) return;
-  if (excl) excl[p] = r;
-  if (!h) return;
-  const uint64_t k = key[p];
-  rstart[r] = (uint32_t)p;
-  rcls[r] = (uint32_t)(k >> 32) & 0xFFFFu;
-  rlab[r] = (uint32_t)k;
+  const int lane = lane_id();
+  const int64_t W = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
+  const int64_t base = W * (kWave * kHeadsIpt);
+  if (base >= n) return;                                   // whole wave
+  const int64_t p0 = base + (int64_t)lane * kHeadsIpt;
+  const bool full = p0 + kHeadsIpt <= n;
+  uint32_t h[kHeadsIpt];
+  if (full) {
+    const uint4 v = *reinterpret_cast<const uint4*>(head + p0);
+    h[0] = v.x; h[1] = v.y; h[2] = v.z; h[3] = v.w;
+  } else {
+#pragma unroll
+    for (int j = 0; j < kHeadsIpt; ++j) h[j] = p0 + j < n ? head[p0 + j] : 0u;
+  }
+  const uint32_t c = h[0] + h[1] + h[2] + h[3];
+  uint32_t r = tpre[W] + wave_incl(c, OpAdd(), 0u) - c;
+  uint32_t ex[kHeadsIpt];
+#pragma unroll
+  for (int j = 0; j < kHeadsIpt; ++j) {
+    ex[j] = r;
+    if (h[j]) {
+      const int64_t p = p0 + j;
+      const uint64_t k = key[p];
+      rstart[r] = (uint32_t)p;
+      rcls[r] = (uint32_t)(k >> 32) & 0xFFFFu;
+      rlab[r] = (uint32_t)k;
+    }
+    r += h[j];
+  }
+  if (!excl) return;
+  if (full) {
+    *reinterpret_cast<uint4*>(excl + p0) = make_uint4(ex[0], ex[1], ex[2], ex[3]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < kHeadsIpt; ++j)
+      if (p0 + j < n) excl[p0 + j] = ex[j];
+  }
 }
 
 // run and ordinal of every record, stored at the record (NONE: no
@@ -548,7 +570,8 @@ extern "C" int chopper_join_counters(
                      dim3(kBlock), s, R, B.head, B.rkey, B.tcnt));
   CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gn.x, B.tmp,
                                        B.tot, s));
-  CHOPPER_HIP(launch("join_runs", k_join_runs, gn, dim3(kBlock), s, n,
+  const dim3 gw((unsigned)ceil_div((int64_t)gn.x, (int64_t)kWavesPerBlock));
+  CHOPPER_HIP(launch("join_runs", k_join_runs, gw, dim3(kBlock), s, n,
                      (const uint32_t*)B.head, (const uint32_t*)B.tpre,
                      (const uint64_t*)B.rkey, B.rstart, B.rcls, B.rlab,
                      B.excl));
@@ -589,7 +612,10 @@ extern "C" int chopper_join_counters(
                          Q_.key, B.tcnt));
       CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gm.x,
                                            B.tmp, nq, s));
-      CHOPPER_HIP(launch("join_runs", k_join_runs, gm, dim3(kBlock), s, m,
+      CHOPPER_HIP(launch("join_runs", k_join_runs,
+                         dim3((unsigned)ceil_div((int64_t)gm.x,
+                                                 (int64_t)kWavesPerBlock)),
+                         dim3(kBlock), s, m,
                          (const uint32_t*)B.qhead, (const uint32_t*)B.tpre,
                          (const uint64_t*)Q_.key, Q_.qstart, B.qcls, B.qlab,
                          (uint32_t*)nullptr));
