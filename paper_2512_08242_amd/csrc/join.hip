@@ -46,20 +46,61 @@ __global__ void k_join_fill_u8(uint8_t* p, int64_t n, uint32_t* pres) {
 }
 
 // iteration label of every record (NONE: no iteration marker)
-__global__ void k_join_rec_labels(int64_t n, const uint32_t* idx_iter,
-                                  int64_t nm, const uint32_t* m_label,
-                                  uint32_t* lab) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const uint32_t m = idx_iter[i];
-  lab[i] = (int64_t)m < nm ? m_label[m] : kNone;
+// (four per lane: more label gathers in flight)
+__global__ __launch_bounds__(kBlock) void k_join_rec_labels(
+    int64_t n, const uint32_t* idx_iter, int64_t nm, const uint32_t* m_label,
+    uint32_t* lab) {
+  const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i0 >= n) return;
+  uint32_t m[4], l[4];
+  const bool full = i0 + 4 <= n && ((uintptr_t)idx_iter & 15) == 0;
+  if (full) {
+    const uint4 v = *reinterpret_cast<const uint4*>(idx_iter + i0);
+    m[0] = v.x; m[1] = v.y; m[2] = v.z; m[3] = v.w;
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) m[j] = i0 + j < n ? idx_iter[i0 + j] : kNone;
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) l[j] = (int64_t)m[j] < nm ? m_label[m[j]] : kNone;
+  if (full) {
+    *reinterpret_cast<uint4*>(lab + i0) = make_uint4(l[0], l[1], l[2], l[3]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (i0 + j < n) lab[i0 + j] = l[j];
+  }
 }
 
 // the (gpu, stream) pairs of the records
-__global__ void k_join_presence(int64_t n, const uint8_t* gpu,
-                                const uint8_t* stream, uint8_t* pres) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) pres[(uint32_t)gpu[i] * 256u + stream[i]] = 1;
+// Four records per lane (word loads of the byte columns); a pair is written
+// only where it differs from the record before: records come in long runs
+// of one pair, and equal writes would queue on one byte.
+__global__ __launch_bounds__(kBlock) void k_join_presence(
+    int64_t n, const uint8_t* gpu, const uint8_t* stream, uint8_t* pres) {
+  const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  uint32_t pr[4];
+  const bool full = i0 + 4 <= n && ((uintptr_t)gpu & 3) == 0 &&
+                    ((uintptr_t)stream & 3) == 0;
+  if (full) {
+    const uint32_t g4 = *reinterpret_cast<const uint32_t*>(gpu + i0);
+    const uint32_t s4 = *reinterpret_cast<const uint32_t*>(stream + i0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      pr[j] = ((g4 >> (8 * j)) & 255u) * 256u + ((s4 >> (8 * j)) & 255u);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      pr[j] = i0 + j < n ? (uint32_t)gpu[i0 + j] * 256u + stream[i0 + j]
+                         : kNone;
+  }
+  uint32_t prev = wave_shr1_u32(kNone, pr[3]);
+  if (lane_id() == 0) prev = kNone;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (pr[j] != kNone && pr[j] != prev) pres[pr[j]] = 1;
+    prev = pr[j];
+  }
 }
 
 // Dense class ids of the records' (gpu, stream) pairs in (gpu, stream)
@@ -551,7 +592,8 @@ extern "C" int chopper_join_counters(
   // dense classes of the records' (gpu, stream) pairs (one read-back)
   CHOPPER_HIP(launch("join_fill", k_join_fill_u8, dim3(64), dim3(kBlock), s,
                      (uint8_t*)nullptr, (int64_t)0, (uint32_t*)B.pres));
-  CHOPPER_HIP(launch("join_pass_prep", k_join_presence, gn, dim3(kBlock), s,
+  CHOPPER_HIP(launch("join_pass_prep", k_join_presence,
+                     grid_for(n, kBlock * 4), dim3(kBlock), s,
                      n, rec->gpu, rec->stream, B.pres));
   CHOPPER_HIP(launch("join_dense", k_join_dense, dim3(1), dim3(kDenseT), s,
                      (const uint8_t*)B.pres, B.cmap, B.tot + 1));
@@ -560,7 +602,8 @@ extern "C" int chopper_join_counters(
   // (pass entries of other pairs take one more class)
   if (nclass + 1 > 256) return CHOPPER_EINVAL;
   // the records' runs along `order`, then each record's run and ordinal
-  CHOPPER_HIP(launch("join_labels", k_join_rec_labels, gn, dim3(kBlock), s,
+  CHOPPER_HIP(launch("join_labels", k_join_rec_labels,
+                     grid_for(n, kBlock * 4), dim3(kBlock), s,
                      n, idx + (int64_t)iter_level * n, nm, mk->label,
                      B.rlabv));
   const Seq R{order, rec->gpu, rec->stream, B.rlabv, B.cmap, n};
