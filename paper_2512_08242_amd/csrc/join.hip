@@ -394,11 +394,14 @@ __global__ void k_join_order(const uint32_t* nruns, const uint32_t* rcls,
     atomicOr(status, CHOPPER_ST_JOIN_ORDER);
 }
 
-// pass run of every record run: binary search by (gpu, stream, label)
+// pass run of every record run: binary search by (gpu, stream, label); the
+// record run gets the class-order positions [start, next run's start) of
+// that pass run, or an empty range
 __global__ void k_join_match(const uint32_t* nr, const uint32_t* rcls,
                              const uint32_t* rlab, const uint32_t* nq,
                              const uint32_t* qcls, const uint32_t* qlab,
-                             uint32_t* match) {
+                             const uint32_t* qstart, int64_t m,
+                             uint2* match) {
   const int64_t n_r = (int64_t)*nr, n_q = (int64_t)*nq;
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < n_r;
        r += (int64_t)gridDim.x * blockDim.x) {
@@ -412,15 +415,17 @@ __global__ void k_join_match(const uint32_t* nr, const uint32_t* rcls,
     }
     const bool hit =
         lo < n_q && ((uint64_t)qcls[lo] << 32 | qlab[lo]) == key;
-    match[r] = hit ? (uint32_t)lo : kNone;
+    match[r] = hit ? make_uint2(qstart[lo], lo + 1 < n_q
+                                                ? qstart[lo + 1]
+                                                : (uint32_t)m)
+                   : make_uint2(0u, 0u);
   }
 }
 
 // one pass as the gather sees it
 struct PassView {
-  const uint32_t* match;    // record run -> pass run (NONE: no such run)
-  const uint32_t* qstart;   // pass run -> first position in class order
-  const uint32_t* nq;       // number of pass runs (device)
+  const uint2* match;       // record run -> class-order positions of its
+                            // pass run [x, y) (empty: no such run)
   const uint32_t* qorder;   // class-order position -> entry
   const uint64_t* qkey;     // class-order position -> entry key
   const uint64_t* values;   // [n_cols][m]
@@ -460,14 +465,11 @@ __global__ __launch_bounds__(kBlock) void k_join_gather(
       q[p] = -1;
       if (p >= J.np || run == kNone) continue;
       const PassView& P = J.p[p];
-      const uint32_t qr = P.match[run];
-      if (qr == kNone) continue;
-      const int64_t pos = (int64_t)P.qstart[qr] + ord;
-      const int64_t q1 =
-          (int64_t)qr + 1 < (int64_t)*P.nq ? (int64_t)P.qstart[qr + 1] : P.m;
+      const uint2 qr = P.match[run];
+      const int64_t pos = (int64_t)qr.x + ord;
       // the entry at the ordinal is the record's only if it still has the
       // run's key (entries without an iteration may follow the run)
-      if (pos < q1) {
+      if (pos < (int64_t)qr.y) {
         const uint64_t k = P.qkey[pos];
         if ((uint32_t)k == kl && ((uint32_t)(k >> 32) & 0xFFFFu) == kc &&
             (uint32_t)(k >> 48) == kk)
@@ -528,7 +530,8 @@ extern "C" int chopper_join_counters(
   // temporaries (reused) and what the gather reads of every pass
   const int64_t nmax = n > mmax ? n : mmax;
   struct PassBuf {
-    uint32_t *match, *qstart, *qorder;
+    uint2* match;
+    uint32_t *qstart, *qorder;
     uint64_t* key;
   };
   struct Bufs {
@@ -562,7 +565,7 @@ extern "C" int chopper_join_counters(
     B.rord = sc.take<uint32_t>(n);
     for (int p = 0; p < n_passes; ++p) {
       const int64_t m = passes[p].n;
-      B.pb[p].match = sc.take<uint32_t>(n + 1);
+      B.pb[p].match = sc.take<uint2>(n + 1);
       B.pb[p].qstart = sc.take<uint32_t>(m + 1);
       B.pb[p].qorder = sc.take<uint32_t>(m);
       B.pb[p].key = sc.take<uint64_t>(m);
@@ -673,11 +676,9 @@ extern "C" int chopper_join_counters(
                        (const uint32_t*)B.tot, (const uint32_t*)B.rcls,
                        (const uint32_t*)B.rlab, (const uint32_t*)nq,
                        (const uint32_t*)B.qcls, (const uint32_t*)B.qlab,
-                       Q_.match));
+                       (const uint32_t*)Q_.qstart, m, Q_.match));
     PassView& V = J.p[p];
     V.match = Q_.match;
-    V.qstart = Q_.qstart;
-    V.nq = nq;
     V.qorder = Q_.qorder;
     V.qkey = Q_.key;
     V.values = P.values;
