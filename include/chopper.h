@@ -30,7 +30,8 @@
  * Memory.  Every pointer is a DEVICE pointer unless marked [host].  The caller
  * owns every buffer.  The library allocates no device memory, frees nothing
  * and keeps no data between calls; all temporary storage comes from the
- * caller's `scratch`.  Scratch protocol (every call taking scratch): pass
+ * caller's `scratch` (chopper_launch_split_noalloc alone uses a static 6 KiB
+ * device table of the library instead).  Scratch protocol (every call taking scratch): pass
  * scratch == NULL to receive the required size in *scratch_bytes (nothing
  * else is read or written, no GPU work is done, CHOPPER_OK is returned); then
  * call again with a buffer of at least that many bytes, 256-byte aligned.
@@ -416,6 +417,28 @@ int chopper_launch_split(const chopper_records* records,
                          int64_t* call_out, void* scratch,
                          size_t* scratch_bytes, uint32_t* status,
                          void* stream);
+
+/*
+ * chopper_launch_split_noalloc -- chopper_launch_split for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): same arguments and results, but
+ * no scratch argument.  The clock table that chopper_launch_split keeps in
+ * the caller's scratch lives here in a static device array of the library
+ * (256 entries of 24 bytes, 6 KiB per device, held by every device the
+ * library runs on until the process ends).  The call allocates and frees
+ * nothing; the device address of the array is looked up once per device, on
+ * the first call made on it.  Limits: n_gpus <= 256 (CHOPPER_ESCRATCH
+ * otherwise, nothing enqueued); `stream` must belong to the current device
+ * (CHOPPER_EHIP otherwise).  The table is rewritten by every call before its
+ * kernel reads it, so nothing needs clearing, but calls that overlap on one
+ * GPU (different streams, or threads) race on it: serialize them.
+ */
+int chopper_launch_split_noalloc(const chopper_records* records,
+                                 const chopper_clock* clocks,
+                                 const int64_t* launch_ns,
+                                 const int64_t* start_al, const int64_t* gap,
+                                 int64_t* prep_out, int64_t* call_out,
+                                 uint32_t* status, void* stream);
 
 /*
  * chopper_join_counters -- counters of serialized hardware-profiling passes

@@ -138,6 +138,9 @@ def _load():
     lib.chopper_launch_split.argtypes = [ctypes.POINTER(Records),
                                          ctypes.POINTER(Clock), P, P, P, P, P,
                                          P, SZ, P, P]
+    lib.chopper_launch_split_noalloc.argtypes = [ctypes.POINTER(Records),
+                                                 ctypes.POINTER(Clock), P, P,
+                                                 P, P, P, P, P]
     lib.chopper_op_stats.argtypes = [ctypes.POINTER(Rows), i32, i32,
                                      ctypes.POINTER(Markers),
                                      ctypes.POINTER(StatsSpec), P, P, P, SZ,
@@ -161,7 +164,8 @@ def _load():
                  "chopper_aggregate", "chopper_ratios",
                  "chopper_window_fractions", "chopper_version",
                  "chopper_time_kernel", "chopper_views",
-                 "chopper_launch_split", "chopper_join_counters",
+                 "chopper_launch_split", "chopper_launch_split_noalloc",
+                 "chopper_join_counters",
                  "chopper_op_stats"):
         getattr(lib, name).restype = ctypes.c_int
     return lib
@@ -460,6 +464,23 @@ class Pipeline:
             self._scr["launch"] = _scratch(go, dev)
         scr, sb = _aligned(self._scr["launch"])
         _check(go(scr, ctypes.byref(sb)), "launch_split")
+        return prep[:dt.n], call[:dt.n]
+
+    def launch_split_noalloc(self, launch_ns: torch.Tensor, prep=None,
+                             call=None):
+        """chopper_launch_split_noalloc: the same split without scratch (the
+        library's static device table); writes into prep / call when given,
+        else into new tensors, and returns them."""
+        dt = self.dt
+        dev = dt.start.device
+        if prep is None:
+            prep = torch.empty(max(dt.n, 1), dtype=torch.int64, device=dev)
+        if call is None:
+            call = torch.empty(max(dt.n, 1), dtype=torch.int64, device=dev)
+        _check(lib.chopper_launch_split_noalloc(
+            ctypes.byref(self._rec), self.clocks, _ptr(launch_ns),
+            _ptr(self.start), _ptr(self.gap), _ptr(prep), _ptr(call),
+            _ptr(self.status), _stream()), "launch_split_noalloc")
         return prep[:dt.n], call[:dt.n]
 
     def op_stats(self, phase_level: int = 1, op_level: int = 3,

@@ -8,10 +8,18 @@
 // call overhead the rest.  One wave tile of records per wave, loads striped
 // across the lanes and all issued before any use; the clock table sits in
 // LDS.
+#include <mutex>
 #include <vector>
 
 #include "clock.h"
 #include "wave.h"
+
+// Scratch of chopper_launch_split_noalloc: the clock table of up to 256 GPUs
+// (6 KiB).  Every device the library runs on holds its own copy until the
+// process ends.  Host code never passes this name to a kernel or a copy (on
+// the host it is only a stand-in for the symbol); it uses the device address
+// that static_scratch() looks up once per device.
+static __device__ __align__(256) chopper::ClockDev scratch[256];
 
 namespace chopper {
 
@@ -20,6 +28,8 @@ bool validate_records(const chopper_records* r);
 namespace {
 
 constexpr int kMaxGpus = 256;
+static_assert(sizeof(::scratch) == kMaxGpus * sizeof(ClockDev),
+              "the static clock table holds kMaxGpus entries");
 
 __global__ __launch_bounds__(kBlock) void k_launch_split(
     int64_t n, int G, const uint8_t* gpu, const ClockDev* clk,
@@ -68,6 +78,36 @@ __global__ __launch_bounds__(kBlock) void k_launch_split(
   if (lane == 0 && v) atomicOr(status, v);
 }
 
+constexpr int kMaxDevices = 64;
+
+// Device address of `scratch` on the current device, looked up on the first
+// call made on that device.  The caller's stream must belong to the current
+// device (hipErrorInvalidDevice otherwise).
+hipError_t static_scratch(hipStream_t s, ClockDev** out) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  if (s != nullptr) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(s, &sdev);
+    if (e != hipSuccess) return e;
+    if ((int)sdev != dev) return hipErrorInvalidDevice;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(::scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = static_cast<ClockDev*>(addr[dev]);
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" int chopper_launch_split(const chopper_records* rec,
@@ -99,6 +139,46 @@ extern "C" int chopper_launch_split(const chopper_records* rec,
     cd[g] = ClockDev{clocks[g].x0, clocks[g].c, clocks[g].d_q48};
   // (a copy from pageable memory is staged before the call returns)
   CHOPPER_HIP(hipMemcpyAsync(clk, cd.data(), sizeof(ClockDev) * G,
+                             hipMemcpyHostToDevice, s));
+  CHOPPER_HIP(launch("launch_split", k_launch_split,
+                     dim3((unsigned)ceil_div(n, (int64_t)kWaveTile *
+                                                    kWavesPerBlock)),
+                     dim3(kBlock), s, n, G, rec->gpu, (const ClockDev*)clk,
+                     launch_ns, start_al, gap, prep_out, call_out, status));
+  return CHOPPER_OK;
+}
+
+
+// Allocation-free variant: the clock table lives in the library's static
+// device array instead of the caller's scratch.  No hipMalloc, hipFree or
+// other allocating call; the host side builds the table on its stack.
+extern "C" int chopper_launch_split_noalloc(const chopper_records* rec,
+                                            const chopper_clock* clocks,
+                                            const int64_t* launch_ns,
+                                            const int64_t* start_al,
+                                            const int64_t* gap,
+                                            int64_t* prep_out,
+                                            int64_t* call_out,
+                                            uint32_t* status, void* stream) {
+  if (!validate_records(rec) || !clocks || !status) return CHOPPER_EINVAL;
+  const int64_t n = rec->n;
+  const int G = rec->n_gpus;
+  if (n > 0 && (!rec->gpu || !launch_ns || !start_al || !gap || !prep_out ||
+                !call_out))
+    return CHOPPER_EINVAL;
+  // the static table holds the clocks of at most kMaxGpus GPUs
+  if (G < 1 || G > kMaxGpus) return CHOPPER_ESCRATCH;
+  if (n == 0) return CHOPPER_OK;
+  hipStream_t s = (hipStream_t)stream;
+  ClockDev* clk = nullptr;
+  CHOPPER_HIP(static_scratch(s, &clk));
+  ClockDev cd[kMaxGpus];
+  for (int g = 0; g < G; ++g)
+    cd[g] = ClockDev{clocks[g].x0, clocks[g].c, clocks[g].d_q48};
+  // every entry the kernel reads (0 .. G-1) is written here, so nothing left
+  // by an earlier call is read; a copy from pageable memory is staged before
+  // the call returns
+  CHOPPER_HIP(hipMemcpyAsync(clk, cd, sizeof(ClockDev) * G,
                              hipMemcpyHostToDevice, s));
   CHOPPER_HIP(launch("launch_split", k_launch_split,
                      dim3((unsigned)ceil_div(n, (int64_t)kWaveTile *

@@ -279,6 +279,28 @@ def test_launch_split_scratch_query_and_argument_errors(ch):
                                     None) == -1
 
 
+def test_launch_split_noalloc_argument_errors(ch):
+    """The allocation-free variant rejects missing pointers synchronously,
+    before any HIP call (no GPU here)."""
+    lib, b = ch.lib, ch.binding
+    fake = ctypes.c_void_p(0x1000)
+    rec = _records(ch, 1000)
+    clocks = (b.Clock * 2)()
+    for i in range(6):
+        args = [fake] * 6
+        args[i] = None
+        assert lib.chopper_launch_split_noalloc(
+            ctypes.byref(rec), clocks, *args[:5], fake if i < 5 else None,
+            None) == -1, i
+    assert lib.chopper_launch_split_noalloc(ctypes.byref(rec), None, fake,
+                                            fake, fake, fake, fake, fake,
+                                            None) == -1
+    rec.n_gpus = 257
+    assert lib.chopper_launch_split_noalloc(ctypes.byref(rec), clocks, fake,
+                                            fake, fake, fake, fake, fake,
+                                            None) == -1
+
+
 def test_op_stats_scratch_query_and_argument_errors(ch):
     """chopper_op_stats answers the scratch query without GPU work, sizes
     its scratch from the row capacity, and rejects bad specs synchronously."""
