@@ -91,12 +91,13 @@ enum {
   CHOPPER_ST_BAD_LEVEL = 64u,      /* marker level >= depth                 */
   CHOPPER_ST_PATH_CONFLICT = 128u, /* records sharing a deepest marker have
                                       different marker paths (markers not
-                                      nested); aggregate rows unspecified   */
+                                      nested): warning only, rows are still
+                                      grouped by the whole path            */
   CHOPPER_ST_JOIN_MISS = 256u,     /* a record with an iteration found no
                                       entry of some counter pass           */
-  CHOPPER_ST_JOIN_ORDER = 512u     /* iteration labels not increasing run by
-                                      run along a (gpu, stream): the join
-                                      is unspecified                       */
+  CHOPPER_ST_JOIN_ORDER = 512u     /* an iteration label below an earlier
+                                      one along a (gpu, stream): warning
+                                      only, the join is exactly defined    */
 };
 
 /* aggregation levels besides the marker levels 0 .. depth-1 */
@@ -281,7 +282,9 @@ int chopper_overlap(const chopper_records* records, const int64_t* start_al,
  * rows->level_offset is always written.  If the total exceeds rows->cap,
  * ROWS_OVERFLOW is set and the rows are unspecified.  When markers are not
  * nested so that two records with the same deepest marker have different
- * paths, PATH_CONFLICT is set and rows are unspecified.
+ * paths, PATH_CONFLICT is set (a warning); the rows are still those of the
+ * whole paths (the call then waits for `stream` once more and sorts the
+ * records by path, level by level).
  */
 int chopper_aggregate(const chopper_records* records, const int64_t* start_al,
                       const int64_t* end_al, const uint32_t* korder,
@@ -458,14 +461,17 @@ int chopper_launch_split_noalloc(const chopper_records* records,
  * counters_out [16][n] gets the entry's values in the pass's columns (0 when
  * nothing matches, and in columns no pass fills), bit p of matched_out [n]
  * is set for pass p.  Records and entries without an iteration never match.
+ * The ordinal is defined for any order of the labels: a label's kernels
+ * need not be consecutive along their (gpu, stream).
  * JOIN_MISS: a record with an iteration found no entry in some pass.
- * JOIN_ORDER (result unspecified): along a (gpu, stream), in either order,
- * a label's kernels are not consecutive apart from kernels without an
- * iteration, or labels do not increase from one label to the next.
+ * JOIN_ORDER (warning): along a (gpu, stream), in either order, an iteration
+ * label is below an earlier one (iterations out of time order).
  * n_passes <= 8; the records may hold at most 255 (gpu, stream) pairs
  * (CHOPPER_EINVAL otherwise; entries of other pairs never match).  Scratch
  * protocol as above (grows with n and the largest pass).  The call waits
- * once for `stream`: the number of the records' pairs is read back.
+ * for `stream` twice: the number of the records' pairs is read back, then
+ * one word saying which sides hold a label in more than one run (those
+ * sides are sorted by label, which waits again inside the sort).
  */
 typedef struct {
   int64_t n;

@@ -935,11 +935,11 @@ void orc_launch_split(int64_t n, const uint8_t* gpu, const uint8_t* stream,
  * destination counter column of the record and bit p of matched is set.
  * Columns no matched entry fills are 0.  Records and entries without an
  * iteration (label NONE) are never matched.  JOIN_MISS: some record with an
- * iteration found no matching entry in some pass.  JOIN_ORDER: along
- * (gpu, stream) in (start', index) order, or along a pass's own order, a
- * run of equal labels is not above the previous run with an iteration: a
- * label's kernels are not consecutive (kernels without an iteration aside)
- * or labels decrease (the library then leaves the result unspecified).
+ * iteration found no matching entry in some pass.  JOIN_ORDER (a warning:
+ * the join above is defined for any label order): along (gpu, stream) in
+ * (start', index) order, or along a pass's own order, an iteration label is
+ * smaller than an earlier one (NONE labels aside) -- iterations are
+ * annotated in time order (III-A), so the trace or the pass is out of order.
  * ------------------------------------------------------------------------ */
 #define ORC_JOIN_MISS 256u
 #define ORC_JOIN_ORDER 512u
@@ -976,16 +976,13 @@ static uint32_t join_ordinals(jrow_t* v, int64_t n) {
   uint32_t st = 0;
   qsort(v, (size_t)n, sizeof(jrow_t), cmp_jrow_time);
   {
-    /* runs of equal labels along each (g, st): the label of a run must be
-       above that of the previous run with an iteration */
-    uint32_t last = ORC_NONE;   /* label of the last run with an iteration */
+    /* along each (g, st): a label below the last label seen */
+    uint32_t last = ORC_NONE;   /* last label with an iteration */
     for (int64_t i = 0; i < n; ++i) {
-      const int first = i == 0 || v[i].g != v[i - 1].g ||
-                        v[i].st != v[i - 1].st;
-      if (first) last = ORC_NONE;
-      const int new_run = first || v[i].lab != v[i - 1].lab;
-      if (v[i].lab == ORC_NONE || !new_run) continue;
-      if (last != ORC_NONE && last >= v[i].lab) st |= ORC_JOIN_ORDER;
+      if (i == 0 || v[i].g != v[i - 1].g || v[i].st != v[i - 1].st)
+        last = ORC_NONE;
+      if (v[i].lab == ORC_NONE) continue;
+      if (last != ORC_NONE && v[i].lab < last) st |= ORC_JOIN_ORDER;
       last = v[i].lab;
     }
   }

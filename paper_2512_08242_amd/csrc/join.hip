@@ -6,12 +6,15 @@
 // A record and a pass entry match on (gpu, stream, iteration label,
 // ordinal) and class.  Both sides are brought into (gpu, stream) order --
 // the records by `order`, a pass by a stable class partition of its own
-// order -- and cut into runs of equal (gpu, stream, label): with every
-// label's records consecutive along its (gpu, stream) and labels increasing
-// (checked, JOIN_ORDER otherwise), a label is one run and the ordinal is the
-// position inside it.  Record runs find their pass run by a binary search
-// over the pass's run table; each record then reads entry run start +
-// ordinal.
+// order -- and cut into runs of equal (gpu, stream, label).  When along
+// every (gpu, stream) each label is one run and labels increase (what
+// iteration markers in time order give), the ordinal is the position
+// inside the run.  A side whose run table breaks that (checked on the
+// device, one flag word read back for all sides) is first sorted stably by
+// (gpu, stream, label), which keeps each label's time order, and cut into
+// runs again.  Record runs find their pass run by a binary search over the
+// pass's run table; each record then reads entry run start + ordinal.
+// JOIN_ORDER (a warning) marks labels that decrease along a (gpu, stream).
 #include <algorithm>
 #include <vector>
 
@@ -379,19 +382,36 @@ __global__ void k_join_rec_pos(int64_t n, const uint32_t* order,
   rord[r] = (uint32_t)p - rstart[run];
 }
 
-// JOIN_ORDER: a run whose label is not above that of the previous run of
-// its (gpu, stream); otherwise the run table is sorted by (gpu, stream,
-// label) and every label has one run
+// Run-table check: bit `bit` of *flag when a run's label is not above that
+// of the previous run of its (gpu, stream) -- a label in two runs, or labels
+// out of order: the side must be sorted by label first; JOIN_ORDER when a
+// label is below that of the previous run (labels decrease).  Otherwise the
+// table is sorted by (gpu, stream, label) and every label has one run.
 // (run tables are short: a fixed grid strides over them)
 __global__ void k_join_order(const uint32_t* nruns, const uint32_t* rcls,
-                             const uint32_t* rlab, uint32_t* status) {
+                             const uint32_t* rlab, uint32_t* status,
+                             uint32_t* flag, uint32_t bit) {
   const int64_t nr = (int64_t)*nruns;
-  bool bad = false;
+  bool split = false, dec = false;
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < nr;
        r += (int64_t)gridDim.x * blockDim.x)
-    if (r > 0 && rcls[r - 1] == rcls[r] && rlab[r - 1] >= rlab[r]) bad = true;
-  if (__ballot(bad) != 0 && lane_id() == 0)
-    atomicOr(status, CHOPPER_ST_JOIN_ORDER);
+    if (r > 0 && rcls[r - 1] == rcls[r]) {
+      split |= rlab[r - 1] >= rlab[r];
+      dec |= rlab[r - 1] > rlab[r];
+    }
+  const uint64_t any_split = __ballot(split), any_dec = __ballot(dec);
+  if (lane_id() == 0) {
+    if (any_split != 0) atomicOr(flag, bit);
+    if (any_dec != 0) atomicOr(status, CHOPPER_ST_JOIN_ORDER);
+  }
+}
+
+// out[q] = seq[perm[q]]: a sequence reordered by a permutation of its
+// positions
+__global__ void k_join_compose(int64_t n, const uint32_t* seq,
+                               const uint32_t* perm, uint32_t* out) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q < n) out[q] = seq[perm[q]];
 }
 
 // pass run of every record run: binary search by (gpu, stream, label); the
@@ -531,12 +551,12 @@ extern "C" int chopper_join_counters(
   const int64_t nmax = n > mmax ? n : mmax;
   struct PassBuf {
     uint2* match;
-    uint32_t *qstart, *qorder;
+    uint32_t *qstart, *qorder, *qcls, *qlab, *coff;
     uint64_t* key;
   };
   struct Bufs {
-    uint32_t *rlabv, *head, *excl, *rstart, *rcls, *rlab, *tot, *tmp, *coff;
-    uint32_t *qhead, *tcnt, *tpre, *qcls, *qlab, *rrun, *rord;
+    uint32_t *rlabv, *head, *excl, *rstart, *rcls, *rlab, *tot, *tmp;
+    uint32_t *qhead, *tcnt, *tpre, *rrun, *rord, *perm, *seq2, *scoff, *flag;
     uint64_t* rkey;
     uint8_t* pres;
     uint16_t* cmap;
@@ -555,25 +575,30 @@ extern "C" int chopper_join_counters(
     B.rkey = sc.take<uint64_t>(n);
     B.pres = sc.take<uint8_t>(65536);
     B.cmap = sc.take<uint16_t>(65536);
-    B.coff = sc.take<uint32_t>(256 + 1);
     B.qhead = sc.take<uint32_t>(mmax);
     B.tcnt = sc.take<uint32_t>(ceil_div(nmax, kBlock) + 1);
     B.tpre = sc.take<uint32_t>(ceil_div(nmax, kBlock) + 1);
-    B.qcls = sc.take<uint32_t>(mmax + 1);
-    B.qlab = sc.take<uint32_t>(mmax + 1);
     B.rrun = sc.take<uint32_t>(n);
     B.rord = sc.take<uint32_t>(n);
+    // re-sort by label of a side whose labels are not one run each
+    B.perm = sc.take<uint32_t>(nmax);
+    B.seq2 = sc.take<uint32_t>(nmax);
+    B.scoff = sc.take<uint32_t>(256 + 1);
+    B.flag = sc.take<uint32_t>(1);
     for (int p = 0; p < n_passes; ++p) {
       const int64_t m = passes[p].n;
       B.pb[p].match = sc.take<uint2>(n + 1);
       B.pb[p].qstart = sc.take<uint32_t>(m + 1);
       B.pb[p].qorder = sc.take<uint32_t>(m);
+      B.pb[p].qcls = sc.take<uint32_t>(m + 1);
+      B.pb[p].qlab = sc.take<uint32_t>(m + 1);
+      B.pb[p].coff = sc.take<uint32_t>(256 + 1);
       B.pb[p].key = sc.take<uint64_t>(m);
     }
   };
   Scratch probe(nullptr);
   layout(probe);
-  ClassSortLayout probe_sort = class_sort_layout(probe, mmax, 256);
+  ClassSortLayout probe_sort = class_sort_layout(probe, nmax, 256);
   (void)probe_sort;
   int rc = scratch_check(scratch, scratch_bytes, probe.used);
   if (rc != 0) return rc > 0 ? CHOPPER_OK : rc;
@@ -582,7 +607,7 @@ extern "C" int chopper_join_counters(
   hipStream_t s = (hipStream_t)stream;
   Scratch sc(scratch);
   layout(sc);
-  ClassSortLayout SL = class_sort_layout(sc, mmax, 256);
+  ClassSortLayout SL = class_sort_layout(sc, nmax, 256);
   const dim3 gn = grid_for(n, kBlock);
 
   // columns no pass fills are zero
@@ -609,73 +634,127 @@ extern "C" int chopper_join_counters(
                      grid_for(n, kBlock * 4), dim3(kBlock), s,
                      n, idx + (int64_t)iter_level * n, nm, mk->label,
                      B.rlabv));
-  const Seq R{order, rec->gpu, rec->stream, B.rlabv, B.cmap, n};
-  CHOPPER_HIP(launch("join_heads", k_join_heads,
-                     dim3((unsigned)ceil_div((int64_t)gn.x,
-                                             (int64_t)kWavesPerBlock)),
-                     dim3(kBlock), s, R, B.head, B.rkey, B.tcnt));
-  CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gn.x, B.tmp,
-                                       B.tot, s));
-  const dim3 gw((unsigned)ceil_div((int64_t)gn.x, (int64_t)kWavesPerBlock));
-  CHOPPER_HIP(launch("join_runs", k_join_runs, gw, dim3(kBlock), s, n,
-                     (const uint32_t*)B.head, (const uint32_t*)B.tpre,
-                     (const uint64_t*)B.rkey, B.rstart, B.rcls, B.rlab,
-                     B.excl));
+  CHOPPER_HIP(launch("join_fill", k_join_zero, dim3(1), dim3(1), s, B.flag));
   const dim3 gr(std::min<unsigned>(gn.x, 1024u));
-  CHOPPER_HIP(launch("join_order", k_join_order, gr, dim3(kBlock), s,
-                     (const uint32_t*)B.tot, (const uint32_t*)B.rcls,
-                     (const uint32_t*)B.rlab, status));
+  const dim3 gw((unsigned)ceil_div((int64_t)gn.x, (int64_t)kWavesPerBlock));
+  // run table of the records along `seq`; the check only on the first cut
+  auto record_runs = [&](const uint32_t* seq, bool check) -> int {
+    const Seq R{seq, rec->gpu, rec->stream, B.rlabv, B.cmap, n};
+    CHOPPER_HIP(launch("join_heads", k_join_heads, gw, dim3(kBlock), s, R,
+                       B.head, B.rkey, B.tcnt));
+    CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gn.x,
+                                         B.tmp, B.tot, s));
+    CHOPPER_HIP(launch("join_runs", k_join_runs, gw, dim3(kBlock), s, n,
+                       (const uint32_t*)B.head, (const uint32_t*)B.tpre,
+                       (const uint64_t*)B.rkey, B.rstart, B.rcls, B.rlab,
+                       B.excl));
+    if (check)
+      CHOPPER_HIP(launch("join_order", k_join_order, gr, dim3(kBlock), s,
+                         (const uint32_t*)B.tot, (const uint32_t*)B.rcls,
+                         (const uint32_t*)B.rlab, status, B.flag, 1u));
+    return CHOPPER_OK;
+  };
+  // run table of pass p along its class order
+  auto pass_runs = [&](int p, bool check) -> int {
+    const chopper_counter_pass& P = passes[p];
+    const PassBuf& Q_ = B.pb[p];
+    const int64_t m = P.n;
+    uint32_t* nq = B.tot + 2 + p;
+    const dim3 gm = grid_for(m, kBlock);
+    const dim3 gmw((unsigned)ceil_div((int64_t)gm.x, (int64_t)kWavesPerBlock));
+    CHOPPER_HIP(launch("join_heads", k_join_heads_pass, gmw, dim3(kBlock), s,
+                       m, (const uint32_t*)Q_.qorder, P.label, P.cls,
+                       (const uint32_t*)Q_.coff, (int)nclass + 1, B.qhead,
+                       Q_.key, B.tcnt));
+    CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gm.x,
+                                         B.tmp, nq, s));
+    CHOPPER_HIP(launch("join_runs", k_join_runs, gmw, dim3(kBlock), s, m,
+                       (const uint32_t*)B.qhead, (const uint32_t*)B.tpre,
+                       (const uint64_t*)Q_.key, Q_.qstart, Q_.qcls, Q_.qlab,
+                       (uint32_t*)nullptr));
+    if (check)
+      CHOPPER_HIP(launch("join_order", k_join_order,
+                         dim3(std::min<unsigned>(gm.x, 1024u)), dim3(kBlock),
+                         s, (const uint32_t*)nq, (const uint32_t*)Q_.qcls,
+                         (const uint32_t*)Q_.qlab, status, B.flag,
+                         2u << p));
+    return CHOPPER_OK;
+  };
+  // stable sort of the positions of `seq` (n items) by (class, label) into
+  // B.seq2
+  auto sort_by_label = [&](const uint32_t* seq, int64_t cnt,
+                           const uint8_t* g, const uint8_t* st,
+                           const uint32_t* lab) -> int {
+    ClassSortLayout L = SL;
+    L.n = cnt;
+    L.ntiles = sort_tiles(cnt);
+    bool range_err = false;
+    const KeySeqLabel acc{seq, g, st, lab, B.cmap, (int)nclass + 1};
+    int r = class_sort(acc, L, B.perm, B.scoff, &range_err, s, 0);
+    if (r != CHOPPER_OK) return r;
+    if (range_err) return CHOPPER_EINVAL;   // 32-bit labels always fit
+    CHOPPER_HIP(launch("join_resort", k_join_compose, grid_for(cnt, kBlock),
+                       dim3(kBlock), s, cnt, seq, (const uint32_t*)B.perm,
+                       B.seq2));
+    return CHOPPER_OK;
+  };
+  rc = record_runs(order, true);
+  if (rc != CHOPPER_OK) return rc;
+  // every pass: class order, keys and run table
+  for (int p = 0; p < n_passes; ++p) {
+    const chopper_counter_pass& P = passes[p];
+    const PassBuf& Q_ = B.pb[p];
+    if (P.n > 0) {
+      // stable partition of the pass by class, in its own order (the
+      // pass's order is its time: the partition needs no time key)
+      ClassSortLayout L = SL;
+      L.n = P.n;
+      L.ntiles = sort_tiles(P.n);
+      bool range_err = false;
+      KeyRecStream kq{P.gpu, P.stream, nullptr, B.cmap, (int)nclass + 1};
+      rc = class_sort(kq, L, Q_.qorder, Q_.coff, &range_err, s, 1);
+      if (rc != CHOPPER_OK) return rc;
+      rc = pass_runs(p, true);
+      if (rc != CHOPPER_OK) return rc;
+    } else {
+      CHOPPER_HIP(launch("join_fill", k_join_zero, dim3(1), dim3(1), s,
+                         B.tot + 2 + p));
+    }
+  }
+  // sides whose labels are not one run each: sorted by label, cut again
+  uint32_t resort = 0;
+  CHOPPER_HIP(read_back(B.flag, &resort, sizeof(uint32_t), s));
+  const uint32_t* rseq = order;
+  if (resort & 1u) {
+    rc = sort_by_label(order, n, rec->gpu, rec->stream, B.rlabv);
+    if (rc != CHOPPER_OK) return rc;
+    rseq = B.seq2;
+    rc = record_runs(rseq, false);
+    if (rc != CHOPPER_OK) return rc;
+  }
   CHOPPER_HIP(launch("join_runs", k_join_rec_pos, gn, dim3(kBlock), s, n,
-                     order, (const uint32_t*)B.head, (const uint32_t*)B.excl,
+                     rseq, (const uint32_t*)B.head, (const uint32_t*)B.excl,
                      (const uint64_t*)B.rkey, (const uint32_t*)B.rstart,
                      B.rrun, B.rord));
-  // every pass: class order, keys, run table, and the pass run of every
-  // record run
+  // (the records' re-sorted sequence is no longer needed: seq2 is reused)
   JoinPasses J;
   J.np = n_passes;
   for (int p = 0; p < n_passes; ++p) {
     const chopper_counter_pass& P = passes[p];
     const PassBuf& Q_ = B.pb[p];
     const int64_t m = P.n;
-    uint32_t* nq = B.tot + 2 + p;
-    if (m > 0) {
-      // stable partition of the pass by class, in its own order (the
-      // pass's order is its time: the partition needs no time key)
-      ClassSortLayout L = SL;
-      L.n = m;
-      L.ntiles = sort_tiles(m);
-      bool range_err = false;
-      KeyRecStream kq{P.gpu, P.stream, nullptr, B.cmap, (int)nclass + 1};
-      rc = class_sort(kq, L, Q_.qorder, B.coff, &range_err, s, 1);
+    if (m > 0 && ((resort >> (p + 1)) & 1u)) {
+      rc = sort_by_label(Q_.qorder, m, P.gpu, P.stream, P.label);
       if (rc != CHOPPER_OK) return rc;
-      const dim3 gm = grid_for(m, kBlock);
-      CHOPPER_HIP(launch("join_heads", k_join_heads_pass,
-                         dim3((unsigned)ceil_div((int64_t)gm.x,
-                                                 (int64_t)kWavesPerBlock)),
-                         dim3(kBlock), s,
-                         m, (const uint32_t*)Q_.qorder, P.label, P.cls,
-                         (const uint32_t*)B.coff, (int)nclass + 1, B.qhead,
-                         Q_.key, B.tcnt));
-      CHOPPER_HIP(exclusive_scan<uint32_t>(B.tcnt, B.tpre, (int64_t)gm.x,
-                                           B.tmp, nq, s));
-      CHOPPER_HIP(launch("join_runs", k_join_runs,
-                         dim3((unsigned)ceil_div((int64_t)gm.x,
-                                                 (int64_t)kWavesPerBlock)),
-                         dim3(kBlock), s, m,
-                         (const uint32_t*)B.qhead, (const uint32_t*)B.tpre,
-                         (const uint64_t*)Q_.key, Q_.qstart, B.qcls, B.qlab,
-                         (uint32_t*)nullptr));
-      CHOPPER_HIP(launch("join_order", k_join_order,
-                         dim3(std::min<unsigned>(gm.x, 1024u)), dim3(kBlock), s,
-                         (const uint32_t*)nq, (const uint32_t*)B.qcls,
-                         (const uint32_t*)B.qlab, status));
-    } else {
-      CHOPPER_HIP(launch("join_fill", k_join_zero, dim3(1), dim3(1), s, nq));
+      CHOPPER_HIP(hipMemcpyAsync(Q_.qorder, B.seq2, sizeof(uint32_t) * m,
+                                 hipMemcpyDeviceToDevice, s));
+      rc = pass_runs(p, false);
+      if (rc != CHOPPER_OK) return rc;
     }
     CHOPPER_HIP(launch("join_match", k_join_match, gr, dim3(kBlock), s,
                        (const uint32_t*)B.tot, (const uint32_t*)B.rcls,
-                       (const uint32_t*)B.rlab, (const uint32_t*)nq,
-                       (const uint32_t*)B.qcls, (const uint32_t*)B.qlab,
+                       (const uint32_t*)B.rlab, (const uint32_t*)(B.tot + 2 + p),
+                       (const uint32_t*)Q_.qcls, (const uint32_t*)Q_.qlab,
                        (const uint32_t*)Q_.qstart, m, Q_.match));
     PassView& V = J.p[p];
     V.match = Q_.match;

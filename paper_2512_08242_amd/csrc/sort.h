@@ -54,6 +54,26 @@ struct KeyMarker {
   __host__ __device__ int nclass() const { return G * D * 2 + 1; }
 };
 
+// Positions of a sequence (position p holds item seq[p]) keyed by (dense
+// class of the item's (gpu, stream), the item's label): their stable sort
+// brings every label of a class together and keeps the sequence order
+// inside it (labels as times; NONE sorts last).
+struct KeySeqLabel {
+  const uint32_t* seq;
+  const uint8_t* gpu;
+  const uint8_t* stream;
+  const uint32_t* lab;
+  const uint16_t* cmap;   // [256 * 256]
+  int C;
+  __device__ uint32_t cls(int64_t p) const {
+    const uint32_t i = seq[p];
+    return cmap[(uint32_t)gpu[i] * 256u + stream[i]];
+  }
+  __device__ int64_t time(int64_t p) const { return (int64_t)lab[seq[p]]; }
+  __device__ uint32_t major(int64_t p) const { return cls(p); }
+  __host__ __device__ int nclass() const { return C; }
+};
+
 struct ClassSortLayout {
   int64_t n = 0;
   int C = 0;
@@ -92,6 +112,12 @@ template <typename AccA, typename AccB>
 int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
                 uint32_t* outA, uint32_t* coffA, uint32_t* outB,
                 uint32_t* coffB, hipStream_t s);
+
+// Stable LSD radix sort of the (L.key0, L.val0) pairs of L.n items by the
+// low `bits` bits of the keys (8 bits per pass, through key1 / val1): the
+// values in key order go to out, the keys (optional) to keys_out.
+int radix_sort_pairs(const ClassSortLayout& L, int bits, uint32_t* out,
+                     uint64_t* keys_out, hipStream_t s);
 
 __global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v);
 __global__ void k_status_set(uint32_t bits, uint32_t* status);

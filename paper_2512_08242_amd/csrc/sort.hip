@@ -446,8 +446,15 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
   CHOPPER_HIP(launch("sort_make_keys", k_make_keys<Acc>, grid_for(n, kBlock),
                      dim3(kBlock), s, acc, n, (const int64_t*)L.mm, tbits,
                      L.key0, L.val0));
-  const int bits = tbits + cbits;
-  const int passes = bits == 0 ? 0 : (bits + 7) / 8;
+  return radix_sort_pairs(L, tbits + cbits, out, nullptr, s);
+}
+
+int radix_sort_pairs(const ClassSortLayout& L, int bits, uint32_t* out,
+                     uint64_t* keys_out, hipStream_t s) {
+  const int64_t n = L.n;
+  const int64_t T = L.ntiles;
+  if (n == 0) return CHOPPER_OK;
+  const int passes = bits <= 0 ? 0 : (bits + 7) / 8;
   uint64_t* kin = L.key0;
   uint64_t* kout = L.key1;
   uint32_t* vin = L.val0;
@@ -463,7 +470,7 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
     CHOPPER_HIP(launch("sort_digit_scatter", k_digit_scatter,
                        dim3((unsigned)T), dim3(kBlock), s,
                        (const uint64_t*)kin, (const uint32_t*)vin, n, shift, T,
-                       (const uint32_t*)L.tileoff, last ? nullptr : kout,
+                       (const uint32_t*)L.tileoff, last ? keys_out : kout,
                        last ? out : vout));
     uint64_t* tk = kin; kin = kout; kout = tk;
     uint32_t* tv = vin; vin = vout; vout = tv;
@@ -471,6 +478,9 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
   if (passes == 0) {
     CHOPPER_HIP(hipMemcpyAsync(out, L.val0, sizeof(uint32_t) * n,
                                hipMemcpyDeviceToDevice, s));
+    if (keys_out)
+      CHOPPER_HIP(hipMemcpyAsync(keys_out, L.key0, sizeof(uint64_t) * n,
+                                 hipMemcpyDeviceToDevice, s));
   }
   return CHOPPER_OK;
 }
@@ -612,5 +622,8 @@ template int class_sort<KeyRecKind>(const KeyRecKind&, const ClassSortLayout&,
 template int class_sort<KeyMarker>(const KeyMarker&, const ClassSortLayout&,
                                    uint32_t*, uint32_t*, bool*, hipStream_t,
                                    int);
+template int class_sort<KeySeqLabel>(const KeySeqLabel&,
+                                     const ClassSortLayout&, uint32_t*,
+                                     uint32_t*, bool*, hipStream_t, int);
 
 }  // namespace chopper

@@ -43,16 +43,41 @@ def test_join_hand_example():
     assert m.tolist() == [1, 1, 0, 0, 1]
     assert st == oracle.JOIN_MISS
     assert int(ctr.sum()) == 100 + 101 + 104 + 200 + 201 + 204
-    # a pass whose labels decrease along a stream
+    # a pass whose labels decrease along a stream: JOIN_ORDER (a warning)
     q = dict(p, lab=np.array([8, 7, 7, 7], np.uint32))
     assert oracle.join(gpu, stream, cls, s, lab, [q])[2] & oracle.JOIN_ORDER
-    # records of one label split by a record without an iteration
+    # records of one label split by a record without an iteration: labels
+    # never decrease, no warning
     lab2 = np.array([7, 7, NONE, 7, 8], np.uint32)
-    assert oracle.join(gpu, stream, cls, s, lab2, [p])[2] & oracle.JOIN_ORDER
+    assert not oracle.join(gpu, stream, cls, s, lab2, [p])[2] & \
+        oracle.JOIN_ORDER
     # a record without an iteration at the start of a stream is fine
     lab3 = np.array([NONE, 7, 7, 8, 8], np.uint32)
     assert not oracle.join(gpu, stream, cls, s, lab3, [p])[2] & \
         oracle.JOIN_ORDER
+
+
+def test_join_hand_example_labels_out_of_order():
+    # GPU 0, stream 0, records in time order with labels 7, 9, 7, 9, 7 and
+    # classes GEMM, NORM, GEMM, GEMM, ELEM: the ordinals count earlier
+    # records of the same label, whatever lies between them:
+    #   record 0 (7, #0), 1 (9, #0), 2 (7, #1), 3 (9, #1), 4 (7, #2)
+    gpu = np.zeros(5, np.uint8)
+    stream = np.zeros(5, np.uint8)
+    cls = np.array([0, 3, 0, 0, 2], np.uint8)
+    s = np.array([10, 20, 30, 40, 50], np.int64)
+    lab = np.array([7, 9, 7, 9, 7], np.uint32)
+    # the pass lists label 9 first, then label 7 (entries in the pass's own
+    # order: 9 #0, 9 #1, 7 #0, 7 #1, 7 #2); the entry 7 #1 has another class
+    p = dict(gpu=np.zeros(5, np.uint8), stream=np.zeros(5, np.uint8),
+             cls=np.array([3, 0, 0, 3, 2], np.uint8),
+             lab=np.array([9, 9, 7, 7, 7], np.uint32),
+             values=np.array([[901, 902, 701, 702, 703]], np.uint64), dst=[2])
+    ctr, m, st = oracle.join(gpu, stream, cls, s, lab, [p])
+    assert ctr[2].tolist() == [701, 901, 0, 902, 703]
+    assert m.tolist() == [1, 1, 0, 1, 1]
+    # labels decrease on both sides (9 -> 7): the warning, and one miss
+    assert st == oracle.JOIN_ORDER | oracle.JOIN_MISS
 
 
 def _dict_join(tr, s, lab, passes):
@@ -94,8 +119,7 @@ def test_join_round_trip_and_dict(seed):
                              passes)
     # unperturbed passes: every record with an iteration matched in every
     # pass, and the join gives back the counters that were split into the
-    # passes (the random labels of these traces may decrease along a
-    # stream: JOIN_ORDER only)
+    # passes, whatever the order of the random labels of these traces
     has = lab != NONE
     assert st & oracle.JOIN_MISS == 0
     assert (m[has] == (1 << len(passes)) - 1).all() and (m[~has] == 0).all()
