@@ -58,6 +58,9 @@ struct RecSrc {
   int nc;
   const uint32_t* mlabel;
   FilterDev f;
+  // exact group ids of the marker levels ([D][n] by korder position), or
+  // null: groups by the deepest marker (exact for nested markers)
+  const uint32_t* gk;
 };
 
 struct RowsDev {
@@ -115,6 +118,17 @@ __device__ inline uint32_t group_key(const uint32_t* p, int D, int64_t M,
   return kind;
 }
 
+// key of an item at level li: its exact group id at the marker levels when
+// those are given (fpos = korder position of the item, or of the first
+// record of a row), else the deepest-marker key
+__device__ inline uint32_t item_key(const uint32_t* gk, int64_t nrec,
+                                    const uint32_t* p, int D, int64_t M,
+                                    int li, uint32_t g, uint32_t kind,
+                                    uint32_t fpos) {
+  if (gk && li < D) return gk[(int64_t)li * nrec + fpos];
+  return group_key(p, D, M, li, g, kind);
+}
+
 // One record position: its record, pass flag, gpu, kind and path.
 struct RecItem {
   uint32_t r;
@@ -146,10 +160,13 @@ __global__ __launch_bounds__(kBlock) void k_agg_elect(RecSrc S, uint32_t act,
   for (int li = 0; li < S.D + 2; ++li) {
     if (!((act >> li) & 1u)) continue;
     uint32_t key[kAggIpt];
-    for (int j = 0; j < kAggIpt; ++j)
+    for (int j = 0; j < kAggIpt; ++j) {
+      const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
       key[j] = (valid[j] && it[j].ok)
-                   ? group_key(it[j].p, S.D, S.M, li, it[j].g, it[j].kind)
+                   ? item_key(S.gk, S.n, it[j].p, S.D, S.M, li, it[j].g,
+                              it[j].kind, (uint32_t)pos)
                    : kNone;
+    }
     s_last[threadIdx.x] = key[kAggIpt - 1];
     __syncthreads();
     uint32_t prev = threadIdx.x > 0 ? s_last[threadIdx.x - 1] : kNone;
@@ -183,9 +200,9 @@ __global__ __launch_bounds__(kBlock) void k_agg_count(RecSrc S, uint32_t act,
     if ((act >> li) & 1u) {
       for (int j = 0; j < kAggIpt; ++j) {
         if (!valid[j] || !it[j].ok) continue;
-        const uint32_t key =
-            group_key(it[j].p, S.D, S.M, li, it[j].g, it[j].kind);
         const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
+        const uint32_t key = item_key(S.gk, S.n, it[j].p, S.D, S.M, li,
+                                      it[j].g, it[j].kind, (uint32_t)pos);
         if (key != kNone && own[li][key] == (uint32_t)pos) ++c;
       }
     }
@@ -227,7 +244,8 @@ __global__ __launch_bounds__(kBlock) void k_agg_assign(
     for (int j = 0; j < kAggIpt; ++j) {
       const int64_t pos = base + (int64_t)threadIdx.x * kAggIpt + j;
       key[j] = (valid[j] && it[j].ok)
-                   ? group_key(it[j].p, S.D, S.M, li, it[j].g, it[j].kind)
+                   ? item_key(S.gk, S.n, it[j].p, S.D, S.M, li, it[j].g,
+                              it[j].kind, (uint32_t)pos)
                    : kNone;
       mine[j] = key[j] != kNone && own[li][key[j]] == (uint32_t)pos;
       c += mine[j] ? 1u : 0u;
@@ -395,6 +413,10 @@ struct FromRecords {
     for (int l = 0; l < S.D; ++l) p[l] = pathv(r, l);
     return group_key(p, S.D, S.M, li, gpuv(r), kindv(r));
   }
+  __device__ uint32_t key_at(int li, const uint32_t* p, uint32_t g,
+                             uint32_t kind, uint32_t fpos) const {
+    return item_key(S.gk, S.n, p, S.D, S.M, li, g, kind, fpos);
+  }
   // column of field f, resolved once per field: mode 0 constant 1,
   // 1 a[r] - b[r], 2 a[r]
   __device__ FieldRef fref(int f) const {
@@ -427,6 +449,8 @@ struct FromRows {
   int64_t M;        // number of markers (key space)
   const int64_t* level_offset;
   int lo_slot;      // level_offset index of the finer level
+  const uint32_t* gk = nullptr;   // exact group ids (RecSrc::gk) or null
+  int64_t nrec = 0;               // records (row stride of gk)
   // columns of the fast reduction: tmin and tmax, then the plain sums
   // n, dur, gap, ovl and the counters
   __device__ const int64_t* start_col() const { return R.tmin; }
@@ -465,6 +489,10 @@ struct FromRows {
     uint32_t p[8];
     for (int l = 0; l < R.D; ++l) p[l] = pathv(r, l);
     return group_key(p, R.D, M, li, gpuv(r), kindv(r));
+  }
+  __device__ uint32_t key_at(int li, const uint32_t* p, uint32_t g,
+                             uint32_t kind, uint32_t fpos) const {
+    return item_key(gk, nrec, p, R.D, M, li, g, kind, fpos);
   }
   __device__ FieldRef fref(int f) const {
     return FieldRef{(const uint64_t*)row_column(R, f), nullptr, 2};
@@ -544,7 +572,7 @@ __global__ __launch_bounds__(kBlock) void k_agg_reduce(
     bool ok;
     src.load(i, rid[j], ok, p, g, kind, fpos);
     if (!ok) continue;
-    const uint32_t key = group_key(p, D, M, li, g, kind);
+    const uint32_t key = src.key_at(li, p, g, kind, fpos);
     if (key == kNone) continue;
     const uint32_t row = rowof[key];
     tgt[j] = row;
@@ -748,8 +776,12 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads(
     if (lane == 0) tilecnt[(int64_t)(li - lv0) * nwt + w] = tot;
   }
   if (__ballot(notinc) != 0 && lane == 0) atomicOr(&flags[0], 1u);
-  if (__ballot(conflict) != 0 && lane == 0)
+  // a conflict sends the call to the general path, which groups by the
+  // whole path
+  if (__ballot(conflict) != 0 && lane == 0) {
+    atomicOr(&flags[0], 2u);
     atomicOr(status, (uint32_t)CHOPPER_ST_PATH_CONFLICT);
+  }
   // kinds present: the shared word is zeroed before the launch and only
   // gains bits, so a bit read as set here was set by this launch
   const uint32_t kk = (__ballot(kinds & 1u) != 0 ? 1u : 0u) |
@@ -1212,8 +1244,12 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads_nat(
     }
   }
   if (__ballot(notinc) != 0 && lane == 0) atomicOr(&flags[0], 1u);
-  if (__ballot(conflict) != 0 && lane == 0)
+  // a conflict sends the call to the general path, which groups by the
+  // whole path
+  if (__ballot(conflict) != 0 && lane == 0) {
+    atomicOr(&flags[0], 2u);
     atomicOr(status, (uint32_t)CHOPPER_ST_PATH_CONFLICT);
+  }
   const uint32_t kk = (__ballot(kinds & 1u) != 0 ? 1u : 0u) |
                       (__ballot(kinds & 2u) != 0 ? 2u : 0u);
   if (lane == 0 && kk &&
@@ -1823,6 +1859,96 @@ __global__ __launch_bounds__(kBlock) void k_agg_zero_rows(
   }
 }
 
+// ------------------------------------------------------- exact group ids
+// General path, deepest-marker keys: a record whose path at a requested
+// marker level differs from that of its key's owner (the group's first
+// record) shares that marker with a record of another path -- markers not
+// nested.  Sets PATH_CONFLICT and *flag; the host then groups by the whole
+// path instead.
+__global__ __launch_bounds__(kBlock) void k_agg_conflict(RecSrc S,
+                                                         uint32_t act,
+                                                         uint32_t** own,
+                                                         uint32_t* flag,
+                                                         uint32_t* status) {
+  const int64_t pos = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  bool conflict = false;
+  if (pos < S.n) {
+    RecItem it;
+    load_item(S, pos, it);
+    if (it.ok) {
+      for (int li = 0; li < S.D; ++li) {
+        if (!((act >> li) & 1u)) continue;
+        const uint32_t key = group_key(it.p, S.D, S.M, li, it.g, it.kind);
+        if (key == kNone) continue;
+        const uint32_t o = own[li][key];
+        if (o == kNone || (int64_t)o >= S.n) continue;
+        const uint32_t ro = S.korder[o];
+        for (int l = 0; l <= li; ++l)
+          if (S.idx[(int64_t)l * S.n + ro] != it.p[l]) conflict = true;
+      }
+    }
+  }
+  if (__ballot(conflict) != 0 && lane_id() == 0) {
+    atomicOr(flag, 1u);
+    atomicOr(status, (uint32_t)CHOPPER_ST_PATH_CONFLICT);
+  }
+}
+
+// Exact group ids, level by level from the outermost: the key of korder
+// position p at marker level l is (its group id at level l - 1, or
+// gpu * 2 + kind at l = 0) * (M + 2) + (its level-l marker, M + 1 for
+// NONE), so that equal keys are equal paths; records left out by the filter
+// get kfilt, above every key.  After a stable sort by key the group id of a
+// position is the position of its group's first record.
+__global__ __launch_bounds__(kBlock) void k_xk_keys(RecSrc S, int l,
+                                                    const uint32_t* gprev,
+                                                    uint64_t kfilt,
+                                                    uint64_t* key,
+                                                    uint32_t* val) {
+  const int64_t pos = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (pos >= S.n) return;
+  const uint32_t r = S.korder[pos];
+  uint64_t k = kfilt;
+  if (rec_pass(S, r)) {
+    const uint64_t parent =
+        l == 0 ? (uint64_t)S.gpu[r] * 2u + (uint64_t)kind_of(S.cls[r])
+               : (uint64_t)gprev[pos];
+    const uint32_t m = S.idx[(int64_t)l * S.n + r];
+    const uint64_t mi = m == kNone ? (uint64_t)S.M + 1
+                                   : ((int64_t)m >= S.M ? (uint64_t)S.M : m);
+    k = parent * ((uint64_t)S.M + 2) + mi;
+  }
+  key[pos] = k;
+  val[pos] = (uint32_t)pos;
+}
+
+__global__ __launch_bounds__(kBlock) void k_xk_heads(int64_t n,
+                                                     const uint64_t* skey,
+                                                     uint32_t* head) {
+  const int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (q < n) head[q] = (q == 0 || skey[q] != skey[q - 1]) ? 1u : 0u;
+}
+
+// first[run] = position of the run's first item (the smallest: the sort is
+// stable over ascending positions)
+__global__ __launch_bounds__(kBlock) void k_xk_first(int64_t n,
+                                                     const uint32_t* head,
+                                                     const uint32_t* runx,
+                                                     const uint32_t* sval,
+                                                     uint32_t* first) {
+  const int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (q < n && head[q]) first[runx[q]] = sval[q];
+}
+
+__global__ __launch_bounds__(kBlock) void k_xk_assign(
+    int64_t n, const uint64_t* skey, uint64_t kfilt, const uint32_t* head,
+    const uint32_t* runx, const uint32_t* sval, const uint32_t* first,
+    uint32_t* gid) {
+  const int64_t q = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (q >= n) return;
+  gid[sval[q]] = skey[q] == kfilt ? kNone : first[runx[q] + head[q] - 1u];
+}
+
 __global__ void k_fill_u32_many(uint32_t** p, const int64_t* counts, int L,
                                 uint32_t act) {
   const int li = blockIdx.y;
@@ -1888,6 +2014,17 @@ struct AggLayout {
   uint32_t* gs;           // [G]
   uint32_t* ge;
   uint32_t* gtb;          // [G + 1]
+  // exact group ids (markers not nested)
+  uint32_t* gk;           // [D][n]
+  uint32_t* xflag;
+  uint64_t* xskey;        // sorted keys
+  uint32_t* xsval;        // positions in key order
+  uint32_t* xhead;
+  uint32_t* xrunx;
+  uint32_t* xfirst;
+  uint32_t* xtot;
+  uint32_t* xscan;        // scan temporaries over n items
+  ClassSortLayout xsort;
 };
 
 static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
@@ -1896,7 +2033,10 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
   L.L = D + 2;
   L.ntiles = ceil_div(n, kAggTile);
   for (int li = 0; li < L.L; ++li) {
-    L.ks[li] = ((act >> li) & 1u) ? key_space(li, D, M) : 1;
+    // (exact group ids at the marker levels are korder positions < n)
+    int64_t ks = key_space(li, D, M);
+    if (li < D && n > ks) ks = n;
+    L.ks[li] = ((act >> li) & 1u) ? ks : 1;
     L.own[li] = sc.take<uint32_t>(L.ks[li]);
     L.rowof[li] = sc.take<uint32_t>(L.ks[li]);
   }
@@ -1936,7 +2076,59 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
   L.gs = sc.take<uint32_t>(G);
   L.ge = sc.take<uint32_t>(G);
   L.gtb = sc.take<uint32_t>(G + 1);
+  L.gk = sc.take<uint32_t>((int64_t)(D > 0 ? D : 1) * n);
+  L.xflag = sc.take<uint32_t>(1);
+  L.xskey = sc.take<uint64_t>(n);
+  L.xsval = sc.take<uint32_t>(n);
+  L.xhead = sc.take<uint32_t>(n);
+  L.xrunx = sc.take<uint32_t>(n);
+  L.xfirst = sc.take<uint32_t>(n);
+  L.xtot = sc.take<uint32_t>(1);
+  L.xscan = sc.take<uint32_t>(scan_scratch_elems(n));
+  L.xsort = class_sort_layout(sc, n, 256);
   return L;
+}
+
+static int bitlen_of(uint64_t x) {
+  int b = 0;
+  while (x) { ++b; x >>= 1; }
+  return b;
+}
+
+// Exact group ids of the marker levels 0 .. lmax into L.gk (see k_xk_keys).
+static int exact_group_ids(const AggLayout& L, const RecSrc& S, int lmax,
+                           hipStream_t s) {
+  const int64_t n = S.n;
+  const dim3 g = grid_for(n, kBlock);
+  for (int l = 0; l <= lmax; ++l) {
+    // keys below kfilt = (parents) * (M + 2); parents: 512 (gpu, kind) ids
+    // at level 0, positions below n after
+    const unsigned __int128 kf =
+        (unsigned __int128)(l == 0 ? 512u : (uint64_t)n) *
+        (unsigned __int128)((uint64_t)S.M + 2);
+    if (kf >> 63) return CHOPPER_EINVAL;
+    const uint64_t kfilt = (uint64_t)kf;
+    CHOPPER_HIP(launch("agg_exact_keys", k_xk_keys, g, dim3(kBlock), s, S, l,
+                       (const uint32_t*)(l > 0 ? L.gk + (int64_t)(l - 1) * n
+                                               : nullptr),
+                       kfilt, L.xsort.key0, L.xsort.val0));
+    int rc = radix_sort_pairs(L.xsort, bitlen_of(kfilt), L.xsval, L.xskey,
+                              s);
+    if (rc != CHOPPER_OK) return rc;
+    CHOPPER_HIP(launch("agg_exact_keys", k_xk_heads, g, dim3(kBlock), s, n,
+                       (const uint64_t*)L.xskey, L.xhead));
+    CHOPPER_HIP(exclusive_scan<uint32_t>(L.xhead, L.xrunx, n, L.xscan,
+                                         L.xtot, s));
+    CHOPPER_HIP(launch("agg_exact_keys", k_xk_first, g, dim3(kBlock), s, n,
+                       (const uint32_t*)L.xhead, (const uint32_t*)L.xrunx,
+                       (const uint32_t*)L.xsval, L.xfirst));
+    CHOPPER_HIP(launch("agg_exact_keys", k_xk_assign, g, dim3(kBlock), s, n,
+                       (const uint64_t*)L.xskey, kfilt,
+                       (const uint32_t*)L.xhead, (const uint32_t*)L.xrunx,
+                       (const uint32_t*)L.xsval, (const uint32_t*)L.xfirst,
+                       L.gk + (int64_t)l * n));
+  }
+  return CHOPPER_OK;
 }
 
 }  // namespace chopper
@@ -2187,6 +2379,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
   S.nc = nc;
   S.mlabel = mk ? mk->label : nullptr;
   memset(&S.f, 0, sizeof(S.f));
+  S.gk = nullptr;
   if (filter) {
     for (int q = 0; q < 4; ++q) S.f.gpu_mask[q] = filter->gpu_mask[q];
     S.f.class_mask = filter->class_mask;
@@ -2245,6 +2438,30 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
   if (n > 0) {
     CHOPPER_HIP(launch("agg_elect", k_agg_elect, dim3((unsigned)T),
                        dim3(kBlock), s, S, act, L.own_tab));
+    // markers not nested (a record's path differs from its key owner's):
+    // group by the whole path, with exact group ids
+    int lmax = -1;
+    for (int li = 0; li < D; ++li)
+      if ((act >> li) & 1u) lmax = li;
+    if (lmax >= 0) {
+      CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
+                         L.xflag, 1));
+      CHOPPER_HIP(launch("agg_conflict", k_agg_conflict, grid_for(n, kBlock),
+                         dim3(kBlock), s, S, act, L.own_tab, L.xflag,
+                         status));
+      uint32_t conflict = 0;
+      CHOPPER_HIP(read_back(L.xflag, &conflict, sizeof(uint32_t), s));
+      if (conflict) {
+        rc = exact_group_ids(L, S, lmax, s);
+        if (rc != CHOPPER_OK) return rc;
+        S.gk = L.gk;
+        CHOPPER_HIP(launch("agg_fill_owner", k_fill_u32_many, dim3(fx, Lv),
+                           dim3(kBlock), s, L.own_tab,
+                           (const int64_t*)L.ks_dev, Lv, act));
+        CHOPPER_HIP(launch("agg_elect", k_agg_elect, dim3((unsigned)T),
+                           dim3(kBlock), s, S, act, L.own_tab));
+      }
+    }
     CHOPPER_HIP(launch("agg_count", k_agg_count, dim3((unsigned)T),
                        dim3(kBlock), s, S, act, L.own_tab, T, L.tilecnt));
   }
@@ -2280,7 +2497,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
                          (const uint32_t*)L.rowof[li], R, ovf, nfields,
                          status));
     } else {
-      FromRows src{R, M, rows->level_offset, finer};
+      FromRows src{R, M, rows->level_offset, finer, S.gk, n};
       // rows of the finer level never outnumber the records
       CHOPPER_HIP(launch("agg_reduce_rows", k_agg_reduce<FromRows>,
                          dim3((unsigned)T), dim3(kBlock), s, src, li, D, M,
@@ -2300,7 +2517,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
                            grid_for(n, kBlock), dim3(kBlock), s, src, D, M,
                            (const uint32_t*)L.rowof[li], R));
       } else {
-        FromRows src{R, M, rows->level_offset, finer};
+        FromRows src{R, M, rows->level_offset, finer, S.gk, n};
         CHOPPER_HIP(launch("agg_workload_first", k_agg_workload_first<FromRows>,
                            grid_for(n, kBlock), dim3(kBlock), s, src, D, M,
                            (const uint32_t*)L.rowof[li], R));
