@@ -89,11 +89,25 @@ def measured_traffic(kernel):
     return None
 
 
-def cpu_baseline(cid, iters):
-    """The CPU oracle, as it stands, on a bounded sample of the workload."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cid, iters, tr=None):
+    """The CPU oracle, as it stands (single-threaded C), over the whole
+    pipeline: on the benchmark's own trace when `tr` is given, else on a
+    trace of the same shape with `iters` iterations."""
     import oracle
     import tracegen as tg
-    tr = tg.make_config(cid, iters=iters, with_truth=False)
+    whole = tr is not None
+    if tr is None:
+        tr = tg.make_config(cid, iters=iters, with_truth=False)
     t0 = time.perf_counter()
     oracle.run(tr)
     dt = time.perf_counter() - t0
@@ -101,12 +115,15 @@ def cpu_baseline(cid, iters):
         cores = len(os.sched_getaffinity(0))
     except AttributeError:
         cores = os.cpu_count()
+    what = (f"the whole benchmark trace ({tr.n} records, {tr.n_markers} "
+            "markers)" if whole else
+            f"config-{cid} trace shape with {iters} iterations ({tr.n} "
+            f"records, {tr.n_markers} markers)")
     return {"value": tr.n / dt, "unit": "records/s", "cores": 1,
-            "host_cores_available": cores, "kind": "oracle",
-            "seconds": dt,
-            "sample": f"config-{cid} trace shape with {iters} iterations "
-                      f"({tr.n} records, {tr.n_markers} markers), "
-                      "single-threaded C oracle, whole pipeline"}
+            "host_cores_available": cores, "cpu_model": cpu_model(),
+            "kind": "oracle", "seconds": dt,
+            "sample": what + ", single-threaded C oracle: align, sort, "
+                      "attribute, overlap, aggregate, ratios"}
 
 
 def main():
@@ -116,7 +133,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-iters", type=int, default=500)
+    ap.add_argument("--cpu-iters", type=int, default=0,
+                    help="time the oracle on a trace of this many iterations "
+                         "instead of the benchmark's own (0: the whole "
+                         "benchmark trace up to 25M records, else 500)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run plain device copies of this many MiB (the "
                          "reference kernel for scaling HBM byte counters)")
@@ -315,22 +335,26 @@ def main():
         v1.record()
         torch.cuda.synchronize()
         jms = v0.elapsed_time(v1) / K
-        # per pass entry gpu, stream, class, label and its columns read; per
-        # record and pass order, gpu, stream, class, label read and its
-        # columns written; matched bits
+        # per pass entry gpu, stream, class, label and its columns read;
+        # per record (once for all passes) order, gpu, stream, class and
+        # its iteration marker read, the 16 counters and the matched bits
+        # written
         cols = 16
-        jb = (len(dp) * n * (1 + 1 + 1 + 4) + n * 8 * cols
-              + len(dp) * n * (4 + 1 + 1 + 1 + 4) + n * 8 * cols + n)
+        m_tot = sum(int(q["gpu"].shape[0]) for q in dp)
+        jb = (m_tot * (1 + 1 + 1 + 4) + n * 8 * cols
+              + n * (4 + 1 + 1 + 1 + 4) + n * 8 * cols + n)
         out["join_counters"] = {
             "ms": jms, "passes": len(dp), "bytes": jb,
             "achieved": jb / (jms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": jb / (jms * 1e-3) / 1e9 / HBM_PEAK_GBS}
         log(f"[bench] join counters {jms:.3f} ms")
         del dp
-    del trace_host
     if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(cid, args.cpu_iters)
+        whole = args.cpu_iters == 0 and n <= 25_000_000
+        log("[bench] timing the CPU oracle")
+        out["cpu_baseline"] = cpu_baseline(
+            cid, args.cpu_iters or 500, trace_host if whole else None)
+    del trace_host
     print(json.dumps(out), flush=True)
 
 

@@ -36,10 +36,19 @@
  * else is read or written, no GPU work is done, CHOPPER_OK is returned); then
  * call again with a buffer of at least that many bytes, 256-byte aligned.
  *
- * Streams.  `stream` is a hipStream_t.  Work is enqueued on it; a call may
- * synchronize that stream internally to size later launches, so do not
- * capture these calls in a HIP graph.  Outputs are valid after the stream
- * has been synchronized.  Concurrent calls must use distinct scratch buffers.
+ * Streams.  `stream` is a hipStream_t.  Work is enqueued on it.  Some calls
+ * wait for that stream to read back a few words (counts and flags that size
+ * or choose later launches), copied into the call's own host variables:
+ * chopper_align once (record classes and whether the input is in start
+ * order), chopper_attribute once (whether the markers are in start order),
+ * chopper_aggregate once when the records come grouped by GPU in start
+ * order (row counts per level, whether groups are runs), twice otherwise
+ * and twice more on the general path, chopper_join_counters twice; the sorts wait
+ * again when their input is not in time order.  chopper_overlap, the
+ * derived metrics, the launch split and the statistics never wait.  So do
+ * not capture the waiting calls in a HIP graph.  Outputs are valid after
+ * the stream has been synchronized.  Concurrent calls must use distinct
+ * scratch buffers.
  *
  * Errors.  Argument errors are detected on the host before any GPU work and
  * returned synchronously (negative codes below).  Problems in the DATA are
