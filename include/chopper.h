@@ -527,9 +527,26 @@ int chopper_join_counters(const chopper_records* records,
  *   10 D_act = Sy / m;  11 D_peak = sum ctr[0] * 1000 / freq_peak_mhz / m
  *   12 Ovr_util = 1 / (sum ctr[1] / sum ctr[0])  (eq. 8)
  *   13 Ovr_inst = (sum ctr[11] / m) / f_gemm[o]  (eq. 7)
- *   14 Ovr_overlap = D50 / D0  (eq. 9)
+ *   14 Ovr_overlap (eq. 9): the median over the GPUs with instances of
+ *      their per-GPU D_50% / D_0% (below), sorted, (v[(k-1)/2] + v[k/2]) / 2
  *   15 Ovr_freq = D_act / D_peak / Ovr_overlap  (eq. 10)
  *   16 D_thr = f_gemm[o] / tpt_peak  (eq. 6)
+ * (3 and 4 are the least-squares line at 0 and 50 % overlap.)
+ *
+ * Per-GPU overlap CDF (Fig. per_gpu_overlap_variation: overlap ratio from 0
+ * to 1 against duration normalised to the GPU's minimum; Section VI
+ * "Overlap overhead": D_50% and D_0% are read off such a CDF).  The
+ * instances of group g on GPU h < n_gpus, c = g * n_gpus + h, in CDF order
+ * (ascending x, equal x in row order, which is time order on a GPU): with
+ * v_k the k-th of m_h instances and y_min their smallest y,
+ * gpu_out [9][n_phases * n_ops * n_gpus] at c =
+ *   0..4 quantiles v[0], v[(m-1)/4], (v[(m-1)/2] + v[m/2]) / 2, v[3(m-1)/4],
+ *        v[m-1] of x, times 2^-30
+ *   5 y_min   6 D_0% = y(v_0) / y_min
+ *   7 D_50% = (y(v_(m-1)/2) / y_min + y(v_m/2) / y_min) / 2
+ *   8 D_50% / D_0%
+ * (NaN when m_h = 0); gpu_cnt [n_phases * n_ops * n_gpus] = m_h.  Both
+ * may be NULL (computed in scratch, not returned).
  * in exactly these IEEE operations; cnt [n_phases * n_ops] = m.  Empty
  * groups: NaN.  11-13 and 15 need n_counters = 16 (else NaN); f_gemm
  * ([host], n_ops theoretical FLOP counts, per operation label) may be NULL
@@ -541,10 +558,11 @@ int chopper_join_counters(const chopper_records* records,
  * (device; labels read); n_counters: the rows' counter columns (0 .. 16).
  * out and cnt: device arrays, every element written.  Scratch:
  * caller-owned device memory, size query with scratch == NULL (grows with
- * rows->cap and n_phases * n_ops), 256-byte aligned.  status: device word
+ * rows->cap and n_phases * n_ops * n_gpus), 256-byte aligned.  status: device word
  * (RANGE bit).  Enqueued on `stream` without synchronizing.  Returns
  * CHOPPER_EINVAL for a level outside 0 .. depth-1, depth above the markers'
- * depth, sizes out of range or a missing pointer, CHOPPER_ESCRATCH for a
+ * depth, sizes out of range (n_gpus included) or a missing pointer
+ * (rows->gpu is read), CHOPPER_ESCRATCH for a
  * short scratch buffer.
  */
 typedef struct {
@@ -555,12 +573,15 @@ typedef struct {
   double freq_peak_mhz;
   double tpt_peak;    /* FLOP per ns */
   const double* f_gemm;
+  int32_t n_gpus;     /* 1 .. 256: GPUs of the per-GPU CDFs */
+  int32_t reserved;
 } chopper_stats_spec;
 
 int chopper_op_stats(const chopper_rows* rows, int32_t depth,
                      int32_t n_counters, const chopper_markers* markers,
                      const chopper_stats_spec* spec, double* out,
-                     int64_t* cnt, void* scratch, size_t* scratch_bytes,
+                     int64_t* cnt, double* gpu_out, int64_t* gpu_cnt,
+                     void* scratch, size_t* scratch_bytes,
                      uint32_t* status, void* stream);
 
 /* Text for a return code. */

@@ -131,7 +131,7 @@ def _load():
     lib.orc_join.restype = ctypes.c_uint32
     lib.orc_op_stats.argtypes = [i64, i64, i64, P, i32, i32, P, P, P, P, P,
                                  i32, P, i32, i32, ctypes.c_double,
-                                 ctypes.c_double, P, P, P]
+                                 ctypes.c_double, P, P, P, P, i32, P, P]
     lib.orc_op_stats.restype = None
     _lib = lib
     return lib
@@ -272,22 +272,35 @@ OP_STATS = ("pearson", "slope", "intercept", "d0", "d50", "q0", "q25",
             "ovr_overlap", "ovr_freq", "d_thr")
 
 
+OP_CDF = ("q0", "q25", "q50", "q75", "q100", "y_min", "d0", "d50", "ovr")
+
+
 def op_stats(rows: Dict, m_label, depth, phase_level=1, op_level=3,
              n_phases=3, n_ops=64, freq_peak_mhz=2100.0, tpt_peak=1.0,
-             f_gemm=None):
+             f_gemm=None, n_gpus=None, per_gpu=False):
     """Overlap statistics and overhead breakdown per (phase, operation)
     (Fig. gemm_overlap, Section VI eqs. 6-10) from the rows of the
-    operation level; definitions in oracle.c.  Returns (out [17][P*O],
-    cnt [P*O])."""
+    operation level, with the per-GPU overlap CDFs (Fig.
+    per_gpu_overlap_variation) that eq. 9 is read from; definitions in
+    oracle.c.  Returns (out [17][P*O], cnt [P*O]), and with per_gpu also
+    (gout [9][P*O*NG], gcnt [P*O*NG]).  n_gpus defaults to one more than
+    the largest GPU id of the rows."""
     lib = _load()
+    gpu = _c(rows["gpu"], np.uint8) if "gpu" in rows else \
+        np.zeros(int(rows["n"].shape[0]), np.uint8)
+    if n_gpus is None:
+        n_gpus = int(gpu.max()) + 1 if gpu.size else 1
     lo = rows["level_offset"]
     nr = int(rows["n"].shape[0])
     path = _c(rows["path"], np.uint32)
     nc = int(rows["ctr"].shape[0]) if rows["ctr"] is not None else 0
     ctr = _c(rows["ctr"], np.uint64) if nc else np.zeros(1, np.uint64)
     P_, O_ = int(n_phases), int(n_ops)
+    NG = int(n_gpus)
     out = np.zeros((17, P_ * O_))
     cnt = np.zeros(P_ * O_, np.int64)
+    gout = np.zeros((9, P_ * O_ * NG))
+    gcnt = np.zeros(P_ * O_ * NG, np.int64)
     fg = None if f_gemm is None else _c(f_gemm, np.float64)
     a = [path, _c(rows["kind"], np.uint8), _c(rows["dur"], np.int64),
          _c(rows["gap"], np.int64), _c(rows["ovl"], np.int64), ctr,
@@ -296,7 +309,9 @@ def op_stats(rows: Dict, m_label, depth, phase_level=1, op_level=3,
                      _p(a[0]), phase_level, op_level, _p(a[1]), _p(a[2]),
                      _p(a[3]), _p(a[4]), _p(a[5]), nc, _p(a[6]), P_, O_,
                      float(freq_peak_mhz), float(tpt_peak), _p(fg), _p(out),
-                     _p(cnt))
+                     _p(cnt), _p(gpu), NG, _p(gout), _p(gcnt))
+    if per_gpu:
+        return out, cnt, gout, gcnt
     return out, cnt
 
 

@@ -1095,8 +1095,40 @@ uint32_t orc_join(int64_t n, const uint8_t* gpu, const uint8_t* stream,
  * out [17][P * O]: pearson, slope, intercept, D0, D50, q0, q25, q50, q75,
  * q100, D_act, D_peak, Ovr_util, Ovr_inst, Ovr_overlap, Ovr_freq, D_thr;
  * cnt [P * O] = m.  Limits: y < 2^34, m < 2^26 per group.
+ *
+ * Per-GPU overlap CDF (Fig. per_gpu_overlap_variation: per GPU, the CDF of
+ * an operation's overlap ratio against its duration normalised to that
+ * GPU's minimum; Section VI "Overlap overhead": D_50% and D_0% are read off
+ * such a CDF, eq. 9).  The instances of (p, o) on GPU h (row gpu h < NG) in
+ * CDF order: ascending x, equal x in row order (rows of a GPU are in time
+ * order).  With v_k the k-th instance in that order (k = 0 .. m_h - 1) and
+ * y_min the smallest y of the group:
+ *   q0, q25, q50, q75, q100 of x / 2^30 as above;
+ *   D_0%  = y(v_0) / y_min                 (the CDF at 0),
+ *   D_50% = (y(v_(m-1)/2) / y_min + y(v_m/2) / y_min) / 2  (the CDF at 1/2),
+ *   Ovr_h = D_50% / D_0%.
+ * gout [9][P * O * NG] at g * NG + h: q0, q25, q50, q75, q100, y_min, D_0%,
+ * D_50%, Ovr_h (NaN when m_h = 0); gcnt = m_h.  The operation's
+ * Ovr_overlap (out 14, eq. 9) is the median over the GPUs with m_h > 0 of
+ * Ovr_h (sorted, (v[(k-1)/2] + v[k/2]) / 2), and Ovr_freq (out 15, eq. 10)
+ * divides by it.  D0 and D50 (out 3, 4) stay the least-squares line's
+ * values at 0 and 50 % overlap.
  * ------------------------------------------------------------------------ */
 typedef unsigned __int128 u128;
+
+typedef struct { uint32_t x; int64_t r, y; } cdf_item;
+
+static int cmp_cdf(const void* a_, const void* b_) {
+  const cdf_item* a = (const cdf_item*)a_;
+  const cdf_item* b = (const cdf_item*)b_;
+  if (a->x != b->x) return a->x < b->x ? -1 : 1;
+  return a->r < b->r ? -1 : a->r > b->r;
+}
+
+static int cmp_f64(const void* a_, const void* b_) {
+  const double a = *(const double*)a_, b = *(const double*)b_;
+  return a < b ? -1 : a > b;
+}
 
 static int cmp_u32(const void* x, const void* y) {
   const uint32_t a = *(const uint32_t*)x, b = *(const uint32_t*)y;
@@ -1108,7 +1140,9 @@ void orc_op_stats(int64_t lo, int64_t hi, int64_t cap, const uint32_t* path,
                   const int64_t* dur, const int64_t* gap, const int64_t* ovl,
                   const uint64_t* ctr, int nc, const uint32_t* m_label,
                   int P, int O, double freq_peak, double tpt_peak,
-                  const double* f_gemm, double* out, int64_t* cnt) {
+                  const double* f_gemm, double* out, int64_t* cnt,
+                  const uint8_t* rgpu, int NG, double* gout,
+                  int64_t* gcnt) {
   const int G = P * O;
   const double nan = __builtin_nan("");
   /* the group of every row (-1: not an instance), then each group's rows */
@@ -1159,6 +1193,11 @@ void orc_op_stats(int64_t lo, int64_t hi, int64_t cap, const uint32_t* path,
     cnt[g] = m;
     double* o_ = out;
     for (int k = 0; k < 17; ++k) o_[(int64_t)k * G + g] = nan;
+    for (int h = 0; h < NG; ++h) {
+      gcnt[(int64_t)g * NG + h] = 0;
+      for (int z = 0; z < 9; ++z)
+        gout[(int64_t)z * G * NG + (int64_t)g * NG + h] = nan;
+    }
     if (m > 0) {
       const i128 cov = (i128)m * sxy - sx * sy;
       const i128 vx = (i128)m * sxx - sx * sx;
@@ -1185,7 +1224,53 @@ void orc_op_stats(int64_t lo, int64_t hi, int64_t cap, const uint32_t* path,
       o_[9 * G + g] = (double)xs[m - 1] * q;
       const double dact = (double)sy / dm;
       o_[10 * G + g] = dact;
-      const double ovr_ov = d50 / d0;
+      /* per-GPU CDFs of the group, and eq. 9 as their median over GPUs */
+      cdf_item* it = (cdf_item*)malloc(sizeof(cdf_item) * (size_t)m);
+      double* ovr_h = (double*)malloc(sizeof(double) * (size_t)(NG > 0 ? NG : 1));
+      int k_h = 0;
+      for (int h = 0; h < NG; ++h) {
+        const int64_t gi = (int64_t)g * NG + h;
+        int64_t mh = 0;
+        for (int64_t q2 = start[g]; q2 < start[g + 1]; ++q2) {
+          const int64_t r = rows[q2];
+          if (rgpu[r] != h) continue;
+          it[mh].x = (uint32_t)(((i128)ovl[r] << 30) / dur[r]);
+          it[mh].r = r;
+          it[mh].y = dur[r] + gap[r];
+          ++mh;
+        }
+        gcnt[gi] = mh;
+        for (int z = 0; z < 9; ++z) gout[(int64_t)z * G * NG + gi] = nan;
+        if (mh == 0) continue;
+        qsort(it, (size_t)mh, sizeof(cdf_item), cmp_cdf);
+        int64_t ymin = it[0].y;
+        for (int64_t k = 1; k < mh; ++k)
+          if (it[k].y < ymin) ymin = it[k].y;
+        const double qq = 1.0 / 1073741824.0, dy = (double)ymin;
+        double* go = gout + gi;
+        const int64_t GN = (int64_t)G * NG;
+        go[0 * GN] = (double)it[0].x * qq;
+        go[1 * GN] = (double)it[(mh - 1) / 4].x * qq;
+        go[2 * GN] = ((double)it[(mh - 1) / 2].x + (double)it[mh / 2].x) /
+                     2.0 * qq;
+        go[3 * GN] = (double)it[3 * (mh - 1) / 4].x * qq;
+        go[4 * GN] = (double)it[mh - 1].x * qq;
+        go[5 * GN] = dy;
+        const double c0 = (double)it[0].y / dy;
+        const double c50 = ((double)it[(mh - 1) / 2].y / dy +
+                            (double)it[mh / 2].y / dy) / 2.0;
+        go[6 * GN] = c0;
+        go[7 * GN] = c50;
+        go[8 * GN] = c50 / c0;
+        ovr_h[k_h++] = c50 / c0;
+      }
+      double ovr_ov = nan;
+      if (k_h > 0) {
+        qsort(ovr_h, (size_t)k_h, sizeof(double), cmp_f64);
+        ovr_ov = (ovr_h[(k_h - 1) / 2] + ovr_h[k_h / 2]) / 2.0;
+      }
+      free(it);
+      free(ovr_h);
       o_[14 * G + g] = ovr_ov;
       if (nc >= 16) {
         const double dpeak = (double)cyc * 1000.0 / freq_peak / dm;

@@ -82,7 +82,8 @@ class StatsSpec(ctypes.Structure):
                 ("n_phases", ctypes.c_int32), ("n_ops", ctypes.c_int32),
                 ("freq_peak_mhz", ctypes.c_double),
                 ("tpt_peak", ctypes.c_double),
-                ("f_gemm", ctypes.POINTER(ctypes.c_double))]
+                ("f_gemm", ctypes.POINTER(ctypes.c_double)),
+                ("n_gpus", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class CounterPass(ctypes.Structure):
@@ -143,8 +144,8 @@ def _load():
                                                  P, P, P, P, P]
     lib.chopper_op_stats.argtypes = [ctypes.POINTER(Rows), i32, i32,
                                      ctypes.POINTER(Markers),
-                                     ctypes.POINTER(StatsSpec), P, P, P, SZ,
-                                     P, P]
+                                     ctypes.POINTER(StatsSpec), P, P, P, P,
+                                     P, SZ, P, P]
     lib.chopper_join_counters.argtypes = [ctypes.POINTER(Records), P, P, P,
                                           i32, i32, ctypes.POINTER(Markers),
                                           ctypes.POINTER(CounterPass), i32, P,
@@ -486,33 +487,41 @@ class Pipeline:
     def op_stats(self, phase_level: int = 1, op_level: int = 3,
                  n_phases: int = 3, n_ops: int = 64,
                  freq_peak_mhz: float = 2100.0, tpt_peak: float = 1.0,
-                 f_gemm=None):
+                 f_gemm=None, per_gpu: bool = False):
         """Overlap statistics and overhead breakdown per (phase, operation)
         from the aggregated rows (chopper_op_stats); returns device tensors
-        out [17][n_phases * n_ops] and cnt [n_phases * n_ops]."""
+        out [17][n_phases * n_ops] and cnt [n_phases * n_ops], and with
+        per_gpu also the per-GPU overlap CDFs gout [9][n_phases * n_ops *
+        n_gpus] and gcnt [n_phases * n_ops * n_gpus]."""
         dt = self.dt
         dev = dt.start.device
         G = n_phases * n_ops
+        NG = dt.n_gpus
         out = torch.empty(17, G, dtype=torch.float64, device=dev)
         cnt = torch.empty(G, dtype=torch.int64, device=dev)
+        gout = torch.empty(9, G * NG, dtype=torch.float64, device=dev)
+        gcnt = torch.empty(G * NG, dtype=torch.int64, device=dev)
         fg = None
         if f_gemm is not None:
             fg = (ctypes.c_double * n_ops)(*[float(v) for v in f_gemm])
         spec = StatsSpec(phase_level, op_level, n_phases, n_ops,
                          float(freq_peak_mhz), float(tpt_peak),
                          ctypes.cast(fg, ctypes.POINTER(ctypes.c_double))
-                         if fg is not None else None)
+                         if fg is not None else None, NG, 0)
         rows = self.rows.struct()
 
         def go(scratch, sbytes):
             return lib.chopper_op_stats(
                 ctypes.byref(rows), dt.depth, dt.n_counters,
                 ctypes.byref(self._mk), ctypes.byref(spec), _ptr(out),
-                _ptr(cnt), scratch, sbytes, _ptr(self.status), _stream())
+                _ptr(cnt), _ptr(gout), _ptr(gcnt), scratch, sbytes,
+                _ptr(self.status), _stream())
         if "stats" not in self._scr:
             self._scr["stats"] = _scratch(go, dev)
         scr, sb = _aligned(self._scr["stats"])
         _check(go(scr, ctypes.byref(sb)), "op_stats")
+        if per_gpu:
+            return out, cnt, gout, gcnt
         return out, cnt
 
     def join_counters(self, passes, iter_level: int = 0):

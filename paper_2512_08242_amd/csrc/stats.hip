@@ -13,6 +13,7 @@
 // -- and build the histograms of a radix selection of six order statistics
 // of the ratio per group, eight bits per pass, all groups at once.
 #include "common.h"
+#include "sort.h"
 #include "wave.h"
 
 namespace chopper {
@@ -92,6 +93,15 @@ __device__ inline uint32_t lds_claim(uint32_t* h, uint32_t bin, bool act) {
     return base + lanes_below(m);
   }
   return act ? atomicAdd(&h[bin], 1u) : 0u;
+}
+
+__global__ void k_stats_clear_cdf(int64_t NGG, uint32_t* cnt,
+                                  uint64_t* ymin) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < NGG) {
+    cnt[i] = 0;
+    ymin[i] = ~0ull;
+  }
 }
 
 __global__ void k_stats_clear(uint32_t* cnt, int G, uint32_t* hist,
@@ -487,19 +497,137 @@ __global__ __launch_bounds__(kBlock) void k_stats_final(
   o[16 * G + g] = fg / S.tpt_peak;
 }
 
+// ------------------------------------------------------ per-GPU overlap CDF
+// Instances of (phase, operation) group g on GPU h form CDF group
+// c = g * NG + h.  Every row slot of the rows output gets the sort key
+// c << 31 | x (x = overlap ratio in Q30), or `sentinel` (above every key)
+// when it is no instance; its value is the slot.  After a stable sort by
+// key each CDF group is a run in CDF order: ascending x, equal x in row
+// order, which is time order on a GPU.
+struct CdfArgs {
+  StatArgs A;
+  const uint8_t* gpu;
+  int NG;
+};
+
+__global__ __launch_bounds__(kBlock) void k_cdf_keys(CdfArgs C,
+                                                     uint64_t sentinel,
+                                                     uint64_t* key,
+                                                     uint32_t* val,
+                                                     uint32_t* gcnt,
+                                                     uint64_t* ymin) {
+  const StatArgs& A = C.A;
+  const int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (r >= A.cap) return;
+  int64_t lo, hi;
+  level_range(A, lo, hi);
+  uint64_t k = sentinel;
+  if (r >= lo && r < hi && A.kind[r] == 0 && A.dur[r] > 0) {
+    const uint32_t mp = A.path[(int64_t)A.lv_phase * A.cap + r];
+    const uint32_t mo = A.path[(int64_t)A.lv_op * A.cap + r];
+    const uint32_t h = C.gpu[r];
+    if ((int64_t)mp < A.nm && (int64_t)mo < A.nm && (int)h < C.NG) {
+      const uint32_t p = A.label[mp], o = A.label[mo];
+      if (p < (uint32_t)A.P && o < (uint32_t)A.O) {
+        const uint64_t c = (uint64_t)(p * (uint32_t)A.O + o) * C.NG + h;
+        const uint64_t d = (uint64_t)A.dur[r];
+        uint64_t x = ((uint64_t)A.ovl[r] << 30) / d;
+        if (x > 0x7FFFFFFFull) x = 0x7FFFFFFFull;   // (RANGE, set elsewhere)
+        k = c << 31 | x;
+        atomicAdd(&gcnt[c], 1u);
+        atomicMin((unsigned long long*)&ymin[c],
+                  (unsigned long long)(d + (uint64_t)A.gap[r]));
+      }
+    }
+  }
+  key[r] = k;
+  val[r] = (uint32_t)r;
+}
+
+// one thread per CDF group: quantiles of x, y_min, D_0%, D_50% and their
+// ratio, in the same IEEE operations as their definition
+__global__ __launch_bounds__(kBlock) void k_cdf_final(
+    CdfArgs C, int64_t NGG, const uint32_t* gcnt, const uint32_t* goff,
+    const uint64_t* skey, const uint32_t* sval, const uint64_t* ymin,
+    double* gout, int64_t* gcnt_out) {
+  const int64_t c = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (c >= NGG) return;
+  const int64_t m = gcnt[c];
+  gcnt_out[c] = m;
+  const double nan = __builtin_nan("");
+  if (m == 0) {
+    for (int z = 0; z < 9; ++z) gout[(int64_t)z * NGG + c] = nan;
+    return;
+  }
+  const int64_t b = goff[c];
+  auto xq = [&](int64_t k) {
+    return (double)(uint32_t)(skey[b + k] & 0x7FFFFFFFull);
+  };
+  auto yk = [&](int64_t k) {
+    const uint32_t r = sval[b + k];
+    return (double)(C.A.dur[r] + C.A.gap[r]);
+  };
+  const double q = 1.0 / 1073741824.0, dy = (double)ymin[c];
+  gout[0 * NGG + c] = xq(0) * q;
+  gout[1 * NGG + c] = xq((m - 1) / 4) * q;
+  gout[2 * NGG + c] = (xq((m - 1) / 2) + xq(m / 2)) / 2.0 * q;
+  gout[3 * NGG + c] = xq(3 * (m - 1) / 4) * q;
+  gout[4 * NGG + c] = xq(m - 1) * q;
+  gout[5 * NGG + c] = dy;
+  const double c0 = yk(0) / dy;
+  const double c50 = (yk((m - 1) / 2) / dy + yk(m / 2) / dy) / 2.0;
+  gout[6 * NGG + c] = c0;
+  gout[7 * NGG + c] = c50;
+  gout[8 * NGG + c] = c50 / c0;
+}
+
+// eq. 9 per (phase, operation): the median over its GPUs with instances of
+// their D_50% / D_0%; eq. 10 divides by it (overwrites columns 14 and 15 of
+// k_stats_final)
+__global__ __launch_bounds__(kBlock) void k_cdf_pool(int G, int NG, int nc,
+                                                     const int64_t* gcnt,
+                                                     const double* gout,
+                                                     int64_t NGG,
+                                                     double* out) {
+  const int g = (int)(blockIdx.x * kBlock + threadIdx.x);
+  if (g >= G) return;
+  double v[256];
+  int k = 0;
+  for (int h = 0; h < NG; ++h) {
+    const int64_t c = (int64_t)g * NG + h;
+    if (gcnt[c] == 0) continue;
+    // insertion into ascending order
+    const double x = gout[8 * NGG + c];
+    int j = k++;
+    while (j > 0 && v[j - 1] > x) {
+      v[j] = v[j - 1];
+      --j;
+    }
+    v[j] = x;
+  }
+  const double ovr = k > 0 ? (v[(k - 1) / 2] + v[k / 2]) / 2.0
+                           : __builtin_nan("");
+  out[14 * (int64_t)G + g] = ovr;
+  if (nc >= 16)
+    out[15 * (int64_t)G + g] =
+        out[10 * (int64_t)G + g] / out[11 * (int64_t)G + g] / ovr;
+}
+
 }  // namespace
 
 extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
                                 int32_t n_counters,
                                 const chopper_markers* mk,
                                 const chopper_stats_spec* spec, double* out,
-                                int64_t* cnt, void* scratch,
+                                int64_t* cnt, double* gpu_out,
+                                int64_t* gpu_cnt, void* scratch,
                                 size_t* scratch_bytes, uint32_t* status,
                                 void* stream) {
   if (!rows || !spec || !mk || !validate_markers(mk) || !scratch_bytes ||
       !out || !cnt)
     return CHOPPER_EINVAL;
-  const int P = spec->n_phases, O = spec->n_ops;
+  const int P = spec->n_phases, O = spec->n_ops, NG = spec->n_gpus;
+  if (NG < 1 || NG > 256) return CHOPPER_EINVAL;
   if (depth < 1 || depth > mk->depth || spec->phase_level < 0 ||
       spec->phase_level >= depth || spec->op_level < 0 ||
       spec->op_level >= depth || P < 1 || P > 16 || O < 1 || O > 128 ||
@@ -507,7 +635,7 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
       rows->cap >= (int64_t)0xFFFFFFFF || !rows->level_offset)
     return CHOPPER_EINVAL;
   if (rows->cap > 0 && (!rows->path || !rows->kind || !rows->dur ||
-                        !rows->gap || !rows->ovl ||
+                        !rows->gap || !rows->ovl || !rows->gpu ||
                         (n_counters > 0 && !rows->ctr)))
     return CHOPPER_EINVAL;
   if (mk->n > 0 && !mk->label) return CHOPPER_EINVAL;
@@ -515,10 +643,17 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
   const int64_t cap = rows->cap;
   const int64_t nchunk = ceil_div(cap, kChunk) + G;
   const int64_t nh = (int64_t)G * kRanks * 256;
+  const int64_t NGG = (int64_t)G * NG;      // CDF groups
+  const int64_t capn = cap > 0 ? cap : 1;
   struct Bufs {
     uint32_t *key, *gcnt, *off, *cur, *coff, *xs, *ghist, *spre;
     uint64_t *ys, *csum, *part;
     int64_t* srank;
+    uint32_t *ccnt, *coffs, *cscan, *ctot, *sval;
+    uint64_t *ymin, *skey;
+    double* gout;
+    int64_t* gcnt_out;
+    ClassSortLayout sort;
   } B;
   auto layout = [&](Scratch& sc) {
     B.key = sc.take<uint32_t>(cap);
@@ -533,6 +668,17 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
     B.ghist = sc.take<uint32_t>(nh);
     B.spre = sc.take<uint32_t>((int64_t)G * kRanks);
     B.srank = sc.take<int64_t>((int64_t)G * kRanks);
+    B.ccnt = sc.take<uint32_t>(NGG);
+    B.coffs = sc.take<uint32_t>(NGG + 1);
+    B.cscan = sc.take<uint32_t>(scan_scratch_elems(NGG));
+    B.ctot = sc.take<uint32_t>(1);
+    B.ymin = sc.take<uint64_t>(NGG);
+    B.skey = sc.take<uint64_t>(capn);
+    B.sval = sc.take<uint32_t>(capn);
+    // (per-GPU results in scratch when the caller passes no arrays)
+    B.gout = gpu_out ? gpu_out : sc.take<double>(9 * NGG);
+    B.gcnt_out = gpu_cnt ? gpu_cnt : sc.take<int64_t>(NGG);
+    B.sort = class_sort_layout(sc, capn, 256);
   };
   Scratch probe(nullptr);
   layout(probe);
@@ -575,6 +721,34 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
                      (const uint32_t*)B.coff, G, O, n_counters,
                      (const uint64_t*)B.part, (const uint64_t*)B.csum,
                      (const uint32_t*)B.spre, S));
+  // per-GPU overlap CDFs, and eq. 9 / eq. 10 from them
+  const CdfArgs C{A, rows->gpu, NG};
+  const uint64_t sentinel = (uint64_t)NGG << 31;
+  int bits = 0;
+  while (bits < 64 && (sentinel >> bits) != 0) ++bits;
+  CHOPPER_HIP(launch("stats_cdf", k_stats_clear_cdf, grid_for(NGG, kBlock),
+                     dim3(kBlock), s, NGG, B.ccnt, B.ymin));
+  if (cap > 0) {
+    CHOPPER_HIP(launch("stats_cdf", k_cdf_keys, grid_for(cap, kBlock),
+                       dim3(kBlock), s, C, sentinel, B.sort.key0, B.sort.val0,
+                       B.ccnt, B.ymin));
+    ClassSortLayout L = B.sort;
+    L.n = cap;
+    L.ntiles = sort_tiles(cap);
+    rc = radix_sort_pairs(L, bits, B.sval, B.skey, s);
+    if (rc != CHOPPER_OK) return rc;
+  }
+  CHOPPER_HIP(exclusive_scan<uint32_t>(B.ccnt, B.coffs, NGG, B.cscan, B.ctot,
+                                       s));
+  CHOPPER_HIP(launch("stats_cdf", k_cdf_final, grid_for(NGG, kBlock),
+                     dim3(kBlock), s, C, NGG, (const uint32_t*)B.ccnt,
+                     (const uint32_t*)B.coffs, (const uint64_t*)B.skey,
+                     (const uint32_t*)B.sval, (const uint64_t*)B.ymin, B.gout,
+                     B.gcnt_out));
+  CHOPPER_HIP(launch("stats_cdf", k_cdf_pool, grid_for(G, kBlock),
+                     dim3(kBlock), s, G, NG, n_counters,
+                     (const int64_t*)B.gcnt_out, (const double*)B.gout, NGG,
+                     out));
   return CHOPPER_OK;
 }
 

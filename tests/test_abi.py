@@ -320,26 +320,35 @@ def test_op_stats_scratch_query_and_argument_errors(ch):
         sz = ctypes.c_size_t(0)
         rc = lib.chopper_op_stats(ctypes.byref(rows), depth, nc,
                                   ctypes.byref(mk), ctypes.byref(spec), out,
-                                  fake, None, ctypes.byref(sz), None, None)
+                                  fake, None, None, None, ctypes.byref(sz),
+                                  None, None)
         return rc, sz.value
 
-    good = b.StatsSpec(1, 3, 3, 64, 2100.0, 1.0, None)
+    def spec(*a, n_gpus=8):
+        return b.StatsSpec(*a, None, n_gpus, 0)
+
+    good = spec(1, 3, 3, 64, 2100.0, 1.0)
     rc, sz = call(good)
     assert rc == 0 and sz > 0
     rc2, sz2 = call(good, cap=10**6)
     assert rc2 == 0 and sz2 > sz + 4 * 10**6
-    for bad in (b.StatsSpec(1, 4, 3, 64, 2100.0, 1.0, None),   # level >= depth
-                b.StatsSpec(-1, 3, 3, 64, 2100.0, 1.0, None),
-                b.StatsSpec(1, 3, 0, 64, 2100.0, 1.0, None),   # no phase
-                b.StatsSpec(1, 3, 17, 64, 2100.0, 1.0, None),  # > 16 phases
-                b.StatsSpec(1, 3, 3, 0, 2100.0, 1.0, None),
-                b.StatsSpec(1, 3, 3, 129, 2100.0, 1.0, None)):  # > 128 ops
+    # the per-GPU CDF tables grow with the GPUs
+    rc3, sz3 = call(spec(1, 3, 3, 64, 2100.0, 1.0, n_gpus=256))
+    assert rc3 == 0 and sz3 > sz
+    for bad in (spec(1, 4, 3, 64, 2100.0, 1.0),   # level >= depth
+                spec(-1, 3, 3, 64, 2100.0, 1.0),
+                spec(1, 3, 0, 64, 2100.0, 1.0),   # no phase
+                spec(1, 3, 17, 64, 2100.0, 1.0),  # > 16 phases
+                spec(1, 3, 3, 0, 2100.0, 1.0),
+                spec(1, 3, 3, 129, 2100.0, 1.0),  # > 128 ops
+                spec(1, 3, 3, 64, 2100.0, 1.0, n_gpus=0),
+                spec(1, 3, 3, 64, 2100.0, 1.0, n_gpus=257)):
         assert call(bad)[0] == -1
     assert call(good, depth=5)[0] == -1          # deeper than the markers
     assert call(good, nc=17)[0] == -1
     assert call(good, out=None)[0] == -1
     sz = ctypes.c_size_t(8)
     assert lib.chopper_op_stats(ctypes.byref(rows), 4, 16, ctypes.byref(mk),
-                                ctypes.byref(good), fake, fake,
+                                ctypes.byref(good), fake, fake, None, None,
                                 ctypes.c_void_p(0x10000), ctypes.byref(sz),
                                 fake, None) == -2

@@ -32,23 +32,32 @@ def stats_both(ch, tr, **spec):
     pipe = ch.Pipeline(ch.DeviceTrace(tr, "cuda"))
     pipe.status.zero_()
     pipe.step()
-    out, cnt = pipe.op_stats(**spec)
+    out, cnt, gout, gcnt = pipe.op_stats(per_gpu=True, **spec)
     got = (out.cpu().numpy(), cnt.cpu().numpy(),
-           int(pipe.status.item()) & 0xFFFFFFFF)
+           int(pipe.status.item()) & 0xFFFFFFFF, gout.cpu().numpy(),
+           gcnt.cpu().numpy())
     ref = oracle.op_stats(oracle.run(tr)["rows"], tr.m_label, tr.depth,
-                          **spec)
+                          n_gpus=tr.n_gpus, per_gpu=True, **spec)
     return got, ref
 
 
-def check(got, ref, name):
-    go, gc, _ = got
-    ro, rc = ref
-    assert np.array_equal(gc, rc), name
-    same = (go == ro) | (np.isnan(go) & np.isnan(ro))
+def _same_doubles(a, b, names, name):
+    same = (a == b) | (np.isnan(a) & np.isnan(b))
     if not same.all():
         k, g = np.argwhere(~same)[0]
-        raise AssertionError(f"{name}: {oracle.OP_STATS[k]} of group {g}: "
-                             f"{go[k, g]!r} vs {ro[k, g]!r}")
+        raise AssertionError(f"{name}: {names[k]} of group {g}: "
+                             f"{a[k, g]!r} vs {b[k, g]!r}")
+
+
+def check(got, ref, name):
+    go, gc, _, gg, ggc = got
+    ro, rc, rg, rgc = ref
+    assert np.array_equal(gc, rc), name
+    _same_doubles(go, ro, oracle.OP_STATS, name)
+    # the per-GPU overlap CDFs behind eq. 9
+    assert np.array_equal(ggc, rgc), name + " per-GPU counts"
+    _same_doubles(gg, rg, oracle.OP_CDF, name + " per GPU")
+    assert ggc.sum() <= gc.sum()
 
 
 @pytest.mark.parametrize("cid", [0, 1, 2])
