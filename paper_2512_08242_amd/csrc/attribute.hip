@@ -60,6 +60,71 @@ __global__ __launch_bounds__(kBlock) void k_marker_links(
 // hundred operation markers)
 constexpr int kMarkWin = 512;
 
+// One thread per (wave tile, level): the window of level-l markers for the
+// tile's records of its first gpu, found ahead of the records kernel so that
+// its waves do not wait on the search.  The tile's time range is taken from
+// its first record and the last record of the same gpu (both found by
+// position, exact for records in (gpu, start') order); the records kernel
+// uses the window only when its records' starts lie inside that range.
+// win [tile][level][2]: first marker position and count (count kNone:
+// none); wt [2][tiles]: the range.
+__global__ __launch_bounds__(kBlock) void k_attr_windows(
+    int64_t n, int64_t ntiles, int G, int D, const uint8_t* gpu,
+    const int64_t* start, BIndex X, uint32_t* win, int64_t* wt) {
+  const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (t >= ntiles * D) return;
+  const int64_t w = t / D;
+  const int l = (int)(t - w * D);
+  const int64_t base = w * (int64_t)kWaveTile;
+  int64_t last = base + kWaveTile - 1 < n - 1 ? base + kWaveTile - 1 : n - 1;
+  const uint32_t g0 = gpu[base];
+  uint32_t* o = win + 2 * t;
+  if (g0 >= (uint32_t)G) {
+    o[0] = 0;
+    o[1] = kNone;
+    if (l == 0) {
+      wt[w] = kI64Max;
+      wt[ntiles + w] = kI64Min;
+    }
+    return;
+  }
+  // last position of gpu g0 in the tile (gpu ids non-decreasing there;
+  // otherwise the range check of the records kernel rejects the window)
+  if (gpu[last] != g0) {
+    int64_t lo = base, hi = last;          // gpu[lo] == g0, gpu[hi] != g0
+    while (hi - lo > 1) {
+      const int64_t mid = (lo + hi) >> 1;
+      if (gpu[mid] == g0) lo = mid;
+      else hi = mid;
+    }
+    last = lo;
+  }
+  const int64_t smin = start[base], smax = start[last];
+  if (smax < smin) {
+    o[0] = 0;
+    o[1] = kNone;
+    if (l == 0) {
+      wt[w] = kI64Max;
+      wt[ntiles + w] = kI64Min;
+    }
+    return;
+  }
+  const BSeg P = X.seg[g0 * D + l];
+  int64_t lo[2], hi[2];
+  const int64_t tt[2] = {smin, smax};
+  bi_range(X, P, smin, &lo[0], &hi[0]);
+  bi_range(X, P, smax, &lo[1], &hi[1]);
+  bsearch_k<2>(X.key, lo, hi, tt);
+  const int64_t wlo = lo[0] - 1 > (int64_t)P.sb ? lo[0] - 1 : (int64_t)P.sb;
+  const int64_t wk = lo[1] - wlo;
+  o[0] = (uint32_t)wlo;
+  o[1] = wk <= (int64_t)kMarkWin ? (uint32_t)wk : kNone;
+  if (l == 0) {
+    wt[w] = smin;
+    wt[ntiles + w] = smax;
+  }
+}
+
 // Records in natural order, wave tiles of kWaveTile, each lane owning eight
 // consecutive records (vector loads and stores).  For the tile's first gpu,
 // lane l finds the window of level-l markers that the tile's starts can
@@ -73,7 +138,8 @@ constexpr int kMarkWin = 512;
 template <int MaxD>
 __global__ __launch_bounds__(kBlock) void k_attribute_records(
     int64_t n, int G, int D, const uint8_t* gpu, const int64_t* start,
-    BIndex X, const int64_t* sme, const uint32_t* sid, uint32_t* idx) {
+    BIndex X, const int64_t* sme, const uint32_t* sid, const uint32_t* pwin,
+    const int64_t* pwt, int64_t ntiles, uint32_t* idx) {
   __shared__ int64_t s_ps[kWavesPerBlock][kMarkWin];
   __shared__ int64_t s_pe[kWavesPerBlock][kMarkWin];
   __shared__ uint32_t s_pi[kWavesPerBlock][kMarkWin];
@@ -86,6 +152,16 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
   uint32_t* pi = s_pi[wv];
   const int64_t k0 = base + (int64_t)lane * kTileIpt;   // lane's first record
   const bool full = base + kWaveTile <= n;                // uniform
+  // the precomputed window of every level and its time range (loaded with
+  // the records)
+  const int64_t tile = base / kWaveTile;
+  uint32_t pw_lo = 0, pw_k = kNone;
+  if (lane < D) {
+    const uint2 v = *reinterpret_cast<const uint2*>(pwin + 2 * (tile * D + lane));
+    pw_lo = v.x;
+    pw_k = v.y;
+  }
+  const int64_t pt_lo = pwt[tile], pt_hi = pwt[ntiles + tile];
   // vector loads only from suitably aligned columns
   const bool vload = full && ((uintptr_t)gpu & 7) == 0 &&
                      ((uintptr_t)start & 15) == 0;
@@ -129,17 +205,24 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
     }
   smin = lane63(wave_incl(smin, OpMin(), kI64Max));
   smax = lane63(wave_incl(smax, OpMax(), kI64Min));
-  // lane l < D: window of level l
+  // lane l < D: window of level l -- the precomputed one when the tile's
+  // starts lie in its range, else searched here
+  const bool pre = smin >= pt_lo && smax <= pt_hi;      // (uniform)
   int64_t wlo = 0, wk = 0;
   if (g0ok && lane < D) {
-    const BSeg P = X.seg[g0 * D + lane];
-    int64_t lo[2], hi[2];
-    const int64_t t[2] = {smin, smax};
-    bi_range(X, P, smin, &lo[0], &hi[0]);
-    bi_range(X, P, smax, &lo[1], &hi[1]);
-    bsearch_k<2>(X.key, lo, hi, t);
-    wlo = lo[0] - 1 > (int64_t)P.sb ? lo[0] - 1 : (int64_t)P.sb;
-    wk = lo[1] - wlo;
+    if (pre) {
+      wlo = pw_lo;
+      wk = pw_k == kNone ? (int64_t)kMarkWin + 1 : (int64_t)pw_k;
+    } else {
+      const BSeg P = X.seg[g0 * D + lane];
+      int64_t lo[2], hi[2];
+      const int64_t t[2] = {smin, smax};
+      bi_range(X, P, smin, &lo[0], &hi[0]);
+      bi_range(X, P, smax, &lo[1], &hi[1]);
+      bsearch_k<2>(X.key, lo, hi, t);
+      wlo = lo[0] - 1 > (int64_t)P.sb ? lo[0] - 1 : (int64_t)P.sb;
+      wk = lo[1] - wlo;
+    }
   }
   // pool offsets: levels in order while they fit
   const int64_t woff = wave_incl(wk, OpAdd(), (int64_t)0) - wk;
@@ -221,11 +304,18 @@ struct AttrLayout {
   uint32_t* btable;
   int64_t btable_cap;
   uint32_t* btmp;
+  uint32_t* pwin;     // [tiles][D][2] precomputed marker windows
+  int64_t* pwt;       // [2][tiles] their time ranges
+  int64_t ntiles;
   ClassSortLayout sort;
 };
 
-static AttrLayout attr_layout(Scratch& sc, int64_t nm, int G, int D) {
+static AttrLayout attr_layout(Scratch& sc, int64_t n, int64_t nm, int G,
+                              int D) {
   AttrLayout L;
+  L.ntiles = ceil_div(n, (int64_t)kWaveTile);
+  L.pwin = sc.take<uint32_t>(L.ntiles * D * 2);
+  L.pwt = sc.take<int64_t>(2 * L.ntiles);
   const int C = G * D * 2 + 1;
   L.mord = sc.take<uint32_t>(nm);
   L.coff = sc.take<uint32_t>(C + 1);
@@ -259,13 +349,13 @@ extern "C" int chopper_attribute(const chopper_records* rec,
   if (n > 0 && (!start_al || !idx_out)) return CHOPPER_EINVAL;
   if (nm > 0 && (!mstart_al || !mend_al)) return CHOPPER_EINVAL;
   Scratch probe(nullptr);
-  attr_layout(probe, nm, G, D);
+  attr_layout(probe, n, nm, G, D);
   int rc = scratch_check(scratch, scratch_bytes, probe.used);
   if (rc != 0) return rc > 0 ? CHOPPER_OK : rc;
   if (!status) return CHOPPER_EINVAL;
   hipStream_t s = (hipStream_t)stream;
   Scratch sc(scratch);
-  AttrLayout L = attr_layout(sc, nm, G, D);
+  AttrLayout L = attr_layout(sc, n, nm, G, D);
   KeyMarker km{mk->gpu, mk->level, mstart_al, mend_al, G, D};
   bool range_err = false;
   rc = class_sort(km, L.sort, L.mord, L.coff, &range_err, s, -1);
@@ -294,10 +384,14 @@ extern "C" int chopper_attribute(const chopper_records* rec,
                            nm > 0));
   const BIndex X{L.sms, L.bsegs, L.btable};
   const unsigned grid = (unsigned)ceil_div(n, (int64_t)kWaveTile * kWavesPerBlock);
+  CHOPPER_HIP(launch("attr_windows", k_attr_windows,
+                     grid_for(L.ntiles * D, kBlock), dim3(kBlock), s, n,
+                     L.ntiles, G, D, rec->gpu, start_al, X, L.pwin, L.pwt));
   auto run = [&](auto kern) -> int {
     CHOPPER_HIP(launch("attr_records", kern, dim3(grid), dim3(kBlock), s, n,
                        G, D, rec->gpu, start_al, X, (const int64_t*)L.sme,
-                       (const uint32_t*)L.sid, idx_out));
+                       (const uint32_t*)L.sid, (const uint32_t*)L.pwin,
+                       (const int64_t*)L.pwt, L.ntiles, idx_out));
     return CHOPPER_OK;
   };
   if (D <= 4) return run(k_attribute_records<4>);

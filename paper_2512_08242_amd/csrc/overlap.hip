@@ -824,6 +824,9 @@ __global__ __launch_bounds__(kBlock) void k_gap(
   int64_t* sl = s_slice[wv];
   uint32_t r[kTileIpt], key[kTileIpt], comp[kTileIpt];
   int64_t s[kTileIpt], e[kTileIpt];
+  // the record before the tile, loaded with the tile's own (it usually
+  // settles the carry below)
+  const uint32_t rb = order[base > 0 ? base - 1 : 0];
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j) {
     const int64_t p = base + (int64_t)j * kWave + lane;
@@ -834,14 +837,29 @@ __global__ __launch_bounds__(kBlock) void k_gap(
     s[j] = start[r[j]];
     e[j] = end[r[j]];
   }
+  const uint32_t kb_key = (uint32_t)gpu[rb] * 256u + stream[rb];
+  const bool kb_compute = !kind_of(cls[rb]);
+  const int64_t kb_end = end[rb];
   // carry into the tile for its first key
   const uint32_t key0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)key[0]);
   bool need = false;
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j) need = need || (comp[j] && key[j] == key0);
   LastComp carry{key0, 0u, 0};
-  if (__ballot(need) != 0 && lane == 0) {
-    for (int64_t q = base - 1; q >= 0; --q) {
+  if (__ballot(need) != 0 && lane == 0 && base > 0) {
+    // the record before the tile decides unless it is a communication
+    // record of the same key; then walk further back
+    int64_t q = base - 1;
+    if (kb_key != key0) {
+      q = -1;
+    } else if (kb_compute) {
+      carry.has = 1u;
+      carry.end = kb_end;
+      q = -1;
+    } else {
+      q = base - 2;
+    }
+    for (; q >= 0; --q) {
       const uint32_t rq = order[q];
       if ((uint32_t)gpu[rq] * 256u + stream[rq] != key0) break;
       if (!kind_of(cls[rq])) {

@@ -31,7 +31,7 @@ static const char* const kKernelNames[] = {
     "agg_workload_from_gpu", "bi_params", "bi_clear", "bi_fill",
     "bi_fixup", "ov_comm_records", "agg_nat_init", "agg_nat_pre",
     "agg_nat_tiles", "agg_heads_nat", "agg_gpu_rows", "agg_conflict",
-    "agg_exact_keys", "join_resort",
+    "agg_exact_keys", "join_resort", "attr_windows",
     "view_flags", "view_units", "view_fill", "view_records", "view_rows",
     "view_iter_max", "view_medians", "launch_split", "join_fill",
     "join_labels", "join_heads", "join_runs", "join_order", "join_pass_prep",
