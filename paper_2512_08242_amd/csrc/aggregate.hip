@@ -61,6 +61,11 @@ struct RecSrc {
   // exact group ids of the marker levels ([D][n] by korder position), or
   // null: groups by the deepest marker (exact for nested markers)
   const uint32_t* gk;
+  // the general path's items gathered once in korder position order (or
+  // null: gathered through korder where used): marker path [D][n] and
+  // gpu * 2 + kind (0xFFFF: left out by the filter)
+  const uint32_t* ipath;
+  const uint16_t* igk;
 };
 
 struct RowsDev {
@@ -139,10 +144,31 @@ struct RecItem {
 
 __device__ inline void load_item(const RecSrc& S, int64_t pos, RecItem& it) {
   it.r = S.korder[pos];
+  if (S.igk) {
+    const uint32_t v = S.igk[pos];
+    it.ok = v != 0xFFFFu;
+    it.g = (v >> 1) & 255u;
+    it.kind = v & 1u;
+    for (int l = 0; l < S.D; ++l) it.p[l] = S.ipath[(int64_t)l * S.n + pos];
+    return;
+  }
   it.g = S.gpu[it.r];
   it.kind = (uint32_t)kind_of(S.cls[it.r]);
   it.ok = rec_pass(S, it.r);
   for (int l = 0; l < S.D; ++l) it.p[l] = S.idx[(int64_t)l * S.n + it.r];
+}
+
+// The general path's items in korder position order, gathered once.
+__global__ __launch_bounds__(kBlock) void k_agg_items(RecSrc S, uint32_t* ipath,
+                                                      uint16_t* igk) {
+  const int64_t pos = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (pos >= S.n) return;
+  const uint32_t r = S.korder[pos];
+  const uint32_t g = S.gpu[r];
+  const uint32_t kind = (uint32_t)kind_of(S.cls[r]);
+  igk[pos] = rec_pass(S, r) ? (uint16_t)(g * 2u + kind) : (uint16_t)0xFFFFu;
+  for (int l = 0; l < S.D; ++l)
+    ipath[(int64_t)l * S.n + pos] = S.idx[(int64_t)l * S.n + r];
 }
 
 // ------------------------------------------------------------------ election
@@ -390,11 +416,13 @@ struct FromRecords {
   __device__ int64_t count() const { return S.n; }
   __device__ void load(int64_t i, uint32_t& r, bool& ok, uint32_t* p,
                        uint32_t& g, uint32_t& kind, uint32_t& fpos) const {
-    r = S.korder[i];
-    g = S.gpu[r];
-    kind = (uint32_t)kind_of(S.cls[r]);
-    ok = rec_pass(S, r);
-    for (int l = 0; l < S.D; ++l) p[l] = S.idx[(int64_t)l * S.n + r];
+    RecItem it;
+    load_item(S, i, it);
+    r = it.r;
+    g = it.g;
+    kind = it.kind;
+    ok = it.ok;
+    for (int l = 0; l < S.D; ++l) p[l] = it.p[l];
     fpos = (uint32_t)i;
   }
   __device__ uint32_t first_of(uint32_t r) const { return r; }
@@ -551,7 +579,7 @@ template <typename Src>
 __global__ __launch_bounds__(kBlock) void k_agg_reduce(
     Src src, int li, int D, int64_t M, bool atomic_mode, const uint32_t* own,
     const uint32_t* rowof, RowsDev R, Overflow ovf, int nfields,
-    uint32_t* status) {
+    uint32_t* status, uint32_t* cflag) {
   __shared__ uint32_t s_last[kBlock];
   __shared__ uint32_t s_head0[kBlock];
   const int64_t cnt = src.count();
@@ -577,13 +605,24 @@ __global__ __launch_bounds__(kBlock) void k_agg_reduce(
     const uint32_t row = rowof[key];
     tgt[j] = row;
     ownbit[j] = (!atomic_mode && own[key] == fpos) ? 1ull : 0ull;
-    if (li < D && (int64_t)row < R.cap) {
-      for (int l = 0; l <= li; ++l)
-        if (R.path[(int64_t)l * R.cap + row] != p[l]) conflict = true;
+    // the row holds its first item's path: another path here means a
+    // marker shared by different paths (markers not nested); past the
+    // capacity the first item is read instead
+    if (li < D) {
+      if ((int64_t)row < R.cap) {
+        for (int l = 0; l <= li; ++l)
+          if (R.path[(int64_t)l * R.cap + row] != p[l]) conflict = true;
+      } else if constexpr (Src::kRecords) {
+        // (rows of a coarser level always precede those of a finer one, so
+        // only the records' level has items past the capacity)
+        const uint32_t ro = src.S.korder[own[key]];
+        for (int l = 0; l <= li; ++l)
+          if (src.S.idx[(int64_t)l * src.S.n + ro] != p[l]) conflict = true;
+      }
     }
   }
-  if (__ballot(conflict) != 0 && (threadIdx.x & (kWave - 1)) == 0)
-    atomicOr(status, (uint32_t)CHOPPER_ST_PATH_CONFLICT);
+  wave_flag_or(status, conflict, (uint32_t)CHOPPER_ST_PATH_CONFLICT);
+  wave_flag_or(cflag, conflict, 1u);
   // piece boundaries
   s_last[threadIdx.x] = tgt[kAggIpt - 1];
   __syncthreads();
@@ -699,6 +738,8 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads(
   const int64_t w =
       (int64_t)blockIdx.x * kWavesPerBlock + (int64_t)(threadIdx.x / kWave);
   if (w >= nwt) return;
+  // groups already known not to be runs: the counts are not used
+  if (__builtin_amdgcn_readfirstlane((int)flag_read(&flags[0])) & 1) return;
   const int64_t cnt = src.count();
   const int64_t base = w * kWaveTile;
   if (base >= cnt) {
@@ -775,7 +816,7 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads(
       tot += (uint32_t)__popcll(__ballot((c >> b) & 1u)) << b;
     if (lane == 0) tilecnt[(int64_t)(li - lv0) * nwt + w] = tot;
   }
-  if (__ballot(notinc) != 0 && lane == 0) atomicOr(&flags[0], 1u);
+  wave_flag_or(&flags[0], notinc, 1u);
   // a conflict sends the call to the general path, which groups by the
   // whole path
   if (__ballot(conflict) != 0 && lane == 0) {
@@ -940,6 +981,8 @@ __global__ __launch_bounds__(kBlock) void k_nat_pre(
   const int64_t nt =
       (int64_t)blockIdx.x * kWavesPerBlock + (int64_t)(threadIdx.x / kWave);
   if (nt >= nnt) return;
+  // (the order is already known not to qualify: nothing here is used)
+  if (__builtin_amdgcn_readfirstlane((int)flag_read(bad)) != 0) return;
   const int64_t base = nt * kWaveTile;
   const int64_t p0 = base + (int64_t)lane * kAggIpt;
   uint32_t g[kAggIpt], k[kAggIpt];
@@ -999,7 +1042,7 @@ __global__ __launch_bounds__(kBlock) void k_nat_pre(
           : -1;
     if (lane == 0) lpraw[(int64_t)q * lps + nt] = v;
   }
-  if (__ballot(wrong) != 0 && lane == 0) atomicOr(bad, 1u);
+  wave_flag_or(bad, wrong, 1u);
 }
 
 // Block 0: GPU ranges, tile offsets and the GPU of every tile.  Blocks
@@ -1137,6 +1180,7 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads_nat(
   const int wv = (int)(threadIdx.x / kWave);
   const int64_t tt = (int64_t)blockIdx.x * kWavesPerBlock + wv;
   if (tt >= N.nnt + N.G) return;
+  if (__builtin_amdgcn_readfirstlane((int)flag_read(&flags[0])) & 1) return;
   NatTile T;
   if (!nat_tile(N, tt, T)) {
     if (lane <= lv1 - lv0) {
@@ -1243,7 +1287,7 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads_nat(
                 (int64_t)k * T.cg + T.tl] = tot;
     }
   }
-  if (__ballot(notinc) != 0 && lane == 0) atomicOr(&flags[0], 1u);
+  wave_flag_or(&flags[0], notinc, 1u);
   // a conflict sends the call to the general path, which groups by the
   // whole path
   if (__ballot(conflict) != 0 && lane == 0) {
@@ -1860,40 +1904,6 @@ __global__ __launch_bounds__(kBlock) void k_agg_zero_rows(
 }
 
 // ------------------------------------------------------- exact group ids
-// General path, deepest-marker keys: a record whose path at a requested
-// marker level differs from that of its key's owner (the group's first
-// record) shares that marker with a record of another path -- markers not
-// nested.  Sets PATH_CONFLICT and *flag; the host then groups by the whole
-// path instead.
-__global__ __launch_bounds__(kBlock) void k_agg_conflict(RecSrc S,
-                                                         uint32_t act,
-                                                         uint32_t** own,
-                                                         uint32_t* flag,
-                                                         uint32_t* status) {
-  const int64_t pos = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  bool conflict = false;
-  if (pos < S.n) {
-    RecItem it;
-    load_item(S, pos, it);
-    if (it.ok) {
-      for (int li = 0; li < S.D; ++li) {
-        if (!((act >> li) & 1u)) continue;
-        const uint32_t key = group_key(it.p, S.D, S.M, li, it.g, it.kind);
-        if (key == kNone) continue;
-        const uint32_t o = own[li][key];
-        if (o == kNone || (int64_t)o >= S.n) continue;
-        const uint32_t ro = S.korder[o];
-        for (int l = 0; l <= li; ++l)
-          if (S.idx[(int64_t)l * S.n + ro] != it.p[l]) conflict = true;
-      }
-    }
-  }
-  if (__ballot(conflict) != 0 && lane_id() == 0) {
-    atomicOr(flag, 1u);
-    atomicOr(status, (uint32_t)CHOPPER_ST_PATH_CONFLICT);
-  }
-}
-
 // Exact group ids, level by level from the outermost: the key of korder
 // position p at marker level l is (its group id at level l - 1, or
 // gpu * 2 + kind at l = 0) * (M + 2) + (its level-l marker, M + 1 for
@@ -2025,6 +2035,8 @@ struct AggLayout {
   uint32_t* xtot;
   uint32_t* xscan;        // scan temporaries over n items
   ClassSortLayout xsort;
+  uint32_t* ipath;        // [D][n] general-path items by korder position
+  uint16_t* igk;          // [n]
 };
 
 static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
@@ -2086,6 +2098,8 @@ static AggLayout agg_layout(Scratch& sc, int64_t n, int D, int64_t M,
   L.xtot = sc.take<uint32_t>(1);
   L.xscan = sc.take<uint32_t>(scan_scratch_elems(n));
   L.xsort = class_sort_layout(sc, n, 256);
+  L.ipath = sc.take<uint32_t>((int64_t)(D > 0 ? D : 1) * n);
+  L.igk = sc.take<uint16_t>(n);
   return L;
 }
 
@@ -2380,6 +2394,8 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
   S.mlabel = mk ? mk->label : nullptr;
   memset(&S.f, 0, sizeof(S.f));
   S.gk = nullptr;
+  S.ipath = nullptr;
+  S.igk = nullptr;
   if (filter) {
     for (int q = 0; q < 4; ++q) S.f.gpu_mask[q] = filter->gpu_mask[q];
     S.f.class_mask = filter->class_mask;
@@ -2436,32 +2452,13 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
                      act));
   const uint32_t atomic_levels = (1u << D) | (1u << (D + 1));
   if (n > 0) {
+    // the items once, in korder order, for the passes below
+    CHOPPER_HIP(launch("agg_items", k_agg_items, grid_for(n, kBlock),
+                       dim3(kBlock), s, S, L.ipath, L.igk));
+    S.ipath = L.ipath;
+    S.igk = L.igk;
     CHOPPER_HIP(launch("agg_elect", k_agg_elect, dim3((unsigned)T),
                        dim3(kBlock), s, S, act, L.own_tab));
-    // markers not nested (a record's path differs from its key owner's):
-    // group by the whole path, with exact group ids
-    int lmax = -1;
-    for (int li = 0; li < D; ++li)
-      if ((act >> li) & 1u) lmax = li;
-    if (lmax >= 0) {
-      CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
-                         L.xflag, 1));
-      CHOPPER_HIP(launch("agg_conflict", k_agg_conflict, grid_for(n, kBlock),
-                         dim3(kBlock), s, S, act, L.own_tab, L.xflag,
-                         status));
-      uint32_t conflict = 0;
-      CHOPPER_HIP(read_back(L.xflag, &conflict, sizeof(uint32_t), s));
-      if (conflict) {
-        rc = exact_group_ids(L, S, lmax, s);
-        if (rc != CHOPPER_OK) return rc;
-        S.gk = L.gk;
-        CHOPPER_HIP(launch("agg_fill_owner", k_fill_u32_many, dim3(fx, Lv),
-                           dim3(kBlock), s, L.own_tab,
-                           (const int64_t*)L.ks_dev, Lv, act));
-        CHOPPER_HIP(launch("agg_elect", k_agg_elect, dim3((unsigned)T),
-                           dim3(kBlock), s, S, act, L.own_tab));
-      }
-    }
     CHOPPER_HIP(launch("agg_count", k_agg_count, dim3((unsigned)T),
                        dim3(kBlock), s, S, act, L.own_tab, T, L.tilecnt));
   }
@@ -2476,6 +2473,8 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
                      L.rowof_tab, T, (const uint32_t*)L.tilebase, R));
   CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
                      L.ovf_count, 2));
+  CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
+                     L.xflag, 1));
 
   // order of work: finest marker level from records, coarser marker levels
   // from the rows below, GPU rows from level-0 rows, workload from GPU rows
@@ -2495,7 +2494,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
                          dim3((unsigned)T), dim3(kBlock), s, src, li, D, M,
                          atomic_mode, (const uint32_t*)L.own[li],
                          (const uint32_t*)L.rowof[li], R, ovf, nfields,
-                         status));
+                         status, L.xflag));
     } else {
       FromRows src{R, M, rows->level_offset, finer, S.gk, n};
       // rows of the finer level never outnumber the records
@@ -2503,7 +2502,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
                          dim3((unsigned)T), dim3(kBlock), s, src, li, D, M,
                          atomic_mode, (const uint32_t*)L.own[li],
                          (const uint32_t*)L.rowof[li], R, ovf, nfields,
-                         status));
+                         status, L.xflag));
     }
     if (!atomic_mode)
       CHOPPER_HIP(launch("agg_apply_overflow", k_agg_apply_overflow,
@@ -2535,6 +2534,42 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
     const int li = order_levels[q];
     rc = run_level(li, (atomic_levels >> li) & 1u);
     if (rc != CHOPPER_OK) return rc;
+  }
+  // markers not nested (a record's path differed from its row's): group by
+  // the whole path, with exact group ids, and run the levels again
+  uint32_t conflict = 0;
+  CHOPPER_HIP(read_back(L.xflag, &conflict, sizeof(uint32_t), s));
+  int lmax = -1;
+  for (int li = 0; li < D; ++li)
+    if ((act >> li) & 1u) lmax = li;
+  if (conflict && lmax >= 0 && S.gk == nullptr) {
+    rc = exact_group_ids(L, S, lmax, s);
+    if (rc != CHOPPER_OK) return rc;
+    S.gk = L.gk;
+    CHOPPER_HIP(launch("agg_fill_owner", k_fill_u32_many, dim3(fx, Lv),
+                       dim3(kBlock), s, L.own_tab, (const int64_t*)L.ks_dev,
+                       Lv, act));
+    CHOPPER_HIP(launch("agg_elect", k_agg_elect, dim3((unsigned)T),
+                       dim3(kBlock), s, S, act, L.own_tab));
+    CHOPPER_HIP(launch("agg_count", k_agg_count, dim3((unsigned)T),
+                       dim3(kBlock), s, S, act, L.own_tab, T, L.tilecnt));
+    CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilecnt, L.tilebase,
+                                         (int64_t)Lv * T, L.scantmp, L.total,
+                                         s));
+    CHOPPER_HIP(launch("agg_offsets", k_agg_offsets, dim3(1), dim3(64), s, Lv,
+                       T, (const uint32_t*)L.tilebase,
+                       (const uint32_t*)L.total, rows->cap,
+                       rows->level_offset, status));
+    CHOPPER_HIP(launch("agg_assign", k_agg_assign, dim3((unsigned)T),
+                       dim3(kBlock), s, S, act, atomic_levels, L.own_tab,
+                       L.rowof_tab, T, (const uint32_t*)L.tilebase, R));
+    CHOPPER_HIP(launch("agg_zero", k_zero_u32, dim3(1), dim3(64), s,
+                       L.ovf_count, 2));
+    for (int q = 0; q < nl; ++q) {
+      const int li = order_levels[q];
+      rc = run_level(li, (atomic_levels >> li) & 1u);
+      if (rc != CHOPPER_OK) return rc;
+    }
   }
   // an overflow list that did not fit: redo the marker levels with atomics
   uint32_t lost = 0;

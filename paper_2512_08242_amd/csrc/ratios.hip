@@ -30,8 +30,8 @@ static const char* const kKernelNames[] = {
     "agg_heads_rows", "agg_fast_reduce_records", "agg_fast_reduce_rows",
     "agg_workload_from_gpu", "bi_params", "bi_clear", "bi_fill",
     "bi_fixup", "ov_comm_records", "agg_nat_init", "agg_nat_pre",
-    "agg_nat_tiles", "agg_heads_nat", "agg_gpu_rows", "agg_conflict",
-    "agg_exact_keys", "join_resort", "attr_windows",
+    "agg_nat_tiles", "agg_heads_nat", "agg_gpu_rows",
+    "agg_exact_keys", "join_resort", "attr_windows", "agg_items",
     "view_flags", "view_units", "view_fill", "view_records", "view_rows",
     "view_iter_max", "view_medians", "launch_split", "join_fill",
     "join_labels", "join_heads", "join_runs", "join_order", "join_pass_prep",

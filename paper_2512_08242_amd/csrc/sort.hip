@@ -15,6 +15,7 @@
 // reordered in LDS so that the global writes of one digit bucket are
 // contiguous.
 #include "sort.h"
+#include "wave.h"
 
 namespace chopper {
 
@@ -195,32 +196,33 @@ __global__ __launch_bounds__(kBlock) void k_class_partition(
   }
 }
 
+// (both checks stop reading once some wave has found the answer)
 template <typename Acc>
 __global__ __launch_bounds__(kBlock) void k_class_verify(Acc acc, int64_t n,
                                                          const uint32_t* perm,
                                                          uint32_t* unsorted) {
+  if (__builtin_amdgcn_readfirstlane((int)flag_read(unsorted)) != 0) return;
   int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   bool bad = false;
   if (p + 1 < n) {
     uint32_t a = perm[p], b = perm[p + 1];
     bad = acc.cls(a) == acc.cls(b) && acc.time(b) < acc.time(a);
   }
-  if (__ballot(bad) != 0 && (threadIdx.x & (kWave - 1)) == 0)
-    atomicOr(unsorted, 1u);
+  wave_flag_or(unsorted, bad, 1u);
 }
 
 // is the input ordered by (major, time)?
 template <typename Acc>
 __global__ __launch_bounds__(kBlock) void k_major_sorted(Acc acc, int64_t n,
                                                          uint32_t* unsorted) {
+  if (__builtin_amdgcn_readfirstlane((int)flag_read(unsorted)) != 0) return;
   int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   bool bad = false;
   if (p + 1 < n) {
     const uint32_t a = acc.major(p), b = acc.major(p + 1);
     bad = a > b || (a == b && acc.time(p + 1) < acc.time(p));
   }
-  if (__ballot(bad) != 0 && (threadIdx.x & (kWave - 1)) == 0)
-    atomicOr(unsorted, 1u);
+  wave_flag_or(unsorted, bad, 1u);
 }
 
 // ---------------------------------------------------------------------------

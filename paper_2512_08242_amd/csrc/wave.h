@@ -44,6 +44,20 @@ __device__ inline void wave_sync() {
 
 __device__ inline int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
 
+// Relaxed device-scope read of a flag word that other waves of the running
+// kernel may set (it bypasses the non-coherent vector L1).
+__device__ inline uint32_t flag_read(const uint32_t* f) {
+  return __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// OR `bits` into *f when some lane of the wave has `cond`: one atomic per
+// wave, and none once the bits are set (a word that most waves set would
+// otherwise serialize them all on one address).
+__device__ inline void wave_flag_or(uint32_t* f, bool cond, uint32_t bits) {
+  if (__ballot(cond) != 0 && lane_id() == 0 && (flag_read(f) & bits) != bits)
+    atomicOr(f, bits);
+}
+
 // number of set bits of m in lanes below this one
 __device__ inline uint32_t lanes_below(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
