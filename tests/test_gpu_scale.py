@@ -3,8 +3,9 @@ adversarial trace), in the launch configuration bench.py times.
 
 Clocks, alignment, attribution, overlap and bubbles are compared with the C
 oracle over every record and marker; the two orders with numpy's stable
-lexsort; the aggregated rows of every level with the vectorized brute-force
-grouping of tests/brute.py (pinned to the oracle on CPU); the derived ratios
+lexsort; the aggregated rows of every level with the oracle's own grouping
+on the 20M-record trace and with the vectorized brute-force grouping of
+tests/brute.py (pinned to the oracle on CPU) on the 50M-record one; the derived ratios
 by recomputing the same IEEE divisions in numpy; the views, the overlap
 statistics, the launch split and (on the 20M-record trace) the counter-pass
 join with the oracle.  One module-scoped run per trace feeds short tests, so
@@ -93,9 +94,25 @@ class Full:
                               tr.m_gpu, a["ms"], a["me"], tr.n_gpus)
 
     def _rows(self):
+        """Rows of every level: the oracle's own aggregation on the 20M-record
+        trace; on the 50M-record shuffled trace (where the oracle's
+        sort-based grouping takes minutes) the vectorized grouping of
+        tests/brute.py, pinned to the oracle on CPU."""
         tr, a = self.tr, self.need("aligned")
         idx, ov = self.need("idx")[0], self.need("ov")
         levels = list(range(tr.depth)) + [100, 101]
+        if self.cid == 3:
+            r = oracle.aggregate(tr.gpu, tr.cls, a["s"], a["e"], idx,
+                                 ov["gap"], ov["ovl"], tr.counters, tr.depth)
+            lo, out = r["level_offset"], {}
+            for li, lev in enumerate(levels):
+                sl = slice(int(lo[li]), int(lo[li + 1]))
+                out[lev] = {k: r[k][sl] for k in ("gpu", "kind", "n", "dur",
+                                                  "gap", "ovl", "tmin",
+                                                  "tmax", "first")}
+                out[lev]["path"] = r["path"][:, sl]
+                out[lev]["ctr"] = r["ctr"][:, sl]
+            return levels, out
         return levels, brute.aggregate_numpy(
             tr.gpu, tr.cls, a["s"], a["e"], idx, ov["gap"], ov["ovl"],
             tr.counters, tr.depth, levels)
