@@ -510,38 +510,74 @@ struct CdfArgs {
   int NG;
 };
 
+// Counts and smallest durations of the CDF groups: a block takes kCdfSpan
+// row slots (rows of one gpu are consecutive, so nearly all of a block's
+// instances are on its first row's gpu) and adds those per (phase,
+// operation) in LDS, with one global atomic per group and block; instances
+// of other gpus go to the global tables directly.
+constexpr int kCdfIpt = 8;
+constexpr int kCdfSpan = kBlock * kCdfIpt;
+
 __global__ __launch_bounds__(kBlock) void k_cdf_keys(CdfArgs C,
                                                      uint64_t sentinel,
                                                      uint64_t* key,
                                                      uint32_t* val,
                                                      uint32_t* gcnt,
                                                      uint64_t* ymin) {
+  __shared__ uint32_t s_cnt[kMaxGroups];
+  __shared__ unsigned long long s_min[kMaxGroups];
   const StatArgs& A = C.A;
-  const int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (r >= A.cap) return;
+  const int G = A.P * A.O;
+  for (int g = threadIdx.x; g < G; g += kBlock) {
+    s_cnt[g] = 0;
+    s_min[g] = ~0ull;
+  }
   int64_t lo, hi;
   level_range(A, lo, hi);
-  uint64_t k = sentinel;
-  if (r >= lo && r < hi && A.kind[r] == 0 && A.dur[r] > 0) {
-    const uint32_t mp = A.path[(int64_t)A.lv_phase * A.cap + r];
-    const uint32_t mo = A.path[(int64_t)A.lv_op * A.cap + r];
-    const uint32_t h = C.gpu[r];
-    if ((int64_t)mp < A.nm && (int64_t)mo < A.nm && (int)h < C.NG) {
-      const uint32_t p = A.label[mp], o = A.label[mo];
-      if (p < (uint32_t)A.P && o < (uint32_t)A.O) {
-        const uint64_t c = (uint64_t)(p * (uint32_t)A.O + o) * C.NG + h;
-        const uint64_t d = (uint64_t)A.dur[r];
-        uint64_t x = ((uint64_t)A.ovl[r] << 30) / d;
-        if (x > 0x7FFFFFFFull) x = 0x7FFFFFFFull;   // (RANGE, set elsewhere)
-        k = c << 31 | x;
-        atomicAdd(&gcnt[c], 1u);
-        atomicMin((unsigned long long*)&ymin[c],
-                  (unsigned long long)(d + (uint64_t)A.gap[r]));
+  const int64_t b0 = (int64_t)blockIdx.x * kCdfSpan;
+  const int64_t f = b0 > lo ? b0 : lo;     // the block's first row in range
+  const uint32_t h0 = f < hi ? (uint32_t)C.gpu[f] : 0xFFFFFFFFu;
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < kCdfIpt; ++q) {
+    const int64_t r = b0 + (int64_t)q * kBlock + threadIdx.x;
+    if (r >= A.cap) break;
+    uint64_t k = sentinel;
+    if (r >= lo && r < hi && A.kind[r] == 0 && A.dur[r] > 0) {
+      const uint32_t mp = A.path[(int64_t)A.lv_phase * A.cap + r];
+      const uint32_t mo = A.path[(int64_t)A.lv_op * A.cap + r];
+      const uint32_t h = C.gpu[r];
+      if ((int64_t)mp < A.nm && (int64_t)mo < A.nm && (int)h < C.NG) {
+        const uint32_t p = A.label[mp], o = A.label[mo];
+        if (p < (uint32_t)A.P && o < (uint32_t)A.O) {
+          const uint32_t g = p * (uint32_t)A.O + o;
+          const uint64_t c = (uint64_t)g * C.NG + h;
+          const uint64_t d = (uint64_t)A.dur[r];
+          uint64_t x = ((uint64_t)A.ovl[r] << 30) / d;
+          if (x > 0x7FFFFFFFull) x = 0x7FFFFFFFull;   // (RANGE, set elsewhere)
+          k = c << 31 | x;
+          const uint64_t y = d + (uint64_t)A.gap[r];
+          if (h == h0) {
+            atomicAdd(&s_cnt[g], 1u);
+            atomicMin(&s_min[g], (unsigned long long)y);
+          } else {
+            atomicAdd(&gcnt[c], 1u);
+            atomicMin((unsigned long long*)&ymin[c], (unsigned long long)y);
+          }
+        }
       }
     }
+    key[r] = k;
+    val[r] = (uint32_t)r;
   }
-  key[r] = k;
-  val[r] = (uint32_t)r;
+  __syncthreads();
+  if (h0 == 0xFFFFFFFFu || (int)h0 >= C.NG) return;
+  for (int g = threadIdx.x; g < G; g += kBlock)
+    if (s_cnt[g]) {
+      const int64_t c = (int64_t)g * C.NG + h0;
+      atomicAdd(&gcnt[c], s_cnt[g]);
+      atomicMin((unsigned long long*)&ymin[c], s_min[g]);
+    }
 }
 
 // one thread per CDF group: quantiles of x, y_min, D_0%, D_50% and their
@@ -729,7 +765,8 @@ extern "C" int chopper_op_stats(const chopper_rows* rows, int32_t depth,
   CHOPPER_HIP(launch("stats_cdf", k_stats_clear_cdf, grid_for(NGG, kBlock),
                      dim3(kBlock), s, NGG, B.ccnt, B.ymin));
   if (cap > 0) {
-    CHOPPER_HIP(launch("stats_cdf", k_cdf_keys, grid_for(cap, kBlock),
+    CHOPPER_HIP(launch("stats_cdf", k_cdf_keys,
+                       dim3((unsigned)ceil_div(cap, (int64_t)kCdfSpan)),
                        dim3(kBlock), s, C, sentinel, B.sort.key0, B.sort.val0,
                        B.ccnt, B.ymin));
     ClassSortLayout L = B.sort;
