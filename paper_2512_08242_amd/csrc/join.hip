@@ -14,6 +14,8 @@
 // (gpu, stream, label), which keeps each label's time order, and cut into
 // runs again.  Record runs find their pass run by a binary search over the
 // pass's run table; each record then reads entry run start + ordinal.
+// Records far from their sorted order are gathered in sorted order through
+// a row-major stage instead (one more pass, no scattered column reads).
 // JOIN_ORDER (a warning) marks labels that decrease along a (gpu, stream).
 #include <algorithm>
 #include <vector>
@@ -459,6 +461,31 @@ struct JoinPasses {
   PassView p[kMaxPasses];
 };
 
+// the entry of every pass for a record of run `run` (kNone: the record has
+// no iteration) at ordinal `ord`, with run key (kc, kl) and kernel class kk:
+// q[p] = entry index, or -1 when none matches.  All entries are found
+// before any value is read, so that the passes' dependent loads overlap.
+__device__ inline void join_entries(const JoinPasses& J, uint32_t run,
+                                    uint32_t ord, uint32_t kc, uint32_t kl,
+                                    uint32_t kk, int64_t (&q)[kMaxPasses]) {
+#pragma unroll
+  for (int p = 0; p < kMaxPasses; ++p) {
+    q[p] = -1;
+    if (p >= J.np || run == kNone) continue;
+    const PassView& P = J.p[p];
+    const uint2 qr = P.match[run];
+    const int64_t pos = (int64_t)qr.x + ord;
+    // the entry at the ordinal is the record's only if it still has the
+    // run's key (entries without an iteration may follow the run)
+    if (pos < (int64_t)qr.y) {
+      const uint64_t k = P.qkey[pos];
+      if ((uint32_t)k == kl && ((uint32_t)(k >> 32) & 0xFFFFu) == kc &&
+          (uint32_t)(k >> 48) == kk)
+        q[p] = P.qorder[pos];
+    }
+  }
+}
+
 // every record, in input order, against every pass: its entry (run start +
 // ordinal), the key and class check, and the pass's columns (0 where
 // nothing matches); the matched bits are written once
@@ -477,25 +504,8 @@ __global__ __launch_bounds__(kBlock) void k_join_gather(
       kl = rlab[run];
       kk = cls[r];
     }
-    // the entry of every pass first (loads only, so that the passes'
-    // dependent chains overlap), then the values and the stores
     int64_t q[kMaxPasses];
-#pragma unroll
-    for (int p = 0; p < kMaxPasses; ++p) {
-      q[p] = -1;
-      if (p >= J.np || run == kNone) continue;
-      const PassView& P = J.p[p];
-      const uint2 qr = P.match[run];
-      const int64_t pos = (int64_t)qr.x + ord;
-      // the entry at the ordinal is the record's only if it still has the
-      // run's key (entries without an iteration may follow the run)
-      if (pos < (int64_t)qr.y) {
-        const uint64_t k = P.qkey[pos];
-        if ((uint32_t)k == kl && ((uint32_t)(k >> 32) & 0xFFFFu) == kc &&
-            (uint32_t)(k >> 48) == kk)
-          q[p] = P.qorder[pos];
-      }
-    }
+    join_entries(J, run, ord, kc, kl, kk, q);
     uint32_t bits = 0;
 #pragma unroll
     for (int p = 0; p < kMaxPasses; ++p) {
@@ -511,6 +521,121 @@ __global__ __launch_bounds__(kBlock) void k_join_gather(
   }
   if (__ballot(miss) != 0 && lane_id() == 0)
     atomicOr(status, CHOPPER_ST_JOIN_MISS);
+}
+
+// Records far from their sorted order (e.g. a shuffled trace): the input
+// order gather would read every run table and pass column at random.
+// Instead the records are taken in their sorted sequence -- run, ordinal
+// and the pass entries then advance together -- and each record's values
+// go to a row of a row-major stage; a second pass copies every record's
+// row (whole cache lines) to the counter columns in input order.
+//
+// Sampled locality of a sequence: bit `bit` of *flag when, in some sampled
+// block of kBlock consecutive positions, more than a quarter of the steps
+// jump by more than kNearJump.
+constexpr int64_t kNearJump = 4096;
+constexpr int kLocalityBlocks = 512;
+__global__ __launch_bounds__(kBlock) void k_join_locality(const uint32_t* seq,
+                                                          int64_t n,
+                                                          int64_t step,
+                                                          uint32_t* flag,
+                                                          uint32_t bit) {
+  const int64_t i = (int64_t)blockIdx.x * step + threadIdx.x;
+  bool far = false;
+  if (i + 1 < n) {
+    const int64_t d = (int64_t)seq[i + 1] - (int64_t)seq[i];
+    far = d > kNearJump || d < -kNearJump;
+  }
+  const int c = __syncthreads_count(far ? 1 : 0);
+  if (threadIdx.x == 0 && c > kBlock / 4) atomicOr(flag, bit);
+}
+
+// position of every record in the sorted sequence
+__global__ void k_join_rec_inv(int64_t n, const uint32_t* seq, uint32_t* pinv) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p < n) pinv[seq[p]] = (uint32_t)p;
+}
+
+// the gather in sorted order: position p's run and ordinal come from the
+// run table (run = heads up to p, ordinal = p - run start); its W values
+// go to stage row p.  The block's rows are consecutive in the stage: they
+// are put together in LDS and stored as one contiguous block.
+__global__ __launch_bounds__(kBlock) void k_join_gather_sorted(
+    int64_t n, const uint32_t* seq, const uint32_t* head, const uint32_t* excl,
+    const uint64_t* key, const uint32_t* rstart, const uint8_t* cls,
+    const uint32_t* rcls, const uint32_t* rlab, JoinPasses J, int W,
+    uint64_t* stage, uint8_t* smatched, uint32_t* status) {
+  __shared__ uint64_t s_rows[kBlock * 16];
+  const int64_t p0 = (int64_t)blockIdx.x * kBlock;
+  const int64_t p = p0 + threadIdx.x;
+  bool miss = false;
+  if (p < n) {
+    uint32_t run = kNone, ord = 0, kc = 0, kl = 0, kk = 0;
+    if ((uint32_t)key[p] != kNone) {
+      run = excl[p] + head[p] - 1;
+      ord = (uint32_t)p - rstart[run];
+      kc = rcls[run];
+      kl = rlab[run];
+      kk = cls[seq[p]];
+    }
+    int64_t q[kMaxPasses];
+    join_entries(J, run, ord, kc, kl, kk, q);
+    uint64_t* row = s_rows + threadIdx.x * W;
+    uint32_t bits = 0;
+    int k = 0;
+#pragma unroll
+    for (int z = 0; z < kMaxPasses; ++z) {
+      if (z >= J.np) break;
+      const PassView& P = J.p[z];
+      if (run != kNone && q[z] < 0) miss = true;
+      for (int c = 0; c < P.n_cols; ++c)
+        row[k++] = q[z] >= 0 ? P.values[(int64_t)c * P.m + q[z]] : 0ull;
+      if (q[z] >= 0) bits |= 1u << z;
+    }
+    smatched[p] = (uint8_t)bits;
+  }
+  __syncthreads();
+  const int64_t rows = n - p0 < kBlock ? n - p0 : kBlock;
+  const int64_t tot = rows * W;
+  uint64_t* dst = stage + p0 * (int64_t)W;
+  for (int64_t i = threadIdx.x; i < tot; i += kBlock) dst[i] = s_rows[i];
+  if (__ballot(miss) != 0 && lane_id() == 0)
+    atomicOr(status, CHOPPER_ST_JOIN_MISS);
+}
+
+struct StageCols {
+  int32_t W;
+  int32_t dst[16];    // counter column of stage column k
+};
+
+// stage rows back to the records: record r reads row pinv[r]
+__global__ __launch_bounds__(kBlock) void k_join_unstage(
+    int64_t n, const uint32_t* pinv, const uint64_t* stage,
+    const uint8_t* smatched, StageCols S, uint64_t* counters,
+    uint8_t* matched) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= n) return;
+  const int64_t p = pinv[r];
+  const uint64_t* row = stage + p * (int64_t)S.W;
+  uint64_t v[16];
+  if ((S.W & 1) == 0) {
+    // rows of an even width are 16-byte aligned (the stage is 256-aligned)
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (2 * k < S.W) {
+        const uint4 x = reinterpret_cast<const uint4*>(row)[k];
+        v[2 * k] = (uint64_t)x.x | (uint64_t)x.y << 32;
+        v[2 * k + 1] = (uint64_t)x.z | (uint64_t)x.w << 32;
+      }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      if (k < S.W) v[k] = row[k];
+  }
+#pragma unroll
+  for (int k = 0; k < 16; ++k)
+    if (k < S.W) counters[(int64_t)S.dst[k] * n + r] = v[k];
+  matched[r] = smatched[p];
 }
 
 }  // namespace
@@ -532,6 +657,7 @@ extern "C" int chopper_join_counters(
   if (nm > 0 && !mk->label) return CHOPPER_EINVAL;
   int64_t mmax = 0;
   uint32_t used = 0;
+  int W = 0;   // stage width: the columns of all passes
   for (int p = 0; p < n_passes; ++p) {
     const chopper_counter_pass& P = passes[p];
     if (P.n < 0 || P.n >= (int64_t)0xFFFFFFFF || P.n_cols < 1 ||
@@ -545,6 +671,7 @@ extern "C" int chopper_join_counters(
       used |= 1u << P.dst[c];
     }
     mmax = P.n > mmax ? P.n : mmax;
+    W += P.n_cols;
   }
   // scratch: record labels, runs and keys, the class map, per-pass
   // temporaries (reused) and what the gather reads of every pass
@@ -557,8 +684,8 @@ extern "C" int chopper_join_counters(
   struct Bufs {
     uint32_t *rlabv, *head, *excl, *rstart, *rcls, *rlab, *tot, *tmp;
     uint32_t *qhead, *tcnt, *tpre, *rrun, *rord, *perm, *seq2, *scoff, *flag;
-    uint64_t* rkey;
-    uint8_t* pres;
+    uint64_t *rkey, *stage;
+    uint8_t *pres, *smatched;
     uint16_t* cmap;
     PassBuf pb[kMaxPasses];
   } B;
@@ -585,6 +712,9 @@ extern "C" int chopper_join_counters(
     B.seq2 = sc.take<uint32_t>(nmax);
     B.scoff = sc.take<uint32_t>(256 + 1);
     B.flag = sc.take<uint32_t>(1);
+    // sorted-order gather of records far from their sorted order
+    B.stage = sc.take<uint64_t>(n * (int64_t)W);
+    B.smatched = sc.take<uint8_t>(n);
     for (int p = 0; p < n_passes; ++p) {
       const int64_t m = passes[p].n;
       B.pb[p].match = sc.take<uint2>(n + 1);
@@ -635,6 +765,15 @@ extern "C" int chopper_join_counters(
                      n, idx + (int64_t)iter_level * n, nm, mk->label,
                      B.rlabv));
   CHOPPER_HIP(launch("join_fill", k_join_zero, dim3(1), dim3(1), s, B.flag));
+  // records far from their sorted order (bit 31, read back with the
+  // re-sort bits)
+  {
+    const int64_t nb = std::min<int64_t>(ceil_div(n, (int64_t)kBlock),
+                                         kLocalityBlocks);
+    CHOPPER_HIP(launch("join_locality", k_join_locality, dim3((unsigned)nb),
+                       dim3(kBlock), s, order, n, n / nb, B.flag,
+                       1u << 31));
+  }
   const dim3 gr(std::min<unsigned>(gn.x, 1024u));
   const dim3 gw((unsigned)ceil_div((int64_t)gn.x, (int64_t)kWavesPerBlock));
   // run table of the records along `seq`; the check only on the first cut
@@ -732,11 +871,26 @@ extern "C" int chopper_join_counters(
     rc = record_runs(rseq, false);
     if (rc != CHOPPER_OK) return rc;
   }
-  CHOPPER_HIP(launch("join_runs", k_join_rec_pos, gn, dim3(kBlock), s, n,
-                     rseq, (const uint32_t*)B.head, (const uint32_t*)B.excl,
-                     (const uint64_t*)B.rkey, (const uint32_t*)B.rstart,
-                     B.rrun, B.rord));
-  // (the records' re-sorted sequence is no longer needed: seq2 is reused)
+  const bool scattered = (resort >> 31) & 1u;
+  if (!scattered) {
+    CHOPPER_HIP(launch("join_runs", k_join_rec_pos, gn, dim3(kBlock), s, n,
+                       rseq, (const uint32_t*)B.head, (const uint32_t*)B.excl,
+                       (const uint64_t*)B.rkey, (const uint32_t*)B.rstart,
+                       B.rrun, B.rord));
+  } else {
+    // sorted-order gather: every record's sorted position (in rrun), and
+    // the sequence kept in rord when it is the re-sorted one (seq2 is
+    // reused by the passes' re-sorts below)
+    CHOPPER_HIP(launch("join_runs", k_join_rec_inv, gn, dim3(kBlock), s, n,
+                       rseq, B.rrun));
+    if (rseq == B.seq2) {
+      CHOPPER_HIP(hipMemcpyAsync(B.rord, B.seq2, sizeof(uint32_t) * n,
+                                 hipMemcpyDeviceToDevice, s));
+      rseq = B.rord;
+    }
+  }
+  // (in input-order mode the records' re-sorted sequence is no longer
+  // needed: seq2 is reused)
   JoinPasses J;
   J.np = n_passes;
   for (int p = 0; p < n_passes; ++p) {
@@ -765,11 +919,32 @@ extern "C" int chopper_join_counters(
     V.n_cols = P.n_cols;
     for (int c = 0; c < 16; ++c) V.dst[c] = c < P.n_cols ? P.dst[c] : 0;
   }
-  CHOPPER_HIP(launch("join_gather", k_join_gather, gn, dim3(kBlock), s, n,
-                     (const uint32_t*)B.rrun, (const uint32_t*)B.rord,
-                     rec->cls, (const uint32_t*)B.rcls,
-                     (const uint32_t*)B.rlab, J, counters_out, matched_out,
-                     status));
+  if (!scattered) {
+    CHOPPER_HIP(launch("join_gather", k_join_gather, gn, dim3(kBlock), s, n,
+                       (const uint32_t*)B.rrun, (const uint32_t*)B.rord,
+                       rec->cls, (const uint32_t*)B.rcls,
+                       (const uint32_t*)B.rlab, J, counters_out, matched_out,
+                       status));
+    return CHOPPER_OK;
+  }
+  CHOPPER_HIP(launch("join_gather", k_join_gather_sorted, gn, dim3(kBlock), s,
+                     n, rseq, (const uint32_t*)B.head,
+                     (const uint32_t*)B.excl, (const uint64_t*)B.rkey,
+                     (const uint32_t*)B.rstart, rec->cls,
+                     (const uint32_t*)B.rcls, (const uint32_t*)B.rlab, J, W,
+                     B.stage, B.smatched, status));
+  StageCols SC;
+  SC.W = W;
+  {
+    int k = 0;
+    for (int p = 0; p < n_passes; ++p)
+      for (int c = 0; c < passes[p].n_cols; ++c) SC.dst[k++] = passes[p].dst[c];
+    for (; k < 16; ++k) SC.dst[k] = 0;
+  }
+  CHOPPER_HIP(launch("join_gather", k_join_unstage, gn, dim3(kBlock), s, n,
+                     (const uint32_t*)B.rrun, (const uint64_t*)B.stage,
+                     (const uint8_t*)B.smatched, SC, counters_out,
+                     matched_out));
   return CHOPPER_OK;
 }
 

@@ -6,6 +6,47 @@
 
 namespace chopper {
 
+// Eight consecutive items i0 .. i0 + 7 of a column (b[j] = 0 past n), as one
+// 8-byte load when the run is whole and aligned.
+__device__ inline void load8_u8(const uint8_t* p, int64_t i0, int64_t n,
+                                uint32_t (&b)[8]) {
+  if (i0 + 8 <= n && ((uintptr_t)(p + i0) & 7) == 0) {
+    const uint64_t w = *reinterpret_cast<const uint64_t*>(p + i0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) b[j] = (uint32_t)(w >> (8 * j)) & 0xFFu;
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) b[j] = i0 + j < n ? (uint32_t)p[i0 + j] : 0u;
+  }
+}
+
+__device__ inline void load8_i64(const int64_t* p, int64_t i0, int64_t n,
+                                 int64_t (&x)[8]) {
+  if (i0 + 8 <= n && ((uintptr_t)(p + i0) & 15) == 0) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint4 v = reinterpret_cast<const uint4*>(p + i0)[k];
+      x[2 * k] = (int64_t)((uint64_t)v.x | (uint64_t)v.y << 32);
+      x[2 * k + 1] = (int64_t)((uint64_t)v.z | (uint64_t)v.w << 32);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = i0 + j < n ? p[i0 + j] : 0;
+  }
+}
+
+// Class ids of the eight items i0 .. i0 + 7 (v[j]: i0 + j < n); accessors
+// over plain columns override it with vector loads.
+template <typename Acc>
+__device__ inline void cls_block(const Acc& acc, int64_t i0, int64_t n,
+                                 uint32_t (&d)[8], bool (&v)[8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    v[j] = i0 + j < n;
+    d[j] = v[j] ? acc.cls(i0 + j) : 0u;
+  }
+}
+
 // Records keyed by (gpu, stream): dense class ids from a 256 x 256 table.
 struct KeyRecStream {
   const uint8_t* gpu;
@@ -19,7 +60,22 @@ struct KeyRecStream {
   __device__ int64_t time(int64_t i) const { return t[i]; }
   __device__ uint32_t major(int64_t i) const { return gpu[i]; }
   __host__ __device__ int nclass() const { return C; }
+  __device__ void cls8(int64_t i0, int64_t n, uint32_t (&d)[8],
+                       bool (&v)[8]) const {
+    uint32_t g[8], s[8];
+    load8_u8(gpu, i0, n, g);
+    load8_u8(stream, i0, n, s);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      v[j] = i0 + j < n;
+      d[j] = v[j] ? cmap[g[j] * 256u + s[j]] : 0u;
+    }
+  }
 };
+__device__ inline void cls_block(const KeyRecStream& a, int64_t i0, int64_t n,
+                                 uint32_t (&d)[8], bool (&v)[8]) {
+  a.cls8(i0, n, d, v);
+}
 
 // Records keyed by (gpu, kind): dense class ids from a 256 x 2 table.
 struct KeyRecKind {
@@ -34,7 +90,22 @@ struct KeyRecKind {
   __device__ int64_t time(int64_t i) const { return t[i]; }
   __device__ uint32_t major(int64_t i) const { return gpu[i]; }
   __host__ __device__ int nclass() const { return C; }
+  __device__ void cls8(int64_t i0, int64_t n, uint32_t (&d)[8],
+                       bool (&v)[8]) const {
+    uint32_t g[8], c[8];
+    load8_u8(gpu, i0, n, g);
+    load8_u8(cl, i0, n, c);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      v[j] = i0 + j < n;
+      d[j] = v[j] ? cmap[g[j] * 2u + (uint32_t)kind_of((uint8_t)c[j])] : 0u;
+    }
+  }
 };
+__device__ inline void cls_block(const KeyRecKind& a, int64_t i0, int64_t n,
+                                 uint32_t (&d)[8], bool (&v)[8]) {
+  a.cls8(i0, n, d, v);
+}
 
 // Markers keyed by (gpu, level, empty): non-empty markers of a (gpu, level)
 // come first; markers with an invalid gpu or level go to the last class.
@@ -52,7 +123,28 @@ struct KeyMarker {
   __device__ int64_t time(int64_t i) const { return ms[i]; }
   __device__ uint32_t major(int64_t i) const { return gpu[i]; }
   __host__ __device__ int nclass() const { return G * D * 2 + 1; }
+  __device__ void cls8(int64_t i0, int64_t n, uint32_t (&d)[8],
+                       bool (&v)[8]) const {
+    uint32_t g[8], l[8];
+    int64_t a[8], b[8];
+    load8_u8(gpu, i0, n, g);
+    load8_u8(level, i0, n, l);
+    load8_i64(ms, i0, n, a);
+    load8_i64(me, i0, n, b);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      v[j] = i0 + j < n;
+      const bool bad = (int)g[j] >= G || (int)l[j] >= D;
+      d[j] = !v[j] ? 0u
+             : bad ? (uint32_t)(G * D * 2)
+                   : (g[j] * (uint32_t)D + l[j]) * 2u + (b[j] <= a[j] ? 1u : 0u);
+    }
+  }
 };
+__device__ inline void cls_block(const KeyMarker& a, int64_t i0, int64_t n,
+                                 uint32_t (&d)[8], bool (&v)[8]) {
+  a.cls8(i0, n, d, v);
+}
 
 // Positions of a sequence (position p holds item seq[p]) keyed by (dense
 // class of the item's (gpu, stream), the item's label): their stable sort
@@ -72,7 +164,59 @@ struct KeySeqLabel {
   __device__ int64_t time(int64_t p) const { return (int64_t)lab[seq[p]]; }
   __device__ uint32_t major(int64_t p) const { return cls(p); }
   __host__ __device__ int nclass() const { return C; }
+  __device__ void cls8(int64_t p0, int64_t n, uint32_t (&d)[8],
+                       bool (&v)[8]) const {
+    uint32_t it[8];
+    if (p0 + 8 <= n && ((uintptr_t)(seq + p0) & 15) == 0) {
+      const uint4 x = reinterpret_cast<const uint4*>(seq + p0)[0];
+      const uint4 y = reinterpret_cast<const uint4*>(seq + p0)[1];
+      it[0] = x.x; it[1] = x.y; it[2] = x.z; it[3] = x.w;
+      it[4] = y.x; it[5] = y.y; it[6] = y.z; it[7] = y.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) it[j] = p0 + j < n ? seq[p0 + j] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      v[j] = p0 + j < n;
+      d[j] = v[j] ? cmap[(uint32_t)gpu[it[j]] * 256u + stream[it[j]]] : 0u;
+    }
+  }
 };
+__device__ inline void cls_block(const KeySeqLabel& a, int64_t i0, int64_t n,
+                                 uint32_t (&d)[8], bool (&v)[8]) {
+  a.cls8(i0, n, d, v);
+}
+
+// (major, time) of the nine items i0 .. i0 + 8 (v[j]: i0 + j < n)
+template <typename Acc>
+__device__ inline void major_time_block(const Acc& acc, int64_t i0, int64_t n,
+                                        uint32_t (&m)[9], int64_t (&t)[9],
+                                        bool (&v)[9]) {
+#pragma unroll
+  for (int j = 0; j < 9; ++j) {
+    v[j] = i0 + j < n;
+    m[j] = v[j] ? acc.major(i0 + j) : 0u;
+    t[j] = v[j] ? acc.time(i0 + j) : 0;
+  }
+}
+__device__ inline void major_time_block(const KeyMarker& a, int64_t i0,
+                                        int64_t n, uint32_t (&m)[9],
+                                        int64_t (&t)[9], bool (&v)[9]) {
+  uint32_t g[8];
+  int64_t x[8];
+  load8_u8(a.gpu, i0, n, g);
+  load8_i64(a.ms, i0, n, x);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    v[j] = i0 + j < n;
+    m[j] = g[j];
+    t[j] = x[j];
+  }
+  v[8] = i0 + 8 < n;
+  m[8] = v[8] ? a.gpu[i0 + 8] : 0u;
+  t[8] = v[8] ? a.ms[i0 + 8] : 0;
+}
 
 struct ClassSortLayout {
   int64_t n = 0;

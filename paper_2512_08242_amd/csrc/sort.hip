@@ -122,6 +122,31 @@ __host__ __device__ inline int class_bits(int c) {
 // ---------------------------------------------------------------------------
 // Class-partition fast path
 // ---------------------------------------------------------------------------
+// Class ids of the tile in the striped arrangement the ranking needs (item
+// j of thread t at position j * kBlock + t): loaded eight consecutive items
+// per lane and turned around through `s_tmp` (kSortTile bytes; class ids
+// are below 256).
+template <typename Acc>
+__device__ inline void striped_classes(const Acc& acc, int64_t base,
+                                       int64_t n, uint8_t* s_tmp,
+                                       uint32_t (&dig)[kSortIpt],
+                                       bool (&valid)[kSortIpt]) {
+  uint32_t d[kSortIpt];
+  bool v[kSortIpt];
+  cls_block(acc, base + (int64_t)threadIdx.x * kSortIpt, n, d, v);
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j)
+    s_tmp[threadIdx.x * kSortIpt + j] = (uint8_t)d[j];
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j) {
+    const int q = j * kBlock + (int)threadIdx.x;
+    valid[j] = base + q < n;
+    dig[j] = valid[j] ? (uint32_t)s_tmp[q] : 0u;
+  }
+  __syncthreads();
+}
+
 template <typename Acc>
 __global__ __launch_bounds__(kBlock) void k_class_hist(Acc acc, int64_t n,
                                                        int64_t ntiles,
@@ -133,14 +158,10 @@ __global__ __launch_bounds__(kBlock) void k_class_hist(Acc acc, int64_t n,
   const int lane = threadIdx.x & (kWave - 1);
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  // (counts need no order: eight consecutive items per lane, vector loads)
   uint32_t d[kSortIpt];
   bool v[kSortIpt];
-#pragma unroll
-  for (int j = 0; j < kSortIpt; ++j) {
-    const int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
-    v[j] = i < n;
-    d[j] = v[j] ? acc.cls(i) : 0u;
-  }
+  cls_block(acc, base + (int64_t)threadIdx.x * kSortIpt, n, d, v);
   // one LDS add per distinct class of every wave-row
 #pragma unroll
   for (int j = 0; j < kSortIpt; ++j) {
@@ -171,11 +192,7 @@ __global__ __launch_bounds__(kBlock) void k_class_partition(
   const int64_t base = (int64_t)blockIdx.x * kSortTile;
   uint32_t dig[kSortIpt], rank[kSortIpt];
   bool valid[kSortIpt];
-  for (int j = 0; j < kSortIpt; ++j) {
-    int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
-    valid[j] = i < n;
-    dig[j] = valid[j] ? acc.cls(i) : 0u;
-  }
+  striped_classes(acc, base, n, s_dig, dig, valid);
   tile_rank(dig, valid, rank, sh, class_bits(acc.nclass()));
   if ((int)threadIdx.x < acc.nclass())
     s_gbase[threadIdx.x] =
@@ -211,16 +228,23 @@ __global__ __launch_bounds__(kBlock) void k_class_verify(Acc acc, int64_t n,
   wave_flag_or(unsorted, bad, 1u);
 }
 
-// is the input ordered by (major, time)?
+// is the input ordered by (major, time)?  (eight consecutive items and the
+// next one per lane)
 template <typename Acc>
 __global__ __launch_bounds__(kBlock) void k_major_sorted(Acc acc, int64_t n,
                                                          uint32_t* unsorted) {
   if (__builtin_amdgcn_readfirstlane((int)flag_read(unsorted)) != 0) return;
-  int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  const int64_t i0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * 8;
   bool bad = false;
-  if (p + 1 < n) {
-    const uint32_t a = acc.major(p), b = acc.major(p + 1);
-    bad = a > b || (a == b && acc.time(p + 1) < acc.time(p));
+  if (i0 < n) {
+    uint32_t m[9];
+    int64_t t[9];
+    bool v[9];
+    major_time_block(acc, i0, n, m, t, v);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (v[j + 1])
+        bad = bad || m[j] > m[j + 1] || (m[j] == m[j + 1] && t[j + 1] < t[j]);
   }
   wave_flag_or(unsorted, bad, 1u);
 }
@@ -393,7 +417,7 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
       CHOPPER_HIP(launch("sort_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
                          L.flag, (int64_t)1, 0u));
       CHOPPER_HIP(launch("sort_major_sorted", k_major_sorted<Acc>,
-                         grid_for(n, kBlock), dim3(kBlock), s, acc, n,
+                         grid_for(n, kBlock * 8), dim3(kBlock), s, acc, n,
                          L.flag));
       uint32_t unsorted = 1;
       CHOPPER_HIP(read_back(L.flag, &unsorted, sizeof(uint32_t), s));
@@ -505,23 +529,19 @@ __global__ __launch_bounds__(kBlock) void k_class_hist2(AccA a, AccB b,
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   const int64_t base = (int64_t)blockIdx.x * kSortTile;
   const int nb[2] = {class_bits(a.nclass()), class_bits(b.nclass())};
-  // every class id of the tile first (all loads in flight), then the counts
-  uint32_t d[kSortIpt][2];
+  // every class id of the tile first (eight consecutive items per lane,
+  // vector loads; counts need no order), then the counts
+  uint32_t d[2][kSortIpt];
   bool v[kSortIpt];
-#pragma unroll
-  for (int j = 0; j < kSortIpt; ++j) {
-    const int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
-    v[j] = i < n;
-    d[j][0] = v[j] ? a.cls(i) : 0u;
-    d[j][1] = v[j] ? b.cls(i) : 0u;
-  }
+  cls_block(a, base + (int64_t)threadIdx.x * kSortIpt, n, d[0], v);
+  cls_block(b, base + (int64_t)threadIdx.x * kSortIpt, n, d[1], v);
 #pragma unroll
   for (int j = 0; j < kSortIpt; ++j) {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const uint64_t peers = digit_peers(d[j][q], v[j], nb[q]);
+      const uint64_t peers = digit_peers(d[q][j], v[j], nb[q]);
       if (v[j] && __popcll(peers & lt) == 0)
-        atomicAdd(&h[q][d[j][q]], (uint32_t)__popcll(peers));
+        atomicAdd(&h[q][d[q][j]], (uint32_t)__popcll(peers));
     }
   }
   __syncthreads();
@@ -554,12 +574,8 @@ __global__ __launch_bounds__(kBlock) void k_class_partition2(
   const int64_t tile_n = (n - base) < kSortTile ? (n - base) : kSortTile;
   uint32_t da[kSortIpt], db[kSortIpt], rank[kSortIpt];
   bool valid[kSortIpt];
-  for (int j = 0; j < kSortIpt; ++j) {
-    const int64_t i = base + (int64_t)j * kBlock + threadIdx.x;
-    valid[j] = i < n;
-    da[j] = valid[j] ? a.cls(i) : 0u;
-    db[j] = valid[j] ? b.cls(i) : 0u;
-  }
+  striped_classes(a, base, n, s_dig, da, valid);
+  striped_classes(b, base, n, s_dig, db, valid);
   const int CA = a.nclass();
 #pragma unroll
   for (int q = 0; q < 2; ++q) {

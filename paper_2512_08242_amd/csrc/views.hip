@@ -8,7 +8,9 @@
 // Units (one GPU's iteration marker) get dense numbers from a scan of the
 // marker levels.  The class view reads the records once in wave tiles: per
 // distinct (unit, phase) of a tile the lanes sum their items per class and
-// one wave reduction per class and field feeds one atomic add.  The
+// one wave reduction per class and field feeds one atomic add; a tile with
+// more distinct pairs than a few (records out of time order) adds the rest
+// item by item.  The
 // operation view re-keys the rows of the operation level the same way,
 // through a per-wave LDS table of (operation, kind) sums.  Medians take one
 // 1024-thread block per group: a radix selection of the two middle order
@@ -29,6 +31,7 @@ constexpr int kMaxPhases = 16;
 constexpr int kMaxOps = 128;
 constexpr int kMedThreads = 1024;
 constexpr int kMedIpt = 8;       // items per thread held in registers
+constexpr int kWaveGroups = 4;   // groups a record wave sums before per-item adds
 constexpr uint64_t kSign = 1ull << 63;
 
 __global__ void k_view_fill(uint64_t* p, int64_t n, uint64_t v) {
@@ -209,8 +212,10 @@ __global__ __launch_bounds__(kBlock) void k_view_records(
   }
   uint64_t k;
   uint32_t hit;
-  // busy: compute records by iteration marker
-  while (next_group(pb, ikey, k, hit)) {
+  // busy: compute records by iteration marker; after kWaveGroups groups the
+  // rest of the tile (an input out of time order) adds item by item
+  for (int grp = 0; grp < kWaveGroups && next_group(pb, ikey, k, hit);
+       ++grp) {
     const uint32_t u = unit_of_marker((uint32_t)k, nm, level, iter_level,
                                       unit_of, ucap);
     uint64_t x = 0;
@@ -221,13 +226,24 @@ __global__ __launch_bounds__(kBlock) void k_view_records(
     if (lane == 0 && u != kNone) atomicAdd((unsigned long long*)&busy[u], x);
     pb &= ~hit;
   }
+  if (__ballot(pb != 0u) != 0) {
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j)
+      if ((pb >> j) & 1u) {
+        const uint32_t u = unit_of_marker((uint32_t)ikey[j], nm, level,
+                                          iter_level, unit_of, ucap);
+        if (u != kNone)
+          atomicAdd((unsigned long long*)&busy[u], d[j] + g[j]);
+      }
+  }
   // class view by (iteration marker, phase marker): each lane adds its items
   // into its own LDS column per class (dur and gap rows, and a count row),
   // then groups of lanes add the rows up
   uint64_t* acc = s_acc[wv];
   uint32_t* cnt = s_cnt[wv];
   const int64_t ncls = cap * P * kViewClasses;
-  while (next_group(pc, key, k, hit)) {
+  for (int grp = 0; grp < kWaveGroups && next_group(pc, key, k, hit);
+       ++grp) {
     const uint32_t u = unit_of_marker((uint32_t)(k >> 32), nm, level,
                                       iter_level, unit_of, ucap);
     const uint32_t mp = (uint32_t)k;
@@ -273,6 +289,20 @@ __global__ __launch_bounds__(kBlock) void k_view_records(
                 (uint64_t)sn);
     wave_sync();
   }
+  if (__ballot(pc != 0u) == 0) return;
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j)
+    if ((pc >> j) & 1u) {
+      const uint32_t u = unit_of_marker((uint32_t)(key[j] >> 32), nm, level,
+                                        iter_level, unit_of, ucap);
+      const uint32_t mp = (uint32_t)key[j];
+      const uint32_t p = (int64_t)mp < nm ? label[mp] : kNone;
+      if (u == kNone || p >= (uint32_t)P) continue;
+      const int64_t col = ((int64_t)p * kViewClasses + c[j]) * cap + u;
+      atomicAdd((unsigned long long*)&cls_tab[col], 1ull);
+      atomicAdd((unsigned long long*)&cls_tab[ncls + col], d[j]);
+      atomicAdd((unsigned long long*)&cls_tab[2 * ncls + col], g[j]);
+    }
 }
 
 // Operation view: the rows of the operation level re-keyed by (unit, phase

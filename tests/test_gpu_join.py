@@ -180,3 +180,30 @@ def test_join_empty_pass(ch):
                  values=np.zeros((2, 0), np.uint64), dst=[10, 11])
     got, ref, _ = join_both(ch, tr, passes + [empty])
     check(got, ref, "empty pass")
+
+
+@pytest.mark.parametrize("variant", [0, 1])
+def test_join_shuffled_records(ch, variant):
+    """Records in shuffled input order (the adversarial trace's shape, five
+    iterations): far from their sorted order, so the join gathers in sorted
+    order through its stage; values, matched bits and status exact."""
+    say(f"join: shuffled records, variant {variant}")
+    tr = tg.make_config(4, iters=5)
+    # the sorted order jumps far at most steps (what sends the join to its
+    # sorted-order gather)
+    order = np.lexsort((np.arange(tr.n), tr.start, tr.stream.astype(np.int64),
+                        tr.gpu.astype(np.int64)))
+    far = np.abs(np.diff(order.astype(np.int64))) > 4096
+    assert far.mean() > 0.5, far.mean()
+    r0 = oracle.run(tr)
+    idx = r0["idx"].reshape(-1, tr.n)[0]
+    lab = np.full(tr.n, NONE, np.uint32)
+    lab[idx != NONE] = tr.m_label[idx[idx != NONE]]
+    passes = tg.make_counter_passes(
+        tr, lab, 11 + variant, drop_frac=0.01 * variant,
+        mismatch_frac=0.01 * variant, extra=2 * variant)
+    got, ref, lab2 = join_both(ch, tr, passes)
+    check(got, ref, f"shuffled variant {variant}")
+    if variant == 0:
+        has = lab2 != NONE
+        assert np.array_equal(got[0][:, has], tr.counters[:, has])
