@@ -28,8 +28,11 @@ sys.path.insert(0, ROOT)
 METRIC = ("kernel records/sec end-to-end (align+attribute+overlap+aggregate);"
           " % HBM peak")
 HBM_PEAK_GBS = 8000.0
-# the kernel whose roofline is reported: it reads every record's counters
-ROOF_KERNEL = "agg_fast_reduce_records"
+# the kernel whose roofline is reported: the records reduction, which reads
+# every record's counters -- the fast path's (groups are runs of the
+# (gpu, kind, start') order) or, where that does not hold (e.g. shuffled
+# input with markers numbered out of order), the general path's
+ROOF_KERNELS = ("agg_fast_reduce_records", "agg_reduce_records")
 
 
 def algorithmic_bytes(n, nm, rows, depth, nc, n_rows_finest):
@@ -42,14 +45,19 @@ def algorithmic_bytes(n, nm, rows, depth, nc, n_rows_finest):
     return rec_in + rec_out + mk + rows * row
 
 
-def roof_kernel_bytes(n, depth, nc, rows_written, input_order):
+def roof_kernel_bytes(kernel, n, depth, nc, rows_written, input_order):
     """Algorithmic bytes of one launch of the records reduction: per record
     gpu, cls, path, start, end, gap, ovl and counters read once (and korder
     when the input is not grouped by GPU in start order, so that the
-    reduction reads through it); per row it produces (the two finest levels)
-    its header (path, gpu, kind, first record) and its sums and counters
-    written once."""
-    per_rec = (0 if input_order else 4) + 1 + 1 + 4 * depth + 8 * 4 + 8 * nc
+    reduction reads through it; the general path reads the gathered path
+    and gpu/kind items, 4 per level + 2 bytes, in place of gpu, cls and
+    path); per row it produces (the two finest levels on the fast path, the
+    finest on the general one) its header (path, gpu, kind, first record)
+    and its sums and counters written once."""
+    if kernel == "agg_reduce_records":
+        per_rec = 4 + 2 + 4 * depth + 8 * 4 + 8 * nc
+    else:
+        per_rec = (0 if input_order else 4) + 1 + 1 + 4 * depth + 8 * 4 + 8 * nc
     per_row = 4 * depth + 1 + 1 + 4 + 8 * (6 + nc)
     return n * per_rec + rows_written * per_row
 
@@ -190,10 +198,26 @@ def main():
     lo = pipe.rows.level_offset.cpu().numpy()
     rows_total = int(lo[-1])
     rows_finest = int(lo[depth] - lo[depth - 1])
-    # the records reduction writes the two finest levels
-    rows_records = int(lo[depth] - lo[max(depth - 2, 0)])
     log(f"[bench] warmup done; rows: {rows_total} (finest level "
         f"{rows_finest})")
+    # which records reduction this trace takes: one probe step per candidate
+    # (events recorded first, so that a kernel that does not run reads 0)
+    probe = {}
+    for name in ROOF_KERNELS:
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        b.record()
+        ch.time_kernel(name, a, b)
+        pipe.step()
+        torch.cuda.synchronize()
+        ch.time_kernel(None)
+        probe[name] = a.elapsed_time(b)
+    ROOF_KERNEL = max(ROOF_KERNELS, key=lambda k: probe[k])
+    # the fast path writes the two finest levels, the general one the finest
+    rows_records = (int(lo[depth] - lo[max(depth - 2, 0)])
+                    if ROOF_KERNEL == "agg_fast_reduce_records"
+                    else rows_finest)
 
     K = args.steps
     kev = [(torch.cuda.Event(enable_timing=True),
@@ -216,7 +240,8 @@ def main():
 
     value = n / (ms * 1e-3)
     bmin = algorithmic_bytes(n, nm, rows_total, depth, nc, rows_finest)
-    kb = roof_kernel_bytes(n, depth, nc, rows_records, input_order)
+    kb = roof_kernel_bytes(ROOF_KERNEL, n, depth, nc, rows_records,
+                           input_order)
     achieved = kb / (kms * 1e-3) / 1e9
     out = {
         "metric": METRIC,

@@ -26,3 +26,20 @@ def test_algorithmic_bytes_definition():
         19 + 8 * nc + 40 + 4 * depth
     assert bench.algorithmic_bytes(n, nm, rows + 1, depth, nc, 200) - b == \
         4 * depth + 1 + 1 + 8 + 5 * 8 + 4 + 8 * nc + 6 * 8
+
+
+def test_roof_kernel_bytes_per_path():
+    """The records reduction's bytes: fast path (two finest levels' rows,
+    records in input order or through korder) and general path (gathered
+    items in place of gpu, class and path)."""
+    import bench
+    n, depth, nc, rows = 1000, 4, 16, 300
+    per_row = 4 * depth + 1 + 1 + 4 + 8 * (6 + nc)
+    fast = bench.roof_kernel_bytes("agg_fast_reduce_records", n, depth, nc,
+                                   rows, True)
+    assert fast == n * (2 + 4 * depth + 32 + 8 * nc) + rows * per_row
+    assert bench.roof_kernel_bytes("agg_fast_reduce_records", n, depth, nc,
+                                   rows, False) == fast + 4 * n
+    gen = bench.roof_kernel_bytes("agg_reduce_records", n, depth, nc, rows,
+                                  False)
+    assert gen == n * (6 + 4 * depth + 32 + 8 * nc) + rows * per_row
