@@ -125,8 +125,9 @@ def cpu_baseline(cid, iters, tr=None):
         cores = os.cpu_count()
     what = (f"the whole benchmark trace ({tr.n} records, {tr.n_markers} "
             "markers)" if whole else
-            f"config-{cid} trace shape with {iters} iterations ({tr.n} "
-            f"records, {tr.n_markers} markers)")
+            f"a trace of the benchmark's shape ({tg.CONFIG_NAMES[cid]}) "
+            f"with {iters} iterations ({tr.n} records, {tr.n_markers} "
+            "markers)")
     return {"value": tr.n / dt, "unit": "records/s", "cores": 1,
             "host_cores_available": cores, "cpu_model": cpu_model(),
             "kind": "oracle", "seconds": dt,
