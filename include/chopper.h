@@ -477,10 +477,13 @@ int chopper_launch_split_noalloc(const chopper_records* records,
  * label is below an earlier one (iterations out of time order).
  * n_passes <= 8; the records may hold at most 255 (gpu, stream) pairs
  * (CHOPPER_EINVAL otherwise; entries of other pairs never match).  Scratch
- * protocol as above (grows with n and the largest pass).  The call waits
- * for `stream` twice: the number of the records' pairs is read back, then
- * one word saying which sides hold a label in more than one run (those
- * sides are sorted by label, which waits again inside the sort).
+ * protocol as above (grows with n, the largest pass and n x 8 bytes per
+ * value column of all passes: records far from their sorted order are
+ * gathered in that order into a row-major stage and copied back).  The
+ * call waits for `stream` twice: the number of the records' pairs is read
+ * back, then one word saying which sides hold a label in more than one run
+ * (those sides are sorted by label, which waits again inside the sort) and
+ * whether the records lie far from their sorted order.
  */
 typedef struct {
   int64_t n;
