@@ -118,3 +118,23 @@ def test_views_no_units(ch):
                            n_phases=16, n_ops=50, n_iters=50, warmup=0)
     assert got["n_units"] == 0
     assert_views(got, ref, "no units")
+
+
+def test_views_shuffled_records(ch):
+    """Records in shuffled order (the adversarial trace's shape, six
+    iterations): a 512-record tile meets far more (iteration, phase) pairs
+    than the class view sums per group, so most records take the item by
+    item path; tables and medians exact."""
+    say("views: shuffled records")
+    tr = tg.make_config(4, iters=6)
+    got, ref, st = run_both(ch, tr, n_phases=3, n_ops=64, n_iters=6,
+                            warmup=1)
+    # distinct (iteration marker, phase marker) pairs per 512-record tile
+    r = oracle.run(tr)
+    idx = r["idx"].reshape(-1, tr.n)
+    key = idx[0].astype(np.uint64) << np.uint64(32) | idx[1].astype(np.uint64)
+    tiles = [np.unique(key[i:i + 512]).size for i in range(0, tr.n, 512)]
+    assert np.mean(tiles) > 16, np.mean(tiles)
+    assert_views(got, ref, "shuffled")
+    # (the trace drops a few markers, iteration markers among them)
+    assert 0 < got["n_units"] <= tr.n_gpus * 6
