@@ -207,3 +207,23 @@ def test_join_shuffled_records(ch, variant):
     if variant == 0:
         has = lab2 != NONE
         assert np.array_equal(got[0][:, has], tr.counters[:, has])
+
+
+def test_join_shuffled_records_odd_width(ch):
+    """The sorted-order gather with an odd number of value columns in all
+    (rows of the stage not 16-byte aligned, copied back one value at a
+    time), a pass with no entries among them."""
+    say("join: shuffled records, five columns")
+    tr = tg.make_config(4, iters=3)
+    r0 = oracle.run(tr)
+    idx = r0["idx"].reshape(-1, tr.n)[0]
+    lab = np.full(tr.n, NONE, np.uint32)
+    lab[idx != NONE] = tr.m_label[idx[idx != NONE]]
+    passes = tg.make_counter_passes(tr, lab, 21, cols=(3, 2),
+                                    drop_frac=0.02, mismatch_frac=0.01)
+    empty = dict(gpu=np.zeros(0, np.uint8), stream=np.zeros(0, np.uint8),
+                 cls=np.zeros(0, np.uint8), lab=np.zeros(0, np.uint32),
+                 values=np.zeros((2, 0), np.uint64), dst=[9, 10])
+    assert sum(q["values"].shape[0] for q in passes + [empty]) % 2 == 1
+    got, ref, _ = join_both(ch, tr, passes + [empty])
+    check(got, ref, "shuffled, seven columns")
