@@ -265,7 +265,6 @@ __global__ __launch_bounds__(kStatT) void k_stats_scatter(
 #pragma unroll
   for (int k = 0; k < kStatIpt; ++k) {
     if (g[k] == kNone) continue;
-    const int64_t r = r0 + (int64_t)k * kStatT;
     const uint64_t d = (uint64_t)du[k];
     const uint64_t ov = (uint64_t)ol[k];
     const uint64_t y = d + (uint64_t)gp[k];
