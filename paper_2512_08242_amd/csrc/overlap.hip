@@ -383,8 +383,8 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
     const int64_t* start, const int64_t* end, const SegMax* tile_pre,
     const uint32_t* tile_run0, const SegSum* tile_inc0, const uint32_t* nruns,
     const SegMax* grand, int64_t* rs, int64_t* re, int64_t* pl,
-    uint32_t* rseg, uint32_t* rbeg, uint32_t* rend, uint32_t* btable,
-    int64_t btable_cap) {
+    uint32_t* rseg, uint32_t* rhead, uint32_t* rbeg, uint32_t* rend,
+    uint32_t* btable, int64_t btable_cap) {
   __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
   // the bucket index table, built right after this pass, starts unset
   bindex_clear(btable, btable_cap, blockIdx.x, gridDim.x);
@@ -481,12 +481,22 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
     wave_sync();
   }
   {
+    // segments, and the korder position of the head of every
+    // communication run
     uint32_t* su = (uint32_t*)sl;
+    uint32_t* sp = su + kWaveTile;
 #pragma unroll
     for (int j = 0; j < kTileIpt; ++j)
-      if ((it.m_head >> j) & 1u) su[k[j]] = it.seg[j];
+      if ((it.m_head >> j) & 1u) {
+        su[k[j]] = it.seg[j];
+        sp[k[j]] = (uint32_t)(wbase + (int64_t)lane * kTileIpt + j);
+      }
     wave_sync();
-    for (uint32_t q = lane; q < H; q += kWave) rseg[r0 + q] = su[q];
+    for (uint32_t q = lane; q < H; q += kWave) {
+      const uint32_t sg = su[q];
+      rseg[r0 + q] = sg;
+      if (sg & 1u) rhead[r0 + q] = sp[q];
+    }
     wave_sync();
   }
 }
@@ -500,8 +510,8 @@ __device__ inline void overlap_gpu(int g, const Runs& R, int64_t* gwin);
 // Block 0 also writes the GPU windows.
 __global__ __launch_bounds__(kBlock) void k_comm_records(
     int G, const uint32_t* korder, const uint32_t* kbeg, const uint32_t* roff,
-    const int64_t* start, const int64_t* end, Runs R, int64_t* ovl,
-    int64_t* gwin) {
+    const uint8_t* cdone, const int64_t* start, const int64_t* end, Runs R,
+    int64_t* ovl, int64_t* gwin) {
   extern __shared__ BSeg s_seg[];   // 2G entries (dynamic LDS)
   __shared__ uint32_t s_roff[kSegs / 2 + 1];
   for (int i = threadIdx.x; i <= G; i += kBlock) s_roff[i] = roff[i];
@@ -511,6 +521,7 @@ __global__ __launch_bounds__(kBlock) void k_comm_records(
   const int64_t total = s_roff[G];
   for (int64_t v = (int64_t)blockIdx.x * kBlock + threadIdx.x; v < total;
        v += (int64_t)gridDim.x * kBlock) {
+    if (cdone[v]) continue;        // alone in its run: written with the run
     int lo = 0, hi = G;            // the last g with roff[g] <= v
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
@@ -567,7 +578,8 @@ __device__ inline void comm_offsets(int G, const BSeg* seg,
 
 __global__ __launch_bounds__(kBlock) void k_runs_comm_overlap(
     Runs R, int G, const uint32_t* kbeg, const uint32_t* kend, uint32_t* voff,
-    uint32_t* roff, int64_t* ovc, int64_t* fcrs) {
+    uint32_t* roff, int64_t* ovc, int64_t* fcrs, const uint32_t* korder,
+    const uint32_t* rhead, int64_t* ovl, uint8_t* cdone) {
   extern __shared__ BSeg s_seg[];   // 2G entries (dynamic LDS)
   __shared__ uint32_t s_voff[kSegs / 2 + 1];
   __shared__ uint32_t s_roff[kSegs / 2 + 1];
@@ -591,8 +603,23 @@ __global__ __launch_bounds__(kBlock) void k_runs_comm_overlap(
     bi_range(R.X, P, t[1], &l2[1], &h2[1]);
     bsearch_k<2>(R.rs, l2, h2, t);
     const int64_t f = F_at(R, P, l2[0], t[0]);
-    ovc[v] = F_at(R, P, l2[1], t[1]) - f;
+    const int64_t oc = F_at(R, P, l2[1], t[1]) - f;
+    ovc[v] = oc;
     fcrs[v] = f;
+    // the run's records: korder positions from its head to the next run's
+    // (or the segment's end); a record alone in its run spans exactly the
+    // run (its end clamped to its start), so its overlapped time is the
+    // run's.  Every communication record of the gpu gets its flag here.
+    const BSeg Pm = s_seg[2 * lo + 1];
+    const uint32_t hp = rhead[r];
+    const uint32_t hq = r + 1 < (int64_t)Pm.se ? rhead[r + 1] : kend[2 * lo + 1];
+    const int64_t d0 = (int64_t)s_roff[lo] - (int64_t)kbeg[2 * lo + 1];
+    if (hq == hp + 1) {
+      ovl[korder[hp]] = oc;
+      cdone[d0 + hp] = 1;
+    } else {
+      for (uint32_t p = hp; p < hq; ++p) cdone[d0 + p] = 0;
+    }
   }
 }
 
@@ -935,6 +962,8 @@ struct OverlapLayout {
   int64_t* rs;
   int64_t* re;
   uint32_t* rseg;
+  uint32_t* rhead;    // korder position of the head of each comm run
+  uint8_t* cdone;     // comm record (dense index) done with its run
   uint32_t* rbeg;     // kSegs, then rend kSegs
   uint32_t* rend;
   int64_t* pl;
@@ -968,6 +997,8 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   L.rs = sc.take<int64_t>(n);
   L.re = sc.take<int64_t>(n);
   L.rseg = sc.take<uint32_t>(n);
+  L.rhead = sc.take<uint32_t>(n);
+  L.cdone = sc.take<uint8_t>(n);
   L.rbeg = sc.take<uint32_t>(4 * kSegs);   // run and korder ranges
   L.rend = L.rbeg ? L.rbeg + kSegs : nullptr;
   L.pl = sc.take<int64_t>(n);
@@ -1045,7 +1076,7 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                        (const SegMax*)L.tile_pre, (const uint32_t*)L.tile_run0,
                        (const SegSum*)L.tile_incp, (const uint32_t*)L.nruns,
                        (const SegMax*)L.grand, L.rs, L.re, L.pl, L.rseg,
-                       L.rbeg, L.rend, L.btable, L.btable_cap));
+                       L.rhead, L.rbeg, L.rend, L.btable, L.btable_cap));
   }
   // bucket index of the run starts of every (gpu, kind) (the write pass
   // cleared its table)
@@ -1064,7 +1095,8 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                          dim3((unsigned)cg), dim3(kBlock), segs_bytes, s, R, G,
                          (const uint32_t*)(L.rbeg + 2 * kSegs),
                          (const uint32_t*)(L.rbeg + 3 * kSegs), L.voff, L.roff,
-                         L.ovc, L.fcrs));
+                         L.ovc, L.fcrs, korder, (const uint32_t*)L.rhead,
+                         ovl_out, L.cdone));
 
   if (n > 0) {
 
@@ -1080,8 +1112,8 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                            dim3((unsigned)cg), dim3(kBlock), segs_bytes, s, G,
                            korder,
                            (const uint32_t*)(L.rbeg + 2 * kSegs),
-                           (const uint32_t*)L.roff, start_al, end_al, R,
-                           ovl_out, gwin_out));
+                           (const uint32_t*)L.roff, (const uint8_t*)L.cdone,
+                           start_al, end_al, R, ovl_out, gwin_out));
   }
   if (nm > 0)
     CHOPPER_HIP(launch_shm("ov_markers", k_overlap_markers,
