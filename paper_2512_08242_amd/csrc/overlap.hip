@@ -324,11 +324,14 @@ __global__ __launch_bounds__(kBlock) void k_runs_count(
     int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
     const int64_t* start, const int64_t* end, const SegMax* tile_pre,
     SegMax* tile_agg, SegMax* tile_first, uint32_t* tile_heads,
-    SegSum* tile_inc, uint32_t* ranges) {
+    SegSum* tile_inc, uint32_t* ranges, uint32_t* mixed) {
   __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
-  // first pass: block 0 clears the segment run and korder ranges
-  if (ranges && blockIdx.x == 0)
+  // first pass: block 0 clears the segment run and korder ranges and the
+  // mixed-streams flag of the bubbles
+  if (ranges && blockIdx.x == 0) {
     for (int i = threadIdx.x; i < 4 * kSegs; i += kBlock) ranges[i] = 0;
+    if (threadIdx.x == 0) *mixed = 0;
+  }
   if (tile_pre) {
     const SegMax c = tile_pre[blockIdx.x], f = tile_first[blockIdx.x];
     if (!(c.seg == f.seg && c.val >= f.val)) return;   // block-uniform
@@ -636,8 +639,9 @@ constexpr int kRunWin = 256;
 
 __global__ __launch_bounds__(kBlock) void k_overlap_records(
     int64_t n, int G, const uint32_t* korder, const uint8_t* gpu,
-    const uint8_t* cls, const int64_t* start, const int64_t* end, Runs R,
-    int64_t* ovl) {
+    const uint8_t* stream, const uint8_t* cls, const int64_t* start,
+    const int64_t* end, Runs R, int64_t* ovl, int64_t* gap,
+    uint32_t* mixed) {
   extern __shared__ BSeg s_seg[];   // 2G entries (dynamic LDS)
   __shared__ int64_t s_win[kWavesPerBlock][3][kRunWin];
   segs_to_lds(s_seg, R.X.seg, 2 * G);
@@ -658,6 +662,42 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
     e[j] = end[r[j]];
     if (in) m_in |= 1u << j;
     if (in && (int)(seg[j] >> 1) < G) m_valid |= 1u << j;
+  }
+  // Bubbles (Section V-D eqs. 1-3): when every GPU runs its compute
+  // kernels on one stream, the previous compute record of a compute
+  // record's (gpu, stream) is its predecessor in its (gpu, kind) segment of
+  // korder.  Predecessors come from the lane below (lane 0: lane 63 of the
+  // row above, or the position before the wave); a predecessor on another
+  // stream sets *mixed, and the bubble pass then recomputes every bubble.
+  {
+    uint32_t lseg = kNone, lst = 0;
+    int64_t lend = 0;
+    if (base > 0) {
+      const uint32_t rb = korder[base - 1];
+      lseg = (uint32_t)gpu[rb] * 2u + (uint32_t)kind_of(cls[rb]);
+      lst = stream[rb];
+      lend = end[rb];
+    }
+    bool mix = false;
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      const uint32_t st = stream[r[j]];
+      const uint32_t pseg = wave_shr1_u32(lseg, seg[j]);
+      const uint32_t pst = wave_shr1_u32(lst, st);
+      const int64_t pe = (int64_t)wave_shr1((uint64_t)lend, (uint64_t)e[j]);
+      lseg = (uint32_t)__builtin_amdgcn_readlane((int)seg[j], kWave - 1);
+      lst = (uint32_t)__builtin_amdgcn_readlane((int)st, kWave - 1);
+      lend = lane63(e[j]);
+      if (!((m_in >> j) & 1u)) continue;
+      int64_t gv = 0;
+      if (!(seg[j] & 1u) && pseg == seg[j]) {
+        mix = mix || pst != st;
+        const int64_t b = s[j] - pe;
+        gv = b > 0 ? b : 0;
+      }
+      gap[r[j]] = gv;
+    }
+    wave_flag_or(mixed, mix, 1u);
   }
   // communication records are done by k_comm_records
 #pragma unroll
@@ -842,8 +882,11 @@ struct OpLastComp {
 __global__ __launch_bounds__(kBlock) void k_gap(
     int64_t n, const uint32_t* order, const uint8_t* gpu, const uint8_t* stream,
     const uint8_t* cls, const int64_t* start, const int64_t* end,
-    int64_t* gap) {
+    const uint32_t* mixed, int64_t* gap) {
   __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
+  // (the compute-record pass wrote every bubble unless some GPU's compute
+  // kernels run on several streams)
+  if (__builtin_amdgcn_readfirstlane((int)flag_read(mixed)) == 0) return;
   const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
   const int64_t base =
       ((int64_t)blockIdx.x * kWavesPerBlock + wv) * (int64_t)kWaveTile;
@@ -964,6 +1007,7 @@ struct OverlapLayout {
   uint32_t* rseg;
   uint32_t* rhead;    // korder position of the head of each comm run
   uint8_t* cdone;     // comm record (dense index) done with its run
+  uint32_t* mixed;    // some GPU's compute records on several streams
   uint32_t* rbeg;     // kSegs, then rend kSegs
   uint32_t* rend;
   int64_t* pl;
@@ -999,6 +1043,7 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   L.rseg = sc.take<uint32_t>(n);
   L.rhead = sc.take<uint32_t>(n);
   L.cdone = sc.take<uint8_t>(n);
+  L.mixed = sc.take<uint32_t>(1);
   L.rbeg = sc.take<uint32_t>(4 * kSegs);   // run and korder ranges
   L.rend = L.rbeg ? L.rbeg + kSegs : nullptr;
   L.pl = sc.take<int64_t>(n);
@@ -1057,7 +1102,7 @@ extern "C" int chopper_overlap(const chopper_records* rec,
     CHOPPER_HIP(launch("ov_runs_count", k_runs_count, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
                        (const SegMax*)nullptr, L.tile_agg, L.tile_first,
-                       L.tile_heads, L.tile_inc, L.rbeg));
+                       L.tile_heads, L.tile_inc, L.rbeg, L.mixed));
     const dim3 sg((unsigned)ceil_div(L.ntiles, (int64_t)kSpineSpan));
     CHOPPER_HIP(launch("ov_runs_spine", k_tile_spine<SegMax, OpSegMax>, sg,
                        dim3(kSpineSpan), s, (const SegMax*)L.tile_agg,
@@ -1066,7 +1111,7 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
                        (const SegMax*)L.tile_pre, (SegMax*)nullptr,
                        L.tile_first, L.tile_heads, L.tile_inc,
-                       (uint32_t*)nullptr));
+                       (uint32_t*)nullptr, (uint32_t*)nullptr));
     CHOPPER_HIP(launch("ov_runs_inc_spine", k_runs_spine2, sg,
                        dim3(kSpineSpan), s, (const uint32_t*)L.tile_heads,
                        L.tile_run0, L.nruns, (const SegSum*)L.tile_inc,
@@ -1106,8 +1151,8 @@ extern "C" int chopper_overlap(const chopper_records* rec,
     CHOPPER_HIP(launch_shm("ov_records", k_overlap_records,
                        dim3((unsigned)ceil_div(n, (int64_t)kOvTile)),
                        dim3(kBlock), segs_bytes, s, n, G, korder, rec->gpu,
-                       rec->cls,
-                       start_al, end_al, R, ovl_out));
+                       rec->stream, rec->cls, start_al, end_al, R, ovl_out,
+                       gap_out, L.mixed));
     CHOPPER_HIP(launch_shm("ov_comm_records", k_comm_records,
                            dim3((unsigned)cg), dim3(kBlock), segs_bytes, s, G,
                            korder,
@@ -1128,7 +1173,7 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                        dim3((unsigned)ceil_div(n, (int64_t)kOvTile)),
                        dim3(kBlock), s,
                        n, order, rec->gpu, rec->stream, rec->cls, start_al,
-                       end_al, gap_out));
+                       end_al, (const uint32_t*)L.mixed, gap_out));
   }
   return CHOPPER_OK;
 }
