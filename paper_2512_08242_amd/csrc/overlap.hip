@@ -649,7 +649,7 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
   const int64_t base =
       ((int64_t)blockIdx.x * kWavesPerBlock + wv) * (int64_t)kWaveTile;
   if (base >= n) return;
-  uint32_t r[kTileIpt], seg[kTileIpt];
+  uint32_t r[kTileIpt], seg[kTileIpt], st[kTileIpt];
   int64_t s[kTileIpt], e[kTileIpt];
   uint32_t m_in = 0, m_valid = 0;   // position exists / and gpu < G
 #pragma unroll
@@ -658,46 +658,11 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
     const bool in = p < n;
     r[j] = korder[in ? p : base];
     seg[j] = (uint32_t)gpu[r[j]] * 2u + (uint32_t)kind_of(cls[r[j]]);
+    st[j] = stream[r[j]];
     s[j] = start[r[j]];
     e[j] = end[r[j]];
     if (in) m_in |= 1u << j;
     if (in && (int)(seg[j] >> 1) < G) m_valid |= 1u << j;
-  }
-  // Bubbles (Section V-D eqs. 1-3): when every GPU runs its compute
-  // kernels on one stream, the previous compute record of a compute
-  // record's (gpu, stream) is its predecessor in its (gpu, kind) segment of
-  // korder.  Predecessors come from the lane below (lane 0: lane 63 of the
-  // row above, or the position before the wave); a predecessor on another
-  // stream sets *mixed, and the bubble pass then recomputes every bubble.
-  {
-    uint32_t lseg = kNone, lst = 0;
-    int64_t lend = 0;
-    if (base > 0) {
-      const uint32_t rb = korder[base - 1];
-      lseg = (uint32_t)gpu[rb] * 2u + (uint32_t)kind_of(cls[rb]);
-      lst = stream[rb];
-      lend = end[rb];
-    }
-    bool mix = false;
-#pragma unroll
-    for (int j = 0; j < kTileIpt; ++j) {
-      const uint32_t st = stream[r[j]];
-      const uint32_t pseg = wave_shr1_u32(lseg, seg[j]);
-      const uint32_t pst = wave_shr1_u32(lst, st);
-      const int64_t pe = (int64_t)wave_shr1((uint64_t)lend, (uint64_t)e[j]);
-      lseg = (uint32_t)__builtin_amdgcn_readlane((int)seg[j], kWave - 1);
-      lst = (uint32_t)__builtin_amdgcn_readlane((int)st, kWave - 1);
-      lend = lane63(e[j]);
-      if (!((m_in >> j) & 1u)) continue;
-      int64_t gv = 0;
-      if (!(seg[j] & 1u) && pseg == seg[j]) {
-        mix = mix || pst != st;
-        const int64_t b = s[j] - pe;
-        gv = b > 0 ? b : 0;
-      }
-      gap[r[j]] = gv;
-    }
-    wave_flag_or(mixed, mix, 1u);
   }
   // communication records are done by k_comm_records
 #pragma unroll
@@ -791,6 +756,46 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
   for (int j = 0; j < kTileIpt; ++j)
     if (((m_in >> j) & 1u) && !((seg[j] & 1u) && (int)(seg[j] >> 1) < G))
       ovl[r[j]] = o[j];
+  // Bubbles (Section V-D eqs. 1-3): when every GPU runs its compute
+  // kernels on one stream, the previous compute record of a compute
+  // record's (gpu, stream) is its predecessor in its (gpu, kind) segment of
+  // korder.  Predecessors come from the lane below (lane 0: lane 63 of the
+  // row above, or the position before the wave); a predecessor on another
+  // stream sets *mixed, and the bubble pass then recomputes every bubble.
+  {
+    uint32_t lseg = kNone, lst = 0;
+    int64_t lend = 0;
+    if (base > 0) {
+      const uint32_t rb = korder[base - 1];
+      lseg = (uint32_t)gpu[rb] * 2u + (uint32_t)kind_of(cls[rb]);
+      lst = stream[rb];
+      lend = end[rb];
+    }
+    bool mix = false;
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      if (j > 0) {
+        // lane 0 takes lane 63 of the row above
+        lseg = wave_ror1_u32(seg[j - 1]);
+        lst = wave_ror1_u32(st[j - 1]);
+        const uint64_t ev = (uint64_t)e[j - 1];
+        lend = (int64_t)((uint64_t)wave_ror1_u32((uint32_t)ev) |
+                         (uint64_t)wave_ror1_u32((uint32_t)(ev >> 32)) << 32);
+      }
+      const uint32_t pseg = wave_shr1_u32(lseg, seg[j]);
+      const uint32_t pst = wave_shr1_u32(lst, st[j]);
+      const int64_t pe = (int64_t)wave_shr1((uint64_t)lend, (uint64_t)e[j]);
+      if (!((m_in >> j) & 1u)) continue;
+      int64_t gv = 0;
+      if (!(seg[j] & 1u) && pseg == seg[j]) {
+        mix = mix || pst != st[j];
+        const int64_t b = s[j] - pe;
+        gv = b > 0 ? b : 0;
+      }
+      gap[r[j]] = gv;
+    }
+    wave_flag_or(mixed, mix, 1u);
+  }
 }
 
 // Window values of every marker, one per thread (more markers per thread
