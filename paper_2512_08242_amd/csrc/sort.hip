@@ -553,10 +553,111 @@ __global__ __launch_bounds__(kBlock) void k_class_hist2(AccA a, AccB b,
         h[1][threadIdx.x];
 }
 
+// Tiles of at most two classes per key -- nearly every tile of records in
+// (gpu, start') order: one GPU's compute and communication streams -- are
+// ranked with one ballot per row by a pass of their own, which needs little
+// LDS and so keeps many blocks per CU; it flags the other tiles, and the
+// general pass below (the LDS ranking) does only those.
+struct TwoShared {
+  uint32_t c[2];
+  uint32_t wcnt[kSortIpt][kWavesPerBlock];
+};
+
+// An item's stable rank among its class: the number of class-c1 items
+// before it (earlier rows, earlier waves of its row, lower lanes of its
+// wave), or its position minus that number.  False (block-uniform) when the
+// tile holds more than two classes.  Invalid items only follow valid ones.
+__device__ inline bool two_class_ranks(const uint32_t (&dig)[kSortIpt],
+                                       const bool (&valid)[kSortIpt],
+                                       TwoShared& sh, uint32_t& c0,
+                                       uint32_t& c1,
+                                       uint32_t (&rank)[kSortIpt]) {
+  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  if (t == 0) {
+    sh.c[0] = dig[0];          // (item 0 of a tile always exists)
+    sh.c[1] = kNone;
+  }
+  __syncthreads();
+  c0 = sh.c[0];
+  uint32_t mine = kNone;
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j)
+    if (valid[j] && dig[j] != c0 && dig[j] < mine) mine = dig[j];
+  if (mine != kNone) atomicMin(&sh.c[1], mine);
+  __syncthreads();
+  c1 = sh.c[1];
+  bool more = false;
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j)
+    more = more || (valid[j] && dig[j] != c0 && dig[j] != c1);
+  if (__syncthreads_or(more ? 1 : 0)) return false;
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  uint64_t bm[kSortIpt];
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j) {
+    bm[j] = __ballot(valid[j] && dig[j] == c1);
+    if (lane == 0) sh.wcnt[j][w] = (uint32_t)__popcll(bm[j]);
+  }
+  __syncthreads();
+  uint32_t before = 0;   // class-c1 items in the rows above
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j) {
+    uint32_t inrow = 0, row = 0;
+#pragma unroll
+    for (int q = 0; q < kWavesPerBlock; ++q) {
+      const uint32_t x = sh.wcnt[j][q];
+      if (q < w) inrow += x;
+      row += x;
+    }
+    const uint32_t c1b = before + inrow + (uint32_t)__popcll(bm[j] & lt);
+    const uint32_t pos = (uint32_t)(j * kBlock + t);
+    rank[j] = (valid[j] && dig[j] == c1) ? c1b : pos - c1b;
+    before += row;
+  }
+  __syncthreads();   // (the shared words are reused by the next call)
+  return true;
+}
+
+template <typename AccA, typename AccB>
+__global__ __launch_bounds__(kBlock) void k_class_partition2_two(
+    AccA a, AccB b, int64_t n, int64_t ntiles, const uint32_t* tileoff,
+    uint32_t* outA, uint32_t* outB, uint8_t* general) {
+  __shared__ uint8_t s_dig[kSortTile];
+  __shared__ TwoShared two;
+  const int64_t base = (int64_t)blockIdx.x * kSortTile;
+  uint32_t da[kSortIpt], db[kSortIpt], ra[kSortIpt], rb[kSortIpt];
+  bool valid[kSortIpt];
+  striped_classes(a, base, n, s_dig, da, valid);
+  striped_classes(b, base, n, s_dig, db, valid);
+  uint32_t a0, a1, b0, b1;
+  const bool ok = two_class_ranks(da, valid, two, a0, a1, ra) &&
+                  two_class_ranks(db, valid, two, b0, b1, rb);
+  if (threadIdx.x == 0) general[blockIdx.x] = ok ? 0 : 1;
+  if (!ok) return;   // (block-uniform)
+  // B's rows of the table follow A's; its scanned values include A's n
+  const int64_t CA = a.nclass();
+  const uint32_t ga0 = tileoff[(int64_t)a0 * ntiles + blockIdx.x];
+  const uint32_t ga1 =
+      a1 != kNone ? tileoff[(int64_t)a1 * ntiles + blockIdx.x] : 0u;
+  const uint32_t gb0 =
+      tileoff[(CA + b0) * ntiles + blockIdx.x] - (uint32_t)n;
+  const uint32_t gb1 =
+      b1 != kNone ? tileoff[(CA + b1) * ntiles + blockIdx.x] - (uint32_t)n
+                  : 0u;
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j) {
+    if (!valid[j]) continue;
+    const uint32_t item = (uint32_t)(base + (int64_t)j * kBlock + threadIdx.x);
+    outA[(int64_t)(da[j] == a0 ? ga0 : ga1) + ra[j]] = item;
+    outB[(int64_t)(db[j] == b0 ? gb0 : gb1) + rb[j]] = item;
+  }
+}
+
 template <typename AccA, typename AccB>
 __global__ __launch_bounds__(kBlock) void k_class_partition2(
     AccA a, AccB b, int64_t n, int64_t ntiles, const uint32_t* tileoff,
-    uint32_t* outA, uint32_t* outB, uint32_t* coffA, uint32_t* coffB) {
+    uint32_t* outA, uint32_t* outB, uint32_t* coffA, uint32_t* coffB,
+    const uint8_t* general) {
   if (blockIdx.x == 0) {
     // class start offsets of both sorts (B's scanned values include A's n)
     const int CA = a.nclass(), CB = b.nclass();
@@ -566,6 +667,7 @@ __global__ __launch_bounds__(kBlock) void k_class_partition2(
       coffB[c] = c < CB ? tileoff[(int64_t)(CA + c) * ntiles] - (uint32_t)n
                         : (uint32_t)n;
   }
+  if (!general[blockIdx.x]) return;   // done by the two-class pass
   __shared__ RankShared sh;
   __shared__ uint32_t s_val[kSortTile];
   __shared__ uint8_t s_dig[kSortTile];
@@ -621,9 +723,16 @@ int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
   CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, L.tileoff,
                                        (int64_t)(CA + CB) * T, L.scantmp,
                                        L.total, s));
+  // (a byte per tile: the radix keys' space is free on this path)
+  uint8_t* general = reinterpret_cast<uint8_t*>(L.key0);
+  CHOPPER_HIP(launch("sort_class_partition",
+                     k_class_partition2_two<AccA, AccB>, dim3((unsigned)T),
+                     dim3(kBlock), s, a, b, n, T, (const uint32_t*)L.tileoff,
+                     outA, outB, general));
   CHOPPER_HIP(launch("sort_class_partition", k_class_partition2<AccA, AccB>,
                      dim3((unsigned)T), dim3(kBlock), s, a, b, n, T,
-                     (const uint32_t*)L.tileoff, outA, outB, coffA, coffB));
+                     (const uint32_t*)L.tileoff, outA, outB, coffA, coffB,
+                     (const uint8_t*)general));
   return CHOPPER_OK;
 }
 
