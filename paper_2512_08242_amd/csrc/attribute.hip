@@ -358,16 +358,23 @@ extern "C" int chopper_attribute(const chopper_records* rec,
   AttrLayout L = attr_layout(sc, n, nm, G, D);
   KeyMarker km{mk->gpu, mk->level, mstart_al, mend_al, G, D};
   bool range_err = false;
-  rc = class_sort(km, L.sort, L.mord, L.coff, &range_err, s, -1);
+  // markers in start order (the usual case): the class partition writes the
+  // sorted columns itself
+  const MarkerColumns cols{mstart_al, mend_al, L.sms, L.sme, L.sid, L.sseg,
+                           G, D};
+  bool gathered = false;
+  rc = class_sort(km, L.sort, L.mord, L.coff, &range_err, s, -1, cols,
+                  &gathered);
   if (rc != CHOPPER_OK) return rc;
   if (range_err)
     CHOPPER_HIP(launch("status_set", k_status_set, dim3(1), dim3(1), s,
                        (uint32_t)CHOPPER_ST_RANGE, status));
   if (nm > 0) {
-    CHOPPER_HIP(launch("attr_marker_gather", k_marker_gather,
-                       grid_for(nm, kBlock), dim3(kBlock), s, nm, km,
-                       (const uint32_t*)L.mord, mstart_al, mend_al, L.sms,
-                       L.sme, L.sid, L.sseg, L.btable, L.btable_cap));
+    if (!gathered)
+      CHOPPER_HIP(launch("attr_marker_gather", k_marker_gather,
+                         grid_for(nm, kBlock), dim3(kBlock), s, nm, km,
+                         (const uint32_t*)L.mord, mstart_al, mend_al, L.sms,
+                         L.sme, L.sid, L.sseg, L.btable, L.btable_cap));
     const int64_t per_seg = ceil_div(nm, (int64_t)G * D);
     unsigned gx = (unsigned)ceil_div(per_seg, kBlock);
     if (gx < 1) gx = 1;
@@ -378,10 +385,11 @@ extern "C" int chopper_attribute(const chopper_records* rec,
                        (const int64_t*)L.sme, status));
   }
   if (n == 0 || D == 0) return CHOPPER_OK;
-  // bucket index of the non-empty marker starts of every (gpu, level)
+  // bucket index of the non-empty marker starts of every (gpu, level) (the
+  // gather pass, when it ran, cleared the table)
   CHOPPER_HIP(bindex_build(L.sms, L.sseg, nm, nullptr, L.coff, L.coff + 1, 2,
                            G * D, L.bsegs, L.btable, L.btable_cap, L.btmp, s,
-                           nm > 0));
+                           nm > 0 && !gathered));
   const BIndex X{L.sms, L.bsegs, L.btable};
   const unsigned grid = (unsigned)ceil_div(n, (int64_t)kWaveTile * kWavesPerBlock);
   CHOPPER_HIP(launch("attr_windows", k_attr_windows,

@@ -146,6 +146,30 @@ __device__ inline void cls_block(const KeyMarker& a, int64_t i0, int64_t n,
   a.cls8(i0, n, d, v);
 }
 
+// What a class partition can write beside the permutation, at each item's
+// sorted position p (item index i, class c): nothing by default.
+struct NoColumns {
+  __device__ void put(int64_t, uint32_t, uint32_t) const {}
+};
+
+// The markers' sorted columns: start', end', input index and (gpu, level)
+// segment (kNone for empty markers and markers of no valid gpu or level).
+struct MarkerColumns {
+  const int64_t* ms;
+  const int64_t* me;
+  int64_t* sms;
+  int64_t* sme;
+  uint32_t* sid;
+  uint32_t* sseg;
+  int G, D;
+  __device__ void put(int64_t p, uint32_t i, uint32_t c) const {
+    sms[p] = ms[i];
+    sme[p] = me[i];
+    sid[p] = i;
+    sseg[p] = ((c & 1u) || c >= (uint32_t)(G * D * 2)) ? kNone : c >> 1;
+  }
+};
+
 // Positions of a sequence (position p holds item seq[p]) keyed by (dense
 // class of the item's (gpu, stream), the item's label): their stable sort
 // brings every label of a class together and keeps the sequence order
@@ -243,11 +267,14 @@ ClassSortLayout class_sort_layout(Scratch& sc, int64_t n, int c_max);
 // bits (only possible on the general path).  known_sorted = 1: the caller
 // knows the input is ordered by (major, time) -- the gpu of every accessor
 // leads its class order -- so each class subsequence is already
-// time-ordered; -1: unknown, checked here.  May synchronize `s`.
-template <typename Acc>
+// time-ordered; -1: unknown, checked here.  May synchronize `s`.  `cols`
+// is written at the sorted positions when the class partition is the sort;
+// *cols_done (optional) says whether it was (else the caller gathers them).
+template <typename Acc, typename Cols = NoColumns>
 int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
                uint32_t* coff, bool* range_error, hipStream_t s,
-               int known_sorted);
+               int known_sorted, const Cols& cols = Cols(),
+               bool* cols_done = nullptr);
 
 // Both class partitions of the same n > 0 items at once, for input ordered
 // by (major, time) (so the partitions are the stable sorts); needs

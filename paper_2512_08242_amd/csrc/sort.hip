@@ -176,10 +176,10 @@ __global__ __launch_bounds__(kBlock) void k_class_hist(Acc acc, int64_t n,
 
 // Block 0 also writes the class start offsets: coff[c] = first position of
 // class c (the scanned table's first tile), coff[C] = n.
-template <typename Acc>
+template <typename Acc, typename Cols>
 __global__ __launch_bounds__(kBlock) void k_class_partition(
     Acc acc, int64_t n, int64_t ntiles, const uint32_t* tileoff,
-    uint32_t* out, uint32_t* coff) {
+    uint32_t* out, uint32_t* coff, Cols cols) {
   if (blockIdx.x == 0) {
     const int C = acc.nclass();
     for (int c = threadIdx.x; c <= C; c += kBlock)
@@ -209,7 +209,9 @@ __global__ __launch_bounds__(kBlock) void k_class_partition(
     int q = j * kBlock + threadIdx.x;
     if (q >= tile_n) continue;
     uint32_t d = s_dig[q];
-    out[(int64_t)s_gbase[d] + (q - sh.start[d])] = s_val[q];
+    const int64_t pos = (int64_t)s_gbase[d] + (q - sh.start[d]);
+    out[pos] = s_val[q];
+    cols.put(pos, s_val[q], d);
   }
 }
 
@@ -396,10 +398,11 @@ ClassSortLayout class_sort_layout(Scratch& sc, int64_t n, int C) {
   return L;
 }
 
-template <typename Acc>
+template <typename Acc, typename Cols>
 int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
                uint32_t* coff, bool* range_error, hipStream_t s,
-               int known_sorted) {
+               int known_sorted, const Cols& cols, bool* cols_done) {
+  if (cols_done) *cols_done = false;
   const int64_t n = L.n;
   const int C = acc.nclass();
   const int64_t T = L.ntiles;
@@ -427,9 +430,9 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
                        dim3(kBlock), s, acc, n, T, L.tilehist));
     CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, L.tileoff, (int64_t)C * T,
                                          L.scantmp, L.total, s));
-    CHOPPER_HIP(launch("sort_class_partition", k_class_partition<Acc>,
+    CHOPPER_HIP(launch("sort_class_partition", k_class_partition<Acc, Cols>,
                        dim3((unsigned)T), dim3(kBlock), s, acc, n, T,
-                       (const uint32_t*)L.tileoff, out, coff));
+                       (const uint32_t*)L.tileoff, out, coff, cols));
     if (known_sorted == 1) {
       sorted = true;
     } else {
@@ -453,7 +456,10 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
     CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, coff, (int64_t)C,
                                          L.scantmp, coff + C, s));
   }
-  if (sorted) return CHOPPER_OK;
+  if (sorted) {
+    if (cols_done) *cols_done = true;
+    return CHOPPER_OK;
+  }
 
   // general path
   CHOPPER_HIP(launch("sort_init_minmax", k_init_minmax, dim3(1), dim3(1), s,
@@ -740,17 +746,17 @@ template int class_sort2<KeyRecStream, KeyRecKind>(
     const KeyRecStream&, const KeyRecKind&, const ClassSortLayout&, uint32_t*,
     uint32_t*, uint32_t*, uint32_t*, hipStream_t);
 
-template int class_sort<KeyRecStream>(const KeyRecStream&,
-                                      const ClassSortLayout&, uint32_t*,
-                                      uint32_t*, bool*, hipStream_t, int);
-template int class_sort<KeyRecKind>(const KeyRecKind&, const ClassSortLayout&,
-                                    uint32_t*, uint32_t*, bool*, hipStream_t,
-                                    int);
-template int class_sort<KeyMarker>(const KeyMarker&, const ClassSortLayout&,
-                                   uint32_t*, uint32_t*, bool*, hipStream_t,
-                                   int);
-template int class_sort<KeySeqLabel>(const KeySeqLabel&,
-                                     const ClassSortLayout&, uint32_t*,
-                                     uint32_t*, bool*, hipStream_t, int);
+template int class_sort<KeyRecStream, NoColumns>(
+    const KeyRecStream&, const ClassSortLayout&, uint32_t*, uint32_t*, bool*,
+    hipStream_t, int, const NoColumns&, bool*);
+template int class_sort<KeyRecKind, NoColumns>(
+    const KeyRecKind&, const ClassSortLayout&, uint32_t*, uint32_t*, bool*,
+    hipStream_t, int, const NoColumns&, bool*);
+template int class_sort<KeyMarker, MarkerColumns>(
+    const KeyMarker&, const ClassSortLayout&, uint32_t*, uint32_t*, bool*,
+    hipStream_t, int, const MarkerColumns&, bool*);
+template int class_sort<KeySeqLabel, NoColumns>(
+    const KeySeqLabel&, const ClassSortLayout&, uint32_t*, uint32_t*, bool*,
+    hipStream_t, int, const NoColumns&, bool*);
 
 }  // namespace chopper
