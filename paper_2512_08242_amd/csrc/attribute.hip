@@ -234,13 +234,38 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
     wo[l] = __shfl(woff, l, kWave);
     wn[l] = __shfl(fits ? wk : (int64_t)-1, l, kWave);
   }
+  // The levels that fit are a prefix of the levels (offsets grow with the
+  // level), packed from pool entry 0; entry q belongs to the last fitting
+  // level whose offset is <= q.  Every lane issues the loads of all its
+  // entries before writing any of them, so the staging costs one round trip
+  // to memory instead of one per level and per 64 markers.
+  int64_t ptot = 0;
 #pragma unroll
-  for (int l = 0; l < MaxD; ++l) {
-    if (l >= D || wn[l] < 0) continue;
-    for (int64_t q = lane; q < wn[l]; q += kWave) {
-      ps[wo[l] + q] = X.key[wl[l] + q];
-      pe[wo[l] + q] = sme[wl[l] + q];
-      pi[wo[l] + q] = sid[wl[l] + q];
+  for (int l = 0; l < MaxD; ++l)
+    if (l < D && wn[l] >= 0) ptot = wo[l] + wn[l];
+  constexpr int kStageIt = kMarkWin / kWave;
+  int64_t vk[kStageIt], ve[kStageIt];
+  uint32_t vi[kStageIt];
+#pragma unroll
+  for (int i = 0; i < kStageIt; ++i) {
+    const int64_t q = lane + (int64_t)i * kWave;
+    if (q < ptot) {
+      int64_t src = wl[0] + q - wo[0];
+#pragma unroll
+      for (int l = 1; l < MaxD; ++l)
+        if (l < D && wn[l] >= 0 && q >= wo[l]) src = wl[l] + q - wo[l];
+      vk[i] = X.key[src];
+      ve[i] = sme[src];
+      vi[i] = sid[src];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kStageIt; ++i) {
+    const int64_t q = lane + (int64_t)i * kWave;
+    if (q < ptot) {
+      ps[q] = vk[i];
+      pe[q] = ve[i];
+      pi[q] = vi[i];
     }
   }
   wave_sync();
