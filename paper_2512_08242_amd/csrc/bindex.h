@@ -24,6 +24,10 @@ struct BSeg {
 
 // table entries that no key wrote (inside a gap longer than the fill run)
 constexpr uint32_t kUnset = 0xFFFFFFFFu;
+// about one bucket per kKeysPerBucket keys; a key writes at most kFillRun
+// entries, so no thread stalls on a long gap
+constexpr int kKeysPerBucket = 4;
+constexpr int kFillRun = 256;
 
 struct BIndex {
   const int64_t* key;
@@ -67,6 +71,44 @@ __device__ inline void bsearch_k(const int64_t* key, int64_t (&lo)[K],
       }
     }
   }
+}
+
+// Bucket width (log2) and count of a segment of cnt keys from lo to last:
+// the smallest power of two with at most ceil(cnt / kKeysPerBucket)
+// buckets over the span.  Any cnt gives a valid index; it only sets the
+// bucket width.
+__device__ inline void bi_geometry(int64_t lo, int64_t last, int64_t cnt,
+                                   uint32_t* shift, uint32_t* nb) {
+  const int64_t d = (int64_t)((uint64_t)last - (uint64_t)lo);
+  const uint64_t span = d > 0 ? (uint64_t)d : 0;
+  const uint64_t target =
+      (uint64_t)((cnt + kKeysPerBucket - 1) / kKeysPerBucket);
+  uint32_t k = 0;
+  while (k < 63 && (span >> k) + 1 > target) ++k;
+  *shift = k;
+  *nb = (uint32_t)((span >> k) + 1);
+}
+
+// Bucket of a key, clamped to the table (keys are sorted, so the clamp only
+// guards against inputs that are not).
+__device__ inline int64_t bi_bucket(const BSeg& P, int64_t kv) {
+  const uint64_t d = (uint64_t)kv - (uint64_t)P.lo;
+  if ((int64_t)d < 0) return 0;
+  const uint64_t b = d >> P.shift;
+  return b < (uint64_t)P.nb ? (int64_t)b : (int64_t)P.nb - 1;
+}
+
+// Entries bp + 1 .. bi of segment P's table take v, at most kFillRun of
+// them (the rest of a longer gap stays unset).  A key at position i whose
+// predecessor in the segment is in bucket bp (-1 for the segment's first
+// key) and which is itself in bucket bi writes i this way, and the
+// segment's last key also writes se into the entries after its bucket up to
+// nb: then entry b is the first position with key >= lo + (b << shift).
+__device__ inline void bi_fill_range(uint32_t* table, const BSeg& P,
+                                     int64_t bp, int64_t bi, uint32_t v) {
+  uint32_t* tb = table + P.toff;
+  const int64_t hi = bi < bp + kFillRun ? bi : bp + kFillRun;
+  for (int64_t b = bp + 1; b <= hi; ++b) tb[b] = v;
 }
 
 // Search range of t in segment P: the answer (first position with key > t)

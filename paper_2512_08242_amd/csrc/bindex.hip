@@ -13,9 +13,6 @@
 
 namespace chopper {
 
-constexpr int kKeysPerBucket = 4;
-constexpr int kFillRun = 256;
-
 int64_t bindex_table_cap(int64_t nkeys, int64_t nseg) {
   return nkeys / kKeysPerBucket + 2 * nseg + 2;
 }
@@ -46,14 +43,7 @@ __global__ __launch_bounds__(1024) void k_bi_params(
       if (P.se > P.sb) {
         const int64_t cnt = (int64_t)P.se - P.sb;
         P.lo = key[P.sb];
-        const int64_t d = (int64_t)((uint64_t)key[P.se - 1] - (uint64_t)P.lo);
-        const uint64_t span = d > 0 ? (uint64_t)d : 0;   // keys sorted
-        const uint64_t target =
-            (uint64_t)((cnt + kKeysPerBucket - 1) / kKeysPerBucket);
-        uint32_t k = 0;
-        while (k < 63 && (span >> k) + 1 > target) ++k;
-        P.shift = k;
-        P.nb = (uint32_t)((span >> k) + 1);
+        bi_geometry(P.lo, key[P.se - 1], cnt, &P.shift, &P.nb);
         ent = P.nb + 1;
       }
     }
@@ -136,24 +126,10 @@ __global__ __launch_bounds__(kBlock) void k_bi_fill(
     if (sidx == kNone || sidx >= (uint32_t)nseg) continue;
     const BSeg P = lds ? s_seg[sidx] : segs[sidx];
     if (P.nb == 0 || i < P.sb || i >= P.se) continue;
-    // bucket of a key, clamped to the table (keys are sorted, so the clamp
-    // only guards against inputs that are not)
-    auto bucket = [&](int64_t kv) -> int64_t {
-      const uint64_t d = (uint64_t)kv - (uint64_t)P.lo;
-      if ((int64_t)d < 0) return 0;
-      const uint64_t b = d >> P.shift;
-      return b < (uint64_t)P.nb ? (int64_t)b : (int64_t)P.nb - 1;
-    };
-    const int64_t bi = bucket(k[j + 1]);
-    const int64_t bp = i == P.sb ? -1 : bucket(k[j]);
-    uint32_t* tb = table + P.toff;
-    const int64_t hi1 = bi < bp + kFillRun ? bi : bp + kFillRun;
-    for (int64_t b = bp + 1; b <= hi1; ++b) tb[b] = (uint32_t)i;
-    if (i == (int64_t)P.se - 1) {
-      const int64_t hi2 =
-          (int64_t)P.nb < bi + kFillRun ? (int64_t)P.nb : bi + kFillRun;
-      for (int64_t b = bi + 1; b <= hi2; ++b) tb[b] = P.se;
-    }
+    const int64_t bi = bi_bucket(P, k[j + 1]);
+    const int64_t bp = i == P.sb ? -1 : bi_bucket(P, k[j]);
+    bi_fill_range(table, P, bp, bi, (uint32_t)i);
+    if (i == (int64_t)P.se - 1) bi_fill_range(table, P, bi, P.nb, P.se);
   }
 }
 

@@ -203,10 +203,20 @@ __global__ __launch_bounds__(kSpineSpan) void k_tile_spine(
 }
 
 // The exclusive scan of the tiles' run counts (with the total) and the
-// segmented scan of their union increments (with the total).
+// segmented scan of their union increments (with the total).  Block 0 also
+// sets up the bucket index of the run starts of every (gpu, kind) segment
+// before the runs are written: a segment's candidate item range is kept
+// only if its first item is the first of the segment and its end the end
+// (each is unique, so stale candidates fail); the buckets then span its
+// items' starts, which include every run start, with about one per
+// kKeysPerBucket items (a valid index for any count).  The run range of
+// each segment (sb, se) is set after the write pass.
 __global__ __launch_bounds__(kSpineSpan) void k_runs_spine2(
     const uint32_t* heads, uint32_t* run0, uint32_t* nruns,
-    const SegSum* inc, SegSum* inc_pre, SegSum* inc_total, int64_t ntiles) {
+    const SegSum* inc, SegSum* inc_pre, SegSum* inc_total, int64_t ntiles,
+    int G, int64_t n, const uint32_t* korder, const uint8_t* gpu,
+    const uint8_t* cls, const int64_t* start, const uint32_t* kcand,
+    BSeg* segs, uint32_t* kr, int64_t btable_cap) {
   __shared__ uint32_t s_h[kSpineWaves + 1];
   __shared__ SegSum s_i[kSpineWaves + 1];
   OpSegSum op;
@@ -227,6 +237,51 @@ __global__ __launch_bounds__(kSpineSpan) void k_runs_spine2(
   if (threadIdx.x == 0 && (int64_t)(blockIdx.x + 1) * kSpineSpan >= ntiles) {
     *nruns = hb + ht;
     *inc_total = op(ib, it);
+  }
+  if (blockIdx.x != 0) return;   // block-uniform
+  const int t = (int)threadIdx.x;
+  BSeg P;
+  P.lo = 0;
+  P.sb = P.se = 0;
+  P.shift = 0;
+  P.nb = 0;
+  P.toff = 0;
+  P.pad = 0;
+  uint32_t ent = 0, kb = 0, ke = 0;
+  if (t < 2 * G && n > 0) {
+    const int64_t cb = kcand[t], ce = kcand[kSegs + t];
+    // every load issued at a clamped position, the checks afterwards
+    const int64_t q[4] = {cb < n ? cb : n - 1,
+                          cb > 0 && cb - 1 < n ? cb - 1 : 0,
+                          ce >= 1 && ce <= n ? ce - 1 : 0,
+                          ce < n ? ce : n - 1};
+    uint32_t r[4], sg[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = korder[q[i]];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      sg[i] = (uint32_t)gpu[r[i]] * 2u + (uint32_t)kind_of(cls[r[i]]);
+    const int64_t lo = start[r[0]], last = start[r[2]];
+    const uint32_t ts = (uint32_t)t;
+    const bool ok = cb < n && ce <= n && ce > cb && sg[0] == ts &&
+                    (cb == 0 || sg[1] != ts) && sg[2] == ts &&
+                    (ce == n || sg[3] != ts);
+    if (ok) {
+      kb = (uint32_t)cb;
+      ke = (uint32_t)ce;
+      P.lo = lo;
+      bi_geometry(lo, last, ce - cb, &P.shift, &P.nb);
+      ent = P.nb + 1;
+    }
+  }
+  uint32_t tot;
+  const uint32_t pre = block_excl_ordered(ent, OpAdd(), 0u, s_h, &tot);
+  if (t < 2 * G) {
+    P.toff = (int64_t)pre < btable_cap ? pre : (uint32_t)btable_cap;
+    if ((int64_t)pre + ent > btable_cap) P.nb = 0;
+    segs[t] = P;
+    kr[t] = kb;
+    kr[kSegs + t] = ke;
   }
 }
 
@@ -320,11 +375,17 @@ __device__ inline void run_items(int64_t n, const uint32_t* korder,
 // whose carry has their first item's segment and reaches its start count
 // again; for the others the first count is exact, since every item of the
 // first segment then starts after the carry.
+// The first pass also clears the bucket table of the run starts (filled by
+// the write pass) and records, for every segment, the korder position of
+// its first item and the end of its items (kcand [2][kSegs]); segments
+// without items keep whatever the array held, so these are candidates that
+// k_runs_spine2 verifies against the items.
 __global__ __launch_bounds__(kBlock) void k_runs_count(
     int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
     const int64_t* start, const int64_t* end, const SegMax* tile_pre,
     SegMax* tile_agg, SegMax* tile_first, uint32_t* tile_heads,
-    SegSum* tile_inc, uint32_t* ranges, uint32_t* mixed) {
+    SegSum* tile_inc, uint32_t* ranges, uint32_t* mixed, uint32_t* kcand,
+    uint32_t* btable, int64_t btable_cap) {
   __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
   // first pass: block 0 clears the segment run and korder ranges and the
   // mixed-streams flag of the bubbles
@@ -332,13 +393,41 @@ __global__ __launch_bounds__(kBlock) void k_runs_count(
     for (int i = threadIdx.x; i < 4 * kSegs; i += kBlock) ranges[i] = 0;
     if (threadIdx.x == 0) *mixed = 0;
   }
+  if (btable) bindex_clear(btable, btable_cap, blockIdx.x, gridDim.x);
   if (tile_pre) {
     const SegMax c = tile_pre[blockIdx.x], f = tile_first[blockIdx.x];
     if (!(c.seg == f.seg && c.val >= f.val)) return;   // block-uniform
   }
+  const int lane0 = lane_id();
+  const int64_t wb0 = (int64_t)blockIdx.x * kOvTile +
+                      (int64_t)(threadIdx.x / kWave) * kWaveTile;
+  // segment of the item before the wave's first (for the boundaries)
+  uint32_t sprev = kNone;
+  if (kcand && lane0 == 0 && wb0 > 0 && wb0 <= n) {
+    const uint32_t r = korder[wb0 - 1];
+    sprev = (uint32_t)gpu[r] * 2u + (uint32_t)kind_of(cls[r]);
+  }
   RunItems it;
   run_items(n, korder, gpu, cls, start, end, tile_pre,
             s_slice[threadIdx.x / kWave], it);
+  if (kcand) {
+    // item p (blocked: wb0 + lane * 8 + j) starts a segment when its
+    // predecessor's differs; the predecessor of a lane's first item is the
+    // lane below's last (lane 0: the item before the wave)
+    const uint32_t ps = wave_shr1_u32(sprev, it.seg[kTileIpt - 1]);
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      const int64_t p = wb0 + (int64_t)lane0 * kTileIpt + j;
+      if (p >= n) break;
+      const uint32_t pv = j ? it.seg[j - 1] : ps;
+      const uint32_t sj = it.seg[j];
+      if (p == 0 || pv != sj) {
+        if (sj < (uint32_t)kSegs) kcand[sj] = (uint32_t)p;
+        if (p > 0 && pv < (uint32_t)kSegs) kcand[kSegs + pv] = (uint32_t)p;
+      }
+      if (p == n - 1 && sj < (uint32_t)kSegs) kcand[kSegs + sj] = (uint32_t)n;
+    }
+  }
   OpSegSum op;
   SegSum acc = segsum_ident();
 #pragma unroll
@@ -378,19 +467,40 @@ __global__ __launch_bounds__(kBlock) void k_runs_count(
     tile_first[blockIdx.x] = SegMax{it.seg[0], it.s[0]};
 }
 
-// Writes the runs: start, segment and union length before the run (the
-// prefix of the segment's run lengths); every head closes the previous run
-// at the running maximum, and segment starts record the run ranges.
+// Writes the runs: start and union length before the run (the prefix of
+// the segment's run lengths); every head closes the previous run at the
+// running maximum, and segment starts record the run ranges.  Also fills
+// the bucket index of the run starts (parameters from k_runs_spine2, table
+// cleared by the first count pass) from the items: item p of segment S
+// writes the entries of the buckets after its predecessor's start up to its
+// own start with the number of the first run at or after p (the first run
+// whose start reaches a bucket's lower bound), the segment's first item
+// from bucket 0, its last item also the entries after its start with the
+// segment's run end.  Over the items of S these are the entries that each
+// run start and the segment's end write in a build from the run starts.
 __global__ __launch_bounds__(kBlock) void k_runs_write(
     int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
     const int64_t* start, const int64_t* end, const SegMax* tile_pre,
     const uint32_t* tile_run0, const SegSum* tile_inc0, const uint32_t* nruns,
     const SegMax* grand, int64_t* rs, int64_t* re, int64_t* pl,
-    uint32_t* rseg, uint32_t* rhead, uint32_t* rbeg, uint32_t* rend,
-    uint32_t* btable, int64_t btable_cap) {
+    uint32_t* rhead, uint32_t* rbeg, uint32_t* rend, int G,
+    const BSeg* bsegs, const uint32_t* kr, uint32_t* btable) {
   __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
-  // the bucket index table, built right after this pass, starts unset
-  bindex_clear(btable, btable_cap, blockIdx.x, gridDim.x);
+  // dynamic LDS: the 2G segments' bucket parameters, then their first item
+  // positions and item ends
+  extern __shared__ BSeg s_seg[];
+  uint32_t* s_kr = reinterpret_cast<uint32_t*>(s_seg + 2 * G);
+  for (int i = threadIdx.x; i < 2 * G; i += kBlock) {
+    s_seg[i] = bsegs[i];
+    s_kr[i] = kr[i];
+    s_kr[2 * G + i] = kr[kSegs + i];
+  }
+  // (visible after the block barrier in run_items)
+  // start of the item before the wave's first
+  const int64_t wb0 = (int64_t)blockIdx.x * kOvTile +
+                      (int64_t)(threadIdx.x / kWave) * kWaveTile;
+  int64_t sbefore = 0;
+  if (lane_id() == 0 && wb0 > 0 && wb0 <= n) sbefore = start[korder[wb0 - 1]];
   RunItems it;
   run_items(n, korder, gpu, cls, start, end, tile_pre,
             s_slice[threadIdx.x / kWave], it);
@@ -469,7 +579,6 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
     for (uint32_t q = lane; q < H; q += kWave) dst[q] = sl[q];
     wave_sync();
   };
-  emit(it.s, rs + r0);
   emit(vpl, pl + r0);
   {
     // every head closes the previous run at the running maximum; the
@@ -483,6 +592,27 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
       if (r0 + q > 0) re[r0 + q - 1] = sl2[q];
     wave_sync();
   }
+  emit(it.s, rs + r0);
+  // bucket entries of the run starts (blocked items: the predecessor of a
+  // lane's first item is the lane below's last, lane 0's the item before
+  // the wave)
+  const int64_t sprev =
+      (int64_t)wave_shr1((uint64_t)sbefore, (uint64_t)it.s[kTileIpt - 1]);
+#pragma unroll
+  for (int j = 0; j < kTileIpt; ++j) {
+    if (!((it.m_valid >> j) & 1u) || it.seg[j] >= (uint32_t)(2 * G)) continue;
+    const uint32_t S = it.seg[j];
+    const BSeg P = s_seg[S];
+    if (P.nb == 0) continue;
+    const int64_t p = wbase + (int64_t)lane * kTileIpt + j;
+    const int64_t bi = bi_bucket(P, it.s[j]);
+    const int64_t bp =
+        p == (int64_t)s_kr[S] ? -1 : bi_bucket(P, j ? it.s[j - 1] : sprev);
+    const uint32_t v = r0 + k[j];
+    bi_fill_range(btable, P, bp, bi, v);
+    if (p == (int64_t)s_kr[2 * G + S] - 1)
+      bi_fill_range(btable, P, bi, P.nb, v + ((it.m_head >> j) & 1u));
+  }
   {
     // segments, and the korder position of the head of every
     // communication run
@@ -495,11 +625,8 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
         sp[k[j]] = (uint32_t)(wbase + (int64_t)lane * kTileIpt + j);
       }
     wave_sync();
-    for (uint32_t q = lane; q < H; q += kWave) {
-      const uint32_t sg = su[q];
-      rseg[r0 + q] = sg;
-      if (sg & 1u) rhead[r0 + q] = sp[q];
-    }
+    for (uint32_t q = lane; q < H; q += kWave)
+      if (su[q] & 1u) rhead[r0 + q] = sp[q];
     wave_sync();
   }
 }
@@ -579,14 +706,25 @@ __device__ inline void comm_offsets(int G, const BSeg* seg,
     }
 }
 
+// Also completes the segment parameters of the run index with the run
+// ranges of the write pass (every block in LDS, block 0 in memory for the
+// later passes; the other fields are the same in both).
 __global__ __launch_bounds__(kBlock) void k_runs_comm_overlap(
     Runs R, int G, const uint32_t* kbeg, const uint32_t* kend, uint32_t* voff,
     uint32_t* roff, int64_t* ovc, int64_t* fcrs, const uint32_t* korder,
-    const uint32_t* rhead, int64_t* ovl, uint8_t* cdone) {
+    const uint32_t* rhead, int64_t* ovl, uint8_t* cdone, BSeg* segs_w,
+    const uint32_t* rbeg, const uint32_t* rend) {
   extern __shared__ BSeg s_seg[];   // 2G entries (dynamic LDS)
   __shared__ uint32_t s_voff[kSegs / 2 + 1];
   __shared__ uint32_t s_roff[kSegs / 2 + 1];
-  segs_to_lds(s_seg, R.X.seg, 2 * G);
+  for (int i = threadIdx.x; i < 2 * G; i += kBlock) {
+    BSeg P = R.X.seg[i];
+    P.sb = rbeg[i];
+    P.se = rend[i];
+    s_seg[i] = P;
+    if (blockIdx.x == 0) segs_w[i] = P;
+  }
+  __syncthreads();
   comm_offsets(G, s_seg, kbeg, kend, s_voff, s_roff, voff, roff);
   const int64_t total = s_voff[G];
   for (int64_t v = (int64_t)blockIdx.x * kBlock + threadIdx.x; v < total;
@@ -1009,7 +1147,8 @@ struct OverlapLayout {
   uint32_t* scan_u32;
   int64_t* rs;
   int64_t* re;
-  uint32_t* rseg;
+  uint32_t* kcand;    // [2][kSegs] candidate item ranges of the segments
+  uint32_t* kr;       // [2][kSegs] verified item ranges
   uint32_t* rhead;    // korder position of the head of each comm run
   uint8_t* cdone;     // comm record (dense index) done with its run
   uint32_t* mixed;    // some GPU's compute records on several streams
@@ -1045,7 +1184,8 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   L.scan_u32 = sc.take<uint32_t>(scan_scratch_elems(L.ntiles));
   L.rs = sc.take<int64_t>(n);
   L.re = sc.take<int64_t>(n);
-  L.rseg = sc.take<uint32_t>(n);
+  L.kcand = sc.take<uint32_t>(2 * kSegs);
+  L.kr = sc.take<uint32_t>(2 * kSegs);
   L.rhead = sc.take<uint32_t>(n);
   L.cdone = sc.take<uint8_t>(n);
   L.mixed = sc.take<uint32_t>(1);
@@ -1107,7 +1247,8 @@ extern "C" int chopper_overlap(const chopper_records* rec,
     CHOPPER_HIP(launch("ov_runs_count", k_runs_count, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
                        (const SegMax*)nullptr, L.tile_agg, L.tile_first,
-                       L.tile_heads, L.tile_inc, L.rbeg, L.mixed));
+                       L.tile_heads, L.tile_inc, L.rbeg, L.mixed, L.kcand,
+                       L.btable, L.btable_cap));
     const dim3 sg((unsigned)ceil_div(L.ntiles, (int64_t)kSpineSpan));
     CHOPPER_HIP(launch("ov_runs_spine", k_tile_spine<SegMax, OpSegMax>, sg,
                        dim3(kSpineSpan), s, (const SegMax*)L.tile_agg,
@@ -1116,23 +1257,33 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
                        (const SegMax*)L.tile_pre, (SegMax*)nullptr,
                        L.tile_first, L.tile_heads, L.tile_inc,
-                       (uint32_t*)nullptr, (uint32_t*)nullptr));
+                       (uint32_t*)nullptr, (uint32_t*)nullptr,
+                       (uint32_t*)nullptr, (uint32_t*)nullptr, (int64_t)0));
     CHOPPER_HIP(launch("ov_runs_inc_spine", k_runs_spine2, sg,
                        dim3(kSpineSpan), s, (const uint32_t*)L.tile_heads,
                        L.tile_run0, L.nruns, (const SegSum*)L.tile_inc,
-                       L.tile_incp, L.inc_total, L.ntiles));
-    CHOPPER_HIP(launch("ov_runs_write", k_runs_write, dim3(T), dim3(kBlock), s,
-                       n, korder, rec->gpu, rec->cls, start_al, end_al,
-                       (const SegMax*)L.tile_pre, (const uint32_t*)L.tile_run0,
-                       (const SegSum*)L.tile_incp, (const uint32_t*)L.nruns,
-                       (const SegMax*)L.grand, L.rs, L.re, L.pl, L.rseg,
-                       L.rhead, L.rbeg, L.rend, L.btable, L.btable_cap));
+                       L.tile_incp, L.inc_total, L.ntiles, G, n, korder,
+                       rec->gpu, rec->cls, start_al, (const uint32_t*)L.kcand,
+                       L.bsegs, L.kr, L.btable_cap));
+    // (the write pass also fills the bucket index of the run starts)
+    CHOPPER_HIP(launch_shm("ov_runs_write", k_runs_write, dim3(T),
+                           dim3(kBlock),
+                           sizeof(BSeg) * (size_t)(2 * G) +
+                               sizeof(uint32_t) * (size_t)(4 * G),
+                           s, n, korder, rec->gpu, rec->cls, start_al, end_al,
+                           (const SegMax*)L.tile_pre,
+                           (const uint32_t*)L.tile_run0,
+                           (const SegSum*)L.tile_incp,
+                           (const uint32_t*)L.nruns, (const SegMax*)L.grand,
+                           L.rs, L.re, L.pl, L.rhead, L.rbeg, L.rend, G,
+                           (const BSeg*)L.bsegs, (const uint32_t*)L.kr,
+                           L.btable));
+  } else {
+    // no runs: empty segments
+    CHOPPER_HIP(bindex_build(L.rs, (const uint32_t*)nullptr, 0, nullptr,
+                             L.rbeg, L.rend, 1, kSegs, L.bsegs, L.btable,
+                             L.btable_cap, L.btmp, s, false));
   }
-  // bucket index of the run starts of every (gpu, kind) (the write pass
-  // cleared its table)
-  CHOPPER_HIP(bindex_build(L.rs, L.rseg, n, L.nruns, L.rbeg, L.rend, 1, kSegs,
-                           L.bsegs, L.btable, L.btable_cap, L.btmp, s,
-                           n > 0));
   Runs R{L.rs, L.re, L.pl, L.pov, L.ovc, L.fcrs, L.voff,
          BIndex{L.rs, L.bsegs, L.btable}};
   // the query kernels hold the 2G segment parameters in LDS
@@ -1146,7 +1297,8 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                          (const uint32_t*)(L.rbeg + 2 * kSegs),
                          (const uint32_t*)(L.rbeg + 3 * kSegs), L.voff, L.roff,
                          L.ovc, L.fcrs, korder, (const uint32_t*)L.rhead,
-                         ovl_out, L.cdone));
+                         ovl_out, L.cdone, L.bsegs, (const uint32_t*)L.rbeg,
+                         (const uint32_t*)L.rend));
 
   if (n > 0) {
 
