@@ -18,38 +18,44 @@ namespace chopper {
 bool validate_records(const chopper_records* r);
 bool validate_markers(const chopper_markers* m);
 
-// sorted marker columns and the (gpu, level) segment of every non-empty
-// marker (kNone for empty or invalid ones)
+// sorted marker columns (when the class partition did not write them)
 __global__ __launch_bounds__(kBlock) void k_marker_gather(
-    int64_t nm, KeyMarker km, const uint32_t* mord, const int64_t* ms,
-    const int64_t* me, int64_t* sms, int64_t* sme, uint32_t* sid,
-    uint32_t* sseg, uint32_t* btable, int64_t btable_cap) {
-  // the bucket index table, built after the links pass, starts unset
-  bindex_clear(btable, btable_cap, blockIdx.x, gridDim.x);
+    int64_t nm, const uint32_t* mord, const int64_t* ms, const int64_t* me,
+    int64_t* sms, int64_t* sme, uint32_t* sid) {
   int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (p >= nm) return;
   uint32_t j = mord[p];
   sms[p] = ms[j];
   sme[p] = me[j];
   sid[p] = j;
-  const uint32_t c = km.cls(j);
-  sseg[p] = ((c & 1u) || c >= (uint32_t)(km.G * km.D * 2)) ? kNone : c >> 1;
 }
 
-// overlap check between neighbours of a (gpu, level) segment
+// Overlap check between neighbours of a (gpu, level) segment and, with a
+// table, the fill of the bucket index of the segment's marker starts
+// (parameters and cleared table from bindex_prepare): every marker writes
+// the entries between its predecessor's bucket and its own.
 __global__ __launch_bounds__(kBlock) void k_marker_links(
     int G, int D, const uint32_t* coff, const int64_t* sms, const int64_t* sme,
-    uint32_t* status) {
+    uint32_t* status, const BSeg* bsegs, uint32_t* btable) {
   // one block column per (gpu, level) segment
   const int seg = blockIdx.y;          // g * D + l
   const uint32_t cls = (uint32_t)seg * 2u;
   const int64_t b = coff[cls], e = coff[cls + 1];
   (void)G;
   (void)D;
+  BSeg P;
+  P.nb = 0;
+  if (btable) P = bsegs[seg];
   bool ov = false;
   for (int64_t p = b + (int64_t)blockIdx.x * kBlock + threadIdx.x; p < e;
        p += (int64_t)gridDim.x * kBlock) {
     if (p + 1 < e && sme[p] > sms[p + 1]) ov = true;
+    if (P.nb != 0) {
+      const int64_t bi = bi_bucket(P, sms[p]);
+      const int64_t bp = p == (int64_t)P.sb ? -1 : bi_bucket(P, sms[p - 1]);
+      bi_fill_range(btable, P, bp, bi, (uint32_t)p);
+      if (p == (int64_t)P.se - 1) bi_fill_range(btable, P, bi, P.nb, P.se);
+    }
   }
   if (__ballot(ov) != 0 && (threadIdx.x & (kWave - 1)) == 0)
     atomicOr(status, (uint32_t)CHOPPER_ST_MARKER_OVERLAP);
@@ -324,7 +330,6 @@ struct AttrLayout {
   int64_t* sms;
   int64_t* sme;
   uint32_t* sid;
-  uint32_t* sseg;
   BSeg* bsegs;
   uint32_t* btable;
   int64_t btable_cap;
@@ -347,7 +352,6 @@ static AttrLayout attr_layout(Scratch& sc, int64_t n, int64_t nm, int G,
   L.sms = sc.take<int64_t>(nm);
   L.sme = sc.take<int64_t>(nm);
   L.sid = sc.take<uint32_t>(nm);
-  L.sseg = sc.take<uint32_t>(nm);
   L.bsegs = sc.take<BSeg>((int64_t)G * D);
   L.btable_cap = bindex_table_cap(nm, (int64_t)G * D);
   L.btable = sc.take<uint32_t>(L.btable_cap);
@@ -385,8 +389,7 @@ extern "C" int chopper_attribute(const chopper_records* rec,
   bool range_err = false;
   // markers in start order (the usual case): the class partition writes the
   // sorted columns itself
-  const MarkerColumns cols{mstart_al, mend_al, L.sms, L.sme, L.sid, L.sseg,
-                           G, D};
+  const MarkerColumns cols{mstart_al, mend_al, L.sms, L.sme, L.sid};
   bool gathered = false;
   rc = class_sort(km, L.sort, L.mord, L.coff, &range_err, s, -1, cols,
                   &gathered);
@@ -394,12 +397,18 @@ extern "C" int chopper_attribute(const chopper_records* rec,
   if (range_err)
     CHOPPER_HIP(launch("status_set", k_status_set, dim3(1), dim3(1), s,
                        (uint32_t)CHOPPER_ST_RANGE, status));
+  // the bucket index of the non-empty marker starts of every (gpu, level)
+  // is needed when there are records to attribute; the links pass fills it
+  const bool index = n > 0 && D > 0;
+  if (nm > 0 && !gathered)
+    CHOPPER_HIP(launch("attr_marker_gather", k_marker_gather,
+                       grid_for(nm, kBlock), dim3(kBlock), s, nm,
+                       (const uint32_t*)L.mord, mstart_al, mend_al, L.sms,
+                       L.sme, L.sid));
+  if (index)
+    CHOPPER_HIP(bindex_prepare(L.sms, L.coff, L.coff + 1, 2, G * D, L.bsegs,
+                               L.btable, L.btable_cap, L.btmp, s));
   if (nm > 0) {
-    if (!gathered)
-      CHOPPER_HIP(launch("attr_marker_gather", k_marker_gather,
-                         grid_for(nm, kBlock), dim3(kBlock), s, nm, km,
-                         (const uint32_t*)L.mord, mstart_al, mend_al, L.sms,
-                         L.sme, L.sid, L.sseg, L.btable, L.btable_cap));
     const int64_t per_seg = ceil_div(nm, (int64_t)G * D);
     unsigned gx = (unsigned)ceil_div(per_seg, kBlock);
     if (gx < 1) gx = 1;
@@ -407,14 +416,11 @@ extern "C" int chopper_attribute(const chopper_records* rec,
     CHOPPER_HIP(launch("attr_marker_links", k_marker_links,
                        dim3(gx, (unsigned)(G * D)), dim3(kBlock), s, G, D,
                        (const uint32_t*)L.coff, (const int64_t*)L.sms,
-                       (const int64_t*)L.sme, status));
+                       (const int64_t*)L.sme, status,
+                       (const BSeg*)L.bsegs,
+                       index ? L.btable : (uint32_t*)nullptr));
   }
-  if (n == 0 || D == 0) return CHOPPER_OK;
-  // bucket index of the non-empty marker starts of every (gpu, level) (the
-  // gather pass, when it ran, cleared the table)
-  CHOPPER_HIP(bindex_build(L.sms, L.sseg, nm, nullptr, L.coff, L.coff + 1, 2,
-                           G * D, L.bsegs, L.btable, L.btable_cap, L.btmp, s,
-                           nm > 0 && !gathered));
+  if (!index) return CHOPPER_OK;
   const BIndex X{L.sms, L.bsegs, L.btable};
   const unsigned grid = (unsigned)ceil_div(n, (int64_t)kWaveTile * kWavesPerBlock);
   CHOPPER_HIP(launch("attr_windows", k_attr_windows,

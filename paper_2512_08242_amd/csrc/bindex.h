@@ -159,6 +159,16 @@ hipError_t bindex_build(const int64_t* key, const uint32_t* keyseg,
                         int64_t table_cap, uint32_t* tmp, hipStream_t s,
                         bool cleared = false);
 
+// The index without its fill: segment parameters and a cleared table, in
+// one launch (block 0 computes the parameters while every block clears).
+// The caller then fills the table, every key i of segment P (bucket bi,
+// its predecessor's bp) with bi_fill_range(table, P, bp, bi, i), the
+// segment's last key also bi_fill_range(table, P, bi, P.nb, P.se).
+hipError_t bindex_prepare(const int64_t* key, const uint32_t* sbeg,
+                          const uint32_t* send, int stride, int nseg,
+                          BSeg* segs, uint32_t* table, int64_t table_cap,
+                          uint32_t* tmp, hipStream_t s);
+
 // Part of a grid-stride clear of the table that a kernel of any grid can
 // take on: block b of nb clears its share.
 __device__ inline void bindex_clear(uint32_t* table, int64_t cap, int64_t b,

@@ -21,10 +21,17 @@ int64_t bindex_table_cap(int64_t nkeys, int64_t nseg) {
 // smallest power of two with at most ceil(count / 4) buckets over the key
 // span, bucket count) and the exclusive scan of the table sizes; segments
 // that would not fit the table keep no table and are searched whole.
+// With `clear`, every block of the grid first clears its share of the
+// whole table (block 0 then computes the parameters).
 __global__ __launch_bounds__(1024) void k_bi_params(
     const int64_t* key, const uint32_t* sbeg, const uint32_t* send, int stride,
-    int nseg, BSeg* segs, int64_t cap, uint32_t* total) {
+    int nseg, BSeg* segs, int64_t cap, uint32_t* total, uint32_t* clear) {
   __shared__ uint32_t s_w[1024 / kWave];
+  if (clear)
+    for (int64_t e = (int64_t)blockIdx.x * 1024 + threadIdx.x; e < cap;
+         e += (int64_t)gridDim.x * 1024)
+      clear[e] = kUnset;
+  if (blockIdx.x != 0) return;   // block-uniform
   const int lane = lane_id(), w = (int)(threadIdx.x / kWave);
   uint64_t carry = 0;
   for (int base = 0; base < nseg; base += 1024) {
@@ -143,7 +150,7 @@ hipError_t bindex_build(const int64_t* key, const uint32_t* keyseg,
   uint32_t* total = tmp + nseg;
   hipError_t e;
   e = launch("bi_params", k_bi_params, dim3(1), dim3(1024), s, key, sbeg, send,
-             stride, nseg, segs, table_cap, total);
+             stride, nseg, segs, table_cap, total, (uint32_t*)nullptr);
   if (e != hipSuccess) return e;
   if (!cleared) {
     e = launch("bi_clear", k_bi_clear, grid_for(table_cap, kBlock),
@@ -157,6 +164,18 @@ hipError_t bindex_build(const int64_t* key, const uint32_t* keyseg,
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+hipError_t bindex_prepare(const int64_t* key, const uint32_t* sbeg,
+                          const uint32_t* send, int stride, int nseg,
+                          BSeg* segs, uint32_t* table, int64_t table_cap,
+                          uint32_t* tmp, hipStream_t s) {
+  if (nseg <= 0) return hipSuccess;
+  int64_t gx = ceil_div(table_cap, (int64_t)1024 * 4);
+  gx = gx < 1 ? 1 : (gx > 1024 ? 1024 : gx);
+  return launch("bi_params", k_bi_params, dim3((unsigned)gx), dim3(1024), s,
+                key, sbeg, send, stride, nseg, segs, table_cap, tmp + nseg,
+                table);
 }
 
 }  // namespace chopper

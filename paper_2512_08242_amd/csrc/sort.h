@@ -152,21 +152,17 @@ struct NoColumns {
   __device__ void put(int64_t, uint32_t, uint32_t) const {}
 };
 
-// The markers' sorted columns: start', end', input index and (gpu, level)
-// segment (kNone for empty markers and markers of no valid gpu or level).
+// The markers' sorted columns: start', end' and input index.
 struct MarkerColumns {
   const int64_t* ms;
   const int64_t* me;
   int64_t* sms;
   int64_t* sme;
   uint32_t* sid;
-  uint32_t* sseg;
-  int G, D;
-  __device__ void put(int64_t p, uint32_t i, uint32_t c) const {
+  __device__ void put(int64_t p, uint32_t i, uint32_t) const {
     sms[p] = ms[i];
     sme[p] = me[i];
     sid[p] = i;
-    sseg[p] = ((c & 1u) || c >= (uint32_t)(G * D * 2)) ? kNone : c >> 1;
   }
 };
 
