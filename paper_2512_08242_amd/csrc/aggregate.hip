@@ -884,6 +884,9 @@ struct NatGeom {
   int64_t nnt;          // natural tiles
   int64_t lps;          // row stride of lp (nnt rounded up to kLpIpt)
   int G;
+  // the fast-path flags, for a launch queued before the host has read them:
+  // it does nothing unless flags[0] and flags[2] are both zero
+  const uint32_t* fflags = nullptr;
 };
 
 struct NatTile {
@@ -1412,6 +1415,11 @@ __global__ __launch_bounds__(kBlock) void k_agg_fast_reduce(
   const int wv = (int)(threadIdx.x / kWave);
   const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + wv;
   if (w >= nwt) return;
+  if constexpr (kNat) {
+    if (N.fflags && __builtin_amdgcn_readfirstlane(
+                        (int)(N.fflags[0] | N.fflags[2])) != 0)
+      return;
+  }
   int64_t base;
   int tile_n;
   NatTile NT;
@@ -2166,14 +2174,51 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
   FromRecords fr{S};
   const NatGeom N{L.gtb, L.tg, L.gs, L.ge, L.lp, L.hflags + 2, Th, L.lps, G};
   const NatGeom none{};
+  // the records reduction on the natural tiles: level li and, with `two`,
+  // li - 1
+  auto nat_records = [&](const NatGeom& NG, int li, bool two) -> int {
+    const uint32_t* tb = L.ntb + (int64_t)li * L.nstride;
+    const dim3 grid((unsigned)ceil_div(NW, (int64_t)kWavesPerBlock));
+    if (two)
+      CHOPPER_HIP(launch("agg_fast_reduce_records",
+                         k_agg_fast_reduce<kMD, FromRecords, true, true>,
+                         grid, dim3(kBlock), s, fr, NG, li, D, M, tb,
+                         (const uint32_t*)(tb - L.nstride),
+                         (const int64_t*)nullptr, R, ovf, NW));
+    else
+      CHOPPER_HIP(launch("agg_fast_reduce_records",
+                         k_agg_fast_reduce<kMD, FromRecords, false, true>,
+                         grid, dim3(kBlock), s, fr, NG, li, D, M, tb,
+                         (const uint32_t*)nullptr, (const int64_t*)nullptr,
+                         R, ovf, NW));
+    return CHOPPER_OK;
+  };
+  // the level the records reduce to (with li0 - 1 when two0)
+  const int li0 = level == CHOPPER_LEVEL_ALL
+                      ? (D > 0 ? D - 1 : D)
+                      : (level == CHOPPER_LEVEL_GPU ? D : level);
+  const bool two0 = level == CHOPPER_LEVEL_ALL && D >= 2;
+  bool spec = false;   // the natural-tile records reduction is queued
   // the fast-path flags and the level offsets (row counts per level size
-  // the launches of the coarser levels)
+  // the launches of the coarser levels); with `speculate` the natural-tile
+  // records reduction, which needs none of them, is queued before the wait
+  // and exits on the device unless the flags let it run
   uint32_t hf[3] = {1u, 0u, 1u};
   int64_t lo_h[kMaxLevels + 1];
-  auto fetch_stage = [&]() -> int {
+  auto fetch_stage = [&](bool speculate) -> int {
     int64_t st[3 + kMaxLevels + 1];
-    CHOPPER_HIP(read_back(L.stage, st,
-                          sizeof(int64_t) * (size_t)(3 + Lv + 1), s));
+    ReadBack rb;
+    CHOPPER_HIP(read_back_start(L.stage,
+                                sizeof(int64_t) * (size_t)(3 + Lv + 1), s,
+                                &rb));
+    if (speculate) {
+      NatGeom NS = N;
+      NS.fflags = L.hflags;
+      const int r = nat_records(NS, li0, two0);
+      if (r != CHOPPER_OK) return r;
+      spec = true;
+    }
+    CHOPPER_HIP(read_back_finish(&rb, st));
     for (int i = 0; i < 3; ++i) hf[i] = (uint32_t)st[i];
     for (int i = 0; i <= Lv; ++i) lo_h[i] = st[3 + i];
     return CHOPPER_OK;
@@ -2200,7 +2245,7 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                      (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
                      want_workload, rows->cap, rows->level_offset, L.stage,
                      status));
-  rc = fetch_stage();
+  rc = fetch_stage(true);
   if (rc != CHOPPER_OK) return rc;
   const bool nat = hf[2] == 0;
   if (!nat) {
@@ -2217,7 +2262,7 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                        (const uint32_t*)L.htotal, (const uint32_t*)L.hflags,
                        want_workload, rows->cap, rows->level_offset, L.stage,
                        status));
-    rc = fetch_stage();
+    rc = fetch_stage(false);
     if (rc != CHOPPER_OK) return rc;
   }
   auto level_rows = [&](int li) -> int64_t {
@@ -2231,20 +2276,11 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
     if (finer < 0) {
       int64_t ns;
       if (nat) {
-        const uint32_t* tb = L.ntb + (int64_t)li * L.nstride;
-        const dim3 grid((unsigned)ceil_div(NW, (int64_t)kWavesPerBlock));
-        if (two)
-          CHOPPER_HIP(launch("agg_fast_reduce_records",
-                             k_agg_fast_reduce<kMD, FromRecords, true, true>,
-                             grid, dim3(kBlock), s, fr, N, li, D, M, tb,
-                             (const uint32_t*)(tb - L.nstride),
-                             (const int64_t*)nullptr, R, ovf, NW));
-        else
-          CHOPPER_HIP(launch("agg_fast_reduce_records",
-                             k_agg_fast_reduce<kMD, FromRecords, false, true>,
-                             grid, dim3(kBlock), s, fr, N, li, D, M, tb,
-                             (const uint32_t*)nullptr,
-                             (const int64_t*)nullptr, R, ovf, NW));
+        // (queued before the flags were read, when they allowed it)
+        if (!(spec && li == li0 && two == two0)) {
+          const int r = nat_records(N, li, two);
+          if (r != CHOPPER_OK) return r;
+        }
         ns = (two ? 4 : 2) * NW;
       } else {
         const uint32_t* tb = L.htb + (int64_t)li * Th;

@@ -423,13 +423,16 @@ extern "C" int chopper_align(const chopper_records* rec,
     cd[g] = ClockDev{clocks[g].x0, clocks[g].c, clocks[g].d_q48};
   CHOPPER_HIP(hipMemcpyAsync(L.clk, cd.data(), sizeof(ClockDev) * G,
                              hipMemcpyHostToDevice, s));
-  if (nm > 0) {
-    CHOPPER_HIP(launch("align_transform_markers", k_transform_markers,
-                       grid_for(nm, kBlock), dim3(kBlock), s, nm, G, mk->depth,
-                       mk->gpu, mk->level, mk->start_ns, mk->end_ns,
-                       (const ClockDev*)L.clk, mstart_out, mend_out, status));
-  }
-  if (n == 0) return CHOPPER_OK;
+  auto markers = [&]() -> int {
+    if (nm > 0)
+      CHOPPER_HIP(launch("align_transform_markers", k_transform_markers,
+                         grid_for(nm, kBlock), dim3(kBlock), s, nm, G,
+                         mk->depth, mk->gpu, mk->level, mk->start_ns,
+                         mk->end_ns, (const ClockDev*)L.clk, mstart_out,
+                         mend_out, status));
+    return CHOPPER_OK;
+  };
+  if (n == 0) return markers();
   CHOPPER_HIP(launch("align_fill", k_align_clear,
                      grid_for(16384 + 128, kBlock), dim3(kBlock), s,
                      reinterpret_cast<uint32_t*>(L.pres_s), L.counts));
@@ -443,8 +446,16 @@ extern "C" int chopper_align(const chopper_records* rec,
   CHOPPER_HIP(launch("align_dense_classes", k_dense_classes, dim3(1),
                      dim3(kDenseThreads), s, (const uint8_t*)L.pres_s, L.cmap_s,
                      (const uint8_t*)L.pres_k, L.cmap_k, L.counts));
+  // the markers are transformed while the host waits for the class counts
   uint32_t counts[3];
-  CHOPPER_HIP(read_back(L.counts, counts, sizeof(counts), s));
+  ReadBack rb;
+  CHOPPER_HIP(read_back_start(L.counts, sizeof(counts), s, &rb));
+  rc = markers();
+  if (rc != CHOPPER_OK) {
+    (void)read_back_finish(&rb, counts);
+    return rc;
+  }
+  CHOPPER_HIP(read_back_finish(&rb, counts));
   // counts[2] != 0: the input is not ordered by (gpu, start')
   const int known = counts[2] ? -1 : 1;
   bool range_err = false, r2 = false;

@@ -161,13 +161,34 @@ inline hipError_t launch(const char* name, Kern kern, dim3 grid, dim3 block,
   return e;
 }
 
-// Copies `bytes` (a multiple of 4, at most 4 KiB) of device memory at `dev`
-// to `host` once the work queued on `s` before it is done, and returns when
-// they are there.  A one-block kernel stores them into pinned memory of the
-// calling host thread (allocated on its first use, kept for the life of the
-// process) and the host polls the stream, which avoids a copy launch and the
-// runtime's blocking wait.  Callers on one host thread are serialized by it.
+// Copies `bytes` of device memory at `dev` to `host` once the work queued
+// on `s` before it is done, and returns when they are there (polling, not
+// the runtime's blocking wait).
 hipError_t read_back(const void* dev, void* host, size_t bytes, hipStream_t s);
+
+// The same in two halves: read_back_start queues the copy (at most
+// kReadBackMax bytes) into pinned memory that the library keeps and records
+// an event after it; work queued on `s` afterwards runs while the host
+// waits in read_back_finish, which polls that event only and then copies
+// the value to `host`.  Every start is followed by one finish on the same
+// host thread.  Without a free pinned slot the copy is done at once by
+// read_back_start (the stream drained), and the finish only hands it over.
+// A read-back left unfinished (an early error return) waits for its copy
+// and frees its slot when it goes out of scope.
+constexpr size_t kReadBackMax = 256;
+struct ReadBack {
+  void* slot = nullptr;
+  size_t bytes = 0;
+  hipError_t err = hipSuccess;
+  alignas(8) unsigned char now[kReadBackMax];
+  ReadBack() = default;
+  ReadBack(const ReadBack&) = delete;
+  ReadBack& operator=(const ReadBack&) = delete;
+  ~ReadBack();
+};
+hipError_t read_back_start(const void* dev, size_t bytes, hipStream_t s,
+                           ReadBack* rb);
+hipError_t read_back_finish(ReadBack* rb, void* host);
 
 // the same as launch() with `shm` bytes of dynamic LDS
 template <typename Kern, typename... Args>

@@ -415,16 +415,17 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
   }
   bool sorted = false;
   if (C <= 256) {
+    // cheap sufficient test on the input, ordered by (major, time); its
+    // read-back is waited for after the partition is queued, which runs
+    // either way
+    ReadBack rb;
     if (known_sorted < 0) {
-      // cheap sufficient test on the input: ordered by (major, time)
       CHOPPER_HIP(launch("sort_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
                          L.flag, (int64_t)1, 0u));
       CHOPPER_HIP(launch("sort_major_sorted", k_major_sorted<Acc>,
                          grid_for(n, kBlock * 8), dim3(kBlock), s, acc, n,
                          L.flag));
-      uint32_t unsorted = 1;
-      CHOPPER_HIP(read_back(L.flag, &unsorted, sizeof(uint32_t), s));
-      if (unsorted == 0) known_sorted = 1;
+      CHOPPER_HIP(read_back_start(L.flag, sizeof(uint32_t), s, &rb));
     }
     CHOPPER_HIP(launch("sort_class_hist", k_class_hist<Acc>, dim3((unsigned)T),
                        dim3(kBlock), s, acc, n, T, L.tilehist));
@@ -433,6 +434,11 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
     CHOPPER_HIP(launch("sort_class_partition", k_class_partition<Acc, Cols>,
                        dim3((unsigned)T), dim3(kBlock), s, acc, n, T,
                        (const uint32_t*)L.tileoff, out, coff, cols));
+    if (known_sorted < 0) {
+      uint32_t unsorted = 1;
+      CHOPPER_HIP(read_back_finish(&rb, &unsorted));
+      if (unsorted == 0) known_sorted = 1;
+    }
     if (known_sorted == 1) {
       sorted = true;
     } else {
