@@ -21,6 +21,8 @@
 // The finest level reads the records (counters exactly once); each coarser
 // level reads the rows of the level below.  GPU and workload rows, which
 // are few, accumulate with atomics.
+#include <type_traits>
+
 #include "sort.h"
 #include "wave.h"
 
@@ -692,6 +694,19 @@ __device__ inline uint32_t slot_key(uint32_t slot, int64_t M, uint32_t gk) {
   return slot * 2u + (gk & 1u);
 }
 
+// The same as selects: m2 = (uint32_t)(2 M) and mlim = min(M, 2^32 - 1)
+// (so that slot >= mlim iff slot >= M for every slot below kNone).
+struct SlotKeys {
+  uint32_t m2, mlim;
+  __device__ explicit SlotKeys(int64_t M)
+      : m2((uint32_t)(2 * M)),
+        mlim(M >= (int64_t)kNone ? kNone : (uint32_t)M) {}
+  __device__ uint32_t operator()(uint32_t slot, uint32_t gk) const {
+    const uint32_t kval = slot >= mlim ? kNone : slot * 2u + (gk & 1u);
+    return slot == kNone ? m2 + gk : kval;
+  }
+};
+
 // key of an item at level li (marker levels, then the GPU level)
 template <int MaxD>
 __device__ inline uint32_t level_key(const uint32_t (&p)[MaxD], uint32_t gk,
@@ -1222,7 +1237,12 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads_nat(
     qv[k] = T.prev[k] >= 0;
     nat_item<MaxD>(S, qv[k] ? T.prev[k] : T.base, T.g, D, qgk[k], qp[k]);
   }
-  uint64_t cpk[2] = {0, 0};   // 4-bit head counts per level, per kind
+  // 4-bit head counts per level (the GPU level D included), per kind
+  using Cnt = typename std::conditional<(MaxD + 1) * 4 <= 32, uint32_t,
+                                        uint64_t>::type;
+  const SlotKeys sk_of(M);
+  const uint64_t two_m = (uint64_t)(2 * M);
+  Cnt cpk[2] = {0, 0};
   bool notinc = false, conflict = false;
   uint32_t kinds = 0;
   // previous item in the regrouped order: lane below for j == 0
@@ -1230,52 +1250,55 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads_nat(
 #pragma unroll
   for (int l = 0; l < MaxD; ++l) cp[l] = wave_shr1_u32(0u, p[kAggIpt - 1][l]);
   cgk = wave_shr1_u32(0u, gk[kAggIpt - 1]);
+  // (selects rather than branches: the conditions differ between lanes)
 #pragma unroll
   for (int j = 0; j < kAggIpt; ++j) {
     const int v = lane * kAggIpt + j;
     const bool vv = v < T.tile_n;
-    const uint32_t kd = v < n0 ? 0u : 1u;
-    uint32_t pp[MaxD], pgk;
-    bool pvalid = true;
-    if (v == n0 || v == 0) {
-      const int k = v == n0 ? 1 : 0;
-      pvalid = qv[k];
+    const bool comm = v >= n0;
+    // the first item of a kind takes the item before the tile of its kind
+    const bool first = v == n0 || v == 0;
+    const bool fk = v == n0;
+    const bool pvalid = first ? (fk ? qv[1] : qv[0]) : true;
+    uint32_t pp[MaxD];
 #pragma unroll
-      for (int l = 0; l < MaxD; ++l) pp[l] = qp[k][l];
-      pgk = qgk[k];
-    } else {
-#pragma unroll
-      for (int l = 0; l < MaxD; ++l) pp[l] = cp[l];
-      pgk = cgk;
-    }
+    for (int l = 0; l < MaxD; ++l)
+      pp[l] = first ? (fk ? qp[1][l] : qp[0][l]) : cp[l];
+    const uint32_t pgk = first ? (fk ? qgk[1] : qgk[0]) : cgk;
 #pragma unroll
     for (int l = 0; l < MaxD; ++l) cp[l] = p[j][l];
     cgk = gk[j];
+    Cnt inc = 0;
     uint32_t slot = kNone, pslot = kNone;
     bool eq = true;
 #pragma unroll
     for (int li = 0; li < MaxD; ++li) {
       slot = p[j][li] != kNone ? p[j][li] : slot;
       pslot = pp[li] != kNone ? pp[li] : pslot;
-      eq = eq && p[j][li] == pp[li];
+      eq = eq & (p[j][li] == pp[li]);
       if (li >= D || li < lv0 || li > lv1 || !((act >> li) & 1u)) continue;
-      const uint32_t key = slot_key(slot, M, gk[j]);
-      const uint32_t pkey = pvalid ? slot_key(pslot, M, pgk) : kNone;
-      if (vv && key == kNone) notinc = true;
-      if (key != pkey && key != kNone) {
-        cpk[kd] += (vv ? 1ull : 0ull) << (4 * li);
-        const int64_t ok = key >= 2 * M ? -1 : (int64_t)key;
-        const int64_t opk = pkey >= 2 * M ? -1 : (int64_t)pkey;
-        if (vv && pvalid && pgk == gk[j] && ok <= opk) notinc = true;
-      } else if (vv && pvalid && key == pkey && key != kNone && !eq) {
-        conflict = true;
-      }
+      const uint32_t key = sk_of(slot, gk[j]);
+      const uint32_t pk = sk_of(pslot, pgk);
+      const uint32_t pkey = pvalid ? pk : kNone;
+      const bool kv = key != kNone;
+      const bool head = kv & (key != pkey);
+      notinc = notinc | (vv & !kv);
+      inc += (vv & head) ? (Cnt)1 << (4 * li) : (Cnt)0;
+      // keys at or above 2 M (no marker at any level) order before all
+      // others: compared as key + 1, those as 0
+      const uint64_t ok = (uint64_t)key >= two_m ? 0 : (uint64_t)key + 1;
+      const uint64_t opk = (uint64_t)pkey >= two_m ? 0 : (uint64_t)pkey + 1;
+      notinc = notinc | (vv & head & pvalid & (pgk == gk[j]) & (ok <= opk));
+      // equal keys over different paths: the groups are not the runs
+      conflict = conflict | (vv & pvalid & kv & (key == pkey) & !eq);
     }
-    if (vv && D >= lv0 && D <= lv1 && ((act >> D) & 1u) &&
-        (!pvalid || gk[j] != pgk)) {
-      cpk[kd] += 1ull << (4 * D);
-      kinds |= 1u << kd;
+    if (D >= lv0 && D <= lv1 && ((act >> D) & 1u)) {
+      const bool g = vv & (!pvalid | (gk[j] != pgk));
+      inc += g ? (Cnt)1 << (4 * D) : (Cnt)0;
+      kinds |= g ? (comm ? 2u : 1u) : 0u;
     }
+    cpk[0] += comm ? (Cnt)0 : inc;
+    cpk[1] += comm ? inc : (Cnt)0;
   }
   for (int li = lv0; li <= lv1; ++li) {
 #pragma unroll
