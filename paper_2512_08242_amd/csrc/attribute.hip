@@ -275,15 +275,18 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
     }
   }
   wave_sync();
-  // per level: the window position of each record, then its marker
-#pragma unroll
-  for (int l = 0; l < MaxD; ++l) {
-    if (l >= D) break;
-    const int64_t* w = ps + wo[l];
-    const int nw = (int)wn[l];
+  // per level (one copy of the code: the level's window comes from the
+  // lane that holds it): the window position of each record, then its
+  // marker
+#pragma unroll 1
+  for (int l = 0; l < D; ++l) {
+    const int wol = (int)__shfl(woff, l, kWave);
+    const int nw = (int)__shfl(fits ? wk : (int64_t)-1, l, kWave);
+    const int64_t* w = ps + wol;
     int a = -1;             // window index of the last key <= previous start
     int64_t prev = kI64Max;
     uint32_t out[kTileIpt];
+    uint32_t need = 0;      // records searched in the bucket index
 #pragma unroll
     for (int j = 0; j < kTileIpt; ++j) {
       out[j] = kNone;
@@ -303,13 +306,31 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
         prev = s[j];
         // a < 0: the record starts before the segment's first marker (the
         // window then begins at that marker)
-        if (a >= 0 && s[j] < pe[wo[l] + a]) out[j] = pi[wo[l] + a];
+        if (a >= 0 && s[j] < pe[wol + a]) out[j] = pi[wol + a];
       } else {
-        // another gpu, or a window that did not fit (rare)
-        const uint32_t sg = g[j] * D + l;
-        const int64_t q = bi_upper(X, sg, s[j]) - 1;
-        if (q >= (int64_t)X.seg[sg].sb && s[j] < sme[q]) out[j] = sid[q];
+        need |= 1u << j;
       }
+    }
+    // another gpu, or a window that did not fit (rare): one search code for
+    // all of them, the record picked by selects
+    while (need) {
+      const int jj = __builtin_ctz(need);
+      need &= need - 1u;
+      int64_t sj = s[0];
+      uint32_t gj = g[0];
+#pragma unroll
+      for (int j = 1; j < kTileIpt; ++j)
+        if (j == jj) {
+          sj = s[j];
+          gj = g[j];
+        }
+      const uint32_t sg = gj * D + l;
+      const int64_t q = bi_upper(X, sg, sj) - 1;
+      const uint32_t r =
+          (q >= (int64_t)X.seg[sg].sb && sj < sme[q]) ? sid[q] : kNone;
+#pragma unroll
+      for (int j = 0; j < kTileIpt; ++j)
+        if (j == jj) out[j] = r;
     }
     uint32_t* dst = idx + (int64_t)l * n + k0;
     if (full && ((uintptr_t)dst & 15) == 0) {
