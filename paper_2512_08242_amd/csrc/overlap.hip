@@ -856,6 +856,7 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
   wave_sync();
   // window searches for the main segment, bucket searches for the rest
   int64_t o[kTileIpt];
+  uint32_t need = 0;    // records searched in the bucket index
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j) {
     o[j] = 0;
@@ -877,23 +878,41 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
       }
       o[j] = F[1] - F[0];
     } else {
-      // a compute kernel's overlapped time is the comm-active time inside
-      // it and vice versa
-      const BSeg P = s_seg[seg[j] ^ 1u];
-      const int64_t t[2] = {s[j], e[j]};
-      int64_t lo[2], hi[2];
-      bi_range(R.X, P, s[j], &lo[0], &hi[0]);
-      bi_range(R.X, P, e[j], &lo[1], &hi[1]);
-      bsearch_k<2>(R.rs, lo, hi, t);
-      o[j] = F_at(R, P, lo[1], e[j]) - F_at(R, P, lo[0], s[j]);
+      need |= 1u << j;
     }
   }
   // every position but the communication records of valid gpus (written
-  // by k_comm_records)
+  // by k_comm_records) and the records searched below
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j)
-    if (((m_in >> j) & 1u) && !((seg[j] & 1u) && (int)(seg[j] >> 1) < G))
+    if (((m_in >> j) & 1u) && !((need >> j) & 1u) &&
+        !((seg[j] & 1u) && (int)(seg[j] >> 1) < G))
       ovl[r[j]] = o[j];
+  // Records of other segments, or tiles whose window did not fit: one
+  // search code for all of them, the record picked by selects.  A compute
+  // kernel's overlapped time is the comm-active time inside it and vice
+  // versa.
+  while (need) {
+    const int jj = __builtin_ctz(need);
+    need &= need - 1u;
+    int64_t sj = s[0], ej = e[0];
+    uint32_t gj = seg[0], rj = r[0];
+#pragma unroll
+    for (int j = 1; j < kTileIpt; ++j)
+      if (j == jj) {
+        sj = s[j];
+        ej = e[j];
+        gj = seg[j];
+        rj = r[j];
+      }
+    const BSeg P = s_seg[gj ^ 1u];
+    const int64_t t[2] = {sj, ej};
+    int64_t lo[2], hi[2];
+    bi_range(R.X, P, sj, &lo[0], &hi[0]);
+    bi_range(R.X, P, ej, &lo[1], &hi[1]);
+    bsearch_k<2>(R.rs, lo, hi, t);
+    ovl[rj] = F_at(R, P, lo[1], ej) - F_at(R, P, lo[0], sj);
+  }
   // Bubbles (Section V-D eqs. 1-3): when every GPU runs its compute
   // kernels on one stream, the previous compute record of a compute
   // record's (gpu, stream) is its predecessor in its (gpu, kind) segment of
