@@ -31,24 +31,34 @@
  * owns every buffer.  The library allocates no device memory, frees nothing
  * and keeps no data between calls; all temporary storage comes from the
  * caller's `scratch` (chopper_launch_split_noalloc alone uses a static 6 KiB
- * device table of the library instead).  Scratch protocol (every call taking scratch): pass
+ * device table of the library instead).  One exception, on the host: for
+ * its read-backs (below) the library keeps, per device, four 256-byte slots
+ * of pinned host memory (hipHostMalloc) with one HIP event each, created on
+ * first use and held until the process ends; a read-back finds its value
+ * there and copies it out, and no slot holds anything between calls.  When
+ * the pinned memory cannot be had, the read-backs copy into the call's own
+ * variables instead.  Scratch protocol (every call taking scratch): pass
  * scratch == NULL to receive the required size in *scratch_bytes (nothing
  * else is read or written, no GPU work is done, CHOPPER_OK is returned); then
  * call again with a buffer of at least that many bytes, 256-byte aligned.
  *
  * Streams.  `stream` is a hipStream_t.  Work is enqueued on it.  Some calls
- * wait for that stream to read back a few words (counts and flags that size
- * or choose later launches), copied into the call's own host variables:
+ * read back a few words (counts and flags that size or choose later
+ * launches): a one-wave kernel stores them into a pinned slot, and the host
+ * waits for an event recorded after it, not for the whole stream, while
+ * work that does not depend on them is already queued behind it:
  * chopper_align once (record classes and whether the input is in start
- * order), chopper_attribute once (whether the markers are in start order),
- * chopper_aggregate once when the records come grouped by GPU in start
- * order (row counts per level, whether groups are runs), twice otherwise
- * and twice more on the general path, chopper_join_counters twice; the sorts wait
- * again when their input is not in time order.  chopper_overlap, the
- * derived metrics, the launch split and the statistics never wait.  So do
- * not capture the waiting calls in a HIP graph.  Outputs are valid after
- * the stream has been synchronized.  Concurrent calls must use distinct
- * scratch buffers.
+ * order; the markers' clock transform runs meanwhile), chopper_attribute
+ * once (whether the markers are in start order; their class partition runs
+ * meanwhile), chopper_aggregate once when the records come grouped by GPU
+ * in start order (row counts per level, whether groups are runs; the
+ * records reduction runs meanwhile and exits on the device if the flags
+ * rule it out), twice otherwise and twice more on the general path,
+ * chopper_join_counters twice; the sorts wait again when their input is not
+ * in time order.  chopper_overlap, the derived metrics, the launch split
+ * and the statistics never wait.  So do not capture the waiting calls in a
+ * HIP graph.  Outputs are valid after the stream has been synchronized.
+ * Concurrent calls must use distinct scratch buffers.
  *
  * Errors.  Argument errors are detected on the host before any GPU work and
  * returned synchronously (negative codes below).  Problems in the DATA are
