@@ -236,9 +236,9 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
   int64_t wl[MaxD], wn[MaxD], wo[MaxD];
 #pragma unroll
   for (int l = 0; l < MaxD; ++l) {
-    wl[l] = __shfl(wlo, l, kWave);
-    wo[l] = __shfl(woff, l, kWave);
-    wn[l] = __shfl(fits ? wk : (int64_t)-1, l, kWave);
+    wl[l] = readlane64(wlo, l);
+    wo[l] = readlane64(woff, l);
+    wn[l] = readlane64(fits ? wk : (int64_t)-1, l);
   }
   // The levels that fit are a prefix of the levels (offsets grow with the
   // level), packed from pool entry 0; entry q belongs to the last fitting
@@ -280,8 +280,8 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
   // marker
 #pragma unroll 1
   for (int l = 0; l < D; ++l) {
-    const int wol = (int)__shfl(woff, l, kWave);
-    const int nw = (int)__shfl(fits ? wk : (int64_t)-1, l, kWave);
+    const int wol = (int)readlane64(woff, l);
+    const int nw = (int)readlane64(fits ? wk : (int64_t)-1, l);
     const int64_t* w = ps + wol;
     int a = -1;             // window index of the last key <= previous start
     int64_t prev = kI64Max;

@@ -42,13 +42,14 @@ int64_t sort_tiles(int64_t n) { return ceil_div(n, kSortTile); }
 __device__ inline uint64_t digit_peers(uint32_t d, bool v, int nbits) {
   const uint64_t vm = __ballot(v);
   if (vm == 0) return 0;
-  const uint32_t d0 = (uint32_t)__shfl((int)d, __ffsll((long long)vm) - 1,
-                                       kWave);
+  // (the lanes read are uniform: a lane read, not a permute through LDS)
+  const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane(
+      (int)d, __ffsll((long long)vm) - 1);
   const uint64_t m0 = __ballot(v && d == d0);
   if (m0 == vm) return vm;
   const uint64_t rest = vm & ~m0;
-  const uint32_t d1 = (uint32_t)__shfl((int)d, __ffsll((long long)rest) - 1,
-                                       kWave);
+  const uint32_t d1 = (uint32_t)__builtin_amdgcn_readlane(
+      (int)d, __ffsll((long long)rest) - 1);
   const uint64_t m1 = __ballot(v && d == d1);
   if ((m0 | m1) == vm) return d == d0 ? m0 : m1;
   uint64_t peers = vm;

@@ -228,4 +228,15 @@ __device__ inline uint32_t wave_ror1_u32(uint32_t v) {
   return dpp32<kDppWaveRor1>(v, v);
 }
 
+// v of a lane that is the same for the whole wave (a lane read, not a
+// permute through LDS)
+__device__ inline int64_t readlane64(int64_t v, int lane) {
+  const uint64_t u = (uint64_t)v;
+  const uint32_t lo =
+      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+  const uint32_t hi =
+      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 }  // namespace chopper
