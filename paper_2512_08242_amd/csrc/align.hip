@@ -125,7 +125,8 @@ __global__ __launch_bounds__(kBlock) void k_transform_records(
     int64_t n, int n_gpus, const uint8_t* gpu, const uint8_t* stream,
     const uint8_t* cls, const int64_t* start, const int64_t* end,
     const ClockDev* clk, int64_t* s_out, int64_t* e_out, uint8_t* pres_s,
-    uint8_t* pres_k, uint32_t* unsorted, uint32_t* status) {
+    uint8_t* pres_k, uint32_t* unsorted, uint32_t* status,
+    WaveClasses* wcls) {
   // each lane owns eight consecutive records (a wave 512)
   const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
   const int64_t base =
@@ -217,6 +218,44 @@ __global__ __launch_bounds__(kBlock) void k_transform_records(
       ps = ks;
       pk = kk;
     }
+  }
+  // the wave's classes in both keys, for the class histogram: the first
+  // record's, then the first other one met, counted by ballots per row
+  // (uniform control: the ballots are the wave's)
+  {
+    uint32_t ks[kTileIpt], kk[kTileIpt];
+#pragma unroll
+    for (int j = 0; j < kTileIpt; ++j) {
+      ks[j] = (uint32_t)g8[j] * 256u + st8[j];
+      kk[j] = (uint32_t)g8[j] * 2u + (uint32_t)kind_of(c8[j]);
+    }
+    WaveClasses wc;
+    auto classes = [&](const uint32_t (&key)[kTileIpt], uint32_t& c0,
+                       uint32_t& n0, uint32_t& c1, uint32_t& n1) {
+      c0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)key[0]);
+      c1 = kNone;
+      n0 = n1 = 0;
+      bool many = false;
+#pragma unroll
+      for (int j = 0; j < kTileIpt; ++j) {
+        const bool v = k0 + j < n;
+        const uint64_t m0 = __ballot(v && key[j] == c0);
+        const uint64_t rest = __ballot(v && key[j] != c0);
+        n0 += (uint32_t)__popcll(m0);
+        if (rest) {
+          if (c1 == kNone)
+            c1 = (uint32_t)__builtin_amdgcn_readlane(
+                (int)key[j], __ffsll((long long)rest) - 1);
+          const uint64_t m1 = __ballot(v && key[j] == c1);
+          n1 += (uint32_t)__popcll(m1);
+          many = many || (rest & ~m1) != 0;
+        }
+      }
+      if (many) c1 = kManyClasses;
+    };
+    classes(ks, wc.a0, wc.na0, wc.a1, wc.na1);
+    classes(kk, wc.b0, wc.nb0, wc.b1, wc.nb1);
+    if (lane == 0) wcls[base / kWaveTile] = wc;
   }
   // is the input ordered by (gpu, start')?  Then every (gpu, stream) and
   // (gpu, kind) subsequence is time-ordered and one stable class pass sorts.
@@ -341,6 +380,7 @@ struct AlignLayout {
   uint16_t* cmap_k;
   uint32_t* counts;
   uint32_t* coff;
+  WaveClasses* wcls;   // classes of every wave tile of the records
   ClassSortLayout sort;
 };
 
@@ -353,6 +393,7 @@ static AlignLayout align_layout(Scratch& sc, int64_t n, int n_gpus) {
   L.cmap_k = sc.take<uint16_t>(512);
   L.counts = sc.take<uint32_t>(4);
   L.coff = sc.take<uint32_t>(65536 + 1);
+  L.wcls = sc.take<WaveClasses>(ceil_div(n, (int64_t)kWaveTile));
   L.sort = class_sort_layout(sc, n, 65536);
   return L;
 }
@@ -442,7 +483,7 @@ extern "C" int chopper_align(const chopper_records* rec,
                      dim3(kBlock), s, n, G, rec->gpu,
                      rec->stream, rec->cls, rec->start_ns, rec->end_ns,
                      (const ClockDev*)L.clk, start_out, end_out, L.pres_s,
-                     L.pres_k, L.counts + 2, status));
+                     L.pres_k, L.counts + 2, status, L.wcls));
   CHOPPER_HIP(launch("align_dense_classes", k_dense_classes, dim3(1),
                      dim3(kDenseThreads), s, (const uint8_t*)L.pres_s, L.cmap_s,
                      (const uint8_t*)L.pres_k, L.cmap_k, L.counts));
@@ -465,7 +506,7 @@ extern "C" int chopper_align(const chopper_records* rec,
     // input in (gpu, start') order: both orders are class partitions,
     // computed together
     rc = class_sort2(ks, kk, L.sort, order_out, L.coff, korder_out,
-                     L.coff + counts[0] + 1, s);
+                     L.coff + counts[0] + 1, s, (const WaveClasses*)L.wcls);
     if (rc != CHOPPER_OK) return rc;
   } else {
     rc = class_sort(ks, L.sort, order_out, L.coff, &range_err, s, known);

@@ -57,6 +57,8 @@ struct KeyRecStream {
   __device__ uint32_t cls(int64_t i) const {
     return cmap[(uint32_t)gpu[i] * 256u + stream[i]];
   }
+  // class of the raw code gpu * 256 + stream
+  __device__ uint32_t cls_of_raw(uint32_t raw) const { return cmap[raw]; }
   __device__ int64_t time(int64_t i) const { return t[i]; }
   __device__ uint32_t major(int64_t i) const { return gpu[i]; }
   __host__ __device__ int nclass() const { return C; }
@@ -87,6 +89,8 @@ struct KeyRecKind {
   __device__ uint32_t cls(int64_t i) const {
     return cmap[(uint32_t)gpu[i] * 2u + (uint32_t)kind_of(cl[i])];
   }
+  // class of the raw code gpu * 2 + kind
+  __device__ uint32_t cls_of_raw(uint32_t raw) const { return cmap[raw]; }
   __device__ int64_t time(int64_t i) const { return t[i]; }
   __device__ uint32_t major(int64_t i) const { return gpu[i]; }
   __host__ __device__ int nclass() const { return C; }
@@ -272,13 +276,25 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
                int known_sorted, const Cols& cols = Cols(),
                bool* cols_done = nullptr);
 
+// The classes of a wave tile of kWaveTile consecutive records in both keys,
+// recorded by the pass that reads the records, as raw codes (gpu * 256 +
+// stream, gpu * 2 + kind): one or two per key with their counts (na1 = 0:
+// one); a1 or b1 is kManyClasses when the wave holds more than two.
+struct WaveClasses {
+  uint32_t a0, na0, a1, na1, b0, nb0, b1, nb1;
+};
+constexpr uint32_t kManyClasses = 0xFFFFFFFEu;
+
 // Both class partitions of the same n > 0 items at once, for input ordered
 // by (major, time) (so the partitions are the stable sorts); needs
-// a.nclass() + b.nclass() <= 256.
+// a.nclass() + b.nclass() <= 256.  With `wcls` (one WaveClasses per wave
+// tile of the items) a sort tile whose waves each hold at most two classes
+// per key takes its histogram from them instead of from its items.
 template <typename AccA, typename AccB>
 int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
                 uint32_t* outA, uint32_t* coffA, uint32_t* outB,
-                uint32_t* coffB, hipStream_t s);
+                uint32_t* coffB, hipStream_t s,
+                const WaveClasses* wcls = nullptr);
 
 // Stable LSD radix sort of the (L.key0, L.val0) pairs of L.n items by the
 // low `bits` bits of the keys (8 bits per pass, through key1 / val1): the

@@ -530,14 +530,47 @@ int radix_sort_pairs(const ClassSortLayout& L, int bits, uint32_t* out,
 // B's), one scan covers both, one pass writes both permutations.
 // ---------------------------------------------------------------------------
 template <typename AccA, typename AccB>
-__global__ __launch_bounds__(kBlock) void k_class_hist2(AccA a, AccB b,
-                                                        int64_t n,
-                                                        int64_t ntiles,
-                                                        uint32_t* tilehist) {
+__global__ __launch_bounds__(kBlock) void k_class_hist2(
+    AccA a, AccB b, int64_t n, int64_t ntiles, const WaveClasses* wcls,
+    uint32_t* tilehist) {
   __shared__ uint32_t h[2][256];
   h[0][threadIdx.x] = 0;
   h[1][threadIdx.x] = 0;
   __syncthreads();
+  static_assert(kSortTile == kWavesPerBlock * kWaveTile,
+                "a sort tile is four wave tiles");
+  if (wcls) {
+    // the tile's wave tiles, when each holds at most two classes per key
+    // (the same decision in every thread)
+    const int64_t w0 = (int64_t)blockIdx.x * kWavesPerBlock;
+    const int64_t nw = ceil_div(n, (int64_t)kWaveTile);
+    bool few = true;
+    for (int q = 0; q < kWavesPerBlock; ++q)
+      if (w0 + q < nw)
+        few = few && wcls[w0 + q].a1 != kManyClasses &&
+              wcls[w0 + q].b1 != kManyClasses;
+    if (few) {
+      // thread q * 4 + k: wave q, key k / 2, class k % 2
+      const int q = (int)threadIdx.x >> 2, k = (int)threadIdx.x & 3;
+      if (q < kWavesPerBlock && w0 + q < nw) {
+        const WaveClasses& c = wcls[w0 + q];
+        const uint32_t raw = k == 0 ? c.a0 : k == 1 ? c.a1 : k == 2 ? c.b0 : c.b1;
+        const uint32_t cnt =
+            k == 0 ? c.na0 : k == 1 ? c.na1 : k == 2 ? c.nb0 : c.nb1;
+        if (cnt > 0)
+          atomicAdd(&h[k >> 1][k < 2 ? a.cls_of_raw(raw) : b.cls_of_raw(raw)],
+                    cnt);
+      }
+      __syncthreads();
+      const int CA = a.nclass();
+      if ((int)threadIdx.x < CA)
+        tilehist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[0][threadIdx.x];
+      if ((int)threadIdx.x < b.nclass())
+        tilehist[(int64_t)(CA + threadIdx.x) * ntiles + blockIdx.x] =
+            h[1][threadIdx.x];
+      return;
+    }
+  }
   const int lane = threadIdx.x & (kWave - 1);
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   const int64_t base = (int64_t)blockIdx.x * kSortTile;
@@ -724,14 +757,14 @@ __global__ __launch_bounds__(kBlock) void k_class_partition2(
 template <typename AccA, typename AccB>
 int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
                 uint32_t* outA, uint32_t* coffA, uint32_t* outB,
-                uint32_t* coffB, hipStream_t s) {
+                uint32_t* coffB, hipStream_t s, const WaveClasses* wcls) {
   const int64_t n = L.n;
   const int CA = a.nclass(), CB = b.nclass();
   const int64_t T = L.ntiles;
   if (n == 0 || CA > 256 || CB > 256 || CA + CB > 256)
     return CHOPPER_EINVAL;
   CHOPPER_HIP(launch("sort_class_hist", k_class_hist2<AccA, AccB>,
-                     dim3((unsigned)T), dim3(kBlock), s, a, b, n, T,
+                     dim3((unsigned)T), dim3(kBlock), s, a, b, n, T, wcls,
                      L.tilehist));
   CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, L.tileoff,
                                        (int64_t)(CA + CB) * T, L.scantmp,
@@ -751,7 +784,7 @@ int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
 
 template int class_sort2<KeyRecStream, KeyRecKind>(
     const KeyRecStream&, const KeyRecKind&, const ClassSortLayout&, uint32_t*,
-    uint32_t*, uint32_t*, uint32_t*, hipStream_t);
+    uint32_t*, uint32_t*, uint32_t*, hipStream_t, const WaveClasses*);
 
 template int class_sort<KeyRecStream, NoColumns>(
     const KeyRecStream&, const ClassSortLayout&, uint32_t*, uint32_t*, bool*,
