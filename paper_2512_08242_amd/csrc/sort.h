@@ -59,6 +59,14 @@ struct KeyRecStream {
   }
   // class of the raw code gpu * 256 + stream
   __device__ uint32_t cls_of_raw(uint32_t raw) const { return cmap[raw]; }
+  // raw codes of items i0 .. i0 + 7
+  __device__ void raw8(int64_t i0, int64_t n, uint32_t (&r)[8]) const {
+    uint32_t g[8], s[8];
+    load8_u8(gpu, i0, n, g);
+    load8_u8(stream, i0, n, s);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) r[j] = g[j] * 256u + s[j];
+  }
   __device__ int64_t time(int64_t i) const { return t[i]; }
   __device__ uint32_t major(int64_t i) const { return gpu[i]; }
   __host__ __device__ int nclass() const { return C; }
@@ -91,6 +99,14 @@ struct KeyRecKind {
   }
   // class of the raw code gpu * 2 + kind
   __device__ uint32_t cls_of_raw(uint32_t raw) const { return cmap[raw]; }
+  // raw codes of items i0 .. i0 + 7
+  __device__ void raw8(int64_t i0, int64_t n, uint32_t (&r)[8]) const {
+    uint32_t g[8], c[8];
+    load8_u8(gpu, i0, n, g);
+    load8_u8(cl, i0, n, c);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) r[j] = g[j] * 2u + (uint32_t)kind_of(c[j]);
+  }
   __device__ int64_t time(int64_t i) const { return t[i]; }
   __device__ uint32_t major(int64_t i) const { return gpu[i]; }
   __host__ __device__ int nclass() const { return C; }
@@ -287,14 +303,14 @@ constexpr uint32_t kManyClasses = 0xFFFFFFFEu;
 
 // Both class partitions of the same n > 0 items at once, for input ordered
 // by (major, time) (so the partitions are the stable sorts); needs
-// a.nclass() + b.nclass() <= 256.  With `wcls` (one WaveClasses per wave
-// tile of the items) a sort tile whose waves each hold at most two classes
-// per key takes its histogram from them instead of from its items.
+// a.nclass() + b.nclass() <= 256.  `wcls` holds one WaveClasses per wave
+// tile of the items: a sort tile whose waves hold at most two classes per
+// key in all is counted and partitioned from them and the raw codes, the
+// other tiles item by item.
 template <typename AccA, typename AccB>
 int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
                 uint32_t* outA, uint32_t* coffA, uint32_t* outB,
-                uint32_t* coffB, hipStream_t s,
-                const WaveClasses* wcls = nullptr);
+                uint32_t* coffB, hipStream_t s, const WaveClasses* wcls);
 
 // Stable LSD radix sort of the (L.key0, L.val0) pairs of L.n items by the
 // low `bits` bits of the keys (8 bits per pass, through key1 / val1): the

@@ -601,101 +601,102 @@ __global__ __launch_bounds__(kBlock) void k_class_hist2(
 
 // Tiles of at most two classes per key -- nearly every tile of records in
 // (gpu, start') order: one GPU's compute and communication streams -- are
-// ranked with one ballot per row by a pass of their own, which needs little
-// LDS and so keeps many blocks per CU; it flags the other tiles, and the
-// general pass below (the LDS ranking) does only those.
-struct TwoShared {
-  uint32_t c[2];
-  uint32_t wcnt[kSortIpt][kWavesPerBlock];
-};
-
-// An item's stable rank among its class: the number of class-c1 items
-// before it (earlier rows, earlier waves of its row, lower lanes of its
-// wave), or its position minus that number.  False (block-uniform) when the
-// tile holds more than two classes.  Invalid items only follow valid ones.
-__device__ inline bool two_class_ranks(const uint32_t (&dig)[kSortIpt],
-                                       const bool (&valid)[kSortIpt],
-                                       TwoShared& sh, uint32_t& c0,
-                                       uint32_t& c1,
-                                       uint32_t (&rank)[kSortIpt]) {
-  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
-  if (t == 0) {
-    sh.c[0] = dig[0];          // (item 0 of a tile always exists)
-    sh.c[1] = kNone;
-  }
-  __syncthreads();
-  c0 = sh.c[0];
-  uint32_t mine = kNone;
-#pragma unroll
-  for (int j = 0; j < kSortIpt; ++j)
-    if (valid[j] && dig[j] != c0 && dig[j] < mine) mine = dig[j];
-  if (mine != kNone) atomicMin(&sh.c[1], mine);
-  __syncthreads();
-  c1 = sh.c[1];
-  bool more = false;
-#pragma unroll
-  for (int j = 0; j < kSortIpt; ++j)
-    more = more || (valid[j] && dig[j] != c0 && dig[j] != c1);
-  if (__syncthreads_or(more ? 1 : 0)) return false;
-  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  uint64_t bm[kSortIpt];
-#pragma unroll
-  for (int j = 0; j < kSortIpt; ++j) {
-    bm[j] = __ballot(valid[j] && dig[j] == c1);
-    if (lane == 0) sh.wcnt[j][w] = (uint32_t)__popcll(bm[j]);
-  }
-  __syncthreads();
-  uint32_t before = 0;   // class-c1 items in the rows above
-#pragma unroll
-  for (int j = 0; j < kSortIpt; ++j) {
-    uint32_t inrow = 0, row = 0;
-#pragma unroll
-    for (int q = 0; q < kWavesPerBlock; ++q) {
-      const uint32_t x = sh.wcnt[j][q];
-      if (q < w) inrow += x;
-      row += x;
-    }
-    const uint32_t c1b = before + inrow + (uint32_t)__popcll(bm[j] & lt);
-    const uint32_t pos = (uint32_t)(j * kBlock + t);
-    rank[j] = (valid[j] && dig[j] == c1) ? c1b : pos - c1b;
-    before += row;
-  }
-  __syncthreads();   // (the shared words are reused by the next call)
-  return true;
-}
-
+// partitioned by a pass of their own: the tile's classes c0 (its first
+// item's) and c1 come from its waves' class records; every thread takes
+// eight consecutive items and compares their raw codes with c1; one block
+// scan of the class-c1 counts of both keys (packed in one word) ranks every
+// item; both permutations are laid out in LDS in output order, so that the
+// stores are coalesced.  It flags the other tiles, and the general pass
+// below (the LDS ranking) does only those.
 template <typename AccA, typename AccB>
 __global__ __launch_bounds__(kBlock) void k_class_partition2_two(
     AccA a, AccB b, int64_t n, int64_t ntiles, const uint32_t* tileoff,
-    uint32_t* outA, uint32_t* outB, uint8_t* general) {
-  __shared__ uint8_t s_dig[kSortTile];
-  __shared__ TwoShared two;
+    const WaveClasses* wcls, uint32_t* outA, uint32_t* outB,
+    uint8_t* general) {
+  __shared__ uint32_t s_out[2][kSortTile];
+  __shared__ uint32_t s_w[kWavesPerBlock];
   const int64_t base = (int64_t)blockIdx.x * kSortTile;
-  uint32_t da[kSortIpt], db[kSortIpt], ra[kSortIpt], rb[kSortIpt];
-  bool valid[kSortIpt];
-  striped_classes(a, base, n, s_dig, da, valid);
-  striped_classes(b, base, n, s_dig, db, valid);
-  uint32_t a0, a1, b0, b1;
-  const bool ok = two_class_ranks(da, valid, two, a0, a1, ra) &&
-                  two_class_ranks(db, valid, two, b0, b1, rb);
+  const int tile_n =
+      (int)((n - base) < kSortTile ? (n - base) : (int64_t)kSortTile);
+  // the tile's classes per key (the same in every thread): wave 0's first
+  // class is the tile's first item's
+  const int64_t w0 = (int64_t)blockIdx.x * kWavesPerBlock;
+  const int64_t nw = ceil_div(n, (int64_t)kWaveTile);
+  uint32_t A[2] = {kNone, kNone}, B[2] = {kNone, kNone};
+  bool ok = true;
+  auto add = [&](uint32_t (&C)[2], uint32_t c, uint32_t cnt) {
+    if (c == kManyClasses) ok = false;
+    if (!ok || cnt == 0) return;
+    if (C[0] == kNone || C[0] == c) C[0] = c;
+    else if (C[1] == kNone || C[1] == c) C[1] = c;
+    else ok = false;
+  };
+  for (int q = 0; q < kWavesPerBlock; ++q) {
+    if (w0 + q >= nw) break;
+    const WaveClasses c = wcls[w0 + q];
+    add(A, c.a0, c.na0);
+    add(A, c.a1, c.na1);
+    add(B, c.b0, c.nb0);
+    add(B, c.b1, c.nb1);
+  }
   if (threadIdx.x == 0) general[blockIdx.x] = ok ? 0 : 1;
   if (!ok) return;   // (block-uniform)
-  // B's rows of the table follow A's; its scanned values include A's n
-  const int64_t CA = a.nclass();
-  const uint32_t ga0 = tileoff[(int64_t)a0 * ntiles + blockIdx.x];
-  const uint32_t ga1 =
-      a1 != kNone ? tileoff[(int64_t)a1 * ntiles + blockIdx.x] : 0u;
-  const uint32_t gb0 =
-      tileoff[(CA + b0) * ntiles + blockIdx.x] - (uint32_t)n;
-  const uint32_t gb1 =
-      b1 != kNone ? tileoff[(CA + b1) * ntiles + blockIdx.x] - (uint32_t)n
-                  : 0u;
+  const int t = (int)threadIdx.x, lane = t & (kWave - 1), wv = t / kWave;
+  uint32_t ra[kSortIpt], rb[kSortIpt];
+  a.raw8(base + (int64_t)t * kSortIpt, n, ra);
+  b.raw8(base + (int64_t)t * kSortIpt, n, rb);
+  uint32_t ma = 0, mb = 0;   // the thread's class-c1 items
 #pragma unroll
   for (int j = 0; j < kSortIpt; ++j) {
-    if (!valid[j]) continue;
-    const uint32_t item = (uint32_t)(base + (int64_t)j * kBlock + threadIdx.x);
-    outA[(int64_t)(da[j] == a0 ? ga0 : ga1) + ra[j]] = item;
-    outB[(int64_t)(db[j] == b0 ? gb0 : gb1) + rb[j]] = item;
+    const bool v = t * kSortIpt + j < tile_n;
+    if (v && ra[j] == A[1]) ma |= 1u << j;
+    if (v && rb[j] == B[1]) mb |= 1u << j;
+  }
+  // class-c1 items before the thread, both keys in one word (at most
+  // kSortTile each)
+  const uint32_t cnt = ((uint32_t)__popc(ma) << 16) | (uint32_t)__popc(mb);
+  const uint32_t incl = wave_incl(cnt, OpAdd(), 0u);
+  if (lane == kWave - 1) s_w[wv] = incl;
+  __syncthreads();
+  uint32_t pre = incl - cnt, tot = 0;
+#pragma unroll
+  for (int q = 0; q < kWavesPerBlock; ++q) {
+    if (q < wv) pre += s_w[q];
+    tot += s_w[q];
+  }
+  const uint32_t n1a = tot >> 16, n1b = tot & 0xFFFFu;
+  const uint32_t n0a = (uint32_t)tile_n - n1a, n0b = (uint32_t)tile_n - n1b;
+  // output order in LDS: class c0 first, then class c1, each by rank
+#pragma unroll
+  for (int j = 0; j < kSortIpt; ++j) {
+    const uint32_t pos = (uint32_t)(t * kSortIpt + j);
+    if ((int)pos >= tile_n) continue;
+    const uint32_t lo = (1u << j) - 1u;
+    const uint32_t r1a = (pre >> 16) + (uint32_t)__popc(ma & lo);
+    const uint32_t r1b = (pre & 0xFFFFu) + (uint32_t)__popc(mb & lo);
+    s_out[0][((ma >> j) & 1u) ? n0a + r1a : pos - r1a] = (uint32_t)base + pos;
+    s_out[1][((mb >> j) & 1u) ? n0b + r1b : pos - r1b] = (uint32_t)base + pos;
+  }
+  // B's rows of the table follow A's; its scanned values include A's n
+  const int64_t CA = a.nclass();
+  const uint32_t ga0 =
+      tileoff[(int64_t)a.cls_of_raw(A[0]) * ntiles + blockIdx.x];
+  const uint32_t ga1 =
+      A[1] != kNone ? tileoff[(int64_t)a.cls_of_raw(A[1]) * ntiles +
+                              blockIdx.x]
+                    : 0u;
+  const uint32_t gb0 =
+      tileoff[(CA + b.cls_of_raw(B[0])) * ntiles + blockIdx.x] - (uint32_t)n;
+  const uint32_t gb1 =
+      B[1] != kNone
+          ? tileoff[(CA + b.cls_of_raw(B[1])) * ntiles + blockIdx.x] -
+                (uint32_t)n
+          : 0u;
+  __syncthreads();
+  for (int k = t; k < tile_n; k += kBlock) {
+    const uint32_t uk = (uint32_t)k;
+    outA[(int64_t)(uk < n0a ? ga0 + uk : ga1 + (uk - n0a))] = s_out[0][k];
+    outB[(int64_t)(uk < n0b ? gb0 + uk : gb1 + (uk - n0b))] = s_out[1][k];
   }
 }
 
@@ -761,7 +762,7 @@ int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
   const int64_t n = L.n;
   const int CA = a.nclass(), CB = b.nclass();
   const int64_t T = L.ntiles;
-  if (n == 0 || CA > 256 || CB > 256 || CA + CB > 256)
+  if (n == 0 || CA > 256 || CB > 256 || CA + CB > 256 || !wcls)
     return CHOPPER_EINVAL;
   CHOPPER_HIP(launch("sort_class_hist", k_class_hist2<AccA, AccB>,
                      dim3((unsigned)T), dim3(kBlock), s, a, b, n, T, wcls,
@@ -774,7 +775,7 @@ int class_sort2(const AccA& a, const AccB& b, const ClassSortLayout& L,
   CHOPPER_HIP(launch("sort_class_partition",
                      k_class_partition2_two<AccA, AccB>, dim3((unsigned)T),
                      dim3(kBlock), s, a, b, n, T, (const uint32_t*)L.tileoff,
-                     outA, outB, general));
+                     wcls, outA, outB, general));
   CHOPPER_HIP(launch("sort_class_partition", k_class_partition2<AccA, AccB>,
                      dim3((unsigned)T), dim3(kBlock), s, a, b, n, T,
                      (const uint32_t*)L.tileoff, outA, outB, coffA, coffB,
