@@ -148,10 +148,13 @@ __device__ inline void striped_classes(const Acc& acc, int64_t base,
   __syncthreads();
 }
 
+// With `unsorted`, also a cheap sufficient test of sortedness on the same
+// items, while they are at hand: is the input ordered by (major, time)?
 template <typename Acc>
 __global__ __launch_bounds__(kBlock) void k_class_hist(Acc acc, int64_t n,
                                                        int64_t ntiles,
-                                                       uint32_t* tilehist) {
+                                                       uint32_t* tilehist,
+                                                       uint32_t* unsorted) {
   __shared__ uint32_t h[256];
   h[threadIdx.x] = 0;
   __syncthreads();
@@ -169,6 +172,22 @@ __global__ __launch_bounds__(kBlock) void k_class_hist(Acc acc, int64_t n,
     const uint64_t peers = digit_peers(d[j], v[j], nbits);
     if (v[j] && __popcll(peers & lt) == 0)
       atomicAdd(&h[d[j]], (uint32_t)__popcll(peers));
+  }
+  if (unsorted) {
+    // eight consecutive items and the next one per lane
+    const int64_t i0 = base + (int64_t)threadIdx.x * kSortIpt;
+    bool bad = false;
+    if (i0 < n) {
+      uint32_t m[9];
+      int64_t t[9];
+      bool w[9];
+      major_time_block(acc, i0, n, m, t, w);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (w[j + 1])
+          bad = bad || m[j] > m[j + 1] || (m[j] == m[j + 1] && t[j + 1] < t[j]);
+    }
+    wave_flag_or(unsorted, bad, 1u);
   }
   __syncthreads();
   if ((int)threadIdx.x < acc.nclass())
@@ -227,27 +246,6 @@ __global__ __launch_bounds__(kBlock) void k_class_verify(Acc acc, int64_t n,
   if (p + 1 < n) {
     uint32_t a = perm[p], b = perm[p + 1];
     bad = acc.cls(a) == acc.cls(b) && acc.time(b) < acc.time(a);
-  }
-  wave_flag_or(unsorted, bad, 1u);
-}
-
-// is the input ordered by (major, time)?  (eight consecutive items and the
-// next one per lane)
-template <typename Acc>
-__global__ __launch_bounds__(kBlock) void k_major_sorted(Acc acc, int64_t n,
-                                                         uint32_t* unsorted) {
-  if (__builtin_amdgcn_readfirstlane((int)flag_read(unsorted)) != 0) return;
-  const int64_t i0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * 8;
-  bool bad = false;
-  if (i0 < n) {
-    uint32_t m[9];
-    int64_t t[9];
-    bool v[9];
-    major_time_block(acc, i0, n, m, t, v);
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (v[j + 1])
-        bad = bad || m[j] > m[j + 1] || (m[j] == m[j + 1] && t[j + 1] < t[j]);
   }
   wave_flag_or(unsorted, bad, 1u);
 }
@@ -416,20 +414,18 @@ int class_sort(const Acc& acc, const ClassSortLayout& L, uint32_t* out,
   }
   bool sorted = false;
   if (C <= 256) {
-    // cheap sufficient test on the input, ordered by (major, time); its
-    // read-back is waited for after the partition is queued, which runs
-    // either way
+    // cheap sufficient test on the input, ordered by (major, time), made
+    // by the histogram pass; its read-back is waited for after the
+    // partition is queued, which runs either way
     ReadBack rb;
-    if (known_sorted < 0) {
+    if (known_sorted < 0)
       CHOPPER_HIP(launch("sort_fill", k_fill_u32, dim3(1), dim3(kBlock), s,
                          L.flag, (int64_t)1, 0u));
-      CHOPPER_HIP(launch("sort_major_sorted", k_major_sorted<Acc>,
-                         grid_for(n, kBlock * 8), dim3(kBlock), s, acc, n,
-                         L.flag));
-      CHOPPER_HIP(read_back_start(L.flag, sizeof(uint32_t), s, &rb));
-    }
     CHOPPER_HIP(launch("sort_class_hist", k_class_hist<Acc>, dim3((unsigned)T),
-                       dim3(kBlock), s, acc, n, T, L.tilehist));
+                       dim3(kBlock), s, acc, n, T, L.tilehist,
+                       known_sorted < 0 ? L.flag : (uint32_t*)nullptr));
+    if (known_sorted < 0)
+      CHOPPER_HIP(read_back_start(L.flag, sizeof(uint32_t), s, &rb));
     CHOPPER_HIP(exclusive_scan<uint32_t>(L.tilehist, L.tileoff, (int64_t)C * T,
                                          L.scantmp, L.total, s));
     CHOPPER_HIP(launch("sort_class_partition", k_class_partition<Acc, Cols>,
