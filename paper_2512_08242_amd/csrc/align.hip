@@ -204,24 +204,12 @@ __global__ __launch_bounds__(kBlock) void k_transform_records(
         e_out[k0 + j] = e2[j];
       }
   }
-  // presence of (gpu, stream) and (gpu, kind): one plain byte store per run
-  // of equal pairs in the lane
-  {
-    uint32_t ps = 0xFFFFFFFFu, pk = 0xFFFFFFFFu;
-#pragma unroll
-    for (int j = 0; j < kTileIpt; ++j) {
-      if (k0 + j >= n) break;
-      const uint32_t ks = (uint32_t)g8[j] * 256u + st8[j];
-      const uint32_t kk = (uint32_t)g8[j] * 2u + (uint32_t)kind_of(c8[j]);
-      if (ks != ps) pres_s[ks] = 1;
-      if (kk != pk) pres_k[kk] = 1;
-      ps = ks;
-      pk = kk;
-    }
-  }
-  // the wave's classes in both keys, for the class histogram: the first
+  // The wave's classes in both keys, for the class histogram: the first
   // record's, then the first other one met, counted by ballots per row
-  // (uniform control: the ballots are the wave's)
+  // (uniform control: the ballots are the wave's).  They also give the
+  // presence of the (gpu, stream) and (gpu, kind) pairs: lane 0 marks them,
+  // and only a wave with more classes marks them record by record (one
+  // plain byte store per run of equal pairs in the lane).
   {
     uint32_t ks[kTileIpt], kk[kTileIpt];
 #pragma unroll
@@ -230,8 +218,9 @@ __global__ __launch_bounds__(kBlock) void k_transform_records(
       kk[j] = (uint32_t)g8[j] * 2u + (uint32_t)kind_of(c8[j]);
     }
     WaveClasses wc;
-    auto classes = [&](const uint32_t (&key)[kTileIpt], uint32_t& c0,
-                       uint32_t& n0, uint32_t& c1, uint32_t& n1) {
+    auto classes = [&](const uint32_t (&key)[kTileIpt], uint8_t* pres,
+                       uint32_t& c0, uint32_t& n0, uint32_t& c1,
+                       uint32_t& n1) {
       c0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)key[0]);
       c1 = kNone;
       n0 = n1 = 0;
@@ -251,10 +240,22 @@ __global__ __launch_bounds__(kBlock) void k_transform_records(
           many = many || (rest & ~m1) != 0;
         }
       }
-      if (many) c1 = kManyClasses;
+      if (many) {
+        c1 = kManyClasses;
+        uint32_t pv = kNone;
+#pragma unroll
+        for (int j = 0; j < kTileIpt; ++j) {
+          if (k0 + j >= n) break;
+          if (key[j] != pv) pres[key[j]] = 1;
+          pv = key[j];
+        }
+      } else if (lane == 0) {
+        pres[c0] = 1;
+        if (c1 != kNone) pres[c1] = 1;
+      }
     };
-    classes(ks, wc.a0, wc.na0, wc.a1, wc.na1);
-    classes(kk, wc.b0, wc.nb0, wc.b1, wc.nb1);
+    classes(ks, pres_s, wc.a0, wc.na0, wc.a1, wc.na1);
+    classes(kk, pres_k, wc.b0, wc.nb0, wc.b1, wc.nb1);
     if (lane == 0) wcls[base / kWaveTile] = wc;
   }
   // is the input ordered by (gpu, start')?  Then every (gpu, stream) and
