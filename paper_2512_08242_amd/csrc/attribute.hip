@@ -194,6 +194,54 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
       s[j] = k < n ? start[k] : 0;
     }
   }
+  // lane l < D: window of level l -- the precomputed one when the tile's
+  // starts lie in its range, else searched here.  The levels that fit the
+  // pool are a prefix of the levels (offsets grow with the level), packed
+  // from pool entry 0; entry q belongs to the last fitting level whose
+  // offset is <= q.  Every lane issues the loads of all its entries before
+  // writing any of them (one round trip to memory instead of one per level
+  // and per 64 markers).
+  constexpr int kStageIt = kMarkWin / kWave;
+  int64_t vk[kStageIt], ve[kStageIt];
+  uint32_t vi[kStageIt];
+  int64_t wlo = 0, wk = 0, woff = 0;
+  bool fits = false;
+  auto stage_loads = [&](bool ok) {
+    woff = wave_incl(wk, OpAdd(), (int64_t)0) - wk;
+    fits = ok && lane < D && woff + wk <= kMarkWin;
+    int64_t wl[MaxD], wn[MaxD], wo[MaxD];
+#pragma unroll
+    for (int l = 0; l < MaxD; ++l) {
+      wl[l] = readlane64(wlo, l);
+      wo[l] = readlane64(woff, l);
+      wn[l] = readlane64(fits ? wk : (int64_t)-1, l);
+    }
+    int64_t ptot = 0;
+#pragma unroll
+    for (int l = 0; l < MaxD; ++l)
+      if (l < D && wn[l] >= 0) ptot = wo[l] + wn[l];
+#pragma unroll
+    for (int i = 0; i < kStageIt; ++i) {
+      const int64_t q = lane + (int64_t)i * kWave;
+      if (q < ptot) {
+        int64_t src = wl[0] + q - wo[0];
+#pragma unroll
+        for (int l = 1; l < MaxD; ++l)
+          if (l < D && wn[l] >= 0 && q >= wo[l]) src = wl[l] + q - wo[l];
+        vk[i] = X.key[src];
+        ve[i] = sme[src];
+        vi[i] = sid[src];
+      }
+    }
+    return ptot;
+  };
+  // the precomputed windows' entries are loaded while the records arrive
+  // (a tile of no valid gpu has none that fit)
+  if (lane < D) {
+    wlo = pw_lo;
+    wk = pw_k == kNone ? (int64_t)kMarkWin + 1 : (int64_t)pw_k;
+  }
+  int64_t ptot = stage_loads(true);
   // a record is searched when it exists and its gpu is in range; records
   // past n (partial last tile) carry g = 0xFFFFFFFF and are never searched
   uint32_t m_ok = 0;
@@ -211,15 +259,11 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
     }
   smin = lane63(wave_incl(smin, OpMin(), kI64Max));
   smax = lane63(wave_incl(smax, OpMax(), kI64Min));
-  // lane l < D: window of level l -- the precomputed one when the tile's
-  // starts lie in its range, else searched here
   const bool pre = smin >= pt_lo && smax <= pt_hi;      // (uniform)
-  int64_t wlo = 0, wk = 0;
-  if (g0ok && lane < D) {
-    if (pre) {
-      wlo = pw_lo;
-      wk = pw_k == kNone ? (int64_t)kMarkWin + 1 : (int64_t)pw_k;
-    } else {
+  if (!pre) {
+    // the tile's starts leave the precomputed range: search the windows
+    wlo = wk = 0;
+    if (g0ok && lane < D) {
       const BSeg P = X.seg[g0 * D + lane];
       int64_t lo[2], hi[2];
       const int64_t t[2] = {smin, smax};
@@ -229,41 +273,7 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
       wlo = lo[0] - 1 > (int64_t)P.sb ? lo[0] - 1 : (int64_t)P.sb;
       wk = lo[1] - wlo;
     }
-  }
-  // pool offsets: levels in order while they fit
-  const int64_t woff = wave_incl(wk, OpAdd(), (int64_t)0) - wk;
-  const bool fits = g0ok && lane < D && woff + wk <= kMarkWin;
-  int64_t wl[MaxD], wn[MaxD], wo[MaxD];
-#pragma unroll
-  for (int l = 0; l < MaxD; ++l) {
-    wl[l] = readlane64(wlo, l);
-    wo[l] = readlane64(woff, l);
-    wn[l] = readlane64(fits ? wk : (int64_t)-1, l);
-  }
-  // The levels that fit are a prefix of the levels (offsets grow with the
-  // level), packed from pool entry 0; entry q belongs to the last fitting
-  // level whose offset is <= q.  Every lane issues the loads of all its
-  // entries before writing any of them, so the staging costs one round trip
-  // to memory instead of one per level and per 64 markers.
-  int64_t ptot = 0;
-#pragma unroll
-  for (int l = 0; l < MaxD; ++l)
-    if (l < D && wn[l] >= 0) ptot = wo[l] + wn[l];
-  constexpr int kStageIt = kMarkWin / kWave;
-  int64_t vk[kStageIt], ve[kStageIt];
-  uint32_t vi[kStageIt];
-#pragma unroll
-  for (int i = 0; i < kStageIt; ++i) {
-    const int64_t q = lane + (int64_t)i * kWave;
-    if (q < ptot) {
-      int64_t src = wl[0] + q - wo[0];
-#pragma unroll
-      for (int l = 1; l < MaxD; ++l)
-        if (l < D && wn[l] >= 0 && q >= wo[l]) src = wl[l] + q - wo[l];
-      vk[i] = X.key[src];
-      ve[i] = sme[src];
-      vi[i] = sid[src];
-    }
+    ptot = stage_loads(g0ok);
   }
 #pragma unroll
   for (int i = 0; i < kStageIt; ++i) {
