@@ -151,6 +151,8 @@ __device__ inline void korder_gather(const uint32_t* korder, const uint8_t* gpu,
 // from t b on, so the fold keeps the tile order); the block of the last
 // tile also writes the total.
 constexpr int kSpineSpan = 1024;
+// most blocks of the fix-up pass (4 per compute unit)
+constexpr unsigned kFixBlocks = 1024;
 
 // Ordered fold of one value per thread over the block: the exclusive
 // prefix of the thread and the block total.  `s_w` holds one value per
@@ -186,19 +188,37 @@ __device__ inline T fold_before(const T* in, Op op, T ident, T* s_w) {
   return tot;
 }
 
-template <typename T, typename Op>
-__global__ __launch_bounds__(kSpineSpan) void k_tile_spine(
-    const T* in, T* out, int64_t ntiles, T ident, T* total) {
-  __shared__ T s_w[kSpineWaves + 1];
-  Op op;
-  const T before = fold_before(in, op, ident, s_w);
+// The exclusive (segment, end) maximum before every tile (the carry; with
+// the total), and the list of the tiles after the first whose carry has
+// their first item's segment and reaches its start (fix[0] their number,
+// cleared by the count pass; fix[1..] the tiles, in no particular order):
+// the counts of only these change with the carry (k_runs_fix).
+__global__ __launch_bounds__(kSpineSpan) void k_runs_carry(
+    const SegMax* agg, SegMax* pre_out, int64_t ntiles, SegMax* total,
+    const SegMax* first, uint32_t* fix) {
+  __shared__ SegMax s_w[kSpineWaves + 1];
+  OpSegMax op;
+  const SegMax ident = segmax_ident();
+  const SegMax before = fold_before(agg, op, ident, s_w);
   const int64_t i = (int64_t)blockIdx.x * kSpineSpan + threadIdx.x;
-  const T v = i < ntiles ? in[i] : ident;
-  T tot;
-  const T pre = op(before, block_excl_ordered(v, op, ident, s_w, &tot));
-  if (i < ntiles) out[i] = pre;
-  if (total && threadIdx.x == 0 &&
-      (int64_t)(blockIdx.x + 1) * kSpineSpan >= ntiles)
+  const SegMax v = i < ntiles ? agg[i] : ident;
+  SegMax tot;
+  const SegMax pre = op(before, block_excl_ordered(v, op, ident, s_w, &tot));
+  bool again = false;
+  if (i < ntiles) {
+    pre_out[i] = pre;
+    const SegMax f = first[i];
+    again = i > 0 && pre.seg == f.seg && pre.val >= f.val;
+  }
+  // one append per wave
+  const uint64_t m = __ballot(again);
+  if (m != 0) {
+    uint32_t base = 0;
+    if (lane_id() == 0) base = atomicAdd(fix, (uint32_t)__popcll(m));
+    base = __shfl(base, 0, kWave);
+    if (again) fix[1 + base + lanes_below(m)] = (uint32_t)i;
+  }
+  if (threadIdx.x == 0 && (int64_t)(blockIdx.x + 1) * kSpineSpan >= ntiles)
     *total = op(before, tot);
 }
 
@@ -298,13 +318,13 @@ struct RunItems {
   SegMax wagg;              // (segment, end) maximum of the wave's items
 };
 
-__device__ inline void run_items(int64_t n, const uint32_t* korder,
-                                 const uint8_t* gpu, const uint8_t* cls,
-                                 const int64_t* start, const int64_t* end,
-                                 const SegMax* tile_pre, int64_t* slice,
-                                 RunItems& it) {
+__device__ inline void run_items(int64_t tile, int64_t n,
+                                 const uint32_t* korder, const uint8_t* gpu,
+                                 const uint8_t* cls, const int64_t* start,
+                                 const int64_t* end, const SegMax* tile_pre,
+                                 int64_t* slice, RunItems& it) {
   const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
-  const int64_t wbase = (int64_t)blockIdx.x * kOvTile + (int64_t)wv * kWaveTile;
+  const int64_t wbase = tile * kOvTile + (int64_t)wv * kWaveTile;
   uint32_t seg[kTileIpt];
   int64_t s[kTileIpt], e[kTileIpt];
 #pragma unroll
@@ -338,12 +358,11 @@ __device__ inline void run_items(int64_t n, const uint32_t* korder,
   __shared__ SegMax s_w[kWavesPerBlock];
   if (lane == kWave - 1) s_w[wv] = incl;
   __syncthreads();
-  SegMax pre = tile_pre ? tile_pre[blockIdx.x] : segmax_ident();
+  SegMax pre = tile_pre ? tile_pre[tile] : segmax_ident();
   for (int i = 0; i < kWavesPerBlock; ++i)
     if (i < wv) pre = op(pre, s_w[i]);
   pre = op(pre, wave_shr1_any(segmax_ident(), incl));
-  const bool first_lane_of_all =
-      blockIdx.x == 0 && wv == 0 && lane == 0;
+  const bool first_lane_of_all = tile == 0 && wv == 0 && lane == 0;
   it.pseg0 = first_lane_of_all ? kNone : pre.seg;
   uint32_t m_head = 0, m_newseg = 0;
 #pragma unroll
@@ -368,49 +387,45 @@ __device__ inline void run_items(int64_t n, const uint32_t* korder,
   it.m_newseg = m_newseg;
 }
 
-// Number of runs (heads) and the segmented sum of union increments per tile.
-// First pass (tile_pre null): counted as if no earlier item reached into
-// the tile, and also the tile's (segment, end) maximum and its first item
-// (segment, start).  Fix-up pass (tile_pre = exclusive maxima): only tiles
-// whose carry has their first item's segment and reaches its start count
-// again; for the others the first count is exact, since every item of the
-// first segment then starts after the carry.
-// The first pass also clears the bucket table of the run starts (filled by
-// the write pass) and records, for every segment, the korder position of
-// its first item and the end of its items (kcand [2][kSegs]); segments
-// without items keep whatever the array held, so these are candidates that
-// k_runs_spine2 verifies against the items.
+// Number of runs (heads) and the segmented sum of union increments per tile,
+// counted as if no earlier item reached into the tile (k_runs_fix corrects
+// the tiles where one does), and also the tile's (segment, end) maximum and
+// its first item (segment, start).
+// Block 0 clears the segment run and korder ranges, the mixed-streams flag
+// of the bubbles and the count of the fix-up list; the blocks together
+// clear the bucket table of the run starts (filled by the write pass) and
+// record, for every segment, the korder position of its first item and the
+// end of its items (kcand [2][kSegs]); segments without items keep
+// whatever the array held, so these are candidates that k_runs_spine2
+// verifies against the items.
 __global__ __launch_bounds__(kBlock) void k_runs_count(
     int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
-    const int64_t* start, const int64_t* end, const SegMax* tile_pre,
-    SegMax* tile_agg, SegMax* tile_first, uint32_t* tile_heads,
-    SegSum* tile_inc, uint32_t* ranges, uint32_t* mixed, uint32_t* kcand,
-    uint32_t* btable, int64_t btable_cap) {
+    const int64_t* start, const int64_t* end, SegMax* tile_agg,
+    SegMax* tile_first, uint32_t* tile_heads, SegSum* tile_inc,
+    uint32_t* ranges, uint32_t* mixed, uint32_t* kcand, uint32_t* btable,
+    int64_t btable_cap, uint32_t* fix) {
   __shared__ int64_t s_slice[kWavesPerBlock][kSlice];
-  // first pass: block 0 clears the segment run and korder ranges and the
-  // mixed-streams flag of the bubbles
-  if (ranges && blockIdx.x == 0) {
+  if (blockIdx.x == 0) {
     for (int i = threadIdx.x; i < 4 * kSegs; i += kBlock) ranges[i] = 0;
-    if (threadIdx.x == 0) *mixed = 0;
+    if (threadIdx.x == 0) {
+      *mixed = 0;
+      fix[0] = 0;
+    }
   }
-  if (btable) bindex_clear(btable, btable_cap, blockIdx.x, gridDim.x);
-  if (tile_pre) {
-    const SegMax c = tile_pre[blockIdx.x], f = tile_first[blockIdx.x];
-    if (!(c.seg == f.seg && c.val >= f.val)) return;   // block-uniform
-  }
+  bindex_clear(btable, btable_cap, blockIdx.x, gridDim.x);
   const int lane0 = lane_id();
   const int64_t wb0 = (int64_t)blockIdx.x * kOvTile +
                       (int64_t)(threadIdx.x / kWave) * kWaveTile;
   // segment of the item before the wave's first (for the boundaries)
   uint32_t sprev = kNone;
-  if (kcand && lane0 == 0 && wb0 > 0 && wb0 <= n) {
+  if (lane0 == 0 && wb0 > 0 && wb0 <= n) {
     const uint32_t r = korder[wb0 - 1];
     sprev = (uint32_t)gpu[r] * 2u + (uint32_t)kind_of(cls[r]);
   }
   RunItems it;
-  run_items(n, korder, gpu, cls, start, end, tile_pre,
+  run_items(blockIdx.x, n, korder, gpu, cls, start, end, nullptr,
             s_slice[threadIdx.x / kWave], it);
-  if (kcand) {
+  {
     // item p (blocked: wb0 + lane * 8 + j) starts a segment when its
     // predecessor's differs; the predecessor of a lane's first item is the
     // lane below's last (lane 0: the item before the wave)
@@ -460,11 +475,78 @@ __global__ __launch_bounds__(kBlock) void k_runs_count(
     }
     tile_heads[blockIdx.x] = tc;
     tile_inc[blockIdx.x] = t;
-    if (!tile_pre) tile_agg[blockIdx.x] = tm;
-  }
-  // the tile's first item (blocked arrangement: lane 0, item 0 of wave 0)
-  if (!tile_pre && threadIdx.x == 0)
+    tile_agg[blockIdx.x] = tm;
+    // the tile's first item (blocked arrangement: lane 0, item 0 of wave 0)
     tile_first[blockIdx.x] = SegMax{it.seg[0], it.s[0]};
+  }
+}
+
+// Corrects the counts of the tiles listed by k_runs_carry, one wave per
+// tile.  The carry c has the segment S of the tile's first item and reaches
+// its start, so it changes the exclusive running maximum only of the tile's
+// first items of S whose running end within the tile stays below c (a
+// prefix of the tile): the first count took the first item as a run head of
+// length end - start (its exclusive value came from no item), the others
+// with their running end in the tile; with c they are heads only if they
+// start after c, and add only what they reach beyond it.  The differences
+// go into the tile's head count, and into its union sum when the whole tile
+// is S (otherwise that sum is of a later segment).  The first tile is never
+// listed: its carry is the empty one, as in its first count.
+__global__ __launch_bounds__(kBlock) void k_runs_fix(
+    int64_t n, const uint32_t* korder, const uint8_t* gpu, const uint8_t* cls,
+    const int64_t* start, const int64_t* end, const SegMax* tile_pre,
+    const uint32_t* fix, uint32_t* tile_heads, SegSum* tile_inc) {
+  const int lane = lane_id();
+  const uint32_t nfix = fix[0];
+  const uint32_t w0 = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave;
+  for (uint32_t k = w0; k < nfix; k += gridDim.x * kWavesPerBlock) {
+    const int64_t t = fix[1 + k];
+    const SegMax c = tile_pre[t];
+    const int64_t b = t * kOvTile;
+    const int64_t te = b + kOvTile < n ? b + kOvTile : n;
+    int64_t run = kI64Min;   // running end of the tile's items before
+    uint32_t dh = 0;
+    uint64_t di = 0;   // (differences modulo 2^64, as the sums wrap)
+    for (int64_t p0 = b; p0 < te; p0 += kWave) {
+      const int64_t p = p0 + lane;
+      uint32_t seg = kNone;
+      int64_t s = 0, e = 0;
+      if (p < te) korder_gather(korder, gpu, cls, start, end, p, seg, s, e);
+      const bool in = seg == c.seg;
+      const int64_t incl = wave_incl(in ? e : kI64Min, OpMax(), kI64Min);
+      const int64_t mo = (int64_t)wave_shr1((uint64_t)run, (uint64_t)incl);
+      const int64_t m = mo > run ? mo : run;   // exclusive, within the tile
+      const bool aff = in && (p == b || c.val > m);
+      if (aff) {
+        bool oh;
+        int64_t oi;
+        if (p == b) {
+          // the first count's exclusive value: the empty one
+          oh = c.seg != 0u || s > kI64Min;
+          oi = oh ? e - s : (e > kI64Min ? e - kI64Min : 0);
+        } else {
+          oh = s > m;
+          oi = oh ? e - s : (e > m ? e - m : 0);
+        }
+        const int64_t x = c.val > m ? c.val : m;
+        const bool nh = s > x;
+        const int64_t ni = nh ? e - s : (e > x ? e - x : 0);
+        dh += (uint32_t)nh - (uint32_t)oh;
+        di += (uint64_t)ni - (uint64_t)oi;
+      }
+      if (__ballot(!aff) != 0) break;   // the prefix ends in this chunk
+      run = readlane64(incl, kWave - 1);
+    }
+    for (int d = kWave / 2; d > 0; d >>= 1) {
+      dh += __shfl_xor(dh, d, kWave);
+      di += __shfl_xor(di, d, kWave);
+    }
+    if (lane == 0) {
+      tile_heads[t] += dh;
+      if (tile_inc[t].seg == c.seg)
+        tile_inc[t].sum = (int64_t)((uint64_t)tile_inc[t].sum + di);
+    }
+  }
 }
 
 // Writes the runs: start and union length before the run (the prefix of
@@ -502,7 +584,7 @@ __global__ __launch_bounds__(kBlock) void k_runs_write(
   int64_t sbefore = 0;
   if (lane_id() == 0 && wb0 > 0 && wb0 <= n) sbefore = start[korder[wb0 - 1]];
   RunItems it;
-  run_items(n, korder, gpu, cls, start, end, tile_pre,
+  run_items(blockIdx.x, n, korder, gpu, cls, start, end, tile_pre,
             s_slice[threadIdx.x / kWave], it);
   const int lane = lane_id(), wv = (int)(threadIdx.x / kWave);
   OpSegSum op;
@@ -1156,6 +1238,7 @@ struct OverlapLayout {
   SegMax* tile_agg;
   SegMax* tile_pre;     // exclusive scan of tile_agg
   SegMax* tile_first;   // first item of every tile: (segment, start)
+  uint32_t* fix;        // tiles that count again: their number, then them
   SegMax* grand;
   uint32_t* tile_heads;
   SegSum* tile_inc;
@@ -1193,6 +1276,7 @@ static OverlapLayout overlap_layout(Scratch& sc, int64_t n, int G) {
   L.tile_agg = sc.take<SegMax>(L.ntiles);
   L.tile_pre = sc.take<SegMax>(L.ntiles);
   L.tile_first = sc.take<SegMax>(L.ntiles);
+  L.fix = sc.take<uint32_t>(L.ntiles + 1);
   L.grand = sc.take<SegMax>(1);
   L.tile_heads = sc.take<uint32_t>(L.ntiles);
   L.tile_inc = sc.take<SegSum>(L.ntiles);
@@ -1265,19 +1349,20 @@ extern "C" int chopper_overlap(const chopper_records* rec,
     // union runs of every (gpu, kind)
     CHOPPER_HIP(launch("ov_runs_count", k_runs_count, dim3(T), dim3(kBlock), s,
                        n, korder, rec->gpu, rec->cls, start_al, end_al,
-                       (const SegMax*)nullptr, L.tile_agg, L.tile_first,
-                       L.tile_heads, L.tile_inc, L.rbeg, L.mixed, L.kcand,
-                       L.btable, L.btable_cap));
+                       L.tile_agg, L.tile_first, L.tile_heads, L.tile_inc,
+                       L.rbeg, L.mixed, L.kcand, L.btable, L.btable_cap,
+                       L.fix));
     const dim3 sg((unsigned)ceil_div(L.ntiles, (int64_t)kSpineSpan));
-    CHOPPER_HIP(launch("ov_runs_spine", k_tile_spine<SegMax, OpSegMax>, sg,
-                       dim3(kSpineSpan), s, (const SegMax*)L.tile_agg,
-                       L.tile_pre, L.ntiles, SegMax{0u, kI64Min}, L.grand));
-    CHOPPER_HIP(launch("ov_runs_fixup", k_runs_count, dim3(T), dim3(kBlock), s,
-                       n, korder, rec->gpu, rec->cls, start_al, end_al,
-                       (const SegMax*)L.tile_pre, (SegMax*)nullptr,
-                       L.tile_first, L.tile_heads, L.tile_inc,
-                       (uint32_t*)nullptr, (uint32_t*)nullptr,
-                       (uint32_t*)nullptr, (uint32_t*)nullptr, (int64_t)0));
+    CHOPPER_HIP(launch("ov_runs_spine", k_runs_carry, sg, dim3(kSpineSpan), s,
+                       (const SegMax*)L.tile_agg, L.tile_pre, L.ntiles,
+                       L.grand, (const SegMax*)L.tile_first, L.fix));
+    // (the waves loop over the listed tiles, however many there are)
+    const unsigned fb = (unsigned)ceil_div(L.ntiles, (int64_t)kWavesPerBlock);
+    CHOPPER_HIP(launch("ov_runs_fixup", k_runs_fix,
+                       dim3(fb < kFixBlocks ? fb : kFixBlocks), dim3(kBlock),
+                       s, n, korder, rec->gpu, rec->cls, start_al, end_al,
+                       (const SegMax*)L.tile_pre, (const uint32_t*)L.fix,
+                       L.tile_heads, L.tile_inc));
     CHOPPER_HIP(launch("ov_runs_inc_spine", k_runs_spine2, sg,
                        dim3(kSpineSpan), s, (const uint32_t*)L.tile_heads,
                        L.tile_run0, L.nruns, (const SegSum*)L.tile_inc,
