@@ -694,6 +694,9 @@ __device__ inline uint32_t slot_key(uint32_t slot, int64_t M, uint32_t gk) {
   return slot * 2u + (gk & 1u);
 }
 
+// Marker counts below which the natural-tile heads pass compares slots.
+constexpr uint32_t kSlotFastM = 1u << 30;
+
 // The same as selects: m2 = (uint32_t)(2 M) and mlim = min(M, 2^32 - 1)
 // (so that slot >= mlim iff slot >= M for every slot below kNone).
 struct SlotKeys {
@@ -1240,16 +1243,20 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads_nat(
   // 4-bit head counts per level (the GPU level D included), per kind
   using Cnt = typename std::conditional<(MaxD + 1) * 4 <= 32, uint32_t,
                                         uint64_t>::type;
-  const SlotKeys sk_of(M);
-  const uint64_t two_m = (uint64_t)(2 * M);
+  // Every item of a run of the tile, and the item before the run, has the
+  // tile's GPU and the run's kind, so the keys of two consecutive items
+  // compare as their slots: equal iff the slots are, ordered as slot + 1
+  // modulo 2^32 (which puts items with no marker first, as their keys are),
+  // a slot at or above M giving no key.  That holds while keys of distinct
+  // slots differ, M < 2^30; beyond, the call takes the general path.
+  const uint32_t mlim = (uint32_t)(M < (int64_t)kSlotFastM ? M : 0);
   Cnt cpk[2] = {0, 0};
-  bool notinc = false, conflict = false;
+  bool notinc = M >= (int64_t)kSlotFastM, conflict = false;
   uint32_t kinds = 0;
   // previous item in the regrouped order: lane below for j == 0
-  uint32_t cp[MaxD], cgk;
+  uint32_t cp[MaxD];
 #pragma unroll
   for (int l = 0; l < MaxD; ++l) cp[l] = wave_shr1_u32(0u, p[kAggIpt - 1][l]);
-  cgk = wave_shr1_u32(0u, gk[kAggIpt - 1]);
   // (selects rather than branches: the conditions differ between lanes)
 #pragma unroll
   for (int j = 0; j < kAggIpt; ++j) {
@@ -1264,10 +1271,8 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads_nat(
 #pragma unroll
     for (int l = 0; l < MaxD; ++l)
       pp[l] = first ? (fk ? qp[1][l] : qp[0][l]) : cp[l];
-    const uint32_t pgk = first ? (fk ? qgk[1] : qgk[0]) : cgk;
 #pragma unroll
     for (int l = 0; l < MaxD; ++l) cp[l] = p[j][l];
-    cgk = gk[j];
     Cnt inc = 0;
     uint32_t slot = kNone, pslot = kNone;
     bool eq = true;
@@ -1277,23 +1282,18 @@ __global__ __launch_bounds__(kBlock) void k_agg_heads_nat(
       pslot = pp[li] != kNone ? pp[li] : pslot;
       eq = eq & (p[j][li] == pp[li]);
       if (li >= D || li < lv0 || li > lv1 || !((act >> li) & 1u)) continue;
-      const uint32_t key = sk_of(slot, gk[j]);
-      const uint32_t pk = sk_of(pslot, pgk);
-      const uint32_t pkey = pvalid ? pk : kNone;
-      const bool kv = key != kNone;
-      const bool head = kv & (key != pkey);
-      notinc = notinc | (vv & !kv);
+      const uint32_t s1 = slot + 1u, ps1 = pslot + 1u;
+      const bool bad = s1 > mlim;        // no key
+      const bool same = slot == pslot;
+      const bool head = !bad & (!pvalid | !same);
+      notinc = notinc | (vv & bad);
       inc += (vv & head) ? (Cnt)1 << (4 * li) : (Cnt)0;
-      // keys at or above 2 M (no marker at any level) order before all
-      // others: compared as key + 1, those as 0
-      const uint64_t ok = (uint64_t)key >= two_m ? 0 : (uint64_t)key + 1;
-      const uint64_t opk = (uint64_t)pkey >= two_m ? 0 : (uint64_t)pkey + 1;
-      notinc = notinc | (vv & head & pvalid & (pgk == gk[j]) & (ok <= opk));
+      notinc = notinc | (vv & head & pvalid & (s1 <= ps1));
       // equal keys over different paths: the groups are not the runs
-      conflict = conflict | (vv & pvalid & kv & (key == pkey) & !eq);
+      conflict = conflict | (vv & pvalid & !bad & same & !eq);
     }
     if (D >= lv0 && D <= lv1 && ((act >> D) & 1u)) {
-      const bool g = vv & (!pvalid | (gk[j] != pgk));
+      const bool g = vv & !pvalid;
       inc += g ? (Cnt)1 << (4 * D) : (Cnt)0;
       kinds |= g ? (comm ? 2u : 1u) : 0u;
     }
