@@ -293,32 +293,55 @@ __global__ __launch_bounds__(kBlock) void k_attribute_records(
     const int wol = (int)readlane64(woff, l);
     const int nw = (int)readlane64(fits ? wk : (int64_t)-1, l);
     const int64_t* w = ps + wol;
-    int a = -1;             // window index of the last key <= previous start
-    int64_t prev = kI64Max;
     uint32_t out[kTileIpt];
     uint32_t need = 0;      // records searched in the bucket index
+    if (nw <= 0) {
+      // (uniform) no window (every record of the tile's gpu is searched)
+      // or an empty one (no marker holds them)
 #pragma unroll
-    for (int j = 0; j < kTileIpt; ++j) {
-      out[j] = kNone;
-      if (!((m_ok >> j) & 1u)) continue;
-      if (g[j] == g0 && nw >= 0) {
-        if (a < 0 || s[j] < prev) {
-          int lo = 0, hi = nw;
-          while (lo < hi) {
-            const int m = (lo + hi) >> 1;
-            if (w[m] <= s[j]) lo = m + 1;
-            else hi = m;
-          }
-          a = lo - 1;
-        } else {
-          while (a + 1 < nw && w[a + 1] <= s[j]) ++a;
+      for (int j = 0; j < kTileIpt; ++j) {
+        out[j] = kNone;
+        if (((m_ok >> j) & 1u) && (nw < 0 || g[j] != g0)) need |= 1u << j;
+      }
+    } else {
+      // window index of the last key <= t, or -1: a search with power-of-two
+      // steps, the same number of probes in every lane
+      const int hb = 1 << (31 - __clz(nw));
+      auto search = [&](int64_t t) {
+        int pos = 0;
+        for (int step = hb; step > 0; step >>= 1) {
+          const bool in = pos + step <= nw;
+          if (in && w[in ? pos + step - 1 : nw - 1] <= t) pos += step;
         }
-        prev = s[j];
-        // a < 0: the record starts before the segment's first marker (the
-        // window then begins at that marker)
-        if (a >= 0 && s[j] < pe[wol + a]) out[j] = pi[wol + a];
-      } else {
-        need |= 1u << j;
+        return pos - 1;
+      };
+      int a = -1;             // window index of the previous record's key
+      int64_t prev = kI64Max;
+#pragma unroll
+      for (int j = 0; j < kTileIpt; ++j) {
+        const bool valid = (m_ok >> j) & 1u;
+        const bool in = valid && g[j] == g0;
+        if (valid && !in) need |= 1u << j;
+        const int64_t sj = s[j];
+        // a record at or after the previous one is at most two keys past
+        // its key (else, and for the lane's first, a search)
+        const int c0 = a >= 0 ? a : 0;
+        const bool a1 = c0 + 1 < nw && w[c0 + 1 < nw ? c0 + 1 : nw - 1] <= sj;
+        const int c1 = c0 + (a1 ? 1 : 0);
+        const bool a2 = a1 && c1 + 1 < nw &&
+                        w[c1 + 1 < nw ? c1 + 1 : nw - 1] <= sj;
+        int pos = c1;
+        if (in && (j == 0 || a < 0 || sj < prev || a2)) pos = search(sj);
+        if (in) {
+          a = pos;
+          prev = sj;
+        }
+        // a < 0: the record starts before the window's first marker (the
+        // window then begins at the segment's first marker)
+        const int pc = pos >= 0 ? pos : 0;
+        const int64_t mend = pe[wol + pc];
+        const uint32_t mid = pi[wol + pc];
+        out[j] = in && pos >= 0 && sj < mend ? mid : kNone;
       }
     }
     // another gpu, or a window that did not fit (rare): one search code for
