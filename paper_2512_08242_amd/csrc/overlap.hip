@@ -936,32 +936,37 @@ __global__ __launch_bounds__(kBlock) void k_overlap_records(
     }
   }
   wave_sync();
-  // window searches for the main segment, bucket searches for the rest
+  // window searches for the main segment, bucket searches for the rest;
+  // the window's are searched with power-of-two steps, the same number of
+  // probes in every lane, both ends at once
+  const int hb = K > 0 ? 1 << (31 - __clz(K)) : 0;
   int64_t o[kTileIpt];
   uint32_t need = 0;    // records searched in the bucket index
 #pragma unroll
   for (int j = 0; j < kTileIpt; ++j) {
     o[j] = 0;
-    if (!((m_valid >> j) & 1u) || e[j] <= s[j]) continue;
-    if (win && seg[j] == seg0) {
-      int64_t F[2];
-#pragma unroll
-      for (int z = 0; z < 2; ++z) {
-        const int64_t t = z ? e[j] : s[j];
-        int lo = 0, hi = K;
-        while (lo < hi) {
-          const int mid = (lo + hi) >> 1;
-          if (wrs[mid] <= t) lo = mid + 1;
-          else hi = mid;
-        }
-        const int q = lo - 1;
-        F[z] = q < 0 ? 0
-                     : wpl[q] + ((wre[q] < t ? wre[q] : t) - wrs[q]);
-      }
-      o[j] = F[1] - F[0];
-    } else {
-      need |= 1u << j;
+    const bool act = ((m_valid >> j) & 1u) && e[j] > s[j];
+    const bool here = act && win && seg[j] == seg0;
+    if (act && !here) need |= 1u << j;
+    if (!here) continue;
+    int ps = 0, pe = 0;   // runs starting at or before s, e
+    for (int step = hb; step > 0; step >>= 1) {
+      const int qs = ps + step <= K ? ps + step - 1 : K - 1;
+      const int qe = pe + step <= K ? pe + step - 1 : K - 1;
+      const int64_t vs = wrs[qs], ve = wrs[qe];
+      ps += (ps + step <= K && vs <= s[j]) ? step : 0;
+      pe += (pe + step <= K && ve <= e[j]) ? step : 0;
     }
+    int64_t F[2];
+#pragma unroll
+    for (int z = 0; z < 2; ++z) {
+      const int64_t t = z ? e[j] : s[j];
+      const int q = (z ? pe : ps) - 1;
+      const int qc = q >= 0 ? q : 0;
+      const int64_t rs0 = wrs[qc], re0 = wre[qc], pl0 = wpl[qc];
+      F[z] = q < 0 ? 0 : pl0 + ((re0 < t ? re0 : t) - rs0);
+    }
+    o[j] = F[1] - F[0];
   }
   // every position but the communication records of valid gpus (written
   // by k_comm_records) and the records searched below
