@@ -438,10 +438,16 @@ class Pipeline:
         self._run("aggregate")
 
     def derive(self):
+        self.derive_rows()
+        self.derive_windows()
+
+    def derive_rows(self):
         rows = self.rows.struct()
         _check(lib.chopper_ratios(ctypes.byref(rows), self.dt.depth,
                                   self.dt.n_counters, self.freq,
                                   _ptr(self.ratios), _stream()), "ratios")
+
+    def derive_windows(self):
         _check(lib.chopper_window_fractions(self.dt.n_markers,
                                             _ptr(self.mwin), _ptr(self.wfrac),
                                             _stream()), "window_fractions")
@@ -559,12 +565,28 @@ class Pipeline:
         return ctr[:, :n], matched[:n]
 
     def step(self):
-        """One pass of the whole pipeline."""
+        """One pass of the whole pipeline.  Attribution and the overlap
+        queries both need only the aligned times, orders and markers, so the
+        overlap call goes on a second stream (default priority) beside the
+        attribution on the caller's, followed there by the window fractions
+        (from the overlap's windows alone) while the aggregation, which
+        waits for the overlap call, runs; the step ends when both streams
+        have."""
+        main = torch.cuda.current_stream()
+        if getattr(self, "_side", None) is None:
+            self._side = torch.cuda.Stream(device=main.device)
+            self._ov_done = torch.cuda.Event()
         self.align()
+        self._side.wait_stream(main)
+        with torch.cuda.stream(self._side):
+            self.overlap()
+            self._ov_done.record(self._side)
+            self.derive_windows()
         self.attribute()
-        self.overlap()
+        main.wait_event(self._ov_done)
         self.aggregate()
-        self.derive()
+        self.derive_rows()
+        main.wait_stream(self._side)
 
     def results(self) -> Dict:
         torch.cuda.synchronize()
