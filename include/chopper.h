@@ -58,7 +58,9 @@
  * in time order.  chopper_overlap, the derived metrics, the launch split
  * and the statistics never wait.  So do not capture the waiting calls in a
  * HIP graph.  Outputs are valid after the stream has been synchronized.
- * Concurrent calls must use distinct scratch buffers.
+ * Concurrent calls must use distinct scratch buffers.  Calls on different
+ * streams are ordered by the caller's events; chopper_aggregate also takes
+ * one (ready) for inputs computed on another stream.
  *
  * Errors.  Argument errors are detected on the host before any GPU work and
  * returned synchronously (negative codes below).  Problems in the DATA are
@@ -304,6 +306,12 @@ int chopper_overlap(const chopper_records* records, const int64_t* start_al,
  * paths, PATH_CONFLICT is set (a warning); the rows are still those of the
  * whole paths (the call then waits for `stream` once more and sorts the
  * records by path, level by level).
+ * ready: NULL, or a hipEvent_t that gap and ovl are complete at (recorded by
+ * the caller, typically after chopper_overlap on another stream, before this
+ * call).  Every pass that reads gap or ovl is queued behind a
+ * hipStreamWaitEvent on it; the passes before them (the order check, the
+ * head counts, the row offsets and their read-back) are not, so they run
+ * while gap and ovl are still being computed.
  */
 int chopper_aggregate(const chopper_records* records, const int64_t* start_al,
                       const int64_t* end_al, const uint32_t* korder,
@@ -311,7 +319,7 @@ int chopper_aggregate(const chopper_records* records, const int64_t* start_al,
                       const int64_t* ovl, const chopper_markers* markers,
                       int32_t level, const chopper_filter* filter,
                       chopper_rows* rows, void* scratch, size_t* scratch_bytes,
-                      uint32_t* status, void* stream);
+                      uint32_t* status, void* ready, void* stream);
 
 /*
  * chopper_ratios -- derived metrics per aggregated row (III-C: metrics derived

@@ -132,7 +132,7 @@ def _load():
     lib.chopper_aggregate.argtypes = [ctypes.POINTER(Records), P, P, P, P, i32,
                                       P, P, ctypes.POINTER(Markers), i32,
                                       ctypes.POINTER(Filter),
-                                      ctypes.POINTER(Rows), P, SZ, P, P]
+                                      ctypes.POINTER(Rows), P, SZ, P, P, P]
     lib.chopper_ratios.argtypes = [ctypes.POINTER(Rows), i32, i32,
                                    ctypes.c_double, P, P]
     lib.chopper_window_fractions.argtypes = [i64, P, P, P]
@@ -368,6 +368,7 @@ class Pipeline:
         self.rows = RowsBuffer(0, D, dt.n_counters, dev)
         self.ratios = e(6, 1, dt_=torch.float64)
         self._scr = {}
+        self._ready = None      # event gap / ovl are complete at (see step)
         for name in ("align", "attribute", "overlap"):
             self._scr[name] = _scratch(
                 lambda s, b, nm_=name: self._call(nm_, s, b), dev)
@@ -418,7 +419,9 @@ class Pipeline:
                 _ptr(self.korder), _ptr(self.idx), dt.depth, _ptr(self.gap),
                 _ptr(self.ovl), ctypes.byref(mk), self.level,
                 None if self.filt is None else ctypes.byref(self.filt),
-                ctypes.byref(rows), scratch, sbytes, st, s)
+                ctypes.byref(rows), scratch, sbytes, st,
+                None if self._ready is None
+                else ctypes.c_void_p(self._ready.cuda_event), s)
         raise ValueError(name)
 
     def _run(self, name):
@@ -569,9 +572,10 @@ class Pipeline:
         queries both need only the aligned times, orders and markers, so the
         overlap call goes on a second stream (default priority) beside the
         attribution on the caller's, followed there by the window fractions
-        (from the overlap's windows alone) while the aggregation, which
-        waits for the overlap call, runs; the step ends when both streams
-        have."""
+        (from the overlap's windows alone).  The aggregation is queued after
+        the attribution with the event recorded after the overlap call, which
+        only its passes that read gap and ovl wait for; the step ends when
+        both streams have."""
         main = torch.cuda.current_stream()
         if getattr(self, "_side", None) is None:
             self._side = torch.cuda.Stream(device=main.device)
@@ -583,8 +587,11 @@ class Pipeline:
             self._ov_done.record(self._side)
             self.derive_windows()
         self.attribute()
-        main.wait_event(self._ov_done)
-        self.aggregate()
+        self._ready = self._ov_done
+        try:
+            self.aggregate()
+        finally:
+            self._ready = None
         self.derive_rows()
         main.wait_stream(self._side)
 

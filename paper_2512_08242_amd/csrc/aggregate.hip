@@ -2189,7 +2189,7 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
                     const Overflow& ovf, int64_t T, int Lv, uint32_t act,
                     int D, int64_t M, int nfields, chopper_rows* rows,
                     int level, bool want_workload, uint32_t* status,
-                    hipStream_t s) {
+                    hipEvent_t ready, hipStream_t s) {
   int rc = CHOPPER_OK;
   const int64_t Th = L.ntiles_h;
   const int G = L.G;
@@ -2234,6 +2234,9 @@ static int agg_fast(const AggLayout& L, const RecSrc& S, const RowsDev& R,
     CHOPPER_HIP(read_back_start(L.stage,
                                 sizeof(int64_t) * (size_t)(3 + Lv + 1), s,
                                 &rb));
+    // gap and ovl are read from here on: the caller's event first (the
+    // read-back above does not wait for it)
+    if (ready) CHOPPER_HIP(hipStreamWaitEvent(s, ready, 0));
     if (speculate) {
       NatGeom NS = N;
       NS.fflags = L.hflags;
@@ -2395,7 +2398,7 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
                                  const chopper_filter* filter,
                                  chopper_rows* rows, void* scratch,
                                  size_t* scratch_bytes, uint32_t* status,
-                                 void* stream) {
+                                 void* ready, void* stream) {
   if (!validate_records(rec) || !validate_markers(mk) || !rows ||
       !scratch_bytes)
     return CHOPPER_EINVAL;
@@ -2488,13 +2491,16 @@ extern "C" int chopper_aggregate(const chopper_records* rec,
   if (n > 0 && !filter && level != CHOPPER_LEVEL_WORKLOAD &&
       n < ((int64_t)1 << 29) && rows->cap < ((int64_t)1 << 29)) {
     rc = D <= 4 ? agg_fast<4>(L, S, R, ovf, T, Lv, act, D, M, nfields, rows,
-                              level, want_workload, status, s)
+                              level, want_workload, status,
+                              (hipEvent_t)ready, s)
                 : agg_fast<8>(L, S, R, ovf, T, Lv, act, D, M, nfields, rows,
-                              level, want_workload, status, s);
+                              level, want_workload, status,
+                              (hipEvent_t)ready, s);
     if (rc != 1) return rc;
   }
 
-  // ---- general path: per-level owner election
+  // ---- general path: per-level owner election (it reads gap and ovl)
+  if (ready) CHOPPER_HIP(hipStreamWaitEvent(s, (hipEvent_t)ready, 0));
   // pointer tables for the per-level owner / row maps
   CHOPPER_HIP(hipMemcpyAsync(L.own_tab, L.own, sizeof(L.own),
                              hipMemcpyHostToDevice, s));

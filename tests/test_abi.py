@@ -105,7 +105,7 @@ def test_scratch_queries_need_no_gpu(ch):
     assert lib.chopper_aggregate(ctypes.byref(rec), fake, fake, fake, fake, 3,
                                  fake, fake, ctypes.byref(mk), 255, None,
                                  ctypes.byref(rows), None, ctypes.byref(sz),
-                                 None, None) == 0
+                                 None, None, None) == 0
     assert sz.value > 0
 
 
@@ -162,7 +162,8 @@ def test_argument_errors_are_synchronous(ch):
                                      fake, depth, fake, fake,
                                      ctypes.byref(mk), lvl, None,
                                      ctypes.byref(rows), None,
-                                     ctypes.byref(sz), None, None) == EINVAL
+                                     ctypes.byref(sz), None, None,
+                                     None) == EINVAL
     # time hook: unknown kernel name
     assert lib.chopper_time_kernel(b"no_such_kernel", fake, fake) == EINVAL
     assert lib.chopper_time_kernel(None, None, None) == 0
