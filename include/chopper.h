@@ -273,9 +273,6 @@ int chopper_attribute(const chopper_records* records, const int64_t* start_al,
  *   gwin_out [n_gpus][6]  start = min s', end = max e' over the GPU's records
  *                 (zeros if none), then CO, MO, OV, ID of that window.
  * order / korder come from chopper_align; markers may be NULL.
- * records_done: NULL, or a hipEvent_t that the call records on `stream` once
- * ovl_out and gap_out are complete, before the marker and GPU windows are
- * computed (for chopper_aggregate's ready on another stream).
  */
 int chopper_overlap(const chopper_records* records, const int64_t* start_al,
                     const int64_t* end_al, const uint32_t* order,
@@ -283,7 +280,7 @@ int chopper_overlap(const chopper_records* records, const int64_t* start_al,
                     const int64_t* mstart_al, const int64_t* mend_al,
                     int64_t* ovl_out, int64_t* gap_out, int64_t* mwin_out,
                     int64_t* gwin_out, void* scratch, size_t* scratch_bytes,
-                    uint32_t* status, void* records_done, void* stream);
+                    uint32_t* status, void* stream);
 
 /*
  * chopper_aggregate -- metric aggregation at a granularity (Section III-C;

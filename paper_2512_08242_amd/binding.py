@@ -128,7 +128,7 @@ def _load():
                                       P, P]
     lib.chopper_overlap.argtypes = [ctypes.POINTER(Records), P, P, P, P,
                                     ctypes.POINTER(Markers), P, P, P, P, P, P,
-                                    P, SZ, P, P, P]
+                                    P, SZ, P, P]
     lib.chopper_aggregate.argtypes = [ctypes.POINTER(Records), P, P, P, P, i32,
                                       P, P, ctypes.POINTER(Markers), i32,
                                       ctypes.POINTER(Filter),
@@ -369,7 +369,6 @@ class Pipeline:
         self.ratios = e(6, 1, dt_=torch.float64)
         self._scr = {}
         self._ready = None      # event gap / ovl are complete at (see step)
-        self._rec_done = None   # event chopper_overlap records there
         for name in ("align", "attribute", "overlap"):
             self._scr[name] = _scratch(
                 lambda s, b, nm_=name: self._call(nm_, s, b), dev)
@@ -411,9 +410,7 @@ class Pipeline:
                 _ptr(self.order), _ptr(self.korder), ctypes.byref(mk),
                 _ptr(self.mstart), _ptr(self.mend), _ptr(self.ovl),
                 _ptr(self.gap), _ptr(self.mwin), _ptr(self.gwin), scratch,
-                sbytes, st,
-                None if self._rec_done is None
-                else ctypes.c_void_p(self._rec_done.cuda_event), s)
+                sbytes, st, s)
         if name == "aggregate":
             rows = self.rows.struct()
             self._rows_struct = rows
@@ -576,25 +573,18 @@ class Pipeline:
         overlap call goes on a second stream (default priority) beside the
         attribution on the caller's, followed there by the window fractions
         (from the overlap's windows alone).  The aggregation is queued after
-        the attribution with the event the overlap call records once ovl
-        and gap are complete (before its marker windows), which only the
-        aggregation's passes that read them wait for; the step ends when
+        the attribution with the event recorded after the overlap call, which
+        only its passes that read gap and ovl wait for; the step ends when
         both streams have."""
         main = torch.cuda.current_stream()
         if getattr(self, "_side", None) is None:
             self._side = torch.cuda.Stream(device=main.device)
             self._ov_done = torch.cuda.Event()
-            # (recorded once, so that its handle exists before the first
-            # call that records it)
-            self._ov_done.record(main)
         self.align()
         self._side.wait_stream(main)
         with torch.cuda.stream(self._side):
-            self._rec_done = self._ov_done
-            try:
-                self.overlap()
-            finally:
-                self._rec_done = None
+            self.overlap()
+            self._ov_done.record(self._side)
             self.derive_windows()
         self.attribute()
         self._ready = self._ov_done

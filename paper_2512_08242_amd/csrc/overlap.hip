@@ -1326,8 +1326,7 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                                int64_t* ovl_out, int64_t* gap_out,
                                int64_t* mwin_out, int64_t* gwin_out,
                                void* scratch, size_t* scratch_bytes,
-                               uint32_t* status, void* records_done,
-                               void* stream) {
+                               uint32_t* status, void* stream) {
   if (!validate_records(rec) || !validate_markers(mk) || !scratch_bytes)
     return CHOPPER_EINVAL;
   const int64_t n = rec->n;
@@ -1427,16 +1426,6 @@ extern "C" int chopper_overlap(const chopper_records* rec,
                            (const uint32_t*)L.roff, (const uint8_t*)L.cdone,
                            start_al, end_al, R, ovl_out, gwin_out));
   }
-  if (n > 0) {
-    CHOPPER_HIP(launch("ov_gap", k_gap,
-                       dim3((unsigned)ceil_div(n, (int64_t)kOvTile)),
-                       dim3(kBlock), s,
-                       n, order, rec->gpu, rec->stream, rec->cls, start_al,
-                       end_al, (const uint32_t*)L.mixed, gap_out));
-  }
-  // ovl and gap are complete: the caller's event, then the windows
-  if (records_done)
-    CHOPPER_HIP(hipEventRecord((hipEvent_t)records_done, s));
   if (nm > 0)
     CHOPPER_HIP(launch_shm("ov_markers", k_overlap_markers,
                            grid_for(nm, kBlock * kMarkPerThread),
@@ -1445,5 +1434,12 @@ extern "C" int chopper_overlap(const chopper_records* rec,
   if (n == 0)   // (otherwise the communication-records pass writes them)
     CHOPPER_HIP(launch("ov_gpus", k_overlap_gpus, grid_for(G, kBlock),
                      dim3(kBlock), s, G, R, gwin_out));
+  if (n > 0) {
+    CHOPPER_HIP(launch("ov_gap", k_gap,
+                       dim3((unsigned)ceil_div(n, (int64_t)kOvTile)),
+                       dim3(kBlock), s,
+                       n, order, rec->gpu, rec->stream, rec->cls, start_al,
+                       end_al, (const uint32_t*)L.mixed, gap_out));
+  }
   return CHOPPER_OK;
 }

@@ -94,7 +94,7 @@ def test_scratch_queries_need_no_gpu(ch):
         lambda: lib.chopper_overlap(ctypes.byref(rec), fake, fake, fake, fake,
                                     ctypes.byref(mk), fake, fake, fake, fake,
                                     fake, fake, None, ctypes.byref(sz), None,
-                                    None, None),
+                                    None),
     ):
         sz.value = 0
         assert call() == 0 and sz.value > 0
