@@ -571,11 +571,12 @@ class Pipeline:
         """One pass of the whole pipeline.  Attribution and the overlap
         queries both need only the aligned times, orders and markers, so the
         overlap call goes on a second stream (default priority) beside the
-        attribution on the caller's, followed there by the window fractions
-        (from the overlap's windows alone).  The aggregation is queued after
-        the attribution with the event recorded after the overlap call, which
-        only its passes that read gap and ovl wait for; the step ends when
-        both streams have."""
+        attribution on the caller's.  The aggregation is queued after the
+        attribution with the event recorded after the overlap call, which
+        only its passes that read gap and ovl wait for, so the records
+        reduction starts once both streams are done and has the GPU to
+        itself; the ratios and the window fractions follow on the caller's
+        stream."""
         main = torch.cuda.current_stream()
         if getattr(self, "_side", None) is None:
             self._side = torch.cuda.Stream(device=main.device)
@@ -585,15 +586,15 @@ class Pipeline:
         with torch.cuda.stream(self._side):
             self.overlap()
             self._ov_done.record(self._side)
-            self.derive_windows()
         self.attribute()
         self._ready = self._ov_done
         try:
             self.aggregate()
         finally:
             self._ready = None
-        self.derive_rows()
         main.wait_stream(self._side)
+        self.derive_rows()
+        self.derive_windows()
 
     def results(self) -> Dict:
         torch.cuda.synchronize()
