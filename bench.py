@@ -202,13 +202,14 @@ def main():
     log(f"[bench] warmup done; rows: {rows_total} (finest level "
         f"{rows_finest})")
     # which records reduction this trace takes: one probe step per candidate
-    # (events recorded first, so that a kernel that does not run reads 0)
+    # (events recorded first, the stop before the start, so that a kernel
+    # that does not run reads at most 0 even beside one that takes a few us)
     probe = {}
     for name in ROOF_KERNELS:
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
-        a.record()
         b.record()
+        a.record()
         ch.time_kernel(name, a, b)
         pipe.step()
         torch.cuda.synchronize()

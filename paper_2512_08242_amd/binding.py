@@ -576,7 +576,16 @@ class Pipeline:
         only its passes that read gap and ovl wait for, so the records
         reduction starts once both streams are done and has the GPU to
         itself; the ratios and the window fractions follow on the caller's
-        stream."""
+        stream.  Traces below 2^20 records run the calls in sequence on the
+        caller's stream: there the waits between streams cost about as much
+        as the work they let overlap."""
+        if self.dt.n < (1 << 20):
+            self.align()
+            self.attribute()
+            self.overlap()
+            self.aggregate()
+            self.derive()
+            return
         main = torch.cuda.current_stream()
         if getattr(self, "_side", None) is None:
             self._side = torch.cuda.Stream(device=main.device)
