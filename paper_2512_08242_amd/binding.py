@@ -592,16 +592,18 @@ class Pipeline:
             self._ov_done = torch.cuda.Event()
         self.align()
         self._side.wait_stream(main)
-        with torch.cuda.stream(self._side):
-            self.overlap()
-            self._ov_done.record(self._side)
-        self.attribute()
-        self._ready = self._ov_done
         try:
+            with torch.cuda.stream(self._side):
+                self.overlap()
+                self._ov_done.record(self._side)
+            self.attribute()
+            self._ready = self._ov_done
             self.aggregate()
         finally:
+            # (also when a call failed: nothing later on the caller's stream
+            # may run beside the second stream's work)
             self._ready = None
-        main.wait_stream(self._side)
+            main.wait_stream(self._side)
         self.derive_rows()
         self.derive_windows()
 

@@ -147,6 +147,47 @@ def test_config_full_parity(ch, cid):
     assert_parity(got, ref, name=f"config{cid}")
 
 
+def _flat(res):
+    out = {}
+    for k, v in res.items():
+        if isinstance(v, dict):
+            for kk, vv in v.items():
+                out[k + "." + kk] = vv
+        else:
+            out[k] = v
+    return out
+
+
+def test_two_stream_step_equals_calls_in_sequence(ch):
+    # config 2 (2,457,600 records) takes the two-stream step; the same
+    # calls one after the other on one stream must give the same bits
+    tr = tg.make_config(2, with_truth=False)
+    assert tr.n >= 1 << 20
+    dt = ch.DeviceTrace(tr, "cuda")
+    a = ch.Pipeline(dt)
+    a.status.zero_()
+    a.step()
+    a.step()          # twice: the second reuses the streams and the event
+    ra = _flat(a.results())
+    b = ch.Pipeline(dt)
+    b.status.zero_()
+    b.align()
+    b.attribute()
+    b.overlap()
+    b.aggregate()
+    b.derive()
+    rb = _flat(b.results())
+    assert ra.keys() == rb.keys()
+    for k in ra:
+        x, y = ra[k], rb[k]
+        if isinstance(x, np.ndarray) and x.dtype.kind == "f":
+            assert_same_float(x, y, k)
+        elif isinstance(x, np.ndarray):
+            assert np.array_equal(x, y), k
+        else:
+            assert x == y, k
+
+
 @pytest.mark.parametrize("level", [0, 1, 2, 100, 101])
 def test_single_level_requests(ch, level):
     tr = tg.make_micro(77, n_gpus=3, n_kernels=400, depth=3, n_counters=4,
