@@ -535,7 +535,8 @@ __global__ __launch_bounds__(kBlock) void k_runs_fix(
         di += (uint64_t)ni - (uint64_t)oi;
       }
       if (__ballot(!aff) != 0) break;   // the prefix ends in this chunk
-      run = readlane64(incl, kWave - 1);
+      const int64_t cm = readlane64(incl, kWave - 1);
+      run = cm > run ? cm : run;        // every earlier chunk's ends too
     }
     for (int d = kWave / 2; d > 0; d >>= 1) {
       dh += __shfl_xor(dh, d, kWave);

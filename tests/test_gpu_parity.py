@@ -312,6 +312,38 @@ def _tiny(n, m=3, G=1, depth=2, overlapping=False):
         name=f"tiny{n}")
 
 
+def test_union_carry_over_many_chunks(ch):
+    # The first record of the trace runs over everything after it, so the
+    # second 2048-record tile of the union runs is corrected for that
+    # carry item by item.  In that tile a long record (ending before the
+    # carry) is followed by short ones: the running end of the tile's items
+    # must keep the long record's end across every 64-item chunk after it.
+    T = 2048
+    s = np.concatenate([[0], 10 * np.arange(1, T), [30000],
+                        30000 + 10 * np.arange(1, T)]).astype(np.int64)
+    e = s + 5
+    e[0] = 10 ** 9
+    e[T] = 5 * 10 ** 8
+    cs = (100 + 3000 * np.arange(8)).astype(np.int64)      # comm records
+    n = 2 * T + 8
+    start = np.concatenate([s, cs])
+    end = np.concatenate([e, cs + 1000])
+    cls = np.concatenate([np.zeros(2 * T, np.uint8), np.full(8, 5, np.uint8)])
+    stream = np.concatenate([np.zeros(2 * T, np.uint8), np.ones(8, np.uint8)])
+    tr = tg.Trace(
+        n_gpus=1, depth=2, gpu=np.zeros(n, np.uint8), stream=stream,
+        start=start, end=end, cls=cls, op_id=np.zeros(n, np.uint32),
+        counters=None, m_gpu=np.zeros(3, np.uint8),
+        m_level=np.array([0, 1, 1], np.uint8),
+        m_start=np.array([0, 0, 25000], np.int64),
+        m_end=np.array([2 * 10 ** 9, 25000, 2 * 10 ** 9], np.int64),
+        m_label=np.arange(3, dtype=np.uint32), a_gpu=np.zeros(0, np.uint8),
+        a_local=np.zeros(0, np.int64), a_ref=np.zeros(0, np.int64),
+        name="carry over chunks")
+    say("union carry over many chunks")
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+
+
 @pytest.mark.parametrize("n", [0, 1, 2, 3, 2047, 2048, 2049, 4097])
 def test_edge_sizes(ch, n):
     tr = _tiny(n, m=5)
