@@ -344,6 +344,37 @@ def test_union_carry_over_many_chunks(ch):
     assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_union_runs_heavy_tails(ch, seed):
+    # several 2048-record tiles of two GPUs, starts dense, durations mostly
+    # short with rare ones reaching thousands of records ahead: tiles whose
+    # carry covers many chunks, with chunk maxima that go up and down
+    rng = np.random.default_rng(4000 + seed)
+    n = 7000 + 500 * seed
+    gpu = np.sort(rng.integers(0, 2, size=n)).astype(np.uint8)
+    start = np.zeros(n, np.int64)
+    for g in (0, 1):
+        k = int((gpu == g).sum())
+        start[gpu == g] = np.sort(rng.integers(0, 20 * k, size=k))
+    dur = rng.integers(0, 40, size=n).astype(np.int64)
+    big = rng.random(n) < 0.004
+    dur[big] = rng.integers(1000, 60000, size=int(big.sum()))
+    cls = np.where(rng.random(n) < 0.1, 5, 0).astype(np.uint8)
+    stream = np.where(cls == 5, 2, rng.integers(0, 2, size=n)).astype(np.uint8)
+    ms = np.array([0, 0, 0, 0], np.int64)
+    me = np.array([10 ** 7, 50000, 10 ** 7, 50000], np.int64)
+    tr = tg.Trace(
+        n_gpus=2, depth=2, gpu=gpu, stream=stream, start=start,
+        end=start + dur, cls=cls, op_id=np.zeros(n, np.uint32),
+        counters=None, m_gpu=np.array([0, 0, 1, 1], np.uint8),
+        m_level=np.array([0, 1, 0, 1], np.uint8), m_start=ms, m_end=me,
+        m_label=np.arange(4, dtype=np.uint32), a_gpu=np.zeros(0, np.uint8),
+        a_local=np.zeros(0, np.int64), a_ref=np.zeros(0, np.int64),
+        name=f"heavy tails {seed}")
+    say("union runs heavy tails", seed, n)
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+
+
 @pytest.mark.parametrize("n", [0, 1, 2, 3, 2047, 2048, 2049, 4097])
 def test_edge_sizes(ch, n):
     tr = _tiny(n, m=5)
