@@ -375,6 +375,45 @@ def test_union_runs_heavy_tails(ch, seed):
     assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_attribution_skips_many_markers(ch, seed):
+    # records in start order on one GPU with short level-1 markers between
+    # them (a record often lies two or more markers past the previous
+    # record's), and records inside, before and after them; about as many
+    # markers as records, so that a tile's markers fit its window
+    rng = np.random.default_rng(5000 + seed)
+    n = 3000
+    start = np.sort(rng.integers(0, 400 * n, size=n)).astype(np.int64)
+    end = start + rng.integers(0, 30, size=n)
+    m1 = (8 * n) // 10
+    ms1 = np.sort(rng.integers(0, 400 * n, size=m1)).astype(np.int64)
+    me1 = ms1 + rng.integers(1, 60, size=m1)
+    # level-1 markers must not overlap each other: keep a non-overlapping
+    # subsequence
+    keep = np.ones(m1, bool)
+    last = -1
+    for i in range(m1):
+        if ms1[i] < last:
+            keep[i] = False
+        else:
+            last = me1[i]
+    ms1, me1 = ms1[keep], me1[keep]
+    ms = np.concatenate([[0, 200 * n], ms1]).astype(np.int64)
+    me = np.concatenate([[200 * n, 400 * n + 100], me1]).astype(np.int64)
+    m = ms.shape[0]
+    tr = tg.Trace(
+        n_gpus=1, depth=2, gpu=np.zeros(n, np.uint8),
+        stream=np.zeros(n, np.uint8), start=start, end=end,
+        cls=np.zeros(n, np.uint8), op_id=np.zeros(n, np.uint32),
+        counters=None, m_gpu=np.zeros(m, np.uint8),
+        m_level=np.concatenate([[0, 0], np.ones(m - 2)]).astype(np.uint8),
+        m_start=ms, m_end=me, m_label=np.arange(m, dtype=np.uint32),
+        a_gpu=np.zeros(0, np.uint8), a_local=np.zeros(0, np.int64),
+        a_ref=np.zeros(0, np.int64), name=f"many markers {seed}")
+    say("attribution skips many markers", seed, n, m)
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+
+
 @pytest.mark.parametrize("n", [0, 1, 2, 3, 2047, 2048, 2049, 4097])
 def test_edge_sizes(ch, n):
     tr = _tiny(n, m=5)
