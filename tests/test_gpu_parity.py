@@ -238,6 +238,20 @@ def test_natural_order_micro(ch, seed, shape):
     assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_natural_order_unnested(ch, seed):
+    """Arbitrary marker intervals with the records grouped by GPU in start
+    order: the natural-tile heads pass must find the shared deepest markers
+    of different paths (PATH_CONFLICT) and send the rows to the general
+    path."""
+    tr = natural_order(tg.make_micro(600 + seed, n_gpus=2, n_kernels=3000,
+                                     n_streams=3, depth=3, nested=False,
+                                     n_counters=2, span=30000))
+    say("natural unnested", seed, tr.n)
+    ref = oracle.run(tr)
+    assert_parity(run_gpu(ch, tr), ref, name=tr.name)
+
+
 @pytest.mark.parametrize("seed", range(3))
 def test_natural_order_many_small_gpus(ch, seed):
     """Forty GPUs of about fifty records: most tiles hold several GPUs."""
