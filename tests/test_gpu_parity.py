@@ -252,6 +252,22 @@ def test_natural_order_unnested(ch, seed):
     assert_parity(run_gpu(ch, tr), ref, name=tr.name)
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_natural_order_markers_shuffled(ch, seed):
+    """Records grouped by GPU in start order, markers numbered in no order:
+    the marker slots of a run do not increase, which the natural-tile heads
+    pass must notice (the rows then come from the general path)."""
+    tr = natural_order(tg.make_micro(620 + seed, n_gpus=2, n_kernels=3000,
+                                     n_streams=2, depth=3, n_counters=2,
+                                     span=30000))
+    p = np.random.default_rng(seed).permutation(tr.n_markers)
+    tr = dataclasses.replace(tr, m_gpu=tr.m_gpu[p], m_level=tr.m_level[p],
+                             m_start=tr.m_start[p], m_end=tr.m_end[p],
+                             m_label=tr.m_label[p], name=tr.name + "/mshuf")
+    say("natural, markers shuffled", seed, tr.n, tr.n_markers)
+    assert_parity(run_gpu(ch, tr), oracle.run(tr), name=tr.name)
+
+
 @pytest.mark.parametrize("seed", range(3))
 def test_natural_order_many_small_gpus(ch, seed):
     """Forty GPUs of about fifty records: most tiles hold several GPUs."""
